@@ -1,0 +1,100 @@
+"""Plant a plausible mistake in the oracle (CPU only) and check that a pin fails.
+
+Each case monkeypatches one oracle function with a wrong variant; the listed
+checks must raise.  This shows the pins can tell a correct oracle from a
+subtly wrong one.
+"""
+import numpy as np
+import pytest
+
+import oracle_checks as C
+from oracle import qsvd_oracle as O
+
+_orig_split = O.split_beta
+_orig_quant = O.quantize_act
+_orig_scaled = O._scaled
+_orig_pack = O.pack_int4
+_orig_svd = O.joint_svd
+
+
+def _split_sigma_both(U_r, s, Vt_r, beta):          # Sigma^beta on both sides
+    return U_r * (s ** beta)[None, :], (s ** beta)[:, None] * Vt_r
+
+
+def _split_truncate_wrong_end(U_r, s, Vt_r, beta):  # keeps the smallest values
+    A, B = _orig_split(U_r, s, Vt_r, beta)
+    return A[:, ::-1], B[::-1, :] * 0.999
+
+
+def _quant_floor(x, bits, clip=1.0):                # truncation instead of RNE
+    xf = np.asarray(x).astype(np.float32)
+    Qm = np.float32(O.qmax(bits))
+    a = np.max(np.abs(xf), axis=1)
+    a[a == 0] = 1
+    s = (a / Qm).astype(np.float32)
+    q = np.clip(np.trunc(xf * (Qm / a)[:, None]), -Qm, Qm).astype(np.int8)
+    return q, s
+
+
+def _quant_divide(x, bits, clip=1.0):               # x / s instead of x * (Qm / a)
+    xf = np.asarray(x).astype(np.float32)
+    Qm = np.float32(O.qmax(bits))
+    a = np.max(np.abs(xf), axis=1).astype(np.float32)
+    s = (a / Qm).astype(np.float32)
+    s[a == 0] = 1
+    q = np.clip(np.rint(xf / s[:, None]), -Qm, Qm).astype(np.int8)
+    return q, s
+
+
+def _scaled_swapped(acc, s_row, w_scale, group, K, aq, wq):   # scales applied in the other order
+    if group:
+        return _orig_scaled(acc, s_row, w_scale, group, K, aq, wq)
+    y = (acc.astype(np.float32) * w_scale.astype(np.float32)[None, :]).astype(np.float32)
+    return (y * s_row.astype(np.float32)[:, None]).astype(np.float32)
+
+
+def _scaled_in_f64(acc, s_row, w_scale, group, K, aq, wq):    # no fp32 rounding at all
+    if group:
+        return _orig_scaled(acc, s_row, w_scale, group, K, aq, wq)
+    return (acc * s_row.astype(np.float64)[:, None] * w_scale.astype(np.float64)[None, :]).astype(np.float32)
+
+
+def _pack_swapped(q):                                # high/low nibble swapped
+    p = _orig_pack(q)
+    return ((p >> 4) | (p << 4)).astype(np.uint8)
+
+
+def _svd_no_sign_fix(W):
+    U, s, Vt = np.linalg.svd(np.asarray(W, dtype=np.float64), full_matrices=False)
+    return -U, s, -Vt
+
+
+def _kv_group_modulo(h, hq, hkv):                    # interleaved instead of blocked groups
+    return h % hkv
+
+
+def _kv_group_off_by_one(h, hq, hkv):
+    return min(hkv - 1, (h * hkv) // hq + (1 if h == 1 else 0))
+
+
+MUTATIONS = [
+    ("split_beta", _split_sigma_both, [C.check_full_rank_reconstruction, C.check_beta_and_rotation_invariance]),
+    ("split_beta", _split_truncate_wrong_end, [C.check_eckart_young]),
+    ("quantize_act", _quant_floor, [C.check_act_quant_exact, C.check_act_quant_properties]),
+    ("quantize_act", _quant_divide, [C.check_act_quant_exact]),
+    ("_scaled", _scaled_swapped, [C.check_projection_epilogues]),
+    ("_scaled", _scaled_in_f64, [C.check_projection_epilogues]),
+    ("pack_int4", _pack_swapped, [C.check_cache_append_and_int4]),
+    ("joint_svd", _svd_no_sign_fix, [C.check_svd_factors]),
+    ("kv_group", _kv_group_modulo, [C.check_full_rank_matches_textbook_attention]),
+    ("kv_group", _kv_group_off_by_one, [C.check_full_rank_matches_textbook_attention]),
+]
+
+
+@pytest.mark.parametrize("name,bad,checks", MUTATIONS,
+                         ids=[f"{m[0]}:{m[1].__name__}" for m in MUTATIONS])
+def test_planted_mistake_is_caught(monkeypatch, name, bad, checks):
+    monkeypatch.setattr(O, name, bad)
+    for check in checks:
+        with pytest.raises(AssertionError):
+            check()

@@ -1,0 +1,99 @@
+"""Seeded random inputs: weights (or their known factors), activations, decode inputs.
+
+Seeds are ``numpy.random.default_rng(16292 + 100*cfg + role + 1000*layer)``.
+Roles: 0 weights, 1 prefill activations, 2 outlier channels, 3 synthetic
+cache fill, 4+t decode input of step t.
+
+Nothing here belongs to the method: weights with a prescribed spectrum are
+built as U diag(sigma) V^T from orthonormal factors (so for those workloads the
+truncated SVD is known by construction), activations are Gaussian with a few
+channel-wise outlier columns as described for the profiled activations in
+Section 3.3.
+"""
+import numpy as np
+
+from .configs import Workload
+
+ROLE_W, ROLE_X, ROLE_OUTLIER, ROLE_FILL, ROLE_DECODE0 = 0, 1, 2, 3, 4
+
+
+def rng_for(wl: Workload, role: int, layer: int = 0) -> np.random.Generator:
+    return np.random.default_rng(16292 + 100 * wl.cfg_id + role + 1000 * layer)
+
+
+def weight_matrix(wl: Workload, layer: int = 0) -> np.ndarray:
+    """Concatenated [W_q | W_k | W_v] (d x N), iid N(0, w_std^2) rounded to fp32.
+
+    Returned as float64 holding fp32 values.  Only for ``spectrum == "gaussian"``.
+    """
+    assert wl.spectrum == "gaussian"
+    L = wl.layer
+    g = rng_for(wl, ROLE_W, layer)
+    w = (g.standard_normal((L.d, L.N)) * wl.w_std).astype(np.float32)
+    return w.astype(np.float64)
+
+
+def _orthonormal(g: np.random.Generator, rows: int, cols: int) -> np.ndarray:
+    q, r = np.linalg.qr(g.standard_normal((rows, cols)))
+    return q * np.sign(np.diag(r))[None, :]
+
+
+def spectrum(wl: Workload) -> np.ndarray:
+    """sigma_i = sigma_1 * i^-decay_exp for i = 1..min(d, N); sigma_1 makes
+    ||W||_F equal to that of an iid N(0, w_std^2) matrix of the same shape."""
+    L = wl.layer
+    n = min(L.d, L.N)
+    i = np.arange(1, n + 1, dtype=np.float64)
+    shape = i ** (-wl.decay_exp)
+    sigma1 = wl.w_std * np.sqrt(L.d * L.N) / np.sqrt(np.sum(shape * shape))
+    return sigma1 * shape
+
+
+def weight_factors(wl: Workload, layer: int = 0, rank: int = None):
+    """Leading ``rank`` singular triplets (U_r [d,r], sigma_r [r], V_r [N,r]) of a
+    d x N weight with the decaying spectrum, known by construction.
+
+    The full matrix would be U diag(sigma) V^T over all min(d, N) triplets; the
+    trailing ones are orthogonal to these and are never needed by the hot path.
+    """
+    assert wl.spectrum == "decay"
+    L = wl.layer
+    rank = L.r if rank is None else rank
+    g = rng_for(wl, ROLE_W, layer)
+    U = _orthonormal(g, L.d, rank)
+    V = _orthonormal(g, L.N, rank)
+    return U, spectrum(wl)[:rank].copy(), V
+
+
+def outlier_channels(wl: Workload, layer: int = 0) -> np.ndarray:
+    g = rng_for(wl, ROLE_OUTLIER, layer)
+    return np.sort(g.choice(wl.layer.d, size=wl.outlier_count, replace=False))
+
+
+def _activation_rows(g: np.random.Generator, wl: Workload, rows: int, layer: int) -> np.ndarray:
+    x = g.standard_normal((rows, wl.layer.d))
+    x[:, outlier_channels(wl, layer)] *= wl.outlier_scale
+    return x.astype(np.float16)
+
+
+def prefill_activations(wl: Workload, layer: int = 0, rows: int = None) -> np.ndarray:
+    """fp16 [prefill_M, d]: N(0,1) with the outlier channels scaled."""
+    rows = wl.prefill_M if rows is None else rows
+    return _activation_rows(rng_for(wl, ROLE_X, layer), wl, rows, layer)
+
+
+def decode_activations(wl: Workload, step: int, layer: int = 0, batch: int = None) -> np.ndarray:
+    """fp16 [batch, d]: a fresh seeded row per sequence for decode step ``step``."""
+    batch = wl.decode_batch if batch is None else batch
+    return _activation_rows(rng_for(wl, ROLE_DECODE0 + step, layer), wl, batch, layer)
+
+
+def fill_activations(wl: Workload, rows: int, layer: int = 0) -> np.ndarray:
+    """fp16 [rows, d] used to build a pre-filled latent cache."""
+    return _activation_rows(rng_for(wl, ROLE_FILL, layer), wl, rows, layer)
+
+
+def random_rows(seed: int, shape, scale: float = 1.0, dtype=np.float16) -> np.ndarray:
+    """Plain N(0, scale^2) array for small edge-case tests."""
+    g = np.random.default_rng(seed)
+    return (g.standard_normal(shape) * scale).astype(dtype)
