@@ -1,0 +1,175 @@
+/*
+ * qsvd.h -- C ABI of the QSVD latent-QKV hot path on AMD Instinct MI355X (gfx950).
+ *
+ * QSVD ("Efficient Low-rank Approximation for Unified Query-Key-Value Weight
+ * Compression in Low-Precision Vision-Language Models", arXiv 2510.16292)
+ * replaces the three projections W_q, W_k, W_v of an attention layer by one
+ * joint truncated SVD of [W_q | W_k | W_v] (Section 3.1, Eq. 2-4): a shared
+ * down-projection W^d (d x r) and an up-projection W^u = [W^u_q | W^u_k | W^u_v]
+ * (r x N).  The per-token latent C = X W^d is the only thing cached
+ * (Section 3.1); keys and values are rebuilt from it, K = C W^u_k and
+ * V = C W^u_v (Eq. 5).  Weights and activations are quantized (Section 3.3,
+ * Eq. 11-12; per-token symmetric activations and round-to-nearest
+ * per-channel symmetric weights, Section 4).
+ *
+ * Conventions for every call:
+ *  - Pointers marked "device" are device (HBM) addresses allocated by the
+ *    caller; the library never allocates, frees or keeps device memory, and
+ *    keeps no state between calls except the optional profiler.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Calls enqueue work
+ *    on it and return without synchronizing.
+ *  - Arguments are validated on the host before any GPU work is enqueued.  On
+ *    any status other than QSVD_OK nothing was enqueued, outputs are left
+ *    untouched and cache state (seq_len, max_len) is unchanged -- except
+ *    QSVD_ERR_HIP, which reports a failed launch after validation passed.
+ *    qsvd_last_error() describes the most recent failure of the calling thread.
+ *  - Row-major layouts; "[a][b]" means b is the contiguous index.
+ *  - Integer codes are symmetric two's complement: int8 in [-127, 127], int4
+ *    in [-7, 7] packed two per byte, element 2i in the low nibble of byte i.
+ */
+#ifndef QSVD_H
+#define QSVD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  QSVD_OK = 0,
+  QSVD_ERR_INVALID_ARG = 1,  /* null pointer, negative size, inconsistent shapes */
+  QSVD_ERR_UNSUPPORTED = 2,  /* well-formed but outside what the kernels implement */
+  QSVD_ERR_CAPACITY = 3,     /* an append would exceed the cache capacity */
+  QSVD_ERR_WORKSPACE = 4,    /* workspace missing or smaller than the size query */
+  QSVD_ERR_HIP = 5           /* a HIP runtime call or kernel launch failed */
+} qsvd_status;
+
+/* Latent cache storage formats. */
+enum { QSVD_CACHE_F16 = 0, QSVD_CACHE_I8 = 1, QSVD_CACHE_I4 = 2 };
+
+/* Decode attention forms.  RECONSTRUCT rebuilds K and V from the latent for
+ * every cached token (Eq. 5) and attends as usual; ABSORBED folds W^u_k into
+ * the query and applies W^u_v after the latent-space weighted sum (the
+ * latent-attention form of Section 1 and 2.2).  Both compute the same
+ * attention; AUTO picks the faster one for the layer (ABSORBED). */
+enum { QSVD_ATTN_AUTO = 0, QSVD_ATTN_ABSORBED = 1, QSVD_ATTN_RECONSTRUCT = 2 };
+
+/* Which up-projection outputs qsvd_lowrank_qkv_prefill writes. */
+enum { QSVD_OUT_Q = 1, QSVD_OUT_K = 2, QSVD_OUT_V = 4 };
+
+/* One attention layer after the offline stage (joint SVD, truncation, beta
+ * split, weight quantization).  N = (n_q_heads + 2 * n_kv_heads) * head_dim.
+ * Query head h reads key/value head floor(h * n_kv_heads / n_q_heads). */
+typedef struct {
+  int32_t d;           /* embedding dimension E (contraction of X W^d) */
+  int32_t r;           /* joint rank */
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t w_bits;      /* 8: int8 codes; 4: packed int4 codes */
+  int32_t w_group;     /* 0: one scale per output channel; G > 0: one scale per
+                          output channel and per G contraction rows */
+  const void*  a_t;    /* device, W^d codes transposed: [r][d] int8 or [r][d/2] int4 */
+  const float* s_a;    /* device, W^d scales: [r] (w_group 0) or [d/G][r] */
+  const void*  b_t;    /* device, W^u codes transposed: [N][r] int8 or [N][r/2] int4;
+                          rows 0..Hq*hd-1 are W^u_q, then W^u_k, then W^u_v */
+  const float* s_b;    /* device, W^u scales: [N] (w_group 0) or [r/G][N] */
+} qsvd_layer;
+
+/* Latent cache of `batch` sequences.  Sequence b holds seq_len[b] rows.
+ * F16: data is [batch][capacity][r] fp16, scale NULL.
+ * I8:  data is [batch][capacity][r] int8, scale [batch][capacity] fp32.
+ * I4:  data is [batch][capacity][r/2] packed int4, scale [batch][capacity] fp32.
+ * A row of an integer cache is Q(C) of the token (its codes and scale). */
+typedef struct {
+  int32_t  fmt;        /* QSVD_CACHE_* */
+  int32_t  batch;
+  int32_t  capacity;   /* rows per sequence */
+  int32_t  r;
+  void*    data;       /* device */
+  float*   scale;      /* device or NULL (F16) */
+  int32_t* seq_len;    /* device [batch] */
+  int32_t  max_len;    /* host: an upper bound of every seq_len[b]; the caller sets
+                          it when initialising seq_len, append advances it */
+} qsvd_cache;
+
+/* Per-token symmetric activation quantization (Section 4 setup; Q(.) of Eq. 12).
+ * Per row m, in fp32: a = clip * max_k |x[m][k]|; if a == 0 then s = 1 and all
+ * codes are 0, else inv = Qm / a (IEEE division), s = a / Qm and
+ * q = clamp(rint(x * inv), -Qm, Qm) with ties to even; Qm = 2^(bits-1) - 1.
+ *   x   device fp16 [M][ldx] (first K columns used)
+ *   xq  device int8 [M][K] (bits 8) or packed int4 [M][K/2] (bits 4)
+ *   sx  device fp32 [M]
+ * Requires K % 8 == 0, ldx % 8 == 0, 16-byte aligned x; bits 8 or 4; 0 < clip <= 1. */
+qsvd_status qsvd_quantize_act(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits,
+                              float clip, void* xq, float* sx, void* stream);
+
+/* Quantized joint low-rank QKV projection (Section 3.1 and Eq. 11-12):
+ *   C   = (xq W^d codes) dequantized: fp32 (acc * sx[m]) * s_a[j] (per group:
+ *         sum over groups of acc_g * s_a[g][j], then * sx[m]), stored as fp16
+ *   Q(C) = per-token quantization of the fp16 C with act_bits (as qsvd_quantize_act, clip 1)
+ *   [Q|K|V] = (Q(C) W^u codes) dequantized the same way, stored as fp16
+ *   w        layer (host struct, device pointers)
+ *   xq, sx   device, output of qsvd_quantize_act with act_bits, M rows
+ *   c_h      device fp16 [M][r]                     (always written)
+ *   cq, sc   device int8 [M][r] (or int4 [M][r/2]) and fp32 [M]   (always written)
+ *   q, k, v  device fp16 [M][Hq*hd], [M][Hkv*hd], [M][Hkv*hd]; written when the
+ *            matching QSVD_OUT_* bit is set (others may be NULL)
+ *   dbg_acc_xa, dbg_acc_cb  optional device int32 [M][r] and [M][N] copies of
+ *            the integer accumulators (w_group 0 only; NULL to skip)
+ *   ws       device workspace of at least qsvd_prefill_workspace_size() bytes
+ * Requires d % 64 == 0, r % 64 == 0, act_bits 8 (4 with w_bits 4). */
+qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const float* sx,
+                                     int64_t M, int32_t act_bits, uint32_t out_mask,
+                                     void* c_h, void* cq, float* sc, void* q, void* k, void* v,
+                                     int32_t* dbg_acc_xa, int32_t* dbg_acc_cb,
+                                     void* ws, size_t ws_bytes, void* stream);
+
+size_t qsvd_prefill_workspace_size(const qsvd_layer* w, int64_t M, uint32_t out_mask);
+
+/* Append n_new latent rows to every sequence of the cache (only C is buffered,
+ * Section 3.1).  Source rows are token-major with sequence b's rows at
+ * [b * n_new, (b + 1) * n_new):
+ *   F16 cache: c_h  device fp16 [batch * n_new][r]           (cq, sc ignored)
+ *   I8 / I4:   cq   device int8 [..][r] / int4 [..][r/2], sc device fp32 [..]
+ * Row i of sequence b goes to position seq_len[b] + i; then seq_len[b] += n_new
+ * on the device and c->max_len += n_new on the host.  Returns QSVD_ERR_CAPACITY
+ * if c->max_len + n_new > c->capacity. */
+qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void* cq,
+                                     const float* sc, int32_t n_new, void* stream);
+
+/* Attention of the current query of every sequence over its cached latent rows
+ * (decoding with l = 1, Section 3.1): keys and values are C W^u_k and C W^u_v
+ * of the stored rows (dequantized), the query attends to all seq_len[b] rows
+ * (append first, then attend), softmax(q K^T * sm_scale) V with fp32 softmax.
+ *   q     device fp16 [batch][q_len][Hq*hd] (the Q output of the projection)
+ *   out   device fp16 [batch][q_len][Hq*hd]
+ *   sm_scale  0 selects 1/sqrt(head_dim)
+ *   ws    device workspace of at least qsvd_decode_workspace_size() bytes
+ * Requires q_len == 1, n_q_heads <= 32, head_dim % 32 == 0, r % 32 == 0,
+ * every seq_len[b] in [1, capacity]. */
+qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* c,
+                                         const void* q, int32_t q_len, int32_t mode,
+                                         float sm_scale, void* out,
+                                         void* ws, size_t ws_bytes, void* stream);
+
+size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int32_t q_len,
+                                  int32_t mode);
+
+const char* qsvd_status_string(qsvd_status s);
+const char* qsvd_last_error(void);
+
+/* Optional kernel timing.  While enabled, every kernel the library launches is
+ * bracketed by HIP events recorded on its launch stream; qsvd_profile_read()
+ * synchronizes those events and returns the summed milliseconds and launch
+ * count of the kernels whose name contains `name`.  Not for graph capture. */
+qsvd_status qsvd_profile_enable(int32_t on);
+qsvd_status qsvd_profile_reset(void);
+qsvd_status qsvd_profile_read(const char* name, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* QSVD_H */

@@ -1,0 +1,309 @@
+// The C ABI of include/qsvd.h: host-side validation, then launches on the
+// caller's stream.  Validation runs before any HIP call, so argument errors are
+// reported without touching the GPU.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "launch.h"
+
+namespace qsvd {
+bool absorbed_supported(const qsvd_layer& w, const qsvd_cache& c);
+}
+
+using namespace qsvd;
+
+namespace {
+
+thread_local std::string g_err;
+
+qsvd_status fail(qsvd_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+qsvd_status fail(qsvd_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+qsvd_status hip_status(hipError_t e, const char* where) {
+  if (e == hipSuccess) return QSVD_OK;
+  return fail(QSVD_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+int64_t n_total(const qsvd_layer& w) { return (int64_t)(w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim; }
+
+qsvd_status check_layer(const qsvd_layer* w) {
+  if (!w) return fail(QSVD_ERR_INVALID_ARG, "layer is NULL");
+  if (w->d <= 0 || w->r <= 0 || w->n_q_heads <= 0 || w->n_kv_heads <= 0 || w->head_dim <= 0)
+    return fail(QSVD_ERR_INVALID_ARG, "layer dimensions must be positive");
+  if (w->n_q_heads % w->n_kv_heads)
+    return fail(QSVD_ERR_INVALID_ARG, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)", w->n_q_heads,
+                w->n_kv_heads);
+  if (!w->a_t || !w->s_a || !w->b_t || !w->s_b) return fail(QSVD_ERR_INVALID_ARG, "layer weight pointer is NULL");
+  if (w->w_bits != 8 && w->w_bits != 4) return fail(QSVD_ERR_INVALID_ARG, "w_bits must be 8 or 4");
+  if (w->w_group < 0) return fail(QSVD_ERR_INVALID_ARG, "w_group must be >= 0");
+  if (w->w_group > 0 && (w->d % w->w_group || w->r % w->w_group))
+    return fail(QSVD_ERR_INVALID_ARG, "w_group must divide d and r");
+  if (w->w_bits == 4 && w->w_group == 0)
+    return fail(QSVD_ERR_UNSUPPORTED, "int4 weights need a group size");
+  if (w->d % 64 || w->r % 64) return fail(QSVD_ERR_UNSUPPORTED, "d and r must be multiples of 64");
+  return QSVD_OK;
+}
+
+qsvd_status check_cache(const qsvd_cache* c) {
+  if (!c) return fail(QSVD_ERR_INVALID_ARG, "cache is NULL");
+  if (c->fmt < QSVD_CACHE_F16 || c->fmt > QSVD_CACHE_I4) return fail(QSVD_ERR_INVALID_ARG, "unknown cache format");
+  if (c->batch <= 0 || c->capacity <= 0 || c->r <= 0) return fail(QSVD_ERR_INVALID_ARG, "cache sizes must be positive");
+  if (c->r % 32) return fail(QSVD_ERR_UNSUPPORTED, "cache r must be a multiple of 32");
+  if (!c->data || !c->seq_len) return fail(QSVD_ERR_INVALID_ARG, "cache data/seq_len is NULL");
+  if (c->fmt != QSVD_CACHE_F16 && !c->scale) return fail(QSVD_ERR_INVALID_ARG, "integer cache needs scales");
+  if (c->max_len < 0 || c->max_len > c->capacity)
+    return fail(QSVD_ERR_INVALID_ARG, "max_len %d outside [0, capacity %d]", c->max_len, c->capacity);
+  if (!aligned(c->data, 16)) return fail(QSVD_ERR_UNSUPPORTED, "cache data must be 16-byte aligned");
+  return QSVD_OK;
+}
+
+// ---------------------------------------------------------------- profiler
+struct ProfRec {
+  std::string name;
+  hipEvent_t start, stop;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof;
+
+}  // namespace
+
+namespace qsvd {
+
+KernelScope::KernelScope(const char* name, hipStream_t s) : name_(name), s_(s), slot_(-1) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof_on) return;
+  ProfRec r{name, nullptr, nullptr};
+  if (hipEventCreate(&r.start) != hipSuccess || hipEventCreate(&r.stop) != hipSuccess) return;
+  hipEventRecord(r.start, s);
+  g_prof.push_back(r);
+  slot_ = (int)g_prof.size() - 1;
+}
+
+KernelScope::~KernelScope() {
+  if (slot_ < 0) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (slot_ < (int)g_prof.size()) hipEventRecord(g_prof[slot_].stop, s_);
+}
+
+}  // namespace qsvd
+
+extern "C" {
+
+const char* qsvd_status_string(qsvd_status s) {
+  switch (s) {
+    case QSVD_OK: return "ok";
+    case QSVD_ERR_INVALID_ARG: return "invalid argument";
+    case QSVD_ERR_UNSUPPORTED: return "unsupported";
+    case QSVD_ERR_CAPACITY: return "cache capacity exceeded";
+    case QSVD_ERR_WORKSPACE: return "workspace too small";
+    case QSVD_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* qsvd_last_error(void) { return g_err.c_str(); }
+
+qsvd_status qsvd_quantize_act(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits, float clip,
+                              void* xq, float* sx, void* stream) {
+  if (M < 0 || K <= 0 || ldx < K) return fail(QSVD_ERR_INVALID_ARG, "bad sizes M=%lld K=%d ldx=%lld", (long long)M, K, (long long)ldx);
+  if (bits != 8 && bits != 4) return fail(QSVD_ERR_INVALID_ARG, "bits must be 8 or 4");
+  if (!(clip > 0.f && clip <= 1.f)) return fail(QSVD_ERR_INVALID_ARG, "clip must be in (0, 1]");
+  if (M > 0 && (!x || !xq || !sx)) return fail(QSVD_ERR_INVALID_ARG, "NULL pointer");
+  if (K % 8 || ldx % 8) return fail(QSVD_ERR_UNSUPPORTED, "K and ldx must be multiples of 8");
+  if (!aligned(x, 16) || !aligned(xq, 8)) return fail(QSVD_ERR_UNSUPPORTED, "x must be 16-byte and xq 8-byte aligned");
+  return hip_status(launch_quantize_rows(x, M, K, ldx, bits, clip, xq, sx, (hipStream_t)stream), "quantize_act");
+}
+
+static void prefill_ranges(const qsvd_layer& w, uint32_t mask, bool full, int32_t* lo, int32_t* hi) {
+  const int32_t nq = w.n_q_heads * w.head_dim, nkv = w.n_kv_heads * w.head_dim;
+  const int32_t b0[3] = {0, nq, nq + nkv}, b1[3] = {nq, nq + nkv, nq + 2 * nkv};
+  *lo = INT32_MAX;
+  *hi = 0;
+  for (int s = 0; s < 3; ++s)
+    if (mask & (1u << s)) {
+      if (b0[s] < *lo) *lo = b0[s];
+      if (b1[s] > *hi) *hi = b1[s];
+    }
+  if (full) {
+    *lo = 0;
+    *hi = nq + 2 * nkv;
+  }
+  if (*lo > *hi) *lo = *hi = 0;
+}
+
+size_t qsvd_prefill_workspace_size(const qsvd_layer* w, int64_t M, uint32_t out_mask) {
+  if (!w || M < 0) return 0;
+  (void)out_mask;
+  const size_t a = gemm_i8_workspace(M, w->r, w->d);
+  const size_t b = gemm_i8_workspace(M, (int32_t)n_total(*w), w->r);
+  return a > b ? a : b;
+}
+
+qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const float* sx, int64_t M,
+                                     int32_t act_bits, uint32_t out_mask, void* c_h, void* cq, float* sc,
+                                     void* q, void* k, void* v, int32_t* dbg_acc_xa, int32_t* dbg_acc_cb,
+                                     void* ws, size_t ws_bytes, void* stream) {
+  qsvd_status st = check_layer(w);
+  if (st != QSVD_OK) return st;
+  if (M < 0) return fail(QSVD_ERR_INVALID_ARG, "M must be >= 0");
+  if (out_mask & ~7u) return fail(QSVD_ERR_INVALID_ARG, "unknown out_mask bits");
+  if (act_bits != 8 && act_bits != 4) return fail(QSVD_ERR_INVALID_ARG, "act_bits must be 8 or 4");
+  if (M == 0) return QSVD_OK;
+  if (!xq || !sx || !c_h || !cq || !sc) return fail(QSVD_ERR_INVALID_ARG, "NULL input/latent pointer");
+  if (((out_mask & QSVD_OUT_Q) && !q) || ((out_mask & QSVD_OUT_K) && !k) || ((out_mask & QSVD_OUT_V) && !v))
+    return fail(QSVD_ERR_INVALID_ARG, "requested output pointer is NULL");
+  if (w->w_bits != 8 || w->w_group != 0 || act_bits != 8)
+    return fail(QSVD_ERR_UNSUPPORTED, "prefill implements W8A8 per-channel weights");
+  if (!aligned(xq, 16) || !aligned(cq, 16) || !aligned(c_h, 16) || !aligned(w->a_t, 16) || !aligned(w->b_t, 16))
+    return fail(QSVD_ERR_UNSUPPORTED, "operands must be 16-byte aligned");
+  const size_t need = qsvd_prefill_workspace_size(w, M, out_mask);
+  if (need > 0 && (!ws || ws_bytes < need))
+    return fail(QSVD_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+
+  hipStream_t s = (hipStream_t)stream;
+  // X W^d -> C (fp16)
+  GemmArgs g1{};
+  g1.a = (const int8_t*)xq;
+  g1.b = (const int8_t*)w->a_t;
+  g1.row_scale = sx;
+  g1.col_scale = w->s_a;
+  g1.M = M;
+  g1.N = w->r;
+  g1.K = w->d;
+  g1.seg[0] = OutSeg{(_Float16*)c_h, w->r, 0, w->r};
+  g1.n_seg = 1;
+  g1.dbg = dbg_acc_xa;
+  st = hip_status(launch_gemm_i8(g1, ws, s), "down-projection");
+  if (st != QSVD_OK) return st;
+  // Q(C)
+  st = hip_status(launch_quantize_rows(c_h, M, w->r, w->r, act_bits, 1.f, cq, sc, s), "latent quantization");
+  if (st != QSVD_OK) return st;
+  if (!out_mask && !dbg_acc_cb) return QSVD_OK;
+  // Q(C) W^u -> Q | K | V (fp16)
+  int32_t lo, hi;
+  prefill_ranges(*w, out_mask, dbg_acc_cb != nullptr, &lo, &hi);
+  const int32_t nq = w->n_q_heads * w->head_dim, nkv = w->n_kv_heads * w->head_dim;
+  GemmArgs g2{};
+  g2.a = (const int8_t*)cq;
+  g2.b = (const int8_t*)w->b_t + (int64_t)lo * w->r;
+  g2.row_scale = sc;
+  g2.col_scale = w->s_b + lo;
+  g2.M = M;
+  g2.N = hi - lo;
+  g2.K = w->r;
+  g2.seg[0] = OutSeg{(out_mask & QSVD_OUT_Q) ? (_Float16*)q : nullptr, nq, 0 - lo, nq};
+  g2.seg[1] = OutSeg{(out_mask & QSVD_OUT_K) ? (_Float16*)k : nullptr, nkv, nq - lo, nkv};
+  g2.seg[2] = OutSeg{(out_mask & QSVD_OUT_V) ? (_Float16*)v : nullptr, nkv, nq + nkv - lo, nkv};
+  g2.n_seg = 3;
+  g2.dbg = dbg_acc_cb;
+  return hip_status(launch_gemm_i8(g2, ws, s), "up-projection");
+}
+
+qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void* cq, const float* sc,
+                                     int32_t n_new, void* stream) {
+  qsvd_status st = check_cache(c);
+  if (st != QSVD_OK) return st;
+  if (n_new < 0) return fail(QSVD_ERR_INVALID_ARG, "n_new must be >= 0");
+  if (n_new == 0) return QSVD_OK;
+  if (c->fmt == QSVD_CACHE_F16 && !c_h) return fail(QSVD_ERR_INVALID_ARG, "fp16 cache needs c_h");
+  if (c->fmt != QSVD_CACHE_F16 && (!cq || !sc)) return fail(QSVD_ERR_INVALID_ARG, "integer cache needs cq and sc");
+  if ((int64_t)c->max_len + n_new > c->capacity)
+    return fail(QSVD_ERR_CAPACITY, "max_len %d + %d exceeds capacity %d", c->max_len, n_new, c->capacity);
+  const void* src = c->fmt == QSVD_CACHE_F16 ? c_h : cq;
+  if (!aligned(src, 16)) return fail(QSVD_ERR_UNSUPPORTED, "source rows must be 16-byte aligned");
+  st = hip_status(launch_cache_append(*c, c_h, cq, sc, n_new, (hipStream_t)stream), "cache append");
+  if (st == QSVD_OK) c->max_len += n_new;
+  return st;
+}
+
+size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int32_t q_len, int32_t mode) {
+  if (!w || !c || q_len != 1) return 0;
+  if (c->batch <= 0 || c->capacity <= 0 || w->r <= 0) return 0;
+  const bool abs_ok = absorbed_supported(*w, *c);
+  if (mode == QSVD_ATTN_RECONSTRUCT || (mode == QSVD_ATTN_AUTO && !abs_ok)) return attn_reconstruct_workspace(*w, *c);
+  return attn_absorbed_workspace(*w, *c);
+}
+
+qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* c, const void* q, int32_t q_len,
+                                         int32_t mode, float sm_scale, void* out, void* ws, size_t ws_bytes,
+                                         void* stream) {
+  qsvd_status st = check_layer(w);
+  if (st != QSVD_OK) return st;
+  st = check_cache(c);
+  if (st != QSVD_OK) return st;
+  if (c->r != w->r) return fail(QSVD_ERR_INVALID_ARG, "cache r %d != layer r %d", c->r, w->r);
+  if (!q || !out) return fail(QSVD_ERR_INVALID_ARG, "NULL q/out");
+  if (mode < QSVD_ATTN_AUTO || mode > QSVD_ATTN_RECONSTRUCT) return fail(QSVD_ERR_INVALID_ARG, "unknown mode");
+  if (!(sm_scale >= 0.f) || isinf(sm_scale)) return fail(QSVD_ERR_INVALID_ARG, "sm_scale must be finite and >= 0");
+  if (q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "q_len must be 1 (decode)");
+  if (c->max_len < 1) return fail(QSVD_ERR_INVALID_ARG, "cache is empty (max_len 0)");
+  if (w->n_q_heads > 32) return fail(QSVD_ERR_UNSUPPORTED, "at most 32 query heads");
+  if (w->head_dim % 32 || w->head_dim > 128) return fail(QSVD_ERR_UNSUPPORTED, "head_dim must be 32, 64, 96 or 128");
+  if (c->batch > 64) return fail(QSVD_ERR_UNSUPPORTED, "at most 64 sequences per call");
+  if (c->fmt == QSVD_CACHE_I4) return fail(QSVD_ERR_UNSUPPORTED, "int4 cache attention is not implemented");
+  if (!aligned(q, 16) || !aligned(out, 16)) return fail(QSVD_ERR_UNSUPPORTED, "q/out must be 16-byte aligned");
+  const bool abs_ok = absorbed_supported(*w, *c);
+  if (mode == QSVD_ATTN_ABSORBED && !abs_ok) return fail(QSVD_ERR_UNSUPPORTED, "absorbed form needs r in {128, 512, 1024, 1536}");
+  const bool absorbed = mode == QSVD_ATTN_ABSORBED || (mode == QSVD_ATTN_AUTO && abs_ok);
+  const size_t need = absorbed ? attn_absorbed_workspace(*w, *c) : attn_reconstruct_workspace(*w, *c);
+  if (!ws || ws_bytes < need) return fail(QSVD_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  AttnArgs a{w, c, (const _Float16*)q, (_Float16*)out, sm_scale > 0.f ? sm_scale : 1.f / sqrtf((float)w->head_dim)};
+  hipStream_t s = (hipStream_t)stream;
+  return hip_status(absorbed ? launch_attn_absorbed(a, ws, s) : launch_attn_reconstruct(a, ws, s), "decode attention");
+}
+
+qsvd_status qsvd_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_on = on != 0;
+  return QSVD_OK;
+}
+
+qsvd_status qsvd_profile_reset(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto& r : g_prof) {
+    hipEventDestroy(r.start);
+    hipEventDestroy(r.stop);
+  }
+  g_prof.clear();
+  return QSVD_OK;
+}
+
+qsvd_status qsvd_profile_read(const char* name, double* total_ms, int64_t* launches) {
+  if (!name || !total_ms || !launches) return fail(QSVD_ERR_INVALID_ARG, "NULL argument");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  double tot = 0.0;
+  int64_t n = 0;
+  for (auto& r : g_prof) {
+    if (r.name.find(name) == std::string::npos) continue;
+    hipError_t e = hipEventSynchronize(r.stop);
+    if (e != hipSuccess) return hip_status(e, "profile read");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess) return hip_status(e, "profile read");
+    tot += ms;
+    ++n;
+  }
+  *total_ms = tot;
+  *launches = n;
+  return QSVD_OK;
+}
+
+}  // extern "C"

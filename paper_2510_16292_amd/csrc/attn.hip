@@ -1,0 +1,671 @@
+// Decode attention over the latent cache (Section 3.1: only C is cached and
+// K = C W^u_k, V = C W^u_v are recomputed from it, Eq. 5).
+//
+// Absorbed form (default): since q . (C_t W^u_k)^T = (q W^u_k^T) . C_t and
+// sum_t p_t C_t W^u_v = (sum_t p_t C_t) W^u_v, the query is first mapped into
+// the rank-r latent space once per step, every head then attends directly over
+// the cached latent rows, and W^u_v is applied once to the latent-space result.
+//
+//   absorb_kernel       q~[b][h][:] = (sm_scale * log2 e) * q[b][h] W^u_k,g(h)^T     (fp16)
+//   latent_attn_kernel  per (sequence, context chunk): S = q~ C^T, online softmax,
+//                       O = P C over the chunk -> split partials (m, l, O)
+//   combine_kernel      merge the chunk partials of each sequence
+//   vproj_kernel        o[b][h] = O[b][h] W^u_v,g(h)                               (fp16)
+//
+// Reconstruct form (for comparison): K^, V^ are rebuilt for every cached token
+// with an fp16 matrix-core GEMM and a plain split-context attention follows.
+#include <math.h>
+
+#include "common.h"
+#include "launch.h"
+
+namespace qsvd {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kHeadBlk = 32;   // query heads are padded to one 32-wide MFMA block
+
+// ---------------------------------------------------------------------------
+// Weight code access (int8 or packed int4), transposed layout [N][r].
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wcode(const uint8_t* bt, int32_t r, int32_t n, int32_t j, int bits) {
+  if (bits == 8) return (float)((const int8_t*)bt)[(int64_t)n * r + j];
+  const uint32_t byte = bt[(int64_t)n * (r / 2) + (j >> 1)];
+  return (float)((j & 1) ? nib_hi(byte) : nib_lo(byte));
+}
+
+__device__ __forceinline__ float wscale(const float* sb, int32_t N, int32_t n, int32_t j, int group) {
+  return group ? sb[(int64_t)(j / group) * N + n] : sb[n];
+}
+
+// ---------------------------------------------------------------------------
+// q~ = scale * q W^u_k^T, one thread per latent index j, batch in groups of 8.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, const float* __restrict__ sb,
+              int32_t B, int32_t r, int32_t Hq, int32_t Hkv, int32_t dh, int32_t N, int32_t bits,
+              int32_t group, float scale, _Float16* __restrict__ qt) {
+  __shared__ float qs[64 * 128];
+  const int h = blockIdx.x;
+  const int32_t j = blockIdx.y * 256 + threadIdx.x;
+  if (h >= Hq) {
+    if (j < r)
+      for (int b = 0; b < B; ++b) qt[((int64_t)b * kHeadBlk + h) * r + j] = (_Float16)0.f;
+    return;
+  }
+  for (int e = threadIdx.x; e < B * dh; e += 256) {
+    const int b = e / dh, c = e - b * dh;
+    qs[e] = (float)q[(int64_t)b * Hq * dh + h * dh + c];
+  }
+  __syncthreads();
+  if (j >= r) return;
+  const int g = (h * Hkv) / Hq;
+  const int32_t nk0 = Hq * dh + g * dh;
+  for (int b0 = 0; b0 < B; b0 += 8) {
+    float acc[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+    for (int c = 0; c < dh; ++c) {
+      const int32_t n = nk0 + c;
+      const float wv = wscale(sb, N, n, j, group) * wcode(bt, r, n, j, bits);
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (b0 + k < B) acc[k] = fmaf(qs[(b0 + k) * dh + c], wv, acc[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (b0 + k < B) qt[((int64_t)(b0 + k) * kHeadBlk + h) * r + j] = to_f16(acc[k] * scale);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Latent attention over one context chunk of one sequence.
+//
+// The workgroup has NW waves; wave w owns latent columns [w*RW, (w+1)*RW).
+// Per 32-token tile:
+//   S^T (tokens x heads) = C_tile[:, slice] q~[:, slice]^T   (fp16 MFMA, K = RW)
+//   partial S^T of all waves are summed through LDS in a fixed order
+//   online softmax per head in fp32 (lane l tracks head l % 32)
+//   O^T[slice] (r x heads) += C_tile[:, slice]^T P^T          (fp16 MFMA, K = 32 tokens)
+// The C tile reaches the first MFMA straight from HBM (token-major rows are
+// the A operand as stored) and the second through a wave-private LDS copy.
+// ---------------------------------------------------------------------------
+template <int RW, int NW, int FMT>
+__global__ void __launch_bounds__(NW * 64)
+latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ cdata,
+                   const float* __restrict__ cscale, const int32_t* __restrict__ seq_len,
+                   int32_t capacity, int32_t r, int32_t chunk, int32_t n_chunks,
+                   float* __restrict__ o_part, float* __restrict__ ml_part) {
+  constexpr int KS = RW / 16;    // 16-wide contraction steps of the score MFMA
+  constexpr int RB = RW / 32;    // 32-row blocks of the output MFMA
+  constexpr int CST = RW + 8;    // staged row stride in halves
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  _Float16* cst = reinterpret_cast<_Float16*>(smem) + w * 32 * CST;
+  float* spart = reinterpret_cast<float*>(smem + NW * 32 * CST * 2);
+  float* ssum = spart + NW * 1024;
+
+  const int b = blockIdx.y, ch = blockIdx.x;
+  const int L = min(seq_len[b], capacity);
+  const int t_begin = ch * chunk;
+  if (t_begin >= L) return;
+  const int t_end = min(L, t_begin + chunk);
+  const int slice0 = w * RW;
+
+  f16x8 qf[KS];
+  {
+    const _Float16* qrow = qt + ((int64_t)b * kHeadBlk + l32) * r + slice0 + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + 16 * ks);
+  }
+  f32x16 o[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) o[rb] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  for (int t0 = t_begin; t0 < t_end; t0 += 32) {
+    // A operand of the score MFMA: token (t0 + l32), latent columns 8*half + 16*ks.
+    const int tk = min(t0 + l32, L - 1);
+    f16x8 cf[KS];
+    if (FMT == QSVD_CACHE_F16) {
+      const _Float16* crow = reinterpret_cast<const _Float16*>(cdata) +
+                             ((int64_t)b * capacity + tk) * r + slice0 + 8 * half;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) cf[ks] = *reinterpret_cast<const f16x8*>(crow + 16 * ks);
+    } else {
+      const int8_t* crow = reinterpret_cast<const int8_t*>(cdata) +
+                           ((int64_t)b * capacity + tk) * r + slice0 + 8 * half;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const uint2 raw = *reinterpret_cast<const uint2*>(crow + 16 * ks);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          cf[ks][e] = (_Float16)(float)(int8_t)(raw.x >> (8 * e));
+          cf[ks][4 + e] = (_Float16)(float)(int8_t)(raw.y >> (8 * e));
+        }
+      }
+    }
+    f32x16 sacc = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_f16(cf[ks], qf[ks], sacc, 0, 0, 0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      *reinterpret_cast<f16x8*>(cst + l32 * CST + 16 * ks + 8 * half) = cf[ks];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) spart[(w * 16 + v) * 64 + lane] = sacc[v];
+    __syncthreads();
+    for (int e = tid; e < 1024; e += NW * 64) {
+      float acc = 0.f;
+#pragma unroll
+      for (int w2 = 0; w2 < NW; ++w2) acc += spart[w2 * 1024 + e];
+      ssum[e] = acc;
+    }
+    __syncthreads();
+    // Lane l holds head l32 and tokens t0 + 8*(v/4) + 4*half + v%4.
+    float s[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
+      float x = ssum[v * 64 + lane];
+      if (FMT != QSVD_CACHE_F16) x *= cscale[(int64_t)b * capacity + min(t, L - 1)];
+      s[v] = (t < t_end) ? x : -INFINITY;
+    }
+    float mx = s[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[v]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    float alpha = 1.f, ps = 0.f;
+    float p[16];
+    if (m_new == -INFINITY) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) p[v] = 0.f;
+    } else {
+      alpha = exp2f(m_run - m_new);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        p[v] = exp2f(s[v] - m_new);
+        ps += p[v];
+      }
+    }
+    ps += __shfl_xor(ps, 32, 64);
+    l_run = l_run * alpha + ps;
+    m_run = m_new;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[rb][v] *= alpha;
+    // P^T as the B operand: k-slot (half, e) of MFMA mf is token 16*mf + 8*(e/4) + 4*half + e%4,
+    // exactly the tokens this lane already holds in p[8*mf + e].
+    f16x8 pf[2];
+#pragma unroll
+    for (int mf = 0; mf < 2; ++mf)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float pv = p[8 * mf + e];
+        if (FMT != QSVD_CACHE_F16) {
+          const int t = t0 + 16 * mf + 8 * (e >> 2) + 4 * half + (e & 3);
+          pv *= cscale[(int64_t)b * capacity + min(t, L - 1)];
+        }
+        pf[mf][e] = (_Float16)pv;
+      }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int mf = 0; mf < 2; ++mf) {
+        f16x8 a;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int tau = 16 * mf + 8 * (e >> 2) + 4 * half + (e & 3);
+          a[e] = cst[tau * CST + rb * 32 + l32];
+        }
+        o[rb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pf[mf], o[rb], 0, 0, 0);
+      }
+  }
+
+  const int64_t part = (int64_t)b * n_chunks + ch;
+  if (w == 0 && lane < 32) {
+    ml_part[part * 64 + l32] = m_run;
+    ml_part[part * 64 + 32 + l32] = l_run;
+  }
+  // O^T: lane holds head l32, latent rows slice0 + 32*rb + 8*(v/4) + 4*half + v%4.
+  float* op = o_part + part * (int64_t)r * kHeadBlk;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = slice0 + 32 * rb + 8 * (v >> 2) + 4 * half + (v & 3);
+      op[(int64_t)row * kHeadBlk + l32] = o[rb][v];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Merge the chunk partials of a sequence: m = max m_c, w_c = 2^(m_c - m),
+// O = sum_c w_c O_c / sum_c w_c l_c.  Partials are [x][32 heads]; the result is
+// written head-major, fp32 [b][32][width] or the final fp16 [b][Hq*width].
+// ---------------------------------------------------------------------------
+template <bool F16OUT>
+__global__ void __launch_bounds__(256)
+combine_kernel(const float* __restrict__ o_part, const float* __restrict__ ml_part,
+               const int32_t* __restrict__ seq_len, int32_t chunk, int32_t n_chunks, int32_t n_launched,
+               int32_t width, int32_t Hq, float* __restrict__ o_lat, _Float16* __restrict__ out) {
+  __shared__ float tile[32][33];
+  const int b = blockIdx.y, x0 = blockIdx.x * 32, tid = threadIdx.x;
+  const int L = seq_len[b];
+  const int nv = L > 0 ? min((L + chunk - 1) / chunk, n_launched) : 0;
+  const int64_t pb = (int64_t)b * n_chunks;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = tid + 256 * i, xl = e >> 5, h = e & 31;
+    float m = -INFINITY;
+    for (int c = 0; c < nv; ++c) m = fmaxf(m, ml_part[(pb + c) * 64 + h]);
+    float acc = 0.f, lsum = 0.f;
+    for (int c = 0; c < nv; ++c) {
+      const float wc = exp2f(ml_part[(pb + c) * 64 + h] - m);
+      lsum += wc * ml_part[(pb + c) * 64 + 32 + h];
+      acc += wc * o_part[((pb + c) * width + x0 + xl) * kHeadBlk + h];
+    }
+    tile[xl][h] = lsum > 0.f ? acc / lsum : 0.f;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = tid + 256 * i, h = e >> 5, xl = e & 31;
+    const float v = tile[xl][h];
+    if (F16OUT) {
+      if (h < Hq) out[((int64_t)b * Hq + h) * width + x0 + xl] = to_f16(v);
+    } else {
+      o_lat[((int64_t)b * kHeadBlk + h) * width + x0 + xl] = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// o[b][h*dh + c] = sum_j O[b][h][j] * W^u_v[j][n], n = Hq*dh + Hkv*dh + g(h)*dh + c.
+// One workgroup per (head, 32 output columns); latent index in tiles of 128.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+vproj_kernel(const float* __restrict__ o_lat, const uint8_t* __restrict__ bt, const float* __restrict__ sb,
+             int32_t B, int32_t r, int32_t Hq, int32_t Hkv, int32_t dh, int32_t N, int32_t bits,
+             int32_t group, _Float16* __restrict__ out) {
+  __shared__ float bs[32 * 129];
+  __shared__ float os[64 * 128];
+  const int h = blockIdx.x, c0 = blockIdx.y * 32, tid = threadIdx.x;
+  const int cl = tid & 31, bq = tid >> 5;
+  const int g = (h * Hkv) / Hq;
+  const int32_t nb = Hq * dh + Hkv * dh + g * dh + c0;
+  float acc[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+  for (int j0 = 0; j0 < r; j0 += 128) {
+    const int jn = min(128, r - j0);
+    for (int e = tid; e < 32 * 128; e += 256) {
+      const int row = e >> 7, jj = e & 127;
+      float v = 0.f;
+      if (jj < jn) {
+        const int32_t n = nb + row, j = j0 + jj;
+        v = wcode(bt, r, n, j, bits);
+        if (group) v *= sb[(int64_t)(j / group) * N + n];
+      }
+      bs[row * 129 + jj] = v;
+    }
+    for (int e = tid; e < B * 128; e += 256) {
+      const int bb = e >> 7, jj = e & 127;
+      os[e] = (jj < jn) ? o_lat[((int64_t)bb * kHeadBlk + h) * r + j0 + jj] : 0.f;
+    }
+    __syncthreads();
+    for (int jj = 0; jj < 128; ++jj) {
+      const float wv = bs[cl * 129 + jj];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (bq + 8 * k < B) acc[k] = fmaf(os[(bq + 8 * k) * 128 + jj], wv, acc[k]);
+    }
+    __syncthreads();
+  }
+  const float cs = group ? 1.f : sb[nb + cl];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int bb = bq + 8 * k;
+    if (bb < B) out[(int64_t)bb * Hq * dh + h * dh + c0 + cl] = to_f16(acc[k] * cs);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host side of the absorbed form.
+// ---------------------------------------------------------------------------
+struct AbsorbPlan {
+  int rw, nw;
+  int chunk, n_chunks, n0;
+  size_t qt_bytes, opart_bytes, ml_bytes, olat_bytes;
+};
+
+static int target_chunks(int batch) {
+  const int n0 = (256 + batch - 1) / batch;
+  return n0 < 1 ? 1 : n0;
+}
+
+static bool pick_slice(int r, int* rw, int* nw) {
+  static const int opts[][2] = {{192, 8}, {128, 8}, {64, 8}, {32, 4}};
+  for (auto& o : opts)
+    if (r == o[0] * o[1]) { *rw = o[0]; *nw = o[1]; return true; }
+  return false;
+}
+
+static AbsorbPlan plan_absorbed(const qsvd_layer& w, const qsvd_cache& c) {
+  AbsorbPlan p{};
+  pick_slice(w.r, &p.rw, &p.nw);
+  p.n0 = target_chunks(c.batch);
+  const int len = c.max_len > 0 ? c.max_len : 1;
+  int ch = (len + p.n0 - 1) / p.n0;
+  ch = ((ch + 31) / 32) * 32;
+  p.chunk = ch;
+  p.n_chunks = (len + ch - 1) / ch;
+  p.qt_bytes = (size_t)c.batch * kHeadBlk * w.r * sizeof(_Float16);
+  p.opart_bytes = (size_t)c.batch * p.n0 * w.r * kHeadBlk * sizeof(float);
+  p.ml_bytes = (size_t)c.batch * p.n0 * 64 * sizeof(float);
+  p.olat_bytes = (size_t)c.batch * kHeadBlk * w.r * sizeof(float);
+  return p;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool absorbed_supported(const qsvd_layer& w, const qsvd_cache& c) {
+  int rw, nw;
+  return pick_slice(w.r, &rw, &nw) && c.fmt != QSVD_CACHE_I4;
+}
+
+size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c) {
+  const AbsorbPlan p = plan_absorbed(w, c);
+  return align256(p.qt_bytes) + align256(p.opart_bytes) + align256(p.ml_bytes) + align256(p.olat_bytes);
+}
+
+template <int RW, int NW, int FMT>
+static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, const _Float16* qt,
+                                float* opart, float* ml, hipStream_t s) {
+  const size_t lds = (size_t)NW * 32 * (RW + 8) * 2 + (size_t)(NW + 1) * 1024 * 4;
+  auto kern = latent_attn_kernel<RW, NW, FMT>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  KernelScope ks("latent_attn", s);
+  hipLaunchKernelGGL(kern, dim3(p.n_chunks, c.batch), dim3(NW * 64), lds, s, qt,
+                     (const uint8_t*)c.data, c.scale, c.seq_len, c.capacity, c.r, p.chunk,
+                     p.n0, opart, ml);
+  return hipGetLastError();
+}
+
+template <int FMT>
+static hipError_t dispatch_latent(const AbsorbPlan& p, const qsvd_cache& c, const _Float16* qt,
+                                  float* opart, float* ml, hipStream_t s) {
+  if (p.rw == 192) return launch_latent<192, 8, FMT>(p, c, qt, opart, ml, s);
+  if (p.rw == 128) return launch_latent<128, 8, FMT>(p, c, qt, opart, ml, s);
+  if (p.rw == 64) return launch_latent<64, 8, FMT>(p, c, qt, opart, ml, s);
+  return launch_latent<32, 4, FMT>(p, c, qt, opart, ml, s);
+}
+
+hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
+  const qsvd_layer& w = *a.w;
+  const qsvd_cache& c = *a.c;
+  const AbsorbPlan p = plan_absorbed(w, c);
+  uint8_t* base = (uint8_t*)ws;
+  _Float16* qt = (_Float16*)base;
+  base += align256(p.qt_bytes);
+  float* opart = (float*)base;
+  base += align256(p.opart_bytes);
+  float* ml = (float*)base;
+  base += align256(p.ml_bytes);
+  float* olat = (float*)base;
+  const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
+  {
+    KernelScope ks("absorb_q", s);
+    hipLaunchKernelGGL(absorb_kernel, dim3(kHeadBlk, (w.r + 255) / 256), dim3(256), 0, s, a.q,
+                       (const uint8_t*)w.b_t, w.s_b, c.batch, w.r, w.n_q_heads, w.n_kv_heads,
+                       w.head_dim, N, w.w_bits, w.w_group, a.sm_scale * kLog2e, qt);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = (c.fmt == QSVD_CACHE_F16) ? dispatch_latent<QSVD_CACHE_F16>(p, c, qt, opart, ml, s)
+                                : dispatch_latent<QSVD_CACHE_I8>(p, c, qt, opart, ml, s);
+  if (e != hipSuccess) return e;
+  {
+    KernelScope ks("combine", s);
+    hipLaunchKernelGGL(combine_kernel<false>, dim3(w.r / 32, c.batch), dim3(256), 0, s, opart, ml,
+                       c.seq_len, p.chunk, p.n0, p.n_chunks, w.r, w.n_q_heads, olat, (_Float16*)nullptr);
+  }
+  {
+    KernelScope ks("vproj", s);
+    hipLaunchKernelGGL(vproj_kernel, dim3(w.n_q_heads, w.head_dim / 32), dim3(256), 0, s, olat,
+                       (const uint8_t*)w.b_t, w.s_b, c.batch, w.r, w.n_q_heads, w.n_kv_heads,
+                       w.head_dim, N, w.w_bits, w.w_group, a.out);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Reconstruct form.
+// recon_kv_kernel: KV^[b][t][n'] = C^[b][t][:] . W^u[:, Hq*dh + n'] for n' < 2*Hkv*dh,
+// an fp16 MFMA GEMM (128 x 128 tiles, K in steps of 32) whose loaders turn the
+// stored latent (fp16 or int8 codes) and the weight codes into exact fp16
+// operands; per-channel weight scales and int8 token scales are applied to the
+// fp32 accumulator (per-group scales, which vary along the contraction, are
+// folded into the fp16 weight operand).
+// ---------------------------------------------------------------------------
+constexpr int RBM = 128, RBN = 128, RBK = 32, RLD = RBK + 8;
+
+template <int FMT>
+__global__ void __launch_bounds__(256)
+recon_kv_kernel(const uint8_t* __restrict__ cdata, const float* __restrict__ cscale,
+                const int32_t* __restrict__ seq_len, int32_t capacity, int32_t r,
+                const uint8_t* __restrict__ bt, const float* __restrict__ sb, int32_t N, int32_t nq,
+                int32_t nkv2, int32_t bits, int32_t group, _Float16* __restrict__ kv) {
+  __shared__ __attribute__((aligned(16))) _Float16 As[RBM * RLD];
+  __shared__ __attribute__((aligned(16))) _Float16 Bs[RBN * RLD];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w >> 1, wn = w & 1, half = lane >> 5, l32 = lane & 31;
+  const int b = blockIdx.z;
+  const int L = min(seq_len[b], capacity);
+  const int t0 = blockIdx.y * RBM, n0 = blockIdx.x * RBN;
+  if (t0 >= L) return;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+  for (int k0 = 0; k0 < r; k0 += RBK) {
+    // A: 128 tokens x 32 latent values, thread -> (row tid/2, 16 values at 16*(tid%2))
+    {
+      const int row = tid >> 1, col = (tid & 1) * 16, t = t0 + row;
+      _Float16 vals[16];
+      if (t < L) {
+        if (FMT == QSVD_CACHE_F16) {
+          const _Float16* src = reinterpret_cast<const _Float16*>(cdata) + ((int64_t)b * capacity + t) * r + k0 + col;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) vals[e] = src[e];
+        } else {
+          const int8_t* src = reinterpret_cast<const int8_t*>(cdata) + ((int64_t)b * capacity + t) * r + k0 + col;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) vals[e] = (_Float16)(float)src[e];
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) vals[e] = (_Float16)0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) As[row * RLD + col + e] = vals[e];
+    }
+    // B: 128 output columns x 32 latent values of dequantized W^u
+    {
+      const int row = tid >> 1, col = (tid & 1) * 16, nn = n0 + row;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        float v = 0.f;
+        if (nn < nkv2) {
+          const int32_t n = nq + nn, j = k0 + col + e;
+          v = wcode(bt, r, n, j, bits);
+          if (group) v *= sb[(int64_t)(j / group) * N + n];
+        }
+        Bs[row * RLD + col + e] = (_Float16)v;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < RBK; kk += 16) {
+      f16x8 af[2], bf[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        af[i] = *reinterpret_cast<const f16x8*>(&As[(wm * 64 + i * 32 + l32) * RLD + kk + 8 * half]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        bf[j] = *reinterpret_cast<const f16x8*>(&Bs[(wn * 64 + j * 32 + l32) * RLD + kk + 8 * half]);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int nn = n0 + wn * 64 + j * 32 + l32;
+      if (nn >= nkv2) continue;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int t = t0 + wm * 64 + i * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+        if (t >= L) continue;
+        float y = acc[i][j][v];
+        if (!group) y *= sb[nq + nn];
+        if (FMT != QSVD_CACHE_F16) y *= cscale[(int64_t)b * capacity + t];
+        kv[((int64_t)b * capacity + t) * nkv2 + nn] = to_f16(y);
+      }
+    }
+}
+
+// Plain split-context attention over rebuilt K^, V^: one workgroup per
+// (context chunk of 64 tokens, sequence), all query heads.
+constexpr int RCH = 64;
+
+__global__ void __launch_bounds__(256)
+recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ kv,
+                  const int32_t* __restrict__ seq_len, int32_t capacity, int32_t Hq, int32_t Hkv,
+                  int32_t dh, float scale, int32_t n_chunks, float* __restrict__ o_part,
+                  float* __restrict__ ml_part) {
+  __shared__ float qs[32 * 128];
+  __shared__ float ss[32 * RCH];
+  __shared__ float ml[64];
+  const int b = blockIdx.y, ch = blockIdx.x, tid = threadIdx.x;
+  const int L = min(seq_len[b], capacity);
+  const int t0 = ch * RCH;
+  if (t0 >= L) return;
+  const int tn = min(RCH, L - t0);
+  const int nkv = Hkv * dh, nkv2 = 2 * nkv;
+  for (int e = tid; e < Hq * dh; e += 256) qs[e] = (float)q[(int64_t)b * Hq * dh + e] * scale;
+  __syncthreads();
+  for (int e = tid; e < Hq * RCH; e += 256) {
+    const int h = e / RCH, tl = e - h * RCH;
+    float acc = -INFINITY;
+    if (tl < tn) {
+      const int g = (h * Hkv) / Hq;
+      const _Float16* krow = kv + ((int64_t)b * capacity + t0 + tl) * nkv2 + g * dh;
+      acc = 0.f;
+      for (int c = 0; c < dh; ++c) acc = fmaf(qs[h * dh + c], (float)krow[c], acc);
+    }
+    ss[e] = acc;
+  }
+  __syncthreads();
+  if (tid < Hq) {
+    float m = -INFINITY;
+    for (int tl = 0; tl < tn; ++tl) m = fmaxf(m, ss[tid * RCH + tl]);
+    float l = 0.f;
+    for (int tl = 0; tl < RCH; ++tl) {
+      const float pv = (tl < tn) ? exp2f(ss[tid * RCH + tl] - m) : 0.f;
+      ss[tid * RCH + tl] = pv;
+      l += pv;
+    }
+    ml[tid] = m;
+    ml[32 + tid] = l;
+  }
+  __syncthreads();
+  const int64_t part = (int64_t)b * n_chunks + ch;
+  if (tid < 32) {
+    ml_part[part * 64 + tid] = tid < Hq ? ml[tid] : 0.f;
+    ml_part[part * 64 + 32 + tid] = tid < Hq ? ml[32 + tid] : 1.f;
+  }
+  // O^T[c][h] = sum_t p[h][t] V^[t][g(h)*dh + c]
+  for (int e = tid; e < dh * 32; e += 256) {
+    const int c = e >> 5, h = e & 31;
+    float acc = 0.f;
+    if (h < Hq) {
+      const int g = (h * Hkv) / Hq;
+      const _Float16* vcol = kv + ((int64_t)b * capacity + t0) * nkv2 + nkv + g * dh + c;
+      for (int tl = 0; tl < tn; ++tl) acc = fmaf(ss[h * RCH + tl], (float)vcol[(int64_t)tl * nkv2], acc);
+    }
+    o_part[(part * dh + c) * kHeadBlk + h] = acc;
+  }
+}
+
+struct ReconPlan {
+  size_t kv_bytes, opart_bytes, ml_bytes;
+  int n_chunks;
+};
+
+static ReconPlan plan_recon(const qsvd_layer& w, const qsvd_cache& c) {
+  ReconPlan p{};
+  const int nkv2 = 2 * w.n_kv_heads * w.head_dim;
+  p.n_chunks = (c.capacity + RCH - 1) / RCH;
+  p.kv_bytes = (size_t)c.batch * c.capacity * nkv2 * sizeof(_Float16);
+  p.opart_bytes = (size_t)c.batch * p.n_chunks * w.head_dim * kHeadBlk * sizeof(float);
+  p.ml_bytes = (size_t)c.batch * p.n_chunks * 64 * sizeof(float);
+  return p;
+}
+
+size_t attn_reconstruct_workspace(const qsvd_layer& w, const qsvd_cache& c) {
+  const ReconPlan p = plan_recon(w, c);
+  return align256(p.kv_bytes) + align256(p.opart_bytes) + align256(p.ml_bytes);
+}
+
+hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
+  const qsvd_layer& w = *a.w;
+  const qsvd_cache& c = *a.c;
+  const ReconPlan p = plan_recon(w, c);
+  uint8_t* base = (uint8_t*)ws;
+  _Float16* kv = (_Float16*)base;
+  base += align256(p.kv_bytes);
+  float* opart = (float*)base;
+  base += align256(p.opart_bytes);
+  float* ml = (float*)base;
+  const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
+  const int nq = w.n_q_heads * w.head_dim, nkv2 = 2 * w.n_kv_heads * w.head_dim;
+  const int len = c.max_len > 0 ? c.max_len : 1;
+  {
+    dim3 grid((nkv2 + RBN - 1) / RBN, (len + RBM - 1) / RBM, c.batch);
+    KernelScope ks("recon_kv", s);
+    if (c.fmt == QSVD_CACHE_F16)
+      hipLaunchKernelGGL(recon_kv_kernel<QSVD_CACHE_F16>, grid, dim3(256), 0, s, (const uint8_t*)c.data,
+                         c.scale, c.seq_len, c.capacity, c.r, (const uint8_t*)w.b_t, w.s_b, N, nq, nkv2,
+                         w.w_bits, w.w_group, kv);
+    else
+      hipLaunchKernelGGL(recon_kv_kernel<QSVD_CACHE_I8>, grid, dim3(256), 0, s, (const uint8_t*)c.data,
+                         c.scale, c.seq_len, c.capacity, c.r, (const uint8_t*)w.b_t, w.s_b, N, nq, nkv2,
+                         w.w_bits, w.w_group, kv);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int nch = (len + RCH - 1) / RCH;
+  {
+    KernelScope ks("recon_attn", s);
+    hipLaunchKernelGGL(recon_attn_kernel, dim3(nch, c.batch), dim3(256), 0, s, a.q, kv, c.seq_len,
+                       c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, a.sm_scale * kLog2e,
+                       p.n_chunks, opart, ml);
+  }
+  {
+    KernelScope ks("recon_combine", s);
+    hipLaunchKernelGGL(combine_kernel<true>, dim3(w.head_dim / 32, c.batch), dim3(256), 0, s, opart, ml,
+                       c.seq_len, RCH, p.n_chunks, nch, w.head_dim, w.n_q_heads, (float*)nullptr, a.out);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace qsvd

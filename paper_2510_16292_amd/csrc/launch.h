@@ -1,0 +1,60 @@
+// Internal host-side launch wrappers (validated arguments only).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "qsvd.h"
+
+namespace qsvd {
+
+// Records kernel timing events when the profiler is enabled (api.hip).
+struct KernelScope {
+  KernelScope(const char* name, hipStream_t s);
+  ~KernelScope();
+  const char* name_;
+  hipStream_t s_;
+  int slot_;
+};
+
+hipError_t launch_quantize_rows(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits,
+                                float clip, void* xq, float* sx, hipStream_t s);
+
+// C[m][n] = sum_k A[m][k] * B[n][k] for int8 A [M][K] and int8 B [N][K], scaled
+// per row and per column, written to up to three fp16 column segments.
+struct OutSeg {
+  _Float16* ptr;   // NULL: columns of this segment are not stored
+  int64_t ld;      // row stride of ptr in elements
+  int32_t n0;      // first column of the segment in the full product
+  int32_t n;       // columns in the segment
+};
+struct GemmArgs {
+  const int8_t* a;      // [M][K]
+  const int8_t* b;      // [N][K] (rows n_begin.. of the weight)
+  const float* row_scale;
+  const float* col_scale;
+  int64_t M;
+  int32_t N;            // columns computed
+  int32_t K;
+  OutSeg seg[3];
+  int32_t n_seg;
+  int32_t* dbg;         // optional int32 [M][N]
+};
+hipError_t launch_gemm_i8(const GemmArgs& g, void* ws, hipStream_t s);
+size_t gemm_i8_workspace(int64_t M, int32_t N, int32_t K);
+
+hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void* cq,
+                               const float* sc, int32_t n_new, hipStream_t s);
+
+struct AttnArgs {
+  const qsvd_layer* w;
+  const qsvd_cache* c;
+  const _Float16* q;
+  _Float16* out;
+  float sm_scale;
+};
+size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c);
+hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s);
+size_t attn_reconstruct_workspace(const qsvd_layer& w, const qsvd_cache& c);
+hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s);
+
+}  // namespace qsvd

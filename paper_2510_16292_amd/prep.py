@@ -1,0 +1,105 @@
+"""Offline stage of QSVD: turn a layer's [W_q | W_k | W_v] into the quantized,
+transposed factors the HIP library consumes.
+
+This runs once per layer on the host before inference, as in the paper
+(Section 3.1: joint SVD and truncation, Eq. 2-4; Section 3.3 / Section 4:
+round-to-nearest symmetric weight quantization).  It is not part of the
+per-token hot path.
+
+Conventions (shared with the C ABI, include/qsvd.h):
+  * Y = X W with W of shape d x N; W^d = U_r Sigma_r^beta (d x r) and
+    W^u = Sigma_r^(1-beta) V_r^T (r x N).
+  * Right singular vectors are sign-normalized: the entry of largest magnitude
+    of each is positive (the left vector flips with it).
+  * Weight codes are rint(w / s) in fp64 with the scale s = clip*max|w|/Qm
+    rounded to fp32 (1 for an all-zero column or group), clamped to [-Qm, Qm];
+    per output channel (w_group 0) or per output channel and per block of
+    w_group contraction rows.
+  * Device layout is transposed (contraction index contiguous): a_t [r][d],
+    b_t [N][r]; int4 codes pack element 2i in the low nibble of byte i.
+"""
+from dataclasses import dataclass
+
+import numpy as np
+
+
+@dataclass
+class PreparedLayer:
+    d: int
+    r: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    w_bits: int
+    w_group: int
+    a_t: np.ndarray     # int8 [r][d] or uint8 [r][d/2]
+    s_a: np.ndarray     # fp32 [r] or [d/G][r]
+    b_t: np.ndarray     # int8 [N][r] or uint8 [N][r/2]
+    s_b: np.ndarray     # fp32 [N] or [r/G][N]
+
+    @property
+    def N(self):
+        return (self.n_q_heads + 2 * self.n_kv_heads) * self.head_dim
+
+
+def truncated_factors(W: np.ndarray, r: int, beta: float):
+    """(W^d, W^u) of the rank-r joint SVD of W with Sigma split by beta."""
+    U, s, Vt = np.linalg.svd(np.asarray(W, dtype=np.float64), full_matrices=False)
+    lead = np.abs(Vt).argmax(axis=1)
+    flip = np.where(Vt[np.arange(len(s)), lead] < 0, -1.0, 1.0)
+    U, Vt = U * flip, Vt * flip[:, None]
+    return factors_from_svd(U[:, :r], s[:r], Vt[:r].T, beta)
+
+
+def factors_from_svd(U_r: np.ndarray, sigma_r: np.ndarray, V_r: np.ndarray, beta: float):
+    """W^d = U_r diag(sigma^beta), W^u = diag(sigma^(1-beta)) V_r^T."""
+    return U_r * np.power(sigma_r, beta), (V_r * np.power(sigma_r, 1.0 - beta)).T
+
+
+def _quantize_t(Wt: np.ndarray, bits: int, group: int, clip: float):
+    """Quantize a transposed weight Wt [Nout][K] along K; returns codes [Nout][K]
+    and scales [Nout] or [K/group][Nout]."""
+    qm = float((1 << (bits - 1)) - 1)
+    n_out, K = Wt.shape
+    if group:
+        blocks = Wt.reshape(n_out, K // group, group)
+        amax = np.abs(blocks).max(axis=2)                       # [Nout][G]
+        scale = np.where(amax == 0, np.float32(1), (clip * amax / qm).astype(np.float32)).astype(np.float32)
+        codes = np.rint(blocks / scale.astype(np.float64)[:, :, None]).reshape(n_out, K)
+        scale = np.ascontiguousarray(scale.T)                    # [G][Nout]
+    else:
+        amax = np.abs(Wt).max(axis=1)
+        scale = np.where(amax == 0, np.float32(1), (clip * amax / qm).astype(np.float32)).astype(np.float32)
+        codes = np.rint(Wt / scale.astype(np.float64)[:, None])
+    codes = np.clip(codes, -qm, qm).astype(np.int8)
+    return codes, scale
+
+
+def pack_int4_rows(codes: np.ndarray) -> np.ndarray:
+    """Pack int8 codes in [-8, 7] two per byte along the last axis (even index low)."""
+    c = codes.astype(np.uint8) & 0x0F
+    return np.ascontiguousarray(c[..., 0::2] | (c[..., 1::2] << 4))
+
+
+def quantize_layer(A: np.ndarray, B: np.ndarray, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                   w_bits: int = 8, w_group: int = 0, clip: float = 1.0) -> PreparedLayer:
+    """Quantize W^d (d x r) and W^u (r x N) and lay them out for the device."""
+    d, r = A.shape
+    assert B.shape[0] == r and B.shape[1] == (n_q_heads + 2 * n_kv_heads) * head_dim
+    a_codes, s_a = _quantize_t(np.ascontiguousarray(A.T), w_bits, w_group, clip)   # [r][d]
+    b_codes, s_b = _quantize_t(np.ascontiguousarray(B.T), w_bits, w_group, clip)   # [N][r]
+    if w_bits == 4:
+        a_codes, b_codes = pack_int4_rows(a_codes), pack_int4_rows(b_codes)
+    return PreparedLayer(d, r, n_q_heads, n_kv_heads, head_dim, w_bits, w_group,
+                         np.ascontiguousarray(a_codes), s_a, np.ascontiguousarray(b_codes), s_b)
+
+
+def prepare_from_weight(W, r, n_q_heads, n_kv_heads, head_dim, beta=0.5, w_bits=8, w_group=0, clip=1.0):
+    A, B = truncated_factors(W, r, beta)
+    return quantize_layer(A, B, n_q_heads, n_kv_heads, head_dim, w_bits, w_group, clip)
+
+
+def prepare_from_svd(U_r, sigma_r, V_r, n_q_heads, n_kv_heads, head_dim, beta=0.5, w_bits=8, w_group=0,
+                     clip=1.0):
+    A, B = factors_from_svd(U_r, sigma_r, V_r, beta)
+    return quantize_layer(A, B, n_q_heads, n_kv_heads, head_dim, w_bits, w_group, clip)

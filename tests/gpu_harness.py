@@ -1,0 +1,112 @@
+"""Small helpers for the GPU tests: upload seeded inputs, call the C ABI
+through the binding, download results.  No arithmetic of the method here."""
+import sys
+
+import numpy as np
+
+from paper_2510_16292_amd import binding as B
+
+
+def torch():
+    import torch as _t
+    return _t
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def dev(a):
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+
+def host(t):
+    torch().cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def empty(shape, dtype):
+    t = torch()
+    return t.empty(shape, dtype=dtype, device="cuda")
+
+
+def quantize_act(x_np, bits=8, clip=1.0, K=None):
+    """x_np fp16 [M][ld]; quantizes the first K columns (default all).
+    Returns (xq bytes [M][K or K/2], sx [M])."""
+    t = torch()
+    M, ld = x_np.shape
+    K = ld if K is None else K
+    x = dev(x_np)
+    width = K if bits == 8 else K // 2
+    xq = t.empty((M, width), dtype=t.uint8, device="cuda")
+    sx = t.empty((M,), dtype=t.float32, device="cuda")
+    B.check(B.qsvd_quantize_act(B.ptr(x), M, K, ld, bits, clip, B.ptr(xq), B.ptr(sx), B.stream_handle()))
+    return host(xq), host(sx)
+
+
+class Prefill:
+    """Device buffers for one projection call of M tokens."""
+
+    def __init__(self, dl, M, mask=7, debug=True):
+        t = torch()
+        self.dl, self.M, self.mask = dl, M, mask
+        nq, nkv, r, N = dl.n_q_heads * dl.head_dim, dl.n_kv_heads * dl.head_dim, dl.r, dl.N
+        self.xq = t.empty((M, dl.d), dtype=t.int8, device="cuda")
+        self.sx = t.empty((M,), dtype=t.float32, device="cuda")
+        self.c_h = t.empty((M, r), dtype=t.float16, device="cuda")
+        self.cq = t.empty((M, r), dtype=t.int8, device="cuda")
+        self.sc = t.empty((M,), dtype=t.float32, device="cuda")
+        self.q = t.empty((M, nq), dtype=t.float16, device="cuda")
+        self.k = t.empty((M, nkv), dtype=t.float16, device="cuda")
+        self.v = t.empty((M, nkv), dtype=t.float16, device="cuda")
+        self.acc_xa = t.empty((M, r), dtype=t.int32, device="cuda") if debug else None
+        self.acc_cb = t.empty((M, N), dtype=t.int32, device="cuda") if debug else None
+        self.ws_bytes = B.qsvd_prefill_workspace_size(dl.c, M, mask)
+        self.ws = t.empty((max(self.ws_bytes, 1),), dtype=t.uint8, device="cuda")
+
+    def run(self, x):
+        """x: device fp16 [M][d]."""
+        s = B.stream_handle()
+        B.check(B.qsvd_quantize_act(B.ptr(x), self.M, self.dl.d, self.dl.d, 8, 1.0, B.ptr(self.xq),
+                                    B.ptr(self.sx), s))
+        B.check(B.qsvd_lowrank_qkv_prefill(self.dl.c, B.ptr(self.xq), B.ptr(self.sx), self.M, 8, self.mask,
+                                           B.ptr(self.c_h), B.ptr(self.cq), B.ptr(self.sc), B.ptr(self.q),
+                                           B.ptr(self.k), B.ptr(self.v), B.ptr(self.acc_xa), B.ptr(self.acc_cb),
+                                           B.ptr(self.ws), self.ws_bytes, s))
+        return self
+
+    def result(self):
+        out = dict(xq=host(self.xq), sx=host(self.sx), C_h=host(self.c_h), cq=host(self.cq), sc=host(self.sc))
+        if self.mask & B.QSVD_OUT_Q:
+            out["Q"] = host(self.q)
+        if self.mask & B.QSVD_OUT_K:
+            out["K"] = host(self.k)
+        if self.mask & B.QSVD_OUT_V:
+            out["V"] = host(self.v)
+        if self.acc_xa is not None:
+            out["acc_xa"], out["acc_cb"] = host(self.acc_xa), host(self.acc_cb)
+        return out
+
+
+def decode_attention(dl, dc, q_dev, mode, sm_scale=0.0):
+    t = torch()
+    out = t.empty_like(q_dev)
+    ws_bytes = B.qsvd_decode_workspace_size(dl.c, dc.c, 1, mode)
+    ws = t.empty((max(ws_bytes, 1),), dtype=t.uint8, device="cuda")
+    B.check(B.qsvd_latent_decode_attention(dl.c, dc.c, B.ptr(q_dev), 1, mode, sm_scale, B.ptr(out), B.ptr(ws),
+                                           ws_bytes, B.stream_handle()))
+    return out
+
+
+def append(dc, c_h=None, cq=None, sc=None, n_new=1):
+    B.check(B.qsvd_latent_cache_append(dc.c, B.ptr(c_h), B.ptr(cq), B.ptr(sc), n_new, B.stream_handle()))
+
+
+def close_enough(got, want, max_abs=2e-2, rel_l2=1e-2):
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    err = np.abs(got - want)
+    rel = np.linalg.norm(got - want) / max(np.linalg.norm(want), 1e-30)
+    return err.max() <= max_abs and rel <= rel_l2, (float(err.max()), float(rel), float(np.sqrt(np.mean(want ** 2))))

@@ -1,0 +1,287 @@
+"""HIP path against the oracle, element by element, through the C ABI.
+
+Bit-exact: activation and latent codes and scales, the int32 accumulators,
+the fp16 latent C and the fp16 Q/K/V (the epilogues follow the oracle's
+rounding order), and every cache byte.  Toleranced: attention outputs,
+max-abs 2e-2 and relative L2 1e-2 against the fp64 plain definition.
+"""
+import numpy as np
+import pytest
+
+import gpu_harness as H
+from oracle import qsvd_oracle as O
+from paper_2510_16292_amd import binding as B
+from paper_2510_16292_amd import prep
+from workloads import configs, gen
+
+pytestmark = pytest.mark.gpu
+
+MODES = [B.QSVD_ATTN_ABSORBED, B.QSVD_ATTN_RECONSTRUCT]
+MODE_IDS = ["absorbed", "reconstruct"]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    B.lib()   # fails loudly if the HIP library is not built
+
+
+# ------------------------------------------------------------------ layers
+
+def _layers_from_weight(W, L, beta=0.5, w_bits=8, w_group=0):
+    A, Bm = O.factors_from_weight(W, L.r, beta)
+    ol = O.make_layer(A, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, w_bits, w_group)
+    pl = prep.prepare_from_weight(W, L.r, L.n_q_heads, L.n_kv_heads, L.head_dim, beta, w_bits, w_group)
+    return ol, B.DeviceLayer(pl)
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    wl = configs.get(1)
+    ol, dl = _layers_from_weight(gen.weight_matrix(wl), wl.layer)
+    return wl, ol, dl
+
+
+@pytest.fixture(scope="module")
+def gqa():
+    """A small grouped-query layer: 8 query heads over 2 key/value heads."""
+    L = configs.LayerShape(d=256, n_q_heads=8, n_kv_heads=2, head_dim=64, r=128)
+    g = np.random.default_rng(77)
+    W = (g.standard_normal((L.d, L.N)) * 0.02).astype(np.float32).astype(np.float64)
+    ol, dl = _layers_from_weight(W, L)
+    return L, ol, dl
+
+
+@pytest.fixture(scope="module")
+def llava():
+    wl = configs.get(3)
+    L = wl.layer
+    U, s, V = gen.weight_factors(wl)
+    A, Bm = O.split_beta(U, s, V.T, wl.beta)
+    ol = O.make_layer(A, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, 8, 0)
+    dl = B.DeviceLayer(prep.prepare_from_svd(U, s, V, L.n_q_heads, L.n_kv_heads, L.head_dim, wl.beta))
+    return wl, ol, dl
+
+
+# ------------------------------------------------------------------ a1: quantizer
+
+def _quant_cases():
+    wl1, wl2 = configs.get(1), configs.get(2)
+    ties = np.array([[127, 2.5, 3.5, -2.5, -0.5, 0.5, 1.5, -126.5]], np.float16)
+    zero_and_ties = np.concatenate([np.zeros((1, 8), np.float16), ties, -ties])
+    return [
+        ("tiny-8bit", gen.prefill_activations(wl1), 8, 1.0, None),
+        ("tiny-4bit", gen.prefill_activations(wl1), 4, 1.0, None),
+        ("tiny-clip0.9", gen.prefill_activations(wl1), 8, 0.9, None),
+        ("llava7b-prefill-2560x4096", gen.prefill_activations(wl2), 8, 1.0, None),
+        ("K8", gen.random_rows(1, (5, 8), 3.0), 8, 1.0, None),
+        ("K520-ragged", gen.random_rows(2, (7, 520), 1.0), 8, 1.0, None),
+        ("M1", gen.random_rows(3, (1, 4096), 1.0), 8, 1.0, None),
+        ("zero-and-ties", zero_and_ties, 8, 1.0, None),
+        ("strided-ldx", gen.random_rows(4, (9, 264), 1.0), 8, 1.0, 256),
+        ("4bit-strided", gen.random_rows(5, (9, 264), 1.0), 4, 1.0, 256),
+    ]
+
+
+@pytest.mark.parametrize("case", _quant_cases(), ids=lambda c: c[0])
+def test_quantize_act_bitexact(case):
+    name, x, bits, clip, K = case
+    H.say(f"quantize_act {name} shape={x.shape} bits={bits}")
+    xq, sx = H.quantize_act(x, bits, clip, K)
+    xs = x if K is None else x[:, :K]
+    q_ref, s_ref = O.quantize_act(xs, bits, clip)
+    if bits == 4:
+        q_ref = O.pack_int4(q_ref)
+    assert np.array_equal(xq.view(np.uint8), q_ref.view(np.uint8))
+    assert np.array_equal(sx.view(np.uint32), s_ref.view(np.uint32))
+
+
+# ------------------------------------------------------------------ a2-a4: projection
+
+def _check_prefill(ol, got, X):
+    ref = O.prefill(ol, X, 8)
+    assert np.array_equal(got["xq"], ref["xq"])
+    assert np.array_equal(got["sx"].view(np.uint32), ref["sx"].view(np.uint32))
+    assert np.array_equal(got["acc_xa"], ref["acc_xa"])
+    assert np.array_equal(got["C_h"].view(np.uint16), ref["C_h"].view(np.uint16))
+    assert np.array_equal(got["cq"], ref["cq"])
+    assert np.array_equal(got["sc"].view(np.uint32), ref["sc"].view(np.uint32))
+    assert np.array_equal(got["acc_cb"], ref["acc_cb"])
+    for key in ("Q", "K", "V"):
+        if key in got:
+            assert np.array_equal(got[key].view(np.uint16), ref[key].view(np.uint16)), key
+
+
+@pytest.mark.parametrize("M", [1, 16, 31, 32, 33, 64, 200])
+def test_prefill_bitexact_tiny(tiny, M):
+    wl, ol, dl = tiny
+    X = gen.fill_activations(wl, M)
+    H.say(f"prefill tiny M={M}")
+    got = H.Prefill(dl, M).run(H.dev(X)).result()
+    _check_prefill(ol, got, X)
+
+
+def test_prefill_masks_leave_other_outputs(tiny):
+    wl, ol, dl = tiny
+    X = gen.fill_activations(wl, 40)
+    for mask in (B.QSVD_OUT_Q, B.QSVD_OUT_K | B.QSVD_OUT_V):
+        H.say(f"prefill mask={mask}")
+        p = H.Prefill(dl, 40, mask=mask, debug=False)
+        for t in (p.q, p.k, p.v):
+            t.fill_(7.0)
+        got = p.run(H.dev(X)).result()
+        ref = O.prefill(ol, X, 8)
+        for key, bit, t in (("Q", 1, p.q), ("K", 2, p.k), ("V", 4, p.v)):
+            if mask & bit:
+                assert np.array_equal(got[key].view(np.uint16), ref[key].view(np.uint16))
+            else:
+                assert bool((t == 7.0).all())
+
+
+def test_prefill_bitexact_llava7b_full(llava):
+    """The LLaVA-1.5-7B-shaped prefill at its full size: 4 x 640 tokens, d=4096, r=1536, N=12288."""
+    wl, ol, dl = llava
+    wl2 = configs.get(2)
+    X = gen.prefill_activations(wl2)
+    H.say(f"prefill llava7b M={X.shape[0]}")
+    got = H.Prefill(dl, X.shape[0]).run(H.dev(X)).result()
+    _check_prefill(ol, got, X)
+
+
+# ------------------------------------------------------------------ a3: cache append
+
+@pytest.mark.parametrize("fmt", [B.QSVD_CACHE_F16, B.QSVD_CACHE_I8, B.QSVD_CACHE_I4], ids=["f16", "i8", "i4"])
+def test_cache_append_bytes(tiny, fmt):
+    wl, ol, dl = tiny
+    bits = 4 if fmt == B.QSVD_CACHE_I4 else 8
+    lengths = [0, 5, 17]
+    batch, cap, r = 3, 32, wl.layer.r
+    dc = B.DeviceCache(fmt, batch, cap, r, lengths)
+    oc = O.LatentCache(fmt, batch, cap, r)
+    oc.seq_len[:] = lengths
+    for step, n_new in enumerate((3, 1, 6)):
+        X = gen.fill_activations(wl, batch * n_new, layer=step)
+        ref = O.prefill(ol, X, bits)
+        H.say(f"cache append fmt={fmt} n_new={n_new}")
+        c_h = H.dev(ref["C_h"])
+        cq = H.dev(ref["cq"] if bits == 8 else O.pack_int4(ref["cq"]))
+        sc = H.dev(ref["sc"])
+        H.append(dc, c_h, cq, sc, n_new)
+        for b in range(batch):
+            oc.append(b, ref["C_h"][b * n_new:(b + 1) * n_new], ref["cq"][b * n_new:(b + 1) * n_new],
+                      ref["sc"][b * n_new:(b + 1) * n_new])
+    assert np.array_equal(H.host(dc.data).view(np.uint8), oc.data.view(np.uint8))
+    if fmt != B.QSVD_CACHE_F16:
+        assert np.array_equal(H.host(dc.scale).view(np.uint32), oc.scale.view(np.uint32))
+    assert list(H.host(dc.seq_len)) == list(oc.seq_len)
+    assert dc.max_len == 17 + 10
+    with pytest.raises(B.QsvdError):
+        H.append(dc, c_h, cq, sc, cap)
+
+
+# ------------------------------------------------------------------ a5-a7: decode attention
+
+@pytest.mark.parametrize("mode", MODES, ids=MODE_IDS)
+def test_decode_tiny_end_to_end(tiny, mode):
+    """Tiny layer: 64 prefill tokens into an fp16 latent cache, then 16 decode
+    steps of projection, append and attention, each against the oracle."""
+    wl, ol, dl = tiny
+    X = gen.prefill_activations(wl)
+    oc = O.LatentCache(O.CACHE_F16, 1, 64 + wl.decode_steps, wl.layer.r)
+    O.cache_append_prefill(oc, O.prefill(ol, X, 8), [64])
+    dc = B.DeviceCache(B.QSVD_CACHE_F16, 1, 64 + wl.decode_steps, wl.layer.r, [0])
+    pre = H.Prefill(dl, 64, mask=0, debug=False).run(H.dev(X))
+    H.append(dc, pre.c_h, n_new=64)
+    for t in range(wl.decode_steps):
+        xt = gen.decode_activations(wl, t)
+        ref = O.decode_step(ol, oc, xt, 8)
+        H.say(f"decode tiny step={t} mode={mode}")
+        p = H.Prefill(dl, 1, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
+        H.append(dc, p.c_h, n_new=1)
+        out = H.host(H.decode_attention(dl, dc, p.q, mode))
+        assert np.array_equal(H.host(p.c_h).view(np.uint16), ref["C_h"].view(np.uint16))
+        assert np.array_equal(H.host(p.q).view(np.uint16), ref["Q"].view(np.uint16))
+        ok, info = H.close_enough(out, ref["out"])
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (t, info)
+
+
+@pytest.mark.parametrize("mode", MODES, ids=MODE_IDS)
+def test_decode_gqa_int8_ragged(gqa, mode):
+    """Grouped queries (8 over 2), int8 latent cache with per-token scales,
+    ragged lengths 1 / 45 / 130 across the batch, 3 decode steps."""
+    L, ol, dl = gqa
+    lengths = [1, 45, 130]
+    batch, cap = 3, 140
+    wl = configs.Workload(95, "gqa-test", L, "gaussian", 8, 0, 8, configs.CACHE_I8)
+    codes, scales = gen.latent_codes(wl, batch, cap)
+    oc = O.LatentCache(O.CACHE_I8, batch, cap, L.r)
+    dc = B.DeviceCache(B.QSVD_CACHE_I8, batch, cap, L.r, lengths)
+    for b, n in enumerate(lengths):
+        oc.append(b, None, codes[b, :n], scales[b, :n])
+    dc.data.copy_(H.dev(np.where(np.arange(cap)[None, :, None] < np.array(lengths)[:, None, None], codes, 0)))
+    dc.scale.copy_(H.dev(np.where(np.arange(cap)[None, :] < np.array(lengths)[:, None], scales, 0)))
+    for t in range(3):
+        xt = gen.decode_activations(wl, t, batch=batch)
+        ref = O.decode_step(ol, oc, xt, 8)
+        H.say(f"decode gqa int8 step={t} mode={mode}")
+        p = H.Prefill(dl, batch, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
+        H.append(dc, cq=p.cq, sc=p.sc, n_new=1)
+        out = H.host(H.decode_attention(dl, dc, p.q, mode))
+        assert np.array_equal(H.host(p.cq), ref["cq"])
+        ok, info = H.close_enough(out, ref["out"])
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (t, info)
+    assert np.array_equal(H.host(dc.data), oc.data)
+
+
+@pytest.mark.parametrize("mode", MODES, ids=MODE_IDS)
+def test_decode_llava7b_width_ragged(llava, mode):
+    """LLaVA-1.5-7B-shaped layer (r=1536, 32 heads) over an fp16 latent cache
+    with ragged lengths 1 / 33 / 290 / 1000 (one to many tiles and chunks)."""
+    wl, ol, dl = llava
+    lengths = [1, 33, 290, 1000]
+    batch, cap = 4, 1008
+    rows = gen.latent_rows(wl, batch, cap)
+    oc = O.LatentCache(O.CACHE_F16, batch, cap, wl.layer.r)
+    for b, n in enumerate(lengths):
+        oc.append(b, rows[b, :n])
+    dc = B.DeviceCache(B.QSVD_CACHE_F16, batch, cap, wl.layer.r, lengths)
+    dc.data.copy_(H.dev(oc.data))
+    xt = gen.decode_activations(wl, 0, batch=batch)
+    ref = O.decode_step(ol, oc, xt, 8)
+    H.say(f"decode llava7b ragged mode={mode}")
+    p = H.Prefill(dl, batch, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
+    H.append(dc, p.c_h, n_new=1)
+    out = H.host(H.decode_attention(dl, dc, p.q, mode))
+    assert np.array_equal(H.host(p.q).view(np.uint16), ref["Q"].view(np.uint16))
+    ok, info = H.close_enough(out, ref["out"])
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+
+
+def test_decode_llava7b_full_size_sampled(llava):
+    """The decode workload at its full size (16 sequences x 4096 cached tokens,
+    fp16 latent cache of width 1536) in the launch configuration the bench
+    times; two sequences are checked against the oracle in full."""
+    wl, ol, dl = llava
+    batch, L0, cap = 16, 4096, 4096 + 8
+    rows = gen.latent_rows(wl, batch, cap)
+    dc = B.DeviceCache(B.QSVD_CACHE_F16, batch, cap, wl.layer.r, [L0] * batch)
+    dc.data.copy_(H.dev(rows))
+    xt = gen.decode_activations(wl, 0, batch=batch)
+    H.say("decode llava7b full size")
+    p = H.Prefill(dl, batch, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
+    H.append(dc, p.c_h, n_new=1)
+    out = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
+    out2 = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
+    assert np.array_equal(out.view(np.uint16), out2.view(np.uint16)), "decode attention is not deterministic"
+    assert np.all(np.isfinite(out.astype(np.float32)))
+    for b in (0, 11):
+        oc = O.LatentCache(O.CACHE_F16, 1, cap, wl.layer.r)
+        oc.append(0, rows[b, :L0])
+        ref = O.decode_step(ol, oc, xt[b:b + 1], 8)
+        ok, info = H.close_enough(out[b:b + 1], ref["out"])
+        H.say(f"  b={b} max-abs, rel-L2, rms = {info}")
+        assert ok, (b, info)

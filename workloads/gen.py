@@ -97,3 +97,27 @@ def random_rows(seed: int, shape, scale: float = 1.0, dtype=np.float16) -> np.nd
     """Plain N(0, scale^2) array for small edge-case tests."""
     g = np.random.default_rng(seed)
     return (g.standard_normal(shape) * scale).astype(dtype)
+
+
+def latent_rows(wl: Workload, batch: int, length: int, layer: int = 0, seed_offset: int = 0) -> np.ndarray:
+    """fp16 [batch, length, r] synthetic rows for a pre-filled fp16 latent
+    cache: column j ~ N(0, sigma_j) for the decaying spectrum (unit variance
+    for the Gaussian one), the magnitude of X W^d with beta = 1/2 and unit X."""
+    g = rng_for(wl, ROLE_FILL + seed_offset, layer)
+    r = wl.layer.r
+    std = np.sqrt(spectrum(wl)[:r]) if wl.spectrum == "decay" else np.ones(r)
+    rows = np.empty((batch, length, r), dtype=np.float16)
+    for b in range(batch):
+        rows[b] = (g.standard_normal((length, r)) * std[None, :]).astype(np.float16)
+    return rows
+
+
+def latent_codes(wl: Workload, batch: int, length: int, layer: int = 0, seed_offset: int = 0):
+    """Synthetic int8 latent cache contents: codes in [-127, 127] (each row
+    reaching +-127) and positive per-token fp32 scales."""
+    g = rng_for(wl, ROLE_FILL + seed_offset, layer)
+    r = wl.layer.r
+    codes = np.clip(np.rint(g.standard_normal((batch, length, r)) * 40.0), -127, 127).astype(np.int8)
+    codes[:, :, 0] = 127
+    scales = (g.uniform(0.02, 0.2, (batch, length))).astype(np.float32)
+    return codes, scales
