@@ -1,0 +1,322 @@
+"""Benchmark of the QSVD latent-QKV hot path on one MI355X.
+
+Headline (``value``): decode tokens/s of one LLaVA-1.5-7B-shaped attention
+layer (d=4096, 32 heads x 128, joint rank r=1536, W8A8, fp16 latent cache) at
+batch 16 over a 4096-token context.  One step is the whole decode hot path
+for one layer: per-token quantization of the new activations, the quantized
+down-projection to the latent C, the latent cache append, the Q
+up-projection, and attention over the cached latent (absorbed form).  Steps
+cycle through 32 distinct layers (weights and caches, 6.9 GB of cache) so the
+cache is read from HBM and not from the 256 MB last-level cache; each layer's
+context grows by one token per visit, 4096 -> 4352 over 256 visits.
+
+Also reported: the quantized low-rank QKV prefill of the same layer (batch
+4 x 640 tokens) in TOPS against the int8 matrix-core peak, the kernel-level
+roofline of the latent attention kernel, timed with HIP events on its launch
+stream during the timed region, and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "latent-decode tokens/s + HBM GB/s frac; low-rank QKV prefill TOPS (MFMA frac)"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+INT8_PEAK_TOPS = 5033.0        # MI355X dense int8 matrix peak, TOP/s
+N_LAYERS = 32                  # LLaVA-1.5-7B language-model layers
+DECODE_BATCH, CTX0, DECODE_VISITS = 16, 4096, 256
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=N_LAYERS * DECODE_VISITS)
+    ap.add_argument("--warmup", type=int, default=64)
+    ap.add_argument("--prefill-steps", type=int, default=20)
+    ap.add_argument("--mode", choices=["auto", "absorbed", "reconstruct"], default="auto")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="time without the kernel events")
+    return ap.parse_args()
+
+
+def cpu_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        n = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"), default=1)
+    except Exception:
+        n = 1
+    return int(n)
+
+
+def layer_weights(wl):
+    from paper_2510_16292_amd import prep
+    from workloads import gen
+    U, s, V = gen.weight_factors(wl)
+    L = wl.layer
+    return (U, s, V), prep.prepare_from_svd(U, s, V, L.n_q_heads, L.n_kv_heads, L.head_dim, wl.beta)
+
+
+def bench_decode(args, wl, host_layer):
+    import torch
+
+    from paper_2510_16292_amd import binding as B
+    from workloads import gen
+
+    L = wl.layer
+    r, d, nq = L.r, L.d, L.n_q
+    visits = max(-(-args.steps // N_LAYERS), -(-args.warmup // N_LAYERS), 1)
+    cap = CTX0 + visits + 1
+    mode = {"auto": B.QSVD_ATTN_AUTO, "absorbed": B.QSVD_ATTN_ABSORBED,
+            "reconstruct": B.QSVD_ATTN_RECONSTRUCT}[args.mode]
+    layers = [B.DeviceLayer(host_layer) for _ in range(N_LAYERS)]
+    caches = []
+    for li in range(N_LAYERS):
+        c = B.DeviceCache(B.QSVD_CACHE_F16, DECODE_BATCH, cap, r, [CTX0] * DECODE_BATCH)
+        gen.latent_rows_device(wl, DECODE_BATCH, CTX0, seed=1000 + li, out=c.data)
+        caches.append(c)
+    xs = [torch.from_numpy(gen.decode_activations(wl, t, batch=DECODE_BATCH)).cuda() for t in range(8)]
+    xq = torch.empty((DECODE_BATCH, d), dtype=torch.int8, device="cuda")
+    sx = torch.empty((DECODE_BATCH,), dtype=torch.float32, device="cuda")
+    c_h = torch.empty((DECODE_BATCH, r), dtype=torch.float16, device="cuda")
+    cq = torch.empty((DECODE_BATCH, r), dtype=torch.int8, device="cuda")
+    sc = torch.empty((DECODE_BATCH,), dtype=torch.float32, device="cuda")
+    q = torch.empty((DECODE_BATCH, nq), dtype=torch.float16, device="cuda")
+    out = torch.empty_like(q)
+    pws_b = B.qsvd_prefill_workspace_size(layers[0].c, DECODE_BATCH, B.QSVD_OUT_Q)
+    pws = torch.empty((max(pws_b, 1),), dtype=torch.uint8, device="cuda")
+    dws_b = max(B.qsvd_decode_workspace_size(layers[0].c, c.c, 1, mode) for c in caches)
+    dws = torch.empty((dws_b,), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+
+    lib = B.lib()
+    s = B.stream_handle()
+    P = B.ptr
+    xq_p, sx_p, ch_p, cq_p, sc_p, q_p, out_p = P(xq), P(sx), P(c_h), P(cq), P(sc), P(q), P(out)
+    pws_p, dws_p = P(pws), P(dws)
+    xs_p = [P(x) for x in xs]
+    import ctypes
+    lrefs = [ctypes.byref(l.c) for l in layers]
+    crefs = [ctypes.byref(c.c) for c in caches]
+
+    def step(i):
+        li = i % N_LAYERS
+        st = lib.qsvd_quantize_act(xs_p[i % 8], DECODE_BATCH, d, d, 8, 1.0, xq_p, sx_p, s)
+        st |= lib.qsvd_lowrank_qkv_prefill(lrefs[li], xq_p, sx_p, DECODE_BATCH, 8, B.QSVD_OUT_Q, ch_p, cq_p, sc_p,
+                                           q_p, 0, 0, 0, 0, pws_p, pws_b, s)
+        st |= lib.qsvd_latent_cache_append(crefs[li], ch_p, 0, 0, 1, s)
+        st |= lib.qsvd_latent_decode_attention(lrefs[li], crefs[li], q_p, 1, mode, 0.0, out_p, dws_p, dws_b, s)
+        if st:
+            raise B.QsvdError(st, B.last_error())
+
+    def reset():
+        torch.cuda.synchronize()
+        for c in caches:
+            c.seq_len.fill_(CTX0)
+            c.c.max_len = CTX0
+        torch.cuda.synchronize()
+
+    for i in range(args.warmup):
+        step(i)
+    reset()
+    # cached tokens each attention launch reads (context after the append)
+    ctx_read = sum(DECODE_BATCH * (CTX0 + 1 + i // N_LAYERS) for i in range(args.steps))
+    attn_name = "latent_attn" if mode != B.QSVD_ATTN_RECONSTRUCT else "recon"
+    if not args.no_profile:
+        B.profile_reset()
+        B.profile_enable(True, attn_name)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    B.profile_enable(False)
+    ms_step = (t1 - t0) * 1e3 / max(args.steps, 1)
+    res = dict(ms_per_step=ms_step, tokens_per_s=DECODE_BATCH * args.steps / (t1 - t0),
+               mean_context=ctx_read / max(args.steps, 1) / DECODE_BATCH)
+    if not args.no_profile:
+        kms, n = B.profile_read(attn_name)
+        B.profile_reset()
+        if n:
+            avg_s = kms / n * 1e-3
+            bytes_per_launch = ctx_read / args.steps * r * 2
+            achieved = bytes_per_launch / avg_s / 1e9
+            res["attn_kernel_us"] = avg_s * 1e6
+            res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                               "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                               "kernel": "latent_attn_kernel", "launches": n,
+                               "bytes_per_launch": int(bytes_per_launch)}
+    # absorbed vs reconstruct on this layer, attention call alone (a few calls each)
+    forms = {}
+    for name, m in (("absorbed", B.QSVD_ATTN_ABSORBED), ("reconstruct", B.QSVD_ATTN_RECONSTRUCT)):
+        wsb = B.qsvd_decode_workspace_size(layers[0].c, caches[0].c, 1, m)
+        ws = torch.empty((wsb,), dtype=torch.uint8, device="cuda")
+        reps = 3 if m == B.QSVD_ATTN_RECONSTRUCT else 20
+        for _ in range(2):
+            B.check(lib.qsvd_latent_decode_attention(lrefs[0], crefs[0], q_p, 1, m, 0.0, out_p, P(ws), wsb, s))
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        for _ in range(reps):
+            B.check(lib.qsvd_latent_decode_attention(lrefs[0], crefs[0], q_p, 1, m, 0.0, out_p, P(ws), wsb, s))
+        torch.cuda.synchronize()
+        forms[name] = round((time.perf_counter() - a) * 1e6 / reps, 1)
+        del ws
+    res["attention_form_us"] = forms
+    del caches, layers
+    torch.cuda.empty_cache()
+    return res
+
+
+def bench_prefill(args, wl2, host_layer):
+    import torch
+
+    from paper_2510_16292_amd import binding as B
+    from workloads import gen
+
+    L = wl2.layer
+    M, d, r, nq, nkv = wl2.prefill_M, L.d, L.r, L.n_q, L.n_kv
+    dl = B.DeviceLayer(host_layer)
+    X = torch.from_numpy(gen.prefill_activations(wl2)).cuda()
+    xq = torch.empty((M, d), dtype=torch.int8, device="cuda")
+    sx = torch.empty((M,), dtype=torch.float32, device="cuda")
+    c_h = torch.empty((M, r), dtype=torch.float16, device="cuda")
+    cq = torch.empty((M, r), dtype=torch.int8, device="cuda")
+    sc = torch.empty((M,), dtype=torch.float32, device="cuda")
+    q = torch.empty((M, nq), dtype=torch.float16, device="cuda")
+    k = torch.empty((M, nkv), dtype=torch.float16, device="cuda")
+    v = torch.empty((M, nkv), dtype=torch.float16, device="cuda")
+    wsb = B.qsvd_prefill_workspace_size(dl.c, M, 7)
+    ws = torch.empty((max(wsb, 1),), dtype=torch.uint8, device="cuda")
+    s = B.stream_handle()
+    P = B.ptr
+
+    def call():
+        B.check(B.qsvd_quantize_act(P(X), M, d, d, 8, 1.0, P(xq), P(sx), s))
+        B.check(B.qsvd_lowrank_qkv_prefill(dl.c, P(xq), P(sx), M, 8, 7, P(c_h), P(cq), P(sc), P(q), P(k), P(v),
+                                           0, 0, P(ws), wsb, s))
+
+    for _ in range(3):
+        call()
+    B.profile_reset()
+    B.profile_enable(True, "gemm_i8")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.prefill_steps):
+        call()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    B.profile_enable(False)
+    gms, n = B.profile_read("gemm_i8")
+    B.profile_reset()
+    ops = 2.0 * M * (d * r + r * L.N)            # X W^d then Q(C) W^u, multiply-adds counted twice
+    gemm_s = gms * 1e-3 / args.prefill_steps
+    call_s = (t1 - t0) / args.prefill_steps
+    tops = ops / gemm_s / 1e12
+    return {"value": round(tops, 1), "unit": "TOPS", "ms_per_call": round(call_s * 1e3, 4),
+            "gemm_ms_per_call": round(gemm_s * 1e3, 4), "call_tops": round(ops / call_s / 1e12, 1),
+            "tokens": M, "gop_per_call": round(ops / 1e9, 2),
+            "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
+                         "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None,
+                         "kernel": "gemm_i8 (X W^d and Q(C) W^u)", "launches": n}}
+
+
+def cpu_baseline_decode(wl, factors):
+    """The oracle, as it stands, on one full decode step of the 16-sequence
+    batch at context 4096 (projection, append, attention in the plain
+    reconstruct form); tokens/s of that step."""
+    from oracle import qsvd_oracle as O
+    from workloads import gen
+    L = wl.layer
+    U, s, V = factors
+    A, Bm = O.split_beta(U, s, V.T, wl.beta)
+    ol = O.make_layer(A, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, 8, 0)
+    n_seq = DECODE_BATCH
+    oc = O.LatentCache(O.CACHE_F16, n_seq, CTX0 + 1, L.r)
+    rows = gen.latent_rows(wl, n_seq, CTX0)
+    for b in range(n_seq):
+        oc.append(b, rows[b])
+    xt = gen.decode_activations(wl, 0, batch=n_seq)
+    t0 = time.perf_counter()
+    O.decode_step(ol, oc, xt, 8)
+    dt = time.perf_counter() - t0
+    return {"value": round(n_seq / dt, 2), "unit": "tokens/s", "cores": cpu_threads(), "kind": "oracle",
+            "sample": f"one decode step of all {n_seq} sequences at context {CTX0} (fp64 plain form), {dt:.1f} s"}
+
+
+def cpu_baseline_prefill(wl2, factors):
+    from oracle import qsvd_oracle as O
+    from workloads import gen
+    L = wl2.layer
+    U, s, V = factors
+    A, Bm = O.split_beta(U, s, V.T, wl2.beta)
+    ol = O.make_layer(A, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, 8, 0)
+    X = gen.prefill_activations(wl2)[:640]
+    t0 = time.perf_counter()
+    O.prefill(ol, X, 8)
+    dt = time.perf_counter() - t0
+    ops = 2.0 * X.shape[0] * (L.d * L.r + L.r * L.N)
+    return {"value": round(ops / dt / 1e12, 4), "unit": "TOPS", "cores": cpu_threads(), "kind": "oracle",
+            "sample": f"prefill of one 640-token sequence of the 4 x 640 batch, {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs the QSVD hot path on one GPU only; multi-GPU runs are not part of it "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2510_16292_amd import binding as B
+    from workloads import configs
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    B.lib()
+    wl2, wl3 = configs.get(2), configs.get(3)
+    factors, host_layer = layer_weights(wl2)        # one 7B-shaped layer serves both legs
+    print(f"[bench] decode: {args.steps} steps, warmup {args.warmup}", file=sys.stderr, flush=True)
+    dec = bench_decode(args, wl3, host_layer)
+    print(f"[bench] decode done: {dec['ms_per_step']:.4f} ms/step", file=sys.stderr, flush=True)
+    pre = bench_prefill(args, wl2, host_layer)
+    print(f"[bench] prefill done: {pre['value']} TOPS", file=sys.stderr, flush=True)
+    line = {
+        "metric": METRIC,
+        "value": round(dec["tokens_per_s"], 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dec["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i8+f16",
+        "data": "synthetic",
+        "config": {"workload": "llava-1.5-7b-shaped attention layer decode: batch 16, fp16 latent cache r=1536, "
+                               f"context {CTX0}->{CTX0 + DECODE_VISITS}, W8A8 projections, 32 rotated layers; "
+                               "value is tokens/s per layer step",
+                   "d": 4096, "heads": 32, "head_dim": 128, "rank": 1536, "batch": DECODE_BATCH,
+                   "mean_context": round(dec["mean_context"], 1), "attention": args.mode},
+        "roofline": dec.get("roofline"),
+        "attn_kernel_us": round(dec.get("attn_kernel_us", 0.0), 2),
+        "attention_form_us": dec["attention_form_us"],
+        "prefill": pre,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline_decode(wl3, factors)
+        line["prefill"]["cpu_baseline"] = cpu_baseline_prefill(wl2, factors)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -161,11 +161,13 @@ size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int3
 const char* qsvd_status_string(qsvd_status s);
 const char* qsvd_last_error(void);
 
-/* Optional kernel timing.  While enabled, every kernel the library launches is
- * bracketed by HIP events recorded on its launch stream; qsvd_profile_read()
- * synchronizes those events and returns the summed milliseconds and launch
- * count of the kernels whose name contains `name`.  Not for graph capture. */
-qsvd_status qsvd_profile_enable(int32_t on);
+/* Optional kernel timing.  While enabled, every kernel the library launches
+ * whose name contains `filter` (all kernels if filter is NULL; the string is
+ * copied) is bracketed by HIP events recorded on its launch stream;
+ * qsvd_profile_read() synchronizes those events and returns the summed
+ * milliseconds and launch count of the recorded kernels whose name contains
+ * `name`.  Not for graph capture. */
+qsvd_status qsvd_profile_enable(int32_t on, const char* filter);
 qsvd_status qsvd_profile_reset(void);
 qsvd_status qsvd_profile_read(const char* name, double* total_ms, int64_t* launches);
 

@@ -70,7 +70,7 @@ def lib():
             "qsvd_decode_workspace_size": (SZ, [LP, CP, I32, I32]),
             "qsvd_status_string": (ctypes.c_char_p, [I32]),
             "qsvd_last_error": (ctypes.c_char_p, []),
-            "qsvd_profile_enable": (I32, [I32]),
+            "qsvd_profile_enable": (I32, [I32, ctypes.c_char_p]),
             "qsvd_profile_reset": (I32, []),
             "qsvd_profile_read": (I32, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]),
         }
@@ -118,8 +118,8 @@ def last_error():
     return lib().qsvd_last_error().decode()
 
 
-def profile_enable(on):
-    return lib().qsvd_profile_enable(1 if on else 0)
+def profile_enable(on, filter=None):
+    return lib().qsvd_profile_enable(1 if on else 0, None if filter is None else filter.encode())
 
 
 def profile_reset():

@@ -81,6 +81,7 @@ struct ProfRec {
 };
 std::mutex g_prof_mu;
 bool g_prof_on = false;
+std::string g_prof_filter;
 std::vector<ProfRec> g_prof;
 
 }  // namespace
@@ -90,6 +91,7 @@ namespace qsvd {
 KernelScope::KernelScope(const char* name, hipStream_t s) : name_(name), s_(s), slot_(-1) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   if (!g_prof_on) return;
+  if (!g_prof_filter.empty() && std::string(name).find(g_prof_filter) == std::string::npos) return;
   ProfRec r{name, nullptr, nullptr};
   if (hipEventCreate(&r.start) != hipSuccess || hipEventCreate(&r.stop) != hipSuccess) return;
   hipEventRecord(r.start, s);
@@ -270,9 +272,10 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
   return hip_status(absorbed ? launch_attn_absorbed(a, ws, s) : launch_attn_reconstruct(a, ws, s), "decode attention");
 }
 
-qsvd_status qsvd_profile_enable(int32_t on) {
+qsvd_status qsvd_profile_enable(int32_t on, const char* filter) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   g_prof_on = on != 0;
+  g_prof_filter = filter ? filter : "";
   return QSVD_OK;
 }
 

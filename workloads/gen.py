@@ -121,3 +121,20 @@ def latent_codes(wl: Workload, batch: int, length: int, layer: int = 0, seed_off
     codes[:, :, 0] = 127
     scales = (g.uniform(0.02, 0.2, (batch, length))).astype(np.float32)
     return codes, scales
+
+
+def latent_rows_device(wl: Workload, batch: int, length: int, seed: int, out=None, device="cuda"):
+    """Device-side variant of :func:`latent_rows` for large pre-filled caches
+    (torch's seeded generator on the GPU): fp16 [batch, length, r] with
+    column j ~ N(0, sigma_j).  Writes into ``out[:, :length]`` if given."""
+    import torch
+    r = wl.layer.r
+    std = np.sqrt(spectrum(wl)[:r]) if wl.spectrum == "decay" else np.ones(r)
+    std_t = torch.tensor(std, dtype=torch.float32, device=device)
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    if out is None:
+        out = torch.empty((batch, length, r), dtype=torch.float16, device=device)
+    for b in range(batch):
+        out[b, :length] = (torch.randn((length, r), generator=g, device=device) * std_t).to(torch.float16)
+    return out
