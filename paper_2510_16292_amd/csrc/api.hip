@@ -58,6 +58,7 @@ qsvd_status check_layer(const qsvd_layer* w) {
   if (w->w_bits == 4 && w->w_group == 0)
     return fail(QSVD_ERR_UNSUPPORTED, "int4 weights need a group size");
   if (w->d % 64 || w->r % 64) return fail(QSVD_ERR_UNSUPPORTED, "d and r must be multiples of 64");
+  if (w->r > 4096) return fail(QSVD_ERR_UNSUPPORTED, "r must be at most 4096");
   return QSVD_OK;
 }
 
@@ -151,12 +152,29 @@ static void prefill_ranges(const qsvd_layer& w, uint32_t mask, bool full, int32_
   if (*lo > *hi) *lo = *hi = 0;
 }
 
-size_t qsvd_prefill_workspace_size(const qsvd_layer* w, int64_t M, uint32_t out_mask) {
-  if (!w || M < 0) return 0;
-  (void)out_mask;
-  const size_t a = gemm_i8_workspace(M, w->r, w->d);
-  const size_t b = gemm_i8_workspace(M, (int32_t)n_total(*w), w->r);
+// Workspace of one projection call: the down-projection over r columns and the
+// up-projection over the column range [lo, hi) that the call computes.
+static size_t prefill_need(const qsvd_layer& w, int64_t M, int32_t lo, int32_t hi) {
+  const size_t a = gemm_i8_workspace(M, w.r, w.d);
+  const size_t b = hi > lo ? gemm_i8_workspace(M, hi - lo, w.r) : 0;
   return a > b ? a : b;
+}
+
+size_t qsvd_prefill_workspace_size(const qsvd_layer* w, int64_t M, uint32_t out_mask) {
+  if (!w || M < 0 || w->r <= 0 || w->d <= 0) return 0;
+  (void)out_mask;
+  // The split of the contraction depends on the width computed, so take the
+  // largest need over every output selection (and the full width used when the
+  // integer accumulators are dumped): one size serves every call.
+  size_t need = 0;
+  for (uint32_t mask = 0; mask <= 7; ++mask)
+    for (int full = 0; full < 2; ++full) {
+      int32_t lo, hi;
+      prefill_ranges(*w, mask, full != 0, &lo, &hi);
+      const size_t n = prefill_need(*w, M, lo, hi);
+      if (n > need) need = n;
+    }
+  return need;
 }
 
 qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const float* sx, int64_t M,
@@ -176,7 +194,9 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
     return fail(QSVD_ERR_UNSUPPORTED, "prefill implements W8A8 per-channel weights");
   if (!aligned(xq, 16) || !aligned(cq, 16) || !aligned(c_h, 16) || !aligned(w->a_t, 16) || !aligned(w->b_t, 16))
     return fail(QSVD_ERR_UNSUPPORTED, "operands must be 16-byte aligned");
-  const size_t need = qsvd_prefill_workspace_size(w, M, out_mask);
+  int32_t lo, hi;
+  prefill_ranges(*w, out_mask, dbg_acc_cb != nullptr, &lo, &hi);
+  const size_t need = prefill_need(*w, M, lo, hi);
   if (need > 0 && (!ws || ws_bytes < need))
     return fail(QSVD_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
 
@@ -193,15 +213,13 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
   g1.seg[0] = OutSeg{(_Float16*)c_h, w->r, 0, w->r};
   g1.n_seg = 1;
   g1.dbg = dbg_acc_xa;
-  st = hip_status(launch_gemm_i8(g1, ws, s), "down-projection");
-  if (st != QSVD_OK) return st;
-  // Q(C)
-  st = hip_status(launch_quantize_rows(c_h, M, w->r, w->r, act_bits, 1.f, cq, sc, s), "latent quantization");
+  g1.cq = cq;           // Q(C) is produced with C
+  g1.sc = sc;
+  g1.abits = act_bits;
+  st = hip_status(launch_gemm_i8(g1, ws, ws_bytes, s), "down-projection");
   if (st != QSVD_OK) return st;
   if (!out_mask && !dbg_acc_cb) return QSVD_OK;
   // Q(C) W^u -> Q | K | V (fp16)
-  int32_t lo, hi;
-  prefill_ranges(*w, out_mask, dbg_acc_cb != nullptr, &lo, &hi);
   const int32_t nq = w->n_q_heads * w->head_dim, nkv = w->n_kv_heads * w->head_dim;
   GemmArgs g2{};
   g2.a = (const int8_t*)cq;
@@ -216,7 +234,7 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
   g2.seg[2] = OutSeg{(out_mask & QSVD_OUT_V) ? (_Float16*)v : nullptr, nkv, nq + nkv - lo, nkv};
   g2.n_seg = 3;
   g2.dbg = dbg_acc_cb;
-  return hip_status(launch_gemm_i8(g2, ws, s), "up-projection");
+  return hip_status(launch_gemm_i8(g2, ws, ws_bytes, s), "up-projection");
 }
 
 qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void* cq, const float* sc,
@@ -265,6 +283,8 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
   const bool abs_ok = absorbed_supported(*w, *c);
   if (mode == QSVD_ATTN_ABSORBED && !abs_ok) return fail(QSVD_ERR_UNSUPPORTED, "absorbed form needs r in {128, 512, 1024, 1536}");
   const bool absorbed = mode == QSVD_ATTN_ABSORBED || (mode == QSVD_ATTN_AUTO && abs_ok);
+  if (!absorbed && c->capacity > 16384)
+    return fail(QSVD_ERR_UNSUPPORTED, "reconstruct form supports capacity <= 16384");
   const size_t need = absorbed ? attn_absorbed_workspace(*w, *c) : attn_reconstruct_workspace(*w, *c);
   if (!ws || ws_bytes < need) return fail(QSVD_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   AttnArgs a{w, c, (const _Float16*)q, (_Float16*)out, sm_scale > 0.f ? sm_scale : 1.f / sqrtf((float)w->head_dim)};

@@ -38,42 +38,90 @@ __device__ __forceinline__ float wscale(const float* sb, int32_t N, int32_t n, i
 }
 
 // ---------------------------------------------------------------------------
-// q~ = scale * q W^u_k^T, one thread per latent index j, batch in groups of 8.
+// q~ = scale * q W^u_k^T.  One workgroup per (head, 256 latent columns): lane l
+// owns columns 4l..4l+3 of the block (one coalesced dword of int8 codes per
+// contraction row), wave w owns contraction rows [w*dh/4, (w+1)*dh/4) and
+// loads all of their codes up front.  Sequences go in blocks of 16; the query
+// times the per-channel scale sits in LDS as [c][16].  The four waves' partial
+// sums are added through LDS in a fixed order.
 // ---------------------------------------------------------------------------
+constexpr int kAbsorbBB = 16;
+
 __global__ void __launch_bounds__(256)
 absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, const float* __restrict__ sb,
               int32_t B, int32_t r, int32_t Hq, int32_t Hkv, int32_t dh, int32_t N, int32_t bits,
               int32_t group, float scale, _Float16* __restrict__ qt) {
-  __shared__ float qs[64 * 128];
-  const int h = blockIdx.x;
-  const int32_t j = blockIdx.y * 256 + threadIdx.x;
+  __shared__ __attribute__((aligned(16))) float wq[128 * kAbsorbBB];
+  __shared__ f32x4 red[4][kAbsorbBB][64];
+  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int32_t j0 = blockIdx.y * 256 + 4 * lane;
+  const bool jok = j0 < r;
   if (h >= Hq) {
-    if (j < r)
-      for (int b = 0; b < B; ++b) qt[((int64_t)b * kHeadBlk + h) * r + j] = (_Float16)0.f;
+    if (jok)
+      for (int b = w; b < B; b += 4)
+        *reinterpret_cast<uint2*>(qt + ((int64_t)b * kHeadBlk + h) * r + j0) = make_uint2(0u, 0u);
     return;
   }
-  for (int e = threadIdx.x; e < B * dh; e += 256) {
-    const int b = e / dh, c = e - b * dh;
-    qs[e] = (float)q[(int64_t)b * Hq * dh + h * dh + c];
-  }
-  __syncthreads();
-  if (j >= r) return;
   const int g = (h * Hkv) / Hq;
   const int32_t nk0 = Hq * dh + g * dh;
-  for (int b0 = 0; b0 < B; b0 += 8) {
-    float acc[8];
+  const int cpw = dh / 4;                       // contraction rows per wave (a multiple of 8)
+  const int c_begin = w * cpw;
+  for (int b0 = 0; b0 < B; b0 += kAbsorbBB) {
+    __syncthreads();
+    for (int e = tid; e < dh * kAbsorbBB; e += 256) {
+      const int c = e / kAbsorbBB, bl = e - c * kAbsorbBB, b = b0 + bl;
+      float v = 0.f;
+      if (b < B) {
+        v = (float)q[(int64_t)b * Hq * dh + h * dh + c];
+        if (!group) v *= sb[nk0 + c];
+      }
+      wq[e] = v;
+    }
+    __syncthreads();
+    f32x4 acc[kAbsorbBB];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) acc[k] = 0.f;
-    for (int c = 0; c < dh; ++c) {
-      const int32_t n = nk0 + c;
-      const float wv = wscale(sb, N, n, j, group) * wcode(bt, r, n, j, bits);
+    for (int k = 0; k < kAbsorbBB; ++k) acc[k] = f32x4{};
+    for (int cb = 0; cb < cpw; cb += 8) {
+      uint32_t raw[8];
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (b0 + k < B) acc[k] = fmaf(qs[(b0 + k) * dh + c], wv, acc[k]);
+      for (int k = 0; k < 8; ++k) {
+        const int32_t n = nk0 + c_begin + cb + k;
+        raw[k] = !jok ? 0u
+                      : bits == 8 ? *reinterpret_cast<const uint32_t*>(bt + (int64_t)n * r + j0)
+                                  : (uint32_t)*reinterpret_cast<const uint16_t*>(bt + ((int64_t)n * r + j0) / 2);
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int c = c_begin + cb + k;
+        f32x4 cf;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          cf[i] = bits == 8 ? (float)(int8_t)(raw[k] >> (8 * i)) : (float)(((int)(raw[k] << (28 - 4 * i))) >> 28);
+        if (group) cf *= sb[(int64_t)(j0 / group) * N + nk0 + c];
+#pragma unroll
+        for (int k4 = 0; k4 < kAbsorbBB; k4 += 4) {
+          const f32x4 wv = *reinterpret_cast<const f32x4*>(&wq[c * kAbsorbBB + k4]);
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[k4 + kk][i] = fmaf(wv[kk], cf[i], acc[k4 + kk][i]);
+        }
+      }
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
-      if (b0 + k < B) qt[((int64_t)(b0 + k) * kHeadBlk + h) * r + j] = to_f16(acc[k] * scale);
+    for (int k = 0; k < kAbsorbBB; ++k) red[w][k][lane] = acc[k];
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int bl = 4 * w + kk, b = b0 + bl;
+      if (b < B && jok) {
+        const f32x4 v = red[0][bl][lane] + red[1][bl][lane] + red[2][bl][lane] + red[3][bl][lane];
+        f16x4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = (_Float16)(v[i] * scale);
+        *reinterpret_cast<f16x4*>(qt + ((int64_t)b * kHeadBlk + h) * r + j0) = o;
+      }
+    }
   }
 }
 
@@ -94,7 +142,7 @@ __global__ void __launch_bounds__(NW * 64)
 latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ cdata,
                    const float* __restrict__ cscale, const int32_t* __restrict__ seq_len,
                    int32_t capacity, int32_t r, int32_t chunk, int32_t n_chunks,
-                   float* __restrict__ o_part, float* __restrict__ ml_part) {
+                   _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
   constexpr int KS = RW / 16;    // 16-wide contraction steps of the score MFMA
   constexpr int RB = RW / 32;    // 32-row blocks of the output MFMA
   constexpr int CST = RW + 8;    // staged row stride in halves
@@ -229,105 +277,161 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     ml_part[part * 64 + l32] = m_run;
     ml_part[part * 64 + 32 + l32] = l_run;
   }
-  // O^T: lane holds head l32, latent rows slice0 + 32*rb + 8*(v/4) + 4*half + v%4.
-  float* op = o_part + part * (int64_t)r * kHeadBlk;
+  // O^T / l as fp16 (a weighted mean of latent rows, so it stays in range):
+  // lane holds head l32, latent rows slice0 + 32*rb + 8*(v/4) + 4*half + v%4.
+  const float inv_l = l_run > 0.f ? 1.f / l_run : 0.f;
+  _Float16* op = o_part + part * (int64_t)r * kHeadBlk;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int row = slice0 + 32 * rb + 8 * (v >> 2) + 4 * half + (v & 3);
-      op[(int64_t)row * kHeadBlk + l32] = o[rb][v];
+      op[(int64_t)row * kHeadBlk + l32] = (_Float16)(o[rb][v] * inv_l);
     }
 }
 
 // ---------------------------------------------------------------------------
-// Merge the chunk partials of a sequence: m = max m_c, w_c = 2^(m_c - m),
-// O = sum_c w_c O_c / sum_c w_c l_c.  Partials are [x][32 heads]; the result is
-// written head-major, fp32 [b][32][width] or the final fp16 [b][Hq*width].
+// Merge the chunk partials of a sequence.  Chunk c holds m_c, l_c and the
+// normalized O_c / l_c as fp16 [x][32 heads]; with m = max m_c and
+// w_c = 2^(m_c - m) l_c, the result is sum_c w_c (O_c / l_c) / sum_c w_c.
+// The per-head weights are computed once per workgroup into LDS; each thread
+// then streams 8 heads of one row x with 16-byte loads.  Output is fp16,
+// head-major: [b][32][width] (latent form) or the final [b][Hq*width].
 // ---------------------------------------------------------------------------
-template <bool F16OUT>
+constexpr int kMaxChunks = 256;
+
+template <bool FINAL>
 __global__ void __launch_bounds__(256)
-combine_kernel(const float* __restrict__ o_part, const float* __restrict__ ml_part,
+combine_kernel(const _Float16* __restrict__ o_part, const float* __restrict__ ml_part,
                const int32_t* __restrict__ seq_len, int32_t chunk, int32_t n_chunks, int32_t n_launched,
-               int32_t width, int32_t Hq, float* __restrict__ o_lat, _Float16* __restrict__ out) {
-  __shared__ float tile[32][33];
-  const int b = blockIdx.y, x0 = blockIdx.x * 32, tid = threadIdx.x;
+               int32_t width, int32_t Hq, _Float16* __restrict__ out) {
+  __shared__ float wgt[kMaxChunks * 32];
+  __shared__ float tile[64][33];
+  const int b = blockIdx.y, x0 = blockIdx.x * 64, tid = threadIdx.x;
   const int L = seq_len[b];
-  const int nv = L > 0 ? min((L + chunk - 1) / chunk, n_launched) : 0;
+  const int nv = L > 0 ? min(min((L + chunk - 1) / chunk, n_launched), kMaxChunks) : 0;
   const int64_t pb = (int64_t)b * n_chunks;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int e = tid + 256 * i, xl = e >> 5, h = e & 31;
+  if (tid < 32) {
     float m = -INFINITY;
-    for (int c = 0; c < nv; ++c) m = fmaxf(m, ml_part[(pb + c) * 64 + h]);
-    float acc = 0.f, lsum = 0.f;
+    for (int c = 0; c < nv; ++c) m = fmaxf(m, ml_part[(pb + c) * 64 + tid]);
+    float tot = 0.f;
     for (int c = 0; c < nv; ++c) {
-      const float wc = exp2f(ml_part[(pb + c) * 64 + h] - m);
-      lsum += wc * ml_part[(pb + c) * 64 + 32 + h];
-      acc += wc * o_part[((pb + c) * width + x0 + xl) * kHeadBlk + h];
+      const float wc = exp2f(ml_part[(pb + c) * 64 + tid] - m) * ml_part[(pb + c) * 64 + 32 + tid];
+      wgt[c * 32 + tid] = wc;
+      tot += wc;
     }
-    tile[xl][h] = lsum > 0.f ? acc / lsum : 0.f;
+    const float inv = tot > 0.f ? 1.f / tot : 0.f;
+    for (int c = 0; c < nv; ++c) wgt[c * 32 + tid] *= inv;
   }
   __syncthreads();
+  // thread -> row x0 + tid/4, heads 8*(tid%4) .. +8; chunk loads in batches of 8
+  const int h0 = 8 * (tid & 3);
+  const int xl = tid >> 2;
+  const int x = x0 + xl;
+  float acc[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int e = tid + 256 * i, h = e >> 5, xl = e & 31;
-    const float v = tile[xl][h];
-    if (F16OUT) {
-      if (h < Hq) out[((int64_t)b * Hq + h) * width + x0 + xl] = to_f16(v);
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  if (x < width) {
+    const _Float16* src = o_part + (pb * width + x) * kHeadBlk + h0;
+    for (int c0 = 0; c0 < nv; c0 += 8) {
+      f16x8 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        v[k] = (c0 + k < nv) ? *reinterpret_cast<const f16x8*>(src + (int64_t)(c0 + k) * width * kHeadBlk) : f16x8{};
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (c0 + k < nv)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[e] = fmaf(wgt[(c0 + k) * 32 + h0 + e], (float)v[k][e], acc[e]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) tile[xl][h0 + e] = acc[e];
+  __syncthreads();
+  // write head-major: thread -> head tid/8 (+32 per pass... 32 heads x 64 rows)
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int e = tid + 256 * i, h = e >> 6, xl = e & 63, x = x0 + xl;
+    if (x >= width) continue;
+    const _Float16 v = (_Float16)tile[xl][h];
+    if (FINAL) {
+      if (h < Hq) out[((int64_t)b * Hq + h) * width + x] = v;
     } else {
-      o_lat[((int64_t)b * kHeadBlk + h) * width + x0 + xl] = v;
+      out[((int64_t)b * kHeadBlk + h) * width + x] = v;
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// o[b][h*dh + c] = sum_j O[b][h][j] * W^u_v[j][n], n = Hq*dh + Hkv*dh + g(h)*dh + c.
-// One workgroup per (head, 32 output columns); latent index in tiles of 128.
+// o[b][h*dh + c] = sum_j O[b][h][j] W^u_v[j][n], n = Hq*dh + Hkv*dh + g(h)*dh + c,
+// on the 16x16x32 fp16 matrix cores: rows are 16 sequences, columns 16 output
+// channels, the contraction runs over the latent index j.  One workgroup per
+// (head, 16 columns); its 4 waves split the contraction (whole scale groups
+// each) and their partial results are added through LDS in a fixed order.
+// Both fragments are loaded straight from memory: the latent result is
+// j-contiguous per (b, h), the weight codes are j-contiguous per channel.
+// Integer codes convert to fp16 exactly; the per-channel scale multiplies the
+// fp32 result, per-group scales multiply each group's partial sum.
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(256)
-vproj_kernel(const float* __restrict__ o_lat, const uint8_t* __restrict__ bt, const float* __restrict__ sb,
+vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt, const float* __restrict__ sb,
              int32_t B, int32_t r, int32_t Hq, int32_t Hkv, int32_t dh, int32_t N, int32_t bits,
              int32_t group, _Float16* __restrict__ out) {
-  __shared__ float bs[32 * 129];
-  __shared__ float os[64 * 128];
-  const int h = blockIdx.x, c0 = blockIdx.y * 32, tid = threadIdx.x;
-  const int cl = tid & 31, bq = tid >> 5;
+  __shared__ f32x4 red[4][64];
+  const int h = blockIdx.x, c0 = blockIdx.y * 16, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l16 = lane & 15, quad = lane >> 4;
   const int g = (h * Hkv) / Hq;
-  const int32_t nb = Hq * dh + Hkv * dh + g * dh + c0;
-  float acc[8];
+  const int32_t n = Hq * dh + Hkv * dh + g * dh + c0 + l16;
+  const int gsteps = group ? group / 32 : 1;       // 32-wide steps per scale group
+  const int ngroups = (r / 32) / gsteps;
+  const int g_begin = (w * ngroups) / 4, g_end = ((w + 1) * ngroups) / 4;
+  for (int b0 = 0; b0 < B; b0 += 16) {
+    const int bA = b0 + l16;
+    const _Float16* arow = o_lat + ((int64_t)min(bA, B - 1) * kHeadBlk + h) * r + 8 * quad;
+    f32x4 res = f32x4{};
+    for (int gi = g_begin; gi < g_end; ++gi) {
+      f32x4 acc = f32x4{};
+#pragma unroll 4
+      for (int st = 0; st < gsteps; ++st) {
+        const int j = (gi * gsteps + st) * 32;
+        f16x8 a = *reinterpret_cast<const f16x8*>(arow + j);
+        if (bA >= B) a = f16x8{};
+        f16x8 bw;
+        if (bits == 8) {
+          const uint2 raw = *reinterpret_cast<const uint2*>(bt + (int64_t)n * r + j + 8 * quad);
 #pragma unroll
-  for (int k = 0; k < 8; ++k) acc[k] = 0.f;
-  for (int j0 = 0; j0 < r; j0 += 128) {
-    const int jn = min(128, r - j0);
-    for (int e = tid; e < 32 * 128; e += 256) {
-      const int row = e >> 7, jj = e & 127;
-      float v = 0.f;
-      if (jj < jn) {
-        const int32_t n = nb + row, j = j0 + jj;
-        v = wcode(bt, r, n, j, bits);
-        if (group) v *= sb[(int64_t)(j / group) * N + n];
+          for (int e = 0; e < 4; ++e) {
+            bw[e] = (_Float16)(float)(int8_t)(raw.x >> (8 * e));
+            bw[4 + e] = (_Float16)(float)(int8_t)(raw.y >> (8 * e));
+          }
+        } else {
+          const uint32_t raw = *reinterpret_cast<const uint32_t*>(bt + ((int64_t)n * r + j + 8 * quad) / 2);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) bw[e] = (_Float16)(float)(((int)(raw << (28 - 4 * e))) >> 28);
+        }
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc, 0, 0, 0);
       }
-      bs[row * 129 + jj] = v;
-    }
-    for (int e = tid; e < B * 128; e += 256) {
-      const int bb = e >> 7, jj = e & 127;
-      os[e] = (jj < jn) ? o_lat[((int64_t)bb * kHeadBlk + h) * r + j0 + jj] : 0.f;
+      // acc: lane holds column l16 (channel n) and sequences b0 + 4*quad + v
+      if (group) {
+        const float sc = sb[(int64_t)gi * N + n];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) res[v] = fmaf(acc[v], sc, res[v]);
+      } else {
+        res += acc;
+      }
     }
     __syncthreads();
-    for (int jj = 0; jj < 128; ++jj) {
-      const float wv = bs[cl * 129 + jj];
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (bq + 8 * k < B) acc[k] = fmaf(os[(bq + 8 * k) * 128 + jj], wv, acc[k]);
-    }
+    red[w][lane] = res;
     __syncthreads();
-  }
-  const float cs = group ? 1.f : sb[nb + cl];
+    if (w == 0) {
+      const f32x4 tot = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
+      const float cs = group ? 1.f : sb[n];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int bb = bq + 8 * k;
-    if (bb < B) out[(int64_t)bb * Hq * dh + h * dh + c0 + cl] = to_f16(acc[k] * cs);
+      for (int v = 0; v < 4; ++v) {
+        const int bb = b0 + 4 * quad + v;
+        if (bb < B) out[(int64_t)bb * Hq * dh + h * dh + c0 + l16] = (_Float16)(tot[v] * cs);
+      }
+    }
   }
 }
 
@@ -362,9 +466,9 @@ static AbsorbPlan plan_absorbed(const qsvd_layer& w, const qsvd_cache& c) {
   p.chunk = ch;
   p.n_chunks = (len + ch - 1) / ch;
   p.qt_bytes = (size_t)c.batch * kHeadBlk * w.r * sizeof(_Float16);
-  p.opart_bytes = (size_t)c.batch * p.n0 * w.r * kHeadBlk * sizeof(float);
+  p.opart_bytes = (size_t)c.batch * p.n0 * w.r * kHeadBlk * sizeof(_Float16);
   p.ml_bytes = (size_t)c.batch * p.n0 * 64 * sizeof(float);
-  p.olat_bytes = (size_t)c.batch * kHeadBlk * w.r * sizeof(float);
+  p.olat_bytes = (size_t)c.batch * kHeadBlk * w.r * sizeof(_Float16);
   return p;
 }
 
@@ -382,7 +486,7 @@ size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c) {
 
 template <int RW, int NW, int FMT>
 static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, const _Float16* qt,
-                                float* opart, float* ml, hipStream_t s) {
+                                _Float16* opart, float* ml, hipStream_t s) {
   const size_t lds = (size_t)NW * 32 * (RW + 8) * 2 + (size_t)(NW + 1) * 1024 * 4;
   auto kern = latent_attn_kernel<RW, NW, FMT>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -396,7 +500,7 @@ static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, const 
 
 template <int FMT>
 static hipError_t dispatch_latent(const AbsorbPlan& p, const qsvd_cache& c, const _Float16* qt,
-                                  float* opart, float* ml, hipStream_t s) {
+                                  _Float16* opart, float* ml, hipStream_t s) {
   if (p.rw == 192) return launch_latent<192, 8, FMT>(p, c, qt, opart, ml, s);
   if (p.rw == 128) return launch_latent<128, 8, FMT>(p, c, qt, opart, ml, s);
   if (p.rw == 64) return launch_latent<64, 8, FMT>(p, c, qt, opart, ml, s);
@@ -410,11 +514,11 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   uint8_t* base = (uint8_t*)ws;
   _Float16* qt = (_Float16*)base;
   base += align256(p.qt_bytes);
-  float* opart = (float*)base;
+  _Float16* opart = (_Float16*)base;
   base += align256(p.opart_bytes);
   float* ml = (float*)base;
   base += align256(p.ml_bytes);
-  float* olat = (float*)base;
+  _Float16* olat = (_Float16*)base;
   const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
   {
     KernelScope ks("absorb_q", s);
@@ -429,12 +533,12 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   if (e != hipSuccess) return e;
   {
     KernelScope ks("combine", s);
-    hipLaunchKernelGGL(combine_kernel<false>, dim3(w.r / 32, c.batch), dim3(256), 0, s, opart, ml,
-                       c.seq_len, p.chunk, p.n0, p.n_chunks, w.r, w.n_q_heads, olat, (_Float16*)nullptr);
+    hipLaunchKernelGGL(combine_kernel<false>, dim3((w.r + 63) / 64, c.batch), dim3(256), 0, s, opart, ml,
+                       c.seq_len, p.chunk, p.n0, p.n_chunks, w.r, w.n_q_heads, olat);
   }
   {
     KernelScope ks("vproj", s);
-    hipLaunchKernelGGL(vproj_kernel, dim3(w.n_q_heads, w.head_dim / 32), dim3(256), 0, s, olat,
+    hipLaunchKernelGGL(vproj_kernel, dim3(w.n_q_heads, w.head_dim / 16), dim3(256), 0, s, olat,
                        (const uint8_t*)w.b_t, w.s_b, c.batch, w.r, w.n_q_heads, w.n_kv_heads,
                        w.head_dim, N, w.w_bits, w.w_group, a.out);
   }
@@ -550,7 +654,7 @@ constexpr int RCH = 64;
 __global__ void __launch_bounds__(256)
 recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ kv,
                   const int32_t* __restrict__ seq_len, int32_t capacity, int32_t Hq, int32_t Hkv,
-                  int32_t dh, float scale, int32_t n_chunks, float* __restrict__ o_part,
+                  int32_t dh, float scale, int32_t n_chunks, _Float16* __restrict__ o_part,
                   float* __restrict__ ml_part) {
   __shared__ float qs[32 * 128];
   __shared__ float ss[32 * RCH];
@@ -593,7 +697,7 @@ recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k
     ml_part[part * 64 + tid] = tid < Hq ? ml[tid] : 0.f;
     ml_part[part * 64 + 32 + tid] = tid < Hq ? ml[32 + tid] : 1.f;
   }
-  // O^T[c][h] = sum_t p[h][t] V^[t][g(h)*dh + c]
+  // O^T[c][h] / l = sum_t p[h][t] V^[t][g(h)*dh + c] / l[h], stored as fp16
   for (int e = tid; e < dh * 32; e += 256) {
     const int c = e >> 5, h = e & 31;
     float acc = 0.f;
@@ -601,8 +705,9 @@ recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k
       const int g = (h * Hkv) / Hq;
       const _Float16* vcol = kv + ((int64_t)b * capacity + t0) * nkv2 + nkv + g * dh + c;
       for (int tl = 0; tl < tn; ++tl) acc = fmaf(ss[h * RCH + tl], (float)vcol[(int64_t)tl * nkv2], acc);
+      acc /= ml[32 + h];
     }
-    o_part[(part * dh + c) * kHeadBlk + h] = acc;
+    o_part[(part * dh + c) * kHeadBlk + h] = (_Float16)acc;
   }
 }
 
@@ -616,7 +721,7 @@ static ReconPlan plan_recon(const qsvd_layer& w, const qsvd_cache& c) {
   const int nkv2 = 2 * w.n_kv_heads * w.head_dim;
   p.n_chunks = (c.capacity + RCH - 1) / RCH;
   p.kv_bytes = (size_t)c.batch * c.capacity * nkv2 * sizeof(_Float16);
-  p.opart_bytes = (size_t)c.batch * p.n_chunks * w.head_dim * kHeadBlk * sizeof(float);
+  p.opart_bytes = (size_t)c.batch * p.n_chunks * w.head_dim * kHeadBlk * sizeof(_Float16);
   p.ml_bytes = (size_t)c.batch * p.n_chunks * 64 * sizeof(float);
   return p;
 }
@@ -633,7 +738,7 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
   uint8_t* base = (uint8_t*)ws;
   _Float16* kv = (_Float16*)base;
   base += align256(p.kv_bytes);
-  float* opart = (float*)base;
+  _Float16* opart = (_Float16*)base;
   base += align256(p.opart_bytes);
   float* ml = (float*)base;
   const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
@@ -662,8 +767,8 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
   }
   {
     KernelScope ks("recon_combine", s);
-    hipLaunchKernelGGL(combine_kernel<true>, dim3(w.head_dim / 32, c.batch), dim3(256), 0, s, opart, ml,
-                       c.seq_len, RCH, p.n_chunks, nch, w.head_dim, w.n_q_heads, (float*)nullptr, a.out);
+    hipLaunchKernelGGL(combine_kernel<true>, dim3((w.head_dim + 63) / 64, c.batch), dim3(256), 0, s, opart, ml,
+                       c.seq_len, RCH, p.n_chunks, nch, w.head_dim, w.n_q_heads, a.out);
   }
   return hipGetLastError();
 }

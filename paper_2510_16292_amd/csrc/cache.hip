@@ -22,6 +22,29 @@ cache_append_kernel(const uint8_t* __restrict__ src, const float* __restrict__ s
   if (dst_scale && threadIdx.x == 0) dst_scale[drow] = src_scale[srow];
 }
 
+// Decode-sized appends (few rows per sequence): one workgroup per sequence
+// copies its rows, then advances seq_len[b] itself after a barrier, so no
+// second launch is needed.
+__global__ void __launch_bounds__(256)
+cache_append_fused_kernel(const uint8_t* __restrict__ src, const float* __restrict__ src_scale,
+                          uint8_t* __restrict__ dst, float* __restrict__ dst_scale,
+                          int32_t* __restrict__ seq_len, int32_t capacity, int32_t n_new, int32_t row_bytes) {
+  const int b = blockIdx.x;
+  const int32_t base = seq_len[b];
+  const int per_row = row_bytes / 16;
+  for (int e = threadIdx.x; e < n_new * per_row; e += blockDim.x) {
+    const int i = e / per_row, k = e - i * per_row;
+    const int32_t pos = base + i;
+    if (pos < 0 || pos >= capacity) continue;
+    const int64_t srow = (int64_t)b * n_new + i;
+    const int64_t drow = (int64_t)b * capacity + pos;
+    reinterpret_cast<uint4*>(dst + drow * row_bytes)[k] = reinterpret_cast<const uint4*>(src + srow * row_bytes)[k];
+    if (dst_scale && k == 0) dst_scale[drow] = src_scale[srow];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) seq_len[b] = base + n_new;
+}
+
 __global__ void seq_len_advance_kernel(int32_t* __restrict__ seq_len, int32_t batch, int32_t n_new) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b < batch) seq_len[b] += n_new;
@@ -41,6 +64,13 @@ hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void*
   } else {
     row_bytes = c.r / 2;
     src = cq;
+  }
+  if (n_new <= 16) {
+    KernelScope ks("cache_append", s);
+    hipLaunchKernelGGL(cache_append_fused_kernel, dim3(c.batch), dim3(256), 0, s, (const uint8_t*)src,
+                       c.fmt == QSVD_CACHE_F16 ? nullptr : sc, (uint8_t*)c.data,
+                       c.fmt == QSVD_CACHE_F16 ? nullptr : c.scale, c.seq_len, c.capacity, n_new, row_bytes);
+    return hipGetLastError();
   }
   {
     KernelScope ks("cache_append", s);

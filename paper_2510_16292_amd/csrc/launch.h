@@ -38,8 +38,15 @@ struct GemmArgs {
   OutSeg seg[3];
   int32_t n_seg;
   int32_t* dbg;         // optional int32 [M][N]
+  // Down-projection only: when cq is set, the fp16 result (segment 0, ld == N)
+  // is also quantized per row with abits into cq / sc.
+  void* cq;
+  float* sc;
+  int32_t abits;
 };
-hipError_t launch_gemm_i8(const GemmArgs& g, void* ws, hipStream_t s);
+// Refuses (hipErrorInvalidValue, nothing launched) a workspace smaller than
+// gemm_i8_workspace(g.M, g.N, g.K).
+hipError_t launch_gemm_i8(const GemmArgs& g, void* ws, size_t ws_bytes, hipStream_t s);
 size_t gemm_i8_workspace(int64_t M, int32_t N, int32_t K);
 
 hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void* cq,
