@@ -45,7 +45,23 @@ def parse():
     ap.add_argument("--mode", choices=["auto", "absorbed", "reconstruct"], default="auto")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without the kernel events")
+    ap.add_argument("--legs", default="decode,prefill", help="comma list of legs to run: decode, prefill")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
+                    help="also run a plain device copy of MB megabytes (calibrates memory counters)")
     return ap.parse_args()
+
+
+def copy_probe(mb):
+    """A plain copy of mb * 2^20 bytes, 4 times, for scaling hardware byte counters."""
+    import torch
+    n = mb * (1 << 20) // 2
+    src = torch.ones(n, dtype=torch.float16, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(4):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(f"[bench] copy probe: 4 copies of {mb} MiB", file=sys.stderr, flush=True)
 
 
 def cpu_threads():
@@ -283,11 +299,20 @@ def main():
     B.lib()
     wl2, wl3 = configs.get(2), configs.get(3)
     factors, host_layer = layer_weights(wl2)        # one 7B-shaped layer serves both legs
-    print(f"[bench] decode: {args.steps} steps, warmup {args.warmup}", file=sys.stderr, flush=True)
-    dec = bench_decode(args, wl3, host_layer)
-    print(f"[bench] decode done: {dec['ms_per_step']:.4f} ms/step", file=sys.stderr, flush=True)
-    pre = bench_prefill(args, wl2, host_layer)
-    print(f"[bench] prefill done: {pre['value']} TOPS", file=sys.stderr, flush=True)
+    legs = set(args.legs.split(","))
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+    dec, pre = None, None
+    if "decode" in legs:
+        print(f"[bench] decode: {args.steps} steps, warmup {args.warmup}", file=sys.stderr, flush=True)
+        dec = bench_decode(args, wl3, host_layer)
+        print(f"[bench] decode done: {dec['ms_per_step']:.4f} ms/step", file=sys.stderr, flush=True)
+    if "prefill" in legs:
+        pre = bench_prefill(args, wl2, host_layer)
+        print(f"[bench] prefill done: {pre['value']} TOPS", file=sys.stderr, flush=True)
+    if dec is None:
+        print(json.dumps({"prefill": pre}), flush=True)
+        return
     line = {
         "metric": METRIC,
         "value": round(dec["tokens_per_s"], 1),
@@ -311,10 +336,13 @@ def main():
         "attention_form_us": dec["attention_form_us"],
         "prefill": pre,
     }
+    if pre is None:
+        line.pop("prefill")
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline_decode(wl3, factors)
-        line["prefill"]["cpu_baseline"] = cpu_baseline_prefill(wl2, factors)
+        if pre is not None:
+            line["prefill"]["cpu_baseline"] = cpu_baseline_prefill(wl2, factors)
     print(json.dumps(line), flush=True)
 
 

@@ -16,6 +16,8 @@
 // with an fp16 matrix-core GEMM and a plain split-context attention follows.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
 
@@ -145,13 +147,18 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
                    _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
   constexpr int KS = RW / 16;    // 16-wide contraction steps of the score MFMA
   constexpr int RB = RW / 32;    // 32-row blocks of the output MFMA
-  constexpr int CST = RW + 8;    // staged row stride in halves
+  // Staged row stride in halves: RW + 16 makes the stride 8 (mod 32) dwords, so
+  // the 16 lanes of a transpose read (4 rows x 4 chunks of 8 bytes) hit
+  // distinct banks.
+  constexpr int CST = RW + 16;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
   _Float16* cst = reinterpret_cast<_Float16*>(smem) + w * 32 * CST;
-  float* spart = reinterpret_cast<float*>(smem + NW * 32 * CST * 2);
-  float* ssum = spart + NW * 1024;
+  // Score exchange: wave w stores its 32x32 partial as f32x4 [w][v/4][lane],
+  // 256 threads add the NW partials in wave order into ssum4 [v/4][lane].
+  f32x4* spart4 = reinterpret_cast<f32x4*>(smem + NW * 32 * CST * 2);
+  f32x4* ssum4 = spart4 + NW * 256;
 
   const int b = blockIdx.y, ch = blockIdx.x;
   const int L = min(seq_len[b], capacity);
@@ -171,25 +178,35 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   for (int rb = 0; rb < RB; ++rb) o[rb] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
+  // A operand of the score MFMA: token (t0 + l32), latent columns 8*half + 16*ks.
+  // Raw tile registers: fp16 rows as they are, int8 rows as 8-byte chunks.
+  using RawT = typename std::conditional<FMT == QSVD_CACHE_F16, f16x8, uint2>::type;
+  RawT raw[KS];
+  auto load_tile = [&](int t0) {
+    // rows past the chunk end are masked; re-read the last row instead of
+    // fetching the next chunk's rows
+    const int tk = min(t0 + l32, t_end - 1);
+    const int64_t off = ((int64_t)b * capacity + tk) * r + slice0 + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (FMT == QSVD_CACHE_F16)
+        raw[ks] = *reinterpret_cast<const RawT*>(reinterpret_cast<const _Float16*>(cdata) + off + 16 * ks);
+      else
+        raw[ks] = *reinterpret_cast<const RawT*>(reinterpret_cast<const int8_t*>(cdata) + off + 16 * ks);
+    }
+  };
+  load_tile(t_begin);
   for (int t0 = t_begin; t0 < t_end; t0 += 32) {
-    // A operand of the score MFMA: token (t0 + l32), latent columns 8*half + 16*ks.
-    const int tk = min(t0 + l32, L - 1);
     f16x8 cf[KS];
-    if (FMT == QSVD_CACHE_F16) {
-      const _Float16* crow = reinterpret_cast<const _Float16*>(cdata) +
-                             ((int64_t)b * capacity + tk) * r + slice0 + 8 * half;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) cf[ks] = *reinterpret_cast<const f16x8*>(crow + 16 * ks);
-    } else {
-      const int8_t* crow = reinterpret_cast<const int8_t*>(cdata) +
-                           ((int64_t)b * capacity + tk) * r + slice0 + 8 * half;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const uint2 raw = *reinterpret_cast<const uint2*>(crow + 16 * ks);
+    for (int ks = 0; ks < KS; ++ks) {
+      if constexpr (FMT == QSVD_CACHE_F16) {
+        cf[ks] = raw[ks];
+      } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          cf[ks][e] = (_Float16)(float)(int8_t)(raw.x >> (8 * e));
-          cf[ks][4 + e] = (_Float16)(float)(int8_t)(raw.y >> (8 * e));
+          cf[ks][e] = (_Float16)(float)(int8_t)(raw[ks].x >> (8 * e));
+          cf[ks][4 + e] = (_Float16)(float)(int8_t)(raw[ks].y >> (8 * e));
         }
       }
     }
@@ -200,14 +217,18 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       *reinterpret_cast<f16x8*>(cst + l32 * CST + 16 * ks + 8 * half) = cf[ks];
+    // The next tile streams in while this one is reduced, normalized and
+    // multiplied into the output.
+    if (t0 + 32 < t_end) load_tile(t0 + 32);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) spart[(w * 16 + v) * 64 + lane] = sacc[v];
+    for (int vb = 0; vb < 4; ++vb)
+      spart4[(w * 4 + vb) * 64 + lane] = f32x4{sacc[4 * vb], sacc[4 * vb + 1], sacc[4 * vb + 2], sacc[4 * vb + 3]};
     __syncthreads();
-    for (int e = tid; e < 1024; e += NW * 64) {
-      float acc = 0.f;
+    if (tid < 256) {
+      f32x4 acc = spart4[tid];
 #pragma unroll
-      for (int w2 = 0; w2 < NW; ++w2) acc += spart[w2 * 1024 + e];
-      ssum[e] = acc;
+      for (int w2 = 1; w2 < NW; ++w2) acc += spart4[w2 * 256 + tid];
+      ssum4[tid] = acc;
     }
     __syncthreads();
     // Lane l holds head l32 and tokens t0 + 8*(v/4) + 4*half + v%4.
@@ -215,7 +236,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
-      float x = ssum[v * 64 + lane];
+      float x = ssum4[(v >> 2) * 64 + lane][v & 3];
       if (FMT != QSVD_CACHE_F16) x *= cscale[(int64_t)b * capacity + min(t, L - 1)];
       s[v] = (t < t_end) ? x : -INFINITY;
     }
@@ -230,20 +251,23 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
 #pragma unroll
       for (int v = 0; v < 16; ++v) p[v] = 0.f;
     } else {
-      alpha = exp2f(m_run - m_new);
+      alpha = __builtin_amdgcn_exp2f(m_run - m_new);
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        p[v] = exp2f(s[v] - m_new);
+        p[v] = __builtin_amdgcn_exp2f(s[v] - m_new);
         ps += p[v];
       }
     }
     ps += __shfl_xor(ps, 32, 64);
     l_run = l_run * alpha + ps;
     m_run = m_new;
+    // Once the running maxima settle, alpha is 1 for every head of the wave.
+    if (__any(alpha != 1.f)) {
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) o[rb][v] *= alpha;
+        for (int v = 0; v < 16; ++v) o[rb][v] *= alpha;
+    }
     // P^T as the B operand: k-slot (half, e) of MFMA mf is token 16*mf + 8*(e/4) + 4*half + e%4,
     // exactly the tokens this lane already holds in p[8*mf + e].
     f16x8 pf[2];
@@ -258,16 +282,27 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
         }
         pf[mf][e] = (_Float16)pv;
       }
+    // A operand of the output MFMA: lane l needs column rb*32 + l32 of the
+    // staged tile at tokens 16*mf + 8*(e/4) + 4*half + e%4.  The LDS transpose
+    // read returns, to lane i of each 16-lane group, element i%4 of the 4-half
+    // chunk addressed by lane 4*e + i/4 of that group; so lane s of group
+    // (half, q) addresses token 4*half + s/4 (+8 for the second read), columns
+    // rb*32 + 16*q + 4*(s%4) .. +3, and receives its 4 tokens of one column.
+    const int s16 = lane & 15, q16 = (lane >> 4) & 1;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
       for (int mf = 0; mf < 2; ++mf) {
-        f16x8 a;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int tau = 16 * mf + 8 * (e >> 2) + 4 * half + (e & 3);
-          a[e] = cst[tau * CST + rb * 32 + l32];
-        }
+        const int tok = 16 * mf + 4 * half + (s16 >> 2);
+        const int col = rb * 32 + 16 * q16 + 4 * (s16 & 3);
+        typedef short s16x4 __attribute__((ext_vector_type(4)));
+        typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s16x4*)(cst + tok * CST + col));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s16x4*)(cst + (tok + 8) * CST + col));
+        const f16x4 flo = __builtin_bit_cast(f16x4, lo), fhi = __builtin_bit_cast(f16x4, hi);
+        const f16x8 a = {flo[0], flo[1], flo[2], flo[3], fhi[0], fhi[1], fhi[2], fhi[3]};
         o[rb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pf[mf], o[rb], 0, 0, 0);
       }
   }
@@ -462,7 +497,7 @@ static AbsorbPlan plan_absorbed(const qsvd_layer& w, const qsvd_cache& c) {
   p.n0 = target_chunks(c.batch);
   const int len = c.max_len > 0 ? c.max_len : 1;
   int ch = (len + p.n0 - 1) / p.n0;
-  ch = ((ch + 31) / 32) * 32;
+  ch = ((ch + 15) / 16) * 16;
   p.chunk = ch;
   p.n_chunks = (len + ch - 1) / ch;
   p.qt_bytes = (size_t)c.batch * kHeadBlk * w.r * sizeof(_Float16);
@@ -487,7 +522,7 @@ size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c) {
 template <int RW, int NW, int FMT>
 static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, const _Float16* qt,
                                 _Float16* opart, float* ml, hipStream_t s) {
-  const size_t lds = (size_t)NW * 32 * (RW + 8) * 2 + (size_t)(NW + 1) * 1024 * 4;
+  const size_t lds = (size_t)NW * 32 * (RW + 16) * 2 + (size_t)(NW + 1) * 1024 * 4;
   auto kern = latent_attn_kernel<RW, NW, FMT>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
