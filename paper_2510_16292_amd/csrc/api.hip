@@ -279,6 +279,7 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
   if (w->head_dim % 32 || w->head_dim > 128) return fail(QSVD_ERR_UNSUPPORTED, "head_dim must be 32, 64, 96 or 128");
   if (c->batch > 64) return fail(QSVD_ERR_UNSUPPORTED, "at most 64 sequences per call");
   if (c->fmt == QSVD_CACHE_I4) return fail(QSVD_ERR_UNSUPPORTED, "int4 cache attention is not implemented");
+  if (w->w_group % 64) return fail(QSVD_ERR_UNSUPPORTED, "decode attention needs w_group 0 or a multiple of 64");
   if (!aligned(q, 16) || !aligned(out, 16)) return fail(QSVD_ERR_UNSUPPORTED, "q/out must be 16-byte aligned");
   const bool abs_ok = absorbed_supported(*w, *c);
   if (mode == QSVD_ATTN_ABSORBED && !abs_ok) return fail(QSVD_ERR_UNSUPPORTED, "absorbed form needs r in {128, 512, 1024, 1536}");

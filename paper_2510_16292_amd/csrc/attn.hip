@@ -25,6 +25,7 @@ namespace qsvd {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kHeadBlk = 32;   // query heads are padded to one 32-wide MFMA block
+constexpr int kMaxChunks = 256;  // context chunks per sequence the merge supports
 
 // ---------------------------------------------------------------------------
 // Weight code access (int8 or packed int4), transposed layout [N][r].
@@ -40,90 +41,92 @@ __device__ __forceinline__ float wscale(const float* sb, int32_t N, int32_t n, i
 }
 
 // ---------------------------------------------------------------------------
-// q~ = scale * q W^u_k^T.  One workgroup per (head, 256 latent columns): lane l
-// owns columns 4l..4l+3 of the block (one coalesced dword of int8 codes per
-// contraction row), wave w owns contraction rows [w*dh/4, (w+1)*dh/4) and
-// loads all of their codes up front.  Sequences go in blocks of 16; the query
-// times the per-channel scale sits in LDS as [c][16].  The four waves' partial
-// sums are added through LDS in a fixed order.
+// q~ = scale * q W^u_k^T on the 16x16x32 fp16 matrix cores.  One wave per
+// (head h, 64 latent columns j): the dh x 64 block of W^u_k codes (rows
+// c = key channel, contiguous in j) is staged in LDS as fp16 with its scale
+// folded in; the MFMA needs 8 consecutive c of one column j per lane, which
+// two LDS transpose reads deliver (lane s of each 16-lane group addresses row
+// base + s/4 at columns 4*(s%4)..+3 and receives 4 rows of one column).  Rows
+// of the product are 16 sequences (query rows loaded straight from memory),
+// columns 16 latent indices, the contraction the dh key channels.
 // ---------------------------------------------------------------------------
-constexpr int kAbsorbBB = 16;
+constexpr int kAbsorbJ = 64;
+constexpr int kAbsorbLd = kAbsorbJ + 16;   // stride 40 dwords = 8 (mod 32): conflict-free transpose reads
 
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(64)
 absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, const float* __restrict__ sb,
               int32_t B, int32_t r, int32_t Hq, int32_t Hkv, int32_t dh, int32_t N, int32_t bits,
               int32_t group, float scale, _Float16* __restrict__ qt) {
-  __shared__ __attribute__((aligned(16))) float wq[128 * kAbsorbBB];
-  __shared__ f32x4 red[4][kAbsorbBB][64];
-  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int32_t j0 = blockIdx.y * 256 + 4 * lane;
-  const bool jok = j0 < r;
+  __shared__ __attribute__((aligned(16))) _Float16 wk[128 * kAbsorbLd];
+  const int h = blockIdx.x, lane = threadIdx.x;
+  const int32_t jb = blockIdx.y * kAbsorbJ;
   if (h >= Hq) {
-    if (jok)
-      for (int b = w; b < B; b += 4)
-        *reinterpret_cast<uint2*>(qt + ((int64_t)b * kHeadBlk + h) * r + j0) = make_uint2(0u, 0u);
+    for (int e = lane; e < B * (kAbsorbJ / 8); e += 64) {
+      const int b = e / (kAbsorbJ / 8), j8 = e - b * (kAbsorbJ / 8);
+      *reinterpret_cast<f16x8*>(qt + ((int64_t)b * kHeadBlk + h) * r + jb + 8 * j8) = f16x8{};
+    }
     return;
   }
   const int g = (h * Hkv) / Hq;
   const int32_t nk0 = Hq * dh + g * dh;
-  const int cpw = dh / 4;                       // contraction rows per wave (a multiple of 8)
-  const int c_begin = w * cpw;
-  for (int b0 = 0; b0 < B; b0 += kAbsorbBB) {
-    __syncthreads();
-    for (int e = tid; e < dh * kAbsorbBB; e += 256) {
-      const int c = e / kAbsorbBB, bl = e - c * kAbsorbBB, b = b0 + bl;
-      float v = 0.f;
-      if (b < B) {
-        v = (float)q[(int64_t)b * Hq * dh + h * dh + c];
-        if (!group) v *= sb[nk0 + c];
-      }
-      wq[e] = v;
-    }
-    __syncthreads();
-    f32x4 acc[kAbsorbBB];
-#pragma unroll
-    for (int k = 0; k < kAbsorbBB; ++k) acc[k] = f32x4{};
-    for (int cb = 0; cb < cpw; cb += 8) {
-      uint32_t raw[8];
+  // stage: chunk e -> row c = e / 4, 16 codes at columns 16 * (e % 4)
+  for (int e = lane; e < dh * 4; e += 64) {
+    const int c = e >> 2, j16 = (e & 3) * 16;
+    const int32_t n = nk0 + c;
+    float sc = group ? sb[(int64_t)(jb / group) * N + n] : sb[n];
+    f16x8 lo, hi;
+    if (bits == 8) {
+      const uint4 raw = *reinterpret_cast<const uint4*>(bt + (int64_t)n * r + jb + j16);
+      const uint32_t wv[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const int32_t n = nk0 + c_begin + cb + k;
-        raw[k] = !jok ? 0u
-                      : bits == 8 ? *reinterpret_cast<const uint32_t*>(bt + (int64_t)n * r + j0)
-                                  : (uint32_t)*reinterpret_cast<const uint16_t*>(bt + ((int64_t)n * r + j0) / 2);
+        lo[k] = (_Float16)((float)(int8_t)(wv[k >> 2] >> (8 * (k & 3))) * sc);
+        hi[k] = (_Float16)((float)(int8_t)(wv[2 + (k >> 2)] >> (8 * (k & 3))) * sc);
       }
+    } else {
+      const uint2 raw = *reinterpret_cast<const uint2*>(bt + ((int64_t)n * r + jb + j16) / 2);
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const int c = c_begin + cb + k;
-        f32x4 cf;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          cf[i] = bits == 8 ? (float)(int8_t)(raw[k] >> (8 * i)) : (float)(((int)(raw[k] << (28 - 4 * i))) >> 28);
-        if (group) cf *= sb[(int64_t)(j0 / group) * N + nk0 + c];
-#pragma unroll
-        for (int k4 = 0; k4 < kAbsorbBB; k4 += 4) {
-          const f32x4 wv = *reinterpret_cast<const f32x4*>(&wq[c * kAbsorbBB + k4]);
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) acc[k4 + kk][i] = fmaf(wv[kk], cf[i], acc[k4 + kk][i]);
-        }
+        lo[k] = (_Float16)((float)(((int)(raw.x << (28 - 4 * k))) >> 28) * sc);
+        hi[k] = (_Float16)((float)(((int)(raw.y << (28 - 4 * k))) >> 28) * sc);
       }
     }
+    *reinterpret_cast<f16x8*>(&wk[c * kAbsorbLd + j16]) = lo;
+    *reinterpret_cast<f16x8*>(&wk[c * kAbsorbLd + j16 + 8]) = hi;
+  }
+  __syncthreads();
+  const int l16 = lane & 15, quad = lane >> 4;
+  const int s16 = lane & 15;
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  for (int b0 = 0; b0 < B; b0 += 16) {
+    const int bA = b0 + l16;
+    const _Float16* qrow = q + (int64_t)min(bA, B - 1) * Hq * dh + h * dh + 8 * quad;
+    f32x4 acc[kAbsorbJ / 16];
 #pragma unroll
-    for (int k = 0; k < kAbsorbBB; ++k) red[w][k][lane] = acc[k];
-    __syncthreads();
+    for (int jj = 0; jj < kAbsorbJ / 16; ++jj) acc[jj] = f32x4{};
+    for (int c0 = 0; c0 < dh; c0 += 32) {
+      f16x8 a = *reinterpret_cast<const f16x8*>(qrow + c0);
+      if (bA >= B) a = f16x8{};
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int bl = 4 * w + kk, b = b0 + bl;
-      if (b < B && jok) {
-        const f32x4 v = red[0][bl][lane] + red[1][bl][lane] + red[2][bl][lane] + red[3][bl][lane];
-        f16x4 o;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = (_Float16)(v[i] * scale);
-        *reinterpret_cast<f16x4*>(qt + ((int64_t)b * kHeadBlk + h) * r + j0) = o;
+      for (int jj = 0; jj < kAbsorbJ / 16; ++jj) {
+        const int row = c0 + 8 * quad + (s16 >> 2);
+        const int col = jj * 16 + 4 * (s16 & 3);
+        const s16x4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)&wk[row * kAbsorbLd + col]);
+        const s16x4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)&wk[(row + 4) * kAbsorbLd + col]);
+        const f16x4 f0 = __builtin_bit_cast(f16x4, x0), f1 = __builtin_bit_cast(f16x4, x1);
+        const f16x8 bw = {f0[0], f0[1], f0[2], f0[3], f1[0], f1[1], f1[2], f1[3]};
+        acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc[jj], 0, 0, 0);
       }
     }
+    // lane holds column jb + 16*jj + l16 and sequences b0 + 4*quad + v
+#pragma unroll
+    for (int jj = 0; jj < kAbsorbJ / 16; ++jj)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int b = b0 + 4 * quad + v;
+        if (b < B) qt[((int64_t)b * kHeadBlk + h) * r + jb + 16 * jj + l16] = (_Float16)(acc[jj][v] * scale);
+      }
   }
 }
 
@@ -312,17 +315,86 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     ml_part[part * 64 + l32] = m_run;
     ml_part[part * 64 + 32 + l32] = l_run;
   }
-  // O^T / l as fp16 (a weighted mean of latent rows, so it stays in range):
-  // lane holds head l32, latent rows slice0 + 32*rb + 8*(v/4) + 4*half + v%4.
+  // O^T / l as fp16 (a weighted mean of latent rows, so it stays in range),
+  // stored head-major [h][x]: lane holds head l32 and latent rows
+  // slice0 + 32*rb + 8*(v/4) + 4*half + v%4, so the wave transposes its slice
+  // through its own staging rows and then writes 16-byte runs of one head.
   const float inv_l = l_run > 0.f ? 1.f / l_run : 0.f;
-  _Float16* op = o_part + part * (int64_t)r * kHeadBlk;
+  constexpr int OST = RW + 8;                  // 32 * OST <= 32 * CST halves
+  __syncthreads();
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int row = slice0 + 32 * rb + 8 * (v >> 2) + 4 * half + (v & 3);
-      op[(int64_t)row * kHeadBlk + l32] = (_Float16)(o[rb][v] * inv_l);
+    for (int v = 0; v < 16; ++v)
+      cst[l32 * OST + 32 * rb + 8 * (v >> 2) + 4 * half + (v & 3)] = (_Float16)(o[rb][v] * inv_l);
+  __syncthreads();
+  _Float16* op = o_part + part * (int64_t)r * kHeadBlk;
+  for (int e = lane; e < 32 * (RW / 8); e += 64) {
+    const int hh = e / (RW / 8), x8 = e - hh * (RW / 8);
+    *reinterpret_cast<f16x8*>(op + (int64_t)hh * r + slice0 + 8 * x8) =
+        *reinterpret_cast<const f16x8*>(cst + hh * OST + 8 * x8);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Merge the chunk partials of the latent form.  Chunk c of sequence b holds
+// m_c, l_c per head and the normalized O_c / l_c as fp16, head-major
+// [c][32][r].  One wave per (sequence, head, 512 latent columns): lane l owns
+// 8 columns, issues the loads of every chunk at once, and writes
+// O[b][h][:] = sum_c w_c (O_c / l_c) with w_c = 2^(m_c - m) l_c / sum (fp16).
+// ---------------------------------------------------------------------------
+constexpr int kMergeCols = 512;
+constexpr int kMergeBatch = 16;
+
+__global__ void __launch_bounds__(64)
+merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict__ ml_part,
+                    const int32_t* __restrict__ seq_len, int32_t chunk, int32_t n_chunks, int32_t n_launched,
+                    int32_t r, _Float16* __restrict__ o_lat) {
+  const int b = blockIdx.z, h = blockIdx.y, lane = threadIdx.x;
+  const int j = blockIdx.x * kMergeCols + 8 * lane;
+  const int L = seq_len[b];
+  const int nv = L > 0 ? min((L + chunk - 1) / chunk, n_launched) : 0;
+  const int64_t pb = (int64_t)b * n_chunks;
+  float acc[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+  const bool jok = j < r;
+  const _Float16* src = o_part + (pb * kHeadBlk + h) * r + (jok ? j : 0);
+  // lane c holds chunk c0 + c's weight 2^(m_c - m) l_c / sum (chunks in batches of 64)
+  float m = -INFINITY;
+  for (int c0 = 0; c0 < nv; c0 += 64)
+    if (c0 + lane < nv) m = fmaxf(m, ml_part[(pb + c0 + lane) * 64 + h]);
+  m = wave_max(m);
+  float tot = 0.f;
+  for (int c0 = 0; c0 < nv; c0 += 64)
+    if (c0 + lane < nv) tot += exp2f(ml_part[(pb + c0 + lane) * 64 + h] - m) * ml_part[(pb + c0 + lane) * 64 + 32 + h];
+  tot = wave_sum(tot);
+  const float inv = tot > 0.f ? 1.f / tot : 0.f;
+  for (int c0 = 0; c0 < nv; c0 += 64) {
+    const float wl = (c0 + lane < nv)
+                         ? exp2f(ml_part[(pb + c0 + lane) * 64 + h] - m) * ml_part[(pb + c0 + lane) * 64 + 32 + h] * inv
+                         : 0.f;
+    const int nb = min(64, nv - c0);
+    for (int k0 = 0; k0 < nb; k0 += kMergeBatch) {
+      f16x8 v[kMergeBatch];
+#pragma unroll
+      for (int k = 0; k < kMergeBatch; ++k)
+        v[k] = (jok && k0 + k < nb) ? *reinterpret_cast<const f16x8*>(src + (int64_t)(c0 + k0 + k) * kHeadBlk * r)
+                                    : f16x8{};
+#pragma unroll
+      for (int k = 0; k < kMergeBatch; ++k) {
+        const float wc = __shfl(wl, k0 + k, 64);
+        if (k0 + k < nb)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) acc[q] = fmaf(wc, (float)v[k][q], acc[q]);
+      }
     }
+  }
+  if (!jok) return;
+  f16x8 o8;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) o8[k] = (_Float16)acc[k];
+  *reinterpret_cast<f16x8*>(o_lat + ((int64_t)b * kHeadBlk + h) * r + j) = o8;
 }
 
 // ---------------------------------------------------------------------------
@@ -333,8 +405,6 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
 // then streams 8 heads of one row x with 16-byte loads.  Output is fp16,
 // head-major: [b][32][width] (latent form) or the final [b][Hq*width].
 // ---------------------------------------------------------------------------
-constexpr int kMaxChunks = 256;
-
 template <bool FINAL>
 __global__ void __launch_bounds__(256)
 combine_kernel(const _Float16* __restrict__ o_part, const float* __restrict__ ml_part,
@@ -401,65 +471,79 @@ combine_kernel(const _Float16* __restrict__ o_part, const float* __restrict__ ml
 // o[b][h*dh + c] = sum_j O[b][h][j] W^u_v[j][n], n = Hq*dh + Hkv*dh + g(h)*dh + c,
 // on the 16x16x32 fp16 matrix cores: rows are 16 sequences, columns 16 output
 // channels, the contraction runs over the latent index j.  One workgroup per
-// (head, 16 columns); its 4 waves split the contraction (whole scale groups
-// each) and their partial results are added through LDS in a fixed order.
-// Both fragments are loaded straight from memory: the latent result is
-// j-contiguous per (b, h), the weight codes are j-contiguous per channel.
-// Integer codes convert to fp16 exactly; the per-channel scale multiplies the
-// fp32 result, per-group scales multiply each group's partial sum.
+// (head, 16 columns); its 8 waves split the contraction into equal runs of
+// 32-wide steps, load all fragments of a run at once, and add their partial
+// results through LDS in a fixed order.  Both fragments come straight from
+// memory (j-contiguous).  Integer codes convert to fp16 exactly; the
+// per-channel scale multiplies the final sum, a per-group scale the product of
+// each step (a step never straddles a group).
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256)
+constexpr int kVprojWaves = 8;
+constexpr int kVprojBatch = 8;
+
+__global__ void __launch_bounds__(64 * kVprojWaves)
 vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt, const float* __restrict__ sb,
              int32_t B, int32_t r, int32_t Hq, int32_t Hkv, int32_t dh, int32_t N, int32_t bits,
              int32_t group, _Float16* __restrict__ out) {
-  __shared__ f32x4 red[4][64];
+  __shared__ f32x4 red[kVprojWaves][64];
   const int h = blockIdx.x, c0 = blockIdx.y * 16, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, quad = lane >> 4;
   const int g = (h * Hkv) / Hq;
   const int32_t n = Hq * dh + Hkv * dh + g * dh + c0 + l16;
-  const int gsteps = group ? group / 32 : 1;       // 32-wide steps per scale group
-  const int ngroups = (r / 32) / gsteps;
-  const int g_begin = (w * ngroups) / 4, g_end = ((w + 1) * ngroups) / 4;
+  const int steps = r / 32;
+  const int s_begin = (w * steps) / kVprojWaves, s_end = ((w + 1) * steps) / kVprojWaves;
   for (int b0 = 0; b0 < B; b0 += 16) {
     const int bA = b0 + l16;
     const _Float16* arow = o_lat + ((int64_t)min(bA, B - 1) * kHeadBlk + h) * r + 8 * quad;
     f32x4 res = f32x4{};
-    for (int gi = g_begin; gi < g_end; ++gi) {
-      f32x4 acc = f32x4{};
-#pragma unroll 4
-      for (int st = 0; st < gsteps; ++st) {
-        const int j = (gi * gsteps + st) * 32;
-        f16x8 a = *reinterpret_cast<const f16x8*>(arow + j);
-        if (bA >= B) a = f16x8{};
+    for (int st0 = s_begin; st0 < s_end; st0 += kVprojBatch) {
+      f16x8 a[kVprojBatch];
+      uint2 raw[kVprojBatch];
+#pragma unroll
+      for (int k = 0; k < kVprojBatch; ++k) {
+        const int j = (st0 + k) * 32;
+        if (st0 + k < s_end) {
+          a[k] = *reinterpret_cast<const f16x8*>(arow + j);
+          if (bits == 8) {
+            raw[k] = *reinterpret_cast<const uint2*>(bt + (int64_t)n * r + j + 8 * quad);
+          } else {
+            raw[k].x = *reinterpret_cast<const uint32_t*>(bt + ((int64_t)n * r + j + 8 * quad) / 2);
+            raw[k].y = 0u;
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kVprojBatch; ++k) {
+        if (st0 + k >= s_end) continue;
         f16x8 bw;
         if (bits == 8) {
-          const uint2 raw = *reinterpret_cast<const uint2*>(bt + (int64_t)n * r + j + 8 * quad);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            bw[e] = (_Float16)(float)(int8_t)(raw.x >> (8 * e));
-            bw[4 + e] = (_Float16)(float)(int8_t)(raw.y >> (8 * e));
+            bw[e] = (_Float16)(float)(int8_t)(raw[k].x >> (8 * e));
+            bw[4 + e] = (_Float16)(float)(int8_t)(raw[k].y >> (8 * e));
           }
         } else {
-          const uint32_t raw = *reinterpret_cast<const uint32_t*>(bt + ((int64_t)n * r + j + 8 * quad) / 2);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) bw[e] = (_Float16)(float)(((int)(raw << (28 - 4 * e))) >> 28);
+          for (int e = 0; e < 8; ++e) bw[e] = (_Float16)(float)(((int)(raw[k].x << (28 - 4 * e))) >> 28);
         }
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc, 0, 0, 0);
-      }
-      // acc: lane holds column l16 (channel n) and sequences b0 + 4*quad + v
-      if (group) {
-        const float sc = sb[(int64_t)gi * N + n];
+        const f16x8 av = bA < B ? a[k] : f16x8{};
+        const f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bw, f32x4{}, 0, 0, 0);
+        if (group) {
+          const float sc = sb[(int64_t)(((st0 + k) * 32) / group) * N + n];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) res[v] = fmaf(acc[v], sc, res[v]);
-      } else {
-        res += acc;
+          for (int v = 0; v < 4; ++v) res[v] = fmaf(acc[v], sc, res[v]);
+        } else {
+          res += acc;
+        }
       }
     }
     __syncthreads();
     red[w][lane] = res;
     __syncthreads();
     if (w == 0) {
-      const f32x4 tot = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
+      f32x4 tot = red[0][lane];
+#pragma unroll
+      for (int w2 = 1; w2 < kVprojWaves; ++w2) tot += red[w2][lane];
       const float cs = group ? 1.f : sb[n];
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
@@ -557,7 +641,7 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
   {
     KernelScope ks("absorb_q", s);
-    hipLaunchKernelGGL(absorb_kernel, dim3(kHeadBlk, (w.r + 255) / 256), dim3(256), 0, s, a.q,
+    hipLaunchKernelGGL(absorb_kernel, dim3(kHeadBlk, w.r / kAbsorbJ), dim3(64), 0, s, a.q,
                        (const uint8_t*)w.b_t, w.s_b, c.batch, w.r, w.n_q_heads, w.n_kv_heads,
                        w.head_dim, N, w.w_bits, w.w_group, a.sm_scale * kLog2e, qt);
   }
@@ -567,15 +651,15 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
                                 : dispatch_latent<QSVD_CACHE_I8>(p, c, qt, opart, ml, s);
   if (e != hipSuccess) return e;
   {
-    KernelScope ks("combine", s);
-    hipLaunchKernelGGL(combine_kernel<false>, dim3((w.r + 63) / 64, c.batch), dim3(256), 0, s, opart, ml,
-                       c.seq_len, p.chunk, p.n0, p.n_chunks, w.r, w.n_q_heads, olat);
+    KernelScope ks("merge_latent", s);
+    hipLaunchKernelGGL(merge_latent_kernel, dim3((w.r + kMergeCols - 1) / kMergeCols, kHeadBlk, c.batch), dim3(64),
+                       0, s, opart, ml, c.seq_len, p.chunk, p.n0, p.n_chunks, w.r, olat);
   }
   {
     KernelScope ks("vproj", s);
-    hipLaunchKernelGGL(vproj_kernel, dim3(w.n_q_heads, w.head_dim / 16), dim3(256), 0, s, olat,
-                       (const uint8_t*)w.b_t, w.s_b, c.batch, w.r, w.n_q_heads, w.n_kv_heads,
-                       w.head_dim, N, w.w_bits, w.w_group, a.out);
+    hipLaunchKernelGGL(vproj_kernel, dim3(w.n_q_heads, w.head_dim / 16), dim3(64 * kVprojWaves), 0, s, olat,
+                       (const uint8_t*)w.b_t, w.s_b, c.batch, w.r, w.n_q_heads, w.n_kv_heads, w.head_dim, N,
+                       w.w_bits, w.w_group, a.out);
   }
   return hipGetLastError();
 }
