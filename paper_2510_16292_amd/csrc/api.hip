@@ -152,29 +152,11 @@ static void prefill_ranges(const qsvd_layer& w, uint32_t mask, bool full, int32_
   if (*lo > *hi) *lo = *hi = 0;
 }
 
-// Workspace of one projection call: the down-projection over r columns and the
-// up-projection over the column range [lo, hi) that the call computes.
-static size_t prefill_need(const qsvd_layer& w, int64_t M, int32_t lo, int32_t hi) {
-  const size_t a = gemm_i8_workspace(M, w.r, w.d);
-  const size_t b = hi > lo ? gemm_i8_workspace(M, hi - lo, w.r) : 0;
-  return a > b ? a : b;
-}
-
 size_t qsvd_prefill_workspace_size(const qsvd_layer* w, int64_t M, uint32_t out_mask) {
-  if (!w || M < 0 || w->r <= 0 || w->d <= 0) return 0;
+  (void)w;
+  (void)M;
   (void)out_mask;
-  // The split of the contraction depends on the width computed, so take the
-  // largest need over every output selection (and the full width used when the
-  // integer accumulators are dumped): one size serves every call.
-  size_t need = 0;
-  for (uint32_t mask = 0; mask <= 7; ++mask)
-    for (int full = 0; full < 2; ++full) {
-      int32_t lo, hi;
-      prefill_ranges(*w, mask, full != 0, &lo, &hi);
-      const size_t n = prefill_need(*w, M, lo, hi);
-      if (n > need) need = n;
-    }
-  return need;
+  return 0;   // no kernel of the projection needs device scratch
 }
 
 qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const float* sx, int64_t M,
@@ -190,18 +172,25 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
   if (!xq || !sx || !c_h || !cq || !sc) return fail(QSVD_ERR_INVALID_ARG, "NULL input/latent pointer");
   if (((out_mask & QSVD_OUT_Q) && !q) || ((out_mask & QSVD_OUT_K) && !k) || ((out_mask & QSVD_OUT_V) && !v))
     return fail(QSVD_ERR_INVALID_ARG, "requested output pointer is NULL");
-  if (w->w_bits != 8 || w->w_group != 0 || act_bits != 8)
-    return fail(QSVD_ERR_UNSUPPORTED, "prefill implements W8A8 per-channel weights");
+  const bool skinny = M <= 32 && skinny_supported(M, w->d, w->w_group, false) &&
+                      skinny_supported(M, w->r, w->w_group, true);
+  if (act_bits != 8) return fail(QSVD_ERR_UNSUPPORTED, "projection implements 8-bit activations");
+  if (!skinny && (w->w_bits != 8 || w->w_group != 0))
+    return fail(QSVD_ERR_UNSUPPORTED,
+                "int4 or per-group weights are implemented for at most 32 tokens, groups a multiple of 64");
+  if (w->w_group && (dbg_acc_xa || dbg_acc_cb))
+    return fail(QSVD_ERR_UNSUPPORTED, "integer accumulator dumps need per-channel weights");
   if (!aligned(xq, 16) || !aligned(cq, 16) || !aligned(c_h, 16) || !aligned(w->a_t, 16) || !aligned(w->b_t, 16))
     return fail(QSVD_ERR_UNSUPPORTED, "operands must be 16-byte aligned");
+  (void)ws;
+  (void)ws_bytes;
   int32_t lo, hi;
   prefill_ranges(*w, out_mask, dbg_acc_cb != nullptr, &lo, &hi);
-  const size_t need = prefill_need(*w, M, lo, hi);
-  if (need > 0 && (!ws || ws_bytes < need))
-    return fail(QSVD_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-
+  const int32_t nq = w->n_q_heads * w->head_dim, nkv = w->n_kv_heads * w->head_dim;
+  const int32_t N = nq + 2 * nkv;
   hipStream_t s = (hipStream_t)stream;
-  // X W^d -> C (fp16)
+
+  // X W^d -> C (fp16); on the tiled path Q(C) follows in the same call
   GemmArgs g1{};
   g1.a = (const int8_t*)xq;
   g1.b = (const int8_t*)w->a_t;
@@ -213,17 +202,23 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
   g1.seg[0] = OutSeg{(_Float16*)c_h, w->r, 0, w->r};
   g1.n_seg = 1;
   g1.dbg = dbg_acc_xa;
-  g1.cq = cq;           // Q(C) is produced with C
-  g1.sc = sc;
   g1.abits = act_bits;
-  st = hip_status(launch_gemm_i8(g1, ws, ws_bytes, s), "down-projection");
+  if (!skinny) {
+    g1.cq = cq;
+    g1.sc = sc;
+  }
+  st = hip_status(skinny ? launch_skinny(g1, false, w->w_bits, w->w_group, w->r, s) : launch_gemm_i8(g1, s),
+                  "down-projection");
   if (st != QSVD_OK) return st;
-  if (!out_mask && !dbg_acc_cb) return QSVD_OK;
-  // Q(C) W^u -> Q | K | V (fp16)
-  const int32_t nq = w->n_q_heads * w->head_dim, nkv = w->n_kv_heads * w->head_dim;
+  if (hi <= lo) {
+    if (!skinny) return QSVD_OK;
+    return hip_status(launch_quantize_rows(c_h, M, w->r, w->r, act_bits, 1.f, cq, sc, s), "latent quantization");
+  }
+
+  // Q(C) W^u -> Q | K | V (fp16) over the columns [lo, hi)
   GemmArgs g2{};
-  g2.a = (const int8_t*)cq;
-  g2.b = (const int8_t*)w->b_t + (int64_t)lo * w->r;
+  g2.a = skinny ? (const int8_t*)c_h : (const int8_t*)cq;
+  g2.b = (const int8_t*)w->b_t + (int64_t)lo * (w->w_bits == 8 ? w->r : w->r / 2);
   g2.row_scale = sc;
   g2.col_scale = w->s_b + lo;
   g2.M = M;
@@ -234,7 +229,11 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
   g2.seg[2] = OutSeg{(out_mask & QSVD_OUT_V) ? (_Float16*)v : nullptr, nkv, nq + nkv - lo, nkv};
   g2.n_seg = 3;
   g2.dbg = dbg_acc_cb;
-  return hip_status(launch_gemm_i8(g2, ws, ws_bytes, s), "up-projection");
+  g2.abits = act_bits;
+  g2.cq = skinny ? cq : nullptr;     // the skinny up-projection quantizes C itself and stores Q(C)
+  g2.sc = skinny ? sc : nullptr;
+  return hip_status(skinny ? launch_skinny(g2, true, w->w_bits, w->w_group, N, s) : launch_gemm_i8(g2, s),
+                    "up-projection");
 }
 
 qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void* cq, const float* sc,

@@ -130,136 +130,6 @@ gemm_i8_tiled_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
     }
 }
 
-// ---------------------------------------------------------------------------
-// Skinny kernel for M <= 32 (decode): the weight is streamed once by many
-// workgroups, each owning 128 columns and one slice of the contraction, and
-// writing its int32 partial tile to part[slice][m][n].  The epilogue adds the
-// slices in a fixed order (integer sums are exact in any order anyway).
-// ---------------------------------------------------------------------------
-constexpr int SBN = 128;
-
-__global__ void __launch_bounds__(256)
-gemm_i8_splitk_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B, int64_t M,
-                      int32_t N, int32_t K, int32_t kchunk, int32_t* __restrict__ part) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int32_t ncol = blockIdx.x * SBN + w * 32 + (lane & 31);
-  const int64_t mrow = lane & 31;
-  const int32_t kbeg = blockIdx.y * kchunk;
-  const int half = lane >> 5;
-  const bool arow = mrow < M, brow = ncol < N;
-  const int8_t* pa = A + mrow * K + kbeg + 32 * half;
-  const int8_t* pb = B + (int64_t)ncol * K + kbeg + 32 * half;
-  i32x16 acc = i32x16{};
-  // 64 contraction bytes per step: lane half h supplies bytes [32h, 32h + 32).
-#pragma unroll 4
-  for (int32_t k = 0; k < kchunk; k += 64) {
-    i32x4 a0 = arow ? *reinterpret_cast<const i32x4*>(pa + k) : i32x4{0, 0, 0, 0};
-    i32x4 a1 = arow ? *reinterpret_cast<const i32x4*>(pa + k + 16) : i32x4{0, 0, 0, 0};
-    i32x4 b0 = brow ? *reinterpret_cast<const i32x4*>(pb + k) : i32x4{0, 0, 0, 0};
-    i32x4 b1 = brow ? *reinterpret_cast<const i32x4*>(pb + k + 16) : i32x4{0, 0, 0, 0};
-    acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(a0, b0, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(a1, b1, acc, 0, 0, 0);
-  }
-  if (!brow) return;
-  int32_t* pp = part + (int64_t)blockIdx.y * M * N;
-#pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int64_t m = 8 * (v >> 2) + 4 * half + (v & 3);
-    if (m < M) pp[m * N + ncol] = acc[v];
-  }
-}
-
-// Sum the slices of 4 consecutive columns, dequantize, store fp16.
-__global__ void __launch_bounds__(256)
-splitk_epilogue_kernel(const int32_t* __restrict__ part, int32_t split, const float* __restrict__ rs,
-                       const float* __restrict__ cs, int64_t M, int32_t N, DevSegs sg,
-                       int32_t* __restrict__ dbg) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int32_t n4 = N / 4;
-  if (i >= M * n4) return;
-  const int64_t m = i / n4;
-  const int32_t n = 4 * (int32_t)(i - m * n4);
-  i32x4 acc = i32x4{0, 0, 0, 0};
-#pragma unroll 8
-  for (int sl = 0; sl < split; ++sl) acc += *reinterpret_cast<const i32x4*>(part + ((int64_t)sl * M + m) * N + n);
-  if (dbg) *reinterpret_cast<i32x4*>(dbg + m * N + n) = acc;
-  const float r_s = rs[m];
-  for (int e = 0; e < 4; ++e) store_out(sg, m, n + e, dequant(acc[e], r_s, cs[n + e]));
-}
-
-// Down-projection epilogue for M <= 32 fused with the latent quantization:
-// one workgroup per token row.  Each thread owns 8 consecutive latent
-// columns per pass (two passes cover r <= 4096): sum the slices, dequantize
-// to fp16 C, keep it in registers, reduce max |C| over the row, then quantize
-// the row exactly as the stand-alone quantizer does (clip 1).
-template <int ABITS>
-__global__ void __launch_bounds__(256)
-splitk_latent_epilogue_kernel(const int32_t* __restrict__ part, int32_t split, const float* __restrict__ sx,
-                              const float* __restrict__ sa, int64_t M, int32_t r, _Float16* __restrict__ c_h,
-                              uint8_t* __restrict__ cq, float* __restrict__ sc, int32_t* __restrict__ dbg) {
-  __shared__ float red[4];
-  const int64_t m = blockIdx.x;
-  const int tid = threadIdx.x;
-  const float rs = sx[m];
-  f16x8 hv[2];
-  float amax = 0.f;
-#pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    const int32_t n = 8 * (tid + 256 * pass);
-    hv[pass] = f16x8{};
-    if (n < r) {
-      i32x4 a0 = i32x4{0, 0, 0, 0}, a1 = i32x4{0, 0, 0, 0};
-#pragma unroll 8
-      for (int sl = 0; sl < split; ++sl) {
-        const int32_t* src = part + ((int64_t)sl * M + m) * r + n;
-        a0 += *reinterpret_cast<const i32x4*>(src);
-        a1 += *reinterpret_cast<const i32x4*>(src + 4);
-      }
-      if (dbg) {
-        *reinterpret_cast<i32x4*>(dbg + m * r + n) = a0;
-        *reinterpret_cast<i32x4*>(dbg + m * r + n + 4) = a1;
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const _Float16 hval = to_f16(dequant(e < 4 ? a0[e] : a1[e - 4], rs, sa[n + e]));
-        hv[pass][e] = hval;
-        amax = fmaxf(amax, fabsf((float)hval));
-      }
-      *reinterpret_cast<f16x8*>(c_h + m * r + n) = hv[pass];
-    }
-  }
-  amax = wave_max(amax);
-  if ((tid & 63) == 0) red[tid >> 6] = amax;
-  __syncthreads();
-  amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  const float qm = (float)((1 << (ABITS - 1)) - 1);
-  const float a = mul_rn(1.f, amax);
-  float inv = 0.f, s = 1.f;
-  if (a != 0.f) {
-    inv = div_rn(qm, a);
-    s = div_rn(a, qm);
-  }
-  if (tid == 0) sc[m] = s;
-#pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    const int32_t n = 8 * (tid + 256 * pass);
-    if (n >= r) continue;
-    int q[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) q[e] = (a != 0.f) ? quant_code(mul_rn((float)hv[pass][e], inv), qm) : 0;
-    if (ABITS == 8) {
-      uint32_t lo = (q[0] & 0xff) | ((q[1] & 0xff) << 8) | ((q[2] & 0xff) << 16) | ((uint32_t)(q[3] & 0xff) << 24);
-      uint32_t hi = (q[4] & 0xff) | ((q[5] & 0xff) << 8) | ((q[6] & 0xff) << 16) | ((uint32_t)(q[7] & 0xff) << 24);
-      *reinterpret_cast<uint2*>(cq + m * r + n) = make_uint2(lo, hi);
-    } else {
-      uint32_t p = 0;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) p |= (uint32_t)(q[e] & 0xf) << (4 * e);
-      *reinterpret_cast<uint32_t*>(cq + m * (r / 2) + n / 2) = p;
-    }
-  }
-}
-
 static DevSegs to_dev(const GemmArgs& g) {
   DevSegs d{};
   d.n_seg = g.n_seg;
@@ -272,67 +142,18 @@ static DevSegs to_dev(const GemmArgs& g) {
   return d;
 }
 
-static bool use_splitk(int64_t M) { return M <= 32; }
-
-// Number of contraction slices: about 256 workgroups stream the weight, at
-// most 16 slices for the epilogue to add.
-static int splitk_slices(int32_t N, int32_t K) {
-  const int nblk = (N + SBN - 1) / SBN;
-  const int steps = K / 64;
-  int split = 256 / nblk;
-  if (split < 1) split = 1;
-  if (split > 16) split = 16;
-  if (split > steps) split = steps;
-  while (steps % split) --split;
-  return split;
-}
-
-size_t gemm_i8_workspace(int64_t M, int32_t N, int32_t K) {
-  return use_splitk(M) ? (size_t)splitk_slices(N, K) * M * N * sizeof(int32_t) : 0;
-}
-
-hipError_t launch_gemm_i8(const GemmArgs& g, void* ws, size_t ws_bytes, hipStream_t s) {
+hipError_t launch_gemm_i8(const GemmArgs& g, hipStream_t s) {
   if (g.M == 0 || g.N == 0) return hipSuccess;
-  const size_t need = gemm_i8_workspace(g.M, g.N, g.K);
-  if (need > 0 && (!ws || ws_bytes < need)) return hipErrorInvalidValue;
   const DevSegs sg = to_dev(g);
-  const bool latent = g.cq != nullptr;
-  if (!use_splitk(g.M)) {
-    dim3 grid((g.N + TBN - 1) / TBN, (unsigned)((g.M + TBM - 1) / TBM));
-    {
-      KernelScope ks("gemm_i8_tiled", s);
-      hipLaunchKernelGGL(gemm_i8_tiled_kernel, grid, dim3(256), 0, s, g.a, g.b, g.row_scale, g.col_scale, g.M,
-                         g.N, g.K, sg, g.dbg);
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !latent) return e;
-    return launch_quantize_rows(g.seg[0].ptr, g.M, g.N, g.seg[0].ld, g.abits, 1.f, g.cq, g.sc, s);
-  }
-  int32_t* part = (int32_t*)ws;
-  const int split = splitk_slices(g.N, g.K);
-  const int32_t kchunk = (g.K / 64 / split) * 64;
+  dim3 grid((g.N + TBN - 1) / TBN, (unsigned)((g.M + TBM - 1) / TBM));
   {
-    KernelScope ks("gemm_i8_splitk", s);
-    hipLaunchKernelGGL(gemm_i8_splitk_kernel, dim3((g.N + SBN - 1) / SBN, split), dim3(256), 0, s, g.a, g.b, g.M,
-                       g.N, g.K, kchunk, part);
+    KernelScope ks("gemm_i8_tiled", s);
+    hipLaunchKernelGGL(gemm_i8_tiled_kernel, grid, dim3(256), 0, s, g.a, g.b, g.row_scale, g.col_scale, g.M, g.N,
+                       g.K, sg, g.dbg);
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (latent) {
-    KernelScope ks("splitk_latent_epilogue", s);
-    if (g.abits == 8)
-      hipLaunchKernelGGL(splitk_latent_epilogue_kernel<8>, dim3((unsigned)g.M), dim3(256), 0, s, part, split,
-                         g.row_scale, g.col_scale, g.M, g.N, g.seg[0].ptr, (uint8_t*)g.cq, g.sc, g.dbg);
-    else
-      hipLaunchKernelGGL(splitk_latent_epilogue_kernel<4>, dim3((unsigned)g.M), dim3(256), 0, s, part, split,
-                         g.row_scale, g.col_scale, g.M, g.N, g.seg[0].ptr, (uint8_t*)g.cq, g.sc, g.dbg);
-  } else {
-    const int64_t total = g.M * (g.N / 4);
-    KernelScope ks("splitk_epilogue", s);
-    hipLaunchKernelGGL(splitk_epilogue_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, part, split,
-                       g.row_scale, g.col_scale, g.M, g.N, sg, g.dbg);
-  }
-  return hipGetLastError();
+  if (e != hipSuccess || !g.cq) return e;
+  return launch_quantize_rows(g.seg[0].ptr, g.M, g.N, g.seg[0].ld, g.abits, 1.f, g.cq, g.sc, s);
 }
 
 }  // namespace qsvd

@@ -44,10 +44,18 @@ struct GemmArgs {
   float* sc;
   int32_t abits;
 };
-// Refuses (hipErrorInvalidValue, nothing launched) a workspace smaller than
-// gemm_i8_workspace(g.M, g.N, g.K).
-hipError_t launch_gemm_i8(const GemmArgs& g, void* ws, size_t ws_bytes, hipStream_t s);
-size_t gemm_i8_workspace(int64_t M, int32_t N, int32_t K);
+// Tiled int8 GEMM for M > 32 (prefill); with g.cq set, the fp16 result is also
+// quantized per row into g.cq / g.sc.
+hipError_t launch_gemm_i8(const GemmArgs& g, hipStream_t s);
+
+// Decode-size products (M <= 32): A is int8 codes, or (a_is_f16_latent) the
+// fp16 latent quantized per row inside the kernel, which then also writes
+// g.cq / g.sc.  Weights int8 or int4 (grouped, scale row stride sstride).
+// Whether the decode-size kernel takes M rows over a contraction of K (A from
+// int8 codes, or f16q: from the fp16 latent, quantized on the fly).
+bool skinny_supported(int64_t M, int32_t K, int32_t group, bool f16q);
+hipError_t launch_skinny(const GemmArgs& g, bool a_is_f16_latent, int32_t wbits, int32_t group, int32_t sstride,
+                         hipStream_t s);
 
 hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void* cq,
                                const float* sc, int32_t n_new, hipStream_t s);

@@ -1,0 +1,313 @@
+// Decode-size projections (M <= 32 token rows) on v_mfma_i32_16x16x64_i8.
+//
+// The weight is the large operand here (M is the decode batch), so each
+// workgroup owns 16 output columns over the whole contraction: up to 16 waves
+// split the contraction, each streaming its slice of the 16 weight rows once
+// with all of its loads in flight together, and leave exact int32 partial sums
+// in LDS.  No partial sums go through HBM and no second kernel is needed.
+//
+// 16x16x64 operand layout: lane l supplies row (l % 16) of A and column
+// (l % 16) of B, 16 contraction bytes each (which bytes only has to agree
+// between A and B: integer sums are exact in any order).  Output: lane l holds
+// column l % 16 and rows 4 * (l / 16) + v, v = 0..3.
+//
+// Per-channel weights: the waves' int32 sums are added (exact) and dequantized
+// as (f32(acc) * s_row) * s_col.  Per-group weights (int4, groups of G along the
+// contraction): every group's int32 sum is kept in LDS and one thread per
+// output adds f32(acc_g) * s[g][n] over the groups in order, then * s_row --
+// the same sequence of fp32 roundings as the stand-alone definition.
+//
+// Up-projection (A = the fp16 latent C): every workgroup first takes each row's
+// max |C|, quantizes the rows into LDS (Q(C), Section 4's per-token symmetric
+// rule) and uses them as the A operand; workgroup (m mod grid) also stores row
+// m's codes and scale.  The first batch of weight loads is issued before this
+// so that its HBM latency overlaps the row pass.
+#include <algorithm>
+
+#include "common.h"
+#include "launch.h"
+
+namespace qsvd {
+
+constexpr int kSkCols = 16;        // output columns per workgroup
+constexpr int kSkMaxWaves = 16;
+constexpr int kSkBatch = 4;        // 64-byte contraction steps loaded per batch
+constexpr int kSkMaxRowChunks = 8; // fp16 row pass: K <= 8 * 64 * 8 = 4096
+constexpr size_t kSkLdsLimit = 160 * 1024 - 1024;
+
+struct SkinnyOut {
+  _Float16* ptr[3];
+  int64_t ld[3];
+  int32_t n0[3];
+  int32_t n[3];
+  int32_t n_seg;
+};
+
+__device__ __forceinline__ void sk_store(const SkinnyOut& so, int64_t m, int32_t n, float y) {
+#pragma unroll
+  for (int s = 0; s < 3; ++s) {
+    if (s < so.n_seg && n >= so.n0[s] && n < so.n0[s] + so.n[s]) {
+      if (so.ptr[s]) so.ptr[s][m * so.ld[s] + (n - so.n0[s])] = to_f16(y);
+      return;
+    }
+  }
+}
+
+// 16 int4 codes (8 bytes, element 2i in the low nibble of byte i) -> 16 int8.
+__device__ __forceinline__ i32x4 unpack16_i4(uint2 p) {
+  i32x4 o;
+  const uint32_t w[2] = {p.x, p.y};
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      lo |= (uint32_t)((((int)(w[h] << (28 - 4 * e))) >> 28) & 0xff) << (8 * e);
+      hi |= (uint32_t)((((int)(w[h] << (12 - 4 * e))) >> 28) & 0xff) << (8 * e);
+    }
+    o[2 * h] = (int32_t)lo;
+    o[2 * h + 1] = (int32_t)hi;
+  }
+  return o;
+}
+
+// A operand source: int8 codes (down-projection: the quantized activations), or
+// the fp16 latent quantized by the workgroup itself (up-projection).
+enum { SK_A_I8 = 0, SK_A_F16Q = 1 };
+
+// Contraction steps [s0, s1) of wave w: contiguous ranges, whole groups when the
+// weights carry per-group scales.
+__device__ __forceinline__ void sk_span(int w, int nw, int32_t K, int32_t group, int& s0, int& s1) {
+  if (group) {
+    const int ng = K / group, gs = group / 64;
+    s0 = (w * ng / nw) * gs;
+    s1 = ((w + 1) * ng / nw) * gs;
+  } else {
+    const int steps = K / 64;
+    s0 = w * steps / nw;
+    s1 = (w + 1) * steps / nw;
+  }
+}
+
+template <int ASRC, int WBITS>
+__global__ void __launch_bounds__(64 * kSkMaxWaves)
+skinny_gemm_kernel(const void* __restrict__ a_src, const float* __restrict__ row_scale_in,
+                   const uint8_t* __restrict__ bt, const float* __restrict__ col_scale, int32_t sstride,
+                   int32_t M, int32_t N, int32_t K, int32_t group, int32_t nw, int32_t abits, int32_t qa_off,
+                   SkinnyOut so, int32_t* __restrict__ dbg, uint8_t* __restrict__ cq_out, float* __restrict__ sc_out) {
+  // [0, qa_off): int32 tiles, [slot][row block][lane] (slot = wave for
+  // per-channel weights, group for per-group ones); [qa_off, ...): Q(C) rows.
+  extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];
+  i32x4* red = reinterpret_cast<i32x4*>(sk_lds);
+  int8_t* qa = reinterpret_cast<int8_t*>(sk_lds + qa_off);
+  __shared__ float rsc[32];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l16 = lane & 15, quad = lane >> 4;
+  const int32_t n = blockIdx.x * kSkCols + l16;           // this lane's weight row (output column)
+  const bool ncol = n < N;
+  const int rbl = (M + 15) / 16;
+  const int qa_ld = K + 16;
+  const float qm = (float)((1 << (abits - 1)) - 1);
+
+  int s0, s1;
+  sk_span(w, nw, K, group, s0, s1);
+
+  i32x4 bw[kSkBatch];
+  auto load_b = [&](int st0) {
+#pragma unroll
+    for (int s = 0; s < kSkBatch; ++s) {
+      const int st = st0 + s;
+      const int32_t k = 64 * st + 16 * quad;
+      if (st < s1 && ncol) {
+        if (WBITS == 8)
+          bw[s] = *reinterpret_cast<const i32x4*>(bt + (int64_t)n * K + k);
+        else
+          bw[s] = unpack16_i4(*reinterpret_cast<const uint2*>(bt + ((int64_t)n * K + k) / 2));
+      } else {
+        bw[s] = i32x4{0, 0, 0, 0};
+      }
+    }
+  };
+  load_b(s0);
+
+  if (ASRC == SK_A_F16Q) {
+    // row pass: wave w takes rows w, w + nw, ...; the row sits in registers
+    // (8-element chunks lane, lane + 64, ...), its max goes round the wave.
+    const _Float16* ch = reinterpret_cast<const _Float16*>(a_src);
+    const int nch = K / 8;
+    for (int m = w; m < M; m += nw) {
+      f16x8 v[kSkMaxRowChunks];
+#pragma unroll
+      for (int i = 0; i < kSkMaxRowChunks; ++i) {
+        const int c = lane + 64 * i;
+        v[i] = c < nch ? *reinterpret_cast<const f16x8*>(ch + (int64_t)m * K + 8 * c) : f16x8{};
+      }
+      float mx = 0.f;
+#pragma unroll
+      for (int i = 0; i < kSkMaxRowChunks; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf((float)v[i][e]));
+      const float a = mul_rn(1.f, wave_max(mx));
+      const float inv = a != 0.f ? div_rn(qm, a) : 0.f;
+      const float sc = a != 0.f ? div_rn(a, qm) : 1.f;
+      const bool own = (m % (int)gridDim.x) == (int)blockIdx.x;
+      if (lane == 0) {
+        rsc[m] = sc;
+        if (own) sc_out[m] = sc;
+      }
+#pragma unroll
+      for (int i = 0; i < kSkMaxRowChunks; ++i) {
+        const int c = lane + 64 * i;
+        if (c >= nch) continue;
+        int q[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) q[e] = inv == 0.f ? 0 : quant_code(mul_rn((float)v[i][e], inv), qm);
+        const uint32_t lo = (q[0] & 0xff) | ((q[1] & 0xff) << 8) | ((q[2] & 0xff) << 16) | ((uint32_t)(q[3] & 0xff) << 24);
+        const uint32_t hi = (q[4] & 0xff) | ((q[5] & 0xff) << 8) | ((q[6] & 0xff) << 16) | ((uint32_t)(q[7] & 0xff) << 24);
+        *reinterpret_cast<uint2*>(qa + m * qa_ld + 8 * c) = make_uint2(lo, hi);
+        if (own) {
+          if (abits == 8) {
+            *reinterpret_cast<uint2*>(cq_out + (int64_t)m * K + 8 * c) = make_uint2(lo, hi);
+          } else {
+            uint32_t p = 0;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) p |= (uint32_t)(q[e] & 0xf) << (4 * e);
+            *reinterpret_cast<uint32_t*>(cq_out + (int64_t)m * (K / 2) + 4 * c) = p;
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // --- contraction over this wave's steps ------------------------------------
+  const int gsteps = group ? group / 64 : 0;
+  i32x4 acc[2] = {i32x4{0, 0, 0, 0}, i32x4{0, 0, 0, 0}};
+  int step_in_group = 0;
+  for (int st0 = s0; st0 < s1; st0 += kSkBatch) {
+    if (st0 != s0) load_b(st0);
+    i32x4 aw[kSkBatch][2];
+#pragma unroll
+    for (int s = 0; s < kSkBatch; ++s) {
+      const int32_t k = 64 * (st0 + s) + 16 * quad;
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        const int m = 16 * rb + l16;
+        if (st0 + s < s1 && rb < rbl && m < M) {
+          if (ASRC == SK_A_I8)
+            aw[s][rb] = *reinterpret_cast<const i32x4*>(reinterpret_cast<const int8_t*>(a_src) + (int64_t)m * K + k);
+          else
+            aw[s][rb] = *reinterpret_cast<const i32x4*>(qa + m * qa_ld + k);
+        } else {
+          aw[s][rb] = i32x4{0, 0, 0, 0};
+        }
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < kSkBatch; ++s) {
+      if (st0 + s >= s1) break;
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+        if (rb < rbl) acc[rb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aw[s][rb], bw[s], acc[rb], 0, 0, 0);
+      if (gsteps && ++step_in_group == gsteps) {
+        const int g = (st0 + s) / gsteps;
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+          if (rb < rbl) red[(g * rbl + rb) * 64 + lane] = acc[rb];
+          acc[rb] = i32x4{0, 0, 0, 0};
+        }
+        step_in_group = 0;
+      }
+    }
+  }
+  if (!gsteps)
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+      if (rb < rbl) red[(w * rbl + rb) * 64 + lane] = acc[rb];
+  __syncthreads();
+
+  // --- epilogue: one thread per output (row m, column n) ------------------------
+  const int ng = group ? K / group : 0;
+  for (int t = tid; t < M * kSkCols; t += 64 * nw) {
+    const int m = t / kSkCols, nl = t % kSkCols;
+    const int32_t nn = blockIdx.x * kSkCols + nl;
+    if (nn >= N) continue;
+    const int rb = m >> 4, mm = m & 15, src = 16 * (mm >> 2) + nl, v = mm & 3;
+    const float rs = ASRC == SK_A_I8 ? row_scale_in[m] : rsc[m];
+    float y;
+    if (!group) {
+      int32_t tot = 0;
+      for (int ww = 0; ww < nw; ++ww) tot += red[(ww * rbl + rb) * 64 + src][v];
+      if (dbg) dbg[(int64_t)m * N + nn] = tot;
+      y = mul_rn(mul_rn((float)tot, rs), col_scale[nn]);
+    } else {
+      float S = 0.f;
+      for (int g = 0; g < ng; ++g)
+        S = add_rn(S, mul_rn((float)red[(g * rbl + rb) * 64 + src][v], col_scale[(int64_t)g * sstride + nn]));
+      y = mul_rn(S, rs);
+    }
+    sk_store(so, m, nn, y);
+  }
+}
+
+struct SkinnyPlan {
+  int nw;            // waves per workgroup
+  int32_t qa_off;    // LDS bytes of the int32 tiles
+  size_t lds;        // dynamic LDS bytes
+};
+
+static SkinnyPlan skinny_plan(int64_t M, int32_t K, int32_t group, bool f16q) {
+  SkinnyPlan p{};
+  const int steps = K / 64, ng = group ? K / group : 0;
+  p.nw = std::min(kSkMaxWaves, group ? ng : steps);
+  const int rbl = (int)((M + 15) / 16);
+  const size_t tiles = (size_t)(group ? ng : p.nw) * rbl * 64 * sizeof(i32x4);
+  p.qa_off = (int32_t)tiles;
+  p.lds = tiles + (f16q ? (size_t)M * (K + 16) : 0);
+  return p;
+}
+
+bool skinny_supported(int64_t M, int32_t K, int32_t group, bool f16q) {
+  if (M < 1 || M > 32 || K < 64 || K % 64) return false;
+  if (group && (group % 64 || K % group)) return false;
+  if (f16q && K > kSkMaxRowChunks * 64 * 8) return false;
+  return skinny_plan(M, K, group, f16q).lds <= kSkLdsLimit;
+}
+
+hipError_t launch_skinny(const GemmArgs& g, bool a_is_f16_latent, int32_t wbits, int32_t group, int32_t sstride,
+                         hipStream_t s) {
+  if (g.M == 0 || g.N == 0) return hipSuccess;
+  if (!skinny_supported(g.M, g.K, group, a_is_f16_latent)) return hipErrorInvalidValue;
+  SkinnyOut so{};
+  so.n_seg = g.n_seg;
+  for (int i = 0; i < 3; ++i) {
+    so.ptr[i] = i < g.n_seg ? g.seg[i].ptr : nullptr;
+    so.ld[i] = i < g.n_seg ? g.seg[i].ld : 0;
+    so.n0[i] = i < g.n_seg ? g.seg[i].n0 : 0;
+    so.n[i] = i < g.n_seg ? g.seg[i].n : 0;
+  }
+  const SkinnyPlan p = skinny_plan(g.M, g.K, group, a_is_f16_latent);
+  dim3 grid((g.N + kSkCols - 1) / kSkCols), block(64 * p.nw);
+  const int32_t M = (int32_t)g.M;
+  const uint8_t* bt = (const uint8_t*)g.b;
+  // more than 64 KB of dynamic LDS has to be allowed per kernel before the launch
+  auto allow = [&](const void* fn) -> hipError_t {
+    return p.lds > 65536 ? hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds)
+                         : hipSuccess;
+  };
+  KernelScope ks(a_is_f16_latent ? "skinny_up" : "skinny_down", s);
+  if (!a_is_f16_latent) {
+    auto k = wbits == 8 ? skinny_gemm_kernel<SK_A_I8, 8> : skinny_gemm_kernel<SK_A_I8, 4>;
+    if (hipError_t e = allow((const void*)k); e != hipSuccess) return e;
+    hipLaunchKernelGGL(k, grid, block, p.lds, s, (const void*)g.a, g.row_scale, bt, g.col_scale, sstride, M, g.N,
+                       g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)nullptr, (float*)nullptr);
+  } else {
+    auto k = wbits == 8 ? skinny_gemm_kernel<SK_A_F16Q, 8> : skinny_gemm_kernel<SK_A_F16Q, 4>;
+    if (hipError_t e = allow((const void*)k); e != hipSuccess) return e;
+    hipLaunchKernelGGL(k, grid, block, p.lds, s, (const void*)g.a, (const float*)nullptr, bt, g.col_scale, sstride,
+                       M, g.N, g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)g.cq, g.sc);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace qsvd

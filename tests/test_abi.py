@@ -136,12 +136,12 @@ def test_prefill_validation(lib):
     assert _prefill(layer_struct(), mask=B.QSVD_OUT_K, k=0) == B.QSVD_ERR_INVALID_ARG
     assert _prefill(layer_struct(), c_h=0) == B.QSVD_ERR_INVALID_ARG
     assert _prefill(layer_struct(), M=0) == B.QSVD_OK          # nothing to do, nothing launched
-    # skinny M needs an int32 workspace for the split contraction
-    need = B.qsvd_prefill_workspace_size(layer_struct(), 16, 7)
-    assert need >= 16 * 768 * 4 and need % (16 * 4) == 0
-    assert _prefill(layer_struct(), M=16, ws=FAKE, ws_bytes=need - 1) == B.QSVD_ERR_WORKSPACE
-    assert _prefill(layer_struct(), M=16, ws=0, ws_bytes=need) == B.QSVD_ERR_WORKSPACE
-    assert B.qsvd_prefill_workspace_size(layer_struct(), 4096, 7) == 0
+    assert _prefill(layer_struct(), act_bits=4) == B.QSVD_ERR_UNSUPPORTED
+    assert _prefill(layer_struct(w_bits=4, w_group=64), M=33) == B.QSVD_ERR_UNSUPPORTED   # > 32 tokens: W8 only
+    assert _prefill(layer_struct(w_bits=4, w_group=32)) == B.QSVD_ERR_UNSUPPORTED        # groups of 64 bytes
+    g = layer_struct(w_bits=4, w_group=64)
+    assert B.lib().qsvd_lowrank_qkv_prefill(ctypes.byref(g), FAKE, FAKE, 4, 8, 7, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                            FAKE, 0, 0, 0, 0) == B.QSVD_ERR_UNSUPPORTED   # no dumps with groups
 
 
 def test_cache_append_validation(lib):
@@ -227,38 +227,15 @@ def test_prep_matches_oracle_prep():
     assert np.array_equal(P.b_t, O.pack_int4(np.ascontiguousarray(ol.Bq.T)))
 
 
-def _splitk_need(M, N, K):
-    """Bytes of int32 partials the skinny (M <= 32) product of an M x K by K x N
-    int8 pair writes: one [M][N] slice per contraction split, the split chosen
-    for ~256 workgroups over 128-column blocks, at most 16, dividing K/64."""
-    if M > 32 or N == 0:
-        return 0
-    nblk, steps = -(-N // 128), K // 64
-    split = min(max(1, 256 // nblk), 16, steps)
-    while steps % split:
-        split -= 1
-    return split * M * N * 4
-
-
 @pytest.mark.parametrize("shape", [(256, 128, 4, 4, 64), (4096, 1536, 32, 32, 128), (3584, 1024, 28, 4, 128),
                                    (5120, 2048, 40, 40, 128)], ids=["tiny", "llava7b", "qwen2vl", "13b"])
-def test_prefill_workspace_covers_every_output_selection(lib, shape):
-    """Regression: the size query once covered only the full up-projection width
-    while a Q-only call (decode) splits its narrower product into more slices and
-    needed more partials (LLaVA-7B-shaped layer, M=16: 2.10 MB vs 1.57 MB), so the
-    split kernel wrote past the workspace.  Every selection must fit, and a
-    workspace one byte short of a call's need is refused before any launch."""
+def test_projection_needs_no_workspace(lib, shape):
+    """The projection keeps every partial sum on chip (decode sizes reduce in
+    LDS, prefill tiles accumulate in registers), so its workspace query is 0 for
+    every size and output selection.  (An earlier split-contraction design wrote
+    int32 partials to a workspace and once overflowed it on a Q-only call.)"""
     d, r, hq, hkv, dh = shape
     L = layer_struct(d=d, r=r, n_q_heads=hq, n_kv_heads=hkv, head_dim=dh)
-    nq, nkv = hq * dh, hkv * dh
-    ranges = {B.QSVD_OUT_Q: (0, nq), B.QSVD_OUT_K: (nq, nq + nkv), B.QSVD_OUT_V: (nq + nkv, nq + 2 * nkv),
-              B.QSVD_OUT_K | B.QSVD_OUT_V: (nq, nq + 2 * nkv), 7: (0, nq + 2 * nkv)}
-    for M in (1, 8, 16, 31, 32):
-        size = B.qsvd_prefill_workspace_size(L, M, 7)
-        for mask, (lo, hi) in ranges.items():
-            need = max(_splitk_need(M, r, d), _splitk_need(M, hi - lo, r))
-            assert size >= need, (M, mask, size, need)
-            assert _prefill(L, M=M, mask=mask, ws=FAKE, ws_bytes=need - 1) == B.QSVD_ERR_WORKSPACE
-    # the case that faulted
-    if shape[0] == 4096:
-        assert B.qsvd_prefill_workspace_size(L, 16, B.QSVD_OUT_Q) >= 8 * 16 * 4096 * 4
+    for M in (1, 8, 16, 31, 32, 33, 640, 2560):
+        for mask in range(8):
+            assert B.qsvd_prefill_workspace_size(L, M, mask) == 0

@@ -53,6 +53,28 @@ def gqa():
     return L, ol, dl
 
 
+@pytest.fixture(scope="module", params=[64, 128], ids=["g64", "g128"])
+def tiny_w4(request):
+    """The tiny layer with int4 weights, one scale per output channel and per
+    group of 64 or 128 contraction rows (W4A8)."""
+    wl = configs.get(1)
+    ol, dl = _layers_from_weight(gen.weight_matrix(wl), wl.layer, w_bits=4, w_group=request.param)
+    return wl, ol, dl
+
+
+@pytest.fixture(scope="module")
+def qwen():
+    """Qwen2-VL-7B-shaped grouped-query layer: d=3584, 28 query / 4 key-value
+    heads x 128, r=1024, int4 weights in groups of 128 (W4A8)."""
+    wl = configs.get(4)
+    L = wl.layer
+    U, s, V = gen.weight_factors(wl)
+    A, Bm = O.split_beta(U, s, V.T, wl.beta)
+    ol = O.make_layer(A, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, 4, 128)
+    dl = B.DeviceLayer(prep.prepare_from_svd(U, s, V, L.n_q_heads, L.n_kv_heads, L.head_dim, wl.beta, 4, 128))
+    return wl, ol, dl
+
+
 @pytest.fixture(scope="module")
 def llava():
     wl = configs.get(3)
@@ -120,6 +142,43 @@ def test_prefill_bitexact_tiny(tiny, M):
     H.say(f"prefill tiny M={M}")
     got = H.Prefill(dl, M).run(H.dev(X)).result()
     _check_prefill(ol, got, X)
+
+
+@pytest.mark.parametrize("M", [1, 16, 32])
+def test_projection_bitexact_w4a8(tiny_w4, M):
+    """Decode-size projection with int4 grouped weights: per-group fp32 sums in
+    the definition's order make C, Q(C) and Q/K/V bit-exact."""
+    wl, ol, dl = tiny_w4
+    X = gen.fill_activations(wl, M)
+    H.say(f"projection w4a8 group={dl.w_group} M={M}")
+    got = H.Prefill(dl, M, debug=False).run(H.dev(X)).result()
+    ref = O.prefill(ol, X, 8)
+    for key in ("xq", "cq"):
+        assert np.array_equal(got[key], ref[key]), key
+    for key in ("sx", "sc"):
+        assert np.array_equal(got[key].view(np.uint32), ref[key].view(np.uint32)), key
+    for key in ("C_h", "Q", "K", "V"):
+        assert np.array_equal(got[key].view(np.uint16), ref[key].view(np.uint16)), key
+
+
+def test_projection_bitexact_llava7b_w4a8_g64_m32(llava):
+    """The LLaVA-1.5-7B-shaped layer with int4 weights in groups of 64 and a
+    32-token decode batch: 64 groups x 2 row blocks of int32 tiles (128 KB of
+    LDS) in the down-projection, bit-exact against the oracle."""
+    wl, _, _ = llava
+    L = wl.layer
+    U, s, V = gen.weight_factors(wl)
+    A, Bm = O.split_beta(U, s, V.T, wl.beta)
+    ol = O.make_layer(A, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, 4, 64)
+    dl = B.DeviceLayer(prep.prepare_from_svd(U, s, V, L.n_q_heads, L.n_kv_heads, L.head_dim, wl.beta, 4, 64))
+    X = gen.decode_activations(wl, 0, batch=32)
+    H.say("projection llava7b w4a8 g64 M=32")
+    got = H.Prefill(dl, 32, debug=False).run(H.dev(X)).result()
+    ref = O.prefill(ol, X, 8)
+    assert np.array_equal(got["cq"], ref["cq"])
+    assert np.array_equal(got["sc"].view(np.uint32), ref["sc"].view(np.uint32))
+    for key in ("C_h", "Q", "K", "V"):
+        assert np.array_equal(got[key].view(np.uint16), ref[key].view(np.uint16)), key
 
 
 def test_prefill_masks_leave_other_outputs(tiny):
@@ -282,6 +341,38 @@ def test_decode_llava7b_full_size_sampled(llava):
         oc = O.LatentCache(O.CACHE_F16, 1, cap, wl.layer.r)
         oc.append(0, rows[b, :L0])
         ref = O.decode_step(ol, oc, xt[b:b + 1], 8)
+        ok, info = H.close_enough(out[b:b + 1], ref["out"])
+        H.say(f"  b={b} max-abs, rel-L2, rms = {info}")
+        assert ok, (b, info)
+
+
+def test_decode_qwen2vl_w4a8_int8_cache_full_size(qwen):
+    """The Qwen2-VL-7B-shaped decode workload at full size: 32 sequences x 8192
+    cached tokens in an int8 latent cache with per-token scales, W4A8 projection
+    of the new tokens, grouped-query absorbed attention; two sequences checked
+    against the oracle in full, all outputs finite, run twice bit-identically."""
+    wl, ol, dl = qwen
+    L = wl.layer
+    batch, L0 = wl.decode_batch, wl.decode_ctx
+    cap = L0 + 8
+    codes, scales = gen.latent_codes(wl, batch, cap)
+    dc = B.DeviceCache(B.QSVD_CACHE_I8, batch, cap, L.r, [L0] * batch)
+    dc.data.copy_(H.dev(codes))
+    dc.scale.copy_(H.dev(scales))
+    xt = gen.decode_activations(wl, 0, batch=batch)
+    H.say("decode qwen2vl w4a8 int8 cache full size")
+    p = H.Prefill(dl, batch, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
+    H.append(dc, cq=p.cq, sc=p.sc, n_new=1)
+    out = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
+    out2 = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
+    assert np.array_equal(out.view(np.uint16), out2.view(np.uint16))
+    assert np.all(np.isfinite(out.astype(np.float32)))
+    for b in (0, 29):
+        oc = O.LatentCache(O.CACHE_I8, 1, cap, L.r)
+        oc.append(0, None, codes[b, :L0], scales[b, :L0])
+        ref = O.decode_step(ol, oc, xt[b:b + 1], 8)
+        assert np.array_equal(H.host(p.cq)[b:b + 1], ref["cq"])
+        assert np.array_equal(H.host(p.q)[b:b + 1].view(np.uint16), ref["Q"].view(np.uint16))
         ok, info = H.close_enough(out[b:b + 1], ref["out"])
         H.say(f"  b={b} max-abs, rel-L2, rms = {info}")
         assert ok, (b, info)

@@ -113,13 +113,18 @@ def latent_rows(wl: Workload, batch: int, length: int, layer: int = 0, seed_offs
 
 
 def latent_codes(wl: Workload, batch: int, length: int, layer: int = 0, seed_offset: int = 0):
-    """Synthetic int8 latent cache contents: codes in [-127, 127] (each row
-    reaching +-127) and positive per-token fp32 scales."""
+    """Synthetic int8 latent cache contents with the magnitudes of
+    :func:`latent_rows`: codes in [-127, 127] whose column j spreads in
+    proportion to sigma_j (column 0 at +127, so every row reaches the top code),
+    and positive per-token fp32 scales around sigma_1 / 40, so code * scale has
+    about the spread of the fp16 latent rows."""
     g = rng_for(wl, ROLE_FILL + seed_offset, layer)
     r = wl.layer.r
-    codes = np.clip(np.rint(g.standard_normal((batch, length, r)) * 40.0), -127, 127).astype(np.int8)
+    std = np.sqrt(spectrum(wl)[:r]) if wl.spectrum == "decay" else np.ones(r)
+    z = g.standard_normal((batch, length, r)) * (40.0 * std / std[0])[None, None, :]
+    codes = np.clip(np.rint(z), -127, 127).astype(np.int8)
     codes[:, :, 0] = 127
-    scales = (g.uniform(0.02, 0.2, (batch, length))).astype(np.float32)
+    scales = (g.uniform(0.8, 1.25, (batch, length)) * (std[0] / 40.0)).astype(np.float32)
     return codes, scales
 
 
