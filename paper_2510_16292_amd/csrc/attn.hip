@@ -9,7 +9,7 @@
 //   absorb_kernel       q~[b][h][:] = (sm_scale * log2 e) * q[b][h] W^u_k,g(h)^T     (fp16)
 //   latent_attn_kernel  per (sequence, context chunk): S = q~ C^T, online softmax,
 //                       O = P C over the chunk -> split partials (m, l, O)
-//   combine_kernel      merge the chunk partials of each sequence
+//   merge_latent_kernel merge the chunk partials of each sequence
 //   vproj_kernel        o[b][h] = O[b][h] W^u_v,g(h)                               (fp16)
 //
 // Reconstruct form (for comparison): K^, V^ are rebuilt for every cached token
@@ -316,85 +316,92 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     ml_part[part * 64 + 32 + l32] = l_run;
   }
   // O^T / l as fp16 (a weighted mean of latent rows, so it stays in range),
-  // stored head-major [h][x]: lane holds head l32 and latent rows
-  // slice0 + 32*rb + 8*(v/4) + 4*half + v%4, so the wave transposes its slice
-  // through its own staging rows and then writes 16-byte runs of one head.
+  // stored in accumulator order [x/4][head][4]: lane (head l32, half) holds
+  // latent columns slice0 + 32*rb + 8*vq + 4*half .. +3 in o[rb][4*vq ..],
+  // so each store instruction writes 512 contiguous bytes.
   const float inv_l = l_run > 0.f ? 1.f / l_run : 0.f;
-  constexpr int OST = RW + 8;                  // 32 * OST <= 32 * CST halves
-  __syncthreads();
+  _Float16* op = o_part + part * (int64_t)r * kHeadBlk;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-    for (int v = 0; v < 16; ++v)
-      cst[l32 * OST + 32 * rb + 8 * (v >> 2) + 4 * half + (v & 3)] = (_Float16)(o[rb][v] * inv_l);
-  __syncthreads();
-  _Float16* op = o_part + part * (int64_t)r * kHeadBlk;
-  for (int e = lane; e < 32 * (RW / 8); e += 64) {
-    const int hh = e / (RW / 8), x8 = e - hh * (RW / 8);
-    *reinterpret_cast<f16x8*>(op + (int64_t)hh * r + slice0 + 8 * x8) =
-        *reinterpret_cast<const f16x8*>(cst + hh * OST + 8 * x8);
-  }
+    for (int vq = 0; vq < 4; ++vq) {
+      const int x4 = (slice0 + 32 * rb + 8 * vq + 4 * half) >> 2;
+      const f16x4 v4 = {(_Float16)(o[rb][4 * vq] * inv_l), (_Float16)(o[rb][4 * vq + 1] * inv_l),
+                        (_Float16)(o[rb][4 * vq + 2] * inv_l), (_Float16)(o[rb][4 * vq + 3] * inv_l)};
+      *reinterpret_cast<f16x4*>(op + ((int64_t)x4 * kHeadBlk + l32) * 4) = v4;
+    }
 }
 
 // ---------------------------------------------------------------------------
 // Merge the chunk partials of the latent form.  Chunk c of sequence b holds
-// m_c, l_c per head and the normalized O_c / l_c as fp16, head-major
-// [c][32][r].  One wave per (sequence, head, 512 latent columns): lane l owns
-// 8 columns, issues the loads of every chunk at once, and writes
-// O[b][h][:] = sum_c w_c (O_c / l_c) with w_c = 2^(m_c - m) l_c / sum (fp16).
+// m_c, l_c per head and the normalized O_c / l_c as fp16 in the [x/4][32][4]
+// order above.  With m = max m_c and w_c = 2^(m_c - m) l_c / sum, the result
+// O[b][h][x] = sum_c w_c (O_c / l_c)[h][x] is written head-major [b][32][r].
+// A workgroup takes 2048 consecutive partial elements (16 latent quads x 32
+// heads x 4); its threads first compute all the per-(chunk, head) weights
+// into LDS (8 lanes per head, chunks strided over them), then each thread
+// streams 8 elements (two heads x 4 columns) of every chunk.
 // ---------------------------------------------------------------------------
-constexpr int kMergeCols = 512;
-constexpr int kMergeBatch = 16;
+constexpr int kMergeElems = 2048;
+constexpr int kMergeBatch = 8;
 
-__global__ void __launch_bounds__(64)
+__global__ void __launch_bounds__(256)
 merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict__ ml_part,
                     const int32_t* __restrict__ seq_len, int32_t chunk, int32_t n_chunks, int32_t n_launched,
                     int32_t r, _Float16* __restrict__ o_lat) {
-  const int b = blockIdx.z, h = blockIdx.y, lane = threadIdx.x;
-  const int j = blockIdx.x * kMergeCols + 8 * lane;
+  __shared__ float wgt[kMaxChunks * kHeadBlk];
+  const int b = blockIdx.y, tid = threadIdx.x;
   const int L = seq_len[b];
-  const int nv = L > 0 ? min((L + chunk - 1) / chunk, n_launched) : 0;
+  const int nv = L > 0 ? min(min((L + chunk - 1) / chunk, n_launched), kMaxChunks) : 0;
   const int64_t pb = (int64_t)b * n_chunks;
+  {
+    const int h = tid >> 3, sub = tid & 7;
+    float m = -INFINITY;
+    for (int c = sub; c < nv; c += 8) m = fmaxf(m, ml_part[(pb + c) * 64 + h]);
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    float tot = 0.f;
+    for (int c = sub; c < nv; c += 8) {
+      const float wc = exp2f(ml_part[(pb + c) * 64 + h] - m) * ml_part[(pb + c) * 64 + 32 + h];
+      wgt[c * kHeadBlk + h] = wc;
+      tot += wc;
+    }
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) tot += __shfl_xor(tot, o, 64);
+    const float inv = tot > 0.f ? 1.f / tot : 0.f;
+    for (int c = sub; c < nv; c += 8) wgt[c * kHeadBlk + h] *= inv;
+  }
+  __syncthreads();
+  // element e8 (8 halves): latent quad x4 = e8 / 16, heads 2*(e8 % 16) and +1
+  const int64_t e0 = (int64_t)blockIdx.x * kMergeElems + 8 * tid;
+  if (e0 >= (int64_t)r * kHeadBlk) return;
+  const int x4 = (int)(e0 / (4 * kHeadBlk)), h0 = (int)((e0 / 4) % kHeadBlk);
+  const _Float16* src = o_part + pb * (int64_t)r * kHeadBlk + e0;
   float acc[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) acc[k] = 0.f;
-  const bool jok = j < r;
-  const _Float16* src = o_part + (pb * kHeadBlk + h) * r + (jok ? j : 0);
-  // lane c holds chunk c0 + c's weight 2^(m_c - m) l_c / sum (chunks in batches of 64)
-  float m = -INFINITY;
-  for (int c0 = 0; c0 < nv; c0 += 64)
-    if (c0 + lane < nv) m = fmaxf(m, ml_part[(pb + c0 + lane) * 64 + h]);
-  m = wave_max(m);
-  float tot = 0.f;
-  for (int c0 = 0; c0 < nv; c0 += 64)
-    if (c0 + lane < nv) tot += exp2f(ml_part[(pb + c0 + lane) * 64 + h] - m) * ml_part[(pb + c0 + lane) * 64 + 32 + h];
-  tot = wave_sum(tot);
-  const float inv = tot > 0.f ? 1.f / tot : 0.f;
-  for (int c0 = 0; c0 < nv; c0 += 64) {
-    const float wl = (c0 + lane < nv)
-                         ? exp2f(ml_part[(pb + c0 + lane) * 64 + h] - m) * ml_part[(pb + c0 + lane) * 64 + 32 + h] * inv
-                         : 0.f;
-    const int nb = min(64, nv - c0);
-    for (int k0 = 0; k0 < nb; k0 += kMergeBatch) {
-      f16x8 v[kMergeBatch];
+  for (int c0 = 0; c0 < nv; c0 += kMergeBatch) {
+    f16x8 v[kMergeBatch];
 #pragma unroll
-      for (int k = 0; k < kMergeBatch; ++k)
-        v[k] = (jok && k0 + k < nb) ? *reinterpret_cast<const f16x8*>(src + (int64_t)(c0 + k0 + k) * kHeadBlk * r)
-                                    : f16x8{};
+    for (int k = 0; k < kMergeBatch; ++k)
+      v[k] = (c0 + k < nv) ? *reinterpret_cast<const f16x8*>(src + (int64_t)(c0 + k) * r * kHeadBlk) : f16x8{};
 #pragma unroll
-      for (int k = 0; k < kMergeBatch; ++k) {
-        const float wc = __shfl(wl, k0 + k, 64);
-        if (k0 + k < nb)
+    for (int k = 0; k < kMergeBatch; ++k) {
+      if (c0 + k >= nv) break;
+      const float w0 = wgt[(c0 + k) * kHeadBlk + h0], w1 = wgt[(c0 + k) * kHeadBlk + h0 + 1];
 #pragma unroll
-          for (int q = 0; q < 8; ++q) acc[q] = fmaf(wc, (float)v[k][q], acc[q]);
+      for (int q = 0; q < 4; ++q) {
+        acc[q] = fmaf(w0, (float)v[k][q], acc[q]);
+        acc[4 + q] = fmaf(w1, (float)v[k][4 + q], acc[4 + q]);
       }
     }
   }
-  if (!jok) return;
-  f16x8 o8;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) o8[k] = (_Float16)acc[k];
-  *reinterpret_cast<f16x8*>(o_lat + ((int64_t)b * kHeadBlk + h) * r + j) = o8;
+  for (int hh = 0; hh < 2; ++hh) {
+    const f16x4 o4 = {(_Float16)acc[4 * hh], (_Float16)acc[4 * hh + 1], (_Float16)acc[4 * hh + 2],
+                      (_Float16)acc[4 * hh + 3]};
+    *reinterpret_cast<f16x4*>(o_lat + ((int64_t)b * kHeadBlk + h0 + hh) * r + 4 * x4) = o4;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -652,8 +659,8 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   if (e != hipSuccess) return e;
   {
     KernelScope ks("merge_latent", s);
-    hipLaunchKernelGGL(merge_latent_kernel, dim3((w.r + kMergeCols - 1) / kMergeCols, kHeadBlk, c.batch), dim3(64),
-                       0, s, opart, ml, c.seq_len, p.chunk, p.n0, p.n_chunks, w.r, olat);
+    hipLaunchKernelGGL(merge_latent_kernel, dim3((w.r * kHeadBlk + kMergeElems - 1) / kMergeElems, c.batch),
+                       dim3(256), 0, s, opart, ml, c.seq_len, p.chunk, p.n0, p.n_chunks, w.r, olat);
   }
   {
     KernelScope ks("vproj", s);
