@@ -182,6 +182,8 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
     return fail(QSVD_ERR_UNSUPPORTED, "integer accumulator dumps need per-channel weights");
   if (!aligned(xq, 16) || !aligned(cq, 16) || !aligned(c_h, 16) || !aligned(w->a_t, 16) || !aligned(w->b_t, 16))
     return fail(QSVD_ERR_UNSUPPORTED, "operands must be 16-byte aligned");
+  if (!skinny && (w->head_dim % 8 || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16)))
+    return fail(QSVD_ERR_UNSUPPORTED, "more than 32 tokens: head_dim a multiple of 8 and 16-byte aligned outputs");
   (void)ws;
   (void)ws_bytes;
   int32_t lo, hi;

@@ -13,22 +13,32 @@
 
 namespace qsvd {
 
+// Output segments (columns [n0, n0 + n) of the product go to ptr with row
+// stride ld); fields are spelled out per segment so that a store only ever
+// reads kernel arguments at constant offsets.
 struct DevSegs {
-  _Float16* ptr[3];
-  int64_t ld[3];
-  int32_t n0[3];
-  int32_t n[3];
-  int32_t n_seg;
+  _Float16* p0; _Float16* p1; _Float16* p2;
+  int64_t ld0, ld1, ld2;
+  int32_t a0, a1, a2;      // first column of each segment
+  int32_t e0, e1, e2;      // one past the last column
 };
 
-__device__ __forceinline__ void store_out(const DevSegs& sg, int64_t m, int32_t n, float y) {
-#pragma unroll
-  for (int s = 0; s < 3; ++s) {
-    if (s < sg.n_seg && n >= sg.n0[s] && n < sg.n0[s] + sg.n[s]) {
-      if (sg.ptr[s]) sg.ptr[s][m * sg.ld[s] + (n - sg.n0[s])] = to_f16(y);
-      return;
-    }
-  }
+// Where column n of the product goes: its first element's address and the row
+// stride (NULL if the column is not stored).  Selects rather than branches, so
+// the three segment pointers stay in registers.
+struct ColOut {
+  _Float16* p;
+  int64_t ld;
+};
+
+__device__ __forceinline__ ColOut col_out(const DevSegs& sg, int32_t n) {
+  const bool in0 = n >= sg.a0 && n < sg.e0;
+  const bool in1 = n >= sg.a1 && n < sg.e1;
+  const bool in2 = n >= sg.a2 && n < sg.e2;
+  _Float16* p = in0 ? sg.p0 + (n - sg.a0) : in1 ? sg.p1 + (n - sg.a1) : in2 ? sg.p2 + (n - sg.a2) : nullptr;
+  if (!(in0 ? sg.p0 : in1 ? sg.p1 : in2 ? sg.p2 : nullptr)) p = nullptr;
+  const int64_t ld = in0 ? sg.ld0 : in1 ? sg.ld1 : sg.ld2;
+  return ColOut{p, ld};
 }
 
 // Dequantize one integer accumulator: (f32(acc) * row_scale) * col_scale, each
@@ -38,120 +48,229 @@ __device__ __forceinline__ float dequant(int32_t acc, float rs, float cs) {
 }
 
 // ---------------------------------------------------------------------------
-// Tiled kernel: 128 x 128 output tile per workgroup, 4 waves of 64 x 64,
-// K staged through LDS 64 bytes at a time with a register double buffer.
+// Pipelined kernel: BM x BN output tile per workgroup of 4 waves (2 x 2, each
+// WM x WN), the contraction in stages of 64 bytes.  Operands go from global
+// memory straight into LDS (global_load_lds_dwordx4: lane i of a wave writes
+// 16 bytes at base + 16 i), NS stages deep, so NS - 1 stages are in flight
+// while one is multiplied; one barrier per stage.
+//
+// LDS layout of a stage: blocks of 16 rows x 64 bytes (1 KB); in a block,
+// 16-byte slot 4 * (row % 16) + (chunk ^ ((row / 4) % 4)) holds contraction
+// chunk `chunk` of that row.  A fragment read (16 consecutive rows, one chunk)
+// then touches every bank once.
 // ---------------------------------------------------------------------------
-constexpr int TBM = 128, TBN = 128, TBK = 64, TPAD = 16, TLD = TBK + TPAD;
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
 
-__global__ void __launch_bounds__(256)
-gemm_i8_tiled_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
-                     const float* __restrict__ rs, const float* __restrict__ cs,
-                     int64_t M, int32_t N, int32_t K, DevSegs sg, int32_t* __restrict__ dbg) {
-  __shared__ __attribute__((aligned(16))) int8_t As[2][TBM * TLD];
-  __shared__ __attribute__((aligned(16))) int8_t Bs[2][TBN * TLD];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 1, wn = w & 1;
-  const int64_t m0 = (int64_t)blockIdx.y * TBM;
-  const int32_t n0 = blockIdx.x * TBN;
+constexpr int PBK = 64;
 
-  // global -> register loader: chunk c in [0, 512) of 16 bytes; row c/4, col 16*(c%4)
-  i32x4 ra[2], rb[2];
-  auto gload = [&](int kt) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int c = tid + 256 * h, row = c >> 2, col = (c & 3) * 16;
-      const int64_t gm = m0 + row;
-      const int32_t gn = n0 + row;
-      const int64_t k = (int64_t)kt * TBK + col;
-      ra[h] = (gm < M) ? *reinterpret_cast<const i32x4*>(A + gm * K + k) : i32x4{0, 0, 0, 0};
-      rb[h] = (gn < N) ? *reinterpret_cast<const i32x4*>(B + (int64_t)gn * K + k) : i32x4{0, 0, 0, 0};
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int c = tid + 256 * h, row = c >> 2, col = (c & 3) * 16;
-      *reinterpret_cast<i32x4*>(&As[buf][row * TLD + col]) = ra[h];
-      *reinterpret_cast<i32x4*>(&Bs[buf][row * TLD + col]) = rb[h];
-    }
-  };
-
-  i32x16 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = i32x16{};
-
-  const int nk = K / TBK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-#pragma unroll
-    for (int kk = 0; kk < TBK; kk += 32) {
-      i32x4 af[2], bf[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int row = wm * 64 + i * 32 + (lane & 31);
-        af[i] = *reinterpret_cast<const i32x4*>(&As[cur][row * TLD + kk + 16 * (lane >> 5)]);
-      }
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int row = wn * 64 + j * 32 + (lane & 31);
-        bf[j] = *reinterpret_cast<const i32x4*>(&Bs[cur][row * TLD + kk + 16 * (lane >> 5)]);
-      }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) sstore(cur ^ 1);
-    __syncthreads();
-  }
-
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int32_t n = n0 + wn * 64 + j * 32 + (lane & 31);
-      if (n >= N) continue;
-      const float csn = cs[n];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int64_t m = m0 + wm * 64 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        if (m >= M) continue;
-        const int32_t a = acc[i][j][v];
-        if (dbg) dbg[m * N + n] = a;
-        store_out(sg, m, n, dequant(a, rs[m], csn));
-      }
-    }
+// Wait until at most N direct loads of this wave are outstanding (and its LDS
+// reads are done), then meet the other waves.  Written as one asm statement
+// so that the compiler neither adds a full wait nor moves LDS accesses across.
+template <int N>
+__device__ __forceinline__ void vm_wait_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
+// The stage being consumed was issued `rem` stages before the newest one.
+template <int LPW, int R>
+__device__ __forceinline__ void vm_wait_stage(int rem) {
+  if constexpr (R == 0) {
+    vm_wait_barrier<0>();
+  } else {
+    if (rem >= R) vm_wait_barrier<R * LPW>();
+    else vm_wait_stage<LPW, R - 1>(rem);
+  }
+}
+
+__device__ __forceinline__ int pipe_slot(int row, int chunk) {
+  return (row >> 4) * 1024 + (4 * (row & 15) + (chunk ^ ((row >> 2) & 3))) * 16;
+}
+
+template <int BM, int BN, int WM, int WN, int NS>
+struct PipeCfg {
+  static_assert((BM / WM) * (BN / WN) == 4, "four waves");
+  static constexpr int kABlocks = BM / 16, kBBlocks = BN / 16;
+  static constexpr int kLPW = (kABlocks + kBBlocks) / 4;     // direct loads per wave per stage
+  static constexpr int kStage = (kABlocks + kBBlocks) * 1024;
+  static constexpr size_t kStages = (size_t)NS * kStage;
+  static constexpr size_t kOut = (size_t)4 * WM * (WN + 8) * 2;   // fp16 output staging
+  static constexpr size_t kLds = kStages > kOut ? kStages : kOut;
+};
+
+template <int BM, int BN, int WM, int WN, int NS, bool DBG>
+__global__ void __launch_bounds__(256)
+gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
+                    const float* __restrict__ rs, const float* __restrict__ cs,
+                    int64_t M, int32_t N, int32_t K, int32_t n_tiles_n, DevSegs sg, int32_t* __restrict__ dbg) {
+  using C = PipeCfg<BM, BN, WM, WN, NS>;
+  constexpr int TI = WM / 32, TJ = WN / 32;
+  extern __shared__ __attribute__((aligned(1024))) uint8_t pipe_smem[];
+  __shared__ __attribute__((aligned(16))) float s_rs[BM];
+  __shared__ float s_cs[BN];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w / (BN / WN), wn = w % (BN / WN);
+  const int l32 = lane & 31, hl = lane >> 5;
+  const int tm = blockIdx.x / n_tiles_n, tn = blockIdx.x % n_tiles_n;
+  const int64_t m0 = (int64_t)tm * BM;
+  const int32_t n0 = tn * BN;
+  const int nk = K / PBK;
+
+  auto issue = [&](int st) {
+    uint8_t* base = pipe_smem + (st % NS) * C::kStage;
+    const int64_t k0 = (int64_t)st * PBK;
+#pragma unroll
+    for (int j = 0; j < C::kLPW; ++j) {
+      const int blk = w * C::kLPW + j;                       // wave-uniform
+      const bool is_a = blk < C::kABlocks;
+      const int row = 16 * (is_a ? blk : blk - C::kABlocks) + (lane >> 2);
+      const int chunk = (lane & 3) ^ ((row >> 2) & 3);
+      const int8_t* src;
+      if (is_a) src = A + min(m0 + row, M - 1) * K + k0 + 16 * chunk;
+      else src = B + (int64_t)min(n0 + row, N - 1) * K + k0 + 16 * chunk;
+      __builtin_amdgcn_global_load_lds((glb_void_t*)src, (lds_void_t*)(base + blk * 1024), 16, 0, 0);
+    }
+  };
+
+  // scales first: their wait then leaves the stage loads in flight
+  for (int i = tid; i < BM; i += 256) s_rs[i] = rs[min(m0 + i, M - 1)];
+  for (int i = tid; i < BN; i += 256) s_cs[i] = cs[min(n0 + i, N - 1)];
+#pragma unroll
+  for (int st = 0; st < NS - 1; ++st)
+    if (st < nk) issue(st);
+
+  i32x16 acc[TI][TJ];
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) acc[i][j] = i32x16{};
+
+  for (int kt = 0; kt < nk; ++kt) {
+    vm_wait_stage<C::kLPW, NS - 2>(nk - 1 - kt);
+    if (kt + NS - 1 < nk) issue(kt + NS - 1);
+    const uint8_t* sa = pipe_smem + (kt % NS) * C::kStage;
+    const uint8_t* sb = sa + C::kABlocks * 1024;
+    // all fragments of the stage are read first (in order, so the second
+    // half's latency hides behind the first half's products)
+    i32x4 af[2][TI], bf[2][TJ];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+        af[kk][i] = *reinterpret_cast<const i32x4*>(sa + pipe_slot(wm * WM + 32 * i + l32, 2 * kk + hl));
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+        bf[kk][j] = *reinterpret_cast<const i32x4*>(sb + pipe_slot(wn * WN + 32 * j + l32, 2 * kk + hl));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk][i], bf[kk][j], acc[i][j], 0, 0, 0);
+  }
+
+  // Epilogue.  The integer accumulators are dumped as they are (debug only);
+  // the dequantized fp16 tile of each wave is staged in LDS (the stages are
+  // free once every wave is past its last product) and written back as
+  // 16-byte runs of one row.  Lane holds column wn*WN + 32j + l32 and rows
+  // wm*WM + 32i + 8(v/4) + 4hl + v%4.
+  if (DBG) {
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int32_t n = n0 + wn * WN + 32 * j + l32;
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int64_t m = m0 + wm * WM + 32 * i + 8 * (v >> 2) + 4 * hl + (v & 3);
+          if (m < M && n < N) dbg[m * N + n] = acc[i][j][v];
+        }
+    }
+  }
+  vm_wait_barrier<0>();
+  constexpr int OST = WN + 8;                   // staged row stride in halves
+  _Float16* ost = reinterpret_cast<_Float16*>(pipe_smem) + w * WM * OST;
+#pragma unroll
+  for (int j = 0; j < TJ; ++j) {
+    const float csn = s_cs[wn * WN + 32 * j + l32];
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int vq = 0; vq < 4; ++vq) {
+        const int rl = 32 * i + 8 * vq + 4 * hl;  // 4 consecutive rows of this lane
+        const f32x4 r4 = *reinterpret_cast<const f32x4*>(&s_rs[wm * WM + rl]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          ost[(rl + e) * OST + 32 * j + l32] = to_f16(dequant(acc[i][j][4 * vq + e], r4[e], csn));
+        // one accumulator block at a time: keeps the live registers few
+        __builtin_amdgcn_sched_barrier(0);
+      }
+  }
+  constexpr int CPR = WN / 8;                   // 16-byte chunks per staged row
+  for (int e = lane; e < WM * CPR; e += 64) {
+    const int row = e / CPR, c8 = e % CPR;
+    const int64_t m = m0 + wm * WM + row;
+    const int32_t n = n0 + wn * WN + 8 * c8;
+    if (m >= M || n >= N) continue;
+    const ColOut co = col_out(sg, n);
+    if (co.p) *reinterpret_cast<f16x8*>(co.p + m * co.ld) = *reinterpret_cast<const f16x8*>(ost + row * OST + 8 * c8);
+  }
+}
+
+// Segments are consecutive and ascending in the column range; missing ones
+// become empty ranges past the last column.
 static DevSegs to_dev(const GemmArgs& g) {
   DevSegs d{};
-  d.n_seg = g.n_seg;
+  _Float16** ps[3] = {&d.p0, &d.p1, &d.p2};
+  int64_t* lds[3] = {&d.ld0, &d.ld1, &d.ld2};
+  int32_t* as[3] = {&d.a0, &d.a1, &d.a2};
+  int32_t* es[3] = {&d.e0, &d.e1, &d.e2};
   for (int s = 0; s < 3; ++s) {
-    d.ptr[s] = s < g.n_seg ? g.seg[s].ptr : nullptr;
-    d.ld[s] = s < g.n_seg ? g.seg[s].ld : 0;
-    d.n0[s] = s < g.n_seg ? g.seg[s].n0 : 0;
-    d.n[s] = s < g.n_seg ? g.seg[s].n : 0;
+    if (s < g.n_seg) {
+      *ps[s] = g.seg[s].ptr;
+      *lds[s] = g.seg[s].ld;
+      *as[s] = g.seg[s].n0;
+      *es[s] = g.seg[s].n0 + g.seg[s].n;
+    } else {
+      *ps[s] = nullptr;
+      *lds[s] = 0;
+      *as[s] = *es[s] = s > 0 ? *es[s - 1] : 0;
+    }
   }
   return d;
 }
 
+template <int BM, int BN, int WM, int WN, int NS, bool DBG>
+static hipError_t launch_pipe(const GemmArgs& g, const DevSegs& sg, hipStream_t s) {
+  using C = PipeCfg<BM, BN, WM, WN, NS>;
+  auto kern = gemm_i8_pipe_kernel<BM, BN, WM, WN, NS, DBG>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::kLds);
+  if (e != hipSuccess) return e;
+  const int tn = (g.N + BN - 1) / BN;
+  const int64_t tm = (g.M + BM - 1) / BM;
+  KernelScope ks("gemm_i8_pipe", s);
+  hipLaunchKernelGGL(kern, dim3((unsigned)(tm * tn)), dim3(256), C::kLds, s, g.a, g.b, g.row_scale, g.col_scale,
+                     g.M, g.N, g.K, tn, sg, g.dbg);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_i8(const GemmArgs& g, hipStream_t s) {
   if (g.M == 0 || g.N == 0) return hipSuccess;
+  if (g.K % PBK) return hipErrorInvalidValue;
+  // outputs are written in 16-byte runs of 8 columns
+  for (int i = 0; i < g.n_seg; ++i)
+    if (g.seg[i].n0 % 8 || g.seg[i].n % 8 || g.seg[i].ld % 8 || ((uintptr_t)g.seg[i].ptr & 15))
+      return hipErrorInvalidValue;
   const DevSegs sg = to_dev(g);
-  dim3 grid((g.N + TBN - 1) / TBN, (unsigned)((g.M + TBM - 1) / TBM));
-  {
-    KernelScope ks("gemm_i8_tiled", s);
-    hipLaunchKernelGGL(gemm_i8_tiled_kernel, grid, dim3(256), 0, s, g.a, g.b, g.row_scale, g.col_scale, g.M, g.N,
-                       g.K, sg, g.dbg);
-  }
-  hipError_t e = hipGetLastError();
+  // 256 x 256 tiles once they fill the chip, 128 x 128 otherwise (and for
+  // the accumulator dumps)
+  const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  hipError_t e = g.dbg ? launch_pipe<128, 128, 64, 64, 6, true>(g, sg, s)
+                 : big_tiles >= 256 ? launch_pipe<256, 256, 128, 128, 4, false>(g, sg, s)
+                                    : launch_pipe<128, 128, 64, 64, 6, false>(g, sg, s);
   if (e != hipSuccess || !g.cq) return e;
   return launch_quantize_rows(g.seg[0].ptr, g.M, g.N, g.seg[0].ld, g.abits, 1.f, g.cq, g.sc, s);
 }
