@@ -34,6 +34,8 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5033.0        # MI355X dense int8 matrix peak, TOP/s
 N_LAYERS = 32                  # LLaVA-1.5-7B language-model layers
 DECODE_BATCH, CTX0, DECODE_VISITS = 16, 4096, 256
+# hardware-counter summary of the latent attention kernel on this workload
+ATTN_TRAFFIC_SUMMARY = "latent_attn_llava7b_decode_traffic.txt"
 
 
 def parse():
@@ -49,6 +51,35 @@ def parse():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
                     help="also run a plain device copy of MB megabytes (calibrates memory counters)")
     return ap.parse_args()
+
+
+def file_sha256(rel):
+    import hashlib
+    with open(os.path.join(ROOT, rel), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def counted_traffic(summary):
+    """HBM bytes per launch of a kernel from its committed hardware-counter
+    summary under profiles/ (FETCH_SIZE and WRITE_SIZE per dispatch, each
+    scaled by what the counter reads for a plain copy of known size), or None
+    when the summary is missing or was taken on another version of the
+    kernel's source file."""
+    path = os.path.join(ROOT, "profiles", summary)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.lstrip().startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    try:
+        if file_sha256(kv["source"]) != kv["source_sha256"]:
+            return None
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError, OSError):
+        return None
 
 
 def copy_probe(mb):
@@ -167,8 +198,10 @@ def bench_decode(args, wl, host_layer):
             bytes_per_launch = ctx_read / args.steps * r * 2
             achieved = bytes_per_launch / avg_s / 1e9
             res["attn_kernel_us"] = avg_s * 1e6
+            traffic = counted_traffic(ATTN_TRAFFIC_SUMMARY) if mode != B.QSVD_ATTN_RECONSTRUCT else None
             res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                               "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                               "frac": round(achieved / HBM_PEAK_GBS, 4),
+                               "traffic": None if traffic is None else int(traffic),
                                "kernel": "latent_attn_kernel", "launches": n,
                                "bytes_per_launch": int(bytes_per_launch)}
     # absorbed vs reconstruct on this layer, attention call alone (a few calls each)

@@ -79,6 +79,7 @@ qsvd_status check_cache(const qsvd_cache* c) {
 struct ProfRec {
   std::string name;
   hipEvent_t start, stop;
+  bool valid;      // the events were handed to a launch
 };
 std::mutex g_prof_mu;
 bool g_prof_on = false;
@@ -89,21 +90,33 @@ std::vector<ProfRec> g_prof;
 
 namespace qsvd {
 
-KernelScope::KernelScope(const char* name, hipStream_t s) : name_(name), s_(s), slot_(-1) {
+KernelScope::KernelScope(const char* name, hipStream_t) : slot_(-1), used_(false), start_(nullptr), stop_(nullptr) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   if (!g_prof_on) return;
   if (!g_prof_filter.empty() && std::string(name).find(g_prof_filter) == std::string::npos) return;
-  ProfRec r{name, nullptr, nullptr};
-  if (hipEventCreate(&r.start) != hipSuccess || hipEventCreate(&r.stop) != hipSuccess) return;
-  hipEventRecord(r.start, s);
+  ProfRec r{name, nullptr, nullptr, false};
+  if (hipEventCreate(&r.start) != hipSuccess) return;
+  if (hipEventCreate(&r.stop) != hipSuccess) {
+    hipEventDestroy(r.start);
+    return;
+  }
+  start_ = r.start;
+  stop_ = r.stop;
   g_prof.push_back(r);
   slot_ = (int)g_prof.size() - 1;
 }
 
+hipEvent_t KernelScope::start() {
+  used_ = used_ || start_ != nullptr;
+  return start_;
+}
+
+hipEvent_t KernelScope::stop() { return stop_; }
+
 KernelScope::~KernelScope() {
   if (slot_ < 0) return;
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  if (slot_ < (int)g_prof.size()) hipEventRecord(g_prof[slot_].stop, s_);
+  if (slot_ < (int)g_prof.size() && g_prof[slot_].start == start_) g_prof[slot_].valid = used_;
 }
 
 }  // namespace qsvd
@@ -317,7 +330,7 @@ qsvd_status qsvd_profile_read(const char* name, double* total_ms, int64_t* launc
   double tot = 0.0;
   int64_t n = 0;
   for (auto& r : g_prof) {
-    if (r.name.find(name) == std::string::npos) continue;
+    if (!r.valid || r.name.find(name) == std::string::npos) continue;
     hipError_t e = hipEventSynchronize(r.stop);
     if (e != hipSuccess) return hip_status(e, "profile read");
     float ms = 0.f;

@@ -618,7 +618,7 @@ static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, const 
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   KernelScope ks("latent_attn", s);
-  hipLaunchKernelGGL(kern, dim3(p.n_chunks, c.batch), dim3(NW * 64), lds, s, qt,
+  QSVD_LAUNCH(ks, kern, dim3(p.n_chunks, c.batch), dim3(NW * 64), lds, s, qt,
                      (const uint8_t*)c.data, c.scale, c.seq_len, c.capacity, c.r, p.chunk,
                      p.n0, opart, ml);
   return hipGetLastError();
@@ -648,7 +648,7 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
   {
     KernelScope ks("absorb_q", s);
-    hipLaunchKernelGGL(absorb_kernel, dim3(kHeadBlk, w.r / kAbsorbJ), dim3(64), 0, s, a.q,
+    QSVD_LAUNCH(ks, absorb_kernel, dim3(kHeadBlk, w.r / kAbsorbJ), dim3(64), 0, s, a.q,
                        (const uint8_t*)w.b_t, w.s_b, c.batch, w.r, w.n_q_heads, w.n_kv_heads,
                        w.head_dim, N, w.w_bits, w.w_group, a.sm_scale * kLog2e, qt);
   }
@@ -659,12 +659,12 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   if (e != hipSuccess) return e;
   {
     KernelScope ks("merge_latent", s);
-    hipLaunchKernelGGL(merge_latent_kernel, dim3((w.r * kHeadBlk + kMergeElems - 1) / kMergeElems, c.batch),
+    QSVD_LAUNCH(ks, merge_latent_kernel, dim3((w.r * kHeadBlk + kMergeElems - 1) / kMergeElems, c.batch),
                        dim3(256), 0, s, opart, ml, c.seq_len, p.chunk, p.n0, p.n_chunks, w.r, olat);
   }
   {
     KernelScope ks("vproj", s);
-    hipLaunchKernelGGL(vproj_kernel, dim3(w.n_q_heads, w.head_dim / 16), dim3(64 * kVprojWaves), 0, s, olat,
+    QSVD_LAUNCH(ks, vproj_kernel, dim3(w.n_q_heads, w.head_dim / 16), dim3(64 * kVprojWaves), 0, s, olat,
                        (const uint8_t*)w.b_t, w.s_b, c.batch, w.r, w.n_q_heads, w.n_kv_heads, w.head_dim, N,
                        w.w_bits, w.w_group, a.out);
   }
@@ -874,11 +874,11 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
     dim3 grid((nkv2 + RBN - 1) / RBN, (len + RBM - 1) / RBM, c.batch);
     KernelScope ks("recon_kv", s);
     if (c.fmt == QSVD_CACHE_F16)
-      hipLaunchKernelGGL(recon_kv_kernel<QSVD_CACHE_F16>, grid, dim3(256), 0, s, (const uint8_t*)c.data,
+      QSVD_LAUNCH(ks, recon_kv_kernel<QSVD_CACHE_F16>, grid, dim3(256), 0, s, (const uint8_t*)c.data,
                          c.scale, c.seq_len, c.capacity, c.r, (const uint8_t*)w.b_t, w.s_b, N, nq, nkv2,
                          w.w_bits, w.w_group, kv);
     else
-      hipLaunchKernelGGL(recon_kv_kernel<QSVD_CACHE_I8>, grid, dim3(256), 0, s, (const uint8_t*)c.data,
+      QSVD_LAUNCH(ks, recon_kv_kernel<QSVD_CACHE_I8>, grid, dim3(256), 0, s, (const uint8_t*)c.data,
                          c.scale, c.seq_len, c.capacity, c.r, (const uint8_t*)w.b_t, w.s_b, N, nq, nkv2,
                          w.w_bits, w.w_group, kv);
   }
@@ -887,13 +887,13 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
   const int nch = (len + RCH - 1) / RCH;
   {
     KernelScope ks("recon_attn", s);
-    hipLaunchKernelGGL(recon_attn_kernel, dim3(nch, c.batch), dim3(256), 0, s, a.q, kv, c.seq_len,
+    QSVD_LAUNCH(ks, recon_attn_kernel, dim3(nch, c.batch), dim3(256), 0, s, a.q, kv, c.seq_len,
                        c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, a.sm_scale * kLog2e,
                        p.n_chunks, opart, ml);
   }
   {
     KernelScope ks("recon_combine", s);
-    hipLaunchKernelGGL(combine_kernel<true>, dim3((w.head_dim + 63) / 64, c.batch), dim3(256), 0, s, opart, ml,
+    QSVD_LAUNCH(ks, combine_kernel<true>, dim3((w.head_dim + 63) / 64, c.batch), dim3(256), 0, s, opart, ml,
                        c.seq_len, RCH, p.n_chunks, nch, w.head_dim, w.n_q_heads, a.out);
   }
   return hipGetLastError();

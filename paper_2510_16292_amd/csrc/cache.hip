@@ -67,14 +67,14 @@ hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void*
   }
   if (n_new <= 16) {
     KernelScope ks("cache_append", s);
-    hipLaunchKernelGGL(cache_append_fused_kernel, dim3(c.batch), dim3(256), 0, s, (const uint8_t*)src,
+    QSVD_LAUNCH(ks, cache_append_fused_kernel, dim3(c.batch), dim3(256), 0, s, (const uint8_t*)src,
                        c.fmt == QSVD_CACHE_F16 ? nullptr : sc, (uint8_t*)c.data,
                        c.fmt == QSVD_CACHE_F16 ? nullptr : c.scale, c.seq_len, c.capacity, n_new, row_bytes);
     return hipGetLastError();
   }
   {
     KernelScope ks("cache_append", s);
-    hipLaunchKernelGGL(cache_append_kernel, dim3(n_new, c.batch), dim3(128), 0, s, (const uint8_t*)src,
+    QSVD_LAUNCH(ks, cache_append_kernel, dim3(n_new, c.batch), dim3(128), 0, s, (const uint8_t*)src,
                        c.fmt == QSVD_CACHE_F16 ? nullptr : sc, (uint8_t*)c.data,
                        c.fmt == QSVD_CACHE_F16 ? nullptr : c.scale, c.seq_len, c.capacity, n_new,
                        row_bytes);
@@ -83,7 +83,7 @@ hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void*
   if (e != hipSuccess) return e;
   {
     KernelScope ks("seq_len_advance", s);
-    hipLaunchKernelGGL(seq_len_advance_kernel, dim3((c.batch + 255) / 256), dim3(256), 0, s, c.seq_len,
+    QSVD_LAUNCH(ks, seq_len_advance_kernel, dim3((c.batch + 255) / 256), dim3(256), 0, s, c.seq_len,
                        c.batch, n_new);
   }
   return hipGetLastError();

@@ -252,7 +252,7 @@ static hipError_t launch_pipe(const GemmArgs& g, const DevSegs& sg, hipStream_t 
   const int tn = (g.N + BN - 1) / BN;
   const int64_t tm = (g.M + BM - 1) / BM;
   KernelScope ks("gemm_i8_pipe", s);
-  hipLaunchKernelGGL(kern, dim3((unsigned)(tm * tn)), dim3(256), C::kLds, s, g.a, g.b, g.row_scale, g.col_scale,
+  QSVD_LAUNCH(ks, kern, dim3((unsigned)(tm * tn)), dim3(256), C::kLds, s, g.a, g.b, g.row_scale, g.col_scale,
                      g.M, g.N, g.K, tn, sg, g.dbg);
   return hipGetLastError();
 }

@@ -1,5 +1,6 @@
 // Internal host-side launch wrappers (validated arguments only).
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -7,14 +8,22 @@
 
 namespace qsvd {
 
-// Records kernel timing events when the profiler is enabled (api.hip).
+// Kernel timing for the profiler (api.hip): when it is enabled for this name,
+// start() and stop() are events that hipExtLaunchKernelGGL stamps with the
+// kernel's own start and end times; otherwise they are NULL.  Every profiled
+// launch goes through QSVD_LAUNCH.
 struct KernelScope {
   KernelScope(const char* name, hipStream_t s);
   ~KernelScope();
-  const char* name_;
-  hipStream_t s_;
+  hipEvent_t start();
+  hipEvent_t stop();
   int slot_;
+  bool used_;
+  hipEvent_t start_, stop_;
 };
+
+#define QSVD_LAUNCH(ks, kern, grid, block, lds, stream, ...) \
+  hipExtLaunchKernelGGL(kern, grid, block, (std::uint32_t)(lds), stream, (ks).start(), (ks).stop(), 0, __VA_ARGS__)
 
 hipError_t launch_quantize_rows(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits,
                                 float clip, void* xq, float* sx, hipStream_t s);

@@ -79,11 +79,11 @@ hipError_t launch_quantize_rows(const void* x, int64_t M, int32_t K, int64_t ldx
   const _Float16* xp = (const _Float16*)x;
   uint8_t* q = (uint8_t*)xq;
   if (bits == 8) {
-    if (regs) hipLaunchKernelGGL((quantize_rows_kernel<8, 16>), grid, block, 0, s, xp, M, K, ldx, clip, q, sx);
-    else hipLaunchKernelGGL((quantize_rows_kernel<8, 0>), grid, block, 0, s, xp, M, K, ldx, clip, q, sx);
+    if (regs) QSVD_LAUNCH(ks, (quantize_rows_kernel<8, 16>), grid, block, 0, s, xp, M, K, ldx, clip, q, sx);
+    else QSVD_LAUNCH(ks, (quantize_rows_kernel<8, 0>), grid, block, 0, s, xp, M, K, ldx, clip, q, sx);
   } else {
-    if (regs) hipLaunchKernelGGL((quantize_rows_kernel<4, 16>), grid, block, 0, s, xp, M, K, ldx, clip, q, sx);
-    else hipLaunchKernelGGL((quantize_rows_kernel<4, 0>), grid, block, 0, s, xp, M, K, ldx, clip, q, sx);
+    if (regs) QSVD_LAUNCH(ks, (quantize_rows_kernel<4, 16>), grid, block, 0, s, xp, M, K, ldx, clip, q, sx);
+    else QSVD_LAUNCH(ks, (quantize_rows_kernel<4, 0>), grid, block, 0, s, xp, M, K, ldx, clip, q, sx);
   }
   return hipGetLastError();
 }

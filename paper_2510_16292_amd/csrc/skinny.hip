@@ -299,12 +299,12 @@ hipError_t launch_skinny(const GemmArgs& g, bool a_is_f16_latent, int32_t wbits,
   if (!a_is_f16_latent) {
     auto k = wbits == 8 ? skinny_gemm_kernel<SK_A_I8, 8> : skinny_gemm_kernel<SK_A_I8, 4>;
     if (hipError_t e = allow((const void*)k); e != hipSuccess) return e;
-    hipLaunchKernelGGL(k, grid, block, p.lds, s, (const void*)g.a, g.row_scale, bt, g.col_scale, sstride, M, g.N,
+    QSVD_LAUNCH(ks, k, grid, block, p.lds, s, (const void*)g.a, g.row_scale, bt, g.col_scale, sstride, M, g.N,
                        g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)nullptr, (float*)nullptr);
   } else {
     auto k = wbits == 8 ? skinny_gemm_kernel<SK_A_F16Q, 8> : skinny_gemm_kernel<SK_A_F16Q, 4>;
     if (hipError_t e = allow((const void*)k); e != hipSuccess) return e;
-    hipLaunchKernelGGL(k, grid, block, p.lds, s, (const void*)g.a, (const float*)nullptr, bt, g.col_scale, sstride,
+    QSVD_LAUNCH(ks, k, grid, block, p.lds, s, (const void*)g.a, (const float*)nullptr, bt, g.col_scale, sstride,
                        M, g.N, g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)g.cq, g.sc);
   }
   return hipGetLastError();
