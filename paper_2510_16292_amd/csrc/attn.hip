@@ -69,33 +69,58 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
   }
   const int g = (h * Hkv) / Hq;
   const int32_t nk0 = Hq * dh + g * dh;
-  // stage: chunk e -> row c = e / 4, 16 codes at columns 16 * (e % 4)
-  for (int e = lane; e < dh * 4; e += 64) {
+  // stage: chunk e -> row c = e / 4, 16 codes at columns 16 * (e % 4); every
+  // lane's loads (dh <= 128: at most 8 chunks) go out before any is used
+  constexpr int kStageIt = 128 * 4 / 64;
+  uint4 raw[kStageIt];
+  float sc[kStageIt];
+#pragma unroll
+  for (int it = 0; it < kStageIt; ++it) {
+    const int e = lane + 64 * it;
+    if (e >= dh * 4) break;
     const int c = e >> 2, j16 = (e & 3) * 16;
     const int32_t n = nk0 + c;
-    float sc = group ? sb[(int64_t)(jb / group) * N + n] : sb[n];
+    sc[it] = group ? sb[(int64_t)(jb / group) * N + n] : sb[n];
+    if (bits == 8) {
+      raw[it] = *reinterpret_cast<const uint4*>(bt + (int64_t)n * r + jb + j16);
+    } else {
+      const uint2 r2 = *reinterpret_cast<const uint2*>(bt + ((int64_t)n * r + jb + j16) / 2);
+      raw[it] = make_uint4(r2.x, r2.y, 0u, 0u);
+    }
+  }
+  const int l16 = lane & 15, quad = lane >> 4;
+  // query rows of the first 16 sequences, loaded while the weights arrive
+  f16x8 qa[128 / 32];
+  {
+    const int bA = l16;
+    const _Float16* qrow = q + (int64_t)min(bA, B - 1) * Hq * dh + h * dh + 8 * quad;
+#pragma unroll
+    for (int k = 0; k < 128 / 32; ++k) qa[k] = (32 * k < dh && bA < B) ? *reinterpret_cast<const f16x8*>(qrow + 32 * k) : f16x8{};
+  }
+#pragma unroll
+  for (int it = 0; it < kStageIt; ++it) {
+    const int e = lane + 64 * it;
+    if (e >= dh * 4) break;
+    const int c = e >> 2, j16 = (e & 3) * 16;
     f16x8 lo, hi;
     if (bits == 8) {
-      const uint4 raw = *reinterpret_cast<const uint4*>(bt + (int64_t)n * r + jb + j16);
-      const uint32_t wv[4] = {raw.x, raw.y, raw.z, raw.w};
+      const uint32_t wv[4] = {raw[it].x, raw[it].y, raw[it].z, raw[it].w};
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        lo[k] = (_Float16)((float)(int8_t)(wv[k >> 2] >> (8 * (k & 3))) * sc);
-        hi[k] = (_Float16)((float)(int8_t)(wv[2 + (k >> 2)] >> (8 * (k & 3))) * sc);
+        lo[k] = (_Float16)((float)(int8_t)(wv[k >> 2] >> (8 * (k & 3))) * sc[it]);
+        hi[k] = (_Float16)((float)(int8_t)(wv[2 + (k >> 2)] >> (8 * (k & 3))) * sc[it]);
       }
     } else {
-      const uint2 raw = *reinterpret_cast<const uint2*>(bt + ((int64_t)n * r + jb + j16) / 2);
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        lo[k] = (_Float16)((float)(((int)(raw.x << (28 - 4 * k))) >> 28) * sc);
-        hi[k] = (_Float16)((float)(((int)(raw.y << (28 - 4 * k))) >> 28) * sc);
+        lo[k] = (_Float16)((float)(((int)(raw[it].x << (28 - 4 * k))) >> 28) * sc[it]);
+        hi[k] = (_Float16)((float)(((int)(raw[it].y << (28 - 4 * k))) >> 28) * sc[it]);
       }
     }
     *reinterpret_cast<f16x8*>(&wk[c * kAbsorbLd + j16]) = lo;
     *reinterpret_cast<f16x8*>(&wk[c * kAbsorbLd + j16 + 8]) = hi;
   }
   __syncthreads();
-  const int l16 = lane & 15, quad = lane >> 4;
   const int s16 = lane & 15;
   typedef short s16x4 __attribute__((ext_vector_type(4)));
   typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
@@ -105,8 +130,11 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
     f32x4 acc[kAbsorbJ / 16];
 #pragma unroll
     for (int jj = 0; jj < kAbsorbJ / 16; ++jj) acc[jj] = f32x4{};
-    for (int c0 = 0; c0 < dh; c0 += 32) {
-      f16x8 a = *reinterpret_cast<const f16x8*>(qrow + c0);
+#pragma unroll
+    for (int k = 0; k < 128 / 32; ++k) {
+      const int c0 = 32 * k;
+      if (c0 >= dh) break;
+      f16x8 a = b0 == 0 ? qa[k] : *reinterpret_cast<const f16x8*>(qrow + c0);
       if (bA >= B) a = f16x8{};
 #pragma unroll
       for (int jj = 0; jj < kAbsorbJ / 16; ++jj) {
@@ -354,6 +382,15 @@ merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict
   const int L = seq_len[b];
   const int nv = L > 0 ? min(min((L + chunk - 1) / chunk, n_launched), kMaxChunks) : 0;
   const int64_t pb = (int64_t)b * n_chunks;
+  // element e8 (8 halves): latent quad x4 = e8 / 16, heads 2*(e8 % 16) and +1;
+  // the first batch of partial loads goes out before the weights are known
+  const int64_t e0 = (int64_t)blockIdx.x * kMergeElems + 8 * tid;
+  const bool eok = e0 < (int64_t)r * kHeadBlk;
+  const _Float16* src = o_part + pb * (int64_t)r * kHeadBlk + (eok ? e0 : 0);
+  f16x8 v[kMergeBatch];
+#pragma unroll
+  for (int k = 0; k < kMergeBatch; ++k)
+    v[k] = (eok && k < nv) ? *reinterpret_cast<const f16x8*>(src + (int64_t)k * r * kHeadBlk) : f16x8{};
   {
     const int h = tid >> 3, sub = tid & 7;
     float m = -INFINITY;
@@ -372,19 +409,17 @@ merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict
     for (int c = sub; c < nv; c += 8) wgt[c * kHeadBlk + h] *= inv;
   }
   __syncthreads();
-  // element e8 (8 halves): latent quad x4 = e8 / 16, heads 2*(e8 % 16) and +1
-  const int64_t e0 = (int64_t)blockIdx.x * kMergeElems + 8 * tid;
-  if (e0 >= (int64_t)r * kHeadBlk) return;
+  if (!eok) return;
   const int x4 = (int)(e0 / (4 * kHeadBlk)), h0 = (int)((e0 / 4) % kHeadBlk);
-  const _Float16* src = o_part + pb * (int64_t)r * kHeadBlk + e0;
   float acc[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) acc[k] = 0.f;
   for (int c0 = 0; c0 < nv; c0 += kMergeBatch) {
-    f16x8 v[kMergeBatch];
+    if (c0 > 0) {
 #pragma unroll
-    for (int k = 0; k < kMergeBatch; ++k)
-      v[k] = (c0 + k < nv) ? *reinterpret_cast<const f16x8*>(src + (int64_t)(c0 + k) * r * kHeadBlk) : f16x8{};
+      for (int k = 0; k < kMergeBatch; ++k)
+        v[k] = (c0 + k < nv) ? *reinterpret_cast<const f16x8*>(src + (int64_t)(c0 + k) * r * kHeadBlk) : f16x8{};
+    }
 #pragma unroll
     for (int k = 0; k < kMergeBatch; ++k) {
       if (c0 + k >= nv) break;
@@ -499,6 +534,7 @@ vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt,
   const int32_t n = Hq * dh + Hkv * dh + g * dh + c0 + l16;
   const int steps = r / 32;
   const int s_begin = (w * steps) / kVprojWaves, s_end = ((w + 1) * steps) / kVprojWaves;
+  const float cs = group ? 1.f : sb[n];      // per-channel scale, fetched with the first loads
   for (int b0 = 0; b0 < B; b0 += 16) {
     const int bA = b0 + l16;
     const _Float16* arow = o_lat + ((int64_t)min(bA, B - 1) * kHeadBlk + h) * r + 8 * quad;
@@ -551,7 +587,6 @@ vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt,
       f32x4 tot = red[0][lane];
 #pragma unroll
       for (int w2 = 1; w2 < kVprojWaves; ++w2) tot += red[w2][lane];
-      const float cs = group ? 1.f : sb[n];
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int bb = b0 + 4 * quad + v;

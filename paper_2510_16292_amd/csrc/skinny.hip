@@ -33,7 +33,8 @@ constexpr int kSkCols = 16;        // output columns per workgroup
 constexpr int kSkMaxWaves = 16;
 constexpr int kSkBatch = 4;        // 64-byte contraction steps loaded per batch
 constexpr int kSkMaxRowChunks = 8; // fp16 row pass: K <= 8 * 64 * 8 = 4096
-constexpr size_t kSkLdsLimit = 160 * 1024 - 1024;
+constexpr int kSkMaxGroups = 64;   // scale groups along the contraction
+constexpr size_t kSkLdsLimit = 160 * 1024 - 5 * 1024;   // dynamic LDS beside the static scale arrays
 
 struct SkinnyOut {
   _Float16* ptr[3];
@@ -111,6 +112,24 @@ skinny_gemm_kernel(const void* __restrict__ a_src, const float* __restrict__ row
 
   int s0, s1;
   sk_span(w, nw, K, group, s0, s1);
+
+  // Epilogue scales are fetched first, so that their latency hides behind
+  // the weight stream: this thread's first output (row, column) scales in
+  // registers, per-group column scales of the tile in LDS.
+  __shared__ float s_gscale[kSkMaxGroups * kSkCols];
+  const int ng = group ? K / group : 0;
+  float pre_rs = 1.f, pre_cs = 0.f;
+  if (tid < M * kSkCols) {
+    const int32_t nn = blockIdx.x * kSkCols + tid % kSkCols;
+    if (nn < N) {
+      if (ASRC == SK_A_I8) pre_rs = row_scale_in[tid / kSkCols];
+      if (!group) pre_cs = col_scale[nn];
+    }
+  }
+  for (int i = tid; i < ng * kSkCols; i += 64 * nw) {
+    const int32_t nn = blockIdx.x * kSkCols + i % kSkCols;
+    s_gscale[i] = nn < N ? col_scale[(int64_t)(i / kSkCols) * sstride + nn] : 0.f;
+  }
 
   i32x4 bw[kSkBatch];
   auto load_b = [&](int st0) {
@@ -227,23 +246,23 @@ skinny_gemm_kernel(const void* __restrict__ a_src, const float* __restrict__ row
   __syncthreads();
 
   // --- epilogue: one thread per output (row m, column n) ------------------------
-  const int ng = group ? K / group : 0;
   for (int t = tid; t < M * kSkCols; t += 64 * nw) {
     const int m = t / kSkCols, nl = t % kSkCols;
     const int32_t nn = blockIdx.x * kSkCols + nl;
     if (nn >= N) continue;
     const int rb = m >> 4, mm = m & 15, src = 16 * (mm >> 2) + nl, v = mm & 3;
-    const float rs = ASRC == SK_A_I8 ? row_scale_in[m] : rsc[m];
+    const bool first = t == tid;
+    const float rs = ASRC == SK_A_I8 ? (first ? pre_rs : row_scale_in[m]) : rsc[m];
     float y;
     if (!group) {
       int32_t tot = 0;
       for (int ww = 0; ww < nw; ++ww) tot += red[(ww * rbl + rb) * 64 + src][v];
       if (dbg) dbg[(int64_t)m * N + nn] = tot;
-      y = mul_rn(mul_rn((float)tot, rs), col_scale[nn]);
+      y = mul_rn(mul_rn((float)tot, rs), first ? pre_cs : col_scale[nn]);
     } else {
       float S = 0.f;
       for (int g = 0; g < ng; ++g)
-        S = add_rn(S, mul_rn((float)red[(g * rbl + rb) * 64 + src][v], col_scale[(int64_t)g * sstride + nn]));
+        S = add_rn(S, mul_rn((float)red[(g * rbl + rb) * 64 + src][v], s_gscale[g * kSkCols + nl]));
       y = mul_rn(S, rs);
     }
     sk_store(so, m, nn, y);
@@ -269,7 +288,7 @@ static SkinnyPlan skinny_plan(int64_t M, int32_t K, int32_t group, bool f16q) {
 
 bool skinny_supported(int64_t M, int32_t K, int32_t group, bool f16q) {
   if (M < 1 || M > 32 || K < 64 || K % 64) return false;
-  if (group && (group % 64 || K % group)) return false;
+  if (group && (group % 64 || K % group || K / group > kSkMaxGroups)) return false;
   if (f16q && K > kSkMaxRowChunks * 64 * 8) return false;
   return skinny_plan(M, K, group, f16q).lds <= kSkLdsLimit;
 }
