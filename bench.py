@@ -34,6 +34,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5033.0        # MI355X dense int8 matrix peak, TOP/s
 N_LAYERS = 32                  # LLaVA-1.5-7B language-model layers
 DECODE_BATCH, CTX0, DECODE_VISITS = 16, 4096, 256
+GQA_VISITS = 8                 # visits per layer in the GQA decode leg
 # hardware-counter summary of the latent attention kernel on this workload
 ATTN_TRAFFIC_SUMMARY = "latent_attn_llava7b_decode_traffic.txt"
 
@@ -47,7 +48,8 @@ def parse():
     ap.add_argument("--mode", choices=["auto", "absorbed", "reconstruct"], default="auto")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without the kernel events")
-    ap.add_argument("--legs", default="decode,prefill", help="comma list of legs to run: decode, prefill")
+    ap.add_argument("--legs", default="decode,prefill,gqa",
+                    help="comma list of legs to run: decode, prefill, gqa (Qwen2-VL-shaped decode)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
                     help="also run a plain device copy of MB megabytes (calibrates memory counters)")
     return ap.parse_args()
@@ -104,15 +106,23 @@ def cpu_threads():
     return int(n)
 
 
-def layer_weights(wl):
+def layer_weights(wl, w_bits=8, w_group=0):
     from paper_2510_16292_amd import prep
     from workloads import gen
     U, s, V = gen.weight_factors(wl)
     L = wl.layer
-    return (U, s, V), prep.prepare_from_svd(U, s, V, L.n_q_heads, L.n_kv_heads, L.head_dim, wl.beta)
+    return (U, s, V), prep.prepare_from_svd(U, s, V, L.n_q_heads, L.n_kv_heads, L.head_dim, wl.beta,
+                                            w_bits, w_group)
 
 
-def bench_decode(args, wl, host_layer):
+def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_name, profile, traffic_summary,
+               compare_forms):
+    """Decode steps of one attention layer: quantize the new tokens, project
+    them (C, Q(C), Q), append, attend over the latent cache.  Steps cycle
+    through n_layers distinct layers (weights and caches) so the working set
+    exceeds the last-level cache; each layer's context grows by one per visit."""
+    import ctypes
+
     import torch
 
     from paper_2510_16292_amd import binding as B
@@ -120,25 +130,28 @@ def bench_decode(args, wl, host_layer):
 
     L = wl.layer
     r, d, nq = L.r, L.d, L.n_q
-    visits = max(-(-args.steps // N_LAYERS), -(-args.warmup // N_LAYERS), 1)
-    cap = CTX0 + visits + 1
+    visits = max(-(-steps // n_layers), -(-warmup // n_layers), 1)
+    cap = ctx0 + visits + 1
     mode = {"auto": B.QSVD_ATTN_AUTO, "absorbed": B.QSVD_ATTN_ABSORBED,
-            "reconstruct": B.QSVD_ATTN_RECONSTRUCT}[args.mode]
-    layers = [B.DeviceLayer(host_layer) for _ in range(N_LAYERS)]
+            "reconstruct": B.QSVD_ATTN_RECONSTRUCT}[mode_name]
+    layers = [B.DeviceLayer(host_layer) for _ in range(n_layers)]
     caches = []
-    for li in range(N_LAYERS):
-        c = B.DeviceCache(B.QSVD_CACHE_F16, DECODE_BATCH, cap, r, [CTX0] * DECODE_BATCH)
-        gen.latent_rows_device(wl, DECODE_BATCH, CTX0, seed=1000 + li, out=c.data)
+    for li in range(n_layers):
+        c = B.DeviceCache(fmt, batch, cap, r, [ctx0] * batch)
+        if fmt == B.QSVD_CACHE_F16:
+            gen.latent_rows_device(wl, batch, ctx0, seed=1000 + li, out=c.data)
+        else:
+            gen.latent_codes_device(wl, batch, ctx0, seed=1000 + li, codes=c.data, scales=c.scale)
         caches.append(c)
-    xs = [torch.from_numpy(gen.decode_activations(wl, t, batch=DECODE_BATCH)).cuda() for t in range(8)]
-    xq = torch.empty((DECODE_BATCH, d), dtype=torch.int8, device="cuda")
-    sx = torch.empty((DECODE_BATCH,), dtype=torch.float32, device="cuda")
-    c_h = torch.empty((DECODE_BATCH, r), dtype=torch.float16, device="cuda")
-    cq = torch.empty((DECODE_BATCH, r), dtype=torch.int8, device="cuda")
-    sc = torch.empty((DECODE_BATCH,), dtype=torch.float32, device="cuda")
-    q = torch.empty((DECODE_BATCH, nq), dtype=torch.float16, device="cuda")
+    xs = [torch.from_numpy(gen.decode_activations(wl, t, batch=batch)).cuda() for t in range(8)]
+    xq = torch.empty((batch, d), dtype=torch.int8, device="cuda")
+    sx = torch.empty((batch,), dtype=torch.float32, device="cuda")
+    c_h = torch.empty((batch, r), dtype=torch.float16, device="cuda")
+    cq = torch.empty((batch, r), dtype=torch.int8, device="cuda")
+    sc = torch.empty((batch,), dtype=torch.float32, device="cuda")
+    q = torch.empty((batch, nq), dtype=torch.float16, device="cuda")
     out = torch.empty_like(q)
-    pws_b = B.qsvd_prefill_workspace_size(layers[0].c, DECODE_BATCH, B.QSVD_OUT_Q)
+    pws_b = B.qsvd_prefill_workspace_size(layers[0].c, batch, B.QSVD_OUT_Q)
     pws = torch.empty((max(pws_b, 1),), dtype=torch.uint8, device="cuda")
     dws_b = max(B.qsvd_decode_workspace_size(layers[0].c, c.c, 1, mode) for c in caches)
     dws = torch.empty((dws_b,), dtype=torch.uint8, device="cuda")
@@ -150,16 +163,17 @@ def bench_decode(args, wl, host_layer):
     xq_p, sx_p, ch_p, cq_p, sc_p, q_p, out_p = P(xq), P(sx), P(c_h), P(cq), P(sc), P(q), P(out)
     pws_p, dws_p = P(pws), P(dws)
     xs_p = [P(x) for x in xs]
-    import ctypes
     lrefs = [ctypes.byref(l.c) for l in layers]
     crefs = [ctypes.byref(c.c) for c in caches]
+    f16 = fmt == B.QSVD_CACHE_F16
 
     def step(i):
-        li = i % N_LAYERS
-        st = lib.qsvd_quantize_act(xs_p[i % 8], DECODE_BATCH, d, d, 8, 1.0, xq_p, sx_p, s)
-        st |= lib.qsvd_lowrank_qkv_prefill(lrefs[li], xq_p, sx_p, DECODE_BATCH, 8, B.QSVD_OUT_Q, ch_p, cq_p, sc_p,
+        li = i % n_layers
+        st = lib.qsvd_quantize_act(xs_p[i % 8], batch, d, d, 8, 1.0, xq_p, sx_p, s)
+        st |= lib.qsvd_lowrank_qkv_prefill(lrefs[li], xq_p, sx_p, batch, 8, B.QSVD_OUT_Q, ch_p, cq_p, sc_p,
                                            q_p, 0, 0, 0, 0, pws_p, pws_b, s)
-        st |= lib.qsvd_latent_cache_append(crefs[li], ch_p, 0, 0, 1, s)
+        st |= lib.qsvd_latent_cache_append(crefs[li], ch_p if f16 else 0, 0 if f16 else cq_p, 0 if f16 else sc_p,
+                                           1, s)
         st |= lib.qsvd_latent_decode_attention(lrefs[li], crefs[li], q_p, 1, mode, 0.0, out_p, dws_p, dws_b, s)
         if st:
             raise B.QsvdError(st, B.last_error())
@@ -167,62 +181,94 @@ def bench_decode(args, wl, host_layer):
     def reset():
         torch.cuda.synchronize()
         for c in caches:
-            c.seq_len.fill_(CTX0)
-            c.c.max_len = CTX0
+            c.seq_len.fill_(ctx0)
+            c.c.max_len = ctx0
         torch.cuda.synchronize()
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         step(i)
     reset()
     # cached tokens each attention launch reads (context after the append)
-    ctx_read = sum(DECODE_BATCH * (CTX0 + 1 + i // N_LAYERS) for i in range(args.steps))
+    ctx_read = sum(batch * (ctx0 + 1 + i // n_layers) for i in range(steps))
     attn_name = "latent_attn" if mode != B.QSVD_ATTN_RECONSTRUCT else "recon"
-    if not args.no_profile:
+    if profile:
         B.profile_reset()
         B.profile_enable(True, attn_name)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(steps):
         step(i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     B.profile_enable(False)
-    ms_step = (t1 - t0) * 1e3 / max(args.steps, 1)
-    res = dict(ms_per_step=ms_step, tokens_per_s=DECODE_BATCH * args.steps / (t1 - t0),
-               mean_context=ctx_read / max(args.steps, 1) / DECODE_BATCH)
-    if not args.no_profile:
+    ms_step = (t1 - t0) * 1e3 / max(steps, 1)
+    res = dict(ms_per_step=ms_step, tokens_per_s=batch * steps / (t1 - t0),
+               mean_context=ctx_read / max(steps, 1) / batch)
+    if profile:
         kms, n = B.profile_read(attn_name)
         B.profile_reset()
         if n:
             avg_s = kms / n * 1e-3
-            bytes_per_launch = ctx_read / args.steps * r * 2
+            row_bytes = r * 2 if f16 else r + 4            # cached latent row (+ fp32 scale)
+            bytes_per_launch = ctx_read / steps * row_bytes
             achieved = bytes_per_launch / avg_s / 1e9
+            traffic = counted_traffic(traffic_summary) if traffic_summary and mode != B.QSVD_ATTN_RECONSTRUCT \
+                else None
             res["attn_kernel_us"] = avg_s * 1e6
-            traffic = counted_traffic(ATTN_TRAFFIC_SUMMARY) if mode != B.QSVD_ATTN_RECONSTRUCT else None
             res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                "frac": round(achieved / HBM_PEAK_GBS, 4),
                                "traffic": None if traffic is None else int(traffic),
                                "kernel": "latent_attn_kernel", "launches": n,
                                "bytes_per_launch": int(bytes_per_launch)}
-    # absorbed vs reconstruct on this layer, attention call alone (a few calls each)
-    forms = {}
-    for name, m in (("absorbed", B.QSVD_ATTN_ABSORBED), ("reconstruct", B.QSVD_ATTN_RECONSTRUCT)):
-        wsb = B.qsvd_decode_workspace_size(layers[0].c, caches[0].c, 1, m)
-        ws = torch.empty((wsb,), dtype=torch.uint8, device="cuda")
-        reps = 3 if m == B.QSVD_ATTN_RECONSTRUCT else 20
-        for _ in range(2):
-            B.check(lib.qsvd_latent_decode_attention(lrefs[0], crefs[0], q_p, 1, m, 0.0, out_p, P(ws), wsb, s))
-        torch.cuda.synchronize()
-        a = time.perf_counter()
-        for _ in range(reps):
-            B.check(lib.qsvd_latent_decode_attention(lrefs[0], crefs[0], q_p, 1, m, 0.0, out_p, P(ws), wsb, s))
-        torch.cuda.synchronize()
-        forms[name] = round((time.perf_counter() - a) * 1e6 / reps, 1)
-        del ws
-    res["attention_form_us"] = forms
+    if compare_forms:
+        # absorbed vs reconstruct on this layer, attention call alone (a few calls each)
+        forms = {}
+        for name, m in (("absorbed", B.QSVD_ATTN_ABSORBED), ("reconstruct", B.QSVD_ATTN_RECONSTRUCT)):
+            wsb = B.qsvd_decode_workspace_size(layers[0].c, caches[0].c, 1, m)
+            ws = torch.empty((wsb,), dtype=torch.uint8, device="cuda")
+            reps = 3 if m == B.QSVD_ATTN_RECONSTRUCT else 20
+            for _ in range(2):
+                B.check(lib.qsvd_latent_decode_attention(lrefs[0], crefs[0], q_p, 1, m, 0.0, out_p, P(ws), wsb, s))
+            torch.cuda.synchronize()
+            a = time.perf_counter()
+            for _ in range(reps):
+                B.check(lib.qsvd_latent_decode_attention(lrefs[0], crefs[0], q_p, 1, m, 0.0, out_p, P(ws), wsb, s))
+            torch.cuda.synchronize()
+            forms[name] = round((time.perf_counter() - a) * 1e6 / reps, 1)
+            del ws
+        res["attention_form_us"] = forms
     del caches, layers
     torch.cuda.empty_cache()
     return res
+
+
+def bench_decode(args, wl, host_layer):
+    from paper_2510_16292_amd import binding as B
+    return run_decode(wl, host_layer, B.QSVD_CACHE_F16, N_LAYERS, DECODE_BATCH, CTX0, args.steps, args.warmup,
+                      args.mode, not args.no_profile, ATTN_TRAFFIC_SUMMARY, True)
+
+
+def bench_decode_gqa(args):
+    """The Qwen2-VL-7B-shaped GQA layer (28/4 heads, r=1024, W4A8 with int4
+    per-group-128 weights, int8 latent cache with per-token scales) at batch 32
+    over 8192 cached tokens, 28 distinct layers."""
+    from paper_2510_16292_amd import binding as B
+    from workloads import configs
+    wl4 = configs.get(4)
+    _, host = layer_weights(wl4, wl4.w_bits, wl4.w_group)
+    steps = wl4.n_layers * GQA_VISITS
+    res = run_decode(wl4, host, B.QSVD_CACHE_I8, wl4.n_layers, wl4.decode_batch, wl4.decode_ctx, steps,
+                     wl4.n_layers, "auto", not args.no_profile, None, False)
+    out = {"value": round(res["tokens_per_s"], 1), "unit": "tokens/s", "ms_per_step": round(res["ms_per_step"], 5),
+           "steps": steps,
+           "workload": f"qwen2-vl-7b-shaped GQA layer decode: batch {wl4.decode_batch}, int8 latent cache r=1024 "
+                       f"with per-token scales, context {wl4.decode_ctx}->{wl4.decode_ctx + GQA_VISITS}, "
+                       f"W4A8 (int4 per-group-128 weights), {wl4.n_layers} rotated layers; tokens/s per layer step",
+           "mean_context": round(res["mean_context"], 1)}
+    if "roofline" in res:
+        out["roofline"] = res["roofline"]
+        out["attn_kernel_us"] = round(res["attn_kernel_us"], 2)
+    return out
 
 
 def bench_prefill(args, wl2, host_layer):
@@ -343,8 +389,12 @@ def main():
     if "prefill" in legs:
         pre = bench_prefill(args, wl2, host_layer)
         print(f"[bench] prefill done: {pre['value']} TOPS", file=sys.stderr, flush=True)
+    gqa = None
+    if "gqa" in legs:
+        gqa = bench_decode_gqa(args)
+        print(f"[bench] gqa decode done: {gqa['ms_per_step']:.4f} ms/step", file=sys.stderr, flush=True)
     if dec is None:
-        print(json.dumps({"prefill": pre}), flush=True)
+        print(json.dumps({k: v for k, v in (("prefill", pre), ("gqa_decode", gqa)) if v is not None}), flush=True)
         return
     line = {
         "metric": METRIC,
@@ -371,6 +421,8 @@ def main():
     }
     if pre is None:
         line.pop("prefill")
+    if gqa is not None:
+        line["gqa_decode"] = gqa
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline_decode(wl3, factors)

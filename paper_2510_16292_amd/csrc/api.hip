@@ -43,6 +43,9 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 int64_t n_total(const qsvd_layer& w) { return (int64_t)(w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim; }
 
+// (sequence, query) rows one attention call takes: the grid's second dimension
+constexpr int64_t kMaxQueryRows = 65535;
+
 qsvd_status check_layer(const qsvd_layer* w) {
   if (!w) return fail(QSVD_ERR_INVALID_ARG, "layer is NULL");
   if (w->d <= 0 || w->r <= 0 || w->n_q_heads <= 0 || w->n_kv_heads <= 0 || w->head_dim <= 0)
@@ -269,11 +272,13 @@ qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void*
 }
 
 size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int32_t q_len, int32_t mode) {
-  if (!w || !c || q_len != 1) return 0;
+  if (!w || !c || q_len < 1) return 0;
   if (c->batch <= 0 || c->capacity <= 0 || w->r <= 0) return 0;
+  if ((int64_t)c->batch * q_len > kMaxQueryRows) return 0;
   const bool abs_ok = absorbed_supported(*w, *c);
-  if (mode == QSVD_ATTN_RECONSTRUCT || (mode == QSVD_ATTN_AUTO && !abs_ok)) return attn_reconstruct_workspace(*w, *c);
-  return attn_absorbed_workspace(*w, *c);
+  if (mode == QSVD_ATTN_RECONSTRUCT || (mode == QSVD_ATTN_AUTO && !abs_ok))
+    return q_len == 1 ? attn_reconstruct_workspace(*w, *c) : 0;
+  return attn_absorbed_workspace(*w, *c, q_len);
 }
 
 qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* c, const void* q, int32_t q_len,
@@ -287,22 +292,27 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
   if (!q || !out) return fail(QSVD_ERR_INVALID_ARG, "NULL q/out");
   if (mode < QSVD_ATTN_AUTO || mode > QSVD_ATTN_RECONSTRUCT) return fail(QSVD_ERR_INVALID_ARG, "unknown mode");
   if (!(sm_scale >= 0.f) || isinf(sm_scale)) return fail(QSVD_ERR_INVALID_ARG, "sm_scale must be finite and >= 0");
-  if (q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "q_len must be 1 (decode)");
-  if (c->max_len < 1) return fail(QSVD_ERR_INVALID_ARG, "cache is empty (max_len 0)");
+  if (q_len < 1) return fail(QSVD_ERR_INVALID_ARG, "q_len must be >= 1");
+  if ((int64_t)c->batch * q_len > kMaxQueryRows)
+    return fail(QSVD_ERR_UNSUPPORTED, "batch * q_len must be at most %d", kMaxQueryRows);
+  if (c->max_len < q_len) return fail(QSVD_ERR_INVALID_ARG, "cache holds %d tokens, fewer than q_len %d", c->max_len, q_len);
   if (w->n_q_heads > 32) return fail(QSVD_ERR_UNSUPPORTED, "at most 32 query heads");
   if (w->head_dim % 32 || w->head_dim > 128) return fail(QSVD_ERR_UNSUPPORTED, "head_dim must be 32, 64, 96 or 128");
   if (c->batch > 64) return fail(QSVD_ERR_UNSUPPORTED, "at most 64 sequences per call");
   if (c->fmt == QSVD_CACHE_I4) return fail(QSVD_ERR_UNSUPPORTED, "int4 cache attention is not implemented");
   if (w->w_group % 64) return fail(QSVD_ERR_UNSUPPORTED, "decode attention needs w_group 0 or a multiple of 64");
-  if (!aligned(q, 16) || !aligned(out, 16)) return fail(QSVD_ERR_UNSUPPORTED, "q/out must be 16-byte aligned");
+  if (!aligned(q, 16) || !aligned(out, 16) || !aligned(w->s_b, 16))
+    return fail(QSVD_ERR_UNSUPPORTED, "q, out and s_b must be 16-byte aligned");
   const bool abs_ok = absorbed_supported(*w, *c);
   if (mode == QSVD_ATTN_ABSORBED && !abs_ok) return fail(QSVD_ERR_UNSUPPORTED, "absorbed form needs r in {128, 512, 1024, 1536}");
   const bool absorbed = mode == QSVD_ATTN_ABSORBED || (mode == QSVD_ATTN_AUTO && abs_ok);
   if (!absorbed && c->capacity > 16384)
     return fail(QSVD_ERR_UNSUPPORTED, "reconstruct form supports capacity <= 16384");
-  const size_t need = absorbed ? attn_absorbed_workspace(*w, *c) : attn_reconstruct_workspace(*w, *c);
+  if (!absorbed && q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form takes q_len 1 only");
+  const size_t need = absorbed ? attn_absorbed_workspace(*w, *c, q_len) : attn_reconstruct_workspace(*w, *c);
   if (!ws || ws_bytes < need) return fail(QSVD_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-  AttnArgs a{w, c, (const _Float16*)q, (_Float16*)out, sm_scale > 0.f ? sm_scale : 1.f / sqrtf((float)w->head_dim)};
+  AttnArgs a{w, c, (const _Float16*)q, (_Float16*)out, sm_scale > 0.f ? sm_scale : 1.f / sqrtf((float)w->head_dim),
+             q_len};
   hipStream_t s = (hipStream_t)stream;
   return hip_status(absorbed ? launch_attn_absorbed(a, ws, s) : launch_attn_reconstruct(a, ws, s), "decode attention");
 }

@@ -43,8 +43,9 @@ __device__ __forceinline__ float wscale(const float* sb, int32_t N, int32_t n, i
 // ---------------------------------------------------------------------------
 // q~ = scale * q W^u_k^T on the 16x16x32 fp16 matrix cores.  One wave per
 // (head h, 64 latent columns j): the dh x 64 block of W^u_k codes (rows
-// c = key channel, contiguous in j) is staged in LDS as fp16 with its scale
-// folded in; the MFMA needs 8 consecutive c of one column j per lane, which
+// c = key channel, contiguous in j) is staged in LDS as exact fp16 codes, and
+// the channel scales multiply the query, which enters as an fp16 hi/lo pair
+// (two MFMAs, about fp32 accuracy); the MFMA needs 8 consecutive c of one column j per lane, which
 // two LDS transpose reads deliver (lane s of each 16-lane group addresses row
 // base + s/4 at columns 4*(s%4)..+3 and receives 4 rows of one column).  Rows
 // of the product are 16 sequences (query rows loaded straight from memory),
@@ -69,18 +70,20 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
   }
   const int g = (h * Hkv) / Hq;
   const int32_t nk0 = Hq * dh + g * dh;
+  // The weight scale of key channel c (per channel, or of this block's group:
+  // a 64-column block never straddles a group) multiplies the query, not the
+  // staged codes, which stay exact in fp16.
+  const float* srow = sb + (group ? (int64_t)(jb / group) * N : 0) + nk0;
   // stage: chunk e -> row c = e / 4, 16 codes at columns 16 * (e % 4); every
   // lane's loads (dh <= 128: at most 8 chunks) go out before any is used
   constexpr int kStageIt = 128 * 4 / 64;
   uint4 raw[kStageIt];
-  float sc[kStageIt];
 #pragma unroll
   for (int it = 0; it < kStageIt; ++it) {
     const int e = lane + 64 * it;
     if (e >= dh * 4) break;
     const int c = e >> 2, j16 = (e & 3) * 16;
     const int32_t n = nk0 + c;
-    sc[it] = group ? sb[(int64_t)(jb / group) * N + n] : sb[n];
     if (bits == 8) {
       raw[it] = *reinterpret_cast<const uint4*>(bt + (int64_t)n * r + jb + j16);
     } else {
@@ -89,13 +92,21 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
     }
   }
   const int l16 = lane & 15, quad = lane >> 4;
-  // query rows of the first 16 sequences, loaded while the weights arrive
-  f16x8 qa[128 / 32];
+  // this lane's contraction channels c = 32k + 8*quad + e: their scales, and
+  // the query rows of the first 16 sequences, loaded while the weights arrive
+  constexpr int KC = 128 / 32;
+  f32x4 sc4[KC][2];
+#pragma unroll
+  for (int k = 0; k < KC; ++k)
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+      sc4[k][hh] = 32 * k < dh ? *reinterpret_cast<const f32x4*>(srow + 32 * k + 8 * quad + 4 * hh) : f32x4{};
+  f16x8 qa[KC];
   {
     const int bA = l16;
     const _Float16* qrow = q + (int64_t)min(bA, B - 1) * Hq * dh + h * dh + 8 * quad;
 #pragma unroll
-    for (int k = 0; k < 128 / 32; ++k) qa[k] = (32 * k < dh && bA < B) ? *reinterpret_cast<const f16x8*>(qrow + 32 * k) : f16x8{};
+    for (int k = 0; k < KC; ++k) qa[k] = (32 * k < dh && bA < B) ? *reinterpret_cast<const f16x8*>(qrow + 32 * k) : f16x8{};
   }
 #pragma unroll
   for (int it = 0; it < kStageIt; ++it) {
@@ -107,14 +118,14 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
       const uint32_t wv[4] = {raw[it].x, raw[it].y, raw[it].z, raw[it].w};
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        lo[k] = (_Float16)((float)(int8_t)(wv[k >> 2] >> (8 * (k & 3))) * sc[it]);
-        hi[k] = (_Float16)((float)(int8_t)(wv[2 + (k >> 2)] >> (8 * (k & 3))) * sc[it]);
+        lo[k] = (_Float16)(float)(int8_t)(wv[k >> 2] >> (8 * (k & 3)));
+        hi[k] = (_Float16)(float)(int8_t)(wv[2 + (k >> 2)] >> (8 * (k & 3)));
       }
     } else {
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        lo[k] = (_Float16)((float)(((int)(raw[it].x << (28 - 4 * k))) >> 28) * sc[it]);
-        hi[k] = (_Float16)((float)(((int)(raw[it].y << (28 - 4 * k))) >> 28) * sc[it]);
+        lo[k] = (_Float16)(float)(((int)(raw[it].x << (28 - 4 * k))) >> 28);
+        hi[k] = (_Float16)(float)(((int)(raw[it].y << (28 - 4 * k))) >> 28);
       }
     }
     *reinterpret_cast<f16x8*>(&wk[c * kAbsorbLd + j16]) = lo;
@@ -131,11 +142,20 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
 #pragma unroll
     for (int jj = 0; jj < kAbsorbJ / 16; ++jj) acc[jj] = f32x4{};
 #pragma unroll
-    for (int k = 0; k < 128 / 32; ++k) {
+    for (int k = 0; k < KC; ++k) {
       const int c0 = 32 * k;
       if (c0 >= dh) break;
       f16x8 a = b0 == 0 ? qa[k] : *reinterpret_cast<const f16x8*>(qrow + c0);
       if (bA >= B) a = f16x8{};
+      // scaled query q_c * s_c as an fp16 pair hi + lo (the product of two
+      // fp16 MFMAs then carries it to about fp32 accuracy)
+      f16x8 ahi, alo;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = (float)a[e] * sc4[k][e >> 2][e & 3];
+        ahi[e] = (_Float16)x;
+        alo[e] = (_Float16)(x - (float)ahi[e]);
+      }
 #pragma unroll
       for (int jj = 0; jj < kAbsorbJ / 16; ++jj) {
         const int row = c0 + 8 * quad + (s16 >> 2);
@@ -144,7 +164,8 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
         const s16x4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)&wk[(row + 4) * kAbsorbLd + col]);
         const f16x4 f0 = __builtin_bit_cast(f16x4, x0), f1 = __builtin_bit_cast(f16x4, x1);
         const f16x8 bw = {f0[0], f0[1], f0[2], f0[3], f1[0], f1[1], f1[2], f1[3]};
-        acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc[jj], 0, 0, 0);
+        acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ahi, bw, acc[jj], 0, 0, 0);
+        acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(alo, bw, acc[jj], 0, 0, 0);
       }
     }
     // lane holds column jb + 16*jj + l16 and sequences b0 + 4*quad + v
@@ -174,7 +195,7 @@ template <int RW, int NW, int FMT>
 __global__ void __launch_bounds__(NW * 64)
 latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ cdata,
                    const float* __restrict__ cscale, const int32_t* __restrict__ seq_len,
-                   int32_t capacity, int32_t r, int32_t chunk, int32_t n_chunks,
+                   int32_t capacity, int32_t r, int32_t chunk, int32_t n_chunks, int32_t q_len,
                    _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
   constexpr int KS = RW / 16;    // 16-wide contraction steps of the score MFMA
   constexpr int RB = RW / 32;    // 32-row blocks of the output MFMA
@@ -191,53 +212,77 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   f32x4* spart4 = reinterpret_cast<f32x4*>(smem + NW * 32 * CST * 2);
   f32x4* ssum4 = spart4 + NW * 256;
 
-  const int b = blockIdx.y, ch = blockIdx.x;
-  const int L = min(seq_len[b], capacity);
+  // Workgroup row blockIdx.y is query i of sequence b (q_len queries per
+  // sequence, the last q_len cached positions): it sees positions
+  // [0, L - q_len + i], causally.  Decode has q_len = 1.
+  const int vb = blockIdx.y, ch = blockIdx.x;
+  const int b = vb / q_len, qi = vb - b * q_len;
+  const int L = min(seq_len[b], capacity) - (q_len - 1 - qi);
   const int t_begin = ch * chunk;
   if (t_begin >= L) return;
   const int t_end = min(L, t_begin + chunk);
   const int slice0 = w * RW;
 
+  // Contraction slots of the score MFMA: in step ks, lane (l32, half) feeds
+  // token t0 + l32 at latent columns slice0 + kcol(ks, half) .. +7.  fp16 rows
+  // come 8 columns (16 bytes) per load; int8 rows 16 columns per load, which
+  // serve steps 2k and 2k + 1.  The query slots follow the same map.
+  constexpr bool F16C = FMT == QSVD_CACHE_F16;
+  auto kcol = [](int ks, int hf) { return F16C ? 16 * ks + 8 * hf : 32 * (ks >> 1) + 16 * hf + 8 * (ks & 1); };
   f16x8 qf[KS];
   {
-    const _Float16* qrow = qt + ((int64_t)b * kHeadBlk + l32) * r + slice0 + 8 * half;
+    const _Float16* qrow = qt + ((int64_t)vb * kHeadBlk + l32) * r + slice0;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + 16 * ks);
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, half));
   }
   f32x16 o[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) o[rb] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  // A operand of the score MFMA: token (t0 + l32), latent columns 8*half + 16*ks.
-  // Raw tile registers: fp16 rows as they are, int8 rows as 8-byte chunks.
-  using RawT = typename std::conditional<FMT == QSVD_CACHE_F16, f16x8, uint2>::type;
-  RawT raw[KS];
+  // Raw tile registers: fp16 rows as they are, int8 rows as 16-byte chunks;
+  // for int8 also the per-token scales of the 16 tokens whose scores and
+  // probabilities this lane holds (t0 + 8*(v/4) + 4*half + v%4).
+  constexpr int NLD = F16C ? KS : KS / 2;
+  using RawT = typename std::conditional<F16C, f16x8, uint4>::type;
+  RawT raw[NLD];
+  float sc_next[F16C ? 1 : 16], sc_cur[F16C ? 1 : 16];
   auto load_tile = [&](int t0) {
+    if constexpr (!F16C) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
+        sc_next[v] = cscale[(int64_t)b * capacity + min(t, L - 1)];
+      }
+    }
     // rows past the chunk end are masked; re-read the last row instead of
     // fetching the next chunk's rows
     const int tk = min(t0 + l32, t_end - 1);
-    const int64_t off = ((int64_t)b * capacity + tk) * r + slice0 + 8 * half;
+    const int64_t off = ((int64_t)b * capacity + tk) * r + slice0;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (FMT == QSVD_CACHE_F16)
-        raw[ks] = *reinterpret_cast<const RawT*>(reinterpret_cast<const _Float16*>(cdata) + off + 16 * ks);
+    for (int i = 0; i < NLD; ++i) {
+      if constexpr (F16C)
+        raw[i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const _Float16*>(cdata) + off + kcol(i, half));
       else
-        raw[ks] = *reinterpret_cast<const RawT*>(reinterpret_cast<const int8_t*>(cdata) + off + 16 * ks);
+        raw[i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const int8_t*>(cdata) + off + kcol(2 * i, half));
     }
   };
   load_tile(t_begin);
   for (int t0 = t_begin; t0 < t_end; t0 += 32) {
     f16x8 cf[KS];
+    if constexpr (F16C) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if constexpr (FMT == QSVD_CACHE_F16) {
-        cf[ks] = raw[ks];
-      } else {
+      for (int ks = 0; ks < KS; ++ks) cf[ks] = raw[ks];
+    } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          cf[ks][e] = (_Float16)(float)(int8_t)(raw[ks].x >> (8 * e));
-          cf[ks][4 + e] = (_Float16)(float)(int8_t)(raw[ks].y >> (8 * e));
+      for (int v = 0; v < 16; ++v) sc_cur[v] = sc_next[v];
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        const uint32_t wv[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          cf[2 * i][e] = (_Float16)(float)(int8_t)(wv[e >> 2] >> (8 * (e & 3)));
+          cf[2 * i + 1][e] = (_Float16)(float)(int8_t)(wv[2 + (e >> 2)] >> (8 * (e & 3)));
         }
       }
     }
@@ -247,7 +292,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_f16(cf[ks], qf[ks], sacc, 0, 0, 0);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      *reinterpret_cast<f16x8*>(cst + l32 * CST + 16 * ks + 8 * half) = cf[ks];
+      *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(ks, half)) = cf[ks];
     // The next tile streams in while this one is reduced, normalized and
     // multiplied into the output.
     if (t0 + 32 < t_end) load_tile(t0 + 32);
@@ -268,7 +313,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     for (int v = 0; v < 16; ++v) {
       const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
       float x = ssum4[(v >> 2) * 64 + lane][v & 3];
-      if (FMT != QSVD_CACHE_F16) x *= cscale[(int64_t)b * capacity + min(t, L - 1)];
+      if constexpr (!F16C) x *= sc_cur[v];
       s[v] = (t < t_end) ? x : -INFINITY;
     }
     float mx = s[0];
@@ -307,10 +352,8 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float pv = p[8 * mf + e];
-        if (FMT != QSVD_CACHE_F16) {
-          const int t = t0 + 16 * mf + 8 * (e >> 2) + 4 * half + (e & 3);
-          pv *= cscale[(int64_t)b * capacity + min(t, L - 1)];
-        }
+        // token 16*mf + 8*(e/4) + 4*half + e%4 is score slot v = 8*mf + e
+        if constexpr (!F16C) pv *= sc_cur[8 * mf + e];
         pf[mf][e] = (_Float16)pv;
       }
     // A operand of the output MFMA: lane l needs column rb*32 + l32 of the
@@ -338,7 +381,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
       }
   }
 
-  const int64_t part = (int64_t)b * n_chunks + ch;
+  const int64_t part = (int64_t)vb * n_chunks + ch;
   if (w == 0 && lane < 32) {
     ml_part[part * 64 + l32] = m_run;
     ml_part[part * 64 + 32 + l32] = l_run;
@@ -375,11 +418,11 @@ constexpr int kMergeBatch = 8;
 
 __global__ void __launch_bounds__(256)
 merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict__ ml_part,
-                    const int32_t* __restrict__ seq_len, int32_t chunk, int32_t n_chunks, int32_t n_launched,
-                    int32_t r, _Float16* __restrict__ o_lat) {
+                    const int32_t* __restrict__ seq_len, int32_t capacity, int32_t chunk, int32_t n_chunks,
+                    int32_t n_launched, int32_t q_len, int32_t r, _Float16* __restrict__ o_lat) {
   __shared__ float wgt[kMaxChunks * kHeadBlk];
-  const int b = blockIdx.y, tid = threadIdx.x;
-  const int L = seq_len[b];
+  const int b = blockIdx.y, tid = threadIdx.x;      // b: (sequence, query) row as in the attention
+  const int L = min(seq_len[b / q_len], capacity) - (q_len - 1 - b % q_len);
   const int nv = L > 0 ? min(min((L + chunk - 1) / chunk, n_launched), kMaxChunks) : 0;
   const int64_t pb = (int64_t)b * n_chunks;
   // element e8 (8 halves): latent quad x4 = e8 / 16, heads 2*(e8 % 16) and +1;
@@ -617,19 +660,20 @@ static bool pick_slice(int r, int* rw, int* nw) {
   return false;
 }
 
-static AbsorbPlan plan_absorbed(const qsvd_layer& w, const qsvd_cache& c) {
+static AbsorbPlan plan_absorbed(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len) {
   AbsorbPlan p{};
   pick_slice(w.r, &p.rw, &p.nw);
-  p.n0 = target_chunks(c.batch);
+  const int64_t rows = (int64_t)c.batch * q_len;      // one query row block per (sequence, query)
+  p.n0 = target_chunks((int)rows);
   const int len = c.max_len > 0 ? c.max_len : 1;
   int ch = (len + p.n0 - 1) / p.n0;
   ch = ((ch + 15) / 16) * 16;
   p.chunk = ch;
   p.n_chunks = (len + ch - 1) / ch;
-  p.qt_bytes = (size_t)c.batch * kHeadBlk * w.r * sizeof(_Float16);
-  p.opart_bytes = (size_t)c.batch * p.n0 * w.r * kHeadBlk * sizeof(_Float16);
-  p.ml_bytes = (size_t)c.batch * p.n0 * 64 * sizeof(float);
-  p.olat_bytes = (size_t)c.batch * kHeadBlk * w.r * sizeof(_Float16);
+  p.qt_bytes = (size_t)rows * kHeadBlk * w.r * sizeof(_Float16);
+  p.opart_bytes = (size_t)rows * p.n0 * w.r * kHeadBlk * sizeof(_Float16);
+  p.ml_bytes = (size_t)rows * p.n0 * 64 * sizeof(float);
+  p.olat_bytes = (size_t)rows * kHeadBlk * w.r * sizeof(_Float16);
   return p;
 }
 
@@ -640,38 +684,39 @@ bool absorbed_supported(const qsvd_layer& w, const qsvd_cache& c) {
   return pick_slice(w.r, &rw, &nw) && c.fmt != QSVD_CACHE_I4;
 }
 
-size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c) {
-  const AbsorbPlan p = plan_absorbed(w, c);
+size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len) {
+  const AbsorbPlan p = plan_absorbed(w, c, q_len);
   return align256(p.qt_bytes) + align256(p.opart_bytes) + align256(p.ml_bytes) + align256(p.olat_bytes);
 }
 
 template <int RW, int NW, int FMT>
-static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, const _Float16* qt,
+static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, int32_t q_len, const _Float16* qt,
                                 _Float16* opart, float* ml, hipStream_t s) {
   const size_t lds = (size_t)NW * 32 * (RW + 16) * 2 + (size_t)(NW + 1) * 1024 * 4;
   auto kern = latent_attn_kernel<RW, NW, FMT>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   KernelScope ks("latent_attn", s);
-  QSVD_LAUNCH(ks, kern, dim3(p.n_chunks, c.batch), dim3(NW * 64), lds, s, qt,
+  QSVD_LAUNCH(ks, kern, dim3(p.n_chunks, c.batch * q_len), dim3(NW * 64), lds, s, qt,
                      (const uint8_t*)c.data, c.scale, c.seq_len, c.capacity, c.r, p.chunk,
-                     p.n0, opart, ml);
+                     p.n0, q_len, opart, ml);
   return hipGetLastError();
 }
 
 template <int FMT>
-static hipError_t dispatch_latent(const AbsorbPlan& p, const qsvd_cache& c, const _Float16* qt,
+static hipError_t dispatch_latent(const AbsorbPlan& p, const qsvd_cache& c, int32_t q_len, const _Float16* qt,
                                   _Float16* opart, float* ml, hipStream_t s) {
-  if (p.rw == 192) return launch_latent<192, 8, FMT>(p, c, qt, opart, ml, s);
-  if (p.rw == 128) return launch_latent<128, 8, FMT>(p, c, qt, opart, ml, s);
-  if (p.rw == 64) return launch_latent<64, 8, FMT>(p, c, qt, opart, ml, s);
-  return launch_latent<32, 4, FMT>(p, c, qt, opart, ml, s);
+  if (p.rw == 192) return launch_latent<192, 8, FMT>(p, c, q_len, qt, opart, ml, s);
+  if (p.rw == 128) return launch_latent<128, 8, FMT>(p, c, q_len, qt, opart, ml, s);
+  if (p.rw == 64) return launch_latent<64, 8, FMT>(p, c, q_len, qt, opart, ml, s);
+  return launch_latent<32, 4, FMT>(p, c, q_len, qt, opart, ml, s);
 }
 
 hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   const qsvd_layer& w = *a.w;
   const qsvd_cache& c = *a.c;
-  const AbsorbPlan p = plan_absorbed(w, c);
+  const AbsorbPlan p = plan_absorbed(w, c, a.q_len);
+  const int32_t rows = c.batch * a.q_len;     // (sequence, query) rows, sequence-major
   uint8_t* base = (uint8_t*)ws;
   _Float16* qt = (_Float16*)base;
   base += align256(p.qt_bytes);
@@ -684,23 +729,24 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   {
     KernelScope ks("absorb_q", s);
     QSVD_LAUNCH(ks, absorb_kernel, dim3(kHeadBlk, w.r / kAbsorbJ), dim3(64), 0, s, a.q,
-                       (const uint8_t*)w.b_t, w.s_b, c.batch, w.r, w.n_q_heads, w.n_kv_heads,
+                       (const uint8_t*)w.b_t, w.s_b, rows, w.r, w.n_q_heads, w.n_kv_heads,
                        w.head_dim, N, w.w_bits, w.w_group, a.sm_scale * kLog2e, qt);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = (c.fmt == QSVD_CACHE_F16) ? dispatch_latent<QSVD_CACHE_F16>(p, c, qt, opart, ml, s)
-                                : dispatch_latent<QSVD_CACHE_I8>(p, c, qt, opart, ml, s);
+  e = (c.fmt == QSVD_CACHE_F16) ? dispatch_latent<QSVD_CACHE_F16>(p, c, a.q_len, qt, opart, ml, s)
+                                : dispatch_latent<QSVD_CACHE_I8>(p, c, a.q_len, qt, opart, ml, s);
   if (e != hipSuccess) return e;
   {
     KernelScope ks("merge_latent", s);
-    QSVD_LAUNCH(ks, merge_latent_kernel, dim3((w.r * kHeadBlk + kMergeElems - 1) / kMergeElems, c.batch),
-                       dim3(256), 0, s, opart, ml, c.seq_len, p.chunk, p.n0, p.n_chunks, w.r, olat);
+    QSVD_LAUNCH(ks, merge_latent_kernel, dim3((w.r * kHeadBlk + kMergeElems - 1) / kMergeElems, rows),
+                       dim3(256), 0, s, opart, ml, c.seq_len, c.capacity, p.chunk, p.n0, p.n_chunks, a.q_len, w.r,
+                       olat);
   }
   {
     KernelScope ks("vproj", s);
     QSVD_LAUNCH(ks, vproj_kernel, dim3(w.n_q_heads, w.head_dim / 16), dim3(64 * kVprojWaves), 0, s, olat,
-                       (const uint8_t*)w.b_t, w.s_b, c.batch, w.r, w.n_q_heads, w.n_kv_heads, w.head_dim, N,
+                       (const uint8_t*)w.b_t, w.s_b, rows, w.r, w.n_q_heads, w.n_kv_heads, w.head_dim, N,
                        w.w_bits, w.w_group, a.out);
   }
   return hipGetLastError();

@@ -72,11 +72,12 @@ hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void*
 struct AttnArgs {
   const qsvd_layer* w;
   const qsvd_cache* c;
-  const _Float16* q;
-  _Float16* out;
+  const _Float16* q;      // [batch][q_len][Hq * head_dim]
+  _Float16* out;          // same layout
   float sm_scale;
+  int32_t q_len;          // queries per sequence: the last q_len cached positions, causal among them
 };
-size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c);
+size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len);
 hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s);
 size_t attn_reconstruct_workspace(const qsvd_layer& w, const qsvd_cache& c);
 hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s);

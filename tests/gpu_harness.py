@@ -90,12 +90,13 @@ class Prefill:
         return out
 
 
-def decode_attention(dl, dc, q_dev, mode, sm_scale=0.0):
+def decode_attention(dl, dc, q_dev, mode, sm_scale=0.0, q_len=1):
+    """q_dev: [batch, q_len, Hq*head_dim] (or [batch, Hq*head_dim] for q_len 1)."""
     t = torch()
     out = t.empty_like(q_dev)
-    ws_bytes = B.qsvd_decode_workspace_size(dl.c, dc.c, 1, mode)
+    ws_bytes = B.qsvd_decode_workspace_size(dl.c, dc.c, q_len, mode)
     ws = t.empty((max(ws_bytes, 1),), dtype=t.uint8, device="cuda")
-    B.check(B.qsvd_latent_decode_attention(dl.c, dc.c, B.ptr(q_dev), 1, mode, sm_scale, B.ptr(out), B.ptr(ws),
+    B.check(B.qsvd_latent_decode_attention(dl.c, dc.c, B.ptr(q_dev), q_len, mode, sm_scale, B.ptr(out), B.ptr(ws),
                                            ws_bytes, B.stream_handle()))
     return out
 

@@ -166,7 +166,10 @@ def _decode(layer, cache, q_len=1, mode=0, sm=0.0, ws=FAKE, ws_bytes=1 << 40, q=
 
 def test_decode_validation(lib):
     L, C = layer_struct(), cache_struct()
-    assert _decode(L, C, q_len=2) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode(L, C, q_len=0) == B.QSVD_ERR_INVALID_ARG
+    assert _decode(L, C, q_len=11) == B.QSVD_ERR_INVALID_ARG                  # more queries than cached tokens
+    assert _decode(L, C, q_len=2, mode=B.QSVD_ATTN_RECONSTRUCT) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode(L, cache_struct(batch=64, max_len=2000, capacity=4096), q_len=1025) == B.QSVD_ERR_UNSUPPORTED
     assert _decode(L, C, mode=3) == B.QSVD_ERR_INVALID_ARG
     assert _decode(L, C, sm=-1.0) == B.QSVD_ERR_INVALID_ARG
     assert _decode(L, C, q=0) == B.QSVD_ERR_INVALID_ARG
@@ -182,7 +185,12 @@ def test_decode_validation(lib):
     assert _decode(L, C, mode=B.QSVD_ATTN_ABSORBED, ws_bytes=need - 1) == B.QSVD_ERR_WORKSPACE
     need_r = B.qsvd_decode_workspace_size(L, C, 1, B.QSVD_ATTN_RECONSTRUCT)
     assert _decode(L, C, mode=B.QSVD_ATTN_RECONSTRUCT, ws_bytes=need_r - 1) == B.QSVD_ERR_WORKSPACE
-    assert B.qsvd_decode_workspace_size(L, C, 2, 0) == 0
+    assert B.qsvd_decode_workspace_size(L, C, 2, B.QSVD_ATTN_RECONSTRUCT) == 0
+    assert B.qsvd_decode_workspace_size(L, C, 0, 0) == 0
+    # q_len > 1 (absorbed): one query row block per (sequence, query)
+    need2 = B.qsvd_decode_workspace_size(L, C, 2, B.QSVD_ATTN_ABSORBED)
+    assert need2 >= need
+    assert _decode(L, C, q_len=2, mode=B.QSVD_ATTN_ABSORBED, ws_bytes=need2 - 1) == B.QSVD_ERR_WORKSPACE
 
 
 def test_decode_workspace_sizes_cover_growth(lib):

@@ -376,3 +376,94 @@ def test_decode_qwen2vl_w4a8_int8_cache_full_size(qwen):
         ok, info = H.close_enough(out[b:b + 1], ref["out"])
         H.say(f"  b={b} max-abs, rel-L2, rms = {info}")
         assert ok, (b, info)
+
+
+# ------------------------------------------------------------------ prefill attention (q_len > 1)
+
+def test_prefill_attention_tiny_causal(tiny):
+    """The tiny layer's 64 prefill tokens attend causally over their own latent
+    rows (queries = the last q_len = 64 cached positions), absorbed form,
+    against the plain definition."""
+    wl, ol, dl = tiny
+    X = gen.prefill_activations(wl)
+    M, nq = X.shape[0], wl.layer.n_q
+    ref_proj = O.prefill(ol, X, 8)
+    oc = O.LatentCache(O.CACHE_F16, 1, M, wl.layer.r)
+    O.cache_append_prefill(oc, ref_proj, [M])
+    ref = O.attention_reference(ol, oc, ref_proj["Q"].reshape(1, M, nq), M)
+    dc = B.DeviceCache(B.QSVD_CACHE_F16, 1, M, wl.layer.r, [0])
+    H.say("prefill attention tiny q_len=64")
+    p = H.Prefill(dl, M, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(X))
+    H.append(dc, p.c_h, n_new=M)
+    assert np.array_equal(H.host(p.q).view(np.uint16), ref_proj["Q"].view(np.uint16))
+    out = H.host(H.decode_attention(dl, dc, p.q.reshape(1, M, nq), B.QSVD_ATTN_ABSORBED, q_len=M))
+    ok, info = H.close_enough(out, ref)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+    # the last query row is the decode query at the same position
+    out1 = H.host(H.decode_attention(dl, dc, p.q[M - 1:], B.QSVD_ATTN_ABSORBED))
+    ok, info = H.close_enough(out1[0], ref[0, M - 1])
+    assert ok, info
+
+
+def test_prefill_attention_gqa_int8_ragged(gqa):
+    """Five new tokens per sequence (projected together, 15 rows) appended to
+    int8 caches of ragged prior lengths 0 / 40 / 100, then attended causally
+    with q_len = 5: grouped queries (8 over 2), absorbed form."""
+    L, ol, dl = gqa
+    prior, q_len, batch = [0, 40, 100], 5, 3
+    cap = max(prior) + q_len
+    wl = configs.Workload(95, "gqa-test", L, "gaussian", 8, 0, 8, configs.CACHE_I8)
+    codes, scales = gen.latent_codes(wl, batch, cap)
+    oc = O.LatentCache(O.CACHE_I8, batch, cap, L.r)
+    dc = B.DeviceCache(B.QSVD_CACHE_I8, batch, cap, L.r, prior)
+    for b, n in enumerate(prior):
+        if n:
+            oc.append(b, None, codes[b, :n], scales[b, :n])
+    dc.data.copy_(H.dev(np.where(np.arange(cap)[None, :, None] < np.array(prior)[:, None, None], codes, 0)))
+    dc.scale.copy_(H.dev(np.where(np.arange(cap)[None, :] < np.array(prior)[:, None], scales, 0)))
+    X = gen.decode_activations(wl, 7, batch=batch * q_len)
+    ref_proj = O.prefill(ol, X, 8)
+    for b in range(batch):
+        rows = slice(b * q_len, (b + 1) * q_len)
+        oc.append(b, None, ref_proj["cq"][rows], ref_proj["sc"][rows])
+    nq = L.n_q_heads * L.head_dim
+    ref = O.attention_reference(ol, oc, ref_proj["Q"].reshape(batch, q_len, nq), q_len)
+    H.say("prefill attention gqa int8 ragged q_len=5")
+    p = H.Prefill(dl, batch * q_len, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(X))
+    H.append(dc, cq=p.cq, sc=p.sc, n_new=q_len)
+    assert np.array_equal(H.host(dc.data), oc.data)
+    out = H.host(H.decode_attention(dl, dc, p.q.reshape(batch, q_len, nq), B.QSVD_ATTN_AUTO, q_len=q_len))
+    ok, info = H.close_enough(out, ref)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+
+
+def test_prefill_attention_llava7b_chunked(llava):
+    """LLaVA-shaped layer (r = 1536): four new tokens per sequence on top of
+    fp16 caches of 300 / 1000 tokens, q_len = 4, several context chunks per
+    query row; three query rows checked against the plain definition."""
+    wl, ol, dl = llava
+    L = wl.layer
+    prior, q_len, batch = [300, 1000], 4, 2
+    cap = max(prior) + q_len
+    rows = gen.latent_rows(wl, batch, cap)
+    oc = O.LatentCache(O.CACHE_F16, batch, cap, L.r)
+    dc = B.DeviceCache(B.QSVD_CACHE_F16, batch, cap, L.r, prior)
+    for b, n in enumerate(prior):
+        oc.append(b, rows[b, :n])
+    dc.data.copy_(H.dev(np.where(np.arange(cap)[None, :, None] < np.array(prior)[:, None, None], rows, 0)))
+    X = gen.decode_activations(wl, 3, batch=batch * q_len)
+    ref_proj = O.prefill(ol, X, 8)
+    for b in range(batch):
+        oc.append(b, ref_proj["C_h"][b * q_len:(b + 1) * q_len])
+    H.say("prefill attention llava7b q_len=4")
+    p = H.Prefill(dl, batch * q_len, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(X))
+    H.append(dc, p.c_h, n_new=q_len)
+    nq = L.n_q
+    out = H.host(H.decode_attention(dl, dc, p.q.reshape(batch, q_len, nq), B.QSVD_ATTN_ABSORBED, q_len=q_len))
+    for b, i in ((0, 0), (1, 3), (1, 1)):
+        ref = O.attention_reference(ol, oc, ref_proj["Q"].reshape(batch, q_len, nq), q_len, batches=[b])
+        ok, info = H.close_enough(out[b, i], ref[b, i])
+        H.say(f"  b={b} i={i} max-abs, rel-L2, rms = {info}")
+        assert ok, (b, i, info)

@@ -143,3 +143,23 @@ def latent_rows_device(wl: Workload, batch: int, length: int, seed: int, out=Non
     for b in range(batch):
         out[b, :length] = (torch.randn((length, r), generator=g, device=device) * std_t).to(torch.float16)
     return out
+
+
+def latent_codes_device(wl: Workload, batch: int, length: int, seed: int, codes=None, scales=None, device="cuda"):
+    """Device-side variant of :func:`latent_codes` for large pre-filled int8
+    caches (torch's seeded generator on the GPU): writes codes into
+    ``codes[:, :length]`` (int8 [batch, >=length, r]) and per-token scales into
+    ``scales[:, :length]``."""
+    import torch
+    r = wl.layer.r
+    std = np.sqrt(spectrum(wl)[:r]) if wl.spectrum == "decay" else np.ones(r)
+    col = torch.tensor(40.0 * std / std[0], dtype=torch.float32, device=device)
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    for b in range(batch):
+        z = torch.randn((length, r), generator=g, device=device) * col
+        c = torch.clamp(torch.round(z), -127, 127).to(torch.int8)
+        c[:, 0] = 127
+        codes[b, :length] = c
+        u = torch.rand((length,), generator=g, device=device) * 0.45 + 0.8
+        scales[b, :length] = u * float(std[0] / 40.0)
