@@ -119,8 +119,13 @@ qsvd_status qsvd_quantize_act(const void* x, int64_t M, int32_t K, int64_t ldx, 
  *            matching QSVD_OUT_* bit is set (others may be NULL)
  *   dbg_acc_xa, dbg_acc_cb  optional device int32 [M][r] and [M][N] copies of
  *            the integer accumulators (w_group 0 only; NULL to skip)
- *   ws       device workspace of at least qsvd_prefill_workspace_size() bytes
- * Requires d % 64 == 0, r % 64 == 0, act_bits 8 (4 with w_bits 4). */
+ *   ws       unused (qsvd_prefill_workspace_size() returns 0; kept for callers
+ *            that size one anyway)
+ * Requires d % 64 == 0, r % 64 == 0, act_bits 8, 16-byte aligned xq, c_h, cq and
+ * weight codes.  M <= 32 (decode sizes) takes int8 or int4 weights with
+ * per-channel or per-group scales (groups a multiple of 64 dividing d and r);
+ * larger M takes int8 per-channel weights, head_dim a multiple of 8 and
+ * 16-byte aligned q, k, v.  Other combinations return QSVD_ERR_UNSUPPORTED. */
 qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const float* sx,
                                      int64_t M, int32_t act_bits, uint32_t out_mask,
                                      void* c_h, void* cq, float* sc, void* q, void* k, void* v,
@@ -140,16 +145,23 @@ size_t qsvd_prefill_workspace_size(const qsvd_layer* w, int64_t M, uint32_t out_
 qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void* cq,
                                      const float* sc, int32_t n_new, void* stream);
 
-/* Attention of the current query of every sequence over its cached latent rows
- * (decoding with l = 1, Section 3.1): keys and values are C W^u_k and C W^u_v
- * of the stored rows (dequantized), the query attends to all seq_len[b] rows
- * (append first, then attend), softmax(q K^T * sm_scale) V with fp32 softmax.
+/* Attention of the newest queries of every sequence over its cached latent
+ * rows (Section 3.1; decoding is l = 1): keys and values are C W^u_k and
+ * C W^u_v of the stored rows (dequantized), softmax(q K^T * sm_scale) V with an
+ * fp32 softmax.  The q_len queries of sequence b are its last q_len cached
+ * positions (append first, then attend): query i sees positions
+ * [0, seq_len[b] - q_len + i], causally.  A query with no visible position
+ * (seq_len[b] < q_len - i) gets zeros.
  *   q     device fp16 [batch][q_len][Hq*hd] (the Q output of the projection)
  *   out   device fp16 [batch][q_len][Hq*hd]
+ *   mode  QSVD_ATTN_ABSORBED (latent form), QSVD_ATTN_RECONSTRUCT (K, V
+ *         rebuilt per cached token; q_len 1 only) or QSVD_ATTN_AUTO (absorbed
+ *         when its shape is supported)
  *   sm_scale  0 selects 1/sqrt(head_dim)
  *   ws    device workspace of at least qsvd_decode_workspace_size() bytes
- * Requires q_len == 1, n_q_heads <= 32, head_dim % 32 == 0, r % 32 == 0,
- * every seq_len[b] in [1, capacity]. */
+ * Requires n_q_heads <= 32, head_dim % 32 == 0 and <= 128, batch <= 64,
+ * batch * q_len <= 65535, q_len <= max_len, 16-byte aligned q, out and s_b,
+ * an F16 or I8 cache; the absorbed form needs r in {128, 512, 1024, 1536}. */
 qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* c,
                                          const void* q, int32_t q_len, int32_t mode,
                                          float sm_scale, void* out,
