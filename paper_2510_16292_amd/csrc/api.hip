@@ -190,7 +190,10 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
     return fail(QSVD_ERR_INVALID_ARG, "requested output pointer is NULL");
   const bool skinny = M <= 32 && skinny_supported(M, w->d, w->w_group, false) &&
                       skinny_supported(M, w->r, w->w_group, true);
-  if (act_bits != 8) return fail(QSVD_ERR_UNSUPPORTED, "projection implements 8-bit activations");
+  if (act_bits != 8 && !skinny)
+    return fail(QSVD_ERR_UNSUPPORTED, "4-bit activations are implemented for at most 32 tokens");
+  if (act_bits == 4 && (dbg_acc_xa || dbg_acc_cb))
+    return fail(QSVD_ERR_UNSUPPORTED, "integer accumulator dumps need 8-bit activations");
   if (!skinny && (w->w_bits != 8 || w->w_group != 0))
     return fail(QSVD_ERR_UNSUPPORTED,
                 "int4 or per-group weights are implemented for at most 32 tokens, groups a multiple of 64");
@@ -299,7 +302,6 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
   if (w->n_q_heads > 32) return fail(QSVD_ERR_UNSUPPORTED, "at most 32 query heads");
   if (w->head_dim % 32 || w->head_dim > 128) return fail(QSVD_ERR_UNSUPPORTED, "head_dim must be 32, 64, 96 or 128");
   if (c->batch > 64) return fail(QSVD_ERR_UNSUPPORTED, "at most 64 sequences per call");
-  if (c->fmt == QSVD_CACHE_I4) return fail(QSVD_ERR_UNSUPPORTED, "int4 cache attention is not implemented");
   if (w->w_group % 64) return fail(QSVD_ERR_UNSUPPORTED, "decode attention needs w_group 0 or a multiple of 64");
   if (!aligned(q, 16) || !aligned(out, 16) || !aligned(w->s_b, 16))
     return fail(QSVD_ERR_UNSUPPORTED, "q, out and s_b must be 16-byte aligned");
@@ -309,6 +311,7 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
   if (!absorbed && c->capacity > 16384)
     return fail(QSVD_ERR_UNSUPPORTED, "reconstruct form supports capacity <= 16384");
   if (!absorbed && q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form takes q_len 1 only");
+  if (!absorbed && c->fmt == QSVD_CACHE_I4) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form takes F16/I8 caches");
   const size_t need = absorbed ? attn_absorbed_workspace(*w, *c, q_len) : attn_reconstruct_workspace(*w, *c);
   if (!ws || ws_bytes < need) return fail(QSVD_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   AttnArgs a{w, c, (const _Float16*)q, (_Float16*)out, sm_scale > 0.f ? sm_scale : 1.f / sqrtf((float)w->head_dim),

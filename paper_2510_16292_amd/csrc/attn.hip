@@ -240,11 +240,14 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   for (int rb = 0; rb < RB; ++rb) o[rb] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  // Raw tile registers: fp16 rows as they are, int8 rows as 16-byte chunks;
-  // for int8 also the per-token scales of the 16 tokens whose scores and
-  // probabilities this lane holds (t0 + 8*(v/4) + 4*half + v%4).
+  // Raw tile registers: fp16 rows as they are, int8 rows as 16-byte chunks,
+  // int4 rows as 8-byte chunks (16 codes, element 2i in the low nibble of
+  // byte i); for the integer formats also the per-token scales of the 16
+  // tokens whose scores and probabilities this lane holds
+  // (t0 + 8*(v/4) + 4*half + v%4).
+  constexpr bool I4C = FMT == QSVD_CACHE_I4;
   constexpr int NLD = F16C ? KS : KS / 2;
-  using RawT = typename std::conditional<F16C, f16x8, uint4>::type;
+  using RawT = typename std::conditional<F16C, f16x8, typename std::conditional<I4C, uint2, uint4>::type>::type;
   RawT raw[NLD];
   float sc_next[F16C ? 1 : 16], sc_cur[F16C ? 1 : 16];
   auto load_tile = [&](int t0) {
@@ -258,11 +261,13 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     // rows past the chunk end are masked; re-read the last row instead of
     // fetching the next chunk's rows
     const int tk = min(t0 + l32, t_end - 1);
-    const int64_t off = ((int64_t)b * capacity + tk) * r + slice0;
+    const int64_t off = ((int64_t)b * capacity + tk) * r + slice0;     // element index of the row slice
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
       if constexpr (F16C)
         raw[i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const _Float16*>(cdata) + off + kcol(i, half));
+      else if constexpr (I4C)
+        raw[i] = *reinterpret_cast<const RawT*>(cdata + (off + kcol(2 * i, half)) / 2);
       else
         raw[i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const int8_t*>(cdata) + off + kcol(2 * i, half));
     }
@@ -278,11 +283,20 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
       for (int v = 0; v < 16; ++v) sc_cur[v] = sc_next[v];
 #pragma unroll
       for (int i = 0; i < NLD; ++i) {
-        const uint32_t wv[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+        if constexpr (I4C) {
+          const uint32_t wv[2] = {raw[i].x, raw[i].y};
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          cf[2 * i][e] = (_Float16)(float)(int8_t)(wv[e >> 2] >> (8 * (e & 3)));
-          cf[2 * i + 1][e] = (_Float16)(float)(int8_t)(wv[2 + (e >> 2)] >> (8 * (e & 3)));
+          for (int e = 0; e < 8; ++e) {
+            cf[2 * i][e] = (_Float16)(float)(((int)(wv[0] << (28 - 4 * e))) >> 28);
+            cf[2 * i + 1][e] = (_Float16)(float)(((int)(wv[1] << (28 - 4 * e))) >> 28);
+          }
+        } else {
+          const uint32_t wv[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            cf[2 * i][e] = (_Float16)(float)(int8_t)(wv[e >> 2] >> (8 * (e & 3)));
+            cf[2 * i + 1][e] = (_Float16)(float)(int8_t)(wv[2 + (e >> 2)] >> (8 * (e & 3)));
+          }
         }
       }
     }
@@ -681,7 +695,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 bool absorbed_supported(const qsvd_layer& w, const qsvd_cache& c) {
   int rw, nw;
-  return pick_slice(w.r, &rw, &nw) && c.fmt != QSVD_CACHE_I4;
+  return pick_slice(w.r, &rw, &nw);
 }
 
 size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len) {
@@ -734,8 +748,9 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = (c.fmt == QSVD_CACHE_F16) ? dispatch_latent<QSVD_CACHE_F16>(p, c, a.q_len, qt, opart, ml, s)
-                                : dispatch_latent<QSVD_CACHE_I8>(p, c, a.q_len, qt, opart, ml, s);
+  e = c.fmt == QSVD_CACHE_F16 ? dispatch_latent<QSVD_CACHE_F16>(p, c, a.q_len, qt, opart, ml, s)
+      : c.fmt == QSVD_CACHE_I8  ? dispatch_latent<QSVD_CACHE_I8>(p, c, a.q_len, qt, opart, ml, s)
+                                : dispatch_latent<QSVD_CACHE_I4>(p, c, a.q_len, qt, opart, ml, s);
   if (e != hipSuccess) return e;
   {
     KernelScope ks("merge_latent", s);

@@ -72,8 +72,9 @@ __device__ __forceinline__ i32x4 unpack16_i4(uint2 p) {
   return o;
 }
 
-// A operand source: int8 codes (down-projection: the quantized activations), or
-// the fp16 latent quantized by the workgroup itself (up-projection).
+// A operand source: int8 or packed int4 codes (down-projection: the quantized
+// activations), or the fp16 latent quantized by the workgroup itself
+// (up-projection, 8- or 4-bit codes).
 enum { SK_A_I8 = 0, SK_A_F16Q = 1 };
 
 // Contraction steps [s0, s1) of wave w: contiguous ranges, whole groups when the
@@ -213,8 +214,11 @@ skinny_gemm_kernel(const void* __restrict__ a_src, const float* __restrict__ row
       for (int rb = 0; rb < 2; ++rb) {
         const int m = 16 * rb + l16;
         if (st0 + s < s1 && rb < rbl && m < M) {
-          if (ASRC == SK_A_I8)
+          if (ASRC == SK_A_I8 && abits == 8)
             aw[s][rb] = *reinterpret_cast<const i32x4*>(reinterpret_cast<const int8_t*>(a_src) + (int64_t)m * K + k);
+          else if (ASRC == SK_A_I8)     // 4-bit codes, two per byte
+            aw[s][rb] = unpack16_i4(*reinterpret_cast<const uint2*>(reinterpret_cast<const uint8_t*>(a_src) +
+                                                                   ((int64_t)m * K + k) / 2));
           else
             aw[s][rb] = *reinterpret_cast<const i32x4*>(qa + m * qa_ld + k);
         } else {

@@ -49,14 +49,15 @@ def quantize_act(x_np, bits=8, clip=1.0, K=None):
 class Prefill:
     """Device buffers for one projection call of M tokens."""
 
-    def __init__(self, dl, M, mask=7, debug=True):
+    def __init__(self, dl, M, mask=7, debug=True, abits=8):
         t = torch()
-        self.dl, self.M, self.mask = dl, M, mask
+        self.dl, self.M, self.mask, self.abits = dl, M, mask, abits
         nq, nkv, r, N = dl.n_q_heads * dl.head_dim, dl.n_kv_heads * dl.head_dim, dl.r, dl.N
-        self.xq = t.empty((M, dl.d), dtype=t.int8, device="cuda")
+        per = 1 if abits == 8 else 2           # codes per byte
+        self.xq = t.empty((M, dl.d // per), dtype=t.int8 if abits == 8 else t.uint8, device="cuda")
         self.sx = t.empty((M,), dtype=t.float32, device="cuda")
         self.c_h = t.empty((M, r), dtype=t.float16, device="cuda")
-        self.cq = t.empty((M, r), dtype=t.int8, device="cuda")
+        self.cq = t.empty((M, r // per), dtype=t.int8 if abits == 8 else t.uint8, device="cuda")
         self.sc = t.empty((M,), dtype=t.float32, device="cuda")
         self.q = t.empty((M, nq), dtype=t.float16, device="cuda")
         self.k = t.empty((M, nkv), dtype=t.float16, device="cuda")
@@ -69,9 +70,9 @@ class Prefill:
     def run(self, x):
         """x: device fp16 [M][d]."""
         s = B.stream_handle()
-        B.check(B.qsvd_quantize_act(B.ptr(x), self.M, self.dl.d, self.dl.d, 8, 1.0, B.ptr(self.xq),
+        B.check(B.qsvd_quantize_act(B.ptr(x), self.M, self.dl.d, self.dl.d, self.abits, 1.0, B.ptr(self.xq),
                                     B.ptr(self.sx), s))
-        B.check(B.qsvd_lowrank_qkv_prefill(self.dl.c, B.ptr(self.xq), B.ptr(self.sx), self.M, 8, self.mask,
+        B.check(B.qsvd_lowrank_qkv_prefill(self.dl.c, B.ptr(self.xq), B.ptr(self.sx), self.M, self.abits, self.mask,
                                            B.ptr(self.c_h), B.ptr(self.cq), B.ptr(self.sc), B.ptr(self.q),
                                            B.ptr(self.k), B.ptr(self.v), B.ptr(self.acc_xa), B.ptr(self.acc_cb),
                                            B.ptr(self.ws), self.ws_bytes, s))

@@ -136,7 +136,9 @@ def test_prefill_validation(lib):
     assert _prefill(layer_struct(), mask=B.QSVD_OUT_K, k=0) == B.QSVD_ERR_INVALID_ARG
     assert _prefill(layer_struct(), c_h=0) == B.QSVD_ERR_INVALID_ARG
     assert _prefill(layer_struct(), M=0) == B.QSVD_OK          # nothing to do, nothing launched
-    assert _prefill(layer_struct(), act_bits=4) == B.QSVD_ERR_UNSUPPORTED
+    assert _prefill(layer_struct(), M=33, act_bits=4) == B.QSVD_ERR_UNSUPPORTED       # > 32 tokens: 8-bit only
+    assert B.lib().qsvd_lowrank_qkv_prefill(ctypes.byref(layer_struct()), FAKE, FAKE, 4, 4, 7, FAKE, FAKE, FAKE, FAKE,
+                                            FAKE, FAKE, FAKE, 0, 0, 0, 0) == B.QSVD_ERR_UNSUPPORTED  # dumps: A8
     assert _prefill(layer_struct(w_bits=4, w_group=64), M=33) == B.QSVD_ERR_UNSUPPORTED   # > 32 tokens: W8 only
     assert _prefill(layer_struct(w_bits=4, w_group=32)) == B.QSVD_ERR_UNSUPPORTED        # groups of 64 bytes
     g = layer_struct(w_bits=4, w_group=64)
@@ -178,7 +180,8 @@ def test_decode_validation(lib):
     assert _decode(layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64), C) == B.QSVD_ERR_UNSUPPORTED
     assert _decode(layer_struct(head_dim=48, n_q_heads=4), C) == B.QSVD_ERR_UNSUPPORTED
     assert _decode(L, cache_struct(batch=65)) == B.QSVD_ERR_UNSUPPORTED
-    assert _decode(L, cache_struct(fmt=B.QSVD_CACHE_I4, scale=FAKE)) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode(L, cache_struct(fmt=B.QSVD_CACHE_I4, scale=FAKE), mode=B.QSVD_ATTN_RECONSTRUCT) == \
+        B.QSVD_ERR_UNSUPPORTED
     assert _decode(layer_struct(r=192), cache_struct(r=192), mode=B.QSVD_ATTN_ABSORBED) == B.QSVD_ERR_UNSUPPORTED
     need = B.qsvd_decode_workspace_size(L, C, 1, B.QSVD_ATTN_ABSORBED)
     assert need > 0

@@ -181,6 +181,24 @@ def test_projection_bitexact_llava7b_w4a8_g64_m32(llava):
         assert np.array_equal(got[key].view(np.uint16), ref[key].view(np.uint16)), key
 
 
+@pytest.mark.parametrize("M", [1, 16, 32])
+def test_projection_bitexact_w4a4(tiny_w4, M):
+    """W4A4 decode-size projection: 4-bit per-token activation codes (two per
+    byte) and 4-bit Q(C), int4 per-group weights; codes, scales, C and Q/K/V
+    bit-exact against the oracle."""
+    wl, ol, dl = tiny_w4
+    X = gen.fill_activations(wl, M)
+    H.say(f"projection w4a4 group={dl.w_group} M={M}")
+    got = H.Prefill(dl, M, debug=False, abits=4).run(H.dev(X)).result()
+    ref = O.prefill(ol, X, 4)
+    assert np.array_equal(got["xq"].view(np.uint8), O.pack_int4(ref["xq"]))
+    assert np.array_equal(got["cq"].view(np.uint8), O.pack_int4(ref["cq"]))
+    for key in ("sx", "sc"):
+        assert np.array_equal(got[key].view(np.uint32), ref[key].view(np.uint32)), key
+    for key in ("C_h", "Q", "K", "V"):
+        assert np.array_equal(got[key].view(np.uint16), ref[key].view(np.uint16)), key
+
+
 def test_prefill_masks_leave_other_outputs(tiny):
     wl, ol, dl = tiny
     X = gen.fill_activations(wl, 40)
@@ -467,3 +485,46 @@ def test_prefill_attention_llava7b_chunked(llava):
         ok, info = H.close_enough(out[b, i], ref[b, i])
         H.say(f"  b={b} i={i} max-abs, rel-L2, rms = {info}")
         assert ok, (b, i, info)
+
+
+def test_decode_gqa_int4_cache_ragged(gqa):
+    """Int4 latent cache (4-bit per-token codes of C with fp32 scales, two codes
+    per byte): ragged prior lengths 3 / 50 / 97 of synthetic rows, then 3 decode
+    steps whose new rows are the device's 4-bit quantization of the projected C;
+    grouped queries (8 over 2), absorbed form."""
+    L, ol, dl = gqa
+    prior, batch = [3, 50, 97], 3
+    cap = max(prior) + 3
+    wl = configs.Workload(95, "gqa-test", L, "gaussian", 8, 0, 8, configs.CACHE_I4)
+    rows = gen.latent_rows(wl, batch, cap)
+    oc = O.LatentCache(O.CACHE_I4, batch, cap, L.r)
+    data = np.zeros((batch, cap, L.r // 2), np.uint8)
+    scale = np.zeros((batch, cap), np.float32)
+    for b, n in enumerate(prior):
+        codes, sc = O.quantize_act(rows[b, :n], 4)
+        oc.append(b, None, codes, sc)
+        data[b, :n], scale[b, :n] = O.pack_int4(codes), sc
+    dc = B.DeviceCache(B.QSVD_CACHE_I4, batch, cap, L.r, prior)
+    dc.data.copy_(H.dev(data))
+    dc.scale.copy_(H.dev(scale))
+    torch = H.torch()
+    for t in range(3):
+        xt = gen.decode_activations(wl, t, batch=batch)
+        proj = O.prefill(ol, xt, 8)
+        q4, s4 = O.quantize_act(proj["C_h"], 4)
+        for b in range(batch):
+            oc.append(b, None, q4[b:b + 1], s4[b:b + 1])
+        ref = O.attention_reference(ol, oc, proj["Q"][:, None, :], 1)[:, 0, :]
+        H.say(f"decode gqa int4 cache step={t}")
+        p = H.Prefill(dl, batch, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
+        cq4 = torch.empty((batch, L.r // 2), dtype=torch.uint8, device="cuda")
+        sc4 = torch.empty((batch,), dtype=torch.float32, device="cuda")
+        B.check(B.qsvd_quantize_act(B.ptr(p.c_h), batch, L.r, L.r, 4, 1.0, B.ptr(cq4), B.ptr(sc4),
+                                    B.stream_handle()))
+        H.append(dc, cq=cq4, sc=sc4, n_new=1)
+        out = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
+        ok, info = H.close_enough(out, ref)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (t, info)
+    assert np.array_equal(H.host(dc.data), oc.data)
+    assert np.array_equal(H.host(dc.scale).view(np.uint32), oc.scale.view(np.uint32))
