@@ -190,13 +190,11 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
     return fail(QSVD_ERR_INVALID_ARG, "requested output pointer is NULL");
   const bool skinny = M <= 32 && skinny_supported(M, w->d, w->w_group, false) &&
                       skinny_supported(M, w->r, w->w_group, true);
-  if (act_bits != 8 && !skinny)
-    return fail(QSVD_ERR_UNSUPPORTED, "4-bit activations are implemented for at most 32 tokens");
   if (act_bits == 4 && (dbg_acc_xa || dbg_acc_cb))
     return fail(QSVD_ERR_UNSUPPORTED, "integer accumulator dumps need 8-bit activations");
-  if (!skinny && (w->w_bits != 8 || w->w_group != 0))
-    return fail(QSVD_ERR_UNSUPPORTED,
-                "int4 or per-group weights are implemented for at most 32 tokens, groups a multiple of 64");
+  if (w->w_group % 64) return fail(QSVD_ERR_UNSUPPORTED, "w_group must be a multiple of 64");
+  // products with 4-bit operands or per-group scales (M > 32)
+  const bool mixed = !skinny && (w->w_bits != 8 || w->w_group != 0 || act_bits != 8);
   if (w->w_group && (dbg_acc_xa || dbg_acc_cb))
     return fail(QSVD_ERR_UNSUPPORTED, "integer accumulator dumps need per-channel weights");
   if (!aligned(xq, 16) || !aligned(cq, 16) || !aligned(c_h, 16) || !aligned(w->a_t, 16) || !aligned(w->b_t, 16))
@@ -228,7 +226,9 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
     g1.cq = cq;
     g1.sc = sc;
   }
-  st = hip_status(skinny ? launch_skinny(g1, false, w->w_bits, w->w_group, w->r, s) : launch_gemm_i8(g1, s),
+  st = hip_status(skinny  ? launch_skinny(g1, false, w->w_bits, w->w_group, w->r, s)
+                  : mixed ? launch_gemm_q4(g1, act_bits, w->w_bits, w->w_group, w->r, s)
+                          : launch_gemm_i8(g1, s),
                   "down-projection");
   if (st != QSVD_OK) return st;
   if (hi <= lo) {
@@ -253,7 +253,9 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
   g2.abits = act_bits;
   g2.cq = skinny ? cq : nullptr;     // the skinny up-projection quantizes C itself and stores Q(C)
   g2.sc = skinny ? sc : nullptr;
-  return hip_status(skinny ? launch_skinny(g2, true, w->w_bits, w->w_group, N, s) : launch_gemm_i8(g2, s),
+  return hip_status(skinny  ? launch_skinny(g2, true, w->w_bits, w->w_group, N, s)
+                    : mixed ? launch_gemm_q4(g2, act_bits, w->w_bits, w->w_group, N, s)
+                            : launch_gemm_i8(g2, s),
                     "up-projection");
 }
 

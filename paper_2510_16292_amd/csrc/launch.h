@@ -57,6 +57,12 @@ struct GemmArgs {
 // quantized per row into g.cq / g.sc.
 hipError_t launch_gemm_i8(const GemmArgs& g, hipStream_t s);
 
+// The same products with 4-bit activations and/or int4 weights, per-channel or
+// per-group (group contraction elements, a multiple of 64; scale of group g
+// for column n at col_scale[g * sstride + n]).
+hipError_t launch_gemm_q4(const GemmArgs& g, int32_t abits, int32_t wbits, int32_t group, int32_t sstride,
+                          hipStream_t s);
+
 // Decode-size products (M <= 32): A is int8 codes, or (a_is_f16_latent) the
 // fp16 latent quantized per row inside the kernel, which then also writes
 // g.cq / g.sc.  Weights int8 or int4 (grouped, scale row stride sstride).

@@ -136,11 +136,11 @@ def test_prefill_validation(lib):
     assert _prefill(layer_struct(), mask=B.QSVD_OUT_K, k=0) == B.QSVD_ERR_INVALID_ARG
     assert _prefill(layer_struct(), c_h=0) == B.QSVD_ERR_INVALID_ARG
     assert _prefill(layer_struct(), M=0) == B.QSVD_OK          # nothing to do, nothing launched
-    assert _prefill(layer_struct(), M=33, act_bits=4) == B.QSVD_ERR_UNSUPPORTED       # > 32 tokens: 8-bit only
     assert B.lib().qsvd_lowrank_qkv_prefill(ctypes.byref(layer_struct()), FAKE, FAKE, 4, 4, 7, FAKE, FAKE, FAKE, FAKE,
                                             FAKE, FAKE, FAKE, 0, 0, 0, 0) == B.QSVD_ERR_UNSUPPORTED  # dumps: A8
-    assert _prefill(layer_struct(w_bits=4, w_group=64), M=33) == B.QSVD_ERR_UNSUPPORTED   # > 32 tokens: W8 only
-    assert _prefill(layer_struct(w_bits=4, w_group=32)) == B.QSVD_ERR_UNSUPPORTED        # groups of 64 bytes
+    assert _prefill(layer_struct(w_bits=4, w_group=32)) == B.QSVD_ERR_UNSUPPORTED        # groups of 64 codes
+    assert _prefill(layer_struct(w_bits=4, w_group=32), M=33) == B.QSVD_ERR_UNSUPPORTED
+    assert _prefill(layer_struct(d=384, w_bits=4, w_group=192), M=33) == B.QSVD_ERR_INVALID_ARG  # 192 does not divide r
     g = layer_struct(w_bits=4, w_group=64)
     assert B.lib().qsvd_lowrank_qkv_prefill(ctypes.byref(g), FAKE, FAKE, 4, 8, 7, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                                             FAKE, 0, 0, 0, 0) == B.QSVD_ERR_UNSUPPORTED   # no dumps with groups

@@ -199,6 +199,52 @@ def test_projection_bitexact_w4a4(tiny_w4, M):
         assert np.array_equal(got[key].view(np.uint16), ref[key].view(np.uint16)), key
 
 
+def _check_mixed(ol, got, X, abits):
+    ref = O.prefill(ol, X, abits)
+    pack = (lambda c: c.view(np.uint8)) if abits == 8 else O.pack_int4
+    assert np.array_equal(got["xq"].view(np.uint8), pack(ref["xq"]))
+    assert np.array_equal(got["cq"].view(np.uint8), pack(ref["cq"]))
+    for key in ("sx", "sc"):
+        assert np.array_equal(got[key].view(np.uint32), ref[key].view(np.uint32)), key
+    for key in ("C_h", "Q", "K", "V"):
+        assert np.array_equal(got[key].view(np.uint16), ref[key].view(np.uint16)), key
+
+
+@pytest.mark.parametrize("abits", [8, 4], ids=["a8", "a4"])
+@pytest.mark.parametrize("M", [33, 64, 200])
+def test_prefill_bitexact_w4(tiny_w4, M, abits):
+    """Prefill-size projections with int4 per-group weights (groups of 64 or
+    128) and 8- or 4-bit activations: the pipelined kernel widens int4 codes to
+    int8 in registers and folds each group's exact int32 sum into fp32 in group
+    order; everything bit-exact against the oracle, ragged row tiles."""
+    wl, ol, dl = tiny_w4
+    X = gen.fill_activations(wl, M)
+    H.say(f"prefill w4a{abits} group={dl.w_group} M={M}")
+    got = H.Prefill(dl, M, debug=False, abits=abits).run(H.dev(X)).result()
+    _check_mixed(ol, got, X, abits)
+
+
+def test_prefill_bitexact_w8a4_and_grouped_w8(tiny):
+    """W8A4 with per-channel weights, and int8 weights with per-group scales,
+    at 100 tokens."""
+    wl, ol, dl = tiny
+    X = gen.fill_activations(wl, 100)
+    H.say("prefill w8a4 per-channel M=100")
+    _check_mixed(ol, H.Prefill(dl, 100, debug=False, abits=4).run(H.dev(X)).result(), X, 4)
+    ol8g, dl8g = _layers_from_weight(gen.weight_matrix(wl), wl.layer, w_bits=8, w_group=64)
+    H.say("prefill w8a8 group 64 M=100")
+    _check_mixed(ol8g, H.Prefill(dl8g, 100, debug=False).run(H.dev(X)).result(), X, 8)
+
+
+def test_prefill_bitexact_qwen2vl_w4a8(qwen):
+    """Qwen2-VL-shaped layer (d=3584, r=1024, N=4608, int4 groups of 128) over
+    640 tokens, bit-exact."""
+    wl, ol, dl = qwen
+    X = gen.fill_activations(wl, 640)
+    H.say("prefill qwen2vl w4a8 M=640")
+    _check_mixed(ol, H.Prefill(dl, 640, debug=False).run(H.dev(X)).result(), X, 8)
+
+
 def test_prefill_masks_leave_other_outputs(tiny):
     wl, ol, dl = tiny
     X = gen.fill_activations(wl, 40)
