@@ -283,6 +283,7 @@ size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int3
   const bool abs_ok = absorbed_supported(*w, *c);
   if (mode == QSVD_ATTN_RECONSTRUCT || (mode == QSVD_ATTN_AUTO && !abs_ok))
     return q_len == 1 ? attn_reconstruct_workspace(*w, *c) : 0;
+  if (absorbed_grid_rows(*w, *c, q_len) > kMaxQueryRows) return 0;
   return attn_absorbed_workspace(*w, *c, q_len);
 }
 
@@ -301,15 +302,19 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
   if ((int64_t)c->batch * q_len > kMaxQueryRows)
     return fail(QSVD_ERR_UNSUPPORTED, "batch * q_len must be at most %d", kMaxQueryRows);
   if (c->max_len < q_len) return fail(QSVD_ERR_INVALID_ARG, "cache holds %d tokens, fewer than q_len %d", c->max_len, q_len);
-  if (w->n_q_heads > 32) return fail(QSVD_ERR_UNSUPPORTED, "at most 32 query heads");
+  if (w->n_q_heads > 64) return fail(QSVD_ERR_UNSUPPORTED, "at most 64 query heads");
   if (w->head_dim % 32 || w->head_dim > 128) return fail(QSVD_ERR_UNSUPPORTED, "head_dim must be 32, 64, 96 or 128");
   if (c->batch > 64) return fail(QSVD_ERR_UNSUPPORTED, "at most 64 sequences per call");
   if (w->w_group % 64) return fail(QSVD_ERR_UNSUPPORTED, "decode attention needs w_group 0 or a multiple of 64");
   if (!aligned(q, 16) || !aligned(out, 16) || !aligned(w->s_b, 16))
     return fail(QSVD_ERR_UNSUPPORTED, "q, out and s_b must be 16-byte aligned");
   const bool abs_ok = absorbed_supported(*w, *c);
-  if (mode == QSVD_ATTN_ABSORBED && !abs_ok) return fail(QSVD_ERR_UNSUPPORTED, "absorbed form needs r in {128, 512, 1024, 1536}");
+  if (mode == QSVD_ATTN_ABSORBED && !abs_ok)
+    return fail(QSVD_ERR_UNSUPPORTED, "absorbed form needs r in {128, 512, 1024, 1536} or a multiple of 128 up to 3072");
   const bool absorbed = mode == QSVD_ATTN_ABSORBED || (mode == QSVD_ATTN_AUTO && abs_ok);
+  if (absorbed && absorbed_grid_rows(*w, *c, q_len) > kMaxQueryRows)
+    return fail(QSVD_ERR_UNSUPPORTED, "batch * q_len * head blocks must be at most %d", kMaxQueryRows);
+  if (!absorbed && w->n_q_heads > 32) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form takes at most 32 query heads");
   if (!absorbed && c->capacity > 16384)
     return fail(QSVD_ERR_UNSUPPORTED, "reconstruct form supports capacity <= 16384");
   if (!absorbed && q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form takes q_len 1 only");

@@ -26,6 +26,7 @@ namespace qsvd {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kHeadBlk = 32;   // query heads are padded to one 32-wide MFMA block
 constexpr int kMaxChunks = 256;  // context chunks per sequence the merge supports
+constexpr int kMaxAbsorbedHeads = 64;   // query heads per sequence in the absorbed form
 
 // ---------------------------------------------------------------------------
 // Weight code access (int8 or packed int4), transposed layout [N][r].
@@ -57,14 +58,14 @@ constexpr int kAbsorbLd = kAbsorbJ + 16;   // stride 40 dwords = 8 (mod 32): con
 __global__ void __launch_bounds__(64)
 absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, const float* __restrict__ sb,
               int32_t B, int32_t r, int32_t Hq, int32_t Hkv, int32_t dh, int32_t N, int32_t bits,
-              int32_t group, float scale, _Float16* __restrict__ qt) {
+              int32_t group, float scale, int32_t hp, _Float16* __restrict__ qt) {
   __shared__ __attribute__((aligned(16))) _Float16 wk[128 * kAbsorbLd];
   const int h = blockIdx.x, lane = threadIdx.x;
   const int32_t jb = blockIdx.y * kAbsorbJ;
   if (h >= Hq) {
     for (int e = lane; e < B * (kAbsorbJ / 8); e += 64) {
       const int b = e / (kAbsorbJ / 8), j8 = e - b * (kAbsorbJ / 8);
-      *reinterpret_cast<f16x8*>(qt + ((int64_t)b * kHeadBlk + h) * r + jb + 8 * j8) = f16x8{};
+      *reinterpret_cast<f16x8*>(qt + ((int64_t)b * hp + h) * r + jb + 8 * j8) = f16x8{};
     }
     return;
   }
@@ -174,7 +175,7 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int b = b0 + 4 * quad + v;
-        if (b < B) qt[((int64_t)b * kHeadBlk + h) * r + jb + 16 * jj + l16] = (_Float16)(acc[jj][v] * scale);
+        if (b < B) qt[((int64_t)b * hp + h) * r + jb + 16 * jj + l16] = (_Float16)(acc[jj][v] * scale);
       }
   }
 }
@@ -418,56 +419,269 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// Merge the chunk partials of the latent form.  Chunk c of sequence b holds
-// m_c, l_c per head and the normalized O_c / l_c as fp16 in the [x/4][32][4]
-// order above.  With m = max m_c and w_c = 2^(m_c - m) l_c / sum, the result
-// O[b][h][x] = sum_c w_c (O_c / l_c)[h][x] is written head-major [b][32][r].
-// A workgroup takes 2048 consecutive partial elements (16 latent quads x 32
-// heads x 4); its threads first compute all the per-(chunk, head) weights
-// into LDS (8 lanes per head, chunks strided over them), then each thread
-// streams 8 elements (two heads x 4 columns) of every chunk.
+// Latent attention for wide layers: 16 query heads per workgroup (grid row =
+// (sequence-query row, head block)), 16-token tiles, the latent columns split
+// over 8 waves in units of 128.  Used where a 32-head block's output state
+// (32 x r fp32) would not fit one CU's registers (r > 1536) or a sequence has
+// more than 32 query heads.  Per tile:
+//   S^T (16 tokens x 16 heads) = C_tile[:, slice] q~[:, slice]^T  (16x16x32 fp16 MFMA)
+//   partial S^T of all waves summed through LDS in wave order
+//   online softmax per head in fp32 (lane l: head l % 16, tokens 4(l/16) + v)
+//   O^T[slice] (r x 16 heads) += C_tile[:, slice]^T P^T           (16x16x16 fp16 MFMA)
+// The C tile reaches the first product straight from HBM (one 16-byte load
+// per lane serves 1, 2 or 4 contraction steps for fp16, int8, int4 rows) and
+// the second through a wave-private LDS copy read with transposing loads.
+// ---------------------------------------------------------------------------
+constexpr int kH16Waves = 8;
+constexpr int kH16Tile = 16;
+
+template <int UMAX, int FMT>
+__global__ void __launch_bounds__(kH16Waves * 64)
+latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ cdata,
+                       const float* __restrict__ cscale, const int32_t* __restrict__ seq_len,
+                       int32_t capacity, int32_t r, int32_t hp, int32_t chunk, int32_t n_chunks,
+                       int32_t q_len, _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
+  constexpr int NW = kH16Waves;
+  constexpr int KS = 4 * UMAX;          // 32-wide contraction steps of the score product
+  constexpr int RB = 8 * UMAX;          // 16-row blocks of the output product
+  constexpr int CST = 128 * UMAX + 16;  // staged row stride in halves: 8 (mod 64) dwords
+  constexpr bool F16C = FMT == QSVD_CACHE_F16, I4C = FMT == QSVD_CACHE_I4;
+  constexpr int NLD = F16C ? KS : (I4C ? KS / 4 : KS / 2);   // 16-byte loads per row slice
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  _Float16* cst = reinterpret_cast<_Float16*>(smem) + w * kH16Tile * CST;
+  f32x4* spart = reinterpret_cast<f32x4*>(smem + (size_t)NW * kH16Tile * CST * 2);
+  f32x4* ssum = spart + NW * 64;
+
+  const int n_hb = hp >> 4;
+  const int row = blockIdx.y, vb = row / n_hb, hb = row - vb * n_hb;
+  const int b = vb / q_len, qi = vb - b * q_len;
+  const int L = min(seq_len[b], capacity) - (q_len - 1 - qi);
+  const int ch = blockIdx.x, t_begin = ch * chunk;
+  if (t_begin >= L) return;
+  const int t_end = min(L, t_begin + chunk);
+  // this wave's latent units [u0, u0 + nu) of 128 columns (nu <= UMAX, may be 0)
+  const int m_units = r >> 7;
+  const int u0 = (w * m_units) / NW, nu = ((w + 1) * m_units) / NW - u0;
+  const int slice0 = 128 * u0, ksn = 4 * nu;
+  const int nldn = F16C ? ksn : (I4C ? nu : ksn / 2);
+
+  // Contraction slots of the score product: in step ks, lane group g feeds
+  // latent columns slice0 + kcol(ks, g) .. +7 of token t0 + l16, and the
+  // query slots follow the same map.
+  auto kcol = [](int ks, int gg) {
+    return F16C ? 32 * ks + 8 * gg : (I4C ? 128 * (ks >> 2) + 32 * gg + 8 * (ks & 3) : 64 * (ks >> 1) + 16 * gg + 8 * (ks & 1));
+  };
+  f16x8 qf[KS];
+  {
+    const _Float16* qrow = qt + ((int64_t)vb * hp + hb * 16 + l16) * r + slice0;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      if (ks < ksn) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, g));
+  }
+  f32x4 o[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) o[rb] = f32x4{};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  uint4 raw[NLD];
+  float sc_next[F16C ? 1 : 4], sc_cur[F16C ? 1 : 4];
+  auto load_tile = [&](int t0) {
+    if constexpr (!F16C) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) sc_next[v] = cscale[(int64_t)b * capacity + min(t0 + 4 * g + v, L - 1)];
+    }
+    // rows past the chunk end are masked; re-read the last row of the chunk
+    const int tk = min(t0 + l16, t_end - 1);
+    const int64_t off = ((int64_t)b * capacity + tk) * r + slice0;     // element index of the row slice
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      if (i >= nldn) continue;
+      if constexpr (F16C)
+        raw[i] = *reinterpret_cast<const uint4*>(reinterpret_cast<const _Float16*>(cdata) + off + kcol(i, g));
+      else if constexpr (I4C)
+        raw[i] = *reinterpret_cast<const uint4*>(cdata + (off + 128 * i + 32 * g) / 2);
+      else
+        raw[i] = *reinterpret_cast<const uint4*>(cdata + off + 64 * i + 16 * g);
+    }
+  };
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  load_tile(t_begin);
+  for (int t0 = t_begin; t0 < t_end; t0 += kH16Tile) {
+    if constexpr (!F16C) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) sc_cur[v] = sc_next[v];
+    }
+    f32x4 sacc = f32x4{};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks >= ksn) continue;
+      f16x8 cf;
+      if constexpr (F16C) {
+        cf = __builtin_bit_cast(f16x8, raw[ks]);
+      } else if constexpr (I4C) {
+        const uint4 q4 = raw[ks >> 2];
+        const uint32_t wv = (ks & 3) == 0 ? q4.x : (ks & 3) == 1 ? q4.y : (ks & 3) == 2 ? q4.z : q4.w;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cf[e] = (_Float16)(float)(((int)(wv << (28 - 4 * e))) >> 28);
+      } else {
+        const uint4 q8 = raw[ks >> 1];
+        const uint32_t w0 = (ks & 1) ? q8.z : q8.x, w1 = (ks & 1) ? q8.w : q8.y;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          cf[e] = (_Float16)(float)(int8_t)(w0 >> (8 * e));
+          cf[4 + e] = (_Float16)(float)(int8_t)(w1 >> (8 * e));
+        }
+      }
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(cf, qf[ks], sacc, 0, 0, 0);
+      *reinterpret_cast<f16x8*>(cst + l16 * CST + kcol(ks, g)) = cf;
+    }
+    // the next tile streams in while this one is reduced and multiplied
+    if (t0 + kH16Tile < t_end) load_tile(t0 + kH16Tile);
+    spart[w * 64 + lane] = sacc;
+    __syncthreads();
+    if (w == 0) {
+      f32x4 acc = spart[lane];
+#pragma unroll
+      for (int w2 = 1; w2 < NW; ++w2) acc += spart[w2 * 64 + lane];
+      ssum[lane] = acc;
+    }
+    __syncthreads();
+    const f32x4 sv = ssum[lane];
+    // lane holds head l16 at tokens t0 + 4g + v
+    float s[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      float x = sv[v];
+      if constexpr (!F16C) x *= sc_cur[v];
+      s[v] = (t0 + 4 * g + v < t_end) ? x : -INFINITY;
+    }
+    float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    float alpha = 1.f, ps = 0.f;
+    float p[4];
+    if (m_new == -INFINITY) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) p[v] = 0.f;
+    } else {
+      alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        p[v] = __builtin_amdgcn_exp2f(s[v] - m_new);
+        ps += p[v];
+      }
+    }
+    ps += __shfl_xor(ps, 16, 64);
+    ps += __shfl_xor(ps, 32, 64);
+    l_run = l_run * alpha + ps;
+    m_run = m_new;
+    if (__any(alpha != 1.f)) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) o[rb] *= alpha;
+    }
+    // P^T as the B operand: k-slot e of lane group g is token 4g + e, the
+    // tokens this lane's probabilities belong to.
+    f16x4 pf;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float pv = p[e];
+      if constexpr (!F16C) pv *= sc_cur[e];
+      pf[e] = (_Float16)pv;
+    }
+    // A operand: lane (l16, g) needs latent column 16rb + l16 at tokens
+    // 4g .. 4g+3.  In the transposing read, lane a of group g addresses token
+    // 4g + a/4, columns 16rb + 4(a%4) .. +3, and lane i receives element i%4
+    // of the chunks of lanes i/4, 4 + i/4, 8 + i/4, 12 + i/4: column
+    // 16rb + i at tokens 4g .. 4g+3.
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      if (rb >= 2 * ksn) continue;
+      const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_s16x4*)(cst + (4 * g + (l16 >> 2)) * CST + 16 * rb + 4 * (l16 & 3)));
+      o[rb] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, x), pf, o[rb], 0, 0, 0);
+    }
+  }
+
+  const int64_t part = (int64_t)row * n_chunks + ch;
+  if (w == 0 && lane < 16) {
+    ml_part[part * 32 + l16] = m_run;
+    ml_part[part * 32 + 16 + l16] = l_run;
+  }
+  // O^T / l as fp16 in [x/4][16 heads][4] order: lane (head l16, g) holds
+  // latent columns slice0 + 16rb + 4g .. +3, so each store writes 512
+  // contiguous bytes.
+  const float inv_l = l_run > 0.f ? 1.f / l_run : 0.f;
+  _Float16* op = o_part + part * (int64_t)r * 16;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    if (rb >= 2 * ksn) continue;
+    const int x4 = (slice0 + 16 * rb + 4 * g) >> 2;
+    const f16x4 v4 = {(_Float16)(o[rb][0] * inv_l), (_Float16)(o[rb][1] * inv_l), (_Float16)(o[rb][2] * inv_l),
+                      (_Float16)(o[rb][3] * inv_l)};
+    *reinterpret_cast<f16x4*>(op + ((int64_t)x4 * 16 + l16) * 4) = v4;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Merge the chunk partials of the latent form.  The attention grid row
+// (sequence-query row vb, head block hb) of HB heads holds, per chunk c,
+// m_c, l_c per head and the normalized O_c / l_c as fp16 in the [x/4][HB][4]
+// order the attention kernels write.  With m = max m_c and
+// w_c = 2^(m_c - m) l_c / sum, the result O[vb][h][x] = sum_c w_c (O_c / l_c)[h][x]
+// is written head-major [vb][hp][r] at heads hb*HB ...
+// A workgroup takes 2048 consecutive partial elements (2048 / (4 HB) latent
+// quads x HB heads x 4); its threads first compute all the per-(chunk, head)
+// weights into LDS (256 / HB lanes per head, chunks strided over them), then
+// each thread streams 8 elements (two heads x 4 columns) of every chunk.
 // ---------------------------------------------------------------------------
 constexpr int kMergeElems = 2048;
 constexpr int kMergeBatch = 8;
 
+template <int HB>
 __global__ void __launch_bounds__(256)
 merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict__ ml_part,
                     const int32_t* __restrict__ seq_len, int32_t capacity, int32_t chunk, int32_t n_chunks,
-                    int32_t n_launched, int32_t q_len, int32_t r, _Float16* __restrict__ o_lat) {
-  __shared__ float wgt[kMaxChunks * kHeadBlk];
-  const int b = blockIdx.y, tid = threadIdx.x;      // b: (sequence, query) row as in the attention
-  const int L = min(seq_len[b / q_len], capacity) - (q_len - 1 - b % q_len);
+                    int32_t n_launched, int32_t q_len, int32_t r, int32_t hp, _Float16* __restrict__ o_lat) {
+  constexpr int LPH = 256 / HB;      // lanes per head in the weights phase
+  __shared__ float wgt[kMaxChunks * HB];
+  const int n_hb = hp / HB;
+  const int row = blockIdx.y, vb = row / n_hb, hb = row - vb * n_hb, tid = threadIdx.x;
+  const int L = min(seq_len[vb / q_len], capacity) - (q_len - 1 - vb % q_len);
   const int nv = L > 0 ? min(min((L + chunk - 1) / chunk, n_launched), kMaxChunks) : 0;
-  const int64_t pb = (int64_t)b * n_chunks;
-  // element e8 (8 halves): latent quad x4 = e8 / 16, heads 2*(e8 % 16) and +1;
+  const int64_t pb = (int64_t)row * n_chunks;
+  // element e8 (8 halves): latent quad x4 = e8 / (HB / 2), heads 2*(e8 % (HB / 2)) and +1;
   // the first batch of partial loads goes out before the weights are known
   const int64_t e0 = (int64_t)blockIdx.x * kMergeElems + 8 * tid;
-  const bool eok = e0 < (int64_t)r * kHeadBlk;
-  const _Float16* src = o_part + pb * (int64_t)r * kHeadBlk + (eok ? e0 : 0);
+  const bool eok = e0 < (int64_t)r * HB;
+  const _Float16* src = o_part + pb * (int64_t)r * HB + (eok ? e0 : 0);
   f16x8 v[kMergeBatch];
 #pragma unroll
   for (int k = 0; k < kMergeBatch; ++k)
-    v[k] = (eok && k < nv) ? *reinterpret_cast<const f16x8*>(src + (int64_t)k * r * kHeadBlk) : f16x8{};
+    v[k] = (eok && k < nv) ? *reinterpret_cast<const f16x8*>(src + (int64_t)k * r * HB) : f16x8{};
   {
-    const int h = tid >> 3, sub = tid & 7;
+    const int h = tid / LPH, sub = tid % LPH;
     float m = -INFINITY;
-    for (int c = sub; c < nv; c += 8) m = fmaxf(m, ml_part[(pb + c) * 64 + h]);
+    for (int c = sub; c < nv; c += LPH) m = fmaxf(m, ml_part[(pb + c) * 2 * HB + h]);
 #pragma unroll
-    for (int o = 1; o < 8; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    for (int o = 1; o < LPH; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
     float tot = 0.f;
-    for (int c = sub; c < nv; c += 8) {
-      const float wc = exp2f(ml_part[(pb + c) * 64 + h] - m) * ml_part[(pb + c) * 64 + 32 + h];
-      wgt[c * kHeadBlk + h] = wc;
+    for (int c = sub; c < nv; c += LPH) {
+      const float wc = exp2f(ml_part[(pb + c) * 2 * HB + h] - m) * ml_part[(pb + c) * 2 * HB + HB + h];
+      wgt[c * HB + h] = wc;
       tot += wc;
     }
 #pragma unroll
-    for (int o = 1; o < 8; o <<= 1) tot += __shfl_xor(tot, o, 64);
+    for (int o = 1; o < LPH; o <<= 1) tot += __shfl_xor(tot, o, 64);
     const float inv = tot > 0.f ? 1.f / tot : 0.f;
-    for (int c = sub; c < nv; c += 8) wgt[c * kHeadBlk + h] *= inv;
+    for (int c = sub; c < nv; c += LPH) wgt[c * HB + h] *= inv;
   }
   __syncthreads();
   if (!eok) return;
-  const int x4 = (int)(e0 / (4 * kHeadBlk)), h0 = (int)((e0 / 4) % kHeadBlk);
+  const int x4 = (int)(e0 / (4 * HB)), h0 = (int)((e0 / 4) % HB);
   float acc[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) acc[k] = 0.f;
@@ -475,12 +689,12 @@ merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict
     if (c0 > 0) {
 #pragma unroll
       for (int k = 0; k < kMergeBatch; ++k)
-        v[k] = (c0 + k < nv) ? *reinterpret_cast<const f16x8*>(src + (int64_t)(c0 + k) * r * kHeadBlk) : f16x8{};
+        v[k] = (c0 + k < nv) ? *reinterpret_cast<const f16x8*>(src + (int64_t)(c0 + k) * r * HB) : f16x8{};
     }
 #pragma unroll
     for (int k = 0; k < kMergeBatch; ++k) {
       if (c0 + k >= nv) break;
-      const float w0 = wgt[(c0 + k) * kHeadBlk + h0], w1 = wgt[(c0 + k) * kHeadBlk + h0 + 1];
+      const float w0 = wgt[(c0 + k) * HB + h0], w1 = wgt[(c0 + k) * HB + h0 + 1];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         acc[q] = fmaf(w0, (float)v[k][q], acc[q]);
@@ -492,7 +706,7 @@ merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict
   for (int hh = 0; hh < 2; ++hh) {
     const f16x4 o4 = {(_Float16)acc[4 * hh], (_Float16)acc[4 * hh + 1], (_Float16)acc[4 * hh + 2],
                       (_Float16)acc[4 * hh + 3]};
-    *reinterpret_cast<f16x4*>(o_lat + ((int64_t)b * kHeadBlk + h0 + hh) * r + 4 * x4) = o4;
+    *reinterpret_cast<f16x4*>(o_lat + ((int64_t)vb * hp + hb * HB + h0 + hh) * r + 4 * x4) = o4;
   }
 }
 
@@ -583,7 +797,7 @@ constexpr int kVprojBatch = 8;
 __global__ void __launch_bounds__(64 * kVprojWaves)
 vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt, const float* __restrict__ sb,
              int32_t B, int32_t r, int32_t Hq, int32_t Hkv, int32_t dh, int32_t N, int32_t bits,
-             int32_t group, _Float16* __restrict__ out) {
+             int32_t group, int32_t hp, _Float16* __restrict__ out) {
   __shared__ f32x4 red[kVprojWaves][64];
   const int h = blockIdx.x, c0 = blockIdx.y * 16, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, quad = lane >> 4;
@@ -594,7 +808,7 @@ vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt,
   const float cs = group ? 1.f : sb[n];      // per-channel scale, fetched with the first loads
   for (int b0 = 0; b0 < B; b0 += 16) {
     const int bA = b0 + l16;
-    const _Float16* arow = o_lat + ((int64_t)min(bA, B - 1) * kHeadBlk + h) * r + 8 * quad;
+    const _Float16* arow = o_lat + ((int64_t)min(bA, B - 1) * hp + h) * r + 8 * quad;
     f32x4 res = f32x4{};
     for (int st0 = s_begin; st0 < s_end; st0 += kVprojBatch) {
       f16x8 a[kVprojBatch];
@@ -657,13 +871,16 @@ vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt,
 // Host side of the absorbed form.
 // ---------------------------------------------------------------------------
 struct AbsorbPlan {
-  int rw, nw;
+  int hb;            // heads per attention workgroup: 32 (latent_attn_kernel) or 16 (the wide variant)
+  int n_hb, hp;      // head blocks per row and padded heads per row (n_hb * hb)
+  int rw, nw;        // 32-head kernel: latent columns per wave, waves
+  int umax;          // 16-head kernel: 128-column units per wave (at most)
   int chunk, n_chunks, n0;
   size_t qt_bytes, opart_bytes, ml_bytes, olat_bytes;
 };
 
-static int target_chunks(int batch) {
-  const int n0 = (256 + batch - 1) / batch;
+static int target_chunks(int rows) {
+  const int n0 = (256 + rows - 1) / rows;
   return n0 < 1 ? 1 : n0;
 }
 
@@ -674,20 +891,33 @@ static bool pick_slice(int r, int* rw, int* nw) {
   return false;
 }
 
+// The 16-head kernel takes r a multiple of 128 up to 3 * 128 columns per wave.
+static bool h16_rank_ok(int r) { return r % 128 == 0 && r / 128 <= 3 * kH16Waves; }
+
 static AbsorbPlan plan_absorbed(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len) {
   AbsorbPlan p{};
-  pick_slice(w.r, &p.rw, &p.nw);
-  const int64_t rows = (int64_t)c.batch * q_len;      // one query row block per (sequence, query)
-  p.n0 = target_chunks((int)rows);
+  if (w.n_q_heads <= kHeadBlk && pick_slice(w.r, &p.rw, &p.nw)) {
+    p.hb = kHeadBlk;
+    p.n_hb = 1;
+  } else {
+    p.hb = 16;
+    p.n_hb = (w.n_q_heads + 15) / 16;
+    const int m_units = w.r / 128;
+    p.umax = (m_units + kH16Waves - 1) / kH16Waves;
+  }
+  p.hp = p.hb * p.n_hb;
+  const int64_t rows = (int64_t)c.batch * q_len;      // one query row per (sequence, query)
+  const int64_t grows = rows * p.n_hb;                // attention grid rows
+  p.n0 = target_chunks((int)grows);
   const int len = c.max_len > 0 ? c.max_len : 1;
   int ch = (len + p.n0 - 1) / p.n0;
   ch = ((ch + 15) / 16) * 16;
   p.chunk = ch;
   p.n_chunks = (len + ch - 1) / ch;
-  p.qt_bytes = (size_t)rows * kHeadBlk * w.r * sizeof(_Float16);
-  p.opart_bytes = (size_t)rows * p.n0 * w.r * kHeadBlk * sizeof(_Float16);
-  p.ml_bytes = (size_t)rows * p.n0 * 64 * sizeof(float);
-  p.olat_bytes = (size_t)rows * kHeadBlk * w.r * sizeof(_Float16);
+  p.qt_bytes = (size_t)rows * p.hp * w.r * sizeof(_Float16);
+  p.opart_bytes = (size_t)grows * p.n0 * w.r * p.hb * sizeof(_Float16);
+  p.ml_bytes = (size_t)grows * p.n0 * 2 * p.hb * sizeof(float);
+  p.olat_bytes = (size_t)rows * p.hp * w.r * sizeof(_Float16);
   return p;
 }
 
@@ -695,7 +925,13 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 bool absorbed_supported(const qsvd_layer& w, const qsvd_cache& c) {
   int rw, nw;
-  return pick_slice(w.r, &rw, &nw);
+  if (w.n_q_heads <= kHeadBlk && pick_slice(w.r, &rw, &nw)) return true;
+  return w.n_q_heads <= kMaxAbsorbedHeads && h16_rank_ok(w.r);
+}
+
+int64_t absorbed_grid_rows(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len) {
+  const AbsorbPlan p = plan_absorbed(w, c, 1);
+  return (int64_t)c.batch * q_len * p.n_hb;
 }
 
 size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len) {
@@ -717,9 +953,27 @@ static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, int32_
   return hipGetLastError();
 }
 
+template <int UMAX, int FMT>
+static hipError_t launch_latent_h16(const AbsorbPlan& p, const qsvd_cache& c, int32_t q_len, const _Float16* qt,
+                                    _Float16* opart, float* ml, hipStream_t s) {
+  const size_t lds = (size_t)kH16Waves * kH16Tile * (128 * UMAX + 16) * 2 + (size_t)(kH16Waves + 1) * 64 * 16;
+  auto kern = latent_attn_h16_kernel<UMAX, FMT>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  KernelScope ks("latent_attn_h16", s);
+  QSVD_LAUNCH(ks, kern, dim3(p.n_chunks, c.batch * q_len * p.n_hb), dim3(kH16Waves * 64), lds, s, qt,
+              (const uint8_t*)c.data, c.scale, c.seq_len, c.capacity, c.r, p.hp, p.chunk, p.n0, q_len, opart, ml);
+  return hipGetLastError();
+}
+
 template <int FMT>
 static hipError_t dispatch_latent(const AbsorbPlan& p, const qsvd_cache& c, int32_t q_len, const _Float16* qt,
                                   _Float16* opart, float* ml, hipStream_t s) {
+  if (p.hb == 16) {
+    if (p.umax == 1) return launch_latent_h16<1, FMT>(p, c, q_len, qt, opart, ml, s);
+    if (p.umax == 2) return launch_latent_h16<2, FMT>(p, c, q_len, qt, opart, ml, s);
+    return launch_latent_h16<3, FMT>(p, c, q_len, qt, opart, ml, s);
+  }
   if (p.rw == 192) return launch_latent<192, 8, FMT>(p, c, q_len, qt, opart, ml, s);
   if (p.rw == 128) return launch_latent<128, 8, FMT>(p, c, q_len, qt, opart, ml, s);
   if (p.rw == 64) return launch_latent<64, 8, FMT>(p, c, q_len, qt, opart, ml, s);
@@ -742,9 +996,9 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
   {
     KernelScope ks("absorb_q", s);
-    QSVD_LAUNCH(ks, absorb_kernel, dim3(kHeadBlk, w.r / kAbsorbJ), dim3(64), 0, s, a.q,
+    QSVD_LAUNCH(ks, absorb_kernel, dim3(p.hp, w.r / kAbsorbJ), dim3(64), 0, s, a.q,
                        (const uint8_t*)w.b_t, w.s_b, rows, w.r, w.n_q_heads, w.n_kv_heads,
-                       w.head_dim, N, w.w_bits, w.w_group, a.sm_scale * kLog2e, qt);
+                       w.head_dim, N, w.w_bits, w.w_group, a.sm_scale * kLog2e, p.hp, qt);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -754,15 +1008,19 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   if (e != hipSuccess) return e;
   {
     KernelScope ks("merge_latent", s);
-    QSVD_LAUNCH(ks, merge_latent_kernel, dim3((w.r * kHeadBlk + kMergeElems - 1) / kMergeElems, rows),
-                       dim3(256), 0, s, opart, ml, c.seq_len, c.capacity, p.chunk, p.n0, p.n_chunks, a.q_len, w.r,
-                       olat);
+    const dim3 grid((w.r * p.hb + kMergeElems - 1) / kMergeElems, rows * p.n_hb);
+    if (p.hb == 16)
+      QSVD_LAUNCH(ks, merge_latent_kernel<16>, grid, dim3(256), 0, s, opart, ml, c.seq_len, c.capacity, p.chunk,
+                  p.n0, p.n_chunks, a.q_len, w.r, p.hp, olat);
+    else
+      QSVD_LAUNCH(ks, merge_latent_kernel<kHeadBlk>, grid, dim3(256), 0, s, opart, ml, c.seq_len, c.capacity,
+                  p.chunk, p.n0, p.n_chunks, a.q_len, w.r, p.hp, olat);
   }
   {
     KernelScope ks("vproj", s);
     QSVD_LAUNCH(ks, vproj_kernel, dim3(w.n_q_heads, w.head_dim / 16), dim3(64 * kVprojWaves), 0, s, olat,
                        (const uint8_t*)w.b_t, w.s_b, rows, w.r, w.n_q_heads, w.n_kv_heads, w.head_dim, N,
-                       w.w_bits, w.w_group, a.out);
+                       w.w_bits, w.w_group, p.hp, a.out);
   }
   return hipGetLastError();
 }

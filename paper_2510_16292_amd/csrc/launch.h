@@ -84,6 +84,8 @@ struct AttnArgs {
   int32_t q_len;          // queries per sequence: the last q_len cached positions, causal among them
 };
 size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len);
+// Rows of the absorbed attention grid: (sequence, query) rows times head blocks.
+int64_t absorbed_grid_rows(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len);
 hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s);
 size_t attn_reconstruct_workspace(const qsvd_layer& w, const qsvd_cache& c);
 hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s);

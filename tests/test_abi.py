@@ -177,7 +177,20 @@ def test_decode_validation(lib):
     assert _decode(L, C, q=0) == B.QSVD_ERR_INVALID_ARG
     assert _decode(L, cache_struct(r=256)) == B.QSVD_ERR_INVALID_ARG
     assert _decode(L, cache_struct(max_len=0)) == B.QSVD_ERR_INVALID_ARG
-    assert _decode(layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64), C) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode(layer_struct(n_q_heads=80, n_kv_heads=8, head_dim=64), C) == B.QSVD_ERR_UNSUPPORTED
+    # more than 32 query heads: absorbed form only (16-head blocks), r a multiple of 128
+    wide = layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64)
+    assert _decode(wide, C, mode=B.QSVD_ATTN_RECONSTRUCT) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode(layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64, r=192), cache_struct(r=192)) == \
+        B.QSVD_ERR_UNSUPPORTED
+    assert _decode(layer_struct(r=3200), cache_struct(r=3200), mode=B.QSVD_ATTN_ABSORBED) == B.QSVD_ERR_UNSUPPORTED
+    # three head blocks x 64 sequences x 400 queries exceed the grid's rows
+    big = cache_struct(batch=64, max_len=2000, capacity=4096)
+    assert _decode(wide, big, q_len=400) == B.QSVD_ERR_UNSUPPORTED
+    assert B.qsvd_decode_workspace_size(wide, big, 400, B.QSVD_ATTN_ABSORBED) == 0
+    assert B.qsvd_decode_workspace_size(wide, big, 300, B.QSVD_ATTN_ABSORBED) > 0
+    assert _decode(wide, C, mode=B.QSVD_ATTN_ABSORBED, ws_bytes=B.qsvd_decode_workspace_size(wide, C, 1, 1) - 1) \
+        == B.QSVD_ERR_WORKSPACE
     assert _decode(layer_struct(head_dim=48, n_q_heads=4), C) == B.QSVD_ERR_UNSUPPORTED
     assert _decode(L, cache_struct(batch=65)) == B.QSVD_ERR_UNSUPPORTED
     assert _decode(L, cache_struct(fmt=B.QSVD_CACHE_I4, scale=FAKE), mode=B.QSVD_ATTN_RECONSTRUCT) == \

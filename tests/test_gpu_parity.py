@@ -533,6 +533,140 @@ def test_prefill_attention_llava7b_chunked(llava):
         assert ok, (b, i, info)
 
 
+def _random_factor_layer(L, seed, w_bits=8, w_group=0):
+    """A layer straight from random factors A (d x r) ~ N(0, 1/d) and
+    B (r x N) ~ N(0, 1/r), for wide shapes where an SVD would be slow (the
+    attention only sees B and the latent rows)."""
+    g = np.random.default_rng(seed)
+    A = g.standard_normal((L.d, L.r)) / np.sqrt(L.d)
+    Bm = g.standard_normal((L.r, L.N)) / np.sqrt(L.r)
+    ol = O.make_layer(A, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, w_bits, w_group)
+    pl = prep.quantize_layer(A, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, w_bits, w_group)
+    return ol, B.DeviceLayer(pl)
+
+
+def _prefilled_caches(wl, fmt, prior, cap):
+    """Oracle and device caches holding synthetic rows at the given lengths."""
+    L = wl.layer
+    batch = len(prior)
+    oc = O.LatentCache(fmt, batch, cap, L.r)
+    dc = B.DeviceCache(fmt, batch, cap, L.r, prior)
+    rows = gen.latent_rows(wl, batch, cap)
+    if fmt == O.CACHE_F16:
+        for b, n in enumerate(prior):
+            if n:
+                oc.append(b, rows[b, :n])
+        dc.data.copy_(H.dev(np.where(np.arange(cap)[None, :, None] < np.array(prior)[:, None, None], rows, 0)))
+        return oc, dc
+    bits = 4 if fmt == O.CACHE_I4 else 8
+    data = np.zeros((batch, cap, L.r // 2 if bits == 4 else L.r), np.uint8)
+    scale = np.zeros((batch, cap), np.float32)
+    for b, n in enumerate(prior):
+        if n:
+            codes, sc = O.quantize_act(rows[b, :n], bits)
+            oc.append(b, None, codes, sc)
+            data[b, :n] = O.pack_int4(codes) if bits == 4 else codes.view(np.uint8)
+            scale[b, :n] = sc
+    dc.data.copy_(H.dev(data.view(np.int8) if bits == 8 else data))
+    dc.scale.copy_(H.dev(scale))
+    return oc, dc
+
+
+def _append_new_rows(ol, dl, oc, dc, X, q_len):
+    """Project X (batch * q_len rows, sequence-major) on both sides and append
+    the new latent rows in the cache's format; returns (oracle Q, device Q)."""
+    torch = H.torch()
+    batch = dc.batch
+    ref = O.prefill(ol, X, 8)
+    p = H.Prefill(dl, X.shape[0], mask=B.QSVD_OUT_Q, debug=False).run(H.dev(X))
+    if oc.fmt == O.CACHE_F16:
+        new_o = [(ref["C_h"][b * q_len:(b + 1) * q_len],) for b in range(batch)]
+        H.append(dc, c_h=p.c_h, n_new=q_len)
+    elif oc.fmt == O.CACHE_I8:
+        new_o = [(None, ref["cq"][b * q_len:(b + 1) * q_len], ref["sc"][b * q_len:(b + 1) * q_len])
+                 for b in range(batch)]
+        H.append(dc, cq=p.cq, sc=p.sc, n_new=q_len)
+    else:
+        q4, s4 = O.quantize_act(ref["C_h"], 4)
+        new_o = [(None, q4[b * q_len:(b + 1) * q_len], s4[b * q_len:(b + 1) * q_len]) for b in range(batch)]
+        r = oc.r
+        cq4 = torch.empty((X.shape[0], r // 2), dtype=torch.uint8, device="cuda")
+        sc4 = torch.empty((X.shape[0],), dtype=torch.float32, device="cuda")
+        B.check(B.qsvd_quantize_act(B.ptr(p.c_h), X.shape[0], r, r, 4, 1.0, B.ptr(cq4), B.ptr(sc4),
+                                    B.stream_handle()))
+        H.append(dc, cq=cq4, sc=sc4, n_new=q_len)
+    for b in range(batch):
+        oc.append(b, *new_o[b])
+    return ref["Q"], p.q
+
+
+FMTS = [O.CACHE_F16, O.CACHE_I8, O.CACHE_I4]
+FMT_IDS = ["f16", "i8", "i4"]
+
+
+@pytest.mark.parametrize("fmt", FMTS, ids=FMT_IDS)
+@pytest.mark.parametrize("r", [1152, 2176])
+def test_decode_wide_heads(fmt, r):
+    """40 query heads over 8 key/value heads (more than one 32-head block) at
+    ranks 1152 and 2176 (128-column units that do not split evenly over the
+    waves): the 16-head-block attention, ragged prior lengths 1 / 130 / 777,
+    one decode step, every cache format."""
+    L = configs.LayerShape(d=256, n_q_heads=40, n_kv_heads=8, head_dim=128, r=r)
+    ol, dl = _random_factor_layer(L, 4000 + r)
+    wl = configs.Workload(96, "wide-test", L, "gaussian", 8, 0, 8, fmt)
+    prior = [1, 130, 777]
+    oc, dc = _prefilled_caches(wl, fmt, prior, max(prior) + 1)
+    X = gen.decode_activations(wl, 0, batch=len(prior))
+    Qo, Qd = _append_new_rows(ol, dl, oc, dc, X, 1)
+    ref = O.attention_reference(ol, oc, Qo[:, None, :], 1)[:, 0, :]
+    H.say(f"decode wide heads fmt={fmt} r={r}")
+    out = H.host(H.decode_attention(dl, dc, Qd, B.QSVD_ATTN_AUTO))
+    ok, info = H.close_enough(out, ref)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+    assert np.array_equal(H.host(dc.data).view(np.uint8), oc.data.view(np.uint8))
+
+
+@pytest.mark.parametrize("fmt", [O.CACHE_F16, O.CACHE_I4], ids=["f16", "i4"])
+def test_decode_rank_3072_and_2048(fmt):
+    """The widest ranks of the 13B-shaped stack: r = 3072 with 40 heads (three
+    128-column units per wave) and r = 2048 with 32 heads (more than a 32-head
+    block's registers hold, so the 16-head variant also serves <= 32 heads)."""
+    for heads, kv, r in ((40, 40, 3072), (32, 32, 2048)):
+        L = configs.LayerShape(d=256, n_q_heads=heads, n_kv_heads=kv, head_dim=128, r=r)
+        ol, dl = _random_factor_layer(L, 5000 + r)
+        wl = configs.Workload(96, "wide-test", L, "gaussian", 8, 0, 8, fmt)
+        prior = [600, 64]
+        oc, dc = _prefilled_caches(wl, fmt, prior, max(prior) + 1)
+        X = gen.decode_activations(wl, 1, batch=len(prior))
+        Qo, Qd = _append_new_rows(ol, dl, oc, dc, X, 1)
+        ref = O.attention_reference(ol, oc, Qo[:, None, :], 1)[:, 0, :]
+        H.say(f"decode heads={heads} r={r} fmt={fmt}")
+        out = H.host(H.decode_attention(dl, dc, Qd, B.QSVD_ATTN_AUTO))
+        ok, info = H.close_enough(out, ref)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (heads, r, info)
+
+
+def test_prefill_attention_wide_int4(fmt=O.CACHE_I4):
+    """q_len = 6 causal queries per sequence through the 16-head variant:
+    40 heads, r = 1664, int4 cache, prior lengths 0 / 200."""
+    L = configs.LayerShape(d=256, n_q_heads=40, n_kv_heads=40, head_dim=128, r=1664)
+    ol, dl = _random_factor_layer(L, 6664)
+    wl = configs.Workload(96, "wide-test", L, "gaussian", 8, 0, 8, fmt)
+    prior, q_len = [0, 200], 6
+    oc, dc = _prefilled_caches(wl, fmt, prior, max(prior) + q_len)
+    X = gen.decode_activations(wl, 2, batch=len(prior) * q_len)
+    Qo, Qd = _append_new_rows(ol, dl, oc, dc, X, q_len)
+    nq = L.n_q_heads * L.head_dim
+    ref = O.attention_reference(ol, oc, Qo.reshape(len(prior), q_len, nq), q_len)
+    H.say("prefill attention wide int4 q_len=6")
+    out = H.host(H.decode_attention(dl, dc, Qd.reshape(len(prior), q_len, nq), B.QSVD_ATTN_AUTO, q_len=q_len))
+    ok, info = H.close_enough(out, ref)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+
+
 def test_decode_gqa_int4_cache_ragged(gqa):
     """Int4 latent cache (4-bit per-token codes of C with fp32 scales, two codes
     per byte): ragged prior lengths 3 / 50 / 97 of synthetic rows, then 3 decode

@@ -66,6 +66,9 @@ class Workload:
 
 _LLAVA7B = LayerShape(d=4096, n_q_heads=32, n_kv_heads=32, head_dim=128, r=1536)
 _QWEN2VL7B = LayerShape(d=3584, n_q_heads=28, n_kv_heads=4, head_dim=128, r=1024)
+# 13B-shaped stack layer; r here is nominal, each layer's rank comes from
+# gen.stack_ranks (seeded, multiples of 128 in [1024, 3072]).
+_LLAVA13B = LayerShape(d=5120, n_q_heads=40, n_kv_heads=40, head_dim=128, r=2048)
 
 WORKLOADS = {
     # Tiny single layer: correctness case the oracle finishes in seconds.
@@ -85,6 +88,12 @@ WORKLOADS = {
     4: Workload(4, "qwen2vl7b_gqa_decode", _QWEN2VL7B, spectrum="decay", w_bits=4, w_group=128,
                 a_bits=8, cache_fmt=CACHE_I8, outlier_count=36, outlier_scale=30.0,
                 decode_batch=32, decode_ctx=8192, decode_steps=64, n_layers=28),
+    # LLaVA-1.5-13B-shaped stack of 40 layers with per-layer ranks, W4A4 (int4
+    # per-token activations, int4 per-group-128 weights), int4 latent cache;
+    # prefill of 8 x (576 image + 128 text) tokens, decode at batch 8 over 4096.
+    5: Workload(5, "llava13b_stack", _LLAVA13B, spectrum="decay", w_bits=4, w_group=128, a_bits=4,
+                cache_fmt=CACHE_I4, prefill_batch=8, prefill_tokens=(576, 128), outlier_count=51,
+                outlier_scale=30.0, decode_batch=8, decode_ctx=4096, decode_steps=64, n_layers=40),
 }
 
 

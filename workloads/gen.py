@@ -2,7 +2,7 @@
 
 Seeds are ``numpy.random.default_rng(16292 + 100*cfg + role + 1000*layer)``.
 Roles: 0 weights, 1 prefill activations, 2 outlier channels, 3 synthetic
-cache fill, 4+t decode input of step t.
+cache fill, 4+t decode input of step t, 99 per-layer ranks of a stack.
 
 Nothing here belongs to the method: weights with a prescribed spectrum are
 built as U diag(sigma) V^T from orthonormal factors (so for those workloads the
@@ -15,6 +15,41 @@ import numpy as np
 from .configs import Workload
 
 ROLE_W, ROLE_X, ROLE_OUTLIER, ROLE_FILL, ROLE_DECODE0 = 0, 1, 2, 3, 4
+ROLE_RANKS = 99     # per-layer ranks of a stack (drawn once per workload, layer 0)
+
+
+def stack_ranks(wl: Workload) -> list:
+    """Per-layer ranks of a multi-layer stack, standing in for an importance-
+    based rank allocation: multiples of 128 drawn uniformly in [1024, 3072]
+    (multiples of the 128-element weight group, so every group along r is
+    whole)."""
+    g = rng_for(wl, ROLE_RANKS)
+    return [int(128 * k) for k in g.integers(8, 25, size=wl.n_layers)]
+
+
+def with_rank(wl: Workload, r: int) -> Workload:
+    """The same workload with the layer rank replaced (one layer of a stack)."""
+    from dataclasses import replace
+    return replace(wl, layer=replace(wl.layer, r=int(r)))
+
+
+def weight_codes_device(seed: int, rows: int, cols: int, bits: int, groups: int, device="cuda"):
+    """Device-side weight codes and positive scales for timing-only stacks:
+    codes [rows][cols] (int8, or int4 packed two per byte along cols, low
+    nibble first) drawn as a rounded N(0, (qmax/3)^2) clipped to +-qmax, the
+    spread round-to-nearest leaves for Gaussian weights; scales [groups][rows]
+    fp32 around 0.02 / qmax (one row when groups is 1)."""
+    import torch
+    qm = (1 << (bits - 1)) - 1
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    z = torch.randn((rows, cols), generator=g, device=device) * (qm / 3.0)
+    c = torch.clamp(torch.round(z), -qm, qm).to(torch.int8)
+    if bits == 4:
+        u = (c.to(torch.int16) & 0xF).to(torch.uint8)
+        c = (u[:, 0::2] | (u[:, 1::2] << 4)).contiguous()
+    s = (torch.rand((groups, rows), generator=g, device=device) * 0.5 + 0.75) * (0.02 / qm)
+    return c, s.to(torch.float32).contiguous()
 
 
 def rng_for(wl: Workload, role: int, layer: int = 0) -> np.random.Generator:
@@ -145,21 +180,31 @@ def latent_rows_device(wl: Workload, batch: int, length: int, seed: int, out=Non
     return out
 
 
-def latent_codes_device(wl: Workload, batch: int, length: int, seed: int, codes=None, scales=None, device="cuda"):
-    """Device-side variant of :func:`latent_codes` for large pre-filled int8
+def latent_codes_device(wl: Workload, batch: int, length: int, seed: int, codes=None, scales=None, device="cuda",
+                        bits: int = 8):
+    """Device-side variant of :func:`latent_codes` for large pre-filled integer
     caches (torch's seeded generator on the GPU): writes codes into
-    ``codes[:, :length]`` (int8 [batch, >=length, r]) and per-token scales into
-    ``scales[:, :length]``."""
+    ``codes[:, :length]`` (int8 [batch, >=length, r], or for bits 4 uint8
+    [batch, >=length, r/2] with two codes per byte, low nibble first) and
+    per-token scales into ``scales[:, :length]``.  Column j spreads in
+    proportion to sigma_j with column 0 at the top code; the scales put
+    code * scale at the magnitude of the fp16 latent rows."""
     import torch
     r = wl.layer.r
+    qm = (1 << (bits - 1)) - 1
+    spread = 40.0 * qm / 127.0
     std = np.sqrt(spectrum(wl)[:r]) if wl.spectrum == "decay" else np.ones(r)
-    col = torch.tensor(40.0 * std / std[0], dtype=torch.float32, device=device)
+    col = torch.tensor(spread * std / std[0], dtype=torch.float32, device=device)
     g = torch.Generator(device=device)
     g.manual_seed(int(seed))
     for b in range(batch):
         z = torch.randn((length, r), generator=g, device=device) * col
-        c = torch.clamp(torch.round(z), -127, 127).to(torch.int8)
-        c[:, 0] = 127
-        codes[b, :length] = c
+        c = torch.clamp(torch.round(z), -qm, qm).to(torch.int8)
+        c[:, 0] = qm
+        if bits == 4:
+            u = (c.to(torch.int16) & 0xF).to(torch.uint8)
+            codes[b, :length] = u[:, 0::2] | (u[:, 1::2] << 4)
+        else:
+            codes[b, :length] = c
         u = torch.rand((length,), generator=g, device=device) * 0.45 + 0.8
-        scales[b, :length] = u * float(std[0] / 40.0)
+        scales[b, :length] = u * float(std[0] / spread)
