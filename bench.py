@@ -45,11 +45,14 @@ def parse():
     ap.add_argument("--steps", type=int, default=N_LAYERS * DECODE_VISITS)
     ap.add_argument("--warmup", type=int, default=64)
     ap.add_argument("--prefill-steps", type=int, default=20)
+    ap.add_argument("--stack-passes", type=int, default=3, help="passes of the 40-layer prefill stack")
+    ap.add_argument("--stack-steps", type=int, default=64, help="decode steps through the 40-layer stack")
     ap.add_argument("--mode", choices=["auto", "absorbed", "reconstruct"], default="auto")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without the kernel events")
-    ap.add_argument("--legs", default="decode,prefill,gqa",
-                    help="comma list of legs to run: decode, prefill, gqa (Qwen2-VL-shaped decode)")
+    ap.add_argument("--legs", default="decode,prefill,gqa,stack",
+                    help="comma list of legs to run: decode, prefill, gqa (Qwen2-VL-shaped decode), "
+                         "stack (13B-shaped 40-layer prefill and decode)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
                     help="also run a plain device copy of MB megabytes (calibrates memory counters)")
     return ap.parse_args()
@@ -324,6 +327,206 @@ def bench_prefill(args, wl2, host_layer):
                          "kernel": "gemm_i8 (X W^d and Q(C) W^u)", "launches": n}}
 
 
+def stack_layers(wl5):
+    """The 13B-shaped stack: one layer per seeded rank, int4 weight codes and
+    per-group scales drawn on the device (timing only; the stack's shapes,
+    bits and groups are the configuration's, its values are not those of an
+    SVD)."""
+    from paper_2510_16292_amd import binding as B
+    from workloads import gen
+    L, G = wl5.layer, wl5.w_group
+    ranks = gen.stack_ranks(wl5)
+    layers = []
+    for li, r in enumerate(ranks):
+        a_t, s_a = gen.weight_codes_device(50000 + 2 * li, r, L.d, wl5.w_bits, L.d // G)
+        b_t, s_b = gen.weight_codes_device(50001 + 2 * li, L.N, r, wl5.w_bits, r // G)
+        layers.append(B.DeviceLayer.from_device(L.d, r, L.n_q_heads, L.n_kv_heads, L.head_dim, wl5.w_bits, G,
+                                                a_t, s_a, b_t, s_b))
+    return ranks, layers
+
+
+def bench_stack_prefill(args, wl5, ranks, layers):
+    """Prefill of 8 x (576 + 128) tokens through the 40 layers' quantized QKV
+    projections (W4A4): per layer the 4-bit activation quantizer, X W^d with
+    the latent quantization fused, Q(C) W^u into Q, K, V."""
+    import torch
+
+    from paper_2510_16292_amd import binding as B
+    from workloads import gen
+    L = wl5.layer
+    M, d, nq, nkv = wl5.prefill_M, L.d, L.n_q, L.n_kv
+    rmax = max(ranks)
+    xs = [torch.from_numpy(gen.prefill_activations(wl5, layer=li)).cuda() for li in range(2)]
+    xq = torch.empty((M, d // 2), dtype=torch.uint8, device="cuda")
+    sx = torch.empty((M,), dtype=torch.float32, device="cuda")
+    c_h = torch.empty((M, rmax), dtype=torch.float16, device="cuda")
+    cq = torch.empty((M, rmax // 2), dtype=torch.uint8, device="cuda")
+    sc = torch.empty((M,), dtype=torch.float32, device="cuda")
+    q = torch.empty((M, nq), dtype=torch.float16, device="cuda")
+    k = torch.empty((M, nkv), dtype=torch.float16, device="cuda")
+    v = torch.empty((M, nkv), dtype=torch.float16, device="cuda")
+    lib, s, P = B.lib(), B.stream_handle(), B.ptr
+    xs_p = [P(x) for x in xs]
+
+    def stack_pass():
+        for li, dl in enumerate(layers):
+            st = lib.qsvd_quantize_act(xs_p[li % 2], M, d, d, 4, 1.0, P(xq), P(sx), s)
+            st |= lib.qsvd_lowrank_qkv_prefill(dl.c, P(xq), P(sx), M, 4, 7, P(c_h), P(cq), P(sc), P(q), P(k), P(v),
+                                               0, 0, 0, 0, s)
+            if st:
+                raise B.QsvdError(st, B.last_error())
+
+    stack_pass()
+    torch.cuda.synchronize()
+    B.profile_reset()
+    B.profile_enable(True, "gemm")
+    t0 = time.perf_counter()
+    for _ in range(args.stack_passes):
+        stack_pass()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    B.profile_enable(False)
+    gms, n = B.profile_read("gemm")
+    B.profile_reset()
+    ops = sum(2.0 * M * r * (d + L.N) for r in ranks)
+    gemm_s = gms * 1e-3 / args.stack_passes
+    pass_s = (t1 - t0) / args.stack_passes
+    tops = ops / gemm_s / 1e12
+    del xs, xq, c_h, cq, q, k, v
+    return {"value": round(tops, 1), "unit": "TOPS", "ms_per_pass": round(pass_s * 1e3, 3),
+            "gemm_ms_per_pass": round(gemm_s * 1e3, 3), "call_tops": round(ops / pass_s / 1e12, 1),
+            "tokens": M, "layers": len(ranks), "top_per_pass": round(ops / 1e12, 3),
+            "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
+                         "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None,
+                         "kernel": "gemm_q4_pipe (X W^d and Q(C) W^u, int4 x int4)", "launches": n}}
+
+
+def bench_stack_decode(args, wl5, ranks, layers):
+    """Decode through the 40-layer stack at batch 8 over 4096 cached tokens
+    (int4 latent caches, W4A4 projections): per layer the 4-bit quantizer, the
+    Q-only projection with the latent quantization fused, the append, and the
+    absorbed attention (16-head blocks).  Timed eagerly and as one captured
+    graph of the 40 layers replayed once per step."""
+    import torch
+
+    from paper_2510_16292_amd import binding as B
+    from workloads import gen
+    L = wl5.layer
+    batch, ctx0, steps = wl5.decode_batch, wl5.decode_ctx, args.stack_steps
+    d, nq = L.d, L.n_q
+    rmax = max(ranks)
+    cap = ctx0 + steps + 4
+    caches = []
+    for li, r in enumerate(ranks):
+        c = B.DeviceCache(B.QSVD_CACHE_I4, batch, cap, r, [ctx0] * batch)
+        gen.latent_codes_device(gen.with_rank(wl5, r), batch, ctx0, seed=3000 + li, codes=c.data, scales=c.scale,
+                                bits=4)
+        caches.append(c)
+    xs = [torch.from_numpy(gen.decode_activations(wl5, t, batch=batch)).cuda() for t in range(8)]
+    xq = torch.empty((batch, d // 2), dtype=torch.uint8, device="cuda")
+    sx = torch.empty((batch,), dtype=torch.float32, device="cuda")
+    c_h = torch.empty((batch, rmax), dtype=torch.float16, device="cuda")
+    cq = torch.empty((batch, rmax // 2), dtype=torch.uint8, device="cuda")
+    sc = torch.empty((batch,), dtype=torch.float32, device="cuda")
+    q = torch.empty((batch, nq), dtype=torch.float16, device="cuda")
+    out = torch.empty_like(q)
+    for c in caches:
+        c.c.max_len = cap - 1
+    dws_b = max(B.qsvd_decode_workspace_size(l.c, c.c, 1, B.QSVD_ATTN_AUTO) for l, c in zip(layers, caches))
+    dws = torch.empty((dws_b,), dtype=torch.uint8, device="cuda")
+    lib, P = B.lib(), B.ptr
+    xs_p = [P(x) for x in xs]
+
+    def step_all(s):
+        for li, (dl, c) in enumerate(zip(layers, caches)):
+            st = lib.qsvd_quantize_act(xs_p[li % 8], batch, d, d, 4, 1.0, P(xq), P(sx), s)
+            st |= lib.qsvd_lowrank_qkv_prefill(dl.c, P(xq), P(sx), batch, 4, B.QSVD_OUT_Q, P(c_h), P(cq), P(sc),
+                                               P(q), 0, 0, 0, 0, 0, 0, s)
+            st |= lib.qsvd_latent_cache_append(c.c, 0, P(cq), P(sc), 1, s)
+            st |= lib.qsvd_latent_decode_attention(dl.c, c.c, P(q), 1, B.QSVD_ATTN_AUTO, 0.0, P(out), P(dws), dws_b,
+                                                   s)
+            if st:
+                raise B.QsvdError(st, B.last_error())
+
+    def reset(max_len):
+        torch.cuda.synchronize()
+        for c in caches:
+            c.seq_len.fill_(ctx0)
+            c.c.max_len = max_len
+        torch.cuda.synchronize()
+
+    # Launch grids follow each cache's host max_len: holding it at the final
+    # length makes every step (eager or replayed) use the same configuration;
+    # chunks past a sequence's device length return at once.
+    s = B.stream_handle()
+
+    def eager_steps(profile):
+        reset(ctx0 + steps - 1)
+        if profile:
+            B.profile_reset()
+            B.profile_enable(True, "latent_attn")
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step_all(s)
+            for c in caches:
+                c.c.max_len = ctx0 + steps - 1
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        B.profile_enable(False)
+        return (t1 - t0) / steps
+
+    reset(ctx0 + steps - 1)
+    step_all(s)
+    eager_s = eager_steps(False)
+    eager_steps(True)
+    kms, n = B.profile_read("latent_attn")
+    B.profile_reset()
+    ctx_mean = ctx0 + (steps + 1) / 2.0
+    attn_bytes = sum(batch * ctx_mean * (r // 2 + 4) for r in ranks) * steps
+    # the same step captured once as a graph of all layers, replayed per step
+    reset(ctx0 + steps - 1)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step_all(B.stream_handle())
+    reset(ctx0 + steps)
+    g.replay()
+    reset(ctx0 + steps)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.replay()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    graph_s = (t1 - t0) / steps
+    res = {"value": round(batch / graph_s, 1), "unit": "tokens/s", "ms_per_step": round(graph_s * 1e3, 4),
+           "eager_ms_per_step": round(eager_s * 1e3, 4), "eager_tokens_per_s": round(batch / eager_s, 1),
+           "steps": steps, "layers": len(ranks), "batch": batch, "mean_context": round(ctx_mean, 1),
+           "us_per_layer_step": round(graph_s * 1e6 / len(ranks), 2)}
+    if n:
+        avg_s = kms * 1e-3 / n
+        achieved = attn_bytes / (kms * 1e-3) / 1e9
+        res["attn_kernel_us"] = round(avg_s * 1e6, 2)
+        res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                           "kernel": "latent_attn_h16_kernel (int4 cache)", "launches": n,
+                           "bytes_per_launch": int(attn_bytes / n)}
+    del g, caches
+    torch.cuda.empty_cache()
+    return res
+
+
+def bench_stack(args):
+    from workloads import configs
+    wl5 = configs.get(5)
+    ranks, layers = stack_layers(wl5)
+    out = {"workload": "llava-1.5-13b-shaped stack: 40 layers, d=5120, 40 heads x 128, per-layer ranks "
+                       f"{min(ranks)}..{max(ranks)} (mean {sum(ranks) / len(ranks):.0f}), W4A4 with int4 "
+                       "per-group-128 weights, int4 latent cache; weight codes drawn on the device",
+           "prefill": bench_stack_prefill(args, wl5, ranks, layers)}
+    print(f"[bench] stack prefill done: {out['prefill']['value']} TOPS", file=sys.stderr, flush=True)
+    out["decode"] = bench_stack_decode(args, wl5, ranks, layers)
+    return out
+
+
 def cpu_baseline_decode(wl, factors):
     """The oracle, as it stands, on one full decode step of the 16-sequence
     batch at context 4096 (projection, append, attention in the plain
@@ -393,8 +596,13 @@ def main():
     if "gqa" in legs:
         gqa = bench_decode_gqa(args)
         print(f"[bench] gqa decode done: {gqa['ms_per_step']:.4f} ms/step", file=sys.stderr, flush=True)
+    stack = None
+    if "stack" in legs:
+        stack = bench_stack(args)
+        print(f"[bench] stack decode done: {stack['decode']['ms_per_step']:.4f} ms/step", file=sys.stderr, flush=True)
     if dec is None:
-        print(json.dumps({k: v for k, v in (("prefill", pre), ("gqa_decode", gqa)) if v is not None}), flush=True)
+        print(json.dumps({k: v for k, v in (("prefill", pre), ("gqa_decode", gqa), ("stack13b", stack))
+                          if v is not None}), flush=True)
         return
     line = {
         "metric": METRIC,
@@ -423,6 +631,8 @@ def main():
         line.pop("prefill")
     if gqa is not None:
         line["gqa_decode"] = gqa
+    if stack is not None:
+        line["stack13b"] = stack
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline_decode(wl3, factors)

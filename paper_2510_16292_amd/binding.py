@@ -165,6 +165,19 @@ class DeviceLayer:
         self.c = QsvdLayer(self.d, self.r, self.n_q_heads, self.n_kv_heads, self.head_dim, self.w_bits,
                            self.w_group, ptr(self.a_t), ptr(self.s_a), ptr(self.b_t), ptr(self.s_b))
 
+    @classmethod
+    def from_device(cls, d, r, n_q_heads, n_kv_heads, head_dim, w_bits, w_group, a_t, s_a, b_t, s_b):
+        """Wrap weight codes and scales already in device memory (same layouts
+        as a prepared layer: a_t [r][d], s_a, b_t [N][r], s_b)."""
+        self = cls.__new__(cls)
+        self.d, self.r = d, r
+        self.n_q_heads, self.n_kv_heads, self.head_dim = n_q_heads, n_kv_heads, head_dim
+        self.w_bits, self.w_group = w_bits, w_group
+        self.a_t, self.s_a, self.b_t, self.s_b = a_t, s_a, b_t, s_b
+        self.c = QsvdLayer(d, r, n_q_heads, n_kv_heads, head_dim, w_bits, w_group, ptr(a_t), ptr(s_a), ptr(b_t),
+                           ptr(s_b))
+        return self
+
     @property
     def N(self):
         return (self.n_q_heads + 2 * self.n_kv_heads) * self.head_dim

@@ -29,6 +29,45 @@ constexpr int kMaxChunks = 256;  // context chunks per sequence the merge suppor
 constexpr int kMaxAbsorbedHeads = 64;   // query heads per sequence in the absorbed form
 
 // ---------------------------------------------------------------------------
+// Exact integer code -> fp16 conversion by exponent bias: a code made unsigned
+// (offset binary, by flipping its sign bit) is placed in the low mantissa bits
+// of 1024.0 (0x6400), where every integer below 1024 is exact, and the bias is
+// removed with one packed fp16 operation per two codes.
+// ---------------------------------------------------------------------------
+__device__ inline f16x2 bias_sub(uint32_t d, f16x2 mul, f16x2 add) {
+  return __builtin_elementwise_fma(__builtin_bit_cast(f16x2, d), mul, add);
+}
+
+// 8 int8 codes (bytes of w0 then w1, lowest first) -> fp16, in order.
+__device__ inline f16x8 cvt_i8x8(uint32_t w0, uint32_t w1) {
+  const uint32_t u0 = w0 ^ 0x80808080u, u1 = w1 ^ 0x80808080u;
+  const f16x2 one = {(_Float16)1.f, (_Float16)1.f}, off = {(_Float16)-1152.f, (_Float16)-1152.f};
+  // perm: byte k of the result is byte sel_k of (0x64646464 : u), 4 = a 0x64 byte
+  const f16x2 a = bias_sub(__builtin_amdgcn_perm(0x64646464u, u0, 0x04010400u), one, off);
+  const f16x2 b = bias_sub(__builtin_amdgcn_perm(0x64646464u, u0, 0x04030402u), one, off);
+  const f16x2 c = bias_sub(__builtin_amdgcn_perm(0x64646464u, u1, 0x04010400u), one, off);
+  const f16x2 d = bias_sub(__builtin_amdgcn_perm(0x64646464u, u1, 0x04030402u), one, off);
+  return f16x8{a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
+}
+
+// 8 int4 codes (nibbles of w, lowest first) -> fp16, in order.  Byte i holds
+// codes 2i (low nibble) and 2i + 1 (high nibble): the low one lands in
+// 1024 + n, the high one in 1024 + 16 n, undone by (x * 1/16 - 72).
+__device__ inline f16x8 cvt_i4x8(uint32_t w) {
+  const uint32_t u = w ^ 0x88888888u;
+  const f16x2 mul = {(_Float16)1.f, (_Float16)0.0625f}, off = {(_Float16)-1032.f, (_Float16)-72.f};
+  f16x8 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t sel = 0x04000400u | ((uint32_t)i << 16) | (uint32_t)i;
+    const f16x2 h = bias_sub(__builtin_amdgcn_perm(0x64646464u, u, sel) & 0xFFF0FF0Fu, mul, off);
+    r[2 * i] = h[0];
+    r[2 * i + 1] = h[1];
+  }
+  return r;
+}
+
+// ---------------------------------------------------------------------------
 // Weight code access (int8 or packed int4), transposed layout [N][r].
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float wcode(const uint8_t* bt, int32_t r, int32_t n, int32_t j, int bits) {
@@ -285,19 +324,11 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
 #pragma unroll
       for (int i = 0; i < NLD; ++i) {
         if constexpr (I4C) {
-          const uint32_t wv[2] = {raw[i].x, raw[i].y};
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            cf[2 * i][e] = (_Float16)(float)(((int)(wv[0] << (28 - 4 * e))) >> 28);
-            cf[2 * i + 1][e] = (_Float16)(float)(((int)(wv[1] << (28 - 4 * e))) >> 28);
-          }
+          cf[2 * i] = cvt_i4x8(raw[i].x);
+          cf[2 * i + 1] = cvt_i4x8(raw[i].y);
         } else {
-          const uint32_t wv[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            cf[2 * i][e] = (_Float16)(float)(int8_t)(wv[e >> 2] >> (8 * (e & 3)));
-            cf[2 * i + 1][e] = (_Float16)(float)(int8_t)(wv[2 + (e >> 2)] >> (8 * (e & 3)));
-          }
+          cf[2 * i] = cvt_i8x8(raw[i].x, raw[i].y);
+          cf[2 * i + 1] = cvt_i8x8(raw[i].z, raw[i].w);
         }
       }
     }
@@ -450,6 +481,7 @@ latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restric
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
+  const int wu = __builtin_amdgcn_readfirstlane(w);     // wave-uniform copy: scalar branches below
   _Float16* cst = reinterpret_cast<_Float16*>(smem) + w * kH16Tile * CST;
   f32x4* spart = reinterpret_cast<f32x4*>(smem + (size_t)NW * kH16Tile * CST * 2);
   f32x4* ssum = spart + NW * 64;
@@ -463,7 +495,7 @@ latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restric
   const int t_end = min(L, t_begin + chunk);
   // this wave's latent units [u0, u0 + nu) of 128 columns (nu <= UMAX, may be 0)
   const int m_units = r >> 7;
-  const int u0 = (w * m_units) / NW, nu = ((w + 1) * m_units) / NW - u0;
+  const int u0 = (wu * m_units) / NW, nu = ((wu + 1) * m_units) / NW - u0;
   const int slice0 = 128 * u0, ksn = 4 * nu;
   const int nldn = F16C ? ksn : (I4C ? nu : ksn / 2);
 
@@ -523,17 +555,10 @@ latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restric
         cf = __builtin_bit_cast(f16x8, raw[ks]);
       } else if constexpr (I4C) {
         const uint4 q4 = raw[ks >> 2];
-        const uint32_t wv = (ks & 3) == 0 ? q4.x : (ks & 3) == 1 ? q4.y : (ks & 3) == 2 ? q4.z : q4.w;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) cf[e] = (_Float16)(float)(((int)(wv << (28 - 4 * e))) >> 28);
+        cf = cvt_i4x8((ks & 3) == 0 ? q4.x : (ks & 3) == 1 ? q4.y : (ks & 3) == 2 ? q4.z : q4.w);
       } else {
         const uint4 q8 = raw[ks >> 1];
-        const uint32_t w0 = (ks & 1) ? q8.z : q8.x, w1 = (ks & 1) ? q8.w : q8.y;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          cf[e] = (_Float16)(float)(int8_t)(w0 >> (8 * e));
-          cf[4 + e] = (_Float16)(float)(int8_t)(w1 >> (8 * e));
-        }
+        cf = (ks & 1) ? cvt_i8x8(q8.z, q8.w) : cvt_i8x8(q8.x, q8.y);
       }
       sacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(cf, qf[ks], sacc, 0, 0, 0);
       *reinterpret_cast<f16x8*>(cst + l16 * CST + kcol(ks, g)) = cf;
@@ -908,7 +933,9 @@ static AbsorbPlan plan_absorbed(const qsvd_layer& w, const qsvd_cache& c, int32_
   p.hp = p.hb * p.n_hb;
   const int64_t rows = (int64_t)c.batch * q_len;      // one query row per (sequence, query)
   const int64_t grows = rows * p.n_hb;                // attention grid rows
-  p.n0 = target_chunks((int)grows);
+  // 32-head blocks: about one round of workgroups over the 256 CUs; 16-head
+  // blocks (one workgroup per CU): at most one round
+  p.n0 = p.hb == kHeadBlk ? target_chunks((int)grows) : (int)(grows >= 256 ? 1 : 256 / grows);
   const int len = c.max_len > 0 ? c.max_len : 1;
   int ch = (len + p.n0 - 1) / p.n0;
   ch = ((ch + 15) / 16) * 16;
