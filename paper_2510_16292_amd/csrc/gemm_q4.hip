@@ -6,8 +6,9 @@
 // global_load_lds_dwordx4, NS stages of 64 contraction elements, one barrier
 // per stage) on 128 x 128 tiles of four 64 x 64 waves.  A stage row holds 64
 // codes: 64 bytes (int8) or 32 bytes (int4, element 2i in the low nibble of
-// byte i); int4 fragments are read 8 bytes at a time and widened to int8 in
-// registers before v_mfma_i32_32x32x32_i8, so every product is exact.
+// byte i); int4 fragments are read 8 bytes at a time and widened in registers
+// to int8 bytes holding 16 * code before v_mfma_i32_32x32x32_i8, so every
+// product is exact and the int32 sums are exact multiples of 16 or 256.
 //
 // Per-group scales (groups of G contraction elements, G a multiple of 64):
 // at the end of each group the int32 tile is folded into an fp32 tile as
@@ -49,30 +50,35 @@ __device__ __forceinline__ int q4_slot(int row, int chunk) {
   else return row * 32 + 16 * (chunk ^ ((row >> 3) & 1));
 }
 
-// 16 int4 codes (8 bytes) -> 16 int8.
+// 16 int4 codes (8 bytes, element 2i in the low nibble of byte i) -> 16 int8
+// holding 16 * code, in the element order 0,2,4,6, 1,3,5,7, 8,10,12,14,
+// 9,11,13,15: (w << 4) & 0xF0F0F0F0 moves every even element into the high
+// half of its byte and w & 0xF0F0F0F0 keeps every odd one there, so each
+// code's sign bit lands on bit 7 (three operations per eight codes).
 __device__ __forceinline__ i32x4 q4_widen(uint2 p) {
-  i32x4 o;
-  const uint32_t w[2] = {p.x, p.y};
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    uint32_t lo = 0, hi = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      lo |= (uint32_t)((((int)(w[h] << (28 - 4 * e))) >> 28) & 0xff) << (8 * e);
-      hi |= (uint32_t)((((int)(w[h] << (12 - 4 * e))) >> 28) & 0xff) << (8 * e);
-    }
-    o[2 * h] = (int32_t)lo;
-    o[2 * h + 1] = (int32_t)hi;
-  }
-  return o;
+  return i32x4{(int32_t)((p.x << 4) & 0xF0F0F0F0u), (int32_t)(p.x & 0xF0F0F0F0u),
+               (int32_t)((p.y << 4) & 0xF0F0F0F0u), (int32_t)(p.y & 0xF0F0F0F0u)};
+}
+
+// 16 int8 codes in element order -> the element order of q4_widen (one byte
+// permute per four codes), for an int8 operand multiplied with an int4 one.
+__device__ __forceinline__ i32x4 q4_interleave(i32x4 v) {
+  return i32x4{(int32_t)__builtin_amdgcn_perm((uint32_t)v[1], (uint32_t)v[0], 0x06040200u),
+               (int32_t)__builtin_amdgcn_perm((uint32_t)v[1], (uint32_t)v[0], 0x07050301u),
+               (int32_t)__builtin_amdgcn_perm((uint32_t)v[3], (uint32_t)v[2], 0x06040200u),
+               (int32_t)__builtin_amdgcn_perm((uint32_t)v[3], (uint32_t)v[2], 0x07050301u)};
 }
 
 // Fragment for sub-step kk (32 contraction elements) of a 32x32x32 MFMA: lane
-// (row, hl) supplies elements 32*kk + 16*hl .. +15 of its row.
-template <int BITS>
+// (row, hl) supplies elements 32*kk + 16*hl .. +15 of its row, in natural
+// order when both operands are int8, else in q4_widen's order (the same
+// order in both operands, so the sum runs over the same products).
+template <int BITS, int OTHER>
 __device__ __forceinline__ i32x4 q4_frag(const uint8_t* base, int row, int kk, int hl) {
   if constexpr (BITS == 8) {
-    return *reinterpret_cast<const i32x4*>(base + q4_slot<64>(row, 2 * kk + hl));
+    const i32x4 v = *reinterpret_cast<const i32x4*>(base + q4_slot<64>(row, 2 * kk + hl));
+    if constexpr (OTHER == 8) return v;
+    else return q4_interleave(v);
   } else {
     return q4_widen(*reinterpret_cast<const uint2*>(base + q4_slot<32>(row, kk) + 8 * hl));
   }
@@ -103,6 +109,9 @@ gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B
   constexpr int TI = QWM / 32, TJ = QWN / 32;
   extern __shared__ __attribute__((aligned(1024))) uint8_t q4_smem[];
   __shared__ __attribute__((aligned(16))) float s_rs[QBM];
+  // int4 operands enter the products as 16 * code: the int32 sums are exact
+  // multiples of 16 (or 256) and are shifted back exactly before use
+  constexpr int SH = (ABITS == 4 ? 4 : 0) + (BBITS == 4 ? 4 : 0);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wm = w >> 1, wn = w & 1;
   const int l32 = lane & 31, hl = lane >> 5;
@@ -177,9 +186,9 @@ gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
-      for (int i = 0; i < TI; ++i) af[kk][i] = q4_frag<ABITS>(sa, wm * QWM + 32 * i + l32, kk, hl);
+      for (int i = 0; i < TI; ++i) af[kk][i] = q4_frag<ABITS, BBITS>(sa, wm * QWM + 32 * i + l32, kk, hl);
 #pragma unroll
-      for (int j = 0; j < TJ; ++j) bf[kk][j] = q4_frag<BBITS>(sb, wn * QWN + 32 * j + l32, kk, hl);
+      for (int j = 0; j < TJ; ++j) bf[kk][j] = q4_frag<BBITS, ABITS>(sb, wn * QWN + 32 * j + l32, kk, hl);
     }
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
@@ -197,7 +206,7 @@ gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B
 #pragma unroll
           for (int j = 0; j < TJ; ++j) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) S[i][j][v] = add_rn(S[i][j][v], mul_rn((float)acc[i][j][v], gsc[j]));
+            for (int v = 0; v < 16; ++v) S[i][j][v] = add_rn(S[i][j][v], mul_rn((float)(acc[i][j][v] >> SH), gsc[j]));
             acc[i][j] = i32x16{};
           }
         if (gn * gsteps < nk) {
@@ -225,7 +234,7 @@ gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int v = 4 * vq + e;
-          const float y = GROUPED ? mul_rn(S[i][j][v], r4[e]) : mul_rn(mul_rn((float)acc[i][j][v], r4[e]), csn[j]);
+          const float y = GROUPED ? mul_rn(S[i][j][v], r4[e]) : mul_rn(mul_rn((float)(acc[i][j][v] >> SH), r4[e]), csn[j]);
           ost[(rl + e) * OST + 32 * j + l32] = to_f16(y);
         }
       }
