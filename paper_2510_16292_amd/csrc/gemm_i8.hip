@@ -48,7 +48,7 @@ __device__ __forceinline__ float dequant(int32_t acc, float rs, float cs) {
 }
 
 // ---------------------------------------------------------------------------
-// Pipelined kernel: BM x BN output tile per workgroup of 4 waves (2 x 2, each
+// Pipelined kernel: BM x BN output tile per workgroup of 4 or 8 waves (each
 // WM x WN), the contraction in stages of 64 bytes.  Operands go from global
 // memory straight into LDS (global_load_lds_dwordx4: lane i of a wave writes
 // 16 bytes at base + 16 i), NS stages deep, so NS - 1 stages are in flight
@@ -89,17 +89,20 @@ __device__ __forceinline__ int pipe_slot(int row, int chunk) {
 
 template <int BM, int BN, int WM, int WN, int NS>
 struct PipeCfg {
-  static_assert((BM / WM) * (BN / WN) == 4, "four waves");
+  static constexpr int kWaves = (BM / WM) * (BN / WN);
+  static_assert(kWaves == 4 || kWaves == 8, "four or eight waves");
+  static constexpr int kThreads = 64 * kWaves;
   static constexpr int kABlocks = BM / 16, kBBlocks = BN / 16;
-  static constexpr int kLPW = (kABlocks + kBBlocks) / 4;     // direct loads per wave per stage
+  static_assert((kABlocks + kBBlocks) % kWaves == 0, "whole 1 KB loads per wave");
+  static constexpr int kLPW = (kABlocks + kBBlocks) / kWaves;   // direct loads per wave per stage
   static constexpr int kStage = (kABlocks + kBBlocks) * 1024;
   static constexpr size_t kStages = (size_t)NS * kStage;
-  static constexpr size_t kOut = (size_t)4 * WM * (WN + 8) * 2;   // fp16 output staging
+  static constexpr size_t kOut = (size_t)kWaves * WM * (WN + 8) * 2;   // fp16 output staging
   static constexpr size_t kLds = kStages > kOut ? kStages : kOut;
 };
 
 template <int BM, int BN, int WM, int WN, int NS, bool DBG>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__((PipeCfg<BM, BN, WM, WN, NS>::kThreads))
 gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
                     const float* __restrict__ rs, const float* __restrict__ cs,
                     int64_t M, int32_t N, int32_t K, int32_t n_tiles_n, DevSegs sg, int32_t* __restrict__ dbg) {
@@ -108,7 +111,7 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
   extern __shared__ __attribute__((aligned(1024))) uint8_t pipe_smem[];
   __shared__ __attribute__((aligned(16))) float s_rs[BM];
   __shared__ float s_cs[BN];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w / (BN / WN), wn = w % (BN / WN);
   const int l32 = lane & 31, hl = lane >> 5;
   const int tm = blockIdx.x / n_tiles_n, tn = blockIdx.x % n_tiles_n;
@@ -116,25 +119,35 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
   const int32_t n0 = tn * BN;
   const int nk = K / PBK;
 
+  // Each direct load of this wave covers one 16-row block of A or B; its
+  // per-lane source offset from the tile's first row is fixed, so a stage
+  // only advances the (scalar) tile base by 64 bytes.
+  const int8_t* a_tile = A + m0 * K;
+  const int8_t* b_tile = B + (int64_t)n0 * K;
+  uint32_t voff[C::kLPW];
+#pragma unroll
+  for (int j = 0; j < C::kLPW; ++j) {
+    const int blk = w * C::kLPW + j;                         // wave-uniform
+    const bool is_a = blk < C::kABlocks;
+    const int row = 16 * (is_a ? blk : blk - C::kABlocks) + (lane >> 2);
+    const int chunk = (lane & 3) ^ ((row >> 2) & 3);
+    const int64_t last = is_a ? M - 1 - m0 : (int64_t)N - 1 - n0;   // clamp ragged tiles to the last row
+    voff[j] = (uint32_t)(min((int64_t)row, last) * K + 16 * chunk);
+  }
   auto issue = [&](int st) {
     uint8_t* base = pipe_smem + (st % NS) * C::kStage;
     const int64_t k0 = (int64_t)st * PBK;
 #pragma unroll
     for (int j = 0; j < C::kLPW; ++j) {
-      const int blk = w * C::kLPW + j;                       // wave-uniform
-      const bool is_a = blk < C::kABlocks;
-      const int row = 16 * (is_a ? blk : blk - C::kABlocks) + (lane >> 2);
-      const int chunk = (lane & 3) ^ ((row >> 2) & 3);
-      const int8_t* src;
-      if (is_a) src = A + min(m0 + row, M - 1) * K + k0 + 16 * chunk;
-      else src = B + (int64_t)min(n0 + row, N - 1) * K + k0 + 16 * chunk;
+      const int blk = w * C::kLPW + j;
+      const int8_t* src = (blk < C::kABlocks ? a_tile : b_tile) + k0 + voff[j];
       __builtin_amdgcn_global_load_lds((glb_void_t*)src, (lds_void_t*)(base + blk * 1024), 16, 0, 0);
     }
   };
 
   // scales first: their wait then leaves the stage loads in flight
-  for (int i = tid; i < BM; i += 256) s_rs[i] = rs[min(m0 + i, M - 1)];
-  for (int i = tid; i < BN; i += 256) s_cs[i] = cs[min(n0 + i, N - 1)];
+  for (int i = tid; i < BM; i += C::kThreads) s_rs[i] = rs[min(m0 + i, M - 1)];
+  for (int i = tid; i < BN; i += C::kThreads) s_cs[i] = cs[min(n0 + i, N - 1)];
 #pragma unroll
   for (int st = 0; st < NS - 1; ++st)
     if (st < nk) issue(st);
@@ -145,31 +158,63 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
 #pragma unroll
     for (int j = 0; j < TJ; ++j) acc[i][j] = i32x16{};
 
-  for (int kt = 0; kt < nk; ++kt) {
-    vm_wait_stage<C::kLPW, NS - 2>(nk - 1 - kt);
-    if (kt + NS - 1 < nk) issue(kt + NS - 1);
+  // Fragments of one stage, by contraction half kk: af[kk][i], bf[kk][j].
+  // Half 1 of a stage is read while half 0's products run, and half 0 of the
+  // next stage while half 1's products run.
+  i32x4 af[2][TI], bf[2][TJ];
+  auto read_half = [&](int kt, int kk) {
     const uint8_t* sa = pipe_smem + (kt % NS) * C::kStage;
     const uint8_t* sb = sa + C::kABlocks * 1024;
-    // all fragments of the stage are read first (in order, so the second
-    // half's latency hides behind the first half's products)
-    i32x4 af[2][TI], bf[2][TJ];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+    for (int i = 0; i < TI; ++i)
+      af[kk][i] = *reinterpret_cast<const i32x4*>(sa + pipe_slot(wm * WM + 32 * i + l32, 2 * kk + hl));
 #pragma unroll
-      for (int i = 0; i < TI; ++i)
-        af[kk][i] = *reinterpret_cast<const i32x4*>(sa + pipe_slot(wm * WM + 32 * i + l32, 2 * kk + hl));
+    for (int j = 0; j < TJ; ++j)
+      bf[kk][j] = *reinterpret_cast<const i32x4*>(sb + pipe_slot(wn * WN + 32 * j + l32, 2 * kk + hl));
+  };
+  auto products = [&](int kk) {
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
 #pragma unroll
       for (int j = 0; j < TJ; ++j)
-        bf[kk][j] = *reinterpret_cast<const i32x4*>(sb + pipe_slot(wn * WN + 32 * j + l32, 2 * kk + hl));
+        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk][i], bf[kk][j], acc[i][j], 0, 0, 0);
+  };
+
+  // One MFMA goes out before each LDS read of the other half, so the reads
+  // run under the products and every wait the compiler places before a
+  // product only covers reads issued before it.
+  auto interleave = [&]() {
+    if constexpr (C::kWaves == 8) return;     // two waves per SIMD interleave by themselves
+#pragma unroll
+    for (int r = 0; r < TI + TJ; ++r) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, TI * TJ - (TI + TJ), 0);
+  };
+  static_assert(TI * TJ >= TI + TJ, "at least as many products as reads per half");
+
+  // Waiting for stage s (its loads landed; every wave has finished reading
+  // stage s - 1) frees slot (s - 1) % NS for stage s + NS - 1.
+  vm_wait_stage<C::kLPW, NS - 2>(nk - 1);
+  if (NS - 1 < nk) issue(NS - 1);
+  read_half(0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
     __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int i = 0; i < TI; ++i)
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk][i], bf[kk][j], acc[i][j], 0, 0, 0);
+    products(0);
+    read_half(kt, 1);
+    interleave();
+    __builtin_amdgcn_sched_barrier(0);
+    // (on the last stage: a full wait and barrier, nothing left to issue)
+    vm_wait_stage<C::kLPW, NS - 2>(nk - 2 - kt);
+    if (kt + NS < nk) issue(kt + NS);
+    __builtin_amdgcn_sched_barrier(0);
+    // the next stage's first half (after the last stage: an unused read of a
+    // stage slot, which keeps this loop free of branches around products)
+    products(1);
+    read_half(kt + 1, 0);
+    interleave();
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   // Epilogue.  The integer accumulators are dumped as they are (debug only);
@@ -252,7 +297,7 @@ static hipError_t launch_pipe(const GemmArgs& g, const DevSegs& sg, hipStream_t 
   const int tn = (g.N + BN - 1) / BN;
   const int64_t tm = (g.M + BM - 1) / BM;
   KernelScope ks("gemm_i8_pipe", s);
-  QSVD_LAUNCH(ks, kern, dim3((unsigned)(tm * tn)), dim3(256), C::kLds, s, g.a, g.b, g.row_scale, g.col_scale,
+  QSVD_LAUNCH(ks, kern, dim3((unsigned)(tm * tn)), dim3(C::kThreads), C::kLds, s, g.a, g.b, g.row_scale, g.col_scale,
                      g.M, g.N, g.K, tn, sg, g.dbg);
   return hipGetLastError();
 }
@@ -269,7 +314,7 @@ hipError_t launch_gemm_i8(const GemmArgs& g, hipStream_t s) {
   // the accumulator dumps)
   const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
   hipError_t e = g.dbg ? launch_pipe<128, 128, 64, 64, 6, true>(g, sg, s)
-                 : big_tiles >= 256 ? launch_pipe<256, 256, 128, 128, 4, false>(g, sg, s)
+                 : big_tiles >= 256 ? launch_pipe<256, 256, 128, 64, 4, false>(g, sg, s)
                                     : launch_pipe<128, 128, 64, 64, 6, false>(g, sg, s);
   if (e != hipSuccess || !g.cq) return e;
   return launch_quantize_rows(g.seg[0].ptr, g.M, g.N, g.seg[0].ld, g.abits, 1.f, g.cq, g.sc, s);
