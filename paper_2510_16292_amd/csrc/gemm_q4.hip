@@ -112,7 +112,7 @@ gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B
   // int4 operands enter the products as 16 * code: the int32 sums are exact
   // multiples of 16 (or 256) and are shifted back exactly before use
   constexpr int SH = (ABITS == 4 ? 4 : 0) + (BBITS == 4 ? 4 : 0);
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w >> 1, wn = w & 1;
   const int l32 = lane & 31, hl = lane >> 5;
   const int tm = blockIdx.x / n_tiles_n, tn = blockIdx.x % n_tiles_n;
@@ -123,23 +123,34 @@ gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B
 
   // byte o of a stage: A tile rows first, then B tile rows; lane p of load j
   // of wave w covers bytes 1024*(w*LPW + j) + 16p
+  // Per-lane source offsets of this wave's direct loads from the tile's first
+  // row (fixed over the contraction; a stage advances the base by a row's
+  // stage bytes): byte o of a stage holds A tile rows first, then B tile
+  // rows; lane p of load j of wave w covers bytes 1024*(w*LPW + j) + 16p.
+  const uint8_t* a_tile = A + m0 * KA;
+  const uint8_t* b_tile = B + (int64_t)n0 * KB;
+  uint32_t voff[LPW];
+#pragma unroll
+  for (int j = 0; j < LPW; ++j) {
+    const int blk = w * LPW + j;                                     // wave-uniform
+    const int o = blk * 1024 + 16 * lane;
+    if (blk * 1024 < SA) {
+      const int row = o / RBA, phys = (o % RBA) / 16;
+      const int chunk = RBA == 64 ? (phys ^ ((row >> 2) & 3)) : (phys ^ ((row >> 3) & 1));
+      voff[j] = (uint32_t)(min((int64_t)row, M - 1 - m0) * KA + 16 * chunk);
+    } else {
+      const int ob = o - SA;
+      const int row = ob / RBB, phys = (ob % RBB) / 16;
+      const int chunk = RBB == 64 ? (phys ^ ((row >> 2) & 3)) : (phys ^ ((row >> 3) & 1));
+      voff[j] = (uint32_t)(min((int64_t)row, (int64_t)N - 1 - n0) * KB + 16 * chunk);
+    }
+  }
   auto issue = [&](int st) {
     uint8_t* base = q4_smem + (st % QNS) * STAGE;
 #pragma unroll
     for (int j = 0; j < LPW; ++j) {
       const int blk = w * LPW + j;
-      const int o = blk * 1024 + 16 * lane;
-      const uint8_t* src;
-      if (blk * 1024 < SA) {                                         // wave-uniform
-        const int row = o / RBA, phys = (o % RBA) / 16;
-        const int chunk = RBA == 64 ? (phys ^ ((row >> 2) & 3)) : (phys ^ ((row >> 3) & 1));
-        src = A + min(m0 + row, M - 1) * KA + (int64_t)st * RBA + 16 * chunk;
-      } else {
-        const int ob = o - SA;
-        const int row = ob / RBB, phys = (ob % RBB) / 16;
-        const int chunk = RBB == 64 ? (phys ^ ((row >> 2) & 3)) : (phys ^ ((row >> 3) & 1));
-        src = B + (int64_t)min(n0 + row, N - 1) * KB + (int64_t)st * RBB + 16 * chunk;
-      }
+      const uint8_t* src = blk * 1024 < SA ? a_tile + (int64_t)st * RBA + voff[j] : b_tile + (int64_t)st * RBB + voff[j];
       __builtin_amdgcn_global_load_lds((q4_glb_void_t*)src, (q4_lds_void_t*)(base + blk * 1024), 16, 0, 0);
     }
   };
@@ -177,26 +188,54 @@ gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B
       for (int j = 0; j < TJ; ++j) S[i][j] = f32x16{};
   }
 
-  for (int kt = 0; kt < nk; ++kt) {
-    q4_wait_stage<LPW, QNS - 2>(nk - 1 - kt);
-    if (kt + QNS - 1 < nk) issue(kt + QNS - 1);
+  // Fragments by contraction half kk (32 elements): half 1 of a stage is read
+  // while half 0's products run, half 0 of the next stage while half 1's run;
+  // one MFMA goes out before each read so that the reads run under them.
+  i32x4 af[2][TI], bf[2][TJ];
+  auto read_half = [&](int kt, int kk) {
     const uint8_t* sa = q4_smem + (kt % QNS) * STAGE;
     const uint8_t* sb = sa + SA;
-    i32x4 af[2][TI], bf[2][TJ];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+    for (int i = 0; i < TI; ++i) af[kk][i] = q4_frag<ABITS, BBITS>(sa, wm * QWM + 32 * i + l32, kk, hl);
 #pragma unroll
-      for (int i = 0; i < TI; ++i) af[kk][i] = q4_frag<ABITS, BBITS>(sa, wm * QWM + 32 * i + l32, kk, hl);
+    for (int j = 0; j < TJ; ++j) bf[kk][j] = q4_frag<BBITS, ABITS>(sb, wn * QWN + 32 * j + l32, kk, hl);
+  };
+  auto products = [&](int kk) {
 #pragma unroll
-      for (int j = 0; j < TJ; ++j) bf[kk][j] = q4_frag<BBITS, ABITS>(sb, wn * QWN + 32 * j + l32, kk, hl);
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk][i], bf[kk][j], acc[i][j], 0, 0, 0);
+  };
+  auto interleave = [&]() {
+#pragma unroll
+    for (int r = 0; r < TI + TJ; ++r) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
     }
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int i = 0; i < TI; ++i)
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk][i], bf[kk][j], acc[i][j], 0, 0, 0);
+  };
+  static_assert(TI * TJ == TI + TJ, "as many products as reads per half");
+
+  // Waiting for stage s (its loads landed; every wave has finished reading
+  // stage s - 1) frees slot (s - 1) % QNS for stage s + QNS - 1.
+  q4_wait_stage<LPW, QNS - 2>(nk - 1);
+  if (QNS - 1 < nk) issue(QNS - 1);
+  read_half(0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    __builtin_amdgcn_sched_barrier(0);
+    products(0);
+    read_half(kt, 1);
+    interleave();
+    __builtin_amdgcn_sched_barrier(0);
+    // (on the last stage: a full wait and barrier, nothing left to issue)
+    q4_wait_stage<LPW, QNS - 2>(nk - 2 - kt);
+    if (kt + QNS < nk) issue(kt + QNS);
+    __builtin_amdgcn_sched_barrier(0);
+    // after the last stage this reads a stage slot whose values go unused
+    products(1);
+    read_half(kt + 1, 0);
+    interleave();
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (GROUPED) {
       if ((kt + 1) % gsteps == 0) {
         // group g = (kt + 1) / gsteps - 1 ends here: fold it, fetch the next group's scales
