@@ -170,7 +170,7 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
     crefs = [ctypes.byref(c.c) for c in caches]
     f16 = fmt == B.QSVD_CACHE_F16
 
-    def step(i):
+    def step(i, s=s):
         li = i % n_layers
         st = lib.qsvd_quantize_act(xs_p[i % 8], batch, d, d, 8, 1.0, xq_p, sx_p, s)
         st |= lib.qsvd_lowrank_qkv_prefill(lrefs[li], xq_p, sx_p, batch, 8, B.QSVD_OUT_Q, ch_p, cq_p, sc_p,
@@ -223,6 +223,38 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
                                "traffic": None if traffic is None else int(traffic),
                                "kernel": "latent_attn_kernel", "launches": n,
                                "bytes_per_launch": int(bytes_per_launch)}
+    # The same steps replayed from one captured graph of a full rotation
+    # through the layers (launch grids follow each cache's host max_len, held
+    # at the final length; chunks past a sequence's length return at once).
+    def hold(max_len):
+        torch.cuda.synchronize()
+        for c in caches:
+            c.seq_len.fill_(ctx0)
+            c.c.max_len = max_len
+        torch.cuda.synchronize()
+
+    final = ctx0 + visits
+    hold(final - 1)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        gs = B.stream_handle()
+        for i in range(n_layers):
+            step(i, gs)
+    rounds = max(steps // n_layers, 1)
+    hold(final)
+    g.replay()
+    hold(final)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(rounds):
+        g.replay()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    res["graph_ms_per_step"] = (t1 - t0) * 1e3 / (rounds * n_layers)
+    res["graph_tokens_per_s"] = batch * rounds * n_layers / (t1 - t0)
+    del g
+    for c in caches:
+        c.c.max_len = ctx0 + rounds          # the replays left every sequence at this length
     if compare_forms:
         # absorbed vs reconstruct on this layer, attention call alone (a few calls each)
         forms = {}
@@ -267,7 +299,9 @@ def bench_decode_gqa(args):
            "workload": f"qwen2-vl-7b-shaped GQA layer decode: batch {wl4.decode_batch}, int8 latent cache r=1024 "
                        f"with per-token scales, context {wl4.decode_ctx}->{wl4.decode_ctx + GQA_VISITS}, "
                        f"W4A8 (int4 per-group-128 weights), {wl4.n_layers} rotated layers; tokens/s per layer step",
-           "mean_context": round(res["mean_context"], 1)}
+           "mean_context": round(res["mean_context"], 1),
+           "graph_replay": {"value": round(res["graph_tokens_per_s"], 1), "unit": "tokens/s",
+                            "ms_per_step": round(res["graph_ms_per_step"], 5)}}
     if "roofline" in res:
         out["roofline"] = res["roofline"]
         out["attn_kernel_us"] = round(res["attn_kernel_us"], 2)
@@ -624,6 +658,8 @@ def main():
                    "mean_context": round(dec["mean_context"], 1), "attention": args.mode},
         "roofline": dec.get("roofline"),
         "attn_kernel_us": round(dec.get("attn_kernel_us", 0.0), 2),
+        "graph_replay": {"value": round(dec["graph_tokens_per_s"], 1), "unit": "tokens/s",
+                         "ms_per_step": round(dec["graph_ms_per_step"], 5)},
         "attention_form_us": dec["attention_form_us"],
         "prefill": pre,
     }
