@@ -121,11 +121,12 @@ qsvd_status qsvd_quantize_act(const void* x, int64_t M, int32_t K, int64_t ldx, 
  *            the integer accumulators (w_group 0 only; NULL to skip)
  *   ws       unused (qsvd_prefill_workspace_size() returns 0; kept for callers
  *            that size one anyway)
- * Requires d % 64 == 0, r % 64 == 0, act_bits 8, 16-byte aligned xq, c_h, cq and
- * weight codes.  M <= 32 (decode sizes) takes int8 or int4 weights with
- * per-channel or per-group scales (groups a multiple of 64 dividing d and r);
- * larger M takes int8 per-channel weights, head_dim a multiple of 8 and
- * 16-byte aligned q, k, v.  Other combinations return QSVD_ERR_UNSUPPORTED. */
+ * Requires d % 64 == 0, r % 64 == 0, act_bits 8 or 4, int8 or int4 weights
+ * with per-channel or per-group scales (groups a multiple of 64 dividing d and
+ * r), 16-byte aligned xq, c_h, cq and weight codes.  More than 32 tokens also
+ * need head_dim a multiple of 8 and 16-byte aligned q, k, v.  The integer
+ * accumulator dumps need act_bits 8 and per-channel weights.  Other
+ * combinations return QSVD_ERR_UNSUPPORTED. */
 qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const float* sx,
                                      int64_t M, int32_t act_bits, uint32_t out_mask,
                                      void* c_h, void* cq, float* sc, void* q, void* k, void* v,
@@ -159,9 +160,17 @@ qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void*
  *         when its shape is supported)
  *   sm_scale  0 selects 1/sqrt(head_dim)
  *   ws    device workspace of at least qsvd_decode_workspace_size() bytes
- * Requires n_q_heads <= 32, head_dim % 32 == 0 and <= 128, batch <= 64,
- * batch * q_len <= 65535, q_len <= max_len, 16-byte aligned q, out and s_b,
- * an F16 or I8 cache; the absorbed form needs r in {128, 512, 1024, 1536}. */
+ * Requires head_dim % 32 == 0 and <= 128, batch <= 64, q_len <= max_len,
+ * 16-byte aligned q, out and s_b.  The absorbed form takes n_q_heads <= 64,
+ * r in {128, 512, 1024, 1536} (with at most 32 heads) or r a multiple of 128
+ * up to 3072, any cache format, and batch * q_len * ceil(n_q_heads / 16)
+ * <= 65535 (batch * q_len <= 65535 with 32-head blocks); the reconstruct
+ * form takes n_q_heads <= 32, q_len 1, capacity <= 16384 and an F16 or I8
+ * cache.
+ * Launch grids are sized from the host c->max_len and every length is read
+ * from seq_len on the device, so a call may be captured in a graph and
+ * replayed while the cache grows, provided c->max_len at capture is at least
+ * every length the replays reach. */
 qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* c,
                                          const void* q, int32_t q_len, int32_t mode,
                                          float sm_scale, void* out,
