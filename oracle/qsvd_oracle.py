@@ -92,6 +92,64 @@ def fold_rotations(A: np.ndarray, B: np.ndarray, H1: np.ndarray, H2: np.ndarray)
     return H1 @ A @ H2.T, H2 @ B
 
 
+def hadamard_block(d: int) -> int:
+    """Block size of the randomized block Walsh-Hadamard rotation: the largest
+    power of two dividing d (reading: the paper asks only for orthogonal
+    H1, H2 in the QuaRot/DFRot style, Section 3.3)."""
+    return d & -d
+
+
+def rotation_signs(d: int, seed: int) -> np.ndarray:
+    """A seeded +-1 diagonal (int8 [d]) of the randomized rotation."""
+    g = np.random.default_rng(seed)
+    return np.where(g.integers(0, 2, size=d) == 0, 1, -1).astype(np.int8)
+
+
+def walsh_hadamard_rows(v: np.ndarray, block: int, dtype=F32) -> np.ndarray:
+    """Unnormalized Walsh-Hadamard transform of every length-`block` segment
+    of every row, v -> v H_block (Sylvester order), by the radix-2 stages
+    h = 1, 2, 4, ..., block/2: (v_i, v_{i+h}) -> (v_i + v_{i+h}, v_i - v_{i+h})
+    for every i whose bit h is clear, each sum rounded to `dtype`."""
+    out = np.array(v, dtype=dtype, copy=True)
+    M, K = out.shape
+    assert K % block == 0 and block & (block - 1) == 0
+    h = 1
+    while h < block:
+        w = out.reshape(M, K // (2 * h), 2, h)
+        a = w[:, :, 0, :].copy()
+        b = w[:, :, 1, :].copy()
+        w[:, :, 0, :] = (a + b).astype(dtype)
+        w[:, :, 1, :] = (a - b).astype(dtype)
+        h *= 2
+    return out
+
+
+def rotation_matrix(signs: np.ndarray, block: int) -> np.ndarray:
+    """H1 = blockdiag(H_B, ..., H_B) diag(signs) / sqrt(B) as an explicit fp64
+    matrix (H_B the Sylvester Hadamard matrix), for the pins and for folding."""
+    d = signs.size
+    Hb = walsh_hadamard_rows(np.eye(block), block, np.float64)      # rows of H_B
+    H = np.zeros((d, d))
+    for k in range(d // block):
+        H[k * block:(k + 1) * block, k * block:(k + 1) * block] = Hb
+    return H * signs.astype(np.float64)[None, :] / np.sqrt(block)
+
+
+def rotate_act(x: np.ndarray, signs: np.ndarray, block: int) -> np.ndarray:
+    """Online rotation X H1^T of Eq. 11 / Q(X H1^T) of Eq. 12 for
+    H1 = blockdiag(H_B) diag(signs) / sqrt(B): in fp32, x_i * s_i (exact), the
+    Walsh-Hadamard stages of each block, then one product by fp32(1/sqrt(B))."""
+    v = (np.asarray(x).astype(F32) * signs.astype(F32)[None, :]).astype(F32)
+    y = walsh_hadamard_rows(v, block, F32)
+    c = F32(1.0 / np.sqrt(float(block)))
+    return (y * c).astype(F32)
+
+
+def quantize_act_rotated(x: np.ndarray, signs: np.ndarray, block: int, bits: int, clip: float = 1.0):
+    """Q(X H1^T): the rotated rows (fp32) through the per-token quantizer."""
+    return quantize_act(rotate_act(x, signs, block), bits, clip)
+
+
 def quantize_weight(W: np.ndarray, bits: int, group: int = 0, clip: float = 1.0):
     """Round-to-nearest symmetric weight quantization (Section 4 setup).
 

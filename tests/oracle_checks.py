@@ -519,6 +519,64 @@ def check_cache_append_and_int4():
         raise AssertionError("capacity overflow not detected")
 
 
+# ---------------------------------------------------------------- online H1 rotation
+
+def check_rotation_matrix_and_transform():
+    """H1 = blockdiag(H_B) diag(s) / sqrt(B) is orthogonal, H_B matches the
+    Sylvester construction H_2k = [[H_k, H_k], [H_k, -H_k]], the fast transform
+    of integer rows is exact and equals the explicit matrix product, applying
+    it twice gives B times the input, and a single spike spreads to a flat row
+    of magnitude spike / sqrt(B)."""
+    # Sylvester construction, built independently
+    Hs = np.array([[1.0]])
+    while Hs.shape[0] < 64:
+        Hs = np.block([[Hs, Hs], [Hs, -Hs]])
+    assert np.array_equal(O.walsh_hadamard_rows(np.eye(64), 64, np.float64), Hs)
+    for d in (256, 384, 640):
+        B = O.hadamard_block(d)
+        assert d % B == 0 and (d // B) % 2 == 1
+        s = O.rotation_signs(d, seed=d)
+        H1 = O.rotation_matrix(s, B)
+        assert np.allclose(H1 @ H1.T, np.eye(d), atol=1e-12)
+        g = np.random.default_rng(d)
+        xi = g.integers(-50, 51, size=(5, d)).astype(np.float64)
+        fast = O.walsh_hadamard_rows(xi * s[None, :], B, np.float64)
+        assert np.array_equal(fast, xi @ (H1.T * np.sqrt(B)))               # exact on integers
+        assert np.array_equal(O.walsh_hadamard_rows(fast, B, np.float64), B * (xi * s[None, :]))
+        xf = g.standard_normal((5, d)).astype(np.float16)
+        y32 = O.rotate_act(xf, s, B)
+        y64 = xf.astype(np.float64) @ H1.T
+        assert np.max(np.abs(y32 - y64)) <= 1e-5 * np.max(np.abs(y64)) * np.log2(B)
+        spike = np.zeros((1, d), np.float16)
+        spike[0, 3] = 32.0
+        ys = O.rotate_act(spike, s, B)
+        blk = ys[0, (3 // B) * B:(3 // B + 1) * B]
+        assert np.allclose(np.abs(blk), 32.0 / np.sqrt(B), rtol=1e-6)
+        assert np.count_nonzero(ys) == B
+
+
+def check_rotation_fold_and_error_reduction():
+    """Folding H1 into W^d leaves the product unchanged, (X H1^T)(H1 W^d) =
+    X W^d (Eq. 11), and on outlier-heavy activations the rotated 4-bit
+    quantization has a smaller error than the plain one."""
+    wl = tiny_workload()
+    X = gen.prefill_activations(wl)
+    d = X.shape[1]
+    B = O.hadamard_block(d)
+    s = O.rotation_signs(d, seed=11)
+    H1 = O.rotation_matrix(s, B)
+    layer = tiny_layer()
+    A = layer.A
+    Xr = X.astype(np.float64) @ H1.T
+    assert np.allclose(Xr @ (H1 @ A), X.astype(np.float64) @ A, rtol=1e-10, atol=1e-10)
+    for bits in (8, 4):
+        q0, s0 = O.quantize_act(X, bits)
+        e0 = np.linalg.norm(q0 * s0[:, None] - X.astype(np.float64))
+        q1, s1 = O.quantize_act_rotated(X, s, B, bits)
+        e1 = np.linalg.norm((q1 * s1[:, None]) @ H1 - X.astype(np.float64))
+        assert e1 < 0.5 * e0, (bits, e0, e1)
+
+
 # ---------------------------------------------------------------- P12-P13: cost model
 
 def check_cost_model():

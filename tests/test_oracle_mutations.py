@@ -77,6 +77,31 @@ def _kv_group_off_by_one(h, hq, hkv):
     return min(hkv - 1, (h * hkv) // hq + (1 if h == 1 else 0))
 
 
+_good_wht = O.walsh_hadamard_rows
+_good_rotate = O.rotate_act
+
+
+def _wht_sub_swapped(v, block, dtype=np.float32):       # (b - a) in the second output
+    out = np.array(v, dtype=dtype, copy=True)
+    M, K = out.shape
+    h = 1
+    while h < block:
+        w = out.reshape(M, K // (2 * h), 2, h)
+        a, b = w[:, :, 0, :].copy(), w[:, :, 1, :].copy()
+        w[:, :, 0, :] = (a + b).astype(dtype)
+        w[:, :, 1, :] = (b - a).astype(dtype)
+        h *= 2
+    return out
+
+
+def _rotate_no_signs(x, signs, block):                  # random diagonal dropped
+    return _good_rotate(x, np.ones_like(signs), block)
+
+
+def _rotate_scale_by_b(x, signs, block):                # 1/B instead of 1/sqrt(B)
+    return (_good_rotate(x, signs, block) * np.float32(1.0 / np.sqrt(block))).astype(np.float32)
+
+
 MUTATIONS = [
     ("split_beta", _split_sigma_both, [C.check_full_rank_reconstruction, C.check_beta_and_rotation_invariance]),
     ("split_beta", _split_truncate_wrong_end, [C.check_eckart_young]),
@@ -88,6 +113,9 @@ MUTATIONS = [
     ("joint_svd", _svd_no_sign_fix, [C.check_svd_factors]),
     ("kv_group", _kv_group_modulo, [C.check_full_rank_matches_textbook_attention]),
     ("kv_group", _kv_group_off_by_one, [C.check_full_rank_matches_textbook_attention]),
+    ("walsh_hadamard_rows", _wht_sub_swapped, [C.check_rotation_matrix_and_transform]),
+    ("rotate_act", _rotate_no_signs, [C.check_rotation_matrix_and_transform]),
+    ("rotate_act", _rotate_scale_by_b, [C.check_rotation_matrix_and_transform]),
 ]
 
 

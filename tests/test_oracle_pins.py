@@ -22,6 +22,8 @@ PINS = [
     C.check_cache_append_and_int4,
     C.check_cost_model,
     C.check_printed_cost_ratios,
+    C.check_rotation_matrix_and_transform,
+    C.check_rotation_fold_and_error_reduction,
 ]
 
 
