@@ -351,11 +351,32 @@ def bench_prefill(args, wl2, host_layer):
     B.profile_reset()
     ops = 2.0 * M * (d * r + r * L.N)            # X W^d then Q(C) W^u, multiply-adds counted twice
     gemm_s = gms * 1e-3 / args.prefill_steps
+    # the activation quantizer alone, plain and with the online H1 rotation
+    # (block Walsh-Hadamard of order 4096 with seeded signs): fp16 in, int8 + scale out
+    signs = torch.from_numpy(np.where(np.arange(d) % 3 == 0, -1, 1).astype(np.int8)).cuda()
+    quant = {}
+    for name, fn in (("plain", lambda: B.check(B.qsvd_quantize_act(P(X), M, d, d, 8, 1.0, P(xq), P(sx), s))),
+                     ("rotated", lambda: B.check(B.qsvd_quantize_act_rotated(P(X), M, d, d, 8, 1.0, P(signs), d,
+                                                                              P(xq), P(sx), s)))):
+        fn()
+        torch.cuda.synchronize()
+        B.profile_reset()
+        B.profile_enable(True, "quantize")
+        for _ in range(20):
+            fn()
+        torch.cuda.synchronize()
+        B.profile_enable(False)
+        qms, qn = B.profile_read("quantize")
+        B.profile_reset()
+        us = qms * 1e3 / qn
+        qbytes = M * (2 * d + d + 4)
+        quant[name] = {"us": round(us, 2), "GB/s": round(qbytes / (us * 1e-6) / 1e9, 1),
+                       "frac": round(qbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
     call_s = (t1 - t0) / args.prefill_steps
     tops = ops / gemm_s / 1e12
     return {"value": round(tops, 1), "unit": "TOPS", "ms_per_call": round(call_s * 1e3, 4),
             "gemm_ms_per_call": round(gemm_s * 1e3, 4), "call_tops": round(ops / call_s / 1e12, 1),
-            "tokens": M, "gop_per_call": round(ops / 1e9, 2),
+            "tokens": M, "gop_per_call": round(ops / 1e9, 2), "quantizer": quant,
             "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
                          "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None,
                          "kernel": "gemm_i8 (X W^d and Q(C) W^u)", "launches": n}}

@@ -106,6 +106,26 @@ typedef struct {
 qsvd_status qsvd_quantize_act(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits,
                               float clip, void* xq, float* sx, void* stream);
 
+/* Per-token quantization of rotated activations, Q(X H1^T) (Eq. 11-12), for
+ * layers whose input rotation H1 cannot be folded into the previous layer;
+ * the layer's W^d then holds H1 W^d (folded offline).
+ *   H1 = blockdiag(H_B, ..., H_B) diag(signs) / sqrt(B), H_B the Sylvester
+ *   Hadamard matrix of order B = block, so X H1^T = (X o signs) blockdiag(H_B) / sqrt(B).
+ * Per row, in fp32: v_k = x_k * signs_k; the Walsh-Hadamard stages
+ * h = 1, 2, 4, ..., B/2 in that order, each replacing (v_i, v_{i+h}) by
+ * (v_i + v_{i+h}, v_i - v_{i+h}) for every i whose bit h is clear (each sum
+ * rounded to fp32); y = v * c with c = fp32(1 / sqrt(B)); then y goes through
+ * the quantizer of qsvd_quantize_act (same clip, scale and codes).
+ *   x      device fp16 [M][ldx] (first K columns used)
+ *   signs  device int8 [K] of +1 / -1 (NULL: all +1)
+ *   block  B: a power of two >= 8 dividing K
+ *   xq, sx as for qsvd_quantize_act
+ * Requires K % 8 == 0, K <= 16384, ldx % 8 == 0, 16-byte aligned x, 8-byte
+ * aligned xq and signs; bits 8 or 4; 0 < clip <= 1. */
+qsvd_status qsvd_quantize_act_rotated(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits,
+                                      float clip, const int8_t* signs, int32_t block, void* xq,
+                                      float* sx, void* stream);
+
 /* Quantized joint low-rank QKV projection (Section 3.1 and Eq. 11-12):
  *   C   = (xq W^d codes) dequantized: fp32 (acc * sx[m]) * s_a[j] (per group:
  *         sum over groups of acc_g * s_a[g][j], then * sx[m]), stored as fp16

@@ -18,7 +18,7 @@ QSVD_ATTN_AUTO, QSVD_ATTN_ABSORBED, QSVD_ATTN_RECONSTRUCT = 0, 1, 2
 QSVD_OUT_Q, QSVD_OUT_K, QSVD_OUT_V = 1, 2, 4
 
 EXPORTED = [
-    "qsvd_quantize_act", "qsvd_lowrank_qkv_prefill", "qsvd_prefill_workspace_size",
+    "qsvd_quantize_act", "qsvd_quantize_act_rotated", "qsvd_lowrank_qkv_prefill", "qsvd_prefill_workspace_size",
     "qsvd_latent_cache_append", "qsvd_latent_decode_attention", "qsvd_decode_workspace_size",
     "qsvd_status_string", "qsvd_last_error", "qsvd_profile_enable", "qsvd_profile_reset",
     "qsvd_profile_read",
@@ -63,6 +63,7 @@ def lib():
         LP, CP = ctypes.POINTER(QsvdLayer), ctypes.POINTER(QsvdCache)
         sig = {
             "qsvd_quantize_act": (I32, [P, I64, I32, I64, I32, F, P, P, P]),
+            "qsvd_quantize_act_rotated": (I32, [P, I64, I32, I64, I32, F, P, I32, P, P, P]),
             "qsvd_lowrank_qkv_prefill": (I32, [LP, P, P, I64, I32, U32, P, P, P, P, P, P, P, P, P, SZ, P]),
             "qsvd_prefill_workspace_size": (SZ, [LP, I64, U32]),
             "qsvd_latent_cache_append": (I32, [CP, P, P, P, I32, P]),
@@ -85,6 +86,10 @@ def lib():
 
 def qsvd_quantize_act(x, M, K, ldx, bits, clip, xq, sx, stream):
     return lib().qsvd_quantize_act(x, M, K, ldx, bits, clip, xq, sx, stream)
+
+
+def qsvd_quantize_act_rotated(x, M, K, ldx, bits, clip, signs, block, xq, sx, stream):
+    return lib().qsvd_quantize_act_rotated(x, M, K, ldx, bits, clip, signs, block, xq, sx, stream)
 
 
 def qsvd_lowrank_qkv_prefill(layer, xq, sx, M, act_bits, out_mask, c_h, cq, sc, q, k, v,

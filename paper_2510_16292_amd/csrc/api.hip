@@ -151,6 +151,23 @@ qsvd_status qsvd_quantize_act(const void* x, int64_t M, int32_t K, int64_t ldx, 
   return hip_status(launch_quantize_rows(x, M, K, ldx, bits, clip, xq, sx, (hipStream_t)stream), "quantize_act");
 }
 
+qsvd_status qsvd_quantize_act_rotated(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits, float clip,
+                                      const int8_t* signs, int32_t block, void* xq, float* sx, void* stream) {
+  if (M < 0 || K <= 0 || ldx < K) return fail(QSVD_ERR_INVALID_ARG, "bad sizes M=%lld K=%d ldx=%lld", (long long)M, K, (long long)ldx);
+  if (bits != 8 && bits != 4) return fail(QSVD_ERR_INVALID_ARG, "bits must be 8 or 4");
+  if (!(clip > 0.f && clip <= 1.f)) return fail(QSVD_ERR_INVALID_ARG, "clip must be in (0, 1]");
+  if (block < 8 || (block & (block - 1)) || K % block)
+    return fail(QSVD_ERR_INVALID_ARG, "block must be a power of two >= 8 dividing K");
+  if (M > 0 && (!x || !xq || !sx)) return fail(QSVD_ERR_INVALID_ARG, "NULL pointer");
+  if (K % 8 || ldx % 8) return fail(QSVD_ERR_UNSUPPORTED, "K and ldx must be multiples of 8");
+  if (K > 16384) return fail(QSVD_ERR_UNSUPPORTED, "K must be at most 16384");
+  if (!aligned(x, 16) || !aligned(xq, 8) || !aligned(signs, 8))
+    return fail(QSVD_ERR_UNSUPPORTED, "x must be 16-byte, xq and signs 8-byte aligned");
+  const float c = (float)(1.0 / sqrt((double)block));
+  return hip_status(launch_quantize_rotated(x, M, K, ldx, bits, clip, signs, block, c, xq, sx, (hipStream_t)stream),
+                    "quantize_act_rotated");
+}
+
 static void prefill_ranges(const qsvd_layer& w, uint32_t mask, bool full, int32_t* lo, int32_t* hi) {
   const int32_t nq = w.n_q_heads * w.head_dim, nkv = w.n_kv_heads * w.head_dim;
   const int32_t b0[3] = {0, nq, nq + nkv}, b1[3] = {nq, nq + nkv, nq + 2 * nkv};

@@ -27,6 +27,10 @@ struct KernelScope {
 
 hipError_t launch_quantize_rows(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits,
                                 float clip, void* xq, float* sx, hipStream_t s);
+// Q(X H1^T) for H1 = blockdiag(H_block) diag(signs) / sqrt(block); c = fp32(1/sqrt(block)).
+hipError_t launch_quantize_rotated(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits, float clip,
+                                   const int8_t* signs, int32_t block, float c, void* xq, float* sx,
+                                   hipStream_t s);
 
 // C[m][n] = sum_k A[m][k] * B[n][k] for int8 A [M][K] and int8 B [N][K], scaled
 // per row and per column, written to up to three fp16 column segments.

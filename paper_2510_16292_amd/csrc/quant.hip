@@ -70,6 +70,164 @@ quantize_rows_kernel(const _Float16* __restrict__ x, int64_t M, int32_t K, int64
   }
 }
 
+// ---------------------------------------------------------------------------
+// Quantization of rotated rows, Q(X H1^T) with H1 = blockdiag(H_B) diag(s) /
+// sqrt(B) (Eq. 11-12; an online H1 for inputs whose rotation is not folded
+// into the previous layer).  One workgroup of 256 threads per row; the row
+// lives in LDS as fp32.  In fp32: x_i * s_i, the Walsh-Hadamard stages
+// h = 1, 2, ..., B/2 ((v_i, v_{i+h}) -> (v_i + v_{i+h}, v_i - v_{i+h})), then
+// one product by c = fp32(1/sqrt(B)); the quantizer of quantize_rows_kernel
+// follows.  Stages 1, 2, 4 run in registers on 8-element chunks; the rest in
+// radix-8 (then radix-4 / radix-2) passes through LDS.  Which thread does a
+// butterfly does not change its operands, so the result is that of the
+// stage-by-stage definition.
+// ---------------------------------------------------------------------------
+constexpr int kRotThreads = 256;
+constexpr int kRotMaxChunks = 8;       // 8-element chunks per thread: K <= 8 * 8 * 256
+
+// LDS word of row element i: 8 pad words after every 64 elements, so that the
+// strided groups of every pass (stride 8 included) fall on distinct banks.
+__device__ __forceinline__ int rot_addr(int i) { return i + ((i >> 6) << 3); }
+
+template <int R>
+__device__ __forceinline__ void rot_pass(float* buf, int K, int lh) {
+  // groups of R elements i + k h (h = 2^lh, k = 0..R-1), i with bits h .. (R/2) h clear
+  constexpr int LR = R == 8 ? 3 : R == 4 ? 2 : 1;
+  const int ngroups = K / R, h = 1 << lh;
+  for (int g = threadIdx.x; g < ngroups; g += kRotThreads) {
+    const int i = ((g >> lh) << (lh + LR)) | (g & (h - 1));
+    float v[R];
+#pragma unroll
+    for (int k = 0; k < R; ++k) v[k] = buf[rot_addr(i + k * h)];
+#pragma unroll
+    for (int st = 1; st < R; st <<= 1)
+#pragma unroll
+      for (int k = 0; k < R; ++k)
+        if (!(k & st)) {
+          const float a = v[k], b = v[k + st];
+          v[k] = add_rn(a, b);
+          v[k + st] = add_rn(a, -b);
+        }
+#pragma unroll
+    for (int k = 0; k < R; ++k) buf[rot_addr(i + k * h)] = v[k];
+  }
+}
+
+template <int BITS>
+__global__ void __launch_bounds__(kRotThreads)
+quantize_rotated_kernel(const _Float16* __restrict__ x, int64_t M, int32_t K, int64_t ldx, float clip,
+                        const int8_t* __restrict__ signs, int32_t block, float c, uint8_t* __restrict__ xq,
+                        float* __restrict__ sx) {
+  extern __shared__ __attribute__((aligned(16))) float rbuf[];
+  __shared__ float wmax[kRotThreads / 64];
+  const int tid = threadIdx.x;
+  const int64_t m = blockIdx.x;
+  const _Float16* row = x + m * ldx;
+  const int nch = K >> 3;
+  // signs, stages 1, 2, 4 on 8-element chunks (B >= 8, so a chunk lies in one block)
+  for (int ch = tid; ch < nch; ch += kRotThreads) {
+    const f16x8 t = *reinterpret_cast<const f16x8*>(row + ch * 8);
+    float v[8];
+    if (signs) {
+      const uint2 sb = *reinterpret_cast<const uint2*>(signs + ch * 8);
+      const uint32_t sw[2] = {sb.x, sb.y};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float f = (float)t[e];
+        v[e] = (int8_t)(sw[e >> 2] >> (8 * (e & 3))) < 0 ? -f : f;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (float)t[e];
+    }
+#pragma unroll
+    for (int st = 1; st < 8; st <<= 1)
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (!(k & st)) {
+          const float a = v[k], b = v[k + st];
+          v[k] = add_rn(a, b);
+          v[k + st] = add_rn(a, -b);
+        }
+    float* dst = rbuf + rot_addr(ch * 8);
+    *reinterpret_cast<f32x4*>(dst) = f32x4{v[0], v[1], v[2], v[3]};
+    *reinterpret_cast<f32x4*>(dst + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  }
+  __syncthreads();
+  int lh = 3;
+  while ((1 << lh) < block) {
+    const int h = 1 << lh;
+    if (h * 8 <= block) rot_pass<8>(rbuf, K, lh), lh += 3;
+    else if (h * 4 <= block) rot_pass<4>(rbuf, K, lh), lh += 2;
+    else rot_pass<2>(rbuf, K, lh), lh += 1;
+    __syncthreads();
+  }
+  // y = v * c kept in registers, row absmax, then the per-token quantizer
+  float y[kRotMaxChunks][8];
+  float amax = 0.f;
+#pragma unroll
+  for (int j = 0; j < kRotMaxChunks; ++j) {
+    const int ch = tid + j * kRotThreads;
+    if (ch < nch) {
+      const float* srcp = rbuf + rot_addr(ch * 8);
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(srcp), hi = *reinterpret_cast<const f32x4*>(srcp + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        y[j][e] = mul_rn(lo[e], c);
+        y[j][4 + e] = mul_rn(hi[e], c);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(y[j][e]));
+    }
+  }
+  amax = wave_max(amax);
+  if ((tid & 63) == 0) wmax[tid >> 6] = amax;
+  __syncthreads();
+  amax = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+  const float qm = (float)((1 << (BITS - 1)) - 1);
+  const float a = mul_rn(clip, amax);
+  float inv = 0.f, s = 1.f;
+  if (a != 0.f) {
+    inv = div_rn(qm, a);
+    s = div_rn(a, qm);
+  }
+  if (tid == 0) sx[m] = s;
+#pragma unroll
+  for (int j = 0; j < kRotMaxChunks; ++j) {
+    const int ch = tid + j * kRotThreads;
+    if (ch >= nch) continue;
+    int q[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q[e] = (a != 0.f) ? quant_code(mul_rn(y[j][e], inv), qm) : 0;
+    if (BITS == 8) {
+      const uint32_t lo = (q[0] & 0xff) | ((q[1] & 0xff) << 8) | ((q[2] & 0xff) << 16) | ((uint32_t)(q[3] & 0xff) << 24);
+      const uint32_t hi = (q[4] & 0xff) | ((q[5] & 0xff) << 8) | ((q[6] & 0xff) << 16) | ((uint32_t)(q[7] & 0xff) << 24);
+      *reinterpret_cast<uint2*>(xq + m * (int64_t)K + ch * 8) = make_uint2(lo, hi);
+    } else {
+      uint32_t pk = 0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pk |= (uint32_t)(q[e] & 0xf) << (4 * e);
+      *reinterpret_cast<uint32_t*>(xq + m * (int64_t)(K / 2) + ch * 4) = pk;
+    }
+  }
+}
+
+hipError_t launch_quantize_rotated(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits, float clip,
+                                   const int8_t* signs, int32_t block, float c, void* xq, float* sx,
+                                   hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  const size_t lds = (size_t)(K + K / 8) * sizeof(float);     // with the pad words
+  auto kern = bits == 8 ? quantize_rotated_kernel<8> : quantize_rotated_kernel<4>;
+  if (lds + 1024 > 64 * 1024) {     // (plus the kernel's static LDS)
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  KernelScope ks("quantize_rotated", s);
+  QSVD_LAUNCH(ks, kern, dim3((unsigned)M), dim3(kRotThreads), lds, s, (const _Float16*)x, M, K, ldx, clip, signs,
+              block, c, (uint8_t*)xq, sx);
+  return hipGetLastError();
+}
+
 hipError_t launch_quantize_rows(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits,
                                 float clip, void* xq, float* sx, hipStream_t s) {
   if (M == 0) return hipSuccess;

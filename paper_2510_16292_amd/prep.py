@@ -51,6 +51,24 @@ def truncated_factors(W: np.ndarray, r: int, beta: float):
     return factors_from_svd(U[:, :r], s[:r], Vt[:r].T, beta)
 
 
+def fold_input_rotation(A: np.ndarray, signs: np.ndarray, block: int) -> np.ndarray:
+    """H1 W^d for the online input rotation H1 = blockdiag(H_B) diag(signs) /
+    sqrt(B) (Eq. 11), so that Q(X H1^T) Q(H1 W^d) replaces Q(X) Q(W^d): rows
+    of W^d are multiplied by the signs, then every column goes through the
+    block Walsh-Hadamard transform along its rows, in fp64."""
+    A = np.asarray(A, dtype=np.float64) * np.asarray(signs, dtype=np.float64)[:, None]
+    d, r = A.shape
+    assert d % block == 0 and block & (block - 1) == 0
+    out = A.reshape(d // block, block, r).copy()
+    h = 1
+    while h < block:
+        v = out.reshape(d // block, block // (2 * h), 2, h, r)
+        a, b = v[:, :, 0].copy(), v[:, :, 1].copy()
+        v[:, :, 0], v[:, :, 1] = a + b, a - b
+        h *= 2
+    return out.reshape(d, r) / np.sqrt(block)
+
+
 def factors_from_svd(U_r: np.ndarray, sigma_r: np.ndarray, V_r: np.ndarray, beta: float):
     """W^d = U_r diag(sigma^beta), W^u = diag(sigma^(1-beta)) V_r^T."""
     return U_r * np.power(sigma_r, beta), (V_r * np.power(sigma_r, 1.0 - beta)).T

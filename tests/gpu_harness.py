@@ -46,6 +46,20 @@ def quantize_act(x_np, bits=8, clip=1.0, K=None):
     return host(xq), host(sx)
 
 
+def quantize_act_rotated(x_np, signs_np, block, bits=8, clip=1.0):
+    """Q(X H1^T) on the device: x_np fp16 [M][K], signs_np int8 [K] or None.
+    Returns (xq bytes [M][K or K/2], sx [M])."""
+    t = torch()
+    M, K = x_np.shape
+    x = dev(x_np)
+    sg = dev(signs_np) if signs_np is not None else None
+    xq = t.empty((M, K if bits == 8 else K // 2), dtype=t.uint8, device="cuda")
+    sx = t.empty((M,), dtype=t.float32, device="cuda")
+    B.check(B.qsvd_quantize_act_rotated(B.ptr(x), M, K, K, bits, clip, B.ptr(sg), block, B.ptr(xq), B.ptr(sx),
+                                        B.stream_handle()))
+    return host(xq), host(sx)
+
+
 class Prefill:
     """Device buffers for one projection call of M tokens."""
 
@@ -67,11 +81,16 @@ class Prefill:
         self.ws_bytes = B.qsvd_prefill_workspace_size(dl.c, M, mask)
         self.ws = t.empty((max(self.ws_bytes, 1),), dtype=t.uint8, device="cuda")
 
-    def run(self, x):
-        """x: device fp16 [M][d]."""
+    def run(self, x, signs=None, block=0):
+        """x: device fp16 [M][d]; with block > 0 the activations are rotated
+        online (device int8 signs [d] or None) before quantization."""
         s = B.stream_handle()
-        B.check(B.qsvd_quantize_act(B.ptr(x), self.M, self.dl.d, self.dl.d, self.abits, 1.0, B.ptr(self.xq),
-                                    B.ptr(self.sx), s))
+        if block:
+            B.check(B.qsvd_quantize_act_rotated(B.ptr(x), self.M, self.dl.d, self.dl.d, self.abits, 1.0, B.ptr(signs),
+                                                block, B.ptr(self.xq), B.ptr(self.sx), s))
+        else:
+            B.check(B.qsvd_quantize_act(B.ptr(x), self.M, self.dl.d, self.dl.d, self.abits, 1.0, B.ptr(self.xq),
+                                        B.ptr(self.sx), s))
         B.check(B.qsvd_lowrank_qkv_prefill(self.dl.c, B.ptr(self.xq), B.ptr(self.sx), self.M, self.abits, self.mask,
                                            B.ptr(self.c_h), B.ptr(self.cq), B.ptr(self.sc), B.ptr(self.q),
                                            B.ptr(self.k), B.ptr(self.v), B.ptr(self.acc_xa), B.ptr(self.acc_cb),

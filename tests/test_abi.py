@@ -110,6 +110,21 @@ def test_status_strings(lib):
 ])
 def test_quantize_act_validation(lib, args, status):
     assert B.qsvd_quantize_act(*args) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    ((0, 4, 16, 16, 8, 1.0, 0, 16, FAKE, FAKE, 0), B.QSVD_ERR_INVALID_ARG),        # NULL x
+    ((FAKE, 4, 16, 16, 3, 1.0, 0, 16, FAKE, FAKE, 0), B.QSVD_ERR_INVALID_ARG),     # bits
+    ((FAKE, 4, 16, 16, 8, 0.0, 0, 16, FAKE, FAKE, 0), B.QSVD_ERR_INVALID_ARG),     # clip
+    ((FAKE, 4, 48, 48, 8, 1.0, 0, 32, FAKE, FAKE, 0), B.QSVD_ERR_INVALID_ARG),     # block does not divide K
+    ((FAKE, 4, 48, 48, 8, 1.0, 0, 24, FAKE, FAKE, 0), B.QSVD_ERR_INVALID_ARG),     # block not a power of two
+    ((FAKE, 4, 16, 16, 8, 1.0, 0, 4, FAKE, FAKE, 0), B.QSVD_ERR_INVALID_ARG),      # block < 8
+    ((FAKE, 4, 32768, 32768, 8, 1.0, 0, 8, FAKE, FAKE, 0), B.QSVD_ERR_UNSUPPORTED),  # K too large
+    ((FAKE, 4, 16, 16, 8, 1.0, FAKE + 4, 16, FAKE, FAKE, 0), B.QSVD_ERR_UNSUPPORTED),  # misaligned signs
+    ((FAKE, 0, 16, 16, 8, 1.0, 0, 16, FAKE, FAKE, 0), B.QSVD_OK),                  # nothing to do
+])
+def test_quantize_act_rotated_validation(lib, args, status):
+    assert B.qsvd_quantize_act_rotated(*args) == status
     assert B.last_error()
 
 
@@ -263,3 +278,15 @@ def test_projection_needs_no_workspace(lib, shape):
     for M in (1, 8, 16, 31, 32, 33, 640, 2560):
         for mask in range(8):
             assert B.qsvd_prefill_workspace_size(L, M, mask) == 0
+
+
+def test_prep_fold_input_rotation_matches_oracle_matrix():
+    """The offline fold H1 W^d (fast transform, fp64) equals the oracle's explicit
+    H1 times W^d."""
+    from oracle import qsvd_oracle as O
+    g = np.random.default_rng(5)
+    for d in (256, 640):
+        B = O.hadamard_block(d)
+        s = O.rotation_signs(d, seed=d + 1)
+        A = g.standard_normal((d, 48))
+        assert np.allclose(prep.fold_input_rotation(A, s, B), O.rotation_matrix(s, B) @ A, rtol=0, atol=1e-12)

@@ -119,6 +119,77 @@ def test_quantize_act_bitexact(case):
     assert np.array_equal(sx.view(np.uint32), s_ref.view(np.uint32))
 
 
+# ------------------------------------------------------------------ online H1 rotation + quantizer
+
+def _rot_cases():
+    wl1, wl2, wl4, wl5 = configs.get(1), configs.get(2), configs.get(4), configs.get(5)
+    spike = np.zeros((2, 1024), np.float16)
+    spike[0, 5], spike[1, 700] = 60000.0, -3.0
+    return [
+        ("tiny-8bit", gen.prefill_activations(wl1), 8, None, 21),
+        ("tiny-4bit", gen.prefill_activations(wl1), 4, None, 22),
+        ("llava7b-2560x4096", gen.prefill_activations(wl2), 8, None, 23),
+        ("qwen-640x3584-b512", gen.fill_activations(wl4, 640), 8, None, 24),
+        ("13b-200x5120-b1024-4bit", gen.fill_activations(wl5, 200), 4, None, 25),
+        ("K4096-b64", gen.random_rows(6, (37, 4096), 2.0), 8, 64, 26),
+        ("K4096-b8", gen.random_rows(7, (5, 4096), 2.0), 8, 8, 27),
+        ("K16384-b16384", gen.random_rows(8, (3, 16384), 1.0), 8, None, 28),
+        ("no-signs", gen.random_rows(9, (11, 2048), 1.0), 8, None, None),
+        ("zero-row-and-spikes", np.concatenate([np.zeros((1, 1024), np.float16), spike]), 8, None, 29),
+    ]
+
+
+@pytest.mark.parametrize("case", _rot_cases(), ids=lambda c: c[0])
+def test_quantize_act_rotated_bitexact(case):
+    """Q(X H1^T) with H1 = blockdiag(H_B) diag(s) / sqrt(B): codes and scales
+    bit-exact against the oracle's stage-by-stage fp32 transform."""
+    name, x, bits, block, seed = case
+    K = x.shape[1]
+    block = O.hadamard_block(K) if block is None else block
+    signs = O.rotation_signs(K, seed) if seed is not None else None
+    H.say(f"quantize_act_rotated {name} shape={x.shape} block={block} bits={bits}")
+    xq, sx = H.quantize_act_rotated(x, signs, block, bits)
+    q_ref, s_ref = O.quantize_act_rotated(x, signs if signs is not None else np.ones(K, np.int8), block, bits)
+    if bits == 4:
+        q_ref = O.pack_int4(q_ref)
+    assert np.array_equal(sx.view(np.uint32), s_ref.view(np.uint32))
+    assert np.array_equal(xq.view(np.uint8), q_ref.view(np.uint8))
+
+
+def test_prefill_with_online_rotation(tiny):
+    """The tiny layer with H1 folded into W^d offline and X rotated online:
+    every stored result bit-exact against the oracle, and the latent closer to
+    the unquantized fp64 X W^d than without the rotation (outlier channels
+    x20 spread over the block)."""
+    wl, _, _ = tiny
+    L = wl.layer
+    A, Bm = O.factors_from_weight(gen.weight_matrix(wl), L.r, 0.5)
+    blk = O.hadamard_block(L.d)
+    s = O.rotation_signs(L.d, seed=31)
+    A_rot = prep.fold_input_rotation(A, s, blk)
+    ol = O.make_layer(A_rot, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, 8, 0)
+    dl = B.DeviceLayer(prep.quantize_layer(A_rot, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, 8, 0))
+    X = gen.prefill_activations(wl)
+    H.say("prefill with online rotation, tiny layer")
+    got = H.Prefill(dl, X.shape[0]).run(H.dev(X), signs=H.dev(s), block=blk).result()
+    xq, sx = O.quantize_act_rotated(X, s, blk, 8)
+    acc_xa, C_h = O.down_projection(ol, xq, sx)
+    cq, sc = O.quantize_latent(C_h, 8)
+    acc_cb, Q, K, V = O.up_projection(ol, cq, sc)
+    assert np.array_equal(got["xq"], xq) and np.array_equal(got["sx"].view(np.uint32), sx.view(np.uint32))
+    assert np.array_equal(got["acc_xa"], acc_xa)
+    assert np.array_equal(got["C_h"].view(np.uint16), C_h.view(np.uint16))
+    assert np.array_equal(got["acc_cb"], acc_cb)
+    for key, ref in (("Q", Q), ("K", K), ("V", V)):
+        assert np.array_equal(got[key].view(np.uint16), ref.view(np.uint16)), key
+    exact = X.astype(np.float64) @ A
+    plain = O.prefill(O.make_layer(A, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, 8, 0), X, 8)["C_h"]
+    e_rot = np.linalg.norm(got["C_h"].astype(np.float64) - exact) / np.linalg.norm(exact)
+    e_plain = np.linalg.norm(plain.astype(np.float64) - exact) / np.linalg.norm(exact)
+    H.say(f"  latent rel. error: rotated {e_rot:.3e}, plain {e_plain:.3e}")
+    assert e_rot < e_plain
+
+
 # ------------------------------------------------------------------ a2-a4: projection
 
 def _check_prefill(ol, got, X):
