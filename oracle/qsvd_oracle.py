@@ -79,6 +79,74 @@ def factors_from_weight(W: np.ndarray, r: int, beta: float):
     return split_beta(U[:, :r], s[:r], Vt[:r, :], beta)
 
 
+# --------------------------------------------------------------------------
+# Offline rank allocation and beta (Section 3.2, Eq. 6-10, Appendix A; Eq. 14)
+# --------------------------------------------------------------------------
+
+def importance_naive(U: np.ndarray, s: np.ndarray, Vt: np.ndarray, grads, S_inv: np.ndarray = None) -> np.ndarray:
+    """Importance score by its definition (Eq. 9): for every singular value,
+    Delta W_i = sigma_i u_i v_i^T (Eq. 6), taken back to the weight space through
+    S^{-1} when the SVD was of the whitened W S (Appendix A), and
+    I_i = mean_n <Delta W_i, G^(n)>_F^2 with the first-order loss change of
+    Eq. 8.  Builds every Delta W_i explicitly: tiny sizes only."""
+    n = s.size
+    out = np.zeros(n)
+    for i in range(n):
+        dW = s[i] * np.outer(U[:, i], Vt[i, :])
+        if S_inv is not None:
+            dW = dW @ S_inv
+        out[i] = np.mean([np.sum(dW * G) ** 2 for G in grads])
+    return out
+
+
+def importance_scores(U: np.ndarray, s: np.ndarray, Vt: np.ndarray, grads, S_inv: np.ndarray = None) -> np.ndarray:
+    """Eq. 10: I_i = mean_n sigma_i^2 [U^T G^(n) V]_(i,i)^2, or with whitening
+    mean_n sigma_i^2 [U^T G^(n) S^{-T} V]_(i,i)^2 (Appendix A)."""
+    V = Vt.T
+    acc = np.zeros(s.size)
+    for G in grads:
+        Gw = G if S_inv is None else G @ S_inv.T
+        acc += np.diag(U.T @ Gw @ V) ** 2
+    return s ** 2 * acc / len(grads)
+
+
+def allocate_ranks(scores, budget: int):
+    """Global ranking across layers (Section 3.2): all singular values of all
+    layers sorted by importance, the top `budget` kept.  Returns, per layer,
+    the sorted indices of its kept singular values.  Reading: ties go to the
+    lower (layer, index) pair."""
+    entries = [(-float(v), l, i) for l, sc in enumerate(scores) for i, v in enumerate(sc)]
+    entries.sort()
+    kept = [[] for _ in scores]
+    for _, l, i in entries[:budget]:
+        kept[l].append(i)
+    return [np.array(sorted(k), dtype=np.int64) for k in kept]
+
+
+def factors_from_selection(U: np.ndarray, s: np.ndarray, Vt: np.ndarray, keep: np.ndarray, beta: float):
+    """W^d and W^u of the kept singular triplets (any subset), Eq. 3-4."""
+    return split_beta(U[:, keep], s[keep], Vt[keep, :], beta)
+
+
+def beta_objective(A: np.ndarray, B: np.ndarray, X: np.ndarray, layer_fn) -> float:
+    """Eq. 14's per-layer term for the projection: sum over the calibration
+    rows of ||Y - Y'||^2 with Y = X W^d W^u in fp64 and Y' the quantized
+    projection of `layer_fn(A, B)` (the concatenated fp16 Q | K | V)."""
+    Y = np.asarray(X, dtype=np.float64) @ A @ B
+    Yq = layer_fn(A, B, X)
+    return float(np.sum((Y - Yq.astype(np.float64)) ** 2))
+
+
+def beta_search(U_r: np.ndarray, s_r: np.ndarray, Vt_r: np.ndarray, X: np.ndarray, betas, layer_fn):
+    """Line search of Eq. 14 over a grid of beta: returns (best beta, the
+    objective at every grid point).  Reading: the first minimum in grid order."""
+    vals = []
+    for b in betas:
+        A, B = split_beta(U_r, s_r, Vt_r, b)
+        vals.append(beta_objective(A, B, X, layer_fn))
+    return betas[int(np.argmin(vals))], vals
+
+
 def random_orthogonal(n: int, seed: int) -> np.ndarray:
     """A seeded orthogonal matrix (QR of a Gaussian) for the rotation pins."""
     g = np.random.default_rng(seed)

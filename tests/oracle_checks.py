@@ -577,6 +577,102 @@ def check_rotation_fold_and_error_reduction():
         assert e1 < 0.5 * e0, (bits, e0, e1)
 
 
+# ---------------------------------------------------------------- P14: importance score, ranks, beta
+
+def _synthetic_grads(d, N, n, seed):
+    """Per-sample weight gradients of a linear map Y = X W: G = X^T dY, with
+    X rows carrying two outlier channels and dY ~ N(0, 1)."""
+    g = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        X = g.standard_normal((6, d))
+        X[:, 1] *= 8.0
+        X[:, d - 2] *= 5.0
+        out.append(X.T @ g.standard_normal((6, N)))
+    return out
+
+
+def check_importance_closed_form():
+    """Eq. 10 equals the Eq. 9 definition built from every Delta W_i (Eq. 6),
+    with and without a (full, non-symmetric) whitening S; Eq. 8 is exact for a
+    loss linear in W; a gradient aligned with one singular pair scores sigma_j^2
+    there and 0 elsewhere."""
+    g = np.random.default_rng(14)
+    d, N = 10, 16
+    W = g.standard_normal((d, N))
+    grads = _synthetic_grads(d, N, 5, 3)
+    U, s, Vt = O.joint_svd(W)
+    assert np.allclose(O.importance_scores(U, s, Vt, grads), O.importance_naive(U, s, Vt, grads), rtol=1e-10)
+    S = np.eye(N) + 0.3 * g.standard_normal((N, N))
+    S_inv = np.linalg.inv(S)
+    Uw, sw, Vtw = O.joint_svd(W @ S)
+    assert np.allclose(Uw @ np.diag(sw) @ Vtw @ S_inv, W, atol=1e-10)
+    assert np.allclose(O.importance_scores(Uw, sw, Vtw, grads, S_inv),
+                       O.importance_naive(Uw, sw, Vtw, grads, S_inv), rtol=1e-10)
+    # Eq. 8 for L(W) = <W, G>: the loss change of truncating sigma_i is exactly <Delta W_i, G>
+    G = grads[0]
+    for i in (0, 4):
+        dW = s[i] * np.outer(U[:, i], Vt[i])
+        assert abs((np.sum(W * G) - np.sum((W - dW) * G)) - np.sum(dW * G)) < 1e-9
+    j = 3
+    sc = O.importance_scores(U, s, Vt, [np.outer(U[:, j], Vt[j])])
+    expect = np.zeros_like(s)
+    expect[j] = s[j] ** 2
+    assert np.allclose(sc, expect, atol=1e-12)
+
+
+def check_rank_allocation():
+    """Global top-k across layers (Section 3.2): the kept set is exactly the k
+    largest scores (brute force over all subsets' sums on a tiny case), the
+    per-layer counts add up to k, a larger budget never drops a component, and
+    with scores that decrease along each layer every layer keeps a prefix."""
+    scores = [np.array([5.0, 1.0, 3.0]), np.array([4.0, 4.0, 0.5, 2.0]), np.array([0.1])]
+    flat = [(l, i) for l, sc in enumerate(scores) for i in range(sc.size)]
+    import itertools
+    for k in range(0, 9):
+        kept = O.allocate_ranks(scores, k)
+        sel = {(l, int(i)) for l, ks in enumerate(kept) for i in ks}
+        assert len(sel) == k
+        best = max(itertools.combinations(flat, k), key=lambda c: (sum(scores[l][i] for l, i in c),
+                                                                      [-l * 10 - i for l, i in sorted(c)]))
+        assert abs(sum(scores[l][i] for l, i in sel) - sum(scores[l][i] for l, i in best)) < 1e-12
+        if k:
+            prev = {(l, int(i)) for l, ks in enumerate(O.allocate_ranks(scores, k - 1)) for i in ks}
+            assert prev <= sel
+    dec = [np.array([9.0, 7.0, 2.0]), np.array([8.0, 3.0, 1.0])]
+    for k in range(7):
+        for ks in O.allocate_ranks(dec, k):
+            assert np.array_equal(ks, np.arange(ks.size))
+
+
+def check_beta_search():
+    """Eq. 14 on the projection: without quantization the objective is the
+    same (to rounding) for every beta, since X W^d W^u does not depend on it;
+    with W8A8 quantization it varies, and the search returns the grid minimum."""
+    wl = tiny_workload()
+    L = wl.layer
+    # a decaying spectrum (sigma_i ~ i^-0.7), where Sigma^beta changes the latent's column scales
+    g = np.random.default_rng(5)
+    Q1, _ = np.linalg.qr(g.standard_normal((L.d, L.d)))
+    Q2, _ = np.linalg.qr(g.standard_normal((L.N, L.d)))
+    W = Q1 @ np.diag(0.5 * np.arange(1, L.d + 1) ** -0.7) @ Q2.T
+    U, s, Vt = O.joint_svd(W)
+    Ur, sr, Vtr = U[:, :L.r], s[:L.r], Vt[:L.r]
+    X = gen.prefill_activations(wl)[:24]
+    betas = [0.0, 0.25, 0.5, 0.75, 1.0]
+    exact = lambda A, B, Xc: np.asarray(Xc, np.float64) @ A @ B
+    _, flat = O.beta_search(Ur, sr, Vtr, X, betas, exact)
+    assert max(flat) < 1e-18 * np.sum((np.asarray(X, np.float64) @ Ur @ np.diag(sr) @ Vtr) ** 2) + 1e-20
+
+    def quant(A, B, Xc):
+        lay = O.make_layer(A, B, L.n_q_heads, L.n_kv_heads, L.head_dim, 8, 0)
+        p = O.prefill(lay, Xc, 8)
+        return np.concatenate([p["Q"], p["K"], p["V"]], axis=1)
+    best, vals = O.beta_search(Ur, sr, Vtr, X, betas, quant)
+    assert max(vals) > 1.2 * min(vals)
+    assert best == betas[int(np.argmin(vals))]
+
+
 # ---------------------------------------------------------------- P12-P13: cost model
 
 def check_cost_model():

@@ -102,6 +102,32 @@ def _rotate_scale_by_b(x, signs, block):                # 1/B instead of 1/sqrt(
     return (_good_rotate(x, signs, block) * np.float32(1.0 / np.sqrt(block))).astype(np.float32)
 
 
+def _importance_sigma_not_squared(U, s, Vt, grads, S_inv=None):   # sigma instead of sigma^2
+    V = Vt.T
+    acc = np.zeros(s.size)
+    for G in grads:
+        Gw = G if S_inv is None else G @ S_inv.T
+        acc += np.diag(U.T @ Gw @ V) ** 2
+    return s * acc / len(grads)
+
+
+def _importance_whitening_untransposed(U, s, Vt, grads, S_inv=None):   # S^-1 where S^-T belongs
+    V = Vt.T
+    acc = np.zeros(s.size)
+    for G in grads:
+        Gw = G if S_inv is None else G @ S_inv
+        acc += np.diag(U.T @ Gw @ V) ** 2
+    return s ** 2 * acc / len(grads)
+
+
+def _allocate_lowest(scores, budget):                   # keeps the least important
+    entries = sorted((float(v), l, i) for l, sc in enumerate(scores) for i, v in enumerate(sc))
+    kept = [[] for _ in scores]
+    for _, l, i in entries[:budget]:
+        kept[l].append(i)
+    return [np.array(sorted(k), dtype=np.int64) for k in kept]
+
+
 MUTATIONS = [
     ("split_beta", _split_sigma_both, [C.check_full_rank_reconstruction, C.check_beta_and_rotation_invariance]),
     ("split_beta", _split_truncate_wrong_end, [C.check_eckart_young]),
@@ -116,6 +142,9 @@ MUTATIONS = [
     ("walsh_hadamard_rows", _wht_sub_swapped, [C.check_rotation_matrix_and_transform]),
     ("rotate_act", _rotate_no_signs, [C.check_rotation_matrix_and_transform]),
     ("rotate_act", _rotate_scale_by_b, [C.check_rotation_matrix_and_transform]),
+    ("importance_scores", _importance_sigma_not_squared, [C.check_importance_closed_form]),
+    ("importance_scores", _importance_whitening_untransposed, [C.check_importance_closed_form]),
+    ("allocate_ranks", _allocate_lowest, [C.check_rank_allocation]),
 ]
 
 

@@ -24,6 +24,9 @@ PINS = [
     C.check_printed_cost_ratios,
     C.check_rotation_matrix_and_transform,
     C.check_rotation_fold_and_error_reduction,
+    C.check_importance_closed_form,
+    C.check_rank_allocation,
+    C.check_beta_search,
 ]
 
 
