@@ -210,3 +210,39 @@ class DeviceCache:
     @property
     def max_len(self):
         return self.c.max_len
+
+
+def projection_evaluator(n_q_heads, n_kv_heads, head_dim, w_bits=8, w_group=0, a_bits=8):
+    """A callable (A, B, X) -> the fp16 Q | K | V of the quantized projection of
+    X through the layer built from W^d = A and W^u = B on the GPU (weights
+    quantized by the offline stage, activations and latent by the library),
+    for offline searches such as the beta search of ``prep.search_beta``."""
+    import numpy as np
+    import torch
+
+    from . import prep
+
+    def project(A, B, X):
+        layer = DeviceLayer(prep.quantize_layer(A, B, n_q_heads, n_kv_heads, head_dim, w_bits, w_group))
+        M, d = X.shape
+        r, N = layer.r, layer.N
+        per = 1 if a_bits == 8 else 2
+        x = torch.from_numpy(np.ascontiguousarray(X, dtype=np.float16)).cuda()
+        xq = torch.empty((M, d // per), dtype=torch.uint8, device="cuda")
+        sx = torch.empty((M,), dtype=torch.float32, device="cuda")
+        c_h = torch.empty((M, r), dtype=torch.float16, device="cuda")
+        cq = torch.empty((M, r // per), dtype=torch.uint8, device="cuda")
+        sc = torch.empty((M,), dtype=torch.float32, device="cuda")
+        nq, nkv = n_q_heads * head_dim, n_kv_heads * head_dim
+        q = torch.empty((M, nq), dtype=torch.float16, device="cuda")
+        k = torch.empty((M, nkv), dtype=torch.float16, device="cuda")
+        v = torch.empty((M, nkv), dtype=torch.float16, device="cuda")
+        s = stream_handle()
+        check(qsvd_quantize_act(ptr(x), M, d, d, a_bits, 1.0, ptr(xq), ptr(sx), s))
+        check(qsvd_lowrank_qkv_prefill(layer.c, ptr(xq), ptr(sx), M, a_bits, 7, ptr(c_h), ptr(cq), ptr(sc),
+                                       ptr(q), ptr(k), ptr(v), 0, 0, 0, 0, s))
+        out = torch.cat([q, k, v], dim=1).cpu().numpy()
+        del layer
+        return out
+
+    return project

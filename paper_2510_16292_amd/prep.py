@@ -51,6 +51,67 @@ def truncated_factors(W: np.ndarray, r: int, beta: float):
     return factors_from_svd(U[:, :r], s[:r], Vt[:r].T, beta)
 
 
+# ---------------------------------------------------------------------------
+# Rank allocation by importance score and the beta search (Section 3.2,
+# Eq. 10 and Appendix A; Eq. 14)
+# ---------------------------------------------------------------------------
+
+def importance_scores(U: np.ndarray, s: np.ndarray, Vt: np.ndarray, grads=None, factored=None,
+                      S_inv: np.ndarray = None) -> np.ndarray:
+    """Importance of every singular value (Eq. 10): mean over calibration
+    samples of sigma_i^2 [U^T G V]_(i,i)^2, with G S^{-T} in place of G when the
+    SVD was of a whitened W S (Appendix A).  Gradients come either explicitly
+    (`grads`: d x N arrays) or factored as a linear layer's (X_n, dY_n) pairs,
+    G_n = X_n^T dY_n, in which case [U^T G V]_(i,i) = sum_t (X_n U)[t,i]
+    (dY_n S^{-T} V)[t,i] and no d x N gradient is formed."""
+    V = np.asarray(Vt, dtype=np.float64).T
+    U = np.asarray(U, dtype=np.float64)
+    total, count = np.zeros(s.size), 0
+    for G in grads or []:
+        Gw = np.asarray(G, dtype=np.float64)
+        if S_inv is not None:
+            Gw = Gw @ S_inv.T
+        total += np.einsum("ji,ji->i", U, Gw @ V) ** 2
+        count += 1
+    for Xn, dYn in factored or []:
+        dYw = np.asarray(dYn, dtype=np.float64)
+        if S_inv is not None:
+            dYw = dYw @ S_inv.T
+        total += np.einsum("ti,ti->i", np.asarray(Xn, dtype=np.float64) @ U, dYw @ V) ** 2
+        count += 1
+    return np.asarray(s, dtype=np.float64) ** 2 * total / max(count, 1)
+
+
+def allocate_ranks(scores, budget: int):
+    """Cross-layer rank selection (Section 3.2): every singular value of every
+    layer ranked by importance, the `budget` highest kept (ties to the lower
+    layer, then the lower index).  Returns each layer's kept indices, sorted."""
+    layer = np.concatenate([np.full(len(sc), l) for l, sc in enumerate(scores)]) if scores else np.zeros(0)
+    index = np.concatenate([np.arange(len(sc)) for sc in scores]) if scores else np.zeros(0)
+    value = np.concatenate([np.asarray(sc, dtype=np.float64) for sc in scores]) if scores else np.zeros(0)
+    order = np.lexsort((index, layer, -value))[:budget]
+    return [np.sort(index[order][layer[order] == l]).astype(np.int64) for l in range(len(scores))]
+
+
+def select_factors(U: np.ndarray, s: np.ndarray, Vt: np.ndarray, keep: np.ndarray, beta: float):
+    """W^d, W^u of the kept singular triplets (any subset of indices), Eq. 3-4."""
+    return factors_from_svd(U[:, keep], s[keep], np.asarray(Vt)[keep].T, beta)
+
+
+def search_beta(U_r: np.ndarray, s_r: np.ndarray, Vt_r: np.ndarray, X: np.ndarray, betas, project):
+    """Per-layer line search of Eq. 14 on the projection: for each beta of the
+    grid, Y' = project(A, B, X) (the quantized Q | K | V of the layer built
+    from W^d = U Sigma^beta, W^u = Sigma^(1 - beta) V^T) against the fp64
+    Y = X W^d W^u; returns (the first beta with the least squared error, all
+    errors)."""
+    Xf = np.asarray(X, dtype=np.float64)
+    errs = []
+    for b in betas:
+        A, B = factors_from_svd(U_r, s_r, np.asarray(Vt_r).T, b)
+        errs.append(float(np.sum((Xf @ A @ B - np.asarray(project(A, B, X), dtype=np.float64)) ** 2)))
+    return betas[int(np.argmin(errs))], errs
+
+
 def fold_input_rotation(A: np.ndarray, signs: np.ndarray, block: int) -> np.ndarray:
     """H1 W^d for the online input rotation H1 = blockdiag(H_B) diag(signs) /
     sqrt(B) (Eq. 11), so that Q(X H1^T) Q(H1 W^d) replaces Q(X) Q(W^d): rows

@@ -190,6 +190,37 @@ def test_prefill_with_online_rotation(tiny):
     assert e_rot < e_plain
 
 
+# ------------------------------------------------------------------ offline beta search on the GPU path
+
+def test_beta_search_with_gpu_projection():
+    """The beta line search (Eq. 14) scoring each beta with the GPU's quantized
+    projection picks the same beta with the same squared errors as with the
+    oracle's (the Q | K | V are bit-exact), on a layer with a decaying
+    spectrum and outlier-heavy activations."""
+    wl = configs.get(1)
+    L = wl.layer
+    g = np.random.default_rng(5)
+    Q1, _ = np.linalg.qr(g.standard_normal((L.d, L.d)))
+    Q2, _ = np.linalg.qr(g.standard_normal((L.N, L.d)))
+    W = Q1 @ np.diag(0.5 * np.arange(1, L.d + 1) ** -0.7) @ Q2.T
+    U, s, Vt = O.joint_svd(W)
+    Ur, sr, Vtr = U[:, :L.r], s[:L.r], Vt[:L.r]
+    X = gen.prefill_activations(wl)
+    betas = [0.0, 0.2, 0.4, 0.5, 0.6, 0.8, 1.0]
+
+    def oracle_proj(A, Bm, Xc):
+        p = O.prefill(O.make_layer(A, Bm, L.n_q_heads, L.n_kv_heads, L.head_dim, 8, 0), Xc, 8)
+        return np.concatenate([p["Q"], p["K"], p["V"]], axis=1)
+
+    H.say("beta search on the GPU projection")
+    best, errs = prep.search_beta(Ur, sr, Vtr, X, betas, B.projection_evaluator(L.n_q_heads, L.n_kv_heads,
+                                                                                L.head_dim))
+    best_o, vals_o = O.beta_search(Ur, sr, Vtr, X, betas, oracle_proj)
+    H.say(f"  beta {best}: errors {[round(e, 4) for e in errs]}")
+    assert best == best_o
+    assert np.array_equal(np.array(errs), np.array(vals_o))
+
+
 # ------------------------------------------------------------------ a2-a4: projection
 
 def _check_prefill(ol, got, X):
