@@ -50,6 +50,7 @@ def parse():
     ap.add_argument("--mode", choices=["auto", "absorbed", "reconstruct"], default="auto")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without the kernel events")
+    ap.add_argument("--no-graph", action="store_true", help="skip the graph-replay timings (for profiler runs)")
     ap.add_argument("--legs", default="decode,prefill,gqa,stack",
                     help="comma list of legs to run: decode, prefill, gqa (Qwen2-VL-shaped decode), "
                          "stack (13B-shaped 40-layer prefill and decode)")
@@ -118,8 +119,45 @@ def layer_weights(wl, w_bits=8, w_group=0):
                                             w_bits, w_group)
 
 
+def graph_line(res):
+    if res.get("graph_tokens_per_s") is None:
+        return None
+    return {"value": round(res["graph_tokens_per_s"], 1), "unit": "tokens/s",
+            "ms_per_step": round(res["graph_ms_per_step"], 5)}
+
+
+def graph_replay(caches, hold, final, rounds, n_layers, batch, step):
+    """The decode steps of a full rotation through the layers captured once as
+    a graph and replayed per visit (launch grids follow each cache's host
+    max_len, held at the final length; chunks past a sequence's length return
+    at once)."""
+    import torch
+
+    from paper_2510_16292_amd import binding as B
+    hold(final - 1)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        gs = B.stream_handle()
+        for i in range(n_layers):
+            step(i, gs)
+    hold(final)
+    g.replay()
+    hold(final)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(rounds):
+        g.replay()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    del g
+    for c in caches:
+        c.c.max_len = int(c.seq_len.max().item())        # where the replays left the sequences
+    return {"graph_ms_per_step": (t1 - t0) * 1e3 / (rounds * n_layers),
+            "graph_tokens_per_s": batch * rounds * n_layers / (t1 - t0)}
+
+
 def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_name, profile, traffic_summary,
-               compare_forms):
+               compare_forms, graph=True):
     """Decode steps of one attention layer: quantize the new tokens, project
     them (C, Q(C), Q), append, attend over the latent cache.  Steps cycle
     through n_layers distinct layers (weights and caches) so the working set
@@ -234,27 +272,11 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
         torch.cuda.synchronize()
 
     final = ctx0 + visits
-    hold(final - 1)
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        gs = B.stream_handle()
-        for i in range(n_layers):
-            step(i, gs)
     rounds = max(steps // n_layers, 1)
-    hold(final)
-    g.replay()
-    hold(final)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(rounds):
-        g.replay()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    res["graph_ms_per_step"] = (t1 - t0) * 1e3 / (rounds * n_layers)
-    res["graph_tokens_per_s"] = batch * rounds * n_layers / (t1 - t0)
-    del g
-    for c in caches:
-        c.c.max_len = ctx0 + rounds          # the replays left every sequence at this length
+    if not graph:
+        res["graph_ms_per_step"] = res["graph_tokens_per_s"] = None
+    else:
+        res.update(graph_replay(caches, hold, final, rounds, n_layers, batch, step))
     if compare_forms:
         # absorbed vs reconstruct on this layer, attention call alone (a few calls each)
         forms = {}
@@ -280,7 +302,7 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
 def bench_decode(args, wl, host_layer):
     from paper_2510_16292_amd import binding as B
     return run_decode(wl, host_layer, B.QSVD_CACHE_F16, N_LAYERS, DECODE_BATCH, CTX0, args.steps, args.warmup,
-                      args.mode, not args.no_profile, ATTN_TRAFFIC_SUMMARY, True)
+                      args.mode, not args.no_profile, ATTN_TRAFFIC_SUMMARY, True, not args.no_graph)
 
 
 def bench_decode_gqa(args):
@@ -293,15 +315,14 @@ def bench_decode_gqa(args):
     _, host = layer_weights(wl4, wl4.w_bits, wl4.w_group)
     steps = wl4.n_layers * GQA_VISITS
     res = run_decode(wl4, host, B.QSVD_CACHE_I8, wl4.n_layers, wl4.decode_batch, wl4.decode_ctx, steps,
-                     wl4.n_layers, "auto", not args.no_profile, None, False)
+                     wl4.n_layers, "auto", not args.no_profile, None, False, not args.no_graph)
     out = {"value": round(res["tokens_per_s"], 1), "unit": "tokens/s", "ms_per_step": round(res["ms_per_step"], 5),
            "steps": steps,
            "workload": f"qwen2-vl-7b-shaped GQA layer decode: batch {wl4.decode_batch}, int8 latent cache r=1024 "
                        f"with per-token scales, context {wl4.decode_ctx}->{wl4.decode_ctx + GQA_VISITS}, "
                        f"W4A8 (int4 per-group-128 weights), {wl4.n_layers} rotated layers; tokens/s per layer step",
            "mean_context": round(res["mean_context"], 1),
-           "graph_replay": {"value": round(res["graph_tokens_per_s"], 1), "unit": "tokens/s",
-                            "ms_per_step": round(res["graph_ms_per_step"], 5)}}
+           "graph_replay": graph_line(res)}
     if "roofline" in res:
         out["roofline"] = res["roofline"]
         out["attn_kernel_us"] = round(res["attn_kernel_us"], 2)
@@ -538,6 +559,21 @@ def bench_stack_decode(args, wl5, ranks, layers):
     B.profile_reset()
     ctx_mean = ctx0 + (steps + 1) / 2.0
     attn_bytes = sum(batch * ctx_mean * (r // 2 + 4) for r in ranks) * steps
+    res = {"eager_ms_per_step": round(eager_s * 1e3, 4), "eager_tokens_per_s": round(batch / eager_s, 1),
+           "steps": steps, "layers": len(ranks), "batch": batch, "mean_context": round(ctx0 + (steps + 1) / 2.0, 1)}
+    if n:
+        res["attn_kernel_us"] = round(kms * 1e-3 / n * 1e6, 2)
+        achieved = attn_bytes / (kms * 1e-3) / 1e9
+        res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                           "kernel": "latent_attn_h16_kernel (int4 cache)", "launches": n,
+                           "bytes_per_launch": int(attn_bytes / n)}
+    if args.no_graph:
+        res.update(value=res["eager_tokens_per_s"], unit="tokens/s", ms_per_step=res["eager_ms_per_step"],
+                   us_per_layer_step=round(eager_s * 1e6 / len(ranks), 2), timing="eager")
+        del caches
+        torch.cuda.empty_cache()
+        return res
     # the same step captured once as a graph of all layers, replayed per step
     reset(ctx0 + steps - 1)
     g = torch.cuda.CUDAGraph()
@@ -552,18 +588,8 @@ def bench_stack_decode(args, wl5, ranks, layers):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     graph_s = (t1 - t0) / steps
-    res = {"value": round(batch / graph_s, 1), "unit": "tokens/s", "ms_per_step": round(graph_s * 1e3, 4),
-           "eager_ms_per_step": round(eager_s * 1e3, 4), "eager_tokens_per_s": round(batch / eager_s, 1),
-           "steps": steps, "layers": len(ranks), "batch": batch, "mean_context": round(ctx_mean, 1),
-           "us_per_layer_step": round(graph_s * 1e6 / len(ranks), 2)}
-    if n:
-        avg_s = kms * 1e-3 / n
-        achieved = attn_bytes / (kms * 1e-3) / 1e9
-        res["attn_kernel_us"] = round(avg_s * 1e6, 2)
-        res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                           "kernel": "latent_attn_h16_kernel (int4 cache)", "launches": n,
-                           "bytes_per_launch": int(attn_bytes / n)}
+    res.update(value=round(batch / graph_s, 1), unit="tokens/s", ms_per_step=round(graph_s * 1e3, 4),
+               us_per_layer_step=round(graph_s * 1e6 / len(ranks), 2), timing="graph replay")
     del g, caches
     torch.cuda.empty_cache()
     return res
@@ -679,8 +705,7 @@ def main():
                    "mean_context": round(dec["mean_context"], 1), "attention": args.mode},
         "roofline": dec.get("roofline"),
         "attn_kernel_us": round(dec.get("attn_kernel_us", 0.0), 2),
-        "graph_replay": {"value": round(dec["graph_tokens_per_s"], 1), "unit": "tokens/s",
-                         "ms_per_step": round(dec["graph_ms_per_step"], 5)},
+        "graph_replay": graph_line(dec),
         "attention_form_us": dec["attention_form_us"],
         "prefill": pre,
     }
