@@ -544,6 +544,87 @@ def test_decode_qwen2vl_w4a8_int8_cache_full_size(qwen):
         assert ok, (b, info)
 
 
+# ------------------------------------------------------------------ 13B-shaped stack layer at full size
+
+@pytest.fixture(scope="module")
+def stack13b():
+    """One layer of the LLaVA-1.5-13B-shaped stack at its widest rank: d=5120,
+    40 heads x 128, r=3072, int4 weights in groups of 128 (random factors:
+    the stack's timing runs draw codes directly, parity needs a prepared
+    layer)."""
+    wl = configs.get(5)
+    L = configs.LayerShape(d=5120, n_q_heads=40, n_kv_heads=40, head_dim=128, r=3072)
+    ol, dl = _random_factor_layer(L, 13013, w_bits=4, w_group=128)
+    return gen.with_rank(wl, 3072), L, ol, dl
+
+
+def test_prefill_13b_w4a4_full_size_sampled(stack13b):
+    """The stack's prefill at full size (8 x 704 = 5632 tokens, W4A4, the launch
+    the bench times): sampled rows bit-exact against the oracle."""
+    wl, L, ol, dl = stack13b
+    X = gen.prefill_activations(wl)
+    M = X.shape[0]
+    H.say(f"prefill 13b w4a4 M={M} r={L.r}")
+    got = H.Prefill(dl, M, debug=False, abits=4).run(H.dev(X)).result()
+    rows = np.array([0, 1, 575, 703, 704, 2816, 4223, M - 1])
+    ref = O.prefill(ol, X[rows], 4)
+    assert np.array_equal(got["xq"][rows].view(np.uint8), O.pack_int4(ref["xq"]))
+    assert np.array_equal(got["cq"][rows].view(np.uint8), O.pack_int4(ref["cq"]))
+    for key in ("sx", "sc"):
+        assert np.array_equal(got[key][rows].view(np.uint32), ref[key].view(np.uint32)), key
+    for key in ("C_h", "Q", "K", "V"):
+        assert np.array_equal(got[key][rows].view(np.uint16), ref[key].view(np.uint16)), key
+    for key in ("Q", "K", "V"):
+        assert np.all(np.isfinite(got[key].astype(np.float32))), key
+
+
+def test_decode_13b_int4_cache_full_size_sampled(stack13b):
+    """The stack's decode at full size for its widest layer: batch 8 over 4096
+    cached tokens in an int4 latent cache (r = 3072, three 128-column units per
+    wave), W4A4 projection of the new tokens, 40 query heads in 16-head blocks;
+    two sequences checked against the oracle's latent form, all outputs finite,
+    run twice bit-identically."""
+    wl, L, ol, dl = stack13b
+    torch = H.torch()
+    batch, L0 = wl.decode_batch, wl.decode_ctx
+    cap = L0 + 4
+    rows = gen.latent_rows(wl, batch, L0)
+    data = np.zeros((batch, cap, L.r // 2), np.uint8)
+    scale = np.zeros((batch, cap), np.float32)
+    codes_of = {}
+    for b in range(batch):
+        codes, sc = O.quantize_act(rows[b], 4)
+        data[b, :L0], scale[b, :L0] = O.pack_int4(codes), sc
+        if b in (0, 5):
+            codes_of[b] = codes
+    dc = B.DeviceCache(B.QSVD_CACHE_I4, batch, cap, L.r, [L0] * batch)
+    dc.data.copy_(H.dev(data))
+    dc.scale.copy_(H.dev(scale))
+    xt = gen.decode_activations(wl, 0, batch=batch)
+    H.say(f"decode 13b int4 cache full size r={L.r}")
+    p = H.Prefill(dl, batch, mask=B.QSVD_OUT_Q, debug=False, abits=4).run(H.dev(xt))
+    cq4 = torch.empty((batch, L.r // 2), dtype=torch.uint8, device="cuda")
+    sc4 = torch.empty((batch,), dtype=torch.float32, device="cuda")
+    B.check(B.qsvd_quantize_act(B.ptr(p.c_h), batch, L.r, L.r, 4, 1.0, B.ptr(cq4), B.ptr(sc4), B.stream_handle()))
+    H.append(dc, cq=cq4, sc=sc4, n_new=1)
+    out = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
+    out2 = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
+    assert np.array_equal(out.view(np.uint16), out2.view(np.uint16))
+    assert np.all(np.isfinite(out.astype(np.float32)))
+    for b in (0, 5):
+        ref = O.prefill(ol, xt[b:b + 1], 4)
+        assert np.array_equal(H.host(p.q)[b:b + 1].view(np.uint16), ref["Q"].view(np.uint16))
+        q4, s4 = O.quantize_act(ref["C_h"], 4)
+        oc = O.LatentCache(O.CACHE_I4, 1, cap, L.r)
+        oc.append(0, None, codes_of[b], scale[b, :L0])
+        oc.append(0, None, q4, s4)
+        assert np.array_equal(H.host(dc.data)[b, :L0 + 1], oc.data[0, :L0 + 1])
+        want = O.attention_absorbed(ol, oc, ref["Q"][:, None, :], 1)[:, 0, :]
+        ok, info = H.close_enough(out[b:b + 1], want)
+        H.say(f"  b={b} max-abs, rel-L2, rms = {info}")
+        assert ok, (b, info)
+
+
 # ------------------------------------------------------------------ prefill attention (q_len > 1)
 
 def test_prefill_attention_tiny_causal(tiny):
