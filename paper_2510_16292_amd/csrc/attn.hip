@@ -228,8 +228,10 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
 //   partial S^T of all waves are summed through LDS in a fixed order
 //   online softmax per head in fp32 (lane l tracks head l % 32)
 //   O^T[slice] (r x heads) += C_tile[:, slice]^T P^T          (fp16 MFMA, K = 32 tokens)
-// The C tile reaches the first MFMA straight from HBM (token-major rows are
-// the A operand as stored) and the second through a wave-private LDS copy.
+// Each wave copies its slice of the C tile (as exact fp16) into a private
+// LDS area as soon as it arrives, reissues the next tile's loads into the
+// same registers, and reads the copy back for both MFMAs (row reads for the
+// scores, transposing reads for P C).
 // ---------------------------------------------------------------------------
 template <int RW, int NW, int FMT>
 __global__ void __launch_bounds__(NW * 64)
@@ -312,8 +314,56 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
         raw[i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const int8_t*>(cdata) + off + kcol(2 * i, half));
     }
   };
+  // Staging the tile before the score product (and reissuing the loads
+  // first) measured faster for fp16 rows and keeps the widest integer
+  // slices from spilling; narrower integer slices convert in registers
+  // and feed the score product directly.
+  constexpr bool kStageFirst = F16C || RW >= 192;
   load_tile(t_begin);
   for (int t0 = t_begin; t0 < t_end; t0 += 32) {
+    f32x16 sacc = f32x16{};
+    if constexpr (kStageFirst) {
+    // The tile (as exact fp16) goes to this wave's LDS copy first, so that
+    // its registers take the next tile's loads before any product runs; the
+    // score product reads its A operand back from the copy, one fragment per
+    // MFMA.
+    if constexpr (F16C) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(ks, half)) = raw[ks];
+    } else {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sc_cur[v] = sc_next[v];
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        f16x8 c0, c1;
+        if constexpr (I4C) {
+          c0 = cvt_i4x8(raw[i].x);
+          c1 = cvt_i4x8(raw[i].y);
+        } else {
+          c0 = cvt_i8x8(raw[i].x, raw[i].y);
+          c1 = cvt_i8x8(raw[i].z, raw[i].w);
+        }
+        *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i, half)) = c0;
+        *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i + 1, half)) = c1;
+      }
+    }
+    if (t0 + 32 < t_end) load_tile(t0 + 32);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const f16x8 cf = *reinterpret_cast<const f16x8*>(cst + l32 * CST + kcol(ks, half));
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_f16(cf, qf[ks], sacc, 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);        // two fragment reads ahead
+#pragma unroll
+    for (int ks = 0; ks < KS - 2; ++ks) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // the next fragment read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    } else {
     f16x8 cf[KS];
     if constexpr (F16C) {
 #pragma unroll
@@ -332,7 +382,6 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
         }
       }
     }
-    f32x16 sacc = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_f16(cf[ks], qf[ks], sacc, 0, 0, 0);
@@ -342,6 +391,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     // The next tile streams in while this one is reduced, normalized and
     // multiplied into the output.
     if (t0 + 32 < t_end) load_tile(t0 + 32);
+    }
 #pragma unroll
     for (int vb = 0; vb < 4; ++vb)
       spart4[(w * 4 + vb) * 64 + lane] = f32x4{sacc[4 * vb], sacc[4 * vb + 1], sacc[4 * vb + 2], sacc[4 * vb + 3]};
