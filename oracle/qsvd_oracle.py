@@ -489,8 +489,29 @@ def _softmax(s: np.ndarray) -> np.ndarray:
     return e / np.sum(e, axis=-1, keepdims=True)
 
 
+def rope(x: np.ndarray, positions: np.ndarray, theta: float, dh: int) -> np.ndarray:
+    """Rotary position embedding of the head vectors of x [T, heads * dh] at
+    the given positions (not in the paper, which has no position encoding;
+    the variant for layers that apply it to q and k).  Reading: rotate-half
+    pairs (j, j + dh/2) turned by the angle pos * theta^(-2j/dh), in fp64:
+    (a, b) -> (a cos - b sin, b cos + a sin)."""
+    x = np.asarray(x, dtype=np.float64)
+    T, n = x.shape
+    half = dh // 2
+    inv = theta ** (-2.0 * np.arange(half) / dh)
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * inv[None, :]      # [T, half]
+    c, s = np.cos(ang), np.sin(ang)
+    out = np.empty_like(x)
+    for h in range(n // dh):
+        a = x[:, h * dh:h * dh + half]
+        b = x[:, h * dh + half:(h + 1) * dh]
+        out[:, h * dh:h * dh + half] = a * c - b * s
+        out[:, h * dh + half:(h + 1) * dh] = b * c + a * s
+    return out
+
+
 def attention_reference(layer: Layer, cache: LatentCache, q: np.ndarray, q_len: int = 1,
-                        sm_scale: float = None, batches=None, heads=None) -> np.ndarray:
+                        sm_scale: float = None, batches=None, heads=None, rope_theta: float = None) -> np.ndarray:
     """Plain definition: rebuild K = C W^u_k and V = C W^u_v from the cached
     latent (Eq. 5) and attend with the current queries (Section 3.1).
 
@@ -498,6 +519,10 @@ def attention_reference(layer: Layer, cache: LatentCache, q: np.ndarray, q_len: 
     q_len positions of each sequence and attend causally to positions
     [0, own position].  Reading: the softmax scale is 1/sqrt(head_dim); the
     latent is used as stored (dequantized), times the dequantized W^u.
+
+    With rope_theta, q and every rebuilt K row are first rotated (:func:`rope`)
+    at their positions; then K can no longer be folded into the query, which
+    is why only this plain form takes it.
 
     Returns fp64 [B, q_len, Hq*head_dim] (rows/heads not requested are 0).
     """
@@ -515,11 +540,15 @@ def attention_reference(layer: Layer, cache: LatentCache, q: np.ndarray, q_len: 
         L = C.shape[0]
         K = C @ Bk                       # [L, Hkv*dh]
         V = C @ Bv
+        qb = q[b]
+        if rope_theta:
+            K = rope(K, np.arange(L), rope_theta, dh)
+            qb = rope(qb, np.arange(L - q_len, L), rope_theta, dh)
         for i in range(q_len):
             pos = L - q_len + i
             for h in heads:
                 g = kv_group(h, Hq, Hkv)
-                qh = q[b, i, h * dh:(h + 1) * dh]
+                qh = qb[i, h * dh:(h + 1) * dh]
                 s = (K[:pos + 1, g * dh:(g + 1) * dh] @ qh) * sm
                 p = _softmax(s)
                 out[b, i, h * dh:(h + 1) * dh] = p @ V[:pos + 1, g * dh:(g + 1) * dh]

@@ -673,6 +673,53 @@ def check_beta_search():
     assert best == betas[int(np.argmin(vals))]
 
 
+# ---------------------------------------------------------------- rotary variant
+
+def check_rope():
+    """Rotary embedding: position 0 is the identity, norms are kept, a single
+    pair at dh = 2 turns by exactly the position, the score of a rotated
+    query and key depends only on the position difference, and attention
+    with rope_theta rotates exactly the rebuilt K and the query."""
+    g = np.random.default_rng(8)
+    dh, heads = 16, 3
+    x = g.standard_normal((5, heads * dh))
+    assert np.allclose(O.rope(x, np.zeros(5), 10000.0, dh), x, atol=0)
+    y = O.rope(x, np.arange(5) * 37, 10000.0, dh)
+    for h in range(heads):
+        assert np.allclose(np.linalg.norm(y[:, h * dh:(h + 1) * dh], axis=1),
+                           np.linalg.norm(x[:, h * dh:(h + 1) * dh], axis=1), rtol=1e-12)
+    v = np.array([[1.0, 0.0]])
+    for pos in (0.0, 1.0, 2.5):
+        assert np.allclose(O.rope(v, np.array([pos]), 10000.0, 2), [[np.cos(pos), np.sin(pos)]], atol=1e-15)
+    # dh = 4: pairs (0, 2) at frequency 1 and (1, 3) at theta^(-1/2)
+    v4 = np.array([[0.0, 1.0, 0.0, 0.0]])
+    w4 = O.rope(v4, np.array([3.0]), 100.0, 4)
+    assert np.allclose(w4, [[0.0, np.cos(0.3), 0.0, np.sin(0.3)]], atol=1e-15)
+    q, k = g.standard_normal((1, dh)), g.standard_normal((1, dh))
+    base = (O.rope(q, [9], 500.0, dh) @ O.rope(k, [4], 500.0, dh).T).item()
+    for shift in (1, 100, 3000):
+        assert abs((O.rope(q, [9 + shift], 500.0, dh) @ O.rope(k, [4 + shift], 500.0, dh).T).item() - base) < 1e-9
+    # attention: rope_theta rotates q and the rebuilt K; the result equals a
+    # textbook attention over explicitly rotated K
+    layer, _ = tiny_gqa_layer()
+    Hq, Hkv, hd = layer.n_q_heads, layer.n_kv_heads, layer.head_dim
+    L = 11
+    C = g.standard_normal((L, layer.r)).astype(np.float16)
+    cache = O.LatentCache(O.CACHE_F16, 1, L, layer.r)
+    cache.append(0, C)
+    qv = g.standard_normal((1, 1, Hq * hd)).astype(np.float16)
+    got = O.attention_reference(layer, cache, qv, 1, rope_theta=1000.0)
+    Bh = layer.B_hat()
+    nq, nkv = Hq * hd, Hkv * hd
+    K = O.rope(C.astype(np.float64) @ Bh[:, nq:nq + nkv], np.arange(L), 1000.0, hd)
+    V = C.astype(np.float64) @ Bh[:, nq + nkv:]
+    qr = O.rope(qv[0].astype(np.float64), [L - 1], 1000.0, hd)
+    want = _textbook_mha(qr, K, V, Hq, Hkv, hd, 1)
+    assert np.allclose(got[0], want, rtol=1e-10, atol=1e-12)
+    plain = O.attention_reference(layer, cache, qv, 1)
+    assert np.max(np.abs(plain - got)) > 1e-3
+
+
 # ---------------------------------------------------------------- P12-P13: cost model
 
 def check_cost_model():

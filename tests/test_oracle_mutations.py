@@ -128,6 +128,25 @@ def _allocate_lowest(scores, budget):                   # keeps the least import
     return [np.array(sorted(k), dtype=np.int64) for k in kept]
 
 
+def _rope_freq_wrong(x, positions, theta, dh):            # theta^(-j/dh) instead of theta^(-2j/dh)
+    x = np.asarray(x, dtype=np.float64)
+    half = dh // 2
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * (theta ** (-1.0 * np.arange(half) / dh))[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    out = np.empty_like(x)
+    for h in range(x.shape[1] // dh):
+        a, b = x[:, h * dh:h * dh + half], x[:, h * dh + half:(h + 1) * dh]
+        out[:, h * dh:h * dh + half], out[:, h * dh + half:(h + 1) * dh] = a * c - b * s, b * c + a * s
+    return out
+
+
+def _rope_sign_wrong(x, positions, theta, dh):            # rotation the other way
+    return _rope_freq_ok(x, -np.asarray(positions, dtype=np.float64), theta, dh)
+
+
+_rope_freq_ok = O.rope
+
+
 MUTATIONS = [
     ("split_beta", _split_sigma_both, [C.check_full_rank_reconstruction, C.check_beta_and_rotation_invariance]),
     ("split_beta", _split_truncate_wrong_end, [C.check_eckart_young]),
@@ -145,6 +164,8 @@ MUTATIONS = [
     ("importance_scores", _importance_sigma_not_squared, [C.check_importance_closed_form]),
     ("importance_scores", _importance_whitening_untransposed, [C.check_importance_closed_form]),
     ("allocate_ranks", _allocate_lowest, [C.check_rank_allocation]),
+    ("rope", _rope_freq_wrong, [C.check_rope]),
+    ("rope", _rope_sign_wrong, [C.check_rope]),
 ]
 
 

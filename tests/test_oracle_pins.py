@@ -27,6 +27,7 @@ PINS = [
     C.check_importance_closed_form,
     C.check_rank_allocation,
     C.check_beta_search,
+    C.check_rope,
 ]
 
 
