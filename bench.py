@@ -278,18 +278,27 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
     else:
         res.update(graph_replay(caches, hold, final, rounds, n_layers, batch, step))
     if compare_forms:
-        # absorbed vs reconstruct on this layer, attention call alone (a few calls each)
+        # absorbed vs reconstruct (plain, and with rotary embeddings of base
+        # 1e4) on this layer, attention call alone (a few calls each)
         forms = {}
-        for name, m in (("absorbed", B.QSVD_ATTN_ABSORBED), ("reconstruct", B.QSVD_ATTN_RECONSTRUCT)):
+        for name, m, theta in (("absorbed", B.QSVD_ATTN_ABSORBED, 0.0),
+                               ("reconstruct", B.QSVD_ATTN_RECONSTRUCT, 0.0),
+                               ("reconstruct_rope", B.QSVD_ATTN_RECONSTRUCT, 1.0e4)):
             wsb = B.qsvd_decode_workspace_size(layers[0].c, caches[0].c, 1, m)
             ws = torch.empty((wsb,), dtype=torch.uint8, device="cuda")
             reps = 3 if m == B.QSVD_ATTN_RECONSTRUCT else 20
+
+            def call():
+                if theta:
+                    return lib.qsvd_latent_decode_attention_rope(lrefs[0], crefs[0], q_p, 1, m, 0.0, theta, out_p,
+                                                                 P(ws), wsb, s)
+                return lib.qsvd_latent_decode_attention(lrefs[0], crefs[0], q_p, 1, m, 0.0, out_p, P(ws), wsb, s)
             for _ in range(2):
-                B.check(lib.qsvd_latent_decode_attention(lrefs[0], crefs[0], q_p, 1, m, 0.0, out_p, P(ws), wsb, s))
+                B.check(call())
             torch.cuda.synchronize()
             a = time.perf_counter()
             for _ in range(reps):
-                B.check(lib.qsvd_latent_decode_attention(lrefs[0], crefs[0], q_p, 1, m, 0.0, out_p, P(ws), wsb, s))
+                B.check(call())
             torch.cuda.synchronize()
             forms[name] = round((time.perf_counter() - a) * 1e6 / reps, 1)
             del ws
@@ -315,14 +324,15 @@ def bench_decode_gqa(args):
     _, host = layer_weights(wl4, wl4.w_bits, wl4.w_group)
     steps = wl4.n_layers * GQA_VISITS
     res = run_decode(wl4, host, B.QSVD_CACHE_I8, wl4.n_layers, wl4.decode_batch, wl4.decode_ctx, steps,
-                     wl4.n_layers, "auto", not args.no_profile, None, False, not args.no_graph)
+                     wl4.n_layers, "auto", not args.no_profile, None, True, not args.no_graph)
     out = {"value": round(res["tokens_per_s"], 1), "unit": "tokens/s", "ms_per_step": round(res["ms_per_step"], 5),
            "steps": steps,
            "workload": f"qwen2-vl-7b-shaped GQA layer decode: batch {wl4.decode_batch}, int8 latent cache r=1024 "
                        f"with per-token scales, context {wl4.decode_ctx}->{wl4.decode_ctx + GQA_VISITS}, "
                        f"W4A8 (int4 per-group-128 weights), {wl4.n_layers} rotated layers; tokens/s per layer step",
            "mean_context": round(res["mean_context"], 1),
-           "graph_replay": graph_line(res)}
+           "graph_replay": graph_line(res),
+           "attention_form_us": res["attention_form_us"]}
     if "roofline" in res:
         out["roofline"] = res["roofline"]
         out["attn_kernel_us"] = round(res["attn_kernel_us"], 2)

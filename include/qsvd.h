@@ -196,6 +196,24 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
                                          float sm_scale, void* out,
                                          void* ws, size_t ws_bytes, void* stream);
 
+/* The same attention for layers that apply a rotary position embedding to q
+ * and k (the paper's layers have none; this is the position-encoded variant
+ * of Section 3.1's decode step).  Every rebuilt key row at position t and the
+ * query at position seq_len[b] - 1 are rotated before the product: each head
+ * vector's pairs (j, j + head_dim/2), j < head_dim/2, are turned by the angle
+ * t * rope_theta^(-2j/head_dim), formed and reduced modulo 2 pi in fp64 and
+ * evaluated in fp32.  Values are not rotated.  Because a key then depends on
+ * its position, it cannot be folded into the query: only the reconstruct form
+ * runs (mode QSVD_ATTN_AUTO or QSVD_ATTN_RECONSTRUCT; QSVD_ATTN_ABSORBED
+ * returns QSVD_ERR_UNSUPPORTED), with its requirements above (q_len 1,
+ * n_q_heads <= 32, capacity <= 16384, F16 or I8 cache) and a workspace of
+ * qsvd_decode_workspace_size(w, c, 1, QSVD_ATTN_RECONSTRUCT) bytes.
+ * rope_theta must be finite and > 1 (QSVD_ERR_INVALID_ARG otherwise). */
+qsvd_status qsvd_latent_decode_attention_rope(const qsvd_layer* w, const qsvd_cache* c,
+                                              const void* q, int32_t q_len, int32_t mode,
+                                              float sm_scale, float rope_theta, void* out,
+                                              void* ws, size_t ws_bytes, void* stream);
+
 size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int32_t q_len,
                                   int32_t mode);
 

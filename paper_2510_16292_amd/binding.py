@@ -19,7 +19,8 @@ QSVD_OUT_Q, QSVD_OUT_K, QSVD_OUT_V = 1, 2, 4
 
 EXPORTED = [
     "qsvd_quantize_act", "qsvd_quantize_act_rotated", "qsvd_lowrank_qkv_prefill", "qsvd_prefill_workspace_size",
-    "qsvd_latent_cache_append", "qsvd_latent_decode_attention", "qsvd_decode_workspace_size",
+    "qsvd_latent_cache_append", "qsvd_latent_decode_attention", "qsvd_latent_decode_attention_rope",
+    "qsvd_decode_workspace_size",
     "qsvd_status_string", "qsvd_last_error", "qsvd_profile_enable", "qsvd_profile_reset",
     "qsvd_profile_read",
 ]
@@ -68,6 +69,7 @@ def lib():
             "qsvd_prefill_workspace_size": (SZ, [LP, I64, U32]),
             "qsvd_latent_cache_append": (I32, [CP, P, P, P, I32, P]),
             "qsvd_latent_decode_attention": (I32, [LP, CP, P, I32, I32, F, P, P, SZ, P]),
+            "qsvd_latent_decode_attention_rope": (I32, [LP, CP, P, I32, I32, F, F, P, P, SZ, P]),
             "qsvd_decode_workspace_size": (SZ, [LP, CP, I32, I32]),
             "qsvd_status_string": (ctypes.c_char_p, [I32]),
             "qsvd_last_error": (ctypes.c_char_p, []),
@@ -109,6 +111,12 @@ def qsvd_latent_cache_append(cache, c_h, cq, sc, n_new, stream):
 def qsvd_latent_decode_attention(layer, cache, q, q_len, mode, sm_scale, out, ws, ws_bytes, stream):
     return lib().qsvd_latent_decode_attention(ctypes.byref(layer), ctypes.byref(cache), q, q_len, mode,
                                               sm_scale, out, ws, ws_bytes, stream)
+
+
+def qsvd_latent_decode_attention_rope(layer, cache, q, q_len, mode, sm_scale, rope_theta, out, ws, ws_bytes,
+                                      stream):
+    return lib().qsvd_latent_decode_attention_rope(ctypes.byref(layer), ctypes.byref(cache), q, q_len, mode,
+                                                   sm_scale, rope_theta, out, ws, ws_bytes, stream)
 
 
 def qsvd_decode_workspace_size(layer, cache, q_len, mode):

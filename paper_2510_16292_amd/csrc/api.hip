@@ -304,9 +304,9 @@ size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int3
   return attn_absorbed_workspace(*w, *c, q_len);
 }
 
-qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* c, const void* q, int32_t q_len,
-                                         int32_t mode, float sm_scale, void* out, void* ws, size_t ws_bytes,
-                                         void* stream) {
+static qsvd_status decode_attention(const qsvd_layer* w, const qsvd_cache* c, const void* q, int32_t q_len,
+                                    int32_t mode, float sm_scale, float rope_theta, void* out, void* ws,
+                                    size_t ws_bytes, void* stream) {
   qsvd_status st = check_layer(w);
   if (st != QSVD_OK) return st;
   st = check_cache(c);
@@ -325,7 +325,10 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
   if (w->w_group % 64) return fail(QSVD_ERR_UNSUPPORTED, "decode attention needs w_group 0 or a multiple of 64");
   if (!aligned(q, 16) || !aligned(out, 16) || !aligned(w->s_b, 16))
     return fail(QSVD_ERR_UNSUPPORTED, "q, out and s_b must be 16-byte aligned");
-  const bool abs_ok = absorbed_supported(*w, *c);
+  const bool rope = rope_theta > 0.f;
+  if (rope && mode == QSVD_ATTN_ABSORBED)
+    return fail(QSVD_ERR_UNSUPPORTED, "rotary embeddings need the reconstruct form (K depends on the position)");
+  const bool abs_ok = !rope && absorbed_supported(*w, *c);
   if (mode == QSVD_ATTN_ABSORBED && !abs_ok)
     return fail(QSVD_ERR_UNSUPPORTED, "absorbed form needs r in {128, 512, 1024, 1536} or a multiple of 128 up to 3072");
   const bool absorbed = mode == QSVD_ATTN_ABSORBED || (mode == QSVD_ATTN_AUTO && abs_ok);
@@ -339,9 +342,22 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
   const size_t need = absorbed ? attn_absorbed_workspace(*w, *c, q_len) : attn_reconstruct_workspace(*w, *c);
   if (!ws || ws_bytes < need) return fail(QSVD_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   AttnArgs a{w, c, (const _Float16*)q, (_Float16*)out, sm_scale > 0.f ? sm_scale : 1.f / sqrtf((float)w->head_dim),
-             q_len};
+             q_len, rope ? rope_theta : 0.f};
   hipStream_t s = (hipStream_t)stream;
   return hip_status(absorbed ? launch_attn_absorbed(a, ws, s) : launch_attn_reconstruct(a, ws, s), "decode attention");
+}
+
+qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* c, const void* q, int32_t q_len,
+                                         int32_t mode, float sm_scale, void* out, void* ws, size_t ws_bytes,
+                                         void* stream) {
+  return decode_attention(w, c, q, q_len, mode, sm_scale, 0.f, out, ws, ws_bytes, stream);
+}
+
+qsvd_status qsvd_latent_decode_attention_rope(const qsvd_layer* w, const qsvd_cache* c, const void* q, int32_t q_len,
+                                              int32_t mode, float sm_scale, float rope_theta, void* out, void* ws,
+                                              size_t ws_bytes, void* stream) {
+  if (!(rope_theta > 1.f) || isinf(rope_theta)) return fail(QSVD_ERR_INVALID_ARG, "rope_theta must be finite and > 1");
+  return decode_attention(w, c, q, q_len, mode, sm_scale, rope_theta, out, ws, ws_bytes, stream);
 }
 
 qsvd_status qsvd_profile_enable(int32_t on, const char* filter) {

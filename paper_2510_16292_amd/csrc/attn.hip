@@ -16,6 +16,7 @@
 // with an fp16 matrix-core GEMM and a plain split-context attention follows.
 #include <math.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -1204,6 +1205,38 @@ recon_kv_kernel(const uint8_t* __restrict__ cdata, const float* __restrict__ csc
     }
 }
 
+// Rotary embedding (rotate-half pairs (j, j + dh/2), angle pos * theta^(-2j/dh)):
+// the angle is formed and reduced modulo 2 pi in fp64, then turned into
+// cos / sin in fp32, so that large positions keep their accuracy.
+__device__ __forceinline__ void rope_cs(int pos, int j, int dh, double log2_theta, float* c, float* s) {
+  const double inv = exp2(-2.0 * (double)j / (double)dh * log2_theta);
+  double ang = (double)pos * inv;
+  const double two_pi = 6.283185307179586476925286766559;
+  ang -= floor(ang / two_pi) * two_pi;
+  sincosf((float)ang, s, c);
+}
+
+// In place on the rebuilt keys kv[b][t][0 .. Hkv*dh) (row stride nkv2) of the
+// visible positions: every (token, head, pair) turned by its angle.
+__global__ void __launch_bounds__(256)
+rope_keys_kernel(_Float16* __restrict__ kv, const int32_t* __restrict__ seq_len, int32_t capacity, int32_t Hkv,
+                 int32_t dh, int32_t nkv2, double log2_theta) {
+  const int b = blockIdx.y, half = dh >> 1;
+  const int L = min(seq_len[b], capacity);
+  const int64_t per_tok = (int64_t)Hkv * half;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < (int64_t)L * per_tok;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int t = (int)(e / per_tok);
+    const int rem = (int)(e - (int64_t)t * per_tok), g = rem / half, j = rem - g * half;
+    float c, s;
+    rope_cs(t, j, dh, log2_theta, &c, &s);
+    _Float16* row = kv + ((int64_t)b * capacity + t) * nkv2 + g * dh;
+    const float a = (float)row[j], bb = (float)row[j + half];
+    row[j] = to_f16(add_rn(mul_rn(a, c), -mul_rn(bb, s)));
+    row[j + half] = to_f16(add_rn(mul_rn(bb, c), mul_rn(a, s)));
+  }
+}
+
 // Plain split-context attention over rebuilt K^, V^: one workgroup per
 // (context chunk of 64 tokens, sequence), all query heads.
 constexpr int RCH = 64;
@@ -1211,7 +1244,7 @@ constexpr int RCH = 64;
 __global__ void __launch_bounds__(256)
 recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ kv,
                   const int32_t* __restrict__ seq_len, int32_t capacity, int32_t Hq, int32_t Hkv,
-                  int32_t dh, float scale, int32_t n_chunks, _Float16* __restrict__ o_part,
+                  int32_t dh, float scale, int32_t n_chunks, double log2_theta, _Float16* __restrict__ o_part,
                   float* __restrict__ ml_part) {
   __shared__ float qs[32 * 128];
   __shared__ float ss[32 * RCH];
@@ -1222,7 +1255,21 @@ recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k
   if (t0 >= L) return;
   const int tn = min(RCH, L - t0);
   const int nkv = Hkv * dh, nkv2 = 2 * nkv;
-  for (int e = tid; e < Hq * dh; e += 256) qs[e] = (float)q[(int64_t)b * Hq * dh + e] * scale;
+  if (log2_theta > 0.0) {
+    // rotary embedding of the query at its position L - 1
+    const int half = dh >> 1;
+    for (int e = tid; e < Hq * dh; e += 256) {
+      const int h = e / dh, cc = e - h * dh, j = cc < half ? cc : cc - half;
+      const float a = (float)q[(int64_t)b * Hq * dh + h * dh + j];
+      const float bb = (float)q[(int64_t)b * Hq * dh + h * dh + j + half];
+      float c, s;
+      rope_cs(L - 1, j, dh, log2_theta, &c, &s);
+      const float y = cc < half ? add_rn(mul_rn(a, c), -mul_rn(bb, s)) : add_rn(mul_rn(bb, c), mul_rn(a, s));
+      qs[e] = y * scale;
+    }
+  } else {
+    for (int e = tid; e < Hq * dh; e += 256) qs[e] = (float)q[(int64_t)b * Hq * dh + e] * scale;
+  }
   __syncthreads();
   for (int e = tid; e < Hq * RCH; e += 256) {
     const int h = e / RCH, tl = e - h * RCH;
@@ -1301,26 +1348,48 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
   const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
   const int nq = w.n_q_heads * w.head_dim, nkv2 = 2 * w.n_kv_heads * w.head_dim;
   const int len = c.max_len > 0 ? c.max_len : 1;
-  {
+  hipError_t e;
+  if (c.fmt == QSVD_CACHE_F16) {
     dim3 grid((nkv2 + RBN - 1) / RBN, (len + RBM - 1) / RBM, c.batch);
     KernelScope ks("recon_kv", s);
-    if (c.fmt == QSVD_CACHE_F16)
-      QSVD_LAUNCH(ks, recon_kv_kernel<QSVD_CACHE_F16>, grid, dim3(256), 0, s, (const uint8_t*)c.data,
-                         c.scale, c.seq_len, c.capacity, c.r, (const uint8_t*)w.b_t, w.s_b, N, nq, nkv2,
-                         w.w_bits, w.w_group, kv);
-    else
-      QSVD_LAUNCH(ks, recon_kv_kernel<QSVD_CACHE_I8>, grid, dim3(256), 0, s, (const uint8_t*)c.data,
-                         c.scale, c.seq_len, c.capacity, c.r, (const uint8_t*)w.b_t, w.s_b, N, nq, nkv2,
-                         w.w_bits, w.w_group, kv);
+    QSVD_LAUNCH(ks, recon_kv_kernel<QSVD_CACHE_F16>, grid, dim3(256), 0, s, (const uint8_t*)c.data,
+                       c.scale, c.seq_len, c.capacity, c.r, (const uint8_t*)w.b_t, w.s_b, N, nq, nkv2,
+                       w.w_bits, w.w_group, kv);
+    e = hipGetLastError();
+  } else {
+    // int8 latent rows times the K / V weight codes on the int8 matrix cores:
+    // every cache row (capacity rows per sequence; rows past seq_len are
+    // computed and never read), dequantized (acc * s_t) * s_n, fp16
+    GemmArgs g{};
+    g.a = (const int8_t*)c.data;
+    g.b = (const int8_t*)w.b_t + (int64_t)nq * (w.w_bits == 8 ? w.r : w.r / 2);
+    g.row_scale = c.scale;
+    g.col_scale = w.s_b + nq;
+    g.M = (int64_t)c.batch * c.capacity;
+    g.N = nkv2;
+    g.K = w.r;
+    g.seg[0] = OutSeg{kv, nkv2, 0, nkv2};
+    g.n_seg = 1;
+    g.abits = 8;
+    e = (w.w_bits == 8 && !w.w_group) ? launch_gemm_i8(g, s) : launch_gemm_q4(g, 8, w.w_bits, w.w_group, N, s);
   }
-  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const double log2_theta = a.rope_theta > 0.f ? log2((double)a.rope_theta) : 0.0;
+  if (a.rope_theta > 0.f) {
+    KernelScope ks("rope_keys", s);
+    const int64_t work = (int64_t)len * w.n_kv_heads * (w.head_dim / 2);
+    const unsigned gx = (unsigned)std::min<int64_t>((work + 255) / 256, 4096);
+    QSVD_LAUNCH(ks, rope_keys_kernel, dim3(gx, c.batch), dim3(256), 0, s, kv, c.seq_len, c.capacity,
+                w.n_kv_heads, w.head_dim, nkv2, log2_theta);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const int nch = (len + RCH - 1) / RCH;
   {
     KernelScope ks("recon_attn", s);
     QSVD_LAUNCH(ks, recon_attn_kernel, dim3(nch, c.batch), dim3(256), 0, s, a.q, kv, c.seq_len,
                        c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, a.sm_scale * kLog2e,
-                       p.n_chunks, opart, ml);
+                       p.n_chunks, log2_theta, opart, ml);
   }
   {
     KernelScope ks("recon_combine", s);

@@ -86,6 +86,7 @@ struct AttnArgs {
   _Float16* out;          // same layout
   float sm_scale;
   int32_t q_len;          // queries per sequence: the last q_len cached positions, causal among them
+  float rope_theta;       // > 0: rotary embedding of q and the rebuilt K (reconstruct form only)
 };
 size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len);
 // Rows of the absorbed attention grid: (sequence, query) rows times head blocks.

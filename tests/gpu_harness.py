@@ -110,14 +110,20 @@ class Prefill:
         return out
 
 
-def decode_attention(dl, dc, q_dev, mode, sm_scale=0.0, q_len=1):
-    """q_dev: [batch, q_len, Hq*head_dim] (or [batch, Hq*head_dim] for q_len 1)."""
+def decode_attention(dl, dc, q_dev, mode, sm_scale=0.0, q_len=1, rope_theta=None):
+    """q_dev: [batch, q_len, Hq*head_dim] (or [batch, Hq*head_dim] for q_len 1).
+    With rope_theta, the rotary variant (reconstruct form only)."""
     t = torch()
     out = t.empty_like(q_dev)
-    ws_bytes = B.qsvd_decode_workspace_size(dl.c, dc.c, q_len, mode)
+    ws_mode = B.QSVD_ATTN_RECONSTRUCT if rope_theta else mode
+    ws_bytes = B.qsvd_decode_workspace_size(dl.c, dc.c, q_len, ws_mode)
     ws = t.empty((max(ws_bytes, 1),), dtype=t.uint8, device="cuda")
-    B.check(B.qsvd_latent_decode_attention(dl.c, dc.c, B.ptr(q_dev), q_len, mode, sm_scale, B.ptr(out), B.ptr(ws),
-                                           ws_bytes, B.stream_handle()))
+    if rope_theta:
+        B.check(B.qsvd_latent_decode_attention_rope(dl.c, dc.c, B.ptr(q_dev), q_len, mode, sm_scale, rope_theta,
+                                                    B.ptr(out), B.ptr(ws), ws_bytes, B.stream_handle()))
+    else:
+        B.check(B.qsvd_latent_decode_attention(dl.c, dc.c, B.ptr(q_dev), q_len, mode, sm_scale, B.ptr(out),
+                                               B.ptr(ws), ws_bytes, B.stream_handle()))
     return out
 
 

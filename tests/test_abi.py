@@ -224,6 +224,27 @@ def test_decode_validation(lib):
     assert _decode(L, C, q_len=2, mode=B.QSVD_ATTN_ABSORBED, ws_bytes=need2 - 1) == B.QSVD_ERR_WORKSPACE
 
 
+def _decode_rope(layer, cache, theta=10000.0, q_len=1, mode=0, ws_bytes=1 << 40):
+    return B.qsvd_latent_decode_attention_rope(layer, cache, FAKE, q_len, mode, 0.0, theta, FAKE, FAKE, ws_bytes, 0)
+
+
+def test_decode_rope_validation(lib):
+    """Every case fails before a launch: the rotary variant takes only the
+    reconstruct form and a base above 1."""
+    L, C = layer_struct(), cache_struct()
+    for theta in (0.0, -5.0, 1.0, float("inf"), float("nan")):
+        assert _decode_rope(L, C, theta=theta) == B.QSVD_ERR_INVALID_ARG
+    assert _decode_rope(L, C, mode=B.QSVD_ATTN_ABSORBED) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode_rope(L, C, q_len=2) == B.QSVD_ERR_UNSUPPORTED            # AUTO falls to reconstruct: q_len 1
+    assert _decode_rope(layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64), C) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode_rope(L, cache_struct(fmt=B.QSVD_CACHE_I4, scale=FAKE)) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode_rope(L, cache_struct(capacity=20000)) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode_rope(L, C, mode=3) == B.QSVD_ERR_INVALID_ARG
+    need = B.qsvd_decode_workspace_size(L, C, 1, B.QSVD_ATTN_RECONSTRUCT)
+    assert _decode_rope(L, C, ws_bytes=need - 1) == B.QSVD_ERR_WORKSPACE
+    assert _decode_rope(L, C, mode=B.QSVD_ATTN_RECONSTRUCT, ws_bytes=need - 1) == B.QSVD_ERR_WORKSPACE
+
+
 def test_decode_workspace_sizes_cover_growth(lib):
     """The absorbed workspace depends on batch and rank, not on the current
     length, so one allocation serves every decode step up to capacity."""

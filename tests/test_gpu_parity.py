@@ -891,3 +891,118 @@ def test_decode_gqa_int4_cache_ragged(gqa):
         assert ok, (t, info)
     assert np.array_equal(H.host(dc.data), oc.data)
     assert np.array_equal(H.host(dc.scale).view(np.uint32), oc.scale.view(np.uint32))
+
+
+# ------------------------------------------------------------------ rotary position embedding (reconstruct form)
+
+def test_decode_rope_tiny_end_to_end(tiny):
+    """Tiny layer with rotary embeddings: 64 prefill tokens into an fp16 latent
+    cache, then 8 decode steps of projection, append and rotary attention (the
+    rebuilt K rows and the query turned at their positions), each against the
+    oracle's plain definition with the same base."""
+    wl, ol, dl = tiny
+    theta = 10000.0
+    X = gen.prefill_activations(wl)
+    oc = O.LatentCache(O.CACHE_F16, 1, 64 + 8, wl.layer.r)
+    O.cache_append_prefill(oc, O.prefill(ol, X, 8), [64])
+    dc = B.DeviceCache(B.QSVD_CACHE_F16, 1, 64 + 8, wl.layer.r, [0])
+    pre = H.Prefill(dl, 64, mask=0, debug=False).run(H.dev(X))
+    H.append(dc, pre.c_h, n_new=64)
+    for t in range(8):
+        xt = gen.decode_activations(wl, t)
+        proj = O.decode_step(ol, oc, xt, 8)
+        ref = O.attention_reference(ol, oc, proj["Q"][:, None, :], 1, rope_theta=theta)[:, 0, :]
+        H.say(f"decode rope tiny step={t}")
+        p = H.Prefill(dl, 1, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
+        H.append(dc, p.c_h, n_new=1)
+        out = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO, rope_theta=theta))
+        ok, info = H.close_enough(out, ref)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (t, info)
+        # the rotation changed the result: it is not the unrotated attention
+        assert not H.close_enough(out, proj["out"], max_abs=1e-3, rel_l2=1e-3)[0]
+
+
+@pytest.mark.parametrize("theta", [1.0e4, 1.0e6], ids=["base1e4", "base1e6"])
+def test_decode_rope_gqa_int8_ragged(gqa, theta):
+    """Grouped queries (8 over 2) over an int8 latent cache with ragged lengths
+    1 / 45 / 130, 3 decode steps of rotary attention (the int8 rows rebuilt on
+    the int8 matrix cores, then rotated)."""
+    L, ol, dl = gqa
+    lengths = [1, 45, 130]
+    batch, cap = 3, 140
+    wl = configs.Workload(95, "gqa-test", L, "gaussian", 8, 0, 8, configs.CACHE_I8)
+    codes, scales = gen.latent_codes(wl, batch, cap)
+    oc = O.LatentCache(O.CACHE_I8, batch, cap, L.r)
+    dc = B.DeviceCache(B.QSVD_CACHE_I8, batch, cap, L.r, lengths)
+    for b, n in enumerate(lengths):
+        oc.append(b, None, codes[b, :n], scales[b, :n])
+    dc.data.copy_(H.dev(np.where(np.arange(cap)[None, :, None] < np.array(lengths)[:, None, None], codes, 0)))
+    dc.scale.copy_(H.dev(np.where(np.arange(cap)[None, :] < np.array(lengths)[:, None], scales, 0)))
+    for t in range(3):
+        xt = gen.decode_activations(wl, t, batch=batch)
+        proj = O.decode_step(ol, oc, xt, 8)
+        ref = O.attention_reference(ol, oc, proj["Q"][:, None, :], 1, rope_theta=theta)[:, 0, :]
+        H.say(f"decode rope gqa int8 step={t} theta={theta}")
+        p = H.Prefill(dl, batch, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
+        H.append(dc, cq=p.cq, sc=p.sc, n_new=1)
+        out = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_RECONSTRUCT, rope_theta=theta))
+        ok, info = H.close_enough(out, ref)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (t, info)
+
+
+def test_decode_reconstruct_and_rope_qwen_w4_int8_cache(qwen):
+    """Qwen2-VL-7B-shaped layer (28 over 4 heads, r=1024, int4 weights in groups
+    of 128) over an int8 latent cache with ragged lengths 7 / 300 / 1029: the
+    rows rebuilt by the int4-weight product, attended without and with rotary
+    embeddings (base 1e6)."""
+    wl, ol, dl = qwen
+    L = wl.layer
+    lengths = [7, 300, 1029]
+    batch, cap = 3, 1040
+    codes, scales = gen.latent_codes(wl, batch, cap)
+    oc = O.LatentCache(O.CACHE_I8, batch, cap, L.r)
+    for b, n in enumerate(lengths):
+        oc.append(b, None, codes[b, :n], scales[b, :n])
+    dc = B.DeviceCache(B.QSVD_CACHE_I8, batch, cap, L.r, lengths)
+    dc.data.copy_(H.dev(codes))
+    dc.scale.copy_(H.dev(scales))
+    g = np.random.default_rng(2024)
+    q = (g.standard_normal((batch, L.n_q_heads * L.head_dim)) * 2.0).astype(np.float16)
+    q_dev = H.dev(q)
+    for theta in (None, 1.0e6):
+        H.say(f"decode qwen int8 cache reconstruct theta={theta}")
+        ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, rope_theta=theta)[:, 0, :]
+        out = H.host(H.decode_attention(dl, dc, q_dev, B.QSVD_ATTN_RECONSTRUCT, rope_theta=theta))
+        ok, info = H.close_enough(out, ref)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (theta, info)
+
+
+def test_decode_rope_long_positions(gqa):
+    """Positions up to the reconstruct form's largest capacity (16384): one
+    sequence filled to capacity and one to 9001 tokens of an int8 cache, a
+    random query at the last position; the angles reach 16383 rad and are
+    reduced in fp64 before the fp32 sine and cosine."""
+    L, ol, dl = gqa
+    lengths = [16384, 9001]
+    batch, cap = 2, 16384
+    wl = configs.Workload(95, "gqa-test", L, "gaussian", 8, 0, 8, configs.CACHE_I8)
+    codes, scales = gen.latent_codes(wl, batch, cap)
+    oc = O.LatentCache(O.CACHE_I8, batch, cap, L.r)
+    for b, n in enumerate(lengths):
+        oc.append(b, None, codes[b, :n], scales[b, :n])
+    dc = B.DeviceCache(B.QSVD_CACHE_I8, batch, cap, L.r, lengths)
+    dc.data.copy_(H.dev(codes))
+    dc.scale.copy_(H.dev(scales))
+    g = np.random.default_rng(16384)
+    # queries large enough for a peaked softmax, so that a wrong angle moves the output
+    q = (g.standard_normal((batch, L.n_q_heads * L.head_dim)) * 20.0).astype(np.float16)
+    for theta in (1.0e4, 5.0e5):
+        H.say(f"decode rope long positions theta={theta}")
+        ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, rope_theta=theta)[:, 0, :]
+        out = H.host(H.decode_attention(dl, dc, H.dev(q), B.QSVD_ATTN_AUTO, rope_theta=theta))
+        ok, info = H.close_enough(out, ref)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (theta, info)
