@@ -69,19 +69,6 @@ __device__ inline f16x8 cvt_i4x8(uint32_t w) {
 }
 
 // ---------------------------------------------------------------------------
-// Weight code access (int8 or packed int4), transposed layout [N][r].
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ float wcode(const uint8_t* bt, int32_t r, int32_t n, int32_t j, int bits) {
-  if (bits == 8) return (float)((const int8_t*)bt)[(int64_t)n * r + j];
-  const uint32_t byte = bt[(int64_t)n * (r / 2) + (j >> 1)];
-  return (float)((j & 1) ? nib_hi(byte) : nib_lo(byte));
-}
-
-__device__ __forceinline__ float wscale(const float* sb, int32_t N, int32_t n, int32_t j, int group) {
-  return group ? sb[(int64_t)(j / group) * N + n] : sb[n];
-}
-
-// ---------------------------------------------------------------------------
 // q~ = scale * q W^u_k^T on the 16x16x32 fp16 matrix cores.  One wave per
 // (head h, 64 latent columns j): the dh x 64 block of W^u_k codes (rows
 // c = key channel, contiguous in j) is staged in LDS as exact fp16 codes, and
@@ -1104,219 +1091,229 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// Reconstruct form.
-// recon_kv_kernel: KV^[b][t][n'] = C^[b][t][:] . W^u[:, Hq*dh + n'] for n' < 2*Hkv*dh,
-// an fp16 MFMA GEMM (128 x 128 tiles, K in steps of 32) whose loaders turn the
-// stored latent (fp16 or int8 codes) and the weight codes into exact fp16
-// operands; per-channel weight scales and int8 token scales are applied to the
-// fp32 accumulator (per-group scales, which vary along the contraction, are
-// folded into the fp16 weight operand).
+// Reconstruct form: K^, V^ = C W^u_{k,v} rebuilt for every cached token
+// (Eq. 5), then plain attention over them.
+//
+// The rebuild is one matrix-core product over all cache rows: int8 caches on
+// the int8 products (exact integer sums, (acc * s_t) * s_n); fp16 caches on the
+// fp16 products, with the weight columns first turned into fp16 in the
+// workspace (the exact codes, per-channel scales in the epilogue; for per-group
+// scales code * s_g rounded once to fp16, since a scale that varies along the
+// contraction cannot leave the product).
 // ---------------------------------------------------------------------------
-constexpr int RBM = 128, RBN = 128, RBK = 32, RLD = RBK + 8;
-
-template <int FMT>
 __global__ void __launch_bounds__(256)
-recon_kv_kernel(const uint8_t* __restrict__ cdata, const float* __restrict__ cscale,
-                const int32_t* __restrict__ seq_len, int32_t capacity, int32_t r,
-                const uint8_t* __restrict__ bt, const float* __restrict__ sb, int32_t N, int32_t nq,
-                int32_t nkv2, int32_t bits, int32_t group, _Float16* __restrict__ kv) {
-  __shared__ __attribute__((aligned(16))) _Float16 As[RBM * RLD];
-  __shared__ __attribute__((aligned(16))) _Float16 Bs[RBN * RLD];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 1, wn = w & 1, half = lane >> 5, l32 = lane & 31;
-  const int b = blockIdx.z;
-  const int L = min(seq_len[b], capacity);
-  const int t0 = blockIdx.y * RBM, n0 = blockIdx.x * RBN;
-  if (t0 >= L) return;
-  f32x16 acc[2][2];
+recon_weights_kernel(const uint8_t* __restrict__ bt, const float* __restrict__ sb, int32_t r, int32_t N, int32_t nq,
+                     int32_t nkv2, int32_t bits, int32_t group, _Float16* __restrict__ w16) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // one 8-element run of a column
+  const int per_col = r / 8;
+  if (e >= (int64_t)nkv2 * per_col) return;
+  const int np = (int)(e / per_col), k0 = 8 * (int)(e - (int64_t)np * per_col);
+  const int n = nq + np;
+  float v[8];
+  if (bits == 8) {
+    const int8_t* src = reinterpret_cast<const int8_t*>(bt) + (int64_t)n * r + k0;
+    const uint2 u = *reinterpret_cast<const uint2*>(src);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-  for (int k0 = 0; k0 < r; k0 += RBK) {
-    // A: 128 tokens x 32 latent values, thread -> (row tid/2, 16 values at 16*(tid%2))
-    {
-      const int row = tid >> 1, col = (tid & 1) * 16, t = t0 + row;
-      _Float16 vals[16];
-      if (t < L) {
-        if (FMT == QSVD_CACHE_F16) {
-          const _Float16* src = reinterpret_cast<const _Float16*>(cdata) + ((int64_t)b * capacity + t) * r + k0 + col;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) vals[e] = src[e];
-        } else {
-          const int8_t* src = reinterpret_cast<const int8_t*>(cdata) + ((int64_t)b * capacity + t) * r + k0 + col;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) vals[e] = (_Float16)(float)src[e];
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) vals[e] = (_Float16)0.f;
-      }
-#pragma unroll
-      for (int e = 0; e < 16; ++e) As[row * RLD + col + e] = vals[e];
+    for (int i = 0; i < 4; ++i) {
+      v[i] = (float)(int8_t)(u.x >> (8 * i));
+      v[4 + i] = (float)(int8_t)(u.y >> (8 * i));
     }
-    // B: 128 output columns x 32 latent values of dequantized W^u
-    {
-      const int row = tid >> 1, col = (tid & 1) * 16, nn = n0 + row;
+  } else {
+    const uint32_t u = *reinterpret_cast<const uint32_t*>(bt + (int64_t)n * (r / 2) + k0 / 2);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float v = 0.f;
-        if (nn < nkv2) {
-          const int32_t n = nq + nn, j = k0 + col + e;
-          v = wcode(bt, r, n, j, bits);
-          if (group) v *= sb[(int64_t)(j / group) * N + n];
-        }
-        Bs[row * RLD + col + e] = (_Float16)v;
-      }
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t byte = (u >> (8 * i)) & 0xFFu;
+      v[2 * i] = (float)nib_lo(byte);
+      v[2 * i + 1] = (float)nib_hi(byte);
     }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < RBK; kk += 16) {
-      f16x8 af[2], bf[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const f16x8*>(&As[(wm * 64 + i * 32 + l32) * RLD + kk + 8 * half]);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bf[j] = *reinterpret_cast<const f16x8*>(&Bs[(wn * 64 + j * 32 + l32) * RLD + kk + 8 * half]);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
-    }
-    __syncthreads();
   }
+  if (group) {
+    const float sg = sb[(int64_t)(k0 / group) * N + n];   // a run never crosses a group (group % 64 == 0)
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 8; ++i) v[i] = mul_rn(v[i], sg);
+  }
+  f16x8 o;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int nn = n0 + wn * 64 + j * 32 + l32;
-      if (nn >= nkv2) continue;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int t = t0 + wm * 64 + i * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-        if (t >= L) continue;
-        float y = acc[i][j][v];
-        if (!group) y *= sb[nq + nn];
-        if (FMT != QSVD_CACHE_F16) y *= cscale[(int64_t)b * capacity + t];
-        kv[((int64_t)b * capacity + t) * nkv2 + nn] = to_f16(y);
-      }
-    }
+  for (int i = 0; i < 8; ++i) o[i] = to_f16(v[i]);
+  *reinterpret_cast<f16x8*>(w16 + (int64_t)np * r + k0) = o;
 }
 
-// Rotary embedding (rotate-half pairs (j, j + dh/2), angle pos * theta^(-2j/dh)):
-// the angle is formed and reduced modulo 2 pi in fp64, then turned into
-// cos / sin in fp32, so that large positions keep their accuracy.
-__device__ __forceinline__ void rope_cs(int pos, int j, int dh, double log2_theta, float* c, float* s) {
-  const double inv = exp2(-2.0 * (double)j / (double)dh * log2_theta);
-  double ang = (double)pos * inv;
+// Rotary embedding angle of pair j at position pos, reduced modulo 2 pi in
+// fp64 (inv = theta^(-2j/dh) from the per-workgroup table), then cos / sin in
+// fp32, so that large positions keep their accuracy.
+__device__ __forceinline__ void rope_cs(int pos, double inv, float* c, float* s) {
   const double two_pi = 6.283185307179586476925286766559;
-  ang -= floor(ang / two_pi) * two_pi;
+  double ang = (double)pos * inv;
+  ang -= floor(ang * (1.0 / two_pi)) * two_pi;
   sincosf((float)ang, s, c);
 }
 
-// In place on the rebuilt keys kv[b][t][0 .. Hkv*dh) (row stride nkv2) of the
-// visible positions: every (token, head, pair) turned by its angle.
-__global__ void __launch_bounds__(256)
-rope_keys_kernel(_Float16* __restrict__ kv, const int32_t* __restrict__ seq_len, int32_t capacity, int32_t Hkv,
-                 int32_t dh, int32_t nkv2, double log2_theta) {
-  const int b = blockIdx.y, half = dh >> 1;
-  const int L = min(seq_len[b], capacity);
-  const int64_t per_tok = (int64_t)Hkv * half;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < (int64_t)L * per_tok;
-       e += (int64_t)gridDim.x * blockDim.x) {
-    const int t = (int)(e / per_tok);
-    const int rem = (int)(e - (int64_t)t * per_tok), g = rem / half, j = rem - g * half;
-    float c, s;
-    rope_cs(t, j, dh, log2_theta, &c, &s);
-    _Float16* row = kv + ((int64_t)b * capacity + t) * nkv2 + g * dh;
-    const float a = (float)row[j], bb = (float)row[j + half];
-    row[j] = to_f16(add_rn(mul_rn(a, c), -mul_rn(bb, s)));
-    row[j + half] = to_f16(add_rn(mul_rn(bb, c), mul_rn(a, s)));
-  }
+__device__ __forceinline__ void rope_pair(float a, float b, float c, float s, float* ra, float* rb) {
+  *ra = add_rn(mul_rn(a, c), -mul_rn(b, s));
+  *rb = add_rn(mul_rn(b, c), mul_rn(a, s));
 }
 
-// Plain split-context attention over rebuilt K^, V^: one workgroup per
-// (context chunk of 64 tokens, sequence), all query heads.
+// Split-context attention over the rebuilt rows kv[b][t][0 .. 2 Hkv dh)
+// (K^ then V^): one workgroup per (chunk of RCH tokens, sequence, key/value
+// head g) serves the G = Hq / Hkv query heads of g.  The chunk's K^ and V^
+// rows are staged in LDS with 16-byte loads (with rotary embeddings, each K^
+// pair (j, j + dh/2) is turned as it is staged, and the queries at position
+// seq_len - 1); scores, the softmax (one wave per head, a lane per token) and
+// P V^ read LDS.  Partials go out in the merge's layout: O/l as fp16
+// [chunk][x][32 heads], (m, l) per head.
 constexpr int RCH = 64;
+
+__host__ __device__ constexpr int recon_kld(int dh) { return dh + 8; }   // staged row stride (halves)
+
+static size_t recon_attn_lds(int dh, int G) {
+  return 64 * sizeof(double) + 2 * (size_t)RCH * recon_kld(dh) * sizeof(_Float16) +
+         (size_t)G * dh * sizeof(float) + (size_t)G * RCH * sizeof(float) + 2 * (size_t)G * sizeof(float);
+}
 
 __global__ void __launch_bounds__(256)
 recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ kv,
                   const int32_t* __restrict__ seq_len, int32_t capacity, int32_t Hq, int32_t Hkv,
                   int32_t dh, float scale, int32_t n_chunks, double log2_theta, _Float16* __restrict__ o_part,
                   float* __restrict__ ml_part) {
-  __shared__ float qs[32 * 128];
-  __shared__ float ss[32 * RCH];
-  __shared__ float ml[64];
-  const int b = blockIdx.y, ch = blockIdx.x, tid = threadIdx.x;
+  extern __shared__ __attribute__((aligned(16))) uint8_t recon_smem[];
+  const int b = blockIdx.y, ch = blockIdx.x, g = blockIdx.z, tid = threadIdx.x;
+  const int lane = tid & 63, wv = tid >> 6;
   const int L = min(seq_len[b], capacity);
   const int t0 = ch * RCH;
   if (t0 >= L) return;
   const int tn = min(RCH, L - t0);
+  const int G = Hq / Hkv, h0 = g * G, half = dh >> 1, kld = recon_kld(dh);
   const int nkv = Hkv * dh, nkv2 = 2 * nkv;
-  if (log2_theta > 0.0) {
-    // rotary embedding of the query at its position L - 1
-    const int half = dh >> 1;
-    for (int e = tid; e < Hq * dh; e += 256) {
-      const int h = e / dh, cc = e - h * dh, j = cc < half ? cc : cc - half;
-      const float a = (float)q[(int64_t)b * Hq * dh + h * dh + j];
-      const float bb = (float)q[(int64_t)b * Hq * dh + h * dh + j + half];
-      float c, s;
-      rope_cs(L - 1, j, dh, log2_theta, &c, &s);
-      const float y = cc < half ? add_rn(mul_rn(a, c), -mul_rn(bb, s)) : add_rn(mul_rn(bb, c), mul_rn(a, s));
-      qs[e] = y * scale;
+  const bool rope = log2_theta > 0.0;
+  double* inv = reinterpret_cast<double*>(recon_smem);                 // [dh/2]
+  _Float16* Ks = reinterpret_cast<_Float16*>(recon_smem + 64 * sizeof(double));
+  _Float16* Vs = Ks + RCH * kld;
+  float* qs = reinterpret_cast<float*>(Vs + RCH * kld);                // [G][dh], rotated and scaled
+  float* ps = qs + G * dh;                                             // [G][RCH] scores, then weights
+  float* red = ps + G * RCH;                                           // m[G], l[G]
+
+  if (rope) {
+    for (int j = tid; j < half; j += 256) inv[j] = exp2(-2.0 * (double)j / (double)dh * log2_theta);
+    __syncthreads();
+  }
+  const _Float16* qb = q + (int64_t)b * Hq * dh + (int64_t)h0 * dh;
+  for (int e = tid; e < G * dh; e += 256) {
+    const int hg = e / dh, c = e - hg * dh;
+    float y = (float)qb[e];
+    if (rope) {
+      const int j = c < half ? c : c - half;
+      float cs, sn, ra, rb;
+      rope_cs(L - 1, inv[j], &cs, &sn);
+      rope_pair((float)qb[hg * dh + j], (float)qb[hg * dh + j + half], cs, sn, &ra, &rb);
+      y = c < half ? ra : rb;
+    }
+    qs[e] = y * scale;
+  }
+  // stage K^ (rotated) and V^ rows of the chunk; rows past the sequence are zero
+  const _Float16* rows = kv + ((int64_t)b * capacity + t0) * nkv2 + (int64_t)g * dh;
+  const int cpr = dh / 8;                                              // 16-byte runs per head row
+  for (int e = tid; e < RCH * cpr; e += 256) {
+    const int tl = e / cpr, x = e - tl * cpr;
+    f16x8 v = f16x8{};
+    if (tl < tn) v = *reinterpret_cast<const f16x8*>(rows + (int64_t)tl * nkv2 + nkv + 8 * x);
+    *reinterpret_cast<f16x8*>(Vs + tl * kld + 8 * x) = v;
+  }
+  if (!rope) {
+    for (int e = tid; e < RCH * cpr; e += 256) {
+      const int tl = e / cpr, x = e - tl * cpr;
+      f16x8 v = f16x8{};
+      if (tl < tn) v = *reinterpret_cast<const f16x8*>(rows + (int64_t)tl * nkv2 + 8 * x);
+      *reinterpret_cast<f16x8*>(Ks + tl * kld + 8 * x) = v;
     }
   } else {
-    for (int e = tid; e < Hq * dh; e += 256) qs[e] = (float)q[(int64_t)b * Hq * dh + e] * scale;
+    const int cph = half / 8;                                          // runs per half row
+    for (int e = tid; e < RCH * cph; e += 256) {
+      const int tl = e / cph, x = e - tl * cph;
+      f16x8 lo = f16x8{}, hi = f16x8{};
+      if (tl < tn) {
+        lo = *reinterpret_cast<const f16x8*>(rows + (int64_t)tl * nkv2 + 8 * x);
+        hi = *reinterpret_cast<const f16x8*>(rows + (int64_t)tl * nkv2 + half + 8 * x);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          float cs, sn, ra, rb;
+          rope_cs(t0 + tl, inv[8 * x + i], &cs, &sn);
+          rope_pair((float)lo[i], (float)hi[i], cs, sn, &ra, &rb);
+          lo[i] = to_f16(ra);
+          hi[i] = to_f16(rb);
+        }
+      }
+      *reinterpret_cast<f16x8*>(Ks + tl * kld + 8 * x) = lo;
+      *reinterpret_cast<f16x8*>(Ks + tl * kld + half + 8 * x) = hi;
+    }
   }
   __syncthreads();
-  for (int e = tid; e < Hq * RCH; e += 256) {
-    const int h = e / RCH, tl = e - h * RCH;
+  // scores (log2 domain): item (head hg, token tl)
+  for (int e = tid; e < G * RCH; e += 256) {
+    const int hg = e / RCH, tl = e - hg * RCH;
     float acc = -INFINITY;
     if (tl < tn) {
-      const int g = (h * Hkv) / Hq;
-      const _Float16* krow = kv + ((int64_t)b * capacity + t0 + tl) * nkv2 + g * dh;
       acc = 0.f;
-      for (int c = 0; c < dh; ++c) acc = fmaf(qs[h * dh + c], (float)krow[c], acc);
+      const float* qh = qs + hg * dh;
+      for (int c = 0; c < dh; c += 8) {
+        const f16x8 k8 = *reinterpret_cast<const f16x8*>(Ks + tl * kld + c);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc = fmaf(qh[c + i], (float)k8[i], acc);
+      }
     }
-    ss[e] = acc;
+    ps[e] = acc;
   }
   __syncthreads();
-  if (tid < Hq) {
-    float m = -INFINITY;
-    for (int tl = 0; tl < tn; ++tl) m = fmaxf(m, ss[tid * RCH + tl]);
-    float l = 0.f;
-    for (int tl = 0; tl < RCH; ++tl) {
-      const float pv = (tl < tn) ? exp2f(ss[tid * RCH + tl] - m) : 0.f;
-      ss[tid * RCH + tl] = pv;
-      l += pv;
+  // softmax per head: one wave, a lane per token (RCH == 64)
+  for (int hg = wv; hg < G; hg += 4) {
+    const float sv = ps[hg * RCH + lane];
+    float m = sv;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    const float pv = lane < tn ? exp2f(sv - m) : 0.f;
+    float l = pv;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) l += __shfl_xor(l, o);
+    ps[hg * RCH + lane] = pv;
+    if (lane == 0) {
+      red[hg] = m;
+      red[G + hg] = l;
     }
-    ml[tid] = m;
-    ml[32 + tid] = l;
   }
   __syncthreads();
   const int64_t part = (int64_t)b * n_chunks + ch;
-  if (tid < 32) {
-    ml_part[part * 64 + tid] = tid < Hq ? ml[tid] : 0.f;
-    ml_part[part * 64 + 32 + tid] = tid < Hq ? ml[32 + tid] : 1.f;
+  for (int hg = tid; hg < G; hg += 256) {
+    ml_part[part * 64 + h0 + hg] = red[hg];
+    ml_part[part * 64 + 32 + h0 + hg] = red[G + hg];
   }
-  // O^T[c][h] / l = sum_t p[h][t] V^[t][g(h)*dh + c] / l[h], stored as fp16
-  for (int e = tid; e < dh * 32; e += 256) {
-    const int c = e >> 5, h = e & 31;
-    float acc = 0.f;
-    if (h < Hq) {
-      const int g = (h * Hkv) / Hq;
-      const _Float16* vcol = kv + ((int64_t)b * capacity + t0) * nkv2 + nkv + g * dh + c;
-      for (int tl = 0; tl < tn; ++tl) acc = fmaf(ss[h * RCH + tl], (float)vcol[(int64_t)tl * nkv2], acc);
-      acc /= ml[32 + h];
+  if (g == 0) {
+    // heads past Hq in the 32-wide partial rows: weight 0 in the merge
+    for (int h = Hq + tid; h < kHeadBlk; h += 256) {
+      ml_part[part * 64 + h] = 0.f;
+      ml_part[part * 64 + 32 + h] = 1.f;
     }
-    o_part[(part * dh + c) * kHeadBlk + h] = (_Float16)acc;
+    for (int e = tid; e < dh * (kHeadBlk - Hq); e += 256) {
+      const int c = e / (kHeadBlk - Hq), h = Hq + e - c * (kHeadBlk - Hq);
+      o_part[(part * dh + c) * kHeadBlk + h] = (_Float16)0.f;
+    }
+  }
+  // O^T[c][h] / l = sum_t p[h][t] V^[t][c] / l[h]: item (head hg, column pair c2)
+  for (int e = tid; e < G * half; e += 256) {
+    const int hg = e / half, c = 2 * (e - hg * half);
+    const float* ph = ps + hg * RCH;
+    float a0 = 0.f, a1 = 0.f;
+    for (int tl = 0; tl < tn; ++tl) {
+      const f16x2 v2 = *reinterpret_cast<const f16x2*>(Vs + tl * kld + c);
+      a0 = fmaf(ph[tl], (float)v2[0], a0);
+      a1 = fmaf(ph[tl], (float)v2[1], a1);
+    }
+    const float il = 1.f / red[G + hg];
+    o_part[(part * dh + c) * kHeadBlk + h0 + hg] = (_Float16)(a0 * il);
+    o_part[(part * dh + c + 1) * kHeadBlk + h0 + hg] = (_Float16)(a1 * il);
   }
 }
 
 struct ReconPlan {
-  size_t kv_bytes, opart_bytes, ml_bytes;
+  size_t kv_bytes, opart_bytes, ml_bytes, w16_bytes;
   int n_chunks;
 };
 
@@ -1327,12 +1324,52 @@ static ReconPlan plan_recon(const qsvd_layer& w, const qsvd_cache& c) {
   p.kv_bytes = (size_t)c.batch * c.capacity * nkv2 * sizeof(_Float16);
   p.opart_bytes = (size_t)c.batch * p.n_chunks * w.head_dim * kHeadBlk * sizeof(_Float16);
   p.ml_bytes = (size_t)c.batch * p.n_chunks * 64 * sizeof(float);
+  p.w16_bytes = c.fmt == QSVD_CACHE_F16 ? (size_t)nkv2 * w.r * sizeof(_Float16) : 0;
   return p;
 }
 
 size_t attn_reconstruct_workspace(const qsvd_layer& w, const qsvd_cache& c) {
   const ReconPlan p = plan_recon(w, c);
-  return align256(p.kv_bytes) + align256(p.opart_bytes) + align256(p.ml_bytes);
+  return align256(p.kv_bytes) + align256(p.opart_bytes) + align256(p.ml_bytes) + align256(p.w16_bytes);
+}
+
+// K^ | V^ rows of the cache into kv.  Rows past a sequence's length are
+// rebuilt too when that keeps one launch (at most a third of the rows wasted);
+// otherwise one launch per sequence over its first max_len rows.
+static hipError_t rebuild_kv(const AttnArgs& a, const _Float16* w16, _Float16* kv, hipStream_t s) {
+  const qsvd_layer& w = *a.w;
+  const qsvd_cache& c = *a.c;
+  const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
+  const int nq = w.n_q_heads * w.head_dim, nkv2 = 2 * w.n_kv_heads * w.head_dim;
+  const int len = c.max_len > 0 ? c.max_len : 1;
+  const bool f16 = c.fmt == QSVD_CACHE_F16;
+  const size_t row_bytes = f16 ? (size_t)c.r * 2 : (size_t)c.r;
+  const bool one = c.batch == 1 || 4 * (int64_t)len >= 3 * (int64_t)c.capacity;
+  const int launches = one ? 1 : c.batch;
+  for (int i = 0; i < launches; ++i) {
+    GemmArgs g{};
+    const int64_t r0 = one ? 0 : (int64_t)i * c.capacity;
+    g.a = reinterpret_cast<const int8_t*>(reinterpret_cast<const uint8_t*>(c.data) + r0 * row_bytes);
+    g.row_scale = f16 ? nullptr : c.scale + r0;
+    g.M = one ? (c.batch == 1 ? len : (int64_t)c.batch * c.capacity) : len;
+    g.N = nkv2;
+    g.K = w.r;
+    g.seg[0] = OutSeg{kv + r0 * nkv2, nkv2, 0, nkv2};
+    g.n_seg = 1;
+    g.abits = 8;
+    hipError_t e;
+    if (f16) {
+      g.b = reinterpret_cast<const int8_t*>(w16);
+      g.col_scale = w.w_group ? nullptr : w.s_b + nq;
+      e = launch_gemm_f16(g, s);
+    } else {
+      g.b = reinterpret_cast<const int8_t*>(w.b_t) + (int64_t)nq * (w.w_bits == 8 ? w.r : w.r / 2);
+      g.col_scale = w.s_b + nq;
+      e = (w.w_bits == 8 && !w.w_group) ? launch_gemm_i8(g, s) : launch_gemm_q4(g, 8, w.w_bits, w.w_group, N, s);
+    }
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
@@ -1345,51 +1382,30 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
   _Float16* opart = (_Float16*)base;
   base += align256(p.opart_bytes);
   float* ml = (float*)base;
+  base += align256(p.ml_bytes);
+  _Float16* w16 = p.w16_bytes ? (_Float16*)base : nullptr;
   const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
   const int nq = w.n_q_heads * w.head_dim, nkv2 = 2 * w.n_kv_heads * w.head_dim;
   const int len = c.max_len > 0 ? c.max_len : 1;
-  hipError_t e;
-  if (c.fmt == QSVD_CACHE_F16) {
-    dim3 grid((nkv2 + RBN - 1) / RBN, (len + RBM - 1) / RBM, c.batch);
-    KernelScope ks("recon_kv", s);
-    QSVD_LAUNCH(ks, recon_kv_kernel<QSVD_CACHE_F16>, grid, dim3(256), 0, s, (const uint8_t*)c.data,
-                       c.scale, c.seq_len, c.capacity, c.r, (const uint8_t*)w.b_t, w.s_b, N, nq, nkv2,
-                       w.w_bits, w.w_group, kv);
-    e = hipGetLastError();
-  } else {
-    // int8 latent rows times the K / V weight codes on the int8 matrix cores:
-    // every cache row (capacity rows per sequence; rows past seq_len are
-    // computed and never read), dequantized (acc * s_t) * s_n, fp16
-    GemmArgs g{};
-    g.a = (const int8_t*)c.data;
-    g.b = (const int8_t*)w.b_t + (int64_t)nq * (w.w_bits == 8 ? w.r : w.r / 2);
-    g.row_scale = c.scale;
-    g.col_scale = w.s_b + nq;
-    g.M = (int64_t)c.batch * c.capacity;
-    g.N = nkv2;
-    g.K = w.r;
-    g.seg[0] = OutSeg{kv, nkv2, 0, nkv2};
-    g.n_seg = 1;
-    g.abits = 8;
-    e = (w.w_bits == 8 && !w.w_group) ? launch_gemm_i8(g, s) : launch_gemm_q4(g, 8, w.w_bits, w.w_group, N, s);
-  }
-  if (e != hipSuccess) return e;
-  const double log2_theta = a.rope_theta > 0.f ? log2((double)a.rope_theta) : 0.0;
-  if (a.rope_theta > 0.f) {
-    KernelScope ks("rope_keys", s);
-    const int64_t work = (int64_t)len * w.n_kv_heads * (w.head_dim / 2);
-    const unsigned gx = (unsigned)std::min<int64_t>((work + 255) / 256, 4096);
-    QSVD_LAUNCH(ks, rope_keys_kernel, dim3(gx, c.batch), dim3(256), 0, s, kv, c.seq_len, c.capacity,
-                w.n_kv_heads, w.head_dim, nkv2, log2_theta);
-    e = hipGetLastError();
+  if (w16) {
+    KernelScope ks("recon_weights", s);
+    const int64_t runs = (int64_t)nkv2 * (w.r / 8);
+    QSVD_LAUNCH(ks, recon_weights_kernel, dim3((unsigned)((runs + 255) / 256)), dim3(256), 0, s,
+                (const uint8_t*)w.b_t, w.s_b, w.r, N, nq, nkv2, w.w_bits, w.w_group, w16);
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  hipError_t e = rebuild_kv(a, w16, kv, s);
+  if (e != hipSuccess) return e;
+  const double log2_theta = a.rope_theta > 0.f ? log2((double)a.rope_theta) : 0.0;
   const int nch = (len + RCH - 1) / RCH;
+  const int G = w.n_q_heads / w.n_kv_heads;
   {
     KernelScope ks("recon_attn", s);
-    QSVD_LAUNCH(ks, recon_attn_kernel, dim3(nch, c.batch), dim3(256), 0, s, a.q, kv, c.seq_len,
-                       c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, a.sm_scale * kLog2e,
-                       p.n_chunks, log2_theta, opart, ml);
+    const size_t lds = recon_attn_lds(w.head_dim, G);
+    QSVD_LAUNCH(ks, recon_attn_kernel, dim3(nch, c.batch, w.n_kv_heads), dim3(256), lds, s, a.q, kv, c.seq_len,
+                c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, a.sm_scale * kLog2e, p.n_chunks, log2_theta,
+                opart, ml);
   }
   {
     KernelScope ks("recon_combine", s);

@@ -10,6 +10,7 @@
 // 8*(v/4) + 4*(l/32) + (v%4) for accumulator registers v = 0..15.
 #include "common.h"
 #include "launch.h"
+#include <type_traits>
 
 namespace qsvd {
 
@@ -46,10 +47,14 @@ __device__ __forceinline__ ColOut col_out(const DevSegs& sg, int32_t n) {
 __device__ __forceinline__ float dequant(int32_t acc, float rs, float cs) {
   return mul_rn(mul_rn((float)acc, rs), cs);
 }
+__device__ __forceinline__ float dequant(float acc, float rs, float cs) { return mul_rn(mul_rn(acc, rs), cs); }
 
 // ---------------------------------------------------------------------------
 // Pipelined kernel: BM x BN output tile per workgroup of 4 or 8 waves (each
-// WM x WN), the contraction in stages of 64 bytes.  Operands go from global
+// WM x WN), the contraction in stages of 64 bytes.  With F16 the operands are
+// fp16 (a stage is 32 contraction elements, v_mfma_f32_32x32x16_f16, fp32
+// accumulators; a 16-byte slot is 8 elements, so the slot layout, the loads
+// and the fragment reads are the same) and K counts bytes per row.  Operands go from global
 // memory straight into LDS (global_load_lds_dwordx4: lane i of a wave writes
 // 16 bytes at base + 16 i), NS stages deep, so NS - 1 stages are in flight
 // while one is multiplied; one barrier per stage.
@@ -101,12 +106,14 @@ struct PipeCfg {
   static constexpr size_t kLds = kStages > kOut ? kStages : kOut;
 };
 
-template <int BM, int BN, int WM, int WN, int NS, bool DBG>
+template <int BM, int BN, int WM, int WN, int NS, bool DBG, bool F16>
 __global__ void __launch_bounds__((PipeCfg<BM, BN, WM, WN, NS>::kThreads))
 gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
                     const float* __restrict__ rs, const float* __restrict__ cs,
                     int64_t M, int32_t N, int32_t K, int32_t n_tiles_n, DevSegs sg, int32_t* __restrict__ dbg) {
   using C = PipeCfg<BM, BN, WM, WN, NS>;
+  using Acc = std::conditional_t<F16, f32x16, i32x16>;
+  static_assert(!(DBG && F16), "accumulator dumps are for the integer products");
   constexpr int TI = WM / 32, TJ = WN / 32;
   extern __shared__ __attribute__((aligned(1024))) uint8_t pipe_smem[];
   __shared__ __attribute__((aligned(16))) float s_rs[BM];
@@ -146,17 +153,18 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
   };
 
   // scales first: their wait then leaves the stage loads in flight
-  for (int i = tid; i < BM; i += C::kThreads) s_rs[i] = rs[min(m0 + i, M - 1)];
-  for (int i = tid; i < BN; i += C::kThreads) s_cs[i] = cs[min(n0 + i, N - 1)];
+  // (fp16 operands: a NULL scale vector means no scale)
+  for (int i = tid; i < BM; i += C::kThreads) s_rs[i] = (!F16 || rs) ? rs[min(m0 + i, M - 1)] : 1.f;
+  for (int i = tid; i < BN; i += C::kThreads) s_cs[i] = (!F16 || cs) ? cs[min(n0 + i, N - 1)] : 1.f;
 #pragma unroll
   for (int st = 0; st < NS - 1; ++st)
     if (st < nk) issue(st);
 
-  i32x16 acc[TI][TJ];
+  Acc acc[TI][TJ];
 #pragma unroll
   for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < TJ; ++j) acc[i][j] = i32x16{};
+    for (int j = 0; j < TJ; ++j) acc[i][j] = Acc{};
 
   // Fragments of one stage, by contraction half kk: af[kk][i], bf[kk][j].
   // Half 1 of a stage is read while half 0's products run, and half 0 of the
@@ -177,7 +185,11 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
     for (int i = 0; i < TI; ++i)
 #pragma unroll
       for (int j = 0; j < TJ; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk][i], bf[kk][j], acc[i][j], 0, 0, 0);
+        if constexpr (F16)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, af[kk][i]),
+                                                             __builtin_bit_cast(f16x8, bf[kk][j]), acc[i][j], 0, 0, 0);
+        else
+          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk][i], bf[kk][j], acc[i][j], 0, 0, 0);
   };
 
   // One MFMA goes out before each LDS read of the other half, so the reads
@@ -222,7 +234,7 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
   // free once every wave is past its last product) and written back as
   // 16-byte runs of one row.  Lane holds column wn*WN + 32j + l32 and rows
   // wm*WM + 32i + 8(v/4) + 4hl + v%4.
-  if (DBG) {
+  if constexpr (DBG) {
 #pragma unroll
     for (int j = 0; j < TJ; ++j) {
       const int32_t n = n0 + wn * WN + 32 * j + l32;
@@ -288,17 +300,18 @@ static DevSegs to_dev(const GemmArgs& g) {
   return d;
 }
 
-template <int BM, int BN, int WM, int WN, int NS, bool DBG>
+template <int BM, int BN, int WM, int WN, int NS, bool DBG, bool F16 = false>
 static hipError_t launch_pipe(const GemmArgs& g, const DevSegs& sg, hipStream_t s) {
   using C = PipeCfg<BM, BN, WM, WN, NS>;
-  auto kern = gemm_i8_pipe_kernel<BM, BN, WM, WN, NS, DBG>;
+  auto kern = gemm_i8_pipe_kernel<BM, BN, WM, WN, NS, DBG, F16>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::kLds);
   if (e != hipSuccess) return e;
   const int tn = (g.N + BN - 1) / BN;
   const int64_t tm = (g.M + BM - 1) / BM;
-  KernelScope ks("gemm_i8_pipe", s);
+  const int32_t kbytes = F16 ? 2 * g.K : g.K;
+  KernelScope ks(F16 ? "gemm_f16_pipe" : "gemm_i8_pipe", s);
   QSVD_LAUNCH(ks, kern, dim3((unsigned)(tm * tn)), dim3(C::kThreads), C::kLds, s, g.a, g.b, g.row_scale, g.col_scale,
-                     g.M, g.N, g.K, tn, sg, g.dbg);
+                     g.M, g.N, kbytes, tn, sg, g.dbg);
   return hipGetLastError();
 }
 
@@ -318,6 +331,18 @@ hipError_t launch_gemm_i8(const GemmArgs& g, hipStream_t s) {
                                     : launch_pipe<128, 128, 64, 64, 6, false>(g, sg, s);
   if (e != hipSuccess || !g.cq) return e;
   return launch_quantize_rows(g.seg[0].ptr, g.M, g.N, g.seg[0].ld, g.abits, 1.f, g.cq, g.sc, s);
+}
+
+hipError_t launch_gemm_f16(const GemmArgs& g, hipStream_t s) {
+  if (g.M == 0 || g.N == 0) return hipSuccess;
+  if (g.K % (PBK / 2) || g.dbg || g.cq) return hipErrorInvalidValue;
+  for (int i = 0; i < g.n_seg; ++i)
+    if (g.seg[i].n0 % 8 || g.seg[i].n % 8 || g.seg[i].ld % 8 || ((uintptr_t)g.seg[i].ptr & 15))
+      return hipErrorInvalidValue;
+  const DevSegs sg = to_dev(g);
+  const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  return big_tiles >= 256 ? launch_pipe<256, 256, 128, 64, 4, false, true>(g, sg, s)
+                          : launch_pipe<128, 128, 64, 64, 6, false, true>(g, sg, s);
 }
 
 }  // namespace qsvd

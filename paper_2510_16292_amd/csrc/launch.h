@@ -60,6 +60,11 @@ struct GemmArgs {
 // Tiled int8 GEMM for M > 32 (prefill); with g.cq set, the fp16 result is also
 // quantized per row into g.cq / g.sc.
 hipError_t launch_gemm_i8(const GemmArgs& g, hipStream_t s);
+// The same pipeline over fp16 operands (a: fp16 [M][K], b: fp16 [N][K], K in
+// elements, a multiple of 32), fp32 accumulation, then (acc * row_scale) *
+// col_scale with NULL scale vectors read as 1; no accumulator dumps or row
+// quantization.
+hipError_t launch_gemm_f16(const GemmArgs& g, hipStream_t s);
 
 // The same products with 4-bit activations and/or int4 weights, per-channel or
 // per-group (group contraction elements, a multiple of 64; scale of group g
