@@ -278,15 +278,18 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
     else:
         res.update(graph_replay(caches, hold, final, rounds, n_layers, batch, step))
     if compare_forms:
-        # absorbed vs reconstruct (plain, and with rotary embeddings of base
-        # 1e4) on this layer, attention call alone (a few calls each)
+        # absorbed vs reconstruct on this layer, attention call alone (a few
+        # calls each); with rotary embeddings (base 1e4): the form with the
+        # value side in latent space (ABSORBED) and the full rebuild
         forms = {}
         for name, m, theta in (("absorbed", B.QSVD_ATTN_ABSORBED, 0.0),
                                ("reconstruct", B.QSVD_ATTN_RECONSTRUCT, 0.0),
-                               ("reconstruct_rope", B.QSVD_ATTN_RECONSTRUCT, 1.0e4)):
-            wsb = B.qsvd_decode_workspace_size(layers[0].c, caches[0].c, 1, m)
+                               ("rope_latent_v", B.QSVD_ATTN_ABSORBED, 1.0e4),
+                               ("rope_reconstruct", B.QSVD_ATTN_RECONSTRUCT, 1.0e4)):
+            wsb = B.qsvd_decode_workspace_size(layers[0].c, caches[0].c, 1,
+                                               B.QSVD_ATTN_RECONSTRUCT if theta else m)
             ws = torch.empty((wsb,), dtype=torch.uint8, device="cuda")
-            reps = 3 if m == B.QSVD_ATTN_RECONSTRUCT else 20
+            reps = 3 if (m == B.QSVD_ATTN_RECONSTRUCT or theta) else 20
 
             def call():
                 if theta:

@@ -326,25 +326,29 @@ static qsvd_status decode_attention(const qsvd_layer* w, const qsvd_cache* c, co
   if (!aligned(q, 16) || !aligned(out, 16) || !aligned(w->s_b, 16))
     return fail(QSVD_ERR_UNSUPPORTED, "q, out and s_b must be 16-byte aligned");
   const bool rope = rope_theta > 0.f;
-  if (rope && mode == QSVD_ATTN_ABSORBED)
-    return fail(QSVD_ERR_UNSUPPORTED, "rotary embeddings need the reconstruct form (K depends on the position)");
-  const bool abs_ok = !rope && absorbed_supported(*w, *c);
+  // Rotary layers: ABSORBED is the form with the value side in latent space
+  // (the keys must be rebuilt and turned per position); RECONSTRUCT rebuilds
+  // K and V.
+  const bool abs_ok = rope ? rope_latent_supported(*w, *c) : absorbed_supported(*w, *c);
   if (mode == QSVD_ATTN_ABSORBED && !abs_ok)
-    return fail(QSVD_ERR_UNSUPPORTED, "absorbed form needs r in {128, 512, 1024, 1536} or a multiple of 128 up to 3072");
+    return fail(QSVD_ERR_UNSUPPORTED, rope ? "the rotary latent-value form needs n_q_heads <= 32 and r in {128, 512, 1024, 1536}"
+                                           : "absorbed form needs r in {128, 512, 1024, 1536} or a multiple of 128 up to 3072");
   const bool absorbed = mode == QSVD_ATTN_ABSORBED || (mode == QSVD_ATTN_AUTO && abs_ok);
   if (absorbed && absorbed_grid_rows(*w, *c, q_len) > kMaxQueryRows)
     return fail(QSVD_ERR_UNSUPPORTED, "batch * q_len * head blocks must be at most %d", kMaxQueryRows);
+  if ((!absorbed || rope) && q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct-side forms take q_len 1 only");
   if (!absorbed && w->n_q_heads > 32) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form takes at most 32 query heads");
   if (!absorbed && c->capacity > 16384)
     return fail(QSVD_ERR_UNSUPPORTED, "reconstruct form supports capacity <= 16384");
-  if (!absorbed && q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form takes q_len 1 only");
-  if (!absorbed && c->fmt == QSVD_CACHE_I4) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form takes F16/I8 caches");
-  const size_t need = absorbed ? attn_absorbed_workspace(*w, *c, q_len) : attn_reconstruct_workspace(*w, *c);
+  const size_t need = absorbed && !rope ? attn_absorbed_workspace(*w, *c, q_len) : attn_reconstruct_workspace(*w, *c);
   if (!ws || ws_bytes < need) return fail(QSVD_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   AttnArgs a{w, c, (const _Float16*)q, (_Float16*)out, sm_scale > 0.f ? sm_scale : 1.f / sqrtf((float)w->head_dim),
              q_len, rope ? rope_theta : 0.f};
   hipStream_t s = (hipStream_t)stream;
-  return hip_status(absorbed ? launch_attn_absorbed(a, ws, s) : launch_attn_reconstruct(a, ws, s), "decode attention");
+  const hipError_t e = !absorbed ? launch_attn_reconstruct(a, ws, s)
+                       : rope    ? launch_attn_rope_latent(a, ws, s)
+                                 : launch_attn_absorbed(a, ws, s);
+  return hip_status(e, "decode attention");
 }
 
 qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* c, const void* q, int32_t q_len,

@@ -220,13 +220,18 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
 // LDS area as soon as it arrives, reissues the next tile's loads into the
 // same registers, and reads the copy back for both MFMAs (row reads for the
 // scores, transposing reads for P C).
+//
+// PRE (rotary layers, decode): the scores come precomputed from the rotated
+// keys, pre[b][t][32 heads] in fp32 (already scaled by sm_scale log2 e), and
+// only the value side runs in latent space; every wave reads the scores of
+// its tile itself, so the tile loop has no barrier.
 // ---------------------------------------------------------------------------
-template <int RW, int NW, int FMT>
+template <int RW, int NW, int FMT, bool PRE>
 __global__ void __launch_bounds__(NW * 64)
 latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ cdata,
                    const float* __restrict__ cscale, const int32_t* __restrict__ seq_len,
                    int32_t capacity, int32_t r, int32_t chunk, int32_t n_chunks, int32_t q_len,
-                   _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
+                   const float* __restrict__ pre, _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
   constexpr int KS = RW / 16;    // 16-wide contraction steps of the score MFMA
   constexpr int RB = RW / 32;    // 32-row blocks of the output MFMA
   // Staged row stride in halves: RW + 16 makes the stride 8 (mod 32) dwords, so
@@ -260,7 +265,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   constexpr bool F16C = FMT == QSVD_CACHE_F16;
   auto kcol = [](int ks, int hf) { return F16C ? 16 * ks + 8 * hf : 32 * (ks >> 1) + 16 * hf + 8 * (ks & 1); };
   f16x8 qf[KS];
-  {
+  if constexpr (!PRE) {
     const _Float16* qrow = qt + ((int64_t)vb * kHeadBlk + l32) * r + slice0;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, half));
@@ -310,6 +315,45 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   load_tile(t_begin);
   for (int t0 = t_begin; t0 < t_end; t0 += 32) {
     f32x16 sacc = f32x16{};
+    float s[16];
+    if constexpr (PRE) {
+      // this lane's scores: head l32, tokens t0 + 8*(v/4) + 4*half + v%4
+      const float* prow = pre + (int64_t)b * capacity * kHeadBlk + l32;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
+        s[v] = prow[(int64_t)min(t, t_end - 1) * kHeadBlk];
+      }
+      asm volatile("" ::: "memory");    // the previous tile's transposing reads stay before these stores
+      if constexpr (F16C) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(ks, half)) = raw[ks];
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sc_cur[v] = sc_next[v];
+#pragma unroll
+        for (int i = 0; i < NLD; ++i) {
+          f16x8 c0, c1;
+          if constexpr (I4C) {
+            c0 = cvt_i4x8(raw[i].x);
+            c1 = cvt_i4x8(raw[i].y);
+          } else {
+            c0 = cvt_i8x8(raw[i].x, raw[i].y);
+            c1 = cvt_i8x8(raw[i].z, raw[i].w);
+          }
+          *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i, half)) = c0;
+          *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i + 1, half)) = c1;
+        }
+      }
+      if (t0 + 32 < t_end) load_tile(t0 + 32);
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
+        if (t >= t_end) s[v] = -INFINITY;
+      }
+    } else {
     if constexpr (kStageFirst) {
     // The tile (as exact fp16) goes to this wave's LDS copy first, so that
     // its registers take the next tile's loads before any product runs; the
@@ -392,13 +436,13 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     }
     __syncthreads();
     // Lane l holds head l32 and tokens t0 + 8*(v/4) + 4*half + v%4.
-    float s[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
       float x = ssum4[(v >> 2) * 64 + lane][v & 3];
       if constexpr (!F16C) x *= sc_cur[v];
       s[v] = (t < t_end) ? x : -INFINITY;
+    }
     }
     float mx = s[0];
 #pragma unroll
@@ -1004,17 +1048,17 @@ size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c, int32_t
   return align256(p.qt_bytes) + align256(p.opart_bytes) + align256(p.ml_bytes) + align256(p.olat_bytes);
 }
 
-template <int RW, int NW, int FMT>
+template <int RW, int NW, int FMT, bool PRE = false>
 static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, int32_t q_len, const _Float16* qt,
-                                _Float16* opart, float* ml, hipStream_t s) {
-  const size_t lds = (size_t)NW * 32 * (RW + 16) * 2 + (size_t)(NW + 1) * 1024 * 4;
-  auto kern = latent_attn_kernel<RW, NW, FMT>;
+                                _Float16* opart, float* ml, hipStream_t s, const float* pre = nullptr) {
+  const size_t lds = (size_t)NW * 32 * (RW + 16) * 2 + (PRE ? 0 : (size_t)(NW + 1) * 1024 * 4);
+  auto kern = latent_attn_kernel<RW, NW, FMT, PRE>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   KernelScope ks("latent_attn", s);
   QSVD_LAUNCH(ks, kern, dim3(p.n_chunks, c.batch * q_len), dim3(NW * 64), lds, s, qt,
                      (const uint8_t*)c.data, c.scale, c.seq_len, c.capacity, c.r, p.chunk,
-                     p.n0, q_len, opart, ml);
+                     p.n0, q_len, pre, opart, ml);
   return hipGetLastError();
 }
 
@@ -1045,6 +1089,19 @@ static hipError_t dispatch_latent(const AbsorbPlan& p, const qsvd_cache& c, int3
   return launch_latent<32, 4, FMT>(p, c, q_len, qt, opart, ml, s);
 }
 
+// Value side only, over precomputed scores (32-head plans, q_len 1).
+template <int FMT>
+static hipError_t dispatch_latent_pre(const AbsorbPlan& p, const qsvd_cache& c, const float* pre, _Float16* opart,
+                                      float* ml, hipStream_t s) {
+  if (p.rw == 192) return launch_latent<192, 8, FMT, true>(p, c, 1, nullptr, opart, ml, s, pre);
+  if (p.rw == 128) return launch_latent<128, 8, FMT, true>(p, c, 1, nullptr, opart, ml, s, pre);
+  if (p.rw == 64) return launch_latent<64, 8, FMT, true>(p, c, 1, nullptr, opart, ml, s, pre);
+  return launch_latent<32, 4, FMT, true>(p, c, 1, nullptr, opart, ml, s, pre);
+}
+
+static hipError_t merge_and_project(const AttnArgs& a, const AbsorbPlan& p, const _Float16* opart, const float* ml,
+                                    _Float16* olat, hipStream_t s);
+
 hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   const qsvd_layer& w = *a.w;
   const qsvd_cache& c = *a.c;
@@ -1071,6 +1128,16 @@ hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
       : c.fmt == QSVD_CACHE_I8  ? dispatch_latent<QSVD_CACHE_I8>(p, c, a.q_len, qt, opart, ml, s)
                                 : dispatch_latent<QSVD_CACHE_I4>(p, c, a.q_len, qt, opart, ml, s);
   if (e != hipSuccess) return e;
+  return merge_and_project(a, p, opart, ml, olat, s);
+}
+
+// Merge the chunk partials into O_lat, then o = O_lat W^u_v.
+static hipError_t merge_and_project(const AttnArgs& a, const AbsorbPlan& p, const _Float16* opart, const float* ml,
+                                    _Float16* olat, hipStream_t s) {
+  const qsvd_layer& w = *a.w;
+  const qsvd_cache& c = *a.c;
+  const int32_t rows = c.batch * a.q_len;
+  const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
   {
     KernelScope ks("merge_latent", s);
     const dim3 grid((w.r * p.hb + kMergeElems - 1) / kMergeElems, rows * p.n_hb);
@@ -1138,14 +1205,22 @@ recon_weights_kernel(const uint8_t* __restrict__ bt, const float* __restrict__ s
   *reinterpret_cast<f16x8*>(w16 + (int64_t)np * r + k0) = o;
 }
 
-// Rotary embedding angle of pair j at position pos, reduced modulo 2 pi in
-// fp64 (inv = theta^(-2j/dh) from the per-workgroup table), then cos / sin in
-// fp32, so that large positions keep their accuracy.
-__device__ __forceinline__ void rope_cs(int pos, double inv, float* c, float* s) {
+// Rotary embedding table, once per call: cs[t][j] = (cos, sin) of the angle
+// t * theta^(-2j/dh) of pair j at position t < len, formed and reduced modulo
+// 2 pi in fp64, then evaluated in fp32 (so large positions keep their
+// accuracy).  Every key/value head and sequence reads the same rows.
+__global__ void __launch_bounds__(256)
+rope_table_kernel(float2* __restrict__ cs, int32_t len, int32_t dh, double log2_theta) {
+  const int half = dh >> 1;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (int64_t)len * half) return;
+  const int t = (int)(e / half), j = (int)(e - (int64_t)t * half);
   const double two_pi = 6.283185307179586476925286766559;
-  double ang = (double)pos * inv;
+  double ang = (double)t * exp2(-2.0 * (double)j / (double)dh * log2_theta);
   ang -= floor(ang * (1.0 / two_pi)) * two_pi;
-  sincosf((float)ang, s, c);
+  float c, sn;
+  sincosf((float)ang, &sn, &c);
+  cs[e] = make_float2(c, sn);
 }
 
 __device__ __forceinline__ void rope_pair(float a, float b, float c, float s, float* ra, float* rb) {
@@ -1166,15 +1241,15 @@ constexpr int RCH = 64;
 __host__ __device__ constexpr int recon_kld(int dh) { return dh + 8; }   // staged row stride (halves)
 
 static size_t recon_attn_lds(int dh, int G) {
-  return 64 * sizeof(double) + 2 * (size_t)RCH * recon_kld(dh) * sizeof(_Float16) +
+  return 2 * (size_t)RCH * recon_kld(dh) * sizeof(_Float16) +
          (size_t)G * dh * sizeof(float) + (size_t)G * RCH * sizeof(float) + 2 * (size_t)G * sizeof(float);
 }
 
 __global__ void __launch_bounds__(256)
 recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ kv,
                   const int32_t* __restrict__ seq_len, int32_t capacity, int32_t Hq, int32_t Hkv,
-                  int32_t dh, float scale, int32_t n_chunks, double log2_theta, _Float16* __restrict__ o_part,
-                  float* __restrict__ ml_part) {
+                  int32_t dh, float scale, int32_t n_chunks, const float2* __restrict__ rope,
+                  _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
   extern __shared__ __attribute__((aligned(16))) uint8_t recon_smem[];
   const int b = blockIdx.y, ch = blockIdx.x, g = blockIdx.z, tid = threadIdx.x;
   const int lane = tid & 63, wv = tid >> 6;
@@ -1184,27 +1259,21 @@ recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k
   const int tn = min(RCH, L - t0);
   const int G = Hq / Hkv, h0 = g * G, half = dh >> 1, kld = recon_kld(dh);
   const int nkv = Hkv * dh, nkv2 = 2 * nkv;
-  const bool rope = log2_theta > 0.0;
-  double* inv = reinterpret_cast<double*>(recon_smem);                 // [dh/2]
-  _Float16* Ks = reinterpret_cast<_Float16*>(recon_smem + 64 * sizeof(double));
+  _Float16* Ks = reinterpret_cast<_Float16*>(recon_smem);
   _Float16* Vs = Ks + RCH * kld;
   float* qs = reinterpret_cast<float*>(Vs + RCH * kld);                // [G][dh], rotated and scaled
   float* ps = qs + G * dh;                                             // [G][RCH] scores, then weights
   float* red = ps + G * RCH;                                           // m[G], l[G]
 
-  if (rope) {
-    for (int j = tid; j < half; j += 256) inv[j] = exp2(-2.0 * (double)j / (double)dh * log2_theta);
-    __syncthreads();
-  }
   const _Float16* qb = q + (int64_t)b * Hq * dh + (int64_t)h0 * dh;
   for (int e = tid; e < G * dh; e += 256) {
     const int hg = e / dh, c = e - hg * dh;
     float y = (float)qb[e];
     if (rope) {
       const int j = c < half ? c : c - half;
-      float cs, sn, ra, rb;
-      rope_cs(L - 1, inv[j], &cs, &sn);
-      rope_pair((float)qb[hg * dh + j], (float)qb[hg * dh + j + half], cs, sn, &ra, &rb);
+      const float2 cs = rope[(int64_t)(L - 1) * half + j];
+      float ra, rb;
+      rope_pair((float)qb[hg * dh + j], (float)qb[hg * dh + j + half], cs.x, cs.y, &ra, &rb);
       y = c < half ? ra : rb;
     }
     qs[e] = y * scale;
@@ -1233,13 +1302,17 @@ recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k
       if (tl < tn) {
         lo = *reinterpret_cast<const f16x8*>(rows + (int64_t)tl * nkv2 + 8 * x);
         hi = *reinterpret_cast<const f16x8*>(rows + (int64_t)tl * nkv2 + half + 8 * x);
+        const float4* cs4 = reinterpret_cast<const float4*>(rope + (int64_t)(t0 + tl) * half + 8 * x);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          float cs, sn, ra, rb;
-          rope_cs(t0 + tl, inv[8 * x + i], &cs, &sn);
-          rope_pair((float)lo[i], (float)hi[i], cs, sn, &ra, &rb);
-          lo[i] = to_f16(ra);
-          hi[i] = to_f16(rb);
+        for (int i2 = 0; i2 < 4; ++i2) {
+          const float4 c2 = cs4[i2];       // pairs 2 i2 and 2 i2 + 1: (cos, sin, cos, sin)
+          float ra, rb;
+          rope_pair((float)lo[2 * i2], (float)hi[2 * i2], c2.x, c2.y, &ra, &rb);
+          lo[2 * i2] = to_f16(ra);
+          hi[2 * i2] = to_f16(rb);
+          rope_pair((float)lo[2 * i2 + 1], (float)hi[2 * i2 + 1], c2.z, c2.w, &ra, &rb);
+          lo[2 * i2 + 1] = to_f16(ra);
+          hi[2 * i2 + 1] = to_f16(rb);
         }
       }
       *reinterpret_cast<f16x8*>(Ks + tl * kld + 8 * x) = lo;
@@ -1312,10 +1385,180 @@ recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k
   }
 }
 
+// Scores of the rotary variant, pre[b][t][h] = (sm log2 e) q_rot(h) . K^_rot(t):
+// one workgroup per (chunk of RCH tokens, sequence, run of up to HPB
+// key/value heads).  A thread keeps the (cos, sin) of its staging slots in
+// registers for every head of the run; per head, the rotated K^ rows go to
+// LDS (the next head's rows are loaded meanwhile).  With G >= 4 query heads
+// per key/value head the scores come from 16x16x16 fp16 MFMAs (wave w:
+// tokens 16w .. 16w+15; the query enters as an fp16 hi/lo pair, about fp32
+// accuracy); with fewer, four lanes share each (query head, token) product
+// in fp32, a quarter of the head dimension each.  Heads past Hq (up to 32)
+// get score 0 from the first run's workgroups.
+constexpr int kRopeSlots = 2;     // staging slots per thread: RCH * dh / 16 <= 512 runs
+
+__host__ __device__ constexpr int rope_gpad(int G) { return (G + 15) / 16 * 16; }
+__host__ __device__ constexpr bool rope_mfma(int G) { return G >= 4; }
+
+static size_t rope_scores_lds(int dh, int hpb, int G) {
+  const size_t q = rope_mfma(G) ? 2 * (size_t)hpb * rope_gpad(G) * dh * sizeof(_Float16)
+                                : (size_t)hpb * G * dh * sizeof(float);
+  return (size_t)RCH * recon_kld(dh) * sizeof(_Float16) + q;
+}
+
+__global__ void __launch_bounds__(256)
+rope_scores_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ khat,
+                   const int32_t* __restrict__ seq_len, int32_t capacity, int32_t Hq, int32_t Hkv, int32_t dh,
+                   int32_t hpb, float scale, const float2* __restrict__ rope, float* __restrict__ pre) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t rs_smem[];
+  const int b = blockIdx.y, ch = blockIdx.x, tid = threadIdx.x;
+  const int L = min(seq_len[b], capacity);
+  const int t0 = ch * RCH;
+  if (t0 >= L) return;
+  const int tn = min(RCH, L - t0);
+  const int G = Hq / Hkv, half = dh >> 1, kld = recon_kld(dh), nkv = Hkv * dh;
+  const int g0 = blockIdx.z * hpb, nh = min(hpb, Hkv - g0);
+  const bool mf = rope_mfma(G);
+  const int GP = mf ? rope_gpad(G) : G;
+  _Float16* Ks = reinterpret_cast<_Float16*>(rs_smem);
+  _Float16* qhi = Ks + RCH * kld;                                  // MFMA: [nh][GP][dh], zero past G
+  _Float16* qlo = qhi + hpb * GP * dh;
+  float* qs = reinterpret_cast<float*>(Ks + RCH * kld);            // else: fp32 [nh][G][dh]
+  const _Float16* qb = q + (int64_t)b * Hq * dh + (int64_t)g0 * G * dh;
+  for (int e = tid; e < nh * GP * dh; e += 256) {
+    const int hp = e / dh, c = e - hp * dh, hh = hp / GP, hg = hp - hh * GP, j = c < half ? c : c - half;
+    float y = 0.f;
+    if (hg < G) {
+      const float2 cs = rope[(int64_t)(L - 1) * half + j];
+      const _Float16* qr = qb + (hh * G + hg) * dh;
+      float ra, rb;
+      rope_pair((float)qr[j], (float)qr[j + half], cs.x, cs.y, &ra, &rb);
+      y = (c < half ? ra : rb) * scale;
+    }
+    if (mf) {
+      const _Float16 yh = (_Float16)y;
+      qhi[e] = yh;
+      qlo[e] = (_Float16)(y - (float)yh);
+    } else {
+      qs[e] = y;
+    }
+  }
+  // staging slot i of this thread: token tl, pairs 8x .. 8x+7 (x < dh/16)
+  const int cph = half / 8;
+  float4 cs4[kRopeSlots][4];
+  f16x8 lo[kRopeSlots], hi[kRopeSlots];
+  const _Float16* rows = khat + ((int64_t)b * capacity + t0) * nkv;
+  auto load_head = [&](int g) {
+#pragma unroll
+    for (int i = 0; i < kRopeSlots; ++i) {
+      const int e = tid + 256 * i, tl = e / cph, x = e - tl * cph;
+      lo[i] = hi[i] = f16x8{};
+      if (e < RCH * cph && tl < tn) {
+        const _Float16* src = rows + (int64_t)tl * nkv + (int64_t)g * dh + 8 * x;
+        lo[i] = *reinterpret_cast<const f16x8*>(src);
+        hi[i] = *reinterpret_cast<const f16x8*>(src + half);
+      }
+    }
+  };
+#pragma unroll
+  for (int i = 0; i < kRopeSlots; ++i) {
+    const int e = tid + 256 * i, tl = e / cph, x = e - tl * cph;
+    if (e < RCH * cph && tl < tn) {
+      const float4* src = reinterpret_cast<const float4*>(rope + (int64_t)(t0 + tl) * half + 8 * x);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) cs4[i][k] = src[k];
+    }
+  }
+  load_head(g0);
+  float* prow = pre + ((int64_t)b * capacity + t0) * kHeadBlk;
+  const int lane = tid & 63, wv = tid >> 6, l16 = lane & 15, kq = lane >> 4;
+  for (int hh = 0; hh < nh; ++hh) {
+#pragma unroll
+    for (int i = 0; i < kRopeSlots; ++i) {
+      const int e = tid + 256 * i, tl = e / cph, x = e - tl * cph;
+      if (e >= RCH * cph) continue;
+      f16x8 a = lo[i], c = hi[i];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {     // pairs 2k, 2k + 1: (cos, sin, cos, sin)
+        float ra, rb;
+        rope_pair((float)a[2 * k], (float)c[2 * k], cs4[i][k].x, cs4[i][k].y, &ra, &rb);
+        a[2 * k] = to_f16(ra);
+        c[2 * k] = to_f16(rb);
+        rope_pair((float)a[2 * k + 1], (float)c[2 * k + 1], cs4[i][k].z, cs4[i][k].w, &ra, &rb);
+        a[2 * k + 1] = to_f16(ra);
+        c[2 * k + 1] = to_f16(rb);
+      }
+      *reinterpret_cast<f16x8*>(Ks + tl * kld + 8 * x) = a;
+      *reinterpret_cast<f16x8*>(Ks + tl * kld + half + 8 * x) = c;
+    }
+    if (hh + 1 < nh) load_head(g0 + hh + 1);
+    __syncthreads();
+    if (!mf) {
+      // every thread runs G iterations (G * RCH * 4 items, 256 per query
+      // head), so the quad reduction is uniform across the wave
+      const int dq = dh / 4;
+      for (int e = tid; e < G * RCH * 4; e += 256) {
+        const int qd = e & 3, tl = (e >> 2) & (RCH - 1), hg = e >> 8;
+        const float* qh = qs + (hh * G + hg) * dh + qd * dq;
+        const _Float16* kr = Ks + tl * kld + qd * dq;
+        float acc = 0.f;
+        for (int c = 0; c < dq; c += 8) {
+          const f16x8 k8 = *reinterpret_cast<const f16x8*>(kr + c);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc = fmaf(qh[c + i], (float)k8[i], acc);
+        }
+        acc += __shfl_xor(acc, 1);
+        acc += __shfl_xor(acc, 2);
+        if (qd == 0 && tl < tn) prow[(int64_t)tl * kHeadBlk + (g0 + hh) * G + hg] = acc;
+      }
+    }
+    // S[token][head]: A = K^ rows (lane: token 16 wv + l16, k 4 kq .. +3 of
+    // each 16-wide step), B = the query rows (lane: head 16 hb + l16); lane
+    // receives head 16 hb + l16 at tokens 16 wv + 4 kq + v
+    for (int hb = 0; mf && hb < GP; hb += 16) {
+      f32x4 acc = f32x4{};
+      const _Float16* ka = Ks + (16 * wv + l16) * kld + 4 * kq;
+      const _Float16* qh = qhi + ((hh * GP) + hb + l16) * dh + 4 * kq;
+      const _Float16* ql = qlo + ((hh * GP) + hb + l16) * dh + 4 * kq;
+      for (int k0 = 0; k0 < dh; k0 += 16) {
+        const f16x4 a = *reinterpret_cast<const f16x4*>(ka + k0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x16f16(a, *reinterpret_cast<const f16x4*>(qh + k0), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x16f16(a, *reinterpret_cast<const f16x4*>(ql + k0), acc, 0, 0, 0);
+      }
+      const int hg = hb + l16;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int tl = 16 * wv + 4 * kq + v;
+        if (hg < G && tl < tn) prow[(int64_t)tl * kHeadBlk + (g0 + hh) * G + hg] = acc[v];
+      }
+    }
+    __syncthreads();
+  }
+  if (blockIdx.z == 0)
+    for (int e = tid; e < tn * (kHeadBlk - Hq); e += 256) {
+      const int tl = e / (kHeadBlk - Hq), h = Hq + e - tl * (kHeadBlk - Hq);
+      prow[(int64_t)tl * kHeadBlk + h] = 0.f;
+    }
+}
+
 struct ReconPlan {
-  size_t kv_bytes, opart_bytes, ml_bytes, w16_bytes;
+  size_t kv_bytes, opart_bytes, ml_bytes, w16_bytes, rope_bytes;
   int n_chunks;
 };
+
+// (cos, sin) rows of the rotary table for every position a cache can hold.
+static size_t rope_table_bytes(const qsvd_layer& w, const qsvd_cache& c) {
+  return (size_t)c.capacity * (w.head_dim / 2) * sizeof(float2);
+}
+
+static hipError_t launch_rope_table(const AttnArgs& a, float2* cs, hipStream_t s) {
+  const int len = a.c->max_len > 0 ? a.c->max_len : 1;
+  const int64_t n = (int64_t)len * (a.w->head_dim / 2);
+  KernelScope ks("rope_table", s);
+  QSVD_LAUNCH(ks, rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, cs, len, a.w->head_dim,
+              log2((double)a.rope_theta));
+  return hipGetLastError();
+}
 
 static ReconPlan plan_recon(const qsvd_layer& w, const qsvd_cache& c) {
   ReconPlan p{};
@@ -1325,25 +1568,70 @@ static ReconPlan plan_recon(const qsvd_layer& w, const qsvd_cache& c) {
   p.opart_bytes = (size_t)c.batch * p.n_chunks * w.head_dim * kHeadBlk * sizeof(_Float16);
   p.ml_bytes = (size_t)c.batch * p.n_chunks * 64 * sizeof(float);
   p.w16_bytes = c.fmt == QSVD_CACHE_F16 ? (size_t)nkv2 * w.r * sizeof(_Float16) : 0;
+  p.rope_bytes = rope_table_bytes(w, c);
   return p;
 }
 
-size_t attn_reconstruct_workspace(const qsvd_layer& w, const qsvd_cache& c) {
-  const ReconPlan p = plan_recon(w, c);
-  return align256(p.kv_bytes) + align256(p.opart_bytes) + align256(p.ml_bytes) + align256(p.w16_bytes);
+// The rotary variant with the value side in latent space: K^ only, the
+// scores, then the latent attention's value half, merge and W^u_v.
+bool rope_latent_supported(const qsvd_layer& w, const qsvd_cache& c) {
+  int rw, nw;
+  return w.n_q_heads <= kHeadBlk && pick_slice(w.r, &rw, &nw);
 }
 
-// K^ | V^ rows of the cache into kv.  Rows past a sequence's length are
-// rebuilt too when that keeps one launch (at most a third of the rows wasted);
-// otherwise one launch per sequence over its first max_len rows.
-static hipError_t rebuild_kv(const AttnArgs& a, const _Float16* w16, _Float16* kv, hipStream_t s) {
+struct RopeLatentPlan {
+  size_t khat_bytes, pre_bytes, w16_bytes, rope_bytes;
+  AbsorbPlan ap;
+};
+
+static RopeLatentPlan plan_rope_latent(const qsvd_layer& w, const qsvd_cache& c) {
+  RopeLatentPlan p{};
+  const int nkv = w.n_kv_heads * w.head_dim;
+  p.khat_bytes = (size_t)c.batch * c.capacity * nkv * sizeof(_Float16);
+  p.pre_bytes = (size_t)c.batch * c.capacity * kHeadBlk * sizeof(float);
+  p.w16_bytes = c.fmt == QSVD_CACHE_F16 ? (size_t)nkv * w.r * sizeof(_Float16) : 0;
+  p.rope_bytes = rope_table_bytes(w, c);
+  p.ap = plan_absorbed(w, c, 1);
+  return p;
+}
+
+static size_t rope_latent_workspace(const qsvd_layer& w, const qsvd_cache& c) {
+  const RopeLatentPlan p = plan_rope_latent(w, c);
+  return align256(p.khat_bytes) + align256(p.pre_bytes) + align256(p.w16_bytes) + align256(p.rope_bytes) +
+         align256(p.ap.opart_bytes) + align256(p.ap.ml_bytes) + align256(p.ap.olat_bytes);
+}
+
+// One workspace size serves both reconstruct-side forms (with and without
+// the value side in latent space).
+size_t attn_reconstruct_workspace(const qsvd_layer& w, const qsvd_cache& c) {
+  const ReconPlan p = plan_recon(w, c);
+  const size_t full = align256(p.kv_bytes) + align256(p.opart_bytes) + align256(p.ml_bytes) + align256(p.w16_bytes) +
+                      align256(p.rope_bytes);
+  const size_t lat = rope_latent_supported(w, c) ? rope_latent_workspace(w, c) : 0;
+  return full > lat ? full : lat;
+}
+
+// Columns [nq, nq + ncols) of C W^u for the cache rows, fp16 into out (row
+// stride ncols): K^ (ncols = Hkv dh) or K^ | V^ (2 Hkv dh).  Rows past a
+// sequence's length are rebuilt too when that keeps one launch (at most a
+// third of the rows wasted); otherwise one launch per sequence over its first
+// max_len rows.
+static hipError_t rebuild_rows(const AttnArgs& a, int ncols, _Float16* w16, _Float16* out, hipStream_t s) {
   const qsvd_layer& w = *a.w;
   const qsvd_cache& c = *a.c;
   const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
-  const int nq = w.n_q_heads * w.head_dim, nkv2 = 2 * w.n_kv_heads * w.head_dim;
+  const int nq = w.n_q_heads * w.head_dim;
   const int len = c.max_len > 0 ? c.max_len : 1;
-  const bool f16 = c.fmt == QSVD_CACHE_F16;
-  const size_t row_bytes = f16 ? (size_t)c.r * 2 : (size_t)c.r;
+  const bool f16 = c.fmt == QSVD_CACHE_F16, i4 = c.fmt == QSVD_CACHE_I4;
+  if (f16) {
+    KernelScope ks("recon_weights", s);
+    const int64_t runs = (int64_t)ncols * (w.r / 8);
+    QSVD_LAUNCH(ks, recon_weights_kernel, dim3((unsigned)((runs + 255) / 256)), dim3(256), 0, s,
+                (const uint8_t*)w.b_t, w.s_b, w.r, N, nq, ncols, w.w_bits, w.w_group, w16);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const size_t row_bytes = f16 ? (size_t)c.r * 2 : i4 ? (size_t)c.r / 2 : (size_t)c.r;
   const bool one = c.batch == 1 || 4 * (int64_t)len >= 3 * (int64_t)c.capacity;
   const int launches = one ? 1 : c.batch;
   for (int i = 0; i < launches; ++i) {
@@ -1352,11 +1640,11 @@ static hipError_t rebuild_kv(const AttnArgs& a, const _Float16* w16, _Float16* k
     g.a = reinterpret_cast<const int8_t*>(reinterpret_cast<const uint8_t*>(c.data) + r0 * row_bytes);
     g.row_scale = f16 ? nullptr : c.scale + r0;
     g.M = one ? (c.batch == 1 ? len : (int64_t)c.batch * c.capacity) : len;
-    g.N = nkv2;
+    g.N = ncols;
     g.K = w.r;
-    g.seg[0] = OutSeg{kv + r0 * nkv2, nkv2, 0, nkv2};
+    g.seg[0] = OutSeg{out + r0 * ncols, ncols, 0, ncols};
     g.n_seg = 1;
-    g.abits = 8;
+    g.abits = i4 ? 4 : 8;
     hipError_t e;
     if (f16) {
       g.b = reinterpret_cast<const int8_t*>(w16);
@@ -1365,7 +1653,8 @@ static hipError_t rebuild_kv(const AttnArgs& a, const _Float16* w16, _Float16* k
     } else {
       g.b = reinterpret_cast<const int8_t*>(w.b_t) + (int64_t)nq * (w.w_bits == 8 ? w.r : w.r / 2);
       g.col_scale = w.s_b + nq;
-      e = (w.w_bits == 8 && !w.w_group) ? launch_gemm_i8(g, s) : launch_gemm_q4(g, 8, w.w_bits, w.w_group, N, s);
+      e = (!i4 && w.w_bits == 8 && !w.w_group) ? launch_gemm_i8(g, s)
+                                               : launch_gemm_q4(g, g.abits, w.w_bits, w.w_group, N, s);
     }
     if (e != hipSuccess) return e;
   }
@@ -1384,28 +1673,20 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
   float* ml = (float*)base;
   base += align256(p.ml_bytes);
   _Float16* w16 = p.w16_bytes ? (_Float16*)base : nullptr;
-  const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
-  const int nq = w.n_q_heads * w.head_dim, nkv2 = 2 * w.n_kv_heads * w.head_dim;
+  base += align256(p.w16_bytes);
+  float2* rope = a.rope_theta > 0.f ? (float2*)base : nullptr;
+  const int nkv2 = 2 * w.n_kv_heads * w.head_dim;
   const int len = c.max_len > 0 ? c.max_len : 1;
-  if (w16) {
-    KernelScope ks("recon_weights", s);
-    const int64_t runs = (int64_t)nkv2 * (w.r / 8);
-    QSVD_LAUNCH(ks, recon_weights_kernel, dim3((unsigned)((runs + 255) / 256)), dim3(256), 0, s,
-                (const uint8_t*)w.b_t, w.s_b, w.r, N, nq, nkv2, w.w_bits, w.w_group, w16);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  hipError_t e = rebuild_kv(a, w16, kv, s);
+  hipError_t e = rebuild_rows(a, nkv2, w16, kv, s);
   if (e != hipSuccess) return e;
-  const double log2_theta = a.rope_theta > 0.f ? log2((double)a.rope_theta) : 0.0;
+  if (rope && (e = launch_rope_table(a, rope, s)) != hipSuccess) return e;
   const int nch = (len + RCH - 1) / RCH;
   const int G = w.n_q_heads / w.n_kv_heads;
   {
     KernelScope ks("recon_attn", s);
     const size_t lds = recon_attn_lds(w.head_dim, G);
     QSVD_LAUNCH(ks, recon_attn_kernel, dim3(nch, c.batch, w.n_kv_heads), dim3(256), lds, s, a.q, kv, c.seq_len,
-                c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, a.sm_scale * kLog2e, p.n_chunks, log2_theta,
-                opart, ml);
+                c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, a.sm_scale * kLog2e, p.n_chunks, rope, opart, ml);
   }
   {
     KernelScope ks("recon_combine", s);
@@ -1413,6 +1694,50 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
                        c.seq_len, RCH, p.n_chunks, nch, w.head_dim, w.n_q_heads, a.out);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_attn_rope_latent(const AttnArgs& a, void* ws, hipStream_t s) {
+  const qsvd_layer& w = *a.w;
+  const qsvd_cache& c = *a.c;
+  const RopeLatentPlan p = plan_rope_latent(w, c);
+  uint8_t* base = (uint8_t*)ws;
+  _Float16* khat = (_Float16*)base;
+  base += align256(p.khat_bytes);
+  float* pre = (float*)base;
+  base += align256(p.pre_bytes);
+  _Float16* w16 = p.w16_bytes ? (_Float16*)base : nullptr;
+  base += align256(p.w16_bytes);
+  float2* rope = (float2*)base;
+  base += align256(p.rope_bytes);
+  _Float16* opart = (_Float16*)base;
+  base += align256(p.ap.opart_bytes);
+  float* ml = (float*)base;
+  base += align256(p.ap.ml_bytes);
+  _Float16* olat = (_Float16*)base;
+  const int nkv = w.n_kv_heads * w.head_dim;
+  const int len = c.max_len > 0 ? c.max_len : 1;
+  hipError_t e = rebuild_rows(a, nkv, w16, khat, s);
+  if (e != hipSuccess) return e;
+  if ((e = launch_rope_table(a, rope, s)) != hipSuccess) return e;
+  {
+    KernelScope ks("rope_scores", s);
+    const int G = w.n_q_heads / w.n_kv_heads, nch = (len + RCH - 1) / RCH;
+    // runs of up to 8 key/value heads share the (cos, sin) registers, as long
+    // as the grid keeps about four workgroups per CU
+    int hpb = std::min(w.n_kv_heads, 8);
+    while (hpb > 1 && (int64_t)nch * c.batch * ((w.n_kv_heads + hpb - 1) / hpb) < 1024) hpb /= 2;
+    const unsigned runs = (unsigned)((w.n_kv_heads + hpb - 1) / hpb);
+    QSVD_LAUNCH(ks, rope_scores_kernel, dim3(nch, c.batch, runs), dim3(256), rope_scores_lds(w.head_dim, hpb, G), s,
+                a.q, khat, c.seq_len, c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, hpb, a.sm_scale * kLog2e,
+                rope, pre);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  e = c.fmt == QSVD_CACHE_F16 ? dispatch_latent_pre<QSVD_CACHE_F16>(p.ap, c, pre, opart, ml, s)
+      : c.fmt == QSVD_CACHE_I8  ? dispatch_latent_pre<QSVD_CACHE_I8>(p.ap, c, pre, opart, ml, s)
+                                : dispatch_latent_pre<QSVD_CACHE_I4>(p.ap, c, pre, opart, ml, s);
+  if (e != hipSuccess) return e;
+  return merge_and_project(a, p.ap, opart, ml, olat, s);
 }
 
 }  // namespace qsvd

@@ -91,13 +91,19 @@ struct AttnArgs {
   _Float16* out;          // same layout
   float sm_scale;
   int32_t q_len;          // queries per sequence: the last q_len cached positions, causal among them
-  float rope_theta;       // > 0: rotary embedding of q and the rebuilt K (reconstruct form only)
+  float rope_theta;       // > 0: rotary embedding of q and the rebuilt K (the two reconstruct-side forms)
 };
 size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len);
 // Rows of the absorbed attention grid: (sequence, query) rows times head blocks.
 int64_t absorbed_grid_rows(const qsvd_layer& w, const qsvd_cache& c, int32_t q_len);
 hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s);
+// Workspace of either reconstruct-side form (the larger of the two).
 size_t attn_reconstruct_workspace(const qsvd_layer& w, const qsvd_cache& c);
+// K^ and V^ rebuilt for every cached token, plain attention over them.
 hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s);
+// Rotary layers: K^ rebuilt and rotated for the scores, the value side in
+// latent space (32-head plans: n_q_heads <= 32, r in {128, 512, 1024, 1536}).
+bool rope_latent_supported(const qsvd_layer& w, const qsvd_cache& c);
+hipError_t launch_attn_rope_latent(const AttnArgs& a, void* ws, hipStream_t s);
 
 }  // namespace qsvd

@@ -208,8 +208,10 @@ def test_decode_validation(lib):
         == B.QSVD_ERR_WORKSPACE
     assert _decode(layer_struct(head_dim=48, n_q_heads=4), C) == B.QSVD_ERR_UNSUPPORTED
     assert _decode(L, cache_struct(batch=65)) == B.QSVD_ERR_UNSUPPORTED
-    assert _decode(L, cache_struct(fmt=B.QSVD_CACHE_I4, scale=FAKE), mode=B.QSVD_ATTN_RECONSTRUCT) == \
-        B.QSVD_ERR_UNSUPPORTED
+    c4 = cache_struct(fmt=B.QSVD_CACHE_I4, scale=FAKE)       # int4 caches rebuild on the 4-bit products
+    need4 = B.qsvd_decode_workspace_size(L, c4, 1, B.QSVD_ATTN_RECONSTRUCT)
+    assert need4 > 0
+    assert _decode(L, c4, mode=B.QSVD_ATTN_RECONSTRUCT, ws_bytes=need4 - 1) == B.QSVD_ERR_WORKSPACE
     assert _decode(layer_struct(r=192), cache_struct(r=192), mode=B.QSVD_ATTN_ABSORBED) == B.QSVD_ERR_UNSUPPORTED
     need = B.qsvd_decode_workspace_size(L, C, 1, B.QSVD_ATTN_ABSORBED)
     assert need > 0
@@ -229,20 +231,28 @@ def _decode_rope(layer, cache, theta=10000.0, q_len=1, mode=0, ws_bytes=1 << 40)
 
 
 def test_decode_rope_validation(lib):
-    """Every case fails before a launch: the rotary variant takes only the
-    reconstruct form and a base above 1."""
+    """Every case fails before a launch.  Rotary layers run the form with the
+    value side in latent space (ABSORBED, or AUTO where its 32-head plans
+    apply) or the full rebuild (RECONSTRUCT), q_len 1, with a base above 1;
+    one workspace size (the reconstruct query) serves both."""
     L, C = layer_struct(), cache_struct()
     for theta in (0.0, -5.0, 1.0, float("inf"), float("nan")):
         assert _decode_rope(L, C, theta=theta) == B.QSVD_ERR_INVALID_ARG
-    assert _decode_rope(L, C, mode=B.QSVD_ATTN_ABSORBED) == B.QSVD_ERR_UNSUPPORTED
-    assert _decode_rope(L, C, q_len=2) == B.QSVD_ERR_UNSUPPORTED            # AUTO falls to reconstruct: q_len 1
-    assert _decode_rope(layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64), C) == B.QSVD_ERR_UNSUPPORTED
-    assert _decode_rope(L, cache_struct(fmt=B.QSVD_CACHE_I4, scale=FAKE)) == B.QSVD_ERR_UNSUPPORTED
-    assert _decode_rope(L, cache_struct(capacity=20000)) == B.QSVD_ERR_UNSUPPORTED
+    # latent-value form: 32-head plans only
+    assert _decode_rope(layer_struct(r=192), cache_struct(r=192), mode=B.QSVD_ATTN_ABSORBED) == \
+        B.QSVD_ERR_UNSUPPORTED
+    wide = layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64)
+    assert _decode_rope(wide, C, mode=B.QSVD_ATTN_ABSORBED) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode_rope(wide, C) == B.QSVD_ERR_UNSUPPORTED                  # AUTO -> full rebuild: <= 32 heads
+    for mode in (B.QSVD_ATTN_AUTO, B.QSVD_ATTN_ABSORBED, B.QSVD_ATTN_RECONSTRUCT):
+        assert _decode_rope(L, C, q_len=2, mode=mode) == B.QSVD_ERR_UNSUPPORTED
+    assert _decode_rope(L, cache_struct(capacity=20000), mode=B.QSVD_ATTN_RECONSTRUCT) == B.QSVD_ERR_UNSUPPORTED
     assert _decode_rope(L, C, mode=3) == B.QSVD_ERR_INVALID_ARG
-    need = B.qsvd_decode_workspace_size(L, C, 1, B.QSVD_ATTN_RECONSTRUCT)
-    assert _decode_rope(L, C, ws_bytes=need - 1) == B.QSVD_ERR_WORKSPACE
-    assert _decode_rope(L, C, mode=B.QSVD_ATTN_RECONSTRUCT, ws_bytes=need - 1) == B.QSVD_ERR_WORKSPACE
+    for c in (C, cache_struct(fmt=B.QSVD_CACHE_I8, scale=FAKE), cache_struct(fmt=B.QSVD_CACHE_I4, scale=FAKE)):
+        need = B.qsvd_decode_workspace_size(L, c, 1, B.QSVD_ATTN_RECONSTRUCT)
+        assert need > 0
+        for mode in (B.QSVD_ATTN_AUTO, B.QSVD_ATTN_ABSORBED, B.QSVD_ATTN_RECONSTRUCT):
+            assert _decode_rope(L, c, mode=mode, ws_bytes=need - 1) == B.QSVD_ERR_WORKSPACE
 
 
 def test_decode_workspace_sizes_cover_growth(lib):

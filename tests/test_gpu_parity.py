@@ -893,9 +893,16 @@ def test_decode_gqa_int4_cache_ragged(gqa):
     assert np.array_equal(H.host(dc.scale).view(np.uint32), oc.scale.view(np.uint32))
 
 
-# ------------------------------------------------------------------ rotary position embedding (reconstruct form)
+# ------------------------------------------------------------------ rotary position embedding
 
-def test_decode_rope_tiny_end_to_end(tiny):
+# Rotary layers: ABSORBED rebuilds and turns K^ for the scores and keeps the
+# value side in latent space; RECONSTRUCT rebuilds K^ and V^.
+ROPE_MODES = [B.QSVD_ATTN_ABSORBED, B.QSVD_ATTN_RECONSTRUCT]
+ROPE_MODE_IDS = ["latent_v", "rebuild_kv"]
+
+
+@pytest.mark.parametrize("mode", ROPE_MODES, ids=ROPE_MODE_IDS)
+def test_decode_rope_tiny_end_to_end(tiny, mode):
     """Tiny layer with rotary embeddings: 64 prefill tokens into an fp16 latent
     cache, then 8 decode steps of projection, append and rotary attention (the
     rebuilt K rows and the query turned at their positions), each against the
@@ -912,10 +919,10 @@ def test_decode_rope_tiny_end_to_end(tiny):
         xt = gen.decode_activations(wl, t)
         proj = O.decode_step(ol, oc, xt, 8)
         ref = O.attention_reference(ol, oc, proj["Q"][:, None, :], 1, rope_theta=theta)[:, 0, :]
-        H.say(f"decode rope tiny step={t}")
+        H.say(f"decode rope tiny step={t} mode={mode}")
         p = H.Prefill(dl, 1, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
         H.append(dc, p.c_h, n_new=1)
-        out = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO, rope_theta=theta))
+        out = H.host(H.decode_attention(dl, dc, p.q, mode, rope_theta=theta))
         ok, info = H.close_enough(out, ref)
         H.say(f"  max-abs, rel-L2, rms = {info}")
         assert ok, (t, info)
@@ -923,40 +930,78 @@ def test_decode_rope_tiny_end_to_end(tiny):
         assert not H.close_enough(out, proj["out"], max_abs=1e-3, rel_l2=1e-3)[0]
 
 
+def _gqa_cache(L, fmt, lengths, cap, codes_bits=8):
+    """Ragged int8 or int4 latent cache of the small GQA layer (rows past each
+    length hold the same synthetic distribution)."""
+    wl = configs.Workload(95, "gqa-test", L, "gaussian", 8, 0, 8, fmt)
+    batch = len(lengths)
+    oc = O.LatentCache(fmt, batch, cap, L.r)
+    dc = B.DeviceCache(fmt, batch, cap, L.r, lengths)
+    if fmt == O.CACHE_I8:
+        codes, scales = gen.latent_codes(wl, batch, cap)
+        for b, n in enumerate(lengths):
+            oc.append(b, None, codes[b, :n], scales[b, :n])
+        dc.data.copy_(H.dev(codes))
+        dc.scale.copy_(H.dev(scales))
+    else:
+        rows = gen.latent_rows(wl, batch, cap)
+        data = np.zeros((batch, cap, L.r // 2), np.uint8)
+        scale = np.zeros((batch, cap), np.float32)
+        for b in range(batch):
+            codes, sc = O.quantize_act(rows[b], 4)
+            data[b], scale[b] = O.pack_int4(codes), sc
+            oc.append(b, None, codes[:lengths[b]], sc[:lengths[b]])
+        dc.data.copy_(H.dev(data))
+        dc.scale.copy_(H.dev(scale))
+    return wl, oc, dc
+
+
+@pytest.mark.parametrize("mode", ROPE_MODES, ids=ROPE_MODE_IDS)
 @pytest.mark.parametrize("theta", [1.0e4, 1.0e6], ids=["base1e4", "base1e6"])
-def test_decode_rope_gqa_int8_ragged(gqa, theta):
+def test_decode_rope_gqa_int8_ragged(gqa, theta, mode):
     """Grouped queries (8 over 2) over an int8 latent cache with ragged lengths
     1 / 45 / 130, 3 decode steps of rotary attention (the int8 rows rebuilt on
     the int8 matrix cores, then rotated)."""
     L, ol, dl = gqa
-    lengths = [1, 45, 130]
-    batch, cap = 3, 140
-    wl = configs.Workload(95, "gqa-test", L, "gaussian", 8, 0, 8, configs.CACHE_I8)
-    codes, scales = gen.latent_codes(wl, batch, cap)
-    oc = O.LatentCache(O.CACHE_I8, batch, cap, L.r)
-    dc = B.DeviceCache(B.QSVD_CACHE_I8, batch, cap, L.r, lengths)
-    for b, n in enumerate(lengths):
-        oc.append(b, None, codes[b, :n], scales[b, :n])
-    dc.data.copy_(H.dev(np.where(np.arange(cap)[None, :, None] < np.array(lengths)[:, None, None], codes, 0)))
-    dc.scale.copy_(H.dev(np.where(np.arange(cap)[None, :] < np.array(lengths)[:, None], scales, 0)))
+    wl, oc, dc = _gqa_cache(L, O.CACHE_I8, [1, 45, 130], 140)
+    batch = 3
     for t in range(3):
         xt = gen.decode_activations(wl, t, batch=batch)
         proj = O.decode_step(ol, oc, xt, 8)
         ref = O.attention_reference(ol, oc, proj["Q"][:, None, :], 1, rope_theta=theta)[:, 0, :]
-        H.say(f"decode rope gqa int8 step={t} theta={theta}")
+        H.say(f"decode rope gqa int8 step={t} theta={theta} mode={mode}")
         p = H.Prefill(dl, batch, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
         H.append(dc, cq=p.cq, sc=p.sc, n_new=1)
-        out = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_RECONSTRUCT, rope_theta=theta))
+        out = H.host(H.decode_attention(dl, dc, p.q, mode, rope_theta=theta))
         ok, info = H.close_enough(out, ref)
         H.say(f"  max-abs, rel-L2, rms = {info}")
         assert ok, (t, info)
 
 
-def test_decode_reconstruct_and_rope_qwen_w4_int8_cache(qwen):
+@pytest.mark.parametrize("mode", ROPE_MODES, ids=ROPE_MODE_IDS)
+def test_decode_rope_and_reconstruct_gqa_int4_cache(gqa, mode):
+    """Int4 latent cache (ragged 3 / 50 / 97): the rows rebuilt on the 4-bit
+    activation products, attended without (RECONSTRUCT only) and with rotary
+    embeddings."""
+    L, ol, dl = gqa
+    wl, oc, dc = _gqa_cache(L, O.CACHE_I4, [3, 50, 97], 100)
+    g = np.random.default_rng(44)
+    q = (g.standard_normal((3, L.n_q_heads * L.head_dim)) * 8.0).astype(np.float16)
+    for theta in ((None, 1.0e4) if mode == B.QSVD_ATTN_RECONSTRUCT else (1.0e4,)):
+        H.say(f"decode gqa int4 cache theta={theta} mode={mode}")
+        ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, rope_theta=theta)[:, 0, :]
+        out = H.host(H.decode_attention(dl, dc, H.dev(q), mode, rope_theta=theta))
+        ok, info = H.close_enough(out, ref)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (theta, info)
+
+
+@pytest.mark.parametrize("mode", ROPE_MODES, ids=ROPE_MODE_IDS)
+def test_decode_reconstruct_and_rope_qwen_w4_int8_cache(qwen, mode):
     """Qwen2-VL-7B-shaped layer (28 over 4 heads, r=1024, int4 weights in groups
     of 128) over an int8 latent cache with ragged lengths 7 / 300 / 1029: the
-    rows rebuilt by the int4-weight product, attended without and with rotary
-    embeddings (base 1e6)."""
+    rows rebuilt by the int4-weight product, attended without (RECONSTRUCT
+    only) and with rotary embeddings (base 1e6)."""
     wl, ol, dl = qwen
     L = wl.layer
     lengths = [7, 300, 1029]
@@ -971,38 +1016,57 @@ def test_decode_reconstruct_and_rope_qwen_w4_int8_cache(qwen):
     g = np.random.default_rng(2024)
     q = (g.standard_normal((batch, L.n_q_heads * L.head_dim)) * 2.0).astype(np.float16)
     q_dev = H.dev(q)
-    for theta in (None, 1.0e6):
-        H.say(f"decode qwen int8 cache reconstruct theta={theta}")
+    for theta in ((None, 1.0e6) if mode == B.QSVD_ATTN_RECONSTRUCT else (1.0e6,)):
+        H.say(f"decode qwen int8 cache theta={theta} mode={mode}")
         ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, rope_theta=theta)[:, 0, :]
-        out = H.host(H.decode_attention(dl, dc, q_dev, B.QSVD_ATTN_RECONSTRUCT, rope_theta=theta))
+        out = H.host(H.decode_attention(dl, dc, q_dev, mode, rope_theta=theta))
         ok, info = H.close_enough(out, ref)
         H.say(f"  max-abs, rel-L2, rms = {info}")
         assert ok, (theta, info)
 
 
-def test_decode_rope_long_positions(gqa):
-    """Positions up to the reconstruct form's largest capacity (16384): one
+@pytest.mark.parametrize("mode", ROPE_MODES, ids=ROPE_MODE_IDS)
+def test_decode_rope_long_positions(gqa, mode):
+    """Positions up to the full rebuild's largest capacity (16384): one
     sequence filled to capacity and one to 9001 tokens of an int8 cache, a
     random query at the last position; the angles reach 16383 rad and are
     reduced in fp64 before the fp32 sine and cosine."""
     L, ol, dl = gqa
-    lengths = [16384, 9001]
-    batch, cap = 2, 16384
-    wl = configs.Workload(95, "gqa-test", L, "gaussian", 8, 0, 8, configs.CACHE_I8)
-    codes, scales = gen.latent_codes(wl, batch, cap)
-    oc = O.LatentCache(O.CACHE_I8, batch, cap, L.r)
-    for b, n in enumerate(lengths):
-        oc.append(b, None, codes[b, :n], scales[b, :n])
-    dc = B.DeviceCache(B.QSVD_CACHE_I8, batch, cap, L.r, lengths)
-    dc.data.copy_(H.dev(codes))
-    dc.scale.copy_(H.dev(scales))
+    wl, oc, dc = _gqa_cache(L, O.CACHE_I8, [16384, 9001], 16384)
     g = np.random.default_rng(16384)
     # queries large enough for a peaked softmax, so that a wrong angle moves the output
-    q = (g.standard_normal((batch, L.n_q_heads * L.head_dim)) * 20.0).astype(np.float16)
+    q = (g.standard_normal((2, L.n_q_heads * L.head_dim)) * 20.0).astype(np.float16)
     for theta in (1.0e4, 5.0e5):
-        H.say(f"decode rope long positions theta={theta}")
+        H.say(f"decode rope long positions theta={theta} mode={mode}")
         ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, rope_theta=theta)[:, 0, :]
-        out = H.host(H.decode_attention(dl, dc, H.dev(q), B.QSVD_ATTN_AUTO, rope_theta=theta))
+        out = H.host(H.decode_attention(dl, dc, H.dev(q), mode, rope_theta=theta))
         ok, info = H.close_enough(out, ref)
         H.say(f"  max-abs, rel-L2, rms = {info}")
         assert ok, (theta, info)
+
+
+def test_decode_rope_latent_v_llava7b_width(llava):
+    """LLaVA-1.5-7B-shaped layer (32 heads x 128, r=1536) over an fp16 latent
+    cache with ragged lengths 1 / 290 / 1000: the latent-value rotary form
+    (fp16 rows rebuilt on the fp16 matrix cores, one workgroup per 32 heads
+    and chunk for the value side) against the oracle."""
+    wl, ol, dl = llava
+    L = wl.layer
+    lengths = [1, 290, 1000]
+    batch, cap = 3, 1008
+    rows = gen.latent_rows(wl, batch, cap)
+    oc = O.LatentCache(O.CACHE_F16, batch, cap, L.r)
+    for b, n in enumerate(lengths):
+        oc.append(b, rows[b, :n])
+    dc = B.DeviceCache(B.QSVD_CACHE_F16, batch, cap, L.r, lengths)
+    dc.data.copy_(H.dev(oc.data))
+    g = np.random.default_rng(7)
+    q = (g.standard_normal((batch, L.n_q_heads * L.head_dim)) * 2.0).astype(np.float16)
+    for theta in (1.0e4,):
+        H.say(f"decode rope llava7b width theta={theta}")
+        ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, rope_theta=theta)[:, 0, :]
+        for mode in ROPE_MODES:
+            out = H.host(H.decode_attention(dl, dc, H.dev(q), mode, rope_theta=theta))
+            ok, info = H.close_enough(out, ref)
+            H.say(f"  mode={mode} max-abs, rel-L2, rms = {info}")
+            assert ok, (mode, info)
