@@ -1070,3 +1070,27 @@ def test_decode_rope_latent_v_llava7b_width(llava):
             ok, info = H.close_enough(out, ref)
             H.say(f"  mode={mode} max-abs, rel-L2, rms = {info}")
             assert ok, (mode, info)
+
+
+@pytest.mark.parametrize("shape", [(12, 4, 96), (32, 4, 32), (16, 16, 64)], ids=["g3_dh96", "g8_dh32", "mha_dh64"])
+@pytest.mark.parametrize("fmt", [O.CACHE_F16, O.CACHE_I8, O.CACHE_I4], ids=["f16", "i8", "i4"])
+def test_decode_rope_head_dims(shape, fmt):
+    """Rotary decode at the other head dimensions (96, 32, 64: 6, 2 and 4
+    16-byte runs per half row) and group sizes on both sides of the MFMA /
+    fp32 score split (3, 8 and 1 query heads per key/value head), r = 512
+    (64 latent columns per wave in the value half), every cache format,
+    ragged lengths 2 / 77 / 300; both forms against the oracle."""
+    Hq, Hkv, dh = shape
+    L = configs.LayerShape(d=512, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=dh, r=512)
+    ol, dl = _random_factor_layer(L, 900 + dh + Hq)
+    wl = configs.Workload(96, "rope-dims", L, "gaussian", 8, 0, 8, fmt)
+    oc, dc = _prefilled_caches(wl, fmt, [2, 77, 300], 304)
+    g = np.random.default_rng(dh * 7 + Hq)
+    q = (g.standard_normal((3, Hq * dh)) * 4.0).astype(np.float16)
+    ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, rope_theta=1.0e4)[:, 0, :]
+    for mode in ROPE_MODES:
+        H.say(f"decode rope dims Hq={Hq} Hkv={Hkv} dh={dh} fmt={fmt} mode={mode}")
+        out = H.host(H.decode_attention(dl, dc, H.dev(q), mode, rope_theta=1.0e4))
+        ok, info = H.close_enough(out, ref)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (mode, info)
