@@ -44,14 +44,17 @@ struct SkinnyOut {
   int32_t n_seg;
 };
 
+// Selects rather than indexes the segment arrays, so that the argument struct
+// is only ever read at constant offsets (an indexed copy would go to scratch).
 __device__ __forceinline__ void sk_store(const SkinnyOut& so, int64_t m, int32_t n, float y) {
-#pragma unroll
-  for (int s = 0; s < 3; ++s) {
-    if (s < so.n_seg && n >= so.n0[s] && n < so.n0[s] + so.n[s]) {
-      if (so.ptr[s]) so.ptr[s][m * so.ld[s] + (n - so.n0[s])] = to_f16(y);
-      return;
-    }
-  }
+  const bool in0 = so.n_seg > 0 && n >= so.n0[0] && n < so.n0[0] + so.n[0];
+  const bool in1 = !in0 && so.n_seg > 1 && n >= so.n0[1] && n < so.n0[1] + so.n[1];
+  const bool in2 = !in0 && !in1 && so.n_seg > 2 && n >= so.n0[2] && n < so.n0[2] + so.n[2];
+  _Float16* base = in0 ? so.ptr[0] : in1 ? so.ptr[1] : in2 ? so.ptr[2] : nullptr;
+  if (!base) return;
+  const int64_t ld = in0 ? so.ld[0] : in1 ? so.ld[1] : so.ld[2];
+  const int32_t n0 = in0 ? so.n0[0] : in1 ? so.n0[1] : so.n0[2];
+  base[m * ld + (n - n0)] = to_f16(y);
 }
 
 // 16 int4 codes (8 bytes, element 2i in the low nibble of byte i) -> 16 int8.
@@ -228,7 +231,7 @@ skinny_gemm_kernel(const void* __restrict__ a_src, const float* __restrict__ row
     }
 #pragma unroll
     for (int s = 0; s < kSkBatch; ++s) {
-      if (st0 + s >= s1) break;
+      if (st0 + s >= s1) continue;     // (not break: keeps the register arrays statically indexed)
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
         if (rb < rbl) acc[rb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aw[s][rb], bw[s], acc[rb], 0, 0, 0);
