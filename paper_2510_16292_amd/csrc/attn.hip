@@ -87,6 +87,7 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
               int32_t B, int32_t r, int32_t Hq, int32_t Hkv, int32_t dh, int32_t N, int32_t bits,
               int32_t group, float scale, int32_t hp, _Float16* __restrict__ qt) {
   __shared__ __attribute__((aligned(16))) _Float16 wk[128 * kAbsorbLd];
+  __shared__ __attribute__((aligned(16))) _Float16 ot[16 * (kAbsorbJ + 8)];   // output tile, 16 sequences
   const int h = blockIdx.x, lane = threadIdx.x;
   const int32_t jb = blockIdx.y * kAbsorbJ;
   if (h >= Hq) {
@@ -196,14 +197,22 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
         acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(alo, bw, acc[jj], 0, 0, 0);
       }
     }
-    // lane holds column jb + 16*jj + l16 and sequences b0 + 4*quad + v
+    // lane holds column jb + 16*jj + l16 and sequences b0 + 4*quad + v; the
+    // tile goes through LDS so that each sequence row leaves as 16-byte runs
 #pragma unroll
     for (int jj = 0; jj < kAbsorbJ / 16; ++jj)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int b = b0 + 4 * quad + v;
-        if (b < B) qt[((int64_t)b * hp + h) * r + jb + 16 * jj + l16] = (_Float16)(acc[jj][v] * scale);
-      }
+      for (int v = 0; v < 4; ++v)
+        ot[(4 * quad + v) * (kAbsorbJ + 8) + 16 * jj + l16] = (_Float16)(acc[jj][v] * scale);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 16 * kAbsorbJ / 8 / 64; ++i) {
+      const int e = lane + 64 * i, bl = e / (kAbsorbJ / 8), j8 = 8 * (e % (kAbsorbJ / 8));
+      if (b0 + bl < B)
+        *reinterpret_cast<f16x8*>(qt + ((int64_t)(b0 + bl) * hp + h) * r + jb + j8) =
+            *reinterpret_cast<const f16x8*>(ot + bl * (kAbsorbJ + 8) + j8);
+    }
+    __syncthreads();
   }
 }
 
@@ -746,7 +755,7 @@ latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restric
 // each thread streams 8 elements (two heads x 4 columns) of every chunk.
 // ---------------------------------------------------------------------------
 constexpr int kMergeElems = 2048;
-constexpr int kMergeBatch = 8;
+constexpr int kMergeBatch = 16;   // chunk partials in flight per thread (one round trip for <= 16 chunks)
 
 template <int HB>
 __global__ void __launch_bounds__(256)
@@ -787,12 +796,11 @@ merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict
     for (int c = sub; c < nv; c += LPH) wgt[c * HB + h] *= inv;
   }
   __syncthreads();
-  if (!eok) return;
   const int x4 = (int)(e0 / (4 * HB)), h0 = (int)((e0 / 4) % HB);
   float acc[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) acc[k] = 0.f;
-  for (int c0 = 0; c0 < nv; c0 += kMergeBatch) {
+  for (int c0 = 0; eok && c0 < nv; c0 += kMergeBatch) {
     if (c0 > 0) {
 #pragma unroll
       for (int k = 0; k < kMergeBatch; ++k)
@@ -800,7 +808,7 @@ merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict
     }
 #pragma unroll
     for (int k = 0; k < kMergeBatch; ++k) {
-      if (c0 + k >= nv) break;
+      if (c0 + k >= nv) continue;
       const float w0 = wgt[(c0 + k) * HB + h0], w1 = wgt[(c0 + k) * HB + h0 + 1];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -809,12 +817,24 @@ merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict
       }
     }
   }
+  // The workgroup's kMergeElems / HB latent columns of its HB heads go
+  // through LDS, so that each head row leaves as 16-byte runs.
+  constexpr int COLS = kMergeElems / HB, OLD = COLS + 8;
+  __shared__ __attribute__((aligned(16))) _Float16 ot[HB * OLD];
+  const int xl = 4 * x4 - blockIdx.x * COLS;
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh) {
     const f16x4 o4 = {(_Float16)acc[4 * hh], (_Float16)acc[4 * hh + 1], (_Float16)acc[4 * hh + 2],
                       (_Float16)acc[4 * hh + 3]};
-    *reinterpret_cast<f16x4*>(o_lat + ((int64_t)vb * hp + hb * HB + h0 + hh) * r + 4 * x4) = o4;
+    *reinterpret_cast<f16x4*>(ot + (h0 + hh) * OLD + xl) = o4;
   }
+  __syncthreads();
+  static_assert(HB * COLS / 8 == 256, "one 16-byte run per thread");
+  const int hr = tid / (COLS / 8), c8 = 8 * (tid % (COLS / 8));
+  const int col = blockIdx.x * COLS + c8;
+  if (col < r)
+    *reinterpret_cast<f16x8*>(o_lat + ((int64_t)vb * hp + hb * HB + hr) * r + col) =
+        *reinterpret_cast<const f16x8*>(ot + hr * OLD + c8);
 }
 
 // ---------------------------------------------------------------------------

@@ -1094,3 +1094,23 @@ def test_decode_rope_head_dims(shape, fmt):
         ok, info = H.close_enough(out, ref)
         H.say(f"  max-abs, rel-L2, rms = {info}")
         assert ok, (mode, info)
+
+
+@pytest.mark.parametrize("mode", ROPE_MODES, ids=ROPE_MODE_IDS)
+def test_decode_rope_empty_sequence(gqa, mode):
+    """A sequence with nothing cached (length 0) beside ragged ones (33, 70):
+    its output is zeros (no visible position), the others match the oracle;
+    with and without rotary embeddings (the latter in the reconstruct form)."""
+    L, ol, dl = gqa
+    wl, oc, dc = _gqa_cache(L, O.CACHE_I8, [0, 33, 70], 72)
+    g = np.random.default_rng(3)
+    q = (g.standard_normal((3, L.n_q_heads * L.head_dim)) * 4.0).astype(np.float16)
+    for theta in ((None, 1.0e4) if mode == B.QSVD_ATTN_RECONSTRUCT else (1.0e4,)):
+        H.say(f"decode empty sequence theta={theta} mode={mode}")
+        ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, batches=[1, 2],
+                                    rope_theta=theta)[:, 0, :]
+        out = H.host(H.decode_attention(dl, dc, H.dev(q), mode, rope_theta=theta))
+        assert np.array_equal(out[0].view(np.uint16), np.zeros_like(out[0]).view(np.uint16))
+        ok, info = H.close_enough(out[1:], ref[1:])
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (theta, info)
