@@ -1743,9 +1743,12 @@ hipError_t launch_attn_rope_latent(const AttnArgs& a, void* ws, hipStream_t s) {
     KernelScope ks("rope_scores", s);
     const int G = w.n_q_heads / w.n_kv_heads, nch = (len + RCH - 1) / RCH;
     // runs of up to 8 key/value heads share the (cos, sin) registers, as long
-    // as the grid keeps about four workgroups per CU
+    // as the grid keeps about four workgroups per CU and the staged queries
+    // fit the default 64 KB of LDS (one head always does)
     int hpb = std::min(w.n_kv_heads, 8);
-    while (hpb > 1 && (int64_t)nch * c.batch * ((w.n_kv_heads + hpb - 1) / hpb) < 1024) hpb /= 2;
+    while (hpb > 1 && ((int64_t)nch * c.batch * ((w.n_kv_heads + hpb - 1) / hpb) < 1024 ||
+                       rope_scores_lds(w.head_dim, hpb, G) > 65536))
+      hpb /= 2;
     const unsigned runs = (unsigned)((w.n_kv_heads + hpb - 1) / hpb);
     QSVD_LAUNCH(ks, rope_scores_kernel, dim3(nch, c.batch, runs), dim3(256), rope_scores_lds(w.head_dim, hpb, G), s,
                 a.q, khat, c.seq_len, c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, hpb, a.sm_scale * kLog2e,

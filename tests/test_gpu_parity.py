@@ -1072,12 +1072,14 @@ def test_decode_rope_latent_v_llava7b_width(llava):
             assert ok, (mode, info)
 
 
-@pytest.mark.parametrize("shape", [(12, 4, 96), (32, 4, 32), (16, 16, 64)], ids=["g3_dh96", "g8_dh32", "mha_dh64"])
+@pytest.mark.parametrize("shape", [(12, 4, 96), (32, 4, 32), (16, 16, 64), (32, 8, 128)],
+                         ids=["g3_dh96", "g8_dh32", "mha_dh64", "g4_dh128"])
 @pytest.mark.parametrize("fmt", [O.CACHE_F16, O.CACHE_I8, O.CACHE_I4], ids=["f16", "i8", "i4"])
 def test_decode_rope_head_dims(shape, fmt):
     """Rotary decode at the other head dimensions (96, 32, 64: 6, 2 and 4
     16-byte runs per half row) and group sizes on both sides of the MFMA /
-    fp32 score split (3, 8 and 1 query heads per key/value head), r = 512
+    fp32 score split (3, 8, 1 and 4 query heads per key/value head; 32 over 8
+    at dh = 128 stages the most query rows per workgroup), r = 512
     (64 latent columns per wave in the value half), every cache format,
     ragged lengths 2 / 77 / 300; both forms against the oracle."""
     Hq, Hkv, dh = shape
