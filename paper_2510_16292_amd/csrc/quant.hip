@@ -212,10 +212,126 @@ quantize_rotated_kernel(const _Float16* __restrict__ x, int64_t M, int32_t K, in
   }
 }
 
+// The same for K = B = 4096 with one wavefront per row and no workgroup
+// barrier: lane l holds elements 64 l .. 64 l + 63, stages h = 1 .. 32 run in
+// its registers; one transpose through LDS (16.6 KB) gives lane l the
+// elements 64 k + l, k = 0 .. 63, so stages h = 64 .. 2048 run in
+// registers too; then the product by c, the row max (a wave reduction), a
+// transpose back, and the codes of 64 consecutive elements per lane.  Each
+// element sees the same fp32 operations in the same order as above.
+constexpr int kRw = 64;          // elements per lane
+constexpr int kRwLd = kRw + 1;   // LDS words per lane row (odd: no bank conflicts either way)
+
+__device__ __forceinline__ void rw_butterflies(float* v, int hmin, int hmax) {
+#pragma unroll
+  for (int h = 1; h < kRw; h <<= 1) {
+    if (h < hmin || h > hmax) continue;
+#pragma unroll
+    for (int k = 0; k < kRw; ++k)
+      if (!(k & h)) {
+        const float a = v[k], b = v[k + h];
+        v[k] = add_rn(a, b);
+        v[k + h] = add_rn(a, -b);
+      }
+  }
+}
+
+template <int BITS>
+__global__ void __launch_bounds__(64)
+quantize_rotated_w64_kernel(const _Float16* __restrict__ x, int64_t M, int64_t ldx, float clip,
+                            const int8_t* __restrict__ signs, float c, uint8_t* __restrict__ xq,
+                            float* __restrict__ sx) {
+  constexpr int K = kRw * 64;
+  __shared__ float tb[64 * kRwLd];   // [lane][element] of one wave
+  const int lane = threadIdx.x;
+  const int64_t m = blockIdx.x;
+  const _Float16* row = x + m * ldx + kRw * lane;
+  float v[kRw];
+#pragma unroll
+  for (int i = 0; i < kRw / 8; ++i) {
+    const f16x8 t = *reinterpret_cast<const f16x8*>(row + 8 * i);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[8 * i + e] = (float)t[e];
+  }
+  if (signs) {
+#pragma unroll
+    for (int i = 0; i < kRw / 16; ++i) {
+      const uint4 sb = *reinterpret_cast<const uint4*>(signs + kRw * lane + 16 * i);
+      const uint32_t sw[4] = {sb.x, sb.y, sb.z, sb.w};
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if ((int8_t)(sw[e >> 2] >> (8 * (e & 3))) < 0) v[16 * i + e] = -v[16 * i + e];
+    }
+  }
+  rw_butterflies(v, 1, kRw / 2);                  // h = 1 .. 32
+  // transpose: element 64 l + k of lane l -> lane k, register l (one wave:
+  // its LDS accesses execute in order; the empty asm keeps the compiler's)
+#pragma unroll
+  for (int k = 0; k < kRw; ++k) tb[lane * kRwLd + k] = v[k];
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int k = 0; k < kRw; ++k) v[k] = tb[k * kRwLd + lane];
+  asm volatile("" ::: "memory");
+  rw_butterflies(v, 1, kRw / 2);                  // h = 64 .. 2048 (register index bits)
+  float amax = 0.f;
+#pragma unroll
+  for (int k = 0; k < kRw; ++k) {
+    v[k] = mul_rn(v[k], c);
+    amax = fmaxf(amax, fabsf(v[k]));
+  }
+  amax = wave_max(amax);
+  // transpose back: lane l (register k = element 64 k + l) -> lane k, register l
+#pragma unroll
+  for (int k = 0; k < kRw; ++k) tb[k * kRwLd + lane] = v[k];
+  asm volatile("" ::: "memory");
+  float z[kRw];
+#pragma unroll
+  for (int k = 0; k < kRw; ++k) z[k] = tb[lane * kRwLd + k];
+  const float qm = (float)((1 << (BITS - 1)) - 1);
+  const float a = mul_rn(clip, amax);
+  float inv = 0.f, sc = 1.f;
+  if (a != 0.f) {
+    inv = div_rn(qm, a);
+    sc = div_rn(a, qm);
+  }
+  if (lane == 0) sx[m] = sc;
+#pragma unroll
+  for (int i = 0; i < kRw / 16; ++i) {
+    int q[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) q[e] = (a != 0.f) ? quant_code(mul_rn(z[16 * i + e], inv), qm) : 0;
+    if (BITS == 8) {
+      uint32_t w[4];
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+        w[d] = (q[4 * d] & 0xff) | ((q[4 * d + 1] & 0xff) << 8) | ((q[4 * d + 2] & 0xff) << 16) |
+               ((uint32_t)(q[4 * d + 3] & 0xff) << 24);
+      *reinterpret_cast<uint4*>(xq + m * (int64_t)K + kRw * lane + 16 * i) = make_uint4(w[0], w[1], w[2], w[3]);
+    } else {
+      uint32_t w[2] = {0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 16; ++e) w[e >> 3] |= (uint32_t)(q[e] & 0xf) << (4 * (e & 7));
+      *reinterpret_cast<uint2*>(xq + m * (int64_t)(K / 2) + (kRw * lane + 16 * i) / 2) = make_uint2(w[0], w[1]);
+    }
+  }
+}
+
 hipError_t launch_quantize_rotated(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits, float clip,
                                    const int8_t* signs, int32_t block, float c, void* xq, float* sx,
                                    hipStream_t s) {
   if (M == 0) return hipSuccess;
+  // (the one-wave kernel moves 16-byte runs of signs and 8-bit codes)
+  if (K == kRw * 64 && block == K && ldx % 8 == 0 && ((uintptr_t)signs & 15) == 0 &&
+      (bits == 4 || ((uintptr_t)xq & 15) == 0)) {
+    KernelScope ks("quantize_rotated", s);
+    if (bits == 8)
+      QSVD_LAUNCH(ks, quantize_rotated_w64_kernel<8>, dim3((unsigned)M), dim3(64), 0, s, (const _Float16*)x, M, ldx,
+                  clip, signs, c, (uint8_t*)xq, sx);
+    else
+      QSVD_LAUNCH(ks, quantize_rotated_w64_kernel<4>, dim3((unsigned)M), dim3(64), 0, s, (const _Float16*)x, M, ldx,
+                  clip, signs, c, (uint8_t*)xq, sx);
+    return hipGetLastError();
+  }
   const size_t lds = (size_t)(K + K / 8) * sizeof(float);     // with the pad words
   auto kern = bits == 8 ? quantize_rotated_kernel<8> : quantize_rotated_kernel<4>;
   if (lds + 1024 > 64 * 1024) {     // (plus the kernel's static LDS)

@@ -125,6 +125,8 @@ def _rot_cases():
     wl1, wl2, wl4, wl5 = configs.get(1), configs.get(2), configs.get(4), configs.get(5)
     spike = np.zeros((2, 1024), np.float16)
     spike[0, 5], spike[1, 700] = 60000.0, -3.0
+    spike4k = gen.random_rows(11, (3, 4096), 0.5)
+    spike4k[0, 4095], spike4k[1, 0], spike4k[2, 2048] = 60000.0, -60000.0, 1000.0
     return [
         ("tiny-8bit", gen.prefill_activations(wl1), 8, None, 21),
         ("tiny-4bit", gen.prefill_activations(wl1), 4, None, 22),
@@ -136,6 +138,9 @@ def _rot_cases():
         ("K16384-b16384", gen.random_rows(8, (3, 16384), 1.0), 8, None, 28),
         ("no-signs", gen.random_rows(9, (11, 2048), 1.0), 8, None, None),
         ("zero-row-and-spikes", np.concatenate([np.zeros((1, 1024), np.float16), spike]), 8, None, 29),
+        # K = B = 4096 (one wavefront per row): 4-bit codes, no signs with a zero row and spikes
+        ("K4096-4bit", gen.random_rows(10, (9, 4096), 1.5), 4, None, 30),
+        ("K4096-no-signs-zero-spike", np.concatenate([np.zeros((1, 4096), np.float16), spike4k]), 8, None, None),
     ]
 
 
