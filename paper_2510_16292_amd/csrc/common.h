@@ -51,6 +51,33 @@ __device__ __forceinline__ int quant_code(float v, float qm) {
   return (int)t;
 }
 
+// Output-tile order of the GEMM grids.  The chip dispatches workgroup i to
+// XCD i % 8, and each XCD has its own L2.  The ids one XCD receives are made
+// consecutive, and consecutive ids walk a block of gm tile rows column by
+// column, so the tiles that run together on one XCD form a compact
+// gm x (tiles / 8 / gm) block and fetch each operand row block into that L2
+// once.  (A bijection on [0, tiles); gm comes from xcd_group_rows.)
+__device__ __forceinline__ void xcd_tile(int id, int tiles, int tiles_n, int gm, int* tm, int* tn) {
+  if (tiles % 8 == 0) id = (id % 8) * (tiles / 8) + id / 8;
+  const int tiles_m = tiles / tiles_n, per_group = gm * tiles_n, grp = id / per_group, first = grp * gm;
+  const int rows = min(tiles_m - first, gm), in_g = id - grp * per_group;
+  *tm = first + in_g % rows;
+  *tn = in_g / rows;
+}
+
+// Tile rows per group: the block height that minimizes the operand row
+// blocks one XCD touches, gm + (tiles / 8) / gm.
+inline int xcd_group_rows(int64_t tiles_m, int64_t tiles_n) {
+  const double per_xcd = (double)(tiles_m * tiles_n) / 8;
+  int best = (int)tiles_m;
+  double best_cost = 1e300;
+  for (int c = 1; c <= tiles_m; ++c) {
+    const double cost = c + per_xcd / c;
+    if (cost < best_cost) { best_cost = cost; best = c; }
+  }
+  return best;
+}
+
 // Signed int4 from a nibble.
 __device__ __forceinline__ int nib_lo(uint32_t b) { return ((int)(b << 28)) >> 28; }
 __device__ __forceinline__ int nib_hi(uint32_t b) { return ((int)(b << 24)) >> 28; }

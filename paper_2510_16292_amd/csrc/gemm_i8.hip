@@ -110,7 +110,8 @@ template <int BM, int BN, int WM, int WN, int NS, bool DBG, bool F16>
 __global__ void __launch_bounds__((PipeCfg<BM, BN, WM, WN, NS>::kThreads))
 gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
                     const float* __restrict__ rs, const float* __restrict__ cs,
-                    int64_t M, int32_t N, int32_t K, int32_t n_tiles_n, DevSegs sg, int32_t* __restrict__ dbg) {
+                    int64_t M, int32_t N, int32_t K, int32_t n_tiles_n, int32_t gm, DevSegs sg,
+                    int32_t* __restrict__ dbg) {
   using C = PipeCfg<BM, BN, WM, WN, NS>;
   using Acc = std::conditional_t<F16, f32x16, i32x16>;
   static_assert(!(DBG && F16), "accumulator dumps are for the integer products");
@@ -121,7 +122,8 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w / (BN / WN), wn = w % (BN / WN);
   const int l32 = lane & 31, hl = lane >> 5;
-  const int tm = blockIdx.x / n_tiles_n, tn = blockIdx.x % n_tiles_n;
+  int tm, tn;
+  xcd_tile(blockIdx.x, gridDim.x, n_tiles_n, gm, &tm, &tn);
   const int64_t m0 = (int64_t)tm * BM;
   const int32_t n0 = tn * BN;
   const int nk = K / PBK;
@@ -311,7 +313,7 @@ static hipError_t launch_pipe(const GemmArgs& g, const DevSegs& sg, hipStream_t 
   const int32_t kbytes = F16 ? 2 * g.K : g.K;
   KernelScope ks(F16 ? "gemm_f16_pipe" : "gemm_i8_pipe", s);
   QSVD_LAUNCH(ks, kern, dim3((unsigned)(tm * tn)), dim3(C::kThreads), C::kLds, s, g.a, g.b, g.row_scale, g.col_scale,
-                     g.M, g.N, kbytes, tn, sg, g.dbg);
+                     g.M, g.N, kbytes, tn, xcd_group_rows(tm, tn), sg, g.dbg);
   return hipGetLastError();
 }
 

@@ -101,7 +101,7 @@ template <int ABITS, int BBITS, bool GROUPED>
 __global__ void __launch_bounds__(256)
 gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B,
                     const float* __restrict__ rs, const float* __restrict__ cs, int32_t sstride,
-                    int64_t M, int32_t N, int32_t K, int32_t group, int32_t n_tiles_n, Q4Segs sg) {
+                    int64_t M, int32_t N, int32_t K, int32_t group, int32_t n_tiles_n, int32_t gm, Q4Segs sg) {
   constexpr int RBA = QBK * ABITS / 8, RBB = QBK * BBITS / 8;        // stage row bytes
   constexpr int SA = QBM * RBA, SB = QBN * RBB, STAGE = SA + SB;
   constexpr int LPW = STAGE / 1024 / 4;                               // direct loads per wave per stage
@@ -115,7 +115,8 @@ gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w >> 1, wn = w & 1;
   const int l32 = lane & 31, hl = lane >> 5;
-  const int tm = blockIdx.x / n_tiles_n, tn = blockIdx.x % n_tiles_n;
+  int tm, tn;
+  xcd_tile(blockIdx.x, gridDim.x, n_tiles_n, gm, &tm, &tn);
   const int64_t m0 = (int64_t)tm * QBM;
   const int32_t n0 = tn * QBN;
   const int nk = K / QBK;
@@ -301,7 +302,7 @@ static hipError_t launch_q4(const GemmArgs& g, const Q4Segs& sg, int32_t group, 
   const int64_t tm = (g.M + QBM - 1) / QBM;
   KernelScope ks("gemm_q4_pipe", s);
   QSVD_LAUNCH(ks, kern, dim3((unsigned)(tm * tn)), dim3(256), lds, s, (const uint8_t*)g.a, (const uint8_t*)g.b,
-              g.row_scale, g.col_scale, sstride, g.M, g.N, g.K, group, tn, sg);
+              g.row_scale, g.col_scale, sstride, g.M, g.N, g.K, group, tn, xcd_group_rows(tm, tn), sg);
   return hipGetLastError();
 }
 
