@@ -274,11 +274,6 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   constexpr bool F16C = FMT == QSVD_CACHE_F16;
   auto kcol = [](int ks, int hf) { return F16C ? 16 * ks + 8 * hf : 32 * (ks >> 1) + 16 * hf + 8 * (ks & 1); };
   f16x8 qf[KS];
-  if constexpr (!PRE) {
-    const _Float16* qrow = qt + ((int64_t)vb * kHeadBlk + l32) * r + slice0;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, half));
-  }
   f32x16 o[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) o[rb] = f32x16{};
@@ -322,6 +317,13 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   // and feed the score product directly.
   constexpr bool kStageFirst = F16C || RW >= 192;
   load_tile(t_begin);
+  // the query slice is read after the first tile's loads are out (it is an
+  // L2 hit, the tile comes from HBM)
+  if constexpr (!PRE) {
+    const _Float16* qrow = qt + ((int64_t)vb * kHeadBlk + l32) * r + slice0;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, half));
+  }
   for (int t0 = t_begin; t0 < t_end; t0 += 32) {
     f32x16 sacc = f32x16{};
     float s[16];
@@ -524,6 +526,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     ml_part[part * 64 + 32 + l32] = l_run;
   }
   // O^T / l as fp16 (a weighted mean of latent rows, so it stays in range),
+  // stored non-temporally (the merge reads it once, in another kernel),
   // stored in accumulator order [x/4][head][4]: lane (head l32, half) holds
   // latent columns slice0 + 32*rb + 8*vq + 4*half .. +3 in o[rb][4*vq ..],
   // so each store instruction writes 512 contiguous bytes.
@@ -536,7 +539,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
       const int x4 = (slice0 + 32 * rb + 8 * vq + 4 * half) >> 2;
       const f16x4 v4 = {(_Float16)(o[rb][4 * vq] * inv_l), (_Float16)(o[rb][4 * vq + 1] * inv_l),
                         (_Float16)(o[rb][4 * vq + 2] * inv_l), (_Float16)(o[rb][4 * vq + 3] * inv_l)};
-      *reinterpret_cast<f16x4*>(op + ((int64_t)x4 * kHeadBlk + l32) * 4) = v4;
+      __builtin_nontemporal_store(v4, reinterpret_cast<f16x4*>(op + ((int64_t)x4 * kHeadBlk + l32) * 4));
     }
 }
 
@@ -729,7 +732,7 @@ latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restric
   }
   // O^T / l as fp16 in [x/4][16 heads][4] order: lane (head l16, g) holds
   // latent columns slice0 + 16rb + 4g .. +3, so each store writes 512
-  // contiguous bytes.
+  // contiguous bytes; non-temporal, as in the 32-head kernel.
   const float inv_l = l_run > 0.f ? 1.f / l_run : 0.f;
   _Float16* op = o_part + part * (int64_t)r * 16;
 #pragma unroll
@@ -738,7 +741,7 @@ latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restric
     const int x4 = (slice0 + 16 * rb + 4 * g) >> 2;
     const f16x4 v4 = {(_Float16)(o[rb][0] * inv_l), (_Float16)(o[rb][1] * inv_l), (_Float16)(o[rb][2] * inv_l),
                       (_Float16)(o[rb][3] * inv_l)};
-    *reinterpret_cast<f16x4*>(op + ((int64_t)x4 * 16 + l16) * 4) = v4;
+    __builtin_nontemporal_store(v4, reinterpret_cast<f16x4*>(op + ((int64_t)x4 * 16 + l16) * 4));
   }
 }
 
