@@ -268,6 +268,8 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
         __builtin_amdgcn_sched_barrier(0);
       }
   }
+  // Output rows leave non-temporally: the tile is written once and read by
+  // a later kernel, so it need not displace the operands in L2.
   constexpr int CPR = WN / 8;                   // 16-byte chunks per staged row
   for (int e = lane; e < WM * CPR; e += 64) {
     const int row = e / CPR, c8 = e % CPR;
@@ -275,7 +277,7 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
     const int32_t n = n0 + wn * WN + 8 * c8;
     if (m >= M || n >= N) continue;
     const ColOut co = col_out(sg, n);
-    if (co.p) *reinterpret_cast<f16x8*>(co.p + m * co.ld) = *reinterpret_cast<const f16x8*>(ost + row * OST + 8 * c8);
+    if (co.p) __builtin_nontemporal_store(*reinterpret_cast<const f16x8*>(ost + row * OST + 8 * c8), reinterpret_cast<f16x8*>(co.p + m * co.ld));
   }
 }
 

@@ -286,7 +286,7 @@ gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B
     if (m >= M || n >= N) continue;
     int64_t ld;
     _Float16* p = q4_col(sg, n, &ld);
-    if (p) *reinterpret_cast<f16x8*>(p + m * ld) = *reinterpret_cast<const f16x8*>(ost + row * OST + 8 * c8);
+    if (p) __builtin_nontemporal_store(*reinterpret_cast<const f16x8*>(ost + row * OST + 8 * c8), reinterpret_cast<f16x8*>(p + m * ld));
   }
 }
 
