@@ -37,6 +37,7 @@ DECODE_BATCH, CTX0, DECODE_VISITS = 16, 4096, 256
 GQA_VISITS = 8                 # visits per layer in the GQA decode leg
 # hardware-counter summary of the latent attention kernel on this workload
 ATTN_TRAFFIC_SUMMARY = "latent_attn_llava7b_decode_traffic.txt"
+GEMM_TRAFFIC_SUMMARY = "gemm_i8_llava7b_prefill_traffic.txt"
 
 
 def parse():
@@ -408,11 +409,13 @@ def bench_prefill(args, wl2, host_layer):
                        "frac": round(qbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
     call_s = (t1 - t0) / args.prefill_steps
     tops = ops / gemm_s / 1e12
+    # HBM bytes of one call's two products (both launches), from the committed counter summary
+    traffic = counted_traffic(GEMM_TRAFFIC_SUMMARY) if (M, d, r, L.N) == (2560, 4096, 1536, 12288) else None
     return {"value": round(tops, 1), "unit": "TOPS", "ms_per_call": round(call_s * 1e3, 4),
             "gemm_ms_per_call": round(gemm_s * 1e3, 4), "call_tops": round(ops / call_s / 1e12, 1),
             "tokens": M, "gop_per_call": round(ops / 1e9, 2), "quantizer": quant,
             "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
-                         "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None,
+                         "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None if traffic is None else int(traffic),
                          "kernel": "gemm_i8 (X W^d and Q(C) W^u)", "launches": n}}
 
 
