@@ -100,7 +100,7 @@ KernelScope::KernelScope(const char* name, hipStream_t) : slot_(-1), used_(false
   ProfRec r{name, nullptr, nullptr, false};
   if (hipEventCreate(&r.start) != hipSuccess) return;
   if (hipEventCreate(&r.stop) != hipSuccess) {
-    hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.start);
     return;
   }
   start_ = r.start;
@@ -317,7 +317,7 @@ static qsvd_status decode_attention(const qsvd_layer* w, const qsvd_cache* c, co
   if (!(sm_scale >= 0.f) || isinf(sm_scale)) return fail(QSVD_ERR_INVALID_ARG, "sm_scale must be finite and >= 0");
   if (q_len < 1) return fail(QSVD_ERR_INVALID_ARG, "q_len must be >= 1");
   if ((int64_t)c->batch * q_len > kMaxQueryRows)
-    return fail(QSVD_ERR_UNSUPPORTED, "batch * q_len must be at most %d", kMaxQueryRows);
+    return fail(QSVD_ERR_UNSUPPORTED, "batch * q_len must be at most %d", (int)kMaxQueryRows);
   if (c->max_len < q_len) return fail(QSVD_ERR_INVALID_ARG, "cache holds %d tokens, fewer than q_len %d", c->max_len, q_len);
   if (w->n_q_heads > 64) return fail(QSVD_ERR_UNSUPPORTED, "at most 64 query heads");
   if (w->head_dim % 32 || w->head_dim > 128) return fail(QSVD_ERR_UNSUPPORTED, "head_dim must be 32, 64, 96 or 128");
@@ -335,7 +335,7 @@ static qsvd_status decode_attention(const qsvd_layer* w, const qsvd_cache* c, co
                                            : "absorbed form needs r in {128, 512, 1024, 1536} or a multiple of 128 up to 3072");
   const bool absorbed = mode == QSVD_ATTN_ABSORBED || (mode == QSVD_ATTN_AUTO && abs_ok);
   if (absorbed && absorbed_grid_rows(*w, *c, q_len) > kMaxQueryRows)
-    return fail(QSVD_ERR_UNSUPPORTED, "batch * q_len * head blocks must be at most %d", kMaxQueryRows);
+    return fail(QSVD_ERR_UNSUPPORTED, "batch * q_len * head blocks must be at most %d", (int)kMaxQueryRows);
   if ((!absorbed || rope) && q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct-side forms take q_len 1 only");
   if (!absorbed && w->n_q_heads > 32) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form takes at most 32 query heads");
   if (!absorbed && c->capacity > 16384)
@@ -374,8 +374,8 @@ qsvd_status qsvd_profile_enable(int32_t on, const char* filter) {
 qsvd_status qsvd_profile_reset(void) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   for (auto& r : g_prof) {
-    hipEventDestroy(r.start);
-    hipEventDestroy(r.stop);
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
   }
   g_prof.clear();
   return QSVD_OK;
