@@ -38,6 +38,8 @@ GQA_VISITS = 8                 # visits per layer in the GQA decode leg
 # hardware-counter summary of the latent attention kernel on this workload
 ATTN_TRAFFIC_SUMMARY = "latent_attn_llava7b_decode_traffic.txt"
 GEMM_TRAFFIC_SUMMARY = "gemm_i8_llava7b_prefill_traffic.txt"
+GQA_TRAFFIC_SUMMARY = "latent_attn_qwen2vl_gqa_decode_traffic.txt"
+STACK_TRAFFIC_SUMMARY = "latent_attn_h16_13b_stack_decode_traffic.txt"
 CPU_SAMPLE_S = 10.0          # seconds of oracle work per CPU baseline sample
 
 
@@ -329,7 +331,7 @@ def bench_decode_gqa(args):
     _, host = layer_weights(wl4, wl4.w_bits, wl4.w_group)
     steps = wl4.n_layers * GQA_VISITS
     res = run_decode(wl4, host, B.QSVD_CACHE_I8, wl4.n_layers, wl4.decode_batch, wl4.decode_ctx, steps,
-                     wl4.n_layers, "auto", not args.no_profile, None, True, not args.no_graph)
+                     wl4.n_layers, "auto", not args.no_profile, GQA_TRAFFIC_SUMMARY, True, not args.no_graph)
     out = {"value": round(res["tokens_per_s"], 1), "unit": "tokens/s", "ms_per_step": round(res["ms_per_step"], 5),
            "steps": steps,
            "workload": f"qwen2-vl-7b-shaped GQA layer decode: batch {wl4.decode_batch}, int8 latent cache r=1024 "
@@ -581,8 +583,10 @@ def bench_stack_decode(args, wl5, ranks, layers):
     if n:
         res["attn_kernel_us"] = round(kms * 1e-3 / n * 1e6, 2)
         achieved = attn_bytes / (kms * 1e-3) / 1e9
+        traffic = counted_traffic(STACK_TRAFFIC_SUMMARY)
         res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                           "frac": round(achieved / HBM_PEAK_GBS, 4),
+                           "traffic": None if traffic is None else int(traffic),
                            "kernel": "latent_attn_h16_kernel (int4 cache)", "launches": n,
                            "bytes_per_launch": int(attn_bytes / n)}
     if args.no_graph:

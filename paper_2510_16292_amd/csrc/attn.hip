@@ -581,10 +581,26 @@ latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restric
   f32x4* ssum = spart + NW * 64;
 
   const int n_hb = hp >> 4;
-  const int row = blockIdx.y, vb = row / n_hb, hb = row - vb * n_hb;
+  // Workgroup -> (sequence-query row vb, head block hb, chunk ch).  The n_hb
+  // head blocks of one (vb, ch) read the same cache rows, so they get ids
+  // that one XCD receives together (the chip dispatches the i-th workgroup,
+  // x fastest, to XCD i % 8) and share its L2 instead of each XCD fetching
+  // the rows again.  A bijection on the grid.
+  const int n_launch = gridDim.x, pairs = gridDim.x * gridDim.y / n_hb;
+  const int lin = blockIdx.y * gridDim.x + blockIdx.x;
+  int pair, hb;
+  if (pairs % 8 == 0) {
+    const int j = lin >> 3;
+    pair = (lin & 7) * (pairs >> 3) + j / n_hb;
+    hb = j % n_hb;
+  } else {
+    pair = lin / n_hb;
+    hb = lin % n_hb;
+  }
+  const int vb = pair / n_launch, ch = pair % n_launch, row = vb * n_hb + hb;
   const int b = vb / q_len, qi = vb - b * q_len;
   const int L = min(seq_len[b], capacity) - (q_len - 1 - qi);
-  const int ch = blockIdx.x, t_begin = ch * chunk;
+  const int t_begin = ch * chunk;
   if (t_begin >= L) return;
   const int t_end = min(L, t_begin + chunk);
   // this wave's latent units [u0, u0 + nu) of 128 columns (nu <= UMAX, may be 0)
