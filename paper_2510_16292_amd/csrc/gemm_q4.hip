@@ -241,12 +241,19 @@ gemm_q4_pipe_kernel(const uint8_t* __restrict__ A, const uint8_t* __restrict__ B
       if ((kt + 1) % gsteps == 0) {
         // group g = (kt + 1) / gsteps - 1 ends here: fold it, fetch the next group's scales
         const int gn = (kt + 1) / gsteps;
+        // (float)acc * (s_g 2^-SH) is the same real number as
+        // (float)(acc >> SH) * s_g (acc is an exact multiple of 2^SH below
+        // 2^24, and scaling s_g by a power of two is exact), so it rounds the
+        // same; the shift is saved on every element
+        float gss[TJ];
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) gss[j] = mul_rn(gsc[j], 1.f / (float)(1 << SH));
 #pragma unroll
         for (int i = 0; i < TI; ++i)
 #pragma unroll
           for (int j = 0; j < TJ; ++j) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) S[i][j][v] = add_rn(S[i][j][v], mul_rn((float)(acc[i][j][v] >> SH), gsc[j]));
+            for (int v = 0; v < 16; ++v) S[i][j][v] = add_rn(S[i][j][v], mul_rn((float)acc[i][j][v], gss[j]));
             acc[i][j] = i32x16{};
           }
         if (gn * gsteps < nk) {
