@@ -379,13 +379,14 @@ def test_prefill_bitexact_llava7b_full(llava):
     _check_prefill(ol, got, X)
 
 
-@pytest.mark.parametrize("M", [2560, 2688], ids=["m2560", "m2688"])
+@pytest.mark.parametrize("M", [2560, 2688, 2601], ids=["m2560", "m2688", "m2601"])
 def test_prefill_bitexact_llava7b_production_tiles(llava, M):
     """The launch configuration the bench times: without accumulator dumps the
     up-projection (N=12288) runs on the 256 x 256-tile kernel in the per-XCD
     tile order.  M=2560 is the 4 x 640-token prefill (480 tiles, 60 per XCD);
     M=2688 adds a ragged last tile row (11 rows of tiles) and a last group of
-    3 tile rows after the 8-row groups."""
+    3 tile rows after the 8-row groups; M=2601 ends on a one-row tile row
+    (loads clamped to the last row, stores masked)."""
     wl, ol, dl = llava
     X = gen.prefill_activations(configs.get(2), rows=M)
     H.say(f"prefill llava7b production tiles M={M}")
