@@ -40,7 +40,8 @@ ATTN_TRAFFIC_SUMMARY = "latent_attn_llava7b_decode_traffic.txt"
 GEMM_TRAFFIC_SUMMARY = "gemm_i8_llava7b_prefill_traffic.txt"
 GQA_TRAFFIC_SUMMARY = "latent_attn_qwen2vl_gqa_decode_traffic.txt"
 STACK_TRAFFIC_SUMMARY = "latent_attn_h16_13b_stack_decode_traffic.txt"
-CPU_SAMPLE_S = 10.0          # seconds of oracle work per CPU baseline sample
+STACK_GEMM_TRAFFIC_SUMMARY = "gemm_q4_13b_stack_prefill_traffic.txt"
+CPU_SAMPLE_S = 8.0           # seconds of oracle work per headline CPU baseline sample
 
 
 def parse():
@@ -112,6 +113,30 @@ def cpu_threads():
     except Exception:
         n = 1
     return int(n)
+
+
+def cpu_host():
+    """What the oracle's host offers: logical CPUs, the CPUs this process may
+    run on, and the BLAS threading (library, threads, environment)."""
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [f"{i.get('internal_api')} {i.get('num_threads')} threads" for i in threadpool_info()
+                if i.get("user_api") == "blas"]
+    except Exception:
+        blas = []
+    env = {k: os.environ[k] for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")
+           if k in os.environ}
+    return {"os_cpu_count": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)), "blas": blas, "blas_env": env}
+
+
+def timed_sample(fn, budget_s, max_iters):
+    """Run fn(i) for i = 0, 1, ... until about budget_s seconds (at least once)."""
+    n = 0
+    t0 = time.perf_counter()
+    while n < max_iters and (n == 0 or time.perf_counter() - t0 < budget_s):
+        fn(n)
+        n += 1
+    return n, time.perf_counter() - t0
 
 
 def layer_weights(wl, w_bits=8, w_group=0):
@@ -247,8 +272,10 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
     t1 = time.perf_counter()
     B.profile_enable(False)
     ms_step = (t1 - t0) * 1e3 / max(steps, 1)
+    # contexts the timed attention launches read: one more per visit of a layer
     res = dict(ms_per_step=ms_step, tokens_per_s=batch * steps / (t1 - t0),
-               mean_context=ctx_read / max(steps, 1) / batch)
+               mean_context=ctx_read / max(steps, 1) / batch,
+               ctx_range=(ctx0 + 1, ctx0 + -(-steps // n_layers)))
     if profile:
         kms, n = B.profile_read(attn_name)
         B.profile_reset()
@@ -335,7 +362,7 @@ def bench_decode_gqa(args):
     out = {"value": round(res["tokens_per_s"], 1), "unit": "tokens/s", "ms_per_step": round(res["ms_per_step"], 5),
            "steps": steps,
            "workload": f"qwen2-vl-7b-shaped GQA layer decode: batch {wl4.decode_batch}, int8 latent cache r=1024 "
-                       f"with per-token scales, context {wl4.decode_ctx}->{wl4.decode_ctx + GQA_VISITS}, "
+                       f"with per-token scales, context {res['ctx_range'][0]}..{res['ctx_range'][1]} after the append, "
                        f"W4A8 (int4 per-group-128 weights), {wl4.n_layers} rotated layers; tokens/s per layer step",
            "mean_context": round(res["mean_context"], 1),
            "graph_replay": graph_line(res),
@@ -377,7 +404,7 @@ def bench_prefill(args, wl2, host_layer):
     for _ in range(3):
         call()
     B.profile_reset()
-    B.profile_enable(True, "gemm_i8")
+    B.profile_enable(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.prefill_steps):
@@ -386,9 +413,12 @@ def bench_prefill(args, wl2, host_layer):
     t1 = time.perf_counter()
     B.profile_enable(False)
     gms, n = B.profile_read("gemm_i8")
+    qms, qn = B.profile_read("latent_quant")
     B.profile_reset()
     ops = 2.0 * M * (d * r + r * L.N)            # X W^d then Q(C) W^u, multiply-adds counted twice
     gemm_s = gms * 1e-3 / args.prefill_steps
+    # the projection proper: both products and the latent quantization Q(C) between them
+    proj_s = (gms + qms) * 1e-3 / args.prefill_steps
     # the activation quantizer alone, plain and with the online H1 rotation
     # (block Walsh-Hadamard of order 4096 with seeded signs): fp16 in, int8 + scale out
     signs = torch.from_numpy(np.where(np.arange(d) % 3 == 0, -1, 1).astype(np.int8)).cuda()
@@ -411,15 +441,18 @@ def bench_prefill(args, wl2, host_layer):
         quant[name] = {"us": round(us, 2), "GB/s": round(qbytes / (us * 1e-6) / 1e9, 1),
                        "frac": round(qbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
     call_s = (t1 - t0) / args.prefill_steps
-    tops = ops / gemm_s / 1e12
+    tops = ops / proj_s / 1e12
     # HBM bytes of one call's two products (both launches), from the committed counter summary
     traffic = counted_traffic(GEMM_TRAFFIC_SUMMARY) if (M, d, r, L.N) == (2560, 4096, 1536, 12288) else None
     return {"value": round(tops, 1), "unit": "TOPS", "ms_per_call": round(call_s * 1e3, 4),
-            "gemm_ms_per_call": round(gemm_s * 1e3, 4), "call_tops": round(ops / call_s / 1e12, 1),
+            "kernels_ms_per_call": round(proj_s * 1e3, 4), "gemm_ms_per_call": round(gemm_s * 1e3, 4),
+            "latent_quant_ms_per_call": round(qms / args.prefill_steps, 4),
+            "gemm_only_tops": round(ops / gemm_s / 1e12, 1), "call_tops": round(ops / call_s / 1e12, 1),
             "tokens": M, "gop_per_call": round(ops / 1e9, 2), "quantizer": quant,
             "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
                          "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None if traffic is None else int(traffic),
-                         "kernel": "gemm_i8 (X W^d and Q(C) W^u)", "launches": n}}
+                         "kernel": "gemm_i8 (X W^d, Q(C) W^u) + latent quantization Q(C)",
+                         "launches": n + qn}}
 
 
 def stack_layers(wl5):
@@ -474,7 +507,7 @@ def bench_stack_prefill(args, wl5, ranks, layers):
     stack_pass()
     torch.cuda.synchronize()
     B.profile_reset()
-    B.profile_enable(True, "gemm")
+    B.profile_enable(True)
     t0 = time.perf_counter()
     for _ in range(args.stack_passes):
         stack_pass()
@@ -482,18 +515,23 @@ def bench_stack_prefill(args, wl5, ranks, layers):
     t1 = time.perf_counter()
     B.profile_enable(False)
     gms, n = B.profile_read("gemm")
+    qms, qn = B.profile_read("latent_quant")
     B.profile_reset()
     ops = sum(2.0 * M * r * (d + L.N) for r in ranks)
     gemm_s = gms * 1e-3 / args.stack_passes
+    proj_s = (gms + qms) * 1e-3 / args.stack_passes
     pass_s = (t1 - t0) / args.stack_passes
-    tops = ops / gemm_s / 1e12
+    tops = ops / proj_s / 1e12
     del xs, xq, c_h, cq, q, k, v
+    traffic = counted_traffic(STACK_GEMM_TRAFFIC_SUMMARY)
     return {"value": round(tops, 1), "unit": "TOPS", "ms_per_pass": round(pass_s * 1e3, 3),
-            "gemm_ms_per_pass": round(gemm_s * 1e3, 3), "call_tops": round(ops / pass_s / 1e12, 1),
+            "kernels_ms_per_pass": round(proj_s * 1e3, 3), "gemm_ms_per_pass": round(gemm_s * 1e3, 3),
+            "gemm_only_tops": round(ops / gemm_s / 1e12, 1), "call_tops": round(ops / pass_s / 1e12, 1),
             "tokens": M, "layers": len(ranks), "top_per_pass": round(ops / 1e12, 3),
             "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
-                         "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None,
-                         "kernel": "gemm_q4_pipe (X W^d and Q(C) W^u, int4 x int4)", "launches": n}}
+                         "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None if traffic is None else int(traffic),
+                         "kernel": "gemm_q4_pipe (X W^d and Q(C) W^u, int4 x int4) + latent quantization Q(C)",
+                         "launches": n + qn}}
 
 
 def bench_stack_decode(args, wl5, ranks, layers):
@@ -655,7 +693,7 @@ def cpu_baseline_decode(wl, factors):
     dt = time.perf_counter() - t0
     return {"value": round(n_seq * steps / dt, 2), "unit": "tokens/s", "cores": cpu_threads(), "kind": "oracle",
             "sample": f"{steps} decode step{'s' if steps != 1 else ''} of all {n_seq} sequences from context {CTX0} (fp64 plain form), "
-                      f"{dt:.1f} s"}
+                      f"{dt:.1f} s", "host": cpu_host()}
 
 
 def cpu_baseline_prefill(wl2, factors):
@@ -678,7 +716,94 @@ def cpu_baseline_prefill(wl2, factors):
     dt = time.perf_counter() - t0
     ops = 2.0 * tokens * (L.d * L.r + L.r * L.N)
     return {"value": round(ops / dt / 1e12, 4), "unit": "TOPS", "cores": cpu_threads(), "kind": "oracle",
-            "sample": f"{calls} prefill{'s' if calls != 1 else ''} of 640-token sequences of the 4 x 640 batch, {dt:.1f} s"}
+            "sample": f"{calls} prefill{'s' if calls != 1 else ''} of 640-token sequences of the 4 x 640 batch, {dt:.1f} s",
+            "host": cpu_host()}
+
+
+def cpu_baseline_other(factors2):
+    """Further oracle samples (the oracle as it stands, each a few seconds):
+    single-threaded tiny layer and LLaVA-7B-shaped prefill, the one-off
+    rebuild of K and V for the 4096 cached tokens of one sequence, and decode
+    steps / prefills of the Qwen2-VL-shaped and 13B-shaped layers on a subset
+    of their sequences, each scaled to its unit."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import qsvd_oracle as O
+    from workloads import configs, gen
+    out = {}
+    # tiny layer, end to end (64-token prefill, append, 16 decode steps), one thread
+    wl1 = configs.get(1)
+    L1 = wl1.layer
+    A1, B1 = O.factors_from_weight(gen.weight_matrix(wl1), L1.r, wl1.beta)
+    ol1 = O.make_layer(A1, B1, L1.n_q_heads, L1.n_kv_heads, L1.head_dim, 8, 0)
+    X1 = gen.prefill_activations(wl1)
+
+    def tiny(_):
+        c = O.LatentCache(O.CACHE_F16, 1, 64 + 16, L1.r)
+        O.cache_append_prefill(c, O.prefill(ol1, X1, 8), [64])
+        for t in range(16):
+            O.decode_step(ol1, c, gen.decode_activations(wl1, t), 8)
+    with threadpool_limits(1):
+        n, dt = timed_sample(tiny, 3.0, 50)
+    out["tiny_end_to_end_1thread"] = {"value": round(16 * n / dt, 2), "unit": "decode tokens/s", "cores": 1,
+                                      "sample": f"{n} runs of prefill (64 tokens) + 16 decode steps, {dt:.1f} s"}
+    # LLaVA-7B-shaped prefill of one 640-token sequence, one thread
+    wl2 = configs.get(2)
+    L2 = wl2.layer
+    U, sg, V = factors2
+    A2, B2 = O.split_beta(U, sg, V.T, wl2.beta)
+    ol2 = O.make_layer(A2, B2, L2.n_q_heads, L2.n_kv_heads, L2.head_dim, 8, 0)
+    X2 = gen.prefill_activations(wl2)[:640]
+    with threadpool_limits(1):
+        n, dt = timed_sample(lambda i: O.prefill(ol2, X2, 8), 4.0, 20)
+    ops = 2.0 * 640 * n * (L2.d * L2.r + L2.r * L2.N)
+    out["llava7b_prefill_1thread"] = {"value": round(ops / dt / 1e12, 4), "unit": "TOPS", "cores": 1,
+                                      "sample": f"{n} prefills of one 640-token sequence, {dt:.1f} s"}
+    # the one-off rebuild K^, V^ = C W^u_k,v of one sequence's 4096 cached rows (fp64)
+    rows = gen.latent_rows(configs.get(3), 1, CTX0)[0].astype(np.float64)
+    Bh = ol2.B_hat()[:, L2.n_q:]
+    n, dt = timed_sample(lambda i: rows @ Bh, 4.0, 10)
+    out["llava7b_kv_rebuild"] = {"value": round(dt / n * DECODE_BATCH * 1e3, 1), "unit": "ms for 16 x 4096 tokens",
+                                 "cores": cpu_threads(),
+                                 "sample": f"{n} rebuilds of one sequence's {CTX0} rows, x{DECODE_BATCH} sequences"}
+    # Qwen2-VL-shaped decode: 2 of the 32 sequences at context 8192 (int8 cache), scaled to 32
+    wl4 = configs.get(4)
+    L4 = wl4.layer
+    U4, s4, V4 = gen.weight_factors(wl4)
+    A4, B4 = O.split_beta(U4, s4, V4.T, wl4.beta)
+    ol4 = O.make_layer(A4, B4, L4.n_q_heads, L4.n_kv_heads, L4.head_dim, 4, 128)
+    c4 = O.LatentCache(O.CACHE_I8, 2, wl4.decode_ctx + 8, L4.r)
+    lat = gen.latent_rows(wl4, 2, wl4.decode_ctx)
+    for b in range(2):
+        q8, sc8 = O.quantize_act(lat[b], 8)
+        c4.append(b, None, q8, sc8)
+    n, dt = timed_sample(lambda i: O.decode_step(ol4, c4, gen.decode_activations(wl4, i, batch=2), 8), 4.0, 8)
+    out["qwen2vl_gqa_decode"] = {"value": round(2 * n / dt, 2), "unit": "tokens/s", "cores": cpu_threads(),
+                                 "sample": f"{n} decode steps of 2 sequences from context {wl4.decode_ctx} (int8 "
+                                           f"cache, W4A8); the batch of {wl4.decode_batch} takes "
+                                           f"{wl4.decode_batch // 2}x as long per step"}
+    # 13B-shaped layer at rank 2048 (W4A4, int4 cache): one 704-token prefill, and
+    # decode steps of one of the 8 sequences at context 4096
+    wl5 = gen.with_rank(configs.get(5), 2048)
+    L5 = wl5.layer
+    g = np.random.default_rng(5)
+    A5 = g.standard_normal((L5.d, L5.r)) / np.sqrt(L5.d)
+    B5 = g.standard_normal((L5.r, L5.N)) / np.sqrt(L5.r)
+    ol5 = O.make_layer(A5, B5, L5.n_q_heads, L5.n_kv_heads, L5.head_dim, 4, 128)
+    X5 = gen.prefill_activations(wl5, rows=704)
+    n, dt = timed_sample(lambda i: O.prefill(ol5, X5, 4), 4.0, 10)
+    ops = 2.0 * 704 * n * L5.r * (L5.d + L5.N)
+    out["stack13b_layer_prefill"] = {"value": round(ops / dt / 1e12, 4), "unit": "TOPS", "cores": cpu_threads(),
+                                     "sample": f"{n} prefills of one 704-token sequence through one layer at r=2048"}
+    c5 = O.LatentCache(O.CACHE_I4, 1, wl5.decode_ctx + 8, L5.r)
+    q4, sc4 = O.quantize_act(gen.latent_rows(wl5, 1, wl5.decode_ctx)[0], 4)
+    c5.append(0, None, q4, sc4)
+    n, dt = timed_sample(lambda i: O.decode_step(ol5, c5, gen.decode_activations(wl5, i, batch=1), 4), 4.0, 8)
+    out["stack13b_layer_decode"] = {"value": round(n / dt, 2), "unit": "tokens/s per layer", "cores": cpu_threads(),
+                                    "sample": f"{n} decode steps of 1 sequence from context {wl5.decode_ctx} through "
+                                              "one layer at r=2048 (int4 cache); 40 layers and 8 sequences take "
+                                              "320x as long per token"}
+    return out
 
 
 def main():
@@ -733,8 +858,8 @@ def main():
         "dtype": "i8+f16",
         "data": "synthetic",
         "config": {"workload": "llava-1.5-7b-shaped attention layer decode: batch 16, fp16 latent cache r=1536, "
-                               f"context {CTX0}->{CTX0 + DECODE_VISITS}, W8A8 projections, 32 rotated layers; "
-                               "value is tokens/s per layer step",
+                               f"context {dec['ctx_range'][0]}..{dec['ctx_range'][1]} after the append, W8A8 "
+                               "projections, 32 rotated layers; value is tokens/s per layer step",
                    "d": 4096, "heads": 32, "head_dim": 128, "rank": 1536, "batch": DECODE_BATCH,
                    "mean_context": round(dec["mean_context"], 1), "attention": args.mode},
         "roofline": dec.get("roofline"),
@@ -754,6 +879,7 @@ def main():
         line["cpu_baseline"] = cpu_baseline_decode(wl3, factors)
         if pre is not None:
             line["prefill"]["cpu_baseline"] = cpu_baseline_prefill(wl2, factors)
+        line["cpu_baseline"]["other_samples"] = cpu_baseline_other(factors)
     print(json.dumps(line), flush=True)
 
 

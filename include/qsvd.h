@@ -93,6 +93,10 @@ typedef struct {
   int32_t* seq_len;    /* device [batch] */
   int32_t  max_len;    /* host: an upper bound of every seq_len[b]; the caller sets
                           it when initialising seq_len, append advances it */
+  int32_t* overflow;   /* device, optional (NULL: not reported): an append that finds
+                          seq_len[b] + n_new > capacity on the device (possible only
+                          when the host check was bypassed, e.g. by a graph replay)
+                          stores 1 here; the caller clears it */
 } qsvd_cache;
 
 /* Per-token symmetric activation quantization (Section 4 setup; Q(.) of Eq. 12).
@@ -162,7 +166,10 @@ size_t qsvd_prefill_workspace_size(const qsvd_layer* w, int64_t M, uint32_t out_
  *   I8 / I4:   cq   device int8 [..][r] / int4 [..][r/2], sc device fp32 [..]
  * Row i of sequence b goes to position seq_len[b] + i; then seq_len[b] += n_new
  * on the device and c->max_len += n_new on the host.  Returns QSVD_ERR_CAPACITY
- * if c->max_len + n_new > c->capacity. */
+ * if c->max_len + n_new > c->capacity.  On the device, rows that would land at
+ * or past capacity are not written, seq_len[b] stops at capacity and
+ * *c->overflow is set to 1 (when given): a replayed graph, which skips the
+ * host check, cannot grow a sequence past its buffer. */
 qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void* cq,
                                      const float* sc, int32_t n_new, void* stream);
 
@@ -185,8 +192,9 @@ qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void*
  * r in {128, 512, 1024, 1536} (with at most 32 heads) or r a multiple of 128
  * up to 3072, any cache format, and batch * q_len * ceil(n_q_heads / 16)
  * <= 65535 (batch * q_len <= 65535 with 32-head blocks); the reconstruct
- * form takes n_q_heads <= 32, q_len 1, capacity <= 16384 and an F16 or I8
- * cache.
+ * form takes n_q_heads <= 32, q_len 1, capacity <= 16384 and any cache
+ * format (F16 rows rebuild on the fp16 products, I8 on the int8 products,
+ * I4 on the 4-bit products).
  * Launch grids are sized from the host c->max_len and every length is read
  * from seq_len on the device, so a call may be captured in a graph and
  * replayed while the cache grows, provided c->max_len at capture is at least
@@ -203,12 +211,18 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
  * vector's pairs (j, j + head_dim/2), j < head_dim/2, are turned by the angle
  * t * rope_theta^(-2j/head_dim), formed and reduced modulo 2 pi in fp64 and
  * evaluated in fp32.  Values are not rotated.  Because a key then depends on
- * its position, it cannot be folded into the query: only the reconstruct form
- * runs (mode QSVD_ATTN_AUTO or QSVD_ATTN_RECONSTRUCT; QSVD_ATTN_ABSORBED
- * returns QSVD_ERR_UNSUPPORTED), with its requirements above (q_len 1,
- * n_q_heads <= 32, capacity <= 16384, F16 or I8 cache) and a workspace of
- * qsvd_decode_workspace_size(w, c, 1, QSVD_ATTN_RECONSTRUCT) bytes.
- * rope_theta must be finite and > 1 (QSVD_ERR_INVALID_ARG otherwise). */
+ * its position, it cannot be folded into the query, so the keys are rebuilt
+ * in both forms:
+ *   QSVD_ATTN_ABSORBED     K rebuilt and rotated for the scores, the value side
+ *                          kept in latent space (sum_t p_t C_t, then W^u_v);
+ *                          needs n_q_heads <= 32 and r in {128, 512, 1024, 1536}
+ *                          (QSVD_ERR_UNSUPPORTED otherwise)
+ *   QSVD_ATTN_RECONSTRUCT  K and V rebuilt, plain attention; needs
+ *                          n_q_heads <= 32 and capacity <= 16384
+ *   QSVD_ATTN_AUTO         the first where it applies, else the second
+ * Both take q_len 1 only and any cache format (F16, I8, I4), and one workspace
+ * size serves both: qsvd_decode_workspace_size(w, c, 1, QSVD_ATTN_RECONSTRUCT)
+ * bytes.  rope_theta must be finite and > 1 (QSVD_ERR_INVALID_ARG otherwise). */
 qsvd_status qsvd_latent_decode_attention_rope(const qsvd_layer* w, const qsvd_cache* c,
                                               const void* q, int32_t q_len, int32_t mode,
                                               float sm_scale, float rope_theta, void* out,

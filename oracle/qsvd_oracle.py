@@ -123,18 +123,19 @@ def allocate_ranks(scores, budget: int):
     return [np.array(sorted(k), dtype=np.int64) for k in kept]
 
 
-def factors_from_selection(U: np.ndarray, s: np.ndarray, Vt: np.ndarray, keep: np.ndarray, beta: float):
-    """W^d and W^u of the kept singular triplets (any subset), Eq. 3-4."""
-    return split_beta(U[:, keep], s[keep], Vt[keep, :], beta)
-
-
 def beta_objective(A: np.ndarray, B: np.ndarray, X: np.ndarray, layer_fn) -> float:
-    """Eq. 14's per-layer term for the projection: sum over the calibration
-    rows of ||Y - Y'||^2 with Y = X W^d W^u in fp64 and Y' the quantized
-    projection of `layer_fn(A, B)` (the concatenated fp16 Q | K | V)."""
+    """Eq. 14's per-layer term: the sum over calibration rows d of
+    ||Y_d - Y'_d||^2 (squared Euclidean norm, every output column), with
+    Y = X W^d W^u in fp64 and Y' = `layer_fn(A, B, X)`, the quantized
+    projection (the concatenated fp16 Q | K | V).
+
+    Reading: the paper scores the self-attention block's output; here the
+    score is taken on the block's quantized projection (the part of the block
+    that beta changes), not on the attention that follows it."""
     Y = np.asarray(X, dtype=np.float64) @ A @ B
-    Yq = layer_fn(A, B, X)
-    return float(np.sum((Y - Yq.astype(np.float64)) ** 2))
+    Yq = np.asarray(layer_fn(A, B, X), dtype=np.float64)
+    assert Yq.shape == Y.shape
+    return float(np.sum((Y - Yq) ** 2))
 
 
 def beta_search(U_r: np.ndarray, s_r: np.ndarray, Vt_r: np.ndarray, X: np.ndarray, betas, layer_fn):
@@ -580,6 +581,55 @@ def attention_absorbed(layer: Layer, cache: LatentCache, q: np.ndarray, q_len: i
                 p = _softmax((C[:pos + 1] @ q_lat) * sm)
                 out[b, i, h * dh:(h + 1) * dh] = (p @ C[:pos + 1]) @ Bv
     return out
+
+
+def prefill_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, lengths: List[int], n_q_heads: int,
+                      n_kv_heads: int, head_dim: int, sm_scale: float = None) -> np.ndarray:
+    """Causal self-attention of a prefill block over its own projections.
+
+    In prefill every token of the prompt has its keys and values at hand: the
+    up-projection Y' = Q(C) Q(W^u) (Eq. 11) gives Q, K and V of all tokens at
+    once (K = C W^u_k, V = C W^u_v, Eq. 5), and token i of a sequence attends
+    to tokens 0..i of the same sequence.  Q [M, Hq*dh], K and V [M, Hkv*dh]
+    are token-major with the sequences back to back (`lengths`); query head h
+    reads key/value head floor(h * Hkv / Hq); softmax scale 1/sqrt(dh) unless
+    given; fp64 throughout.  Returns fp64 [M, Hq*dh]."""
+    dh = head_dim
+    sm = 1.0 / np.sqrt(dh) if not sm_scale else sm_scale
+    Q = np.asarray(Q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    out = np.zeros_like(Q)
+    t0 = 0
+    for n in lengths:
+        for h in range(n_q_heads):
+            g = kv_group(h, n_q_heads, n_kv_heads)
+            qh = Q[t0:t0 + n, h * dh:(h + 1) * dh]
+            kh = K[t0:t0 + n, g * dh:(g + 1) * dh]
+            vh = V[t0:t0 + n, g * dh:(g + 1) * dh]
+            s = (qh @ kh.T) * sm
+            s[np.triu_indices(n, 1)] = -np.inf          # query i sees keys 0..i
+            out[t0:t0 + n, h * dh:(h + 1) * dh] = _softmax(s) @ vh
+        t0 += n
+    return out
+
+
+def cache_snapshot(cache: LatentCache) -> Dict[str, np.ndarray]:
+    """Copy of the cache state (rows, scales, lengths) from which a decode can
+    resume."""
+    snap = dict(data=cache.data.copy(), seq_len=cache.seq_len.copy())
+    if cache.scale is not None:
+        snap["scale"] = cache.scale.copy()
+    return snap
+
+
+def cache_restore(cache: LatentCache, snap: Dict[str, np.ndarray]):
+    """Put a snapshot's state back into a cache of the same shape."""
+    assert snap["data"].shape == cache.data.shape
+    cache.data[...] = snap["data"]
+    cache.seq_len[...] = snap["seq_len"]
+    if cache.scale is not None:
+        cache.scale[...] = snap["scale"]
 
 
 def cache_append_prefill(cache: LatentCache, proj: Dict[str, np.ndarray], lengths: List[int]):

@@ -39,7 +39,7 @@ class QsvdCache(ctypes.Structure):
     _fields_ = [
         ("fmt", ctypes.c_int32), ("batch", ctypes.c_int32), ("capacity", ctypes.c_int32),
         ("r", ctypes.c_int32), ("data", ctypes.c_void_p), ("scale", ctypes.c_void_p),
-        ("seq_len", ctypes.c_void_p), ("max_len", ctypes.c_int32),
+        ("seq_len", ctypes.c_void_p), ("max_len", ctypes.c_int32), ("overflow", ctypes.c_void_p),
     ]
 
 
@@ -200,7 +200,8 @@ class DeviceCache:
     """A latent cache in device memory; ``.c`` is the qsvd_cache struct.
 
     ``lengths`` initialises every seq_len[b] (ragged batches allowed); max_len
-    is their maximum."""
+    is their maximum.  ``overflow`` is the device flag an append sets when it
+    would run past capacity on the device."""
 
     def __init__(self, fmt, batch, capacity, r, lengths=None, device="cuda"):
         import torch
@@ -212,12 +213,29 @@ class DeviceCache:
                                                                    device=device)
         lengths = [0] * batch if lengths is None else list(lengths)
         self.seq_len = torch.tensor(lengths, dtype=torch.int32, device=device)
+        self.overflow = torch.zeros((1,), dtype=torch.int32, device=device)
         self.c = QsvdCache(fmt, batch, capacity, r, ptr(self.data), ptr(self.scale), ptr(self.seq_len),
-                           max(lengths) if lengths else 0)
+                           max(lengths) if lengths else 0, ptr(self.overflow))
 
     @property
     def max_len(self):
         return self.c.max_len
+
+    def snapshot(self):
+        """Host copy of the cache state (rows, scales, lengths, host bound) from
+        which a decode resumes; taken after the work queued on the current
+        stream."""
+        return dict(data=self.data.cpu(), scale=None if self.scale is None else self.scale.cpu(),
+                    seq_len=self.seq_len.cpu(), max_len=int(self.c.max_len))
+
+    def restore(self, snap):
+        """Put a snapshot back (same format and shape), ordered on the current stream."""
+        assert tuple(snap["data"].shape) == tuple(self.data.shape) and snap["data"].dtype == self.data.dtype
+        self.data.copy_(snap["data"])
+        if self.scale is not None:
+            self.scale.copy_(snap["scale"])
+        self.seq_len.copy_(snap["seq_len"])
+        self.c.max_len = snap["max_len"]
 
 
 def projection_evaluator(n_q_heads, n_kv_heads, head_dim, w_bits=8, w_group=0, a_bits=8):

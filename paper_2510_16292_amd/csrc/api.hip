@@ -250,7 +250,8 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
   if (st != QSVD_OK) return st;
   if (hi <= lo) {
     if (!skinny) return QSVD_OK;
-    return hip_status(launch_quantize_rows(c_h, M, w->r, w->r, act_bits, 1.f, cq, sc, s), "latent quantization");
+    return hip_status(launch_quantize_rows(c_h, M, w->r, w->r, act_bits, 1.f, cq, sc, s, "latent_quant"),
+                      "latent quantization");
   }
 
   // Q(C) W^u -> Q | K | V (fp16) over the columns [lo, hi)

@@ -22,13 +22,24 @@ cache_append_kernel(const uint8_t* __restrict__ src, const float* __restrict__ s
   if (dst_scale && threadIdx.x == 0) dst_scale[drow] = src_scale[srow];
 }
 
+// New length of a sequence after an append: rows at or past capacity were
+// not written, so the length stops at capacity and the overflow flag (if the
+// caller gave one) records that rows were dropped.
+__device__ __forceinline__ int32_t advanced_len(int32_t base, int32_t n_new, int32_t capacity,
+                                                int32_t* __restrict__ overflow) {
+  const int64_t want = (int64_t)base + n_new;
+  if (want > capacity && overflow) *overflow = 1;
+  return want > capacity ? capacity : (int32_t)want;
+}
+
 // Decode-sized appends (few rows per sequence): one workgroup per sequence
 // copies its rows, then advances seq_len[b] itself after a barrier, so no
 // second launch is needed.
 __global__ void __launch_bounds__(256)
 cache_append_fused_kernel(const uint8_t* __restrict__ src, const float* __restrict__ src_scale,
                           uint8_t* __restrict__ dst, float* __restrict__ dst_scale,
-                          int32_t* __restrict__ seq_len, int32_t capacity, int32_t n_new, int32_t row_bytes) {
+                          int32_t* __restrict__ seq_len, int32_t capacity, int32_t n_new, int32_t row_bytes,
+                          int32_t* __restrict__ overflow) {
   const int b = blockIdx.x;
   const int32_t base = seq_len[b];
   const int per_row = row_bytes / 16;
@@ -42,12 +53,13 @@ cache_append_fused_kernel(const uint8_t* __restrict__ src, const float* __restri
     if (dst_scale && k == 0) dst_scale[drow] = src_scale[srow];
   }
   __syncthreads();
-  if (threadIdx.x == 0) seq_len[b] = base + n_new;
+  if (threadIdx.x == 0) seq_len[b] = advanced_len(base, n_new, capacity, overflow);
 }
 
-__global__ void seq_len_advance_kernel(int32_t* __restrict__ seq_len, int32_t batch, int32_t n_new) {
+__global__ void seq_len_advance_kernel(int32_t* __restrict__ seq_len, int32_t batch, int32_t n_new,
+                                       int32_t capacity, int32_t* __restrict__ overflow) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b < batch) seq_len[b] += n_new;
+  if (b < batch) seq_len[b] = advanced_len(seq_len[b], n_new, capacity, overflow);
 }
 
 hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void* cq,
@@ -69,7 +81,8 @@ hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void*
     KernelScope ks("cache_append", s);
     QSVD_LAUNCH(ks, cache_append_fused_kernel, dim3(c.batch), dim3(256), 0, s, (const uint8_t*)src,
                        c.fmt == QSVD_CACHE_F16 ? nullptr : sc, (uint8_t*)c.data,
-                       c.fmt == QSVD_CACHE_F16 ? nullptr : c.scale, c.seq_len, c.capacity, n_new, row_bytes);
+                       c.fmt == QSVD_CACHE_F16 ? nullptr : c.scale, c.seq_len, c.capacity, n_new, row_bytes,
+                       c.overflow);
     return hipGetLastError();
   }
   {
@@ -84,7 +97,7 @@ hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void*
   {
     KernelScope ks("seq_len_advance", s);
     QSVD_LAUNCH(ks, seq_len_advance_kernel, dim3((c.batch + 255) / 256), dim3(256), 0, s, c.seq_len,
-                       c.batch, n_new);
+                       c.batch, n_new, c.capacity, c.overflow);
   }
   return hipGetLastError();
 }

@@ -334,7 +334,7 @@ hipError_t launch_gemm_i8(const GemmArgs& g, hipStream_t s) {
                  : big_tiles >= 256 ? launch_pipe<256, 256, 128, 64, 4, false>(g, sg, s)
                                     : launch_pipe<128, 128, 64, 64, 6, false>(g, sg, s);
   if (e != hipSuccess || !g.cq) return e;
-  return launch_quantize_rows(g.seg[0].ptr, g.M, g.N, g.seg[0].ld, g.abits, 1.f, g.cq, g.sc, s);
+  return launch_quantize_rows(g.seg[0].ptr, g.M, g.N, g.seg[0].ld, g.abits, 1.f, g.cq, g.sc, s, "latent_quant");
 }
 
 hipError_t launch_gemm_f16(const GemmArgs& g, hipStream_t s) {

@@ -340,7 +340,7 @@ hipError_t launch_gemm_q4(const GemmArgs& g, int32_t abits, int32_t wbits, int32
   else if (abits == 4) e = launch_q4<4, 8, false>(g, sg, 0, sstride, s);
   else e = launch_q4<8, 8, true>(g, sg, group, sstride, s);     // 8-bit codes, per-group scales
   if (e != hipSuccess || !g.cq) return e;
-  return launch_quantize_rows(g.seg[0].ptr, g.M, g.N, g.seg[0].ld, g.abits, 1.f, g.cq, g.sc, s);
+  return launch_quantize_rows(g.seg[0].ptr, g.M, g.N, g.seg[0].ld, g.abits, 1.f, g.cq, g.sc, s, "latent_quant");
 }
 
 }  // namespace qsvd

@@ -25,8 +25,11 @@ struct KernelScope {
 #define QSVD_LAUNCH(ks, kern, grid, block, lds, stream, ...) \
   hipExtLaunchKernelGGL(kern, grid, block, (std::uint32_t)(lds), stream, (ks).start(), (ks).stop(), 0, __VA_ARGS__)
 
+// `name` is the profiler's name of the launch (the latent quantization Q(C)
+// inside a projection call is "latent_quant").
 hipError_t launch_quantize_rows(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits,
-                                float clip, void* xq, float* sx, hipStream_t s);
+                                float clip, void* xq, float* sx, hipStream_t s,
+                                const char* name = "quantize_rows");
 // Q(X H1^T) for H1 = blockdiag(H_block) diag(signs) / sqrt(block); c = fp32(1/sqrt(block)).
 hipError_t launch_quantize_rotated(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits, float clip,
                                    const int8_t* signs, int32_t block, float c, void* xq, float* sx,

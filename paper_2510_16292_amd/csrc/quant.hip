@@ -345,11 +345,11 @@ hipError_t launch_quantize_rotated(const void* x, int64_t M, int32_t K, int64_t 
 }
 
 hipError_t launch_quantize_rows(const void* x, int64_t M, int32_t K, int64_t ldx, int32_t bits,
-                                float clip, void* xq, float* sx, hipStream_t s) {
+                                float clip, void* xq, float* sx, hipStream_t s, const char* name) {
   if (M == 0) return hipSuccess;
   dim3 grid((unsigned)M), block(64);
   const bool regs = K <= 64 * 8 * 16;
-  KernelScope ks("quantize_rows", s);
+  KernelScope ks(name, s);
   const _Float16* xp = (const _Float16*)x;
   uint8_t* q = (uint8_t*)xq;
   if (bits == 8) {

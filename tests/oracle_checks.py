@@ -487,6 +487,76 @@ def check_causal_prefix_consistency():
         assert np.allclose(block[0, i], one[0, 0], rtol=1e-12, atol=1e-15)
 
 
+def check_prefill_attention():
+    """Causal self-attention of a prefill block over its own Q, K, V (the
+    up-projection's outputs, Eq. 11 and Eq. 5): at full rank without
+    quantization it equals textbook attention with Q, K, V taken from the
+    original concatenated weight, sequence by sequence; every query row equals
+    the latent-cache attention of the same query over the cache truncated at
+    its position; zero queries give the running mean of the value rows; and a
+    row does not depend on later tokens or other sequences, but does on
+    earlier ones."""
+    for hq, hkv in ((4, 4), (6, 2)):
+        dh, d = 8, 40
+        N = (hq + 2 * hkv) * dh
+        g = np.random.default_rng(31 + hq + hkv)
+        W = g.standard_normal((d, N)) * 0.3
+        A, B = O.factors_from_weight(W, min(d, N), 0.5)
+        lengths = [9, 5]
+        X = g.standard_normal((sum(lengths), d))
+        Wq, Wk, Wv = W[:, :hq * dh], W[:, hq * dh:(hq + hkv) * dh], W[:, (hq + hkv) * dh:]
+        Y = X @ A @ B
+        Q, K, V = Y[:, :hq * dh], Y[:, hq * dh:(hq + hkv) * dh], Y[:, (hq + hkv) * dh:]
+        got = O.prefill_attention(Q, K, V, lengths, hq, hkv, dh)
+        t0 = 0
+        for n in lengths:
+            Xs = X[t0:t0 + n]
+            want = _textbook_mha(Xs @ Wq, Xs @ Wk, Xs @ Wv, hq, hkv, dh, n)
+            assert np.allclose(got[t0:t0 + n], want, rtol=1e-9, atol=1e-12), (hq, hkv, n)
+            t0 += n
+        # the same rows from the (separately pinned) latent-cache attention
+        layer = _ExactLayer(d, A.shape[1], hq, hkv, dh, 8, 0, None, None, None, None, A, B)
+        Xs = X[:lengths[0]]
+        via_cache = O.attention_reference(layer, _ExactCache([Xs @ A]), Q[None, :lengths[0]], q_len=lengths[0])[0]
+        assert np.allclose(got[:lengths[0]], via_cache, rtol=1e-10, atol=1e-13)
+    # zero queries: the running mean of V; causal and per-sequence independence
+    g = np.random.default_rng(4)
+    hq, hkv, dh = 4, 2, 8
+    lengths = [7, 6]
+    M = sum(lengths)
+    K = g.standard_normal((M, hkv * dh))
+    V = g.standard_normal((M, hkv * dh))
+    out = O.prefill_attention(np.zeros((M, hq * dh)), K, V, lengths, hq, hkv, dh)
+    t0 = 0
+    for n in lengths:
+        for i in range(n):
+            for h in range(hq):
+                gg = h // (hq // hkv)
+                want = V[t0:t0 + i + 1, gg * dh:(gg + 1) * dh].mean(axis=0)
+                assert np.allclose(out[t0 + i, h * dh:(h + 1) * dh], want, rtol=1e-12, atol=1e-14)
+        t0 += n
+    Q = g.standard_normal((M, hq * dh))
+    base = O.prefill_attention(Q, K, V, lengths, hq, hkv, dh)
+    for i in (0, 3, 6):
+        K2, V2 = K.copy(), V.copy()
+        K2[i + 1:] += 5.0
+        V2[i + 1:] -= 3.0
+        later = O.prefill_attention(Q, K2, V2, lengths, hq, hkv, dh)
+        assert np.array_equal(later[:i + 1], base[:i + 1])
+        V3 = V.copy()
+        V3[i] += 2.0
+        own = O.prefill_attention(Q, K, V3, lengths, hq, hkv, dh)
+        assert not np.allclose(own[i], base[i])
+        if i:
+            K3 = K.copy()
+            K3[0] += 2.0
+            earlier = O.prefill_attention(Q, K3, V, lengths, hq, hkv, dh)
+            assert not np.allclose(earlier[i], base[i])
+    # the second sequence alone gives its rows unchanged
+    alone = O.prefill_attention(Q[7:], K[7:], V[7:], [6], hq, hkv, dh)
+    assert np.allclose(alone, base[7:], rtol=1e-13, atol=1e-15)
+
+
 # ---------------------------------------------------------------- P11: cache
 
 def check_cache_append_and_int4():
@@ -517,6 +587,36 @@ def check_cache_append_and_int4():
         pass
     else:
         raise AssertionError("capacity overflow not detected")
+
+
+def check_cache_snapshot_resume():
+    """A decode that resumes from a snapshot of the cache continues exactly as
+    the uninterrupted one: the same cache bytes, scales, lengths and outputs,
+    also when restored into another cache object; the snapshot is a copy that
+    later appends leave unchanged."""
+    layer = tiny_layer()
+    wl = tiny_workload()
+    X = gen.prefill_activations(wl)
+    for fmt, bits in ((O.CACHE_F16, 8), (O.CACHE_I8, 8), (O.CACHE_I4, 4)):
+        cache = O.LatentCache(fmt, 2, 48, layer.r)
+        O.cache_append_prefill(cache, O.prefill(layer, X[:40], bits), [25, 15])
+        snap = O.cache_snapshot(cache)
+        keep = {k: v.copy() for k, v in snap.items()}
+        steps = [gen.decode_activations(wl, t, batch=2) for t in range(3)]
+        first = [O.decode_step(layer, cache, x, bits)["out"] for x in steps]
+        for k in keep:
+            assert np.array_equal(snap[k], keep[k]), "snapshot changed by later appends"
+        after = (cache.data.copy(), cache.seq_len.copy(), None if cache.scale is None else cache.scale.copy())
+        for target in (cache, O.LatentCache(fmt, 2, 48, layer.r)):
+            O.cache_restore(target, snap)
+            assert list(target.seq_len) == [25, 15]
+            again = [O.decode_step(layer, target, x, bits)["out"] for x in steps]
+            for a, b in zip(first, again):
+                assert np.array_equal(a, b)
+            assert np.array_equal(target.data.view(np.uint8), after[0].view(np.uint8))
+            assert np.array_equal(target.seq_len, after[1])
+            if after[2] is not None:
+                assert np.array_equal(target.scale, after[2])
 
 
 # ---------------------------------------------------------------- online H1 rotation
@@ -643,6 +743,25 @@ def check_rank_allocation():
     for k in range(7):
         for ks in O.allocate_ranks(dec, k):
             assert np.array_equal(ks, np.arange(ks.size))
+
+
+def check_beta_objective_value():
+    """Eq. 14's term on a hand-computed case: d = r = 2, one query, key and
+    value column (Hq = Hkv = 1, dh = 1), W^d = I, W^u = [[1, 0, 0], [0, 1, 1]],
+    X = [[1, 2], [3, -1]] so Y = [[1, 2, 2], [3, -1, -1]]; a projection that
+    is off by E = [[0.5, 0, -1], [0, 2, 0]] scores ||E||^2 = 0.25 + 1 + 4 = 5.25
+    (the squared error summed over both rows and all of Q, K and V)."""
+    A = np.eye(2)
+    B = np.array([[1.0, 0.0, 0.0], [0.0, 1.0, 1.0]])
+    X = np.array([[1.0, 2.0], [3.0, -1.0]])
+    E = np.array([[0.5, 0.0, -1.0], [0.0, 2.0, 0.0]])
+    Y = np.array([[1.0, 2.0, 2.0], [3.0, -1.0, -1.0]])
+    assert O.beta_objective(A, B, X, lambda a, b, x: Y + E) == 5.25
+    assert O.beta_objective(A, B, X, lambda a, b, x: Y) == 0.0
+    # one row, error only in the value column: 3^2
+    E2 = np.zeros_like(E)
+    E2[1, 2] = 3.0
+    assert O.beta_objective(A, B, X, lambda a, b, x: (Y + E2).astype(np.float16)) == 9.0
 
 
 def check_beta_search():

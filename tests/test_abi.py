@@ -57,6 +57,7 @@ int main(void) {
   F(qsvd_layer, s_a) F(qsvd_layer, b_t) F(qsvd_layer, s_b)
   F(qsvd_cache, fmt) F(qsvd_cache, batch) F(qsvd_cache, capacity) F(qsvd_cache, r)
   F(qsvd_cache, data) F(qsvd_cache, scale) F(qsvd_cache, seq_len) F(qsvd_cache, max_len)
+  F(qsvd_cache, overflow)
   printf("sizeof.qsvd_layer %zu 0\nsizeof.qsvd_cache %zu 0\n", sizeof(qsvd_layer), sizeof(qsvd_cache));
   return 0;
 }

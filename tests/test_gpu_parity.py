@@ -425,6 +425,72 @@ def test_cache_append_bytes(tiny, fmt):
         H.append(dc, c_h, cq, sc, cap)
 
 
+@pytest.mark.parametrize("n_new", [1, 17], ids=["fused", "two-launch"])
+def test_cache_append_stops_at_capacity_on_device(tiny, n_new):
+    """An append that the host check cannot see running past capacity (the
+    host bound max_len lags the device lengths, as in a replayed graph) writes
+    only the rows that fit, stops seq_len at capacity and raises the device
+    overflow flag; sequences with room are appended as usual."""
+    wl, ol, dl = tiny
+    r = wl.layer.r
+    cap = 4 if n_new == 1 else 18
+    lengths = [cap, 2] if n_new == 1 else [3, 0]
+    dc = B.DeviceCache(B.QSVD_CACHE_F16, 2, cap, r, lengths)
+    before = gen.random_rows(61, (2, cap, r), 1.0)
+    dc.data.copy_(H.dev(before))
+    dc.c.max_len = 0                       # the host bound no longer covers the device lengths
+    src = gen.random_rows(62, (2 * n_new, r), 1.0)
+    H.say(f"cache append past capacity n_new={n_new}")
+    H.append(dc, c_h=H.dev(src), n_new=n_new)
+    got = H.host(dc.data)
+    want = before.copy()
+    for b, n0 in enumerate(lengths):
+        k = max(0, min(n_new, cap - n0))
+        want[b, n0:n0 + k] = src[b * n_new:b * n_new + k]
+    assert np.array_equal(got.view(np.uint16), want.view(np.uint16))
+    assert list(H.host(dc.seq_len)) == [min(n + n_new, cap) for n in lengths]
+    assert int(H.host(dc.overflow)[0]) == 1
+    # a later append that fits leaves the flag as the caller left it
+    dc.overflow.zero_()
+    dc.seq_len.fill_(0)
+    dc.c.max_len = 0
+    H.append(dc, c_h=H.dev(src), n_new=n_new)
+    assert int(H.host(dc.overflow)[0]) == 0
+
+
+@pytest.mark.parametrize("fmt", [B.QSVD_CACHE_F16, B.QSVD_CACHE_I8], ids=["f16", "i8"])
+def test_cache_snapshot_resume(tiny, fmt):
+    """Decode resumed from a snapshot of the device cache continues exactly as
+    before: three steps, restore, the same three steps again give bit-identical
+    outputs, cache bytes and lengths, in the original cache and in a fresh one."""
+    wl, ol, dl = tiny
+    r = wl.layer.r
+    X = gen.prefill_activations(wl)[:40]
+    dc = B.DeviceCache(fmt, 2, 48, r, [0, 0])
+    pre = H.Prefill(dl, 40, mask=0, debug=False).run(H.dev(X))
+    H.append(dc, pre.c_h, pre.cq, pre.sc, n_new=20)
+    snap = dc.snapshot()
+    steps = [gen.decode_activations(wl, t, batch=2) for t in range(3)]
+
+    def run(cache):
+        outs = []
+        for xt in steps:
+            p = H.Prefill(dl, 2, mask=B.QSVD_OUT_Q, debug=False).run(H.dev(xt))
+            H.append(cache, p.c_h, p.cq, p.sc, n_new=1)
+            outs.append(H.host(H.decode_attention(dl, cache, p.q, B.QSVD_ATTN_AUTO)))
+        return outs, H.host(cache.data), H.host(cache.seq_len)
+
+    H.say(f"cache snapshot / resume fmt={fmt}")
+    first = run(dc)
+    for target in (dc, B.DeviceCache(fmt, 2, 48, r, [0, 0])):
+        target.restore(snap)
+        again = run(target)
+        for a, b in zip(first[0], again[0]):
+            assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
+        assert np.array_equal(first[1].view(np.uint8), again[1].view(np.uint8))
+        assert list(first[2]) == list(again[2]) == [23, 23]
+
+
 # ------------------------------------------------------------------ a5-a7: decode attention
 
 @pytest.mark.parametrize("mode", MODES, ids=MODE_IDS)

@@ -145,6 +145,58 @@ def _rope_sign_wrong(x, positions, theta, dh):            # rotation the other w
 
 
 _rope_freq_ok = O.rope
+_good_prefill_attention = O.prefill_attention
+_good_snapshot = O.cache_snapshot
+
+
+def _beta_objective_norm_not_squared(A, B, X, layer_fn):   # ||Y - Y'|| instead of ||Y - Y'||^2
+    Y = np.asarray(X, dtype=np.float64) @ A @ B
+    return float(np.sqrt(np.sum((Y - np.asarray(layer_fn(A, B, X), np.float64)) ** 2)))
+
+
+def _beta_objective_q_only(A, B, X, layer_fn):             # only the query third of the columns
+    Y = np.asarray(X, dtype=np.float64) @ A @ B
+    n = Y.shape[1] // 3
+    return float(np.sum((Y - np.asarray(layer_fn(A, B, X), np.float64))[:, :n] ** 2))
+
+
+def _prefill_attention_no_mask(Q, K, V, lengths, hq, hkv, dh, sm_scale=None):   # every token sees all
+    sm = 1.0 / np.sqrt(dh)
+    out = np.zeros(np.shape(Q))
+    t0 = 0
+    for n in lengths:
+        for h in range(hq):
+            g = O.kv_group(h, hq, hkv)
+            s = (Q[t0:t0 + n, h * dh:(h + 1) * dh] @ K[t0:t0 + n, g * dh:(g + 1) * dh].T) * sm
+            out[t0:t0 + n, h * dh:(h + 1) * dh] = O._softmax(s) @ V[t0:t0 + n, g * dh:(g + 1) * dh]
+        t0 += n
+    return out
+
+
+def _prefill_attention_one_sequence(Q, K, V, lengths, hq, hkv, dh, sm_scale=None):   # sequences not separated
+    return _good_prefill_attention(Q, K, V, [sum(lengths)], hq, hkv, dh, sm_scale)
+
+
+def _prefill_attention_strict(Q, K, V, lengths, hq, hkv, dh, sm_scale=None):   # query i sees 0..i-1 (own key dropped)
+    sm = 1.0 / np.sqrt(dh)
+    out = np.zeros(np.shape(Q))
+    t0 = 0
+    for n in lengths:
+        for h in range(hq):
+            g = O.kv_group(h, hq, hkv)
+            s = (Q[t0:t0 + n, h * dh:(h + 1) * dh] @ K[t0:t0 + n, g * dh:(g + 1) * dh].T) * sm
+            s[np.triu_indices(n, 0)] = -np.inf
+            s[0, 0] = 0.0
+            out[t0:t0 + n, h * dh:(h + 1) * dh] = O._softmax(s) @ V[t0:t0 + n, g * dh:(g + 1) * dh]
+        t0 += n
+    return out
+
+
+def _snapshot_views(cache):                                  # no copy: later appends change it
+    snap = dict(data=cache.data, seq_len=cache.seq_len)
+    if cache.scale is not None:
+        snap["scale"] = cache.scale
+    return snap
 
 
 MUTATIONS = [
@@ -166,6 +218,13 @@ MUTATIONS = [
     ("allocate_ranks", _allocate_lowest, [C.check_rank_allocation]),
     ("rope", _rope_freq_wrong, [C.check_rope]),
     ("rope", _rope_sign_wrong, [C.check_rope]),
+    ("beta_objective", _beta_objective_norm_not_squared, [C.check_beta_objective_value]),
+    ("beta_objective", _beta_objective_q_only, [C.check_beta_objective_value]),
+    ("prefill_attention", _prefill_attention_no_mask, [C.check_prefill_attention]),
+    ("prefill_attention", _prefill_attention_one_sequence, [C.check_prefill_attention]),
+    ("prefill_attention", _prefill_attention_strict, [C.check_prefill_attention]),
+    ("kv_group", _kv_group_modulo, [C.check_prefill_attention]),
+    ("cache_snapshot", _snapshot_views, [C.check_cache_snapshot_resume]),
 ]
 
 

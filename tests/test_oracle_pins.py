@@ -19,13 +19,16 @@ PINS = [
     C.check_full_rank_matches_textbook_attention,
     C.check_softmax_special_cases,
     C.check_causal_prefix_consistency,
+    C.check_prefill_attention,
     C.check_cache_append_and_int4,
+    C.check_cache_snapshot_resume,
     C.check_cost_model,
     C.check_printed_cost_ratios,
     C.check_rotation_matrix_and_transform,
     C.check_rotation_fold_and_error_reduction,
     C.check_importance_closed_form,
     C.check_rank_allocation,
+    C.check_beta_objective_value,
     C.check_beta_search,
     C.check_rope,
 ]
