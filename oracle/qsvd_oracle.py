@@ -602,6 +602,8 @@ def prefill_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, lengths: List
     out = np.zeros_like(Q)
     t0 = 0
     for n in lengths:
+        if n == 0:                                      # an empty sequence has no query rows
+            continue
         for h in range(n_q_heads):
             g = kv_group(h, n_q_heads, n_kv_heads)
             qh = Q[t0:t0 + n, h * dh:(h + 1) * dh]

@@ -552,9 +552,11 @@ def check_prefill_attention():
             K3[0] += 2.0
             earlier = O.prefill_attention(Q, K3, V, lengths, hq, hkv, dh)
             assert not np.allclose(earlier[i], base[i])
-    # the second sequence alone gives its rows unchanged
+    # the second sequence alone gives its rows unchanged, also next to empty sequences
     alone = O.prefill_attention(Q[7:], K[7:], V[7:], [6], hq, hkv, dh)
     assert np.allclose(alone, base[7:], rtol=1e-13, atol=1e-15)
+    with_empty = O.prefill_attention(Q, K, V, [0, 7, 0, 6, 0], hq, hkv, dh)
+    assert np.array_equal(with_empty, base)
 
 
 # ---------------------------------------------------------------- P11: cache
