@@ -442,17 +442,80 @@ def bench_prefill(args, wl2, host_layer):
                        "frac": round(qbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
     call_s = (t1 - t0) / args.prefill_steps
     tops = ops / proj_s / 1e12
+    # causal attention of the 4 x 640 prompt over the projection's own Q, K, V
+    # (fp16 matrix cores), and the latent (absorbed) form of the same
+    # attention over an fp16 latent cache of the prompt, for comparison
+    lengths = [M // wl2.prefill_batch] * wl2.prefill_batch
+    att_s = time_prefill_attention(q, k, v, lengths, L.n_q_heads, L.n_kv_heads, L.head_dim, 20)
+    att_flops = causal_flops(lengths, L.n_q_heads, L.head_dim)
+    dc = B.DeviceCache(B.QSVD_CACHE_F16, len(lengths), lengths[0], r, [0] * len(lengths))
+    B.check(B.qsvd_latent_cache_append(dc.c, P(c_h), 0, 0, lengths[0], s))
+    wsa = B.qsvd_decode_workspace_size(dl.c, dc.c, lengths[0], B.QSVD_ATTN_ABSORBED)
+    wsa_t = torch.empty((wsa,), dtype=torch.uint8, device="cuda")
+    oa = torch.empty_like(q)
+    absorbed = lambda: B.check(B.qsvd_latent_decode_attention(dl.c, dc.c, P(q), lengths[0], B.QSVD_ATTN_ABSORBED,
+                                                                0.0, P(oa), P(wsa_t), wsa, s))
+    absorbed()
+    torch.cuda.synchronize()
+    a0 = time.perf_counter()
+    for _ in range(3):
+        absorbed()
+    torch.cuda.synchronize()
+    abs_s = (time.perf_counter() - a0) / 3
+    del dc, wsa_t, oa
+    attention = {"value": round(att_flops / att_s / 1e12, 1), "unit": "TFLOP/s", "us": round(att_s * 1e6, 2),
+                 "gflop": round(att_flops / 1e9, 2), "lengths": lengths,
+                 "absorbed_form_us": round(abs_s * 1e6, 1),
+                 "roofline": {"bound": "mfma", "achieved": round(att_flops / att_s / 1e12, 1),
+                              "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                              "frac": round(att_flops / att_s / 1e12 / F16_PEAK_TFLOPS, 4), "traffic": None,
+                              "kernel": "prefill_flash_kernel (fp16, 4 dh flop per causal pair and head)"}}
     # HBM bytes of one call's two products (both launches), from the committed counter summary
     traffic = counted_traffic(GEMM_TRAFFIC_SUMMARY) if (M, d, r, L.N) == (2560, 4096, 1536, 12288) else None
     return {"value": round(tops, 1), "unit": "TOPS", "ms_per_call": round(call_s * 1e3, 4),
             "kernels_ms_per_call": round(proj_s * 1e3, 4), "gemm_ms_per_call": round(gemm_s * 1e3, 4),
             "latent_quant_ms_per_call": round(qms / args.prefill_steps, 4),
             "gemm_only_tops": round(ops / gemm_s / 1e12, 1), "call_tops": round(ops / call_s / 1e12, 1),
-            "tokens": M, "gop_per_call": round(ops / 1e9, 2), "quantizer": quant,
+            "tokens": M, "gop_per_call": round(ops / 1e9, 2), "quantizer": quant, "attention": attention,
             "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
                          "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None if traffic is None else int(traffic),
                          "kernel": "gemm_i8 (X W^d, Q(C) W^u) + latent quantization Q(C)",
                          "launches": n + qn}}
+
+
+F16_PEAK_TFLOPS = 2500.0       # MI355X dense fp16 matrix peak, TFLOP/s
+
+
+def causal_flops(lengths, n_q_heads, head_dim):
+    """Algorithmic flops of causal attention: 4 head_dim per (query, visible key) pair and head."""
+    return float(sum(n * (n + 1) // 2 for n in lengths)) * n_q_heads * 4.0 * head_dim
+
+
+def time_prefill_attention(q, k, v, lengths, n_q_heads, n_kv_heads, head_dim, reps):
+    """Mean launch time (s) of the causal prefill attention over the given rows,
+    from the kernel's own events on its launch stream."""
+    import torch
+
+    from paper_2510_16292_amd import binding as B
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32), device="cuda")
+    out = torch.empty_like(q)
+    s = B.stream_handle()
+
+    def call():
+        B.check(B.qsvd_prefill_attention(B.ptr(q), B.ptr(k), B.ptr(v), len(lengths), B.ptr(cu), max(lengths),
+                                         n_q_heads, n_kv_heads, head_dim, 0.0, B.ptr(out), s))
+    for _ in range(3):
+        call()
+    torch.cuda.synchronize()
+    B.profile_reset()
+    B.profile_enable(True, "prefill_flash")
+    for _ in range(reps):
+        call()
+    torch.cuda.synchronize()
+    B.profile_enable(False)
+    ms, n = B.profile_read("prefill_flash")
+    B.profile_reset()
+    return ms * 1e-3 / n
 
 
 def stack_layers(wl5):
@@ -522,12 +585,21 @@ def bench_stack_prefill(args, wl5, ranks, layers):
     proj_s = (gms + qms) * 1e-3 / args.stack_passes
     pass_s = (t1 - t0) / args.stack_passes
     tops = ops / proj_s / 1e12
+    lengths = [M // wl5.prefill_batch] * wl5.prefill_batch
+    att_s = time_prefill_attention(q, k, v, lengths, L.n_q_heads, L.n_kv_heads, L.head_dim, 40)
+    att_flops = causal_flops(lengths, L.n_q_heads, L.head_dim)
+    attention = {"value": round(att_flops / att_s / 1e12, 1), "unit": "TFLOP/s", "us_per_layer": round(att_s * 1e6, 2),
+                 "gflop_per_layer": round(att_flops / 1e9, 2), "lengths": lengths,
+                 "roofline": {"bound": "mfma", "achieved": round(att_flops / att_s / 1e12, 1),
+                              "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                              "frac": round(att_flops / att_s / 1e12 / F16_PEAK_TFLOPS, 4), "traffic": None,
+                              "kernel": "prefill_flash_kernel (fp16)"}}
     del xs, xq, c_h, cq, q, k, v
     traffic = counted_traffic(STACK_GEMM_TRAFFIC_SUMMARY)
     return {"value": round(tops, 1), "unit": "TOPS", "ms_per_pass": round(pass_s * 1e3, 3),
             "kernels_ms_per_pass": round(proj_s * 1e3, 3), "gemm_ms_per_pass": round(gemm_s * 1e3, 3),
             "gemm_only_tops": round(ops / gemm_s / 1e12, 1), "call_tops": round(ops / pass_s / 1e12, 1),
-            "tokens": M, "layers": len(ranks), "top_per_pass": round(ops / 1e12, 3),
+            "tokens": M, "layers": len(ranks), "top_per_pass": round(ops / 1e12, 3), "attention": attention,
             "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
                          "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None if traffic is None else int(traffic),
                          "kernel": "gemm_q4_pipe (X W^d and Q(C) W^u, int4 x int4) + latent quantization Q(C)",

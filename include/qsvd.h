@@ -173,6 +173,27 @@ size_t qsvd_prefill_workspace_size(const qsvd_layer* w, int64_t M, uint32_t out_
 qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void* cq,
                                      const float* sc, int32_t n_new, void* stream);
 
+/* Causal self-attention of a prefill block over its own projections (Section
+ * 3.1: in prefill every prompt token's keys and values are at hand as the rows
+ * K = C W^u_k and V = C W^u_v that qsvd_lowrank_qkv_prefill wrote, Eq. 5 and
+ * Eq. 11).  Token i of a sequence attends to tokens 0..i of the same sequence:
+ * softmax(q k^T * sm_scale) v with an fp32 softmax, query head h reading
+ * key/value head floor(h * n_kv_heads / n_q_heads).
+ *   q           device fp16 [M][n_q_heads * head_dim] (the projection's Q)
+ *   k, v        device fp16 [M][n_kv_heads * head_dim] (its K and V)
+ *   cu_seqlens  device int32 [batch + 1]: sequence b is rows
+ *               [cu_seqlens[b], cu_seqlens[b + 1]); nondecreasing, cu_seqlens[0] = 0
+ *   max_seqlen  host: at least every sequence's length (sizes the launch)
+ *   sm_scale    0 selects 1/sqrt(head_dim)
+ *   out         device fp16 [M][n_q_heads * head_dim]
+ * Requires head_dim 64 or 128 and 16-byte aligned q, k, v, out.  Rows of a
+ * sequence longer than max_seqlen past max_seqlen are left unwritten.  No
+ * workspace; asynchronous on `stream`. */
+qsvd_status qsvd_prefill_attention(const void* q, const void* k, const void* v, int32_t batch,
+                                   const int32_t* cu_seqlens, int32_t max_seqlen, int32_t n_q_heads,
+                                   int32_t n_kv_heads, int32_t head_dim, float sm_scale, void* out,
+                                   void* stream);
+
 /* Attention of the newest queries of every sequence over its cached latent
  * rows (Section 3.1; decoding is l = 1): keys and values are C W^u_k and
  * C W^u_v of the stored rows (dequantized), softmax(q K^T * sm_scale) V with an

@@ -14,7 +14,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_DIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIB_DIR, "libqsvd.so")
 
-SOURCES = ["api.hip", "quant.hip", "gemm_i8.hip", "gemm_q4.hip", "skinny.hip", "cache.hip", "attn.hip"]
+SOURCES = ["api.hip", "quant.hip", "gemm_i8.hip", "gemm_q4.hip", "skinny.hip", "cache.hip", "attn.hip", "flash.hip"]
 
 # -ffp-contract=off: the quantizer and the dequantization epilogues are defined
 # by separately rounded fp32 operations; explicit fmaf() stays fused.

@@ -294,6 +294,27 @@ qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void*
   return st;
 }
 
+qsvd_status qsvd_prefill_attention(const void* q, const void* k, const void* v, int32_t batch,
+                                   const int32_t* cu_seqlens, int32_t max_seqlen, int32_t n_q_heads,
+                                   int32_t n_kv_heads, int32_t head_dim, float sm_scale, void* out, void* stream) {
+  if (batch < 0 || max_seqlen < 0) return fail(QSVD_ERR_INVALID_ARG, "batch and max_seqlen must be >= 0");
+  if (n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0) return fail(QSVD_ERR_INVALID_ARG, "head sizes must be positive");
+  if (n_q_heads % n_kv_heads)
+    return fail(QSVD_ERR_INVALID_ARG, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)", n_q_heads, n_kv_heads);
+  if (!(sm_scale >= 0.f) || isinf(sm_scale)) return fail(QSVD_ERR_INVALID_ARG, "sm_scale must be finite and >= 0");
+  if (batch == 0 || max_seqlen == 0) return QSVD_OK;
+  if (!q || !k || !v || !out || !cu_seqlens) return fail(QSVD_ERR_INVALID_ARG, "NULL pointer");
+  if (!prefill_attention_supported(head_dim)) return fail(QSVD_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
+    return fail(QSVD_ERR_UNSUPPORTED, "q, k, v and out must be 16-byte aligned");
+  if ((int64_t)batch * n_q_heads * ((max_seqlen + 127) / 128) > INT32_MAX)
+    return fail(QSVD_ERR_UNSUPPORTED, "batch * n_q_heads * ceil(max_seqlen / 128) exceeds the grid");
+  PrefillAttnArgs a{(const _Float16*)q, (const _Float16*)k, (const _Float16*)v, cu_seqlens, batch, max_seqlen,
+                    n_q_heads, n_kv_heads, head_dim, sm_scale > 0.f ? sm_scale : 1.f / sqrtf((float)head_dim),
+                    (_Float16*)out};
+  return hip_status(launch_prefill_attention(a, (hipStream_t)stream), "prefill attention");
+}
+
 size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int32_t q_len, int32_t mode) {
   if (!w || !c || q_len < 1) return 0;
   if (c->batch <= 0 || c->capacity <= 0 || w->r <= 0) return 0;

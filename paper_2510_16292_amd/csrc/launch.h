@@ -109,4 +109,18 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s);
 bool rope_latent_supported(const qsvd_layer& w, const qsvd_cache& c);
 hipError_t launch_attn_rope_latent(const AttnArgs& a, void* ws, hipStream_t s);
 
+// Causal prefill attention over the projection's own Q, K, V (token-major,
+// sequences back to back at cu_seqlens).
+struct PrefillAttnArgs {
+  const _Float16* q;        // [M][n_q_heads * head_dim]
+  const _Float16* k;        // [M][n_kv_heads * head_dim]
+  const _Float16* v;
+  const int32_t* cu_seqlens;  // device [batch + 1]
+  int32_t batch, max_seqlen, n_q_heads, n_kv_heads, head_dim;
+  float sm_scale;
+  _Float16* out;            // [M][n_q_heads * head_dim]
+};
+bool prefill_attention_supported(int32_t head_dim);
+hipError_t launch_prefill_attention(const PrefillAttnArgs& a, hipStream_t s);
+
 }  // namespace qsvd

@@ -137,3 +137,17 @@ def close_enough(got, want, max_abs=2e-2, rel_l2=1e-2):
     err = np.abs(got - want)
     rel = np.linalg.norm(got - want) / max(np.linalg.norm(want), 1e-30)
     return err.max() <= max_abs and rel <= rel_l2, (float(err.max()), float(rel), float(np.sqrt(np.mean(want ** 2))))
+
+
+def prefill_attention(q_dev, k_dev, v_dev, lengths, n_q_heads, n_kv_heads, head_dim, max_seqlen=None, sm_scale=0.0):
+    """Causal prefill attention of sequences back to back (lengths) over the
+    device Q, K, V rows; returns the device output."""
+    t = torch()
+    cu = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    cu_d = dev(cu)
+    out = t.empty_like(q_dev)
+    ms = max(lengths) if max_seqlen is None else max_seqlen
+    B.check(B.qsvd_prefill_attention(B.ptr(q_dev), B.ptr(k_dev), B.ptr(v_dev), len(lengths), B.ptr(cu_d), ms,
+                                     n_q_heads, n_kv_heads, head_dim, sm_scale, B.ptr(out), B.stream_handle()))
+    t.cuda.synchronize()
+    return out

@@ -178,6 +178,25 @@ def test_cache_append_validation(lib):
     assert B.qsvd_latent_cache_append(cache_struct(seq_len=0), FAKE, 0, 0, 1, 0) == B.QSVD_ERR_INVALID_ARG
 
 
+def test_prefill_attention_validation(lib):
+    """Every case fails (or returns OK with nothing to do) before a launch."""
+    def call(q=FAKE, k=FAKE, v=FAKE, batch=2, cu=FAKE, ms=64, hq=4, hkv=2, dh=64, sm=0.0, out=FAKE):
+        return B.qsvd_prefill_attention(q, k, v, batch, cu, ms, hq, hkv, dh, sm, out, 0)
+    assert call(batch=-1) == B.QSVD_ERR_INVALID_ARG
+    assert call(ms=-1) == B.QSVD_ERR_INVALID_ARG
+    assert call(hq=0) == B.QSVD_ERR_INVALID_ARG
+    assert call(hq=6, hkv=4) == B.QSVD_ERR_INVALID_ARG
+    assert call(sm=-1.0) == B.QSVD_ERR_INVALID_ARG
+    assert call(sm=float("inf")) == B.QSVD_ERR_INVALID_ARG
+    assert call(batch=0) == B.QSVD_OK
+    assert call(ms=0) == B.QSVD_OK
+    assert call(q=0) == B.QSVD_ERR_INVALID_ARG
+    assert call(cu=0) == B.QSVD_ERR_INVALID_ARG
+    assert call(dh=96) == B.QSVD_ERR_UNSUPPORTED
+    assert call(dh=32) == B.QSVD_ERR_UNSUPPORTED
+    assert call(out=FAKE + 8) == B.QSVD_ERR_UNSUPPORTED
+
+
 def _decode(layer, cache, q_len=1, mode=0, sm=0.0, ws=FAKE, ws_bytes=1 << 40, q=FAKE, out=FAKE):
     return B.qsvd_latent_decode_attention(layer, cache, q, q_len, mode, sm, out, ws, ws_bytes, 0)
 

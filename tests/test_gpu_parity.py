@@ -491,6 +491,89 @@ def test_cache_snapshot_resume(tiny, fmt):
         assert list(first[2]) == list(again[2]) == [23, 23]
 
 
+# ------------------------------------------------------------------ f1: prefill attention over Q, K, V
+
+def test_prefill_attention_flash_tiny_end_to_end(tiny):
+    """Tiny layer (4 heads x 64): the 64 prefill tokens through the projection
+    (Q, K, V bit-exact against the oracle), then causal attention over the
+    projection's own rows, against the oracle's plain definition."""
+    wl, ol, dl = tiny
+    X = gen.prefill_activations(wl)
+    ref = O.prefill(ol, X, 8)
+    L = wl.layer
+    H.say("prefill flash tiny")
+    p = H.Prefill(dl, 64, mask=7, debug=False).run(H.dev(X))
+    for name, t in (("Q", p.q), ("K", p.k), ("V", p.v)):
+        assert np.array_equal(H.host(t).view(np.uint16), ref[name].view(np.uint16)), name
+    out = H.host(H.prefill_attention(p.q, p.k, p.v, [64], L.n_q_heads, L.n_kv_heads, L.head_dim))
+    want = O.prefill_attention(ref["Q"], ref["K"], ref["V"], [64], L.n_q_heads, L.n_kv_heads, L.head_dim)
+    ok, info = H.close_enough(out, want)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+    # the last row equals the latent-cache attention of the same query at that position
+    oc = O.LatentCache(O.CACHE_F16, 1, 64, L.r)
+    oc.append(0, ref["C_h"])
+    last = O.attention_reference(ol, oc, ref["Q"][None, -1:], 1)[0, 0]
+    assert np.abs(out[-1].astype(np.float64) - last).max() <= 2e-2
+
+
+def _qkv(seed, M, hq, hkv, dh, scale=1.0):
+    return (gen.random_rows(seed, (M, hq * dh), scale), gen.random_rows(seed + 1, (M, hkv * dh), scale),
+            gen.random_rows(seed + 2, (M, hkv * dh), 1.0))
+
+
+@pytest.mark.parametrize("shape,lengths", [
+    ((8, 2, 64), [1, 45, 130]),          # grouped, ragged: one row, a partial tile, two query tiles
+    ((4, 4, 128), [0, 200, 129, 1]),     # an empty sequence, tile edges at 128 + 1
+    ((28, 4, 128), [640, 300]),          # Qwen2-VL-shaped grouping
+], ids=["gqa8-2-dh64", "mha4-dh128-empty", "qwen28-4"])
+def test_prefill_attention_flash_ragged(shape, lengths):
+    """Causal prefill attention over seeded Q, K, V rows against the oracle,
+    over ragged sequence lengths and grouped heads."""
+    hq, hkv, dh = shape
+    M = sum(lengths)
+    Q, K, V = _qkv(300 + hq, M, hq, hkv, dh)
+    H.say(f"prefill flash heads={hq}/{hkv} dh={dh} lengths={lengths}")
+    out = H.host(H.prefill_attention(H.dev(Q), H.dev(K), H.dev(V), lengths, hq, hkv, dh))
+    want = O.prefill_attention(Q, K, V, lengths, hq, hkv, dh)
+    ok, info = H.close_enough(out, want)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+
+
+def test_prefill_attention_flash_llava7b_full():
+    """The LLaVA-1.5-7B-shaped prompt batch at full size (4 x 640 tokens,
+    32 heads x 128) in the bench's launch configuration, every output row
+    against the oracle; then the same rows with ragged lengths (640, 640, 620,
+    660) and a larger max_seqlen than any length; run twice bit-identically."""
+    hq, hkv, dh = 32, 32, 128
+    Q, K, V = _qkv(700, 2560, hq, hkv, dh)
+    qd, kd, vd = H.dev(Q), H.dev(K), H.dev(V)
+    for lengths, ms in (([640] * 4, 640), ([640, 640, 620, 660], 700)):
+        H.say(f"prefill flash llava7b lengths={lengths} max_seqlen={ms}")
+        out = H.host(H.prefill_attention(qd, kd, vd, lengths, hq, hkv, dh, max_seqlen=ms))
+        want = O.prefill_attention(Q, K, V, lengths, hq, hkv, dh)
+        ok, info = H.close_enough(out, want)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, info
+    again = H.host(H.prefill_attention(qd, kd, vd, [640, 640, 620, 660], hq, hkv, dh, max_seqlen=700))
+    assert np.array_equal(again.view(np.uint16), out.view(np.uint16))
+
+
+def test_prefill_attention_flash_13b_two_sequences():
+    """The 13B-shaped prompt (40 heads x 128, 704 = 576 + 128 tokens per
+    sequence) on two of the batch's eight sequences, against the oracle, with
+    queries scaled so that the softmax is peaked."""
+    hq, hkv, dh = 40, 40, 128
+    Q, K, V = _qkv(800, 1408, hq, hkv, dh, scale=2.0)
+    H.say("prefill flash 13b two sequences")
+    out = H.host(H.prefill_attention(H.dev(Q), H.dev(K), H.dev(V), [704, 704], hq, hkv, dh))
+    want = O.prefill_attention(Q, K, V, [704, 704], hq, hkv, dh)
+    ok, info = H.close_enough(out, want)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+
+
 # ------------------------------------------------------------------ a5-a7: decode attention
 
 @pytest.mark.parametrize("mode", MODES, ids=MODE_IDS)
