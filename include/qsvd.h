@@ -225,6 +225,22 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
                                          float sm_scale, void* out,
                                          void* ws, size_t ws_bytes, void* stream);
 
+/* qsvd_latent_decode_attention without a caller workspace, for callers that
+ * cannot allocate device memory (code under graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments, forms, results
+ * and errors as qsvd_latent_decode_attention (and the same kernels); its
+ * partial results live in a static device array of
+ * qsvd_noalloc_scratch_bytes() bytes (32 MiB), one per GPU, held from the
+ * first call on that GPU until the process ends.  A call whose workspace
+ * query exceeds that size returns QSVD_ERR_WORKSPACE before any GPU work.
+ * Calls nothing that allocates.  Every call on one GPU shares its array:
+ * calls that may overlap on one GPU (other streams, other threads) race and
+ * must be ordered by the caller. */
+qsvd_status qsvd_latent_decode_attention_noalloc(const qsvd_layer* w, const qsvd_cache* c,
+                                                 const void* q, int32_t q_len, int32_t mode,
+                                                 float sm_scale, void* out, void* stream);
+size_t qsvd_noalloc_scratch_bytes(void);
+
 /* The same attention for layers that apply a rotary position embedding to q
  * and k (the paper's layers have none; this is the position-encoded variant
  * of Section 3.1's decode step).  Every rebuilt key row at position t and the

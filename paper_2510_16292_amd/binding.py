@@ -21,7 +21,7 @@ EXPORTED = [
     "qsvd_quantize_act", "qsvd_quantize_act_rotated", "qsvd_lowrank_qkv_prefill", "qsvd_prefill_workspace_size",
     "qsvd_latent_cache_append", "qsvd_prefill_attention", "qsvd_latent_decode_attention",
     "qsvd_latent_decode_attention_rope",
-    "qsvd_decode_workspace_size",
+    "qsvd_decode_workspace_size", "qsvd_latent_decode_attention_noalloc", "qsvd_noalloc_scratch_bytes",
     "qsvd_status_string", "qsvd_last_error", "qsvd_profile_enable", "qsvd_profile_reset",
     "qsvd_profile_read",
 ]
@@ -73,6 +73,8 @@ def lib():
             "qsvd_latent_decode_attention": (I32, [LP, CP, P, I32, I32, F, P, P, SZ, P]),
             "qsvd_latent_decode_attention_rope": (I32, [LP, CP, P, I32, I32, F, F, P, P, SZ, P]),
             "qsvd_decode_workspace_size": (SZ, [LP, CP, I32, I32]),
+            "qsvd_latent_decode_attention_noalloc": (I32, [LP, CP, P, I32, I32, F, P, P]),
+            "qsvd_noalloc_scratch_bytes": (SZ, []),
             "qsvd_status_string": (ctypes.c_char_p, [I32]),
             "qsvd_last_error": (ctypes.c_char_p, []),
             "qsvd_profile_enable": (I32, [I32, ctypes.c_char_p]),
@@ -125,6 +127,15 @@ def qsvd_latent_decode_attention_rope(layer, cache, q, q_len, mode, sm_scale, ro
                                       stream):
     return lib().qsvd_latent_decode_attention_rope(ctypes.byref(layer), ctypes.byref(cache), q, q_len, mode,
                                                    sm_scale, rope_theta, out, ws, ws_bytes, stream)
+
+
+def qsvd_latent_decode_attention_noalloc(layer, cache, q, q_len, mode, sm_scale, out, stream):
+    return lib().qsvd_latent_decode_attention_noalloc(ctypes.byref(layer), ctypes.byref(cache), q, q_len, mode,
+                                                      sm_scale, out, stream)
+
+
+def qsvd_noalloc_scratch_bytes():
+    return lib().qsvd_noalloc_scratch_bytes()
 
 
 def qsvd_decode_workspace_size(layer, cache, q_len, mode):

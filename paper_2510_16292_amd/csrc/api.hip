@@ -326,9 +326,41 @@ size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int3
   return attn_absorbed_workspace(*w, *c, q_len);
 }
 
+// ---------------------------------------------------------------- static scratch
+// Device scratch of the allocation-free decode attention: one array per GPU,
+// held until the process ends.  Host code never passes `scratch` itself to a
+// kernel (in host code the name is a host-side stand-in); it uses the device
+// address that hipGetSymbolAddress returns for the current device, looked up
+// once per device.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices] = {};
+
+static qsvd_status scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "static scratch: hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(QSVD_ERR_UNSUPPORTED, "device %d beyond the scratch table", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "static scratch: hipGetSymbolAddress");
+    if (!p) return fail(QSVD_ERR_HIP, "static scratch: NULL symbol address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return QSVD_OK;
+}
+
+// use_scratch: the workspace is the device's static scratch array instead of
+// the caller's (ws, ws_bytes are then ignored).
 static qsvd_status decode_attention(const qsvd_layer* w, const qsvd_cache* c, const void* q, int32_t q_len,
                                     int32_t mode, float sm_scale, float rope_theta, void* out, void* ws,
-                                    size_t ws_bytes, void* stream) {
+                                    size_t ws_bytes, void* stream, bool use_scratch = false) {
   qsvd_status st = check_layer(w);
   if (st != QSVD_OK) return st;
   st = check_cache(c);
@@ -363,6 +395,14 @@ static qsvd_status decode_attention(const qsvd_layer* w, const qsvd_cache* c, co
   if (!absorbed && c->capacity > 16384)
     return fail(QSVD_ERR_UNSUPPORTED, "reconstruct form supports capacity <= 16384");
   const size_t need = absorbed && !rope ? attn_absorbed_workspace(*w, *c, q_len) : attn_reconstruct_workspace(*w, *c);
+  if (use_scratch) {
+    if (need > kScratchBytes)
+      return fail(QSVD_ERR_WORKSPACE, "this call needs %zu bytes of scratch, more than the %zu-byte static array",
+                  need, kScratchBytes);
+    st = scratch_address(&ws);
+    if (st != QSVD_OK) return st;
+    ws_bytes = kScratchBytes;
+  }
   if (!ws || ws_bytes < need) return fail(QSVD_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   AttnArgs a{w, c, (const _Float16*)q, (_Float16*)out, sm_scale > 0.f ? sm_scale : 1.f / sqrtf((float)w->head_dim),
              q_len, rope ? rope_theta : 0.f};
@@ -378,6 +418,14 @@ qsvd_status qsvd_latent_decode_attention(const qsvd_layer* w, const qsvd_cache* 
                                          void* stream) {
   return decode_attention(w, c, q, q_len, mode, sm_scale, 0.f, out, ws, ws_bytes, stream);
 }
+
+qsvd_status qsvd_latent_decode_attention_noalloc(const qsvd_layer* w, const qsvd_cache* c, const void* q,
+                                                 int32_t q_len, int32_t mode, float sm_scale, void* out,
+                                                 void* stream) {
+  return decode_attention(w, c, q, q_len, mode, sm_scale, 0.f, out, nullptr, 0, stream, true);
+}
+
+size_t qsvd_noalloc_scratch_bytes(void) { return kScratchBytes; }
 
 qsvd_status qsvd_latent_decode_attention_rope(const qsvd_layer* w, const qsvd_cache* c, const void* q, int32_t q_len,
                                               int32_t mode, float sm_scale, float rope_theta, void* out, void* ws,

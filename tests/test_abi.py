@@ -197,6 +197,24 @@ def test_prefill_attention_validation(lib):
     assert call(out=FAKE + 8) == B.QSVD_ERR_UNSUPPORTED
 
 
+def test_noalloc_decode_validation(lib):
+    """The allocation-free decode attention validates like the workspace entry
+    point and refuses a call whose scratch need exceeds the static array, all
+    before any GPU work."""
+    assert B.qsvd_noalloc_scratch_bytes() == 32 << 20
+    L, C = layer_struct(), cache_struct()
+    call = lambda layer, cache, q_len=1, mode=0: B.qsvd_latent_decode_attention_noalloc(layer, cache, FAKE, q_len,
+                                                                                      mode, 0.0, FAKE, 0)
+    assert call(L, C, q_len=0) == B.QSVD_ERR_INVALID_ARG
+    assert call(L, C, mode=3) == B.QSVD_ERR_INVALID_ARG
+    assert call(L, cache_struct(r=256)) == B.QSVD_ERR_INVALID_ARG
+    wide = layer_struct(d=5120, r=3072, n_q_heads=40, n_kv_heads=40, head_dim=128)
+    big = cache_struct(batch=64, capacity=4096, r=3072, max_len=4096)
+    assert B.qsvd_decode_workspace_size(wide, big, 1, B.QSVD_ATTN_AUTO) > B.qsvd_noalloc_scratch_bytes()
+    assert call(wide, big) == B.QSVD_ERR_WORKSPACE
+    assert "static" in B.last_error()
+
+
 def _decode(layer, cache, q_len=1, mode=0, sm=0.0, ws=FAKE, ws_bytes=1 << 40, q=FAKE, out=FAKE):
     return B.qsvd_latent_decode_attention(layer, cache, q, q_len, mode, sm, out, ws, ws_bytes, 0)
 
