@@ -68,6 +68,38 @@ __device__ inline f16x8 cvt_i4x8(uint32_t w) {
   return r;
 }
 
+// Max and sum of a value over the four 16-lane rows of a wave (lanes l, l ^ 16,
+// l ^ 32, l ^ 48), every lane receiving the result, at vector-ALU latency
+// with gfx950's lane swaps: v_permlane32_swap a, b exchanges rows 2-3 of a
+// with rows 0-1 of b (a row is 16 lanes) and v_permlane16_swap a, b rows 1, 3
+// of a with rows 0, 2 of b, so with a = b = x the pair (a, b) holds each
+// lane's value and its partner's.  (Issued as asm with both registers
+// read-write: the compiler builtin's second result is not usable here; the
+// s_nop covers the hazard of a vector write just before the swap.)  The sum
+// adds in the same order in every lane.
+__device__ __forceinline__ void swap32(uint32_t& a, uint32_t& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void swap16(uint32_t& a, uint32_t& b) {
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+
+__device__ __forceinline__ float rows4_max(float x) {
+  uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
+  swap32(a, b);
+  uint32_t c = __builtin_bit_cast(uint32_t, fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b))), e = c;
+  swap16(c, e);
+  return fmaxf(__builtin_bit_cast(float, c), __builtin_bit_cast(float, e));
+}
+
+__device__ __forceinline__ float rows4_sum(float x) {
+  uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
+  swap32(a, b);
+  uint32_t c = __builtin_bit_cast(uint32_t, __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b)), e = c;
+  swap16(c, e);
+  return __builtin_bit_cast(float, c) + __builtin_bit_cast(float, e);
+}
+
 // ---------------------------------------------------------------------------
 // q~ = scale * q W^u_k^T on the 16x16x32 fp16 matrix cores.  One wave per
 // (head h, 64 latent columns j): the dh x 64 block of W^u_k codes (rows
@@ -556,9 +588,234 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
 // The C tile reaches the first product straight from HBM (one 16-byte load
 // per lane serves 1, 2 or 4 contraction steps for fp16, int8, int4 rows) and
 // the second through a wave-private LDS copy read with transposing loads.
+//
+// Each wave keeps the next D tiles of its slice in flight in a ring of
+// registers (D = 2, 3, 4 for fp16, int8, int4 rows: a 16-token tile of a
+// narrow integer slice is only 0.5-1 KB per wave, so one tile in flight leaves
+// every tile waiting a full memory round trip).  The loads are unconditional
+// (rows past the chunk end re-read its last row and are masked), so the
+// compiler can count them and wait only for the tile it is about to use; the
+// unit count of a wave is a template parameter, so no product or fragment read
+// sits behind a per-wave branch.
 // ---------------------------------------------------------------------------
 constexpr int kH16Waves = 8;
-constexpr int kH16Tile = 16;
+
+// Tokens per tile: 32 (two 16-token blocks per barrier pair) while a
+// workgroup's fp16 staging of them fits LDS (two 128-column units per wave),
+// else 16.
+template <int UMAX>
+struct H16Blocks {
+  static constexpr int value = UMAX <= 2 ? 2 : 1;
+};
+
+// Ring depth: two tiles where the registers allow, one for fp16 rows, int8
+// rows in 32-token tiles and three units per wave (whose accumulators take 96
+// registers).  (Deeper rings measured slower: the tile body is unrolled once
+// per slot.)
+template <int UMAX, int U, int FMT>
+struct H16Depth {
+  static constexpr int value =
+      (FMT == QSVD_CACHE_F16 || U >= 3 || (FMT == QSVD_CACHE_I8 && H16Blocks<UMAX>::value == 2)) ? 1 : 2;
+};
+
+template <int UMAX>
+constexpr size_t h16_lds_bytes() {
+  constexpr int NB = H16Blocks<UMAX>::value;
+  return (size_t)kH16Waves * 16 * NB * (128 * UMAX + 16) * 2 + (size_t)(kH16Waves + 1) * NB * 64 * 16;
+}
+
+// One wave's pass over the chunk [t_begin, t_end) for a wave owning U units
+// of 128 latent columns starting at slice0 (U may be 0: the wave then only
+// takes part in the exchange and the softmax).  Tiles of T = 16 NB tokens,
+// token block bb of a tile being tokens t0 + 16 bb .. +15.
+template <int UMAX, int U, int FMT>
+__device__ __forceinline__ void h16_wave(const _Float16* __restrict__ qrow, const uint8_t* __restrict__ cdata,
+                                         const float* __restrict__ cscale, int64_t seq_row0, int r, int L,
+                                         int t_begin, int t_end, int slice0, _Float16* cst, f32x4* spart,
+                                         f32x4* ssum, int w, int lane, _Float16* __restrict__ op,
+                                         float* __restrict__ mlp) {
+  constexpr int NW = kH16Waves, NB = H16Blocks<UMAX>::value, T = 16 * NB;
+  constexpr int D = H16Depth<UMAX, U, FMT>::value;
+  constexpr bool F16C = FMT == QSVD_CACHE_F16, I4C = FMT == QSVD_CACHE_I4;
+  constexpr int KS = 4 * U;                              // 32-wide contraction steps of the score product
+  constexpr int RB = 8 * U;                              // 16-row blocks of the output product
+  constexpr int NLD = F16C ? KS : (I4C ? U : KS / 2);    // 16-byte loads per token block
+  constexpr int NLDA = NLD > 0 ? NLD : 1, KSA = KS > 0 ? KS : 1, RBA = RB > 0 ? RB : 1;
+  constexpr int CST = 128 * UMAX + 16;                   // staged row stride in halves: 8 (mod 64) dwords
+  const int l16 = lane & 15, g = lane >> 4;
+  // contraction slots of the score product: in step ks, lane group g feeds
+  // latent columns slice0 + kcol(ks, g) .. +7 of token t0 + 16 bb + l16
+  auto kcol = [](int ks, int gg) {
+    return F16C ? 32 * ks + 8 * gg : (I4C ? 128 * (ks >> 2) + 32 * gg + 8 * (ks & 3) : 64 * (ks >> 1) + 16 * gg + 8 * (ks & 1));
+  };
+  f16x8 qf[KSA];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, g));
+  f32x4 o[RBA];
+#pragma unroll
+  for (int rb = 0; rb < RBA; ++rb) o[rb] = f32x4{};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  i32x4 raw[D][NB][NLDA];
+  float scr[D][NB];      // integer rows: the scale of token t0 + 16 bb + l16
+  // tile starting at t0 into ring slot d (every load unconditional)
+  auto load = [&](int d, int t0) {
+#pragma unroll
+    for (int bb = 0; bb < NB; ++bb) {
+      const int t = t0 + 16 * bb + l16;
+      if constexpr (!F16C) scr[d][bb] = cscale[seq_row0 + min(t, L - 1)];
+      const int64_t off = (seq_row0 + min(t, t_end - 1)) * r + slice0;    // element index of the row slice
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        if constexpr (F16C)
+          raw[d][bb][i] = *reinterpret_cast<const i32x4*>(reinterpret_cast<const _Float16*>(cdata) + off + kcol(i, g));
+        else if constexpr (I4C)
+          raw[d][bb][i] = *reinterpret_cast<const i32x4*>(cdata + (off + 128 * i + 32 * g) / 2);
+        else
+          raw[d][bb][i] = *reinterpret_cast<const i32x4*>(cdata + off + 64 * i + 16 * g);
+      }
+    }
+  };
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+#pragma unroll
+  for (int d = 0; d < D; ++d) load(d, t_begin + T * d);
+  for (int base = t_begin; base < t_end; base += T * D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int t0 = base + T * d;
+      // scales of the tokens t0 + 16 bb + 4g + v this lane's scores belong to
+      float sc_cur[NB][4];
+#pragma unroll
+      for (int bb = 0; bb < NB; ++bb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sc_cur[bb][v] = F16C ? 1.f : __shfl(scr[d][bb], 4 * g + v, 64);
+      f32x4 sacc[NB];
+#pragma unroll
+      for (int bb = 0; bb < NB; ++bb) {
+        sacc[bb] = f32x4{};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          f16x8 cf;
+          if constexpr (F16C) {
+            cf = __builtin_bit_cast(f16x8, raw[d][bb][ks]);
+          } else if constexpr (I4C) {
+            const i32x4 q4 = raw[d][bb][ks >> 2];
+            cf = cvt_i4x8((uint32_t)q4[ks & 3]);
+          } else {
+            const i32x4 q8 = raw[d][bb][ks >> 1];
+            cf = (ks & 1) ? cvt_i8x8((uint32_t)q8[2], (uint32_t)q8[3]) : cvt_i8x8((uint32_t)q8[0], (uint32_t)q8[1]);
+          }
+          sacc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(cf, qf[ks], sacc[bb], 0, 0, 0);
+          *reinterpret_cast<f16x8*>(cst + (16 * bb + l16) * CST + kcol(ks, g)) = cf;
+        }
+      }
+      // the slot is refilled D tiles ahead while this tile is reduced and multiplied
+      load(d, t0 + T * D);
+#pragma unroll
+      for (int bb = 0; bb < NB; ++bb) spart[(bb * NW + w) * 64 + lane] = sacc[bb];
+      __syncthreads();
+      // every wave adds, in wave order, the partials of 8 of the 64 lanes of each token block
+      if (lane < 8 * NB) {
+        const int bb = lane >> 3, ln = 8 * w + (lane & 7);
+        f32x4 parts[NW];
+#pragma unroll
+        for (int w2 = 0; w2 < NW; ++w2) parts[w2] = spart[(bb * NW + w2) * 64 + ln];
+        f32x4 acc = parts[0];
+#pragma unroll
+        for (int w2 = 1; w2 < NW; ++w2) acc += parts[w2];
+        ssum[bb * 64 + ln] = acc;
+      }
+      __syncthreads();
+      // lane holds head l16 at tokens t0 + 16 bb + 4g + v
+      float s[NB][4];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int bb = 0; bb < NB; ++bb) {
+        const f32x4 sv = ssum[bb * 64 + lane];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          float x = sv[v];
+          if constexpr (!F16C) x *= sc_cur[bb][v];
+          s[bb][v] = (t0 + 16 * bb + 4 * g + v < t_end) ? x : -INFINITY;
+          mx = fmaxf(mx, s[bb][v]);
+        }
+      }
+      const float m_new = fmaxf(m_run, rows4_max(mx));
+      float alpha = 1.f, ps = 0.f;
+      float p[NB][4];
+      if (m_new == -INFINITY) {
+#pragma unroll
+        for (int bb = 0; bb < NB; ++bb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) p[bb][v] = 0.f;
+      } else {
+        alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+        for (int bb = 0; bb < NB; ++bb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            p[bb][v] = __builtin_amdgcn_exp2f(s[bb][v] - m_new);
+            ps += p[bb][v];
+          }
+      }
+      l_run = l_run * alpha + rows4_sum(ps);
+      m_run = m_new;
+      if (__any(alpha != 1.f)) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) o[rb] *= alpha;
+      }
+      // P^T as the B operand, scaled per token: k-slot e of lane group g is
+      // token 16 (e / 4) + 4g + e % 4 (one 16-token block: token 4g + e).
+      // A operand: lane (l16, g) needs latent column 16rb + l16 at the same
+      // tokens.  In a transposing read, lane a of group g addresses token
+      // 4g + a/4 (of the block), columns 16rb + 4(a%4) .. +3, and lane i
+      // receives element i%4 of the chunks of lanes i/4, 4 + i/4, 8 + i/4,
+      // 12 + i/4: column 16rb + i at tokens 4g .. 4g+3 of the block.
+      if constexpr (NB == 1) {
+        f16x4 pf;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) pf[e] = (_Float16)(F16C ? p[0][e] : p[0][e] * sc_cur[0][e]);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_s16x4*)(cst + (4 * g + (l16 >> 2)) * CST + 16 * rb + 4 * (l16 & 3)));
+          o[rb] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, x), pf, o[rb], 0, 0, 0);
+        }
+      } else {
+        f16x8 pf;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[e] = (_Float16)(F16C ? p[e >> 2][e & 3] : p[e >> 2][e & 3] * sc_cur[e >> 2][e & 3]);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const _Float16* a0 = cst + (4 * g + (l16 >> 2)) * CST + 16 * rb + 4 * (l16 & 3);
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)a0);
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(a0 + 16 * CST));
+          const f16x4 flo = __builtin_bit_cast(f16x4, lo), fhi = __builtin_bit_cast(f16x4, hi);
+          const f16x8 a = {flo[0], flo[1], flo[2], flo[3], fhi[0], fhi[1], fhi[2], fhi[3]};
+          o[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, pf, o[rb], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  if (w == 0 && lane < 16) {
+    mlp[l16] = m_run;
+    mlp[16 + l16] = l_run;
+  }
+  // O^T / l as fp16 in [x/4][16 heads][4] order: lane (head l16, g) holds
+  // latent columns slice0 + 16rb + 4g .. +3, so each store writes 512
+  // contiguous bytes; non-temporal, as in the 32-head kernel.
+  const float inv_l = l_run > 0.f ? 1.f / l_run : 0.f;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int x4 = (slice0 + 16 * rb + 4 * g) >> 2;
+    const f16x4 v4 = {(_Float16)(o[rb][0] * inv_l), (_Float16)(o[rb][1] * inv_l), (_Float16)(o[rb][2] * inv_l),
+                      (_Float16)(o[rb][3] * inv_l)};
+    __builtin_nontemporal_store(v4, reinterpret_cast<f16x4*>(op + ((int64_t)x4 * 16 + l16) * 4));
+  }
+}
 
 template <int UMAX, int FMT>
 __global__ void __launch_bounds__(kH16Waves * 64)
@@ -566,19 +823,14 @@ latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restric
                        const float* __restrict__ cscale, const int32_t* __restrict__ seq_len,
                        int32_t capacity, int32_t r, int32_t hp, int32_t chunk, int32_t n_chunks,
                        int32_t q_len, _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
-  constexpr int NW = kH16Waves;
-  constexpr int KS = 4 * UMAX;          // 32-wide contraction steps of the score product
-  constexpr int RB = 8 * UMAX;          // 16-row blocks of the output product
-  constexpr int CST = 128 * UMAX + 16;  // staged row stride in halves: 8 (mod 64) dwords
-  constexpr bool F16C = FMT == QSVD_CACHE_F16, I4C = FMT == QSVD_CACHE_I4;
-  constexpr int NLD = F16C ? KS : (I4C ? KS / 4 : KS / 2);   // 16-byte loads per row slice
+  constexpr int NW = kH16Waves, NB = H16Blocks<UMAX>::value;
+  constexpr int CST = 128 * UMAX + 16;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int l16 = lane & 15, g = lane >> 4;
   const int wu = __builtin_amdgcn_readfirstlane(w);     // wave-uniform copy: scalar branches below
-  _Float16* cst = reinterpret_cast<_Float16*>(smem) + w * kH16Tile * CST;
-  f32x4* spart = reinterpret_cast<f32x4*>(smem + (size_t)NW * kH16Tile * CST * 2);
-  f32x4* ssum = spart + NW * 64;
+  _Float16* cst = reinterpret_cast<_Float16*>(smem) + w * 16 * NB * CST;
+  f32x4* spart = reinterpret_cast<f32x4*>(smem + (size_t)NW * 16 * NB * CST * 2);
+  f32x4* ssum = spart + NB * NW * 64;
 
   const int n_hb = hp >> 4;
   // Workgroup -> (sequence-query row vb, head block hb, chunk ch).  The n_hb
@@ -603,162 +855,22 @@ latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restric
   const int t_begin = ch * chunk;
   if (t_begin >= L) return;
   const int t_end = min(L, t_begin + chunk);
-  // this wave's latent units [u0, u0 + nu) of 128 columns (nu <= UMAX, may be 0)
+  // this wave's latent units [u0, u0 + nu) of 128 columns: nu is UMAX or UMAX - 1
   const int m_units = r >> 7;
   const int u0 = (wu * m_units) / NW, nu = ((wu + 1) * m_units) / NW - u0;
-  const int slice0 = 128 * u0, ksn = 4 * nu;
-  const int nldn = F16C ? ksn : (I4C ? nu : ksn / 2);
-
-  // Contraction slots of the score product: in step ks, lane group g feeds
-  // latent columns slice0 + kcol(ks, g) .. +7 of token t0 + l16, and the
-  // query slots follow the same map.
-  auto kcol = [](int ks, int gg) {
-    return F16C ? 32 * ks + 8 * gg : (I4C ? 128 * (ks >> 2) + 32 * gg + 8 * (ks & 3) : 64 * (ks >> 1) + 16 * gg + 8 * (ks & 1));
-  };
-  f16x8 qf[KS];
-  {
-    const _Float16* qrow = qt + ((int64_t)vb * hp + hb * 16 + l16) * r + slice0;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      if (ks < ksn) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, g));
-  }
-  f32x4 o[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) o[rb] = f32x4{};
-  float m_run = -INFINITY, l_run = 0.f;
-
-  uint4 raw[NLD];
-  float sc_next[F16C ? 1 : 4], sc_cur[F16C ? 1 : 4];
-  auto load_tile = [&](int t0) {
-    if constexpr (!F16C) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) sc_next[v] = cscale[(int64_t)b * capacity + min(t0 + 4 * g + v, L - 1)];
-    }
-    // rows past the chunk end are masked; re-read the last row of the chunk
-    const int tk = min(t0 + l16, t_end - 1);
-    const int64_t off = ((int64_t)b * capacity + tk) * r + slice0;     // element index of the row slice
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      if (i >= nldn) continue;
-      if constexpr (F16C)
-        raw[i] = *reinterpret_cast<const uint4*>(reinterpret_cast<const _Float16*>(cdata) + off + kcol(i, g));
-      else if constexpr (I4C)
-        raw[i] = *reinterpret_cast<const uint4*>(cdata + (off + 128 * i + 32 * g) / 2);
-      else
-        raw[i] = *reinterpret_cast<const uint4*>(cdata + off + 64 * i + 16 * g);
-    }
-  };
-  typedef short s16x4 __attribute__((ext_vector_type(4)));
-  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-  load_tile(t_begin);
-  for (int t0 = t_begin; t0 < t_end; t0 += kH16Tile) {
-    if constexpr (!F16C) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) sc_cur[v] = sc_next[v];
-    }
-    f32x4 sacc = f32x4{};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (ks >= ksn) continue;
-      f16x8 cf;
-      if constexpr (F16C) {
-        cf = __builtin_bit_cast(f16x8, raw[ks]);
-      } else if constexpr (I4C) {
-        const uint4 q4 = raw[ks >> 2];
-        cf = cvt_i4x8((ks & 3) == 0 ? q4.x : (ks & 3) == 1 ? q4.y : (ks & 3) == 2 ? q4.z : q4.w);
-      } else {
-        const uint4 q8 = raw[ks >> 1];
-        cf = (ks & 1) ? cvt_i8x8(q8.z, q8.w) : cvt_i8x8(q8.x, q8.y);
-      }
-      sacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(cf, qf[ks], sacc, 0, 0, 0);
-      *reinterpret_cast<f16x8*>(cst + l16 * CST + kcol(ks, g)) = cf;
-    }
-    // the next tile streams in while this one is reduced and multiplied
-    if (t0 + kH16Tile < t_end) load_tile(t0 + kH16Tile);
-    spart[w * 64 + lane] = sacc;
-    __syncthreads();
-    if (w == 0) {
-      f32x4 acc = spart[lane];
-#pragma unroll
-      for (int w2 = 1; w2 < NW; ++w2) acc += spart[w2 * 64 + lane];
-      ssum[lane] = acc;
-    }
-    __syncthreads();
-    const f32x4 sv = ssum[lane];
-    // lane holds head l16 at tokens t0 + 4g + v
-    float s[4];
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      float x = sv[v];
-      if constexpr (!F16C) x *= sc_cur[v];
-      s[v] = (t0 + 4 * g + v < t_end) ? x : -INFINITY;
-    }
-    float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    float alpha = 1.f, ps = 0.f;
-    float p[4];
-    if (m_new == -INFINITY) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) p[v] = 0.f;
-    } else {
-      alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        p[v] = __builtin_amdgcn_exp2f(s[v] - m_new);
-        ps += p[v];
-      }
-    }
-    ps += __shfl_xor(ps, 16, 64);
-    ps += __shfl_xor(ps, 32, 64);
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-    if (__any(alpha != 1.f)) {
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) o[rb] *= alpha;
-    }
-    // P^T as the B operand: k-slot e of lane group g is token 4g + e, the
-    // tokens this lane's probabilities belong to.
-    f16x4 pf;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      float pv = p[e];
-      if constexpr (!F16C) pv *= sc_cur[e];
-      pf[e] = (_Float16)pv;
-    }
-    // A operand: lane (l16, g) needs latent column 16rb + l16 at tokens
-    // 4g .. 4g+3.  In the transposing read, lane a of group g addresses token
-    // 4g + a/4, columns 16rb + 4(a%4) .. +3, and lane i receives element i%4
-    // of the chunks of lanes i/4, 4 + i/4, 8 + i/4, 12 + i/4: column
-    // 16rb + i at tokens 4g .. 4g+3.
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      if (rb >= 2 * ksn) continue;
-      const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_s16x4*)(cst + (4 * g + (l16 >> 2)) * CST + 16 * rb + 4 * (l16 & 3)));
-      o[rb] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, x), pf, o[rb], 0, 0, 0);
-    }
-  }
-
+  const int slice0 = 128 * u0;
+  const int l16 = lane & 15;
+  const _Float16* qrow = qt + ((int64_t)vb * hp + hb * 16 + l16) * r + slice0;
   const int64_t part = (int64_t)row * n_chunks + ch;
-  if (w == 0 && lane < 16) {
-    ml_part[part * 32 + l16] = m_run;
-    ml_part[part * 32 + 16 + l16] = l_run;
-  }
-  // O^T / l as fp16 in [x/4][16 heads][4] order: lane (head l16, g) holds
-  // latent columns slice0 + 16rb + 4g .. +3, so each store writes 512
-  // contiguous bytes; non-temporal, as in the 32-head kernel.
-  const float inv_l = l_run > 0.f ? 1.f / l_run : 0.f;
   _Float16* op = o_part + part * (int64_t)r * 16;
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    if (rb >= 2 * ksn) continue;
-    const int x4 = (slice0 + 16 * rb + 4 * g) >> 2;
-    const f16x4 v4 = {(_Float16)(o[rb][0] * inv_l), (_Float16)(o[rb][1] * inv_l), (_Float16)(o[rb][2] * inv_l),
-                      (_Float16)(o[rb][3] * inv_l)};
-    __builtin_nontemporal_store(v4, reinterpret_cast<f16x4*>(op + ((int64_t)x4 * 16 + l16) * 4));
-  }
+  float* mlp = ml_part + part * 32;
+  const int64_t seq_row0 = (int64_t)b * capacity;
+  if (nu == UMAX)
+    h16_wave<UMAX, UMAX, FMT>(qrow, cdata, cscale, seq_row0, r, L, t_begin, t_end, slice0, cst, spart, ssum, w, lane,
+                              op, mlp);
+  else
+    h16_wave<UMAX, UMAX - 1, FMT>(qrow, cdata, cscale, seq_row0, r, L, t_begin, t_end, slice0, cst, spart, ssum, w,
+                                  lane, op, mlp);
 }
 
 // ---------------------------------------------------------------------------
@@ -1059,7 +1171,8 @@ static AbsorbPlan plan_absorbed(const qsvd_layer& w, const qsvd_cache& c, int32_
   p.n0 = p.hb == kHeadBlk ? target_chunks((int)grows) : (int)(grows >= 256 ? 1 : 256 / grows);
   const int len = c.max_len > 0 ? c.max_len : 1;
   int ch = (len + p.n0 - 1) / p.n0;
-  ch = ((ch + 15) / 16) * 16;
+  const int gran = p.hb == kHeadBlk ? 16 : 64;      // 16-head plans: whole tiles and ring rounds
+  ch = ((ch + gran - 1) / gran) * gran;
   p.chunk = ch;
   p.n_chunks = (len + ch - 1) / ch;
   p.qt_bytes = (size_t)rows * p.hp * w.r * sizeof(_Float16);
@@ -1104,7 +1217,7 @@ static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, int32_
 template <int UMAX, int FMT>
 static hipError_t launch_latent_h16(const AbsorbPlan& p, const qsvd_cache& c, int32_t q_len, const _Float16* qt,
                                     _Float16* opart, float* ml, hipStream_t s) {
-  const size_t lds = (size_t)kH16Waves * kH16Tile * (128 * UMAX + 16) * 2 + (size_t)(kH16Waves + 1) * 64 * 16;
+  const size_t lds = h16_lds_bytes<UMAX>();
   auto kern = latent_attn_h16_kernel<UMAX, FMT>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
