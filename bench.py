@@ -237,13 +237,22 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
     crefs = [ctypes.byref(c.c) for c in caches]
     f16 = fmt == B.QSVD_CACHE_F16
 
-    def step(i, s=s):
+    def step_unfused(i, s=s):
         li = i % n_layers
         st = lib.qsvd_quantize_act(xs_p[i % 8], batch, d, d, 8, 1.0, xq_p, sx_p, s)
         st |= lib.qsvd_lowrank_qkv_prefill(lrefs[li], xq_p, sx_p, batch, 8, B.QSVD_OUT_Q, ch_p, cq_p, sc_p,
                                            q_p, 0, 0, 0, 0, pws_p, pws_b, s)
         st |= lib.qsvd_latent_cache_append(crefs[li], ch_p if f16 else 0, 0 if f16 else cq_p, 0 if f16 else sc_p,
                                            1, s)
+        st |= lib.qsvd_latent_decode_attention(lrefs[li], crefs[li], q_p, 1, mode, 0.0, out_p, dws_p, dws_b, s)
+        if st:
+            raise B.QsvdError(st, B.last_error())
+
+    # one step: the fused projection with its cache append, then the attention
+    def step(i, s=s):
+        li = i % n_layers
+        st = lib.qsvd_decode_project_append(lrefs[li], crefs[li], xs_p[i % 8], d, 8, 1.0, xq_p, sx_p, ch_p, cq_p,
+                                            sc_p, q_p, s)
         st |= lib.qsvd_latent_decode_attention(lrefs[li], crefs[li], q_p, 1, mode, 0.0, out_p, dws_p, dws_b, s)
         if st:
             raise B.QsvdError(st, B.last_error())
@@ -292,6 +301,18 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
                                "traffic": None if traffic is None else int(traffic),
                                "kernel": "latent_attn_kernel", "launches": n,
                                "bytes_per_launch": int(bytes_per_launch)}
+    # the same step as four separate calls (quantize, projection, append,
+    # attention), four visits of every layer after one, for comparison
+    reset()
+    for i in range(n_layers):
+        step_unfused(i)
+    torch.cuda.synchronize()
+    u0 = time.perf_counter()
+    for i in range(n_layers, 5 * n_layers):
+        step_unfused(i)
+    torch.cuda.synchronize()
+    res["unfused_ms_per_step"] = (time.perf_counter() - u0) * 1e3 / (4 * n_layers)
+
     # The same steps replayed from one captured graph of a full rotation
     # through the layers (launch grids follow each cache's host max_len, held
     # at the final length; chunks past a sequence's length return at once).
@@ -366,6 +387,7 @@ def bench_decode_gqa(args):
                        f"W4A8 (int4 per-group-128 weights), {wl4.n_layers} rotated layers; tokens/s per layer step",
            "mean_context": round(res["mean_context"], 1),
            "graph_replay": graph_line(res),
+           "unfused_ms_per_step": round(res["unfused_ms_per_step"], 5),
            "attention_form_us": res["attention_form_us"]}
     if "roofline" in res:
         out["roofline"] = res["roofline"]
@@ -644,10 +666,8 @@ def bench_stack_decode(args, wl5, ranks, layers):
 
     def step_all(s):
         for li, (dl, c) in enumerate(zip(layers, caches)):
-            st = lib.qsvd_quantize_act(xs_p[li % 8], batch, d, d, 4, 1.0, P(xq), P(sx), s)
-            st |= lib.qsvd_lowrank_qkv_prefill(dl.c, P(xq), P(sx), batch, 4, B.QSVD_OUT_Q, P(c_h), P(cq), P(sc),
-                                               P(q), 0, 0, 0, 0, 0, 0, s)
-            st |= lib.qsvd_latent_cache_append(c.c, 0, P(cq), P(sc), 1, s)
+            st = lib.qsvd_decode_project_append(dl.c, c.c, xs_p[li % 8], d, 4, 1.0, P(xq), P(sx), P(c_h), P(cq),
+                                                P(sc), P(q), s)
             st |= lib.qsvd_latent_decode_attention(dl.c, c.c, P(q), 1, B.QSVD_ATTN_AUTO, 0.0, P(out), P(dws), dws_b,
                                                    s)
             if st:
@@ -937,6 +957,7 @@ def main():
         "roofline": dec.get("roofline"),
         "attn_kernel_us": round(dec.get("attn_kernel_us", 0.0), 2),
         "graph_replay": graph_line(dec),
+        "unfused_ms_per_step": round(dec["unfused_ms_per_step"], 5),
         "attention_form_us": dec["attention_form_us"],
         "prefill": pre,
     }

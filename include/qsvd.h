@@ -173,6 +173,31 @@ size_t qsvd_prefill_workspace_size(const qsvd_layer* w, int64_t M, uint32_t out_
 qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void* cq,
                                      const float* sc, int32_t n_new, void* stream);
 
+/* One decode step's projection of the new tokens together with the append of
+ * their latent rows (Section 3.1: one new token per sequence; only C is
+ * buffered): per-token quantization of x with act_bits and clip, C = the
+ * quantized down-projection, Q(C), the Q up-projection, and the append of each
+ * sequence's latent row (fp16 C, or Q(C) codes and scale for an integer
+ * cache) at position seq_len[b], then seq_len[b] += 1 on the device and
+ * c->max_len += 1 on the host.  Every output byte, cache byte and length is
+ * the one of qsvd_quantize_act + qsvd_lowrank_qkv_prefill(out_mask QSVD_OUT_Q)
+ * + qsvd_latent_cache_append(n_new 1); the quantizer runs inside the
+ * down-projection and the append inside the two products, so the step takes
+ * two launches instead of four.
+ *   x         device fp16 [batch][ldx], row b the new token of sequence b
+ *   xq, sx    device outputs: Q(x) codes ([batch][d] int8 or [batch][d/2] int4) and scales
+ *   c_h       device fp16 [batch][r]; cq, sc: Q(C) ([batch][r] / [batch][r/2], [batch])
+ *   q         device fp16 [batch][Hq*hd]
+ * Requires batch <= 32, an I8 cache with act_bits 8 or an I4 cache with
+ * act_bits 4 (any act_bits for F16), ldx % 8 == 0, 16-byte aligned x, xq,
+ * c_h, cq and weight codes, and the layer requirements of
+ * qsvd_lowrank_qkv_prefill.  QSVD_ERR_CAPACITY if c->max_len + 1 > capacity;
+ * on the device, a row at or past capacity is dropped as in
+ * qsvd_latent_cache_append. */
+qsvd_status qsvd_decode_project_append(const qsvd_layer* w, qsvd_cache* c, const void* x, int64_t ldx,
+                                       int32_t act_bits, float clip, void* xq, float* sx, void* c_h,
+                                       void* cq, float* sc, void* q, void* stream);
+
 /* Causal self-attention of a prefill block over its own projections (Section
  * 3.1: in prefill every prompt token's keys and values are at hand as the rows
  * K = C W^u_k and V = C W^u_v that qsvd_lowrank_qkv_prefill wrote, Eq. 5 and

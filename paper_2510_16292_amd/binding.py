@@ -19,7 +19,8 @@ QSVD_OUT_Q, QSVD_OUT_K, QSVD_OUT_V = 1, 2, 4
 
 EXPORTED = [
     "qsvd_quantize_act", "qsvd_quantize_act_rotated", "qsvd_lowrank_qkv_prefill", "qsvd_prefill_workspace_size",
-    "qsvd_latent_cache_append", "qsvd_prefill_attention", "qsvd_latent_decode_attention",
+    "qsvd_latent_cache_append", "qsvd_decode_project_append", "qsvd_prefill_attention",
+    "qsvd_latent_decode_attention",
     "qsvd_latent_decode_attention_rope",
     "qsvd_decode_workspace_size", "qsvd_latent_decode_attention_noalloc", "qsvd_noalloc_scratch_bytes",
     "qsvd_status_string", "qsvd_last_error", "qsvd_profile_enable", "qsvd_profile_reset",
@@ -69,6 +70,7 @@ def lib():
             "qsvd_lowrank_qkv_prefill": (I32, [LP, P, P, I64, I32, U32, P, P, P, P, P, P, P, P, P, SZ, P]),
             "qsvd_prefill_workspace_size": (SZ, [LP, I64, U32]),
             "qsvd_latent_cache_append": (I32, [CP, P, P, P, I32, P]),
+            "qsvd_decode_project_append": (I32, [LP, CP, P, I64, I32, F, P, P, P, P, P, P, P]),
             "qsvd_prefill_attention": (I32, [P, P, P, I32, P, I32, I32, I32, I32, F, P, P]),
             "qsvd_latent_decode_attention": (I32, [LP, CP, P, I32, I32, F, P, P, SZ, P]),
             "qsvd_latent_decode_attention_rope": (I32, [LP, CP, P, I32, I32, F, F, P, P, SZ, P]),
@@ -110,6 +112,11 @@ def qsvd_prefill_workspace_size(layer, M, out_mask):
 
 def qsvd_latent_cache_append(cache, c_h, cq, sc, n_new, stream):
     return lib().qsvd_latent_cache_append(ctypes.byref(cache), c_h, cq, sc, n_new, stream)
+
+
+def qsvd_decode_project_append(layer, cache, x, ldx, act_bits, clip, xq, sx, c_h, cq, sc, q, stream):
+    return lib().qsvd_decode_project_append(ctypes.byref(layer), ctypes.byref(cache), x, ldx, act_bits, clip, xq, sx,
+                                            c_h, cq, sc, q, stream)
 
 
 def qsvd_prefill_attention(q, k, v, batch, cu_seqlens, max_seqlen, n_q_heads, n_kv_heads, head_dim, sm_scale, out,

@@ -277,6 +277,82 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
                     "up-projection");
 }
 
+qsvd_status qsvd_decode_project_append(const qsvd_layer* w, qsvd_cache* c, const void* x, int64_t ldx,
+                                       int32_t act_bits, float clip, void* xq, float* sx, void* c_h, void* cq,
+                                       float* sc, void* q, void* stream) {
+  qsvd_status st = check_layer(w);
+  if (st != QSVD_OK) return st;
+  st = check_cache(c);
+  if (st != QSVD_OK) return st;
+  if (c->r != w->r) return fail(QSVD_ERR_INVALID_ARG, "cache r %d != layer r %d", c->r, w->r);
+  if (act_bits != 8 && act_bits != 4) return fail(QSVD_ERR_INVALID_ARG, "act_bits must be 8 or 4");
+  if (!(clip > 0.f && clip <= 1.f)) return fail(QSVD_ERR_INVALID_ARG, "clip must be in (0, 1]");
+  if (!x || !xq || !sx || !c_h || !cq || !sc || !q) return fail(QSVD_ERR_INVALID_ARG, "NULL pointer");
+  if (ldx < w->d) return fail(QSVD_ERR_INVALID_ARG, "ldx %lld < d %d", (long long)ldx, w->d);
+  if ((c->fmt == QSVD_CACHE_I8 && act_bits != 8) || (c->fmt == QSVD_CACHE_I4 && act_bits != 4))
+    return fail(QSVD_ERR_UNSUPPORTED, "an integer cache stores Q(C) at the activation width (I8: 8 bits, I4: 4 bits)");
+  if ((int64_t)c->max_len + 1 > c->capacity)
+    return fail(QSVD_ERR_CAPACITY, "max_len %d + 1 exceeds capacity %d", c->max_len, c->capacity);
+  if (w->w_group % 64) return fail(QSVD_ERR_UNSUPPORTED, "w_group must be a multiple of 64");
+  const int64_t M = c->batch;
+  if (M > 32 || !skinny_supported(M, w->r, w->w_group, true) || !skinny_supported(M, w->d, w->w_group, false))
+    return fail(QSVD_ERR_UNSUPPORTED, "the fused decode projection takes at most 32 sequences");
+  if (ldx % 8 || !aligned(x, 16) || !aligned(c_h, 16) || !aligned(cq, 16) || !aligned(xq, 16) ||
+      !aligned(w->a_t, 16) || !aligned(w->b_t, 16))
+    return fail(QSVD_ERR_UNSUPPORTED, "ldx a multiple of 8 and 16-byte aligned x, xq, c_h, cq and weight codes");
+  hipStream_t s = (hipStream_t)stream;
+  const int32_t nq = w->n_q_heads * w->head_dim;
+  const int32_t N = nq + 2 * w->n_kv_heads * w->head_dim;
+  const bool f16c = c->fmt == QSVD_CACHE_F16;
+
+  // X W^d -> C: the quantizer of the activations runs inside the product
+  // when its rows fit the workgroup's LDS, else as its own launch first
+  GemmArgs g1{};
+  g1.b = (const int8_t*)w->a_t;
+  g1.col_scale = w->s_a;
+  g1.M = M;
+  g1.N = w->r;
+  g1.K = w->d;
+  g1.seg[0] = OutSeg{(_Float16*)c_h, w->r, 0, w->r};
+  g1.n_seg = 1;
+  g1.abits = act_bits;
+  SkinnyAppendArgs a1{c->data, c->scale, c->seq_len, c->overflow, c->capacity, f16c ? 1 : 0};
+  if (skinny_supported(M, w->d, w->w_group, true)) {
+    g1.a = (const int8_t*)x;
+    g1.cq = xq;
+    g1.sc = sx;
+    st = hip_status(launch_skinny_fused(g1, SKA_F16_ACT, clip, ldx, w->w_bits, w->w_group, w->r, a1, s),
+                    "decode down-projection");
+  } else {
+    st = hip_status(launch_quantize_rows(x, M, w->d, ldx, act_bits, clip, xq, sx, s), "quantize_act");
+    if (st != QSVD_OK) return st;
+    g1.a = (const int8_t*)xq;
+    g1.row_scale = sx;
+    st = hip_status(launch_skinny_fused(g1, SKA_CODES, 1.f, w->d, w->w_bits, w->w_group, w->r, a1, s),
+                    "decode down-projection");
+  }
+  if (st != QSVD_OK) return st;
+
+  // Q(C) W^u_q -> Q, with the cache row (integer caches) and the length advance
+  GemmArgs g2{};
+  g2.a = (const int8_t*)c_h;
+  g2.b = (const int8_t*)w->b_t;
+  g2.col_scale = w->s_b;
+  g2.M = M;
+  g2.N = nq;
+  g2.K = w->r;
+  g2.seg[0] = OutSeg{(_Float16*)q, nq, 0, nq};
+  g2.n_seg = 1;
+  g2.abits = act_bits;
+  g2.cq = cq;
+  g2.sc = sc;
+  SkinnyAppendArgs a2{c->data, c->scale, c->seq_len, c->overflow, c->capacity, f16c ? 3 : 2};
+  st = hip_status(launch_skinny_fused(g2, SKA_F16_LATENT, 1.f, w->r, w->w_bits, w->w_group, N, a2, s),
+                  "decode up-projection");
+  if (st == QSVD_OK) c->max_len += 1;
+  return st;
+}
+
 qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void* cq, const float* sc,
                                      int32_t n_new, void* stream) {
   qsvd_status st = check_cache(c);

@@ -84,6 +84,24 @@ bool skinny_supported(int64_t M, int32_t K, int32_t group, bool f16q);
 hipError_t launch_skinny(const GemmArgs& g, bool a_is_f16_latent, int32_t wbits, int32_t group, int32_t sstride,
                          hipStream_t s);
 
+// The decode step's fused variants (one new row per sequence, M = batch):
+// A from fp16 rows quantized in the kernel (the activations X with `clip`,
+// row stride lda, codes and scales optionally stored to g.cq / g.sc; or the
+// latent C with clip 1), and the latent cache append folded in (mode
+// SK_APPEND_* of skinny.hip: the fp16 C row from the down-projection; the
+// Q(C) codes and the seq_len advance from the up-projection).
+enum { SKA_CODES = 0, SKA_F16_LATENT = 1, SKA_F16_ACT = 2 };
+struct SkinnyAppendArgs {
+  void* data;
+  float* scale;
+  int32_t* seq_len;
+  int32_t* overflow;
+  int32_t capacity;
+  int32_t mode;        // 0: none
+};
+hipError_t launch_skinny_fused(const GemmArgs& g, int32_t asrc, float clip, int64_t lda, int32_t wbits, int32_t group,
+                               int32_t sstride, const SkinnyAppendArgs& aa, hipStream_t s);
+
 hipError_t launch_cache_append(const qsvd_cache& c, const void* c_h, const void* cq,
                                const float* sc, int32_t n_new, hipStream_t s);
 

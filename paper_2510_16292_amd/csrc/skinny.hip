@@ -32,7 +32,7 @@ namespace qsvd {
 constexpr int kSkCols = 16;        // output columns per workgroup
 constexpr int kSkMaxWaves = 16;
 constexpr int kSkBatch = 4;        // 64-byte contraction steps loaded per batch
-constexpr int kSkMaxRowChunks = 8; // fp16 row pass: K <= 8 * 64 * 8 = 4096
+constexpr int kSkMaxRowChunks = 8;  // fp16 row pass: K <= 8 * 64 * 8 = 4096
 constexpr int kSkMaxGroups = 64;   // scale groups along the contraction
 constexpr size_t kSkLdsLimit = 160 * 1024 - 5 * 1024;   // dynamic LDS beside the static scale arrays
 
@@ -76,9 +76,29 @@ __device__ __forceinline__ i32x4 unpack16_i4(uint2 p) {
 }
 
 // A operand source: int8 or packed int4 codes (down-projection: the quantized
-// activations), or the fp16 latent quantized by the workgroup itself
-// (up-projection, 8- or 4-bit codes).
+// activations), or fp16 rows quantized per row by the workgroup itself (the
+// latent C in the up-projection, clip 1; or the activations X in the fused
+// decode down-projection, with the caller's clip), 8- or 4-bit codes.
 enum { SK_A_I8 = 0, SK_A_F16Q = 1 };
+
+// The latent cache append fused into the decode-size projections (one new
+// row per sequence, row m of the product being sequence m's):
+//   SK_APPEND_F16_ROW  down-projection: the fp16 C row also goes to the cache
+//                      row seq_len[m] (the epilogue stores each element twice)
+//   SK_APPEND_CODES    up-projection: the row's Q(C) codes and scale also go to
+//                      the cache row seq_len[m], then seq_len[m] advances
+//   SK_APPEND_ADVANCE  up-projection over an fp16 cache: seq_len[m] advances
+// A row at or past capacity is not written; seq_len stops at capacity and the
+// overflow flag (when given) is set.
+enum { SK_APPEND_NONE = 0, SK_APPEND_F16_ROW = 1, SK_APPEND_CODES = 2, SK_APPEND_ADVANCE = 3 };
+struct SkinnyAppend {
+  uint8_t* data;       // cache rows
+  float* scale;        // integer caches: per-row scales
+  int32_t* seq_len;
+  int32_t* overflow;   // optional
+  int32_t capacity;
+  int32_t mode;
+};
 
 // Contraction steps [s0, s1) of wave w: contiguous ranges, whole groups when the
 // weights carry per-group scales.
@@ -96,10 +116,11 @@ __device__ __forceinline__ void sk_span(int w, int nw, int32_t K, int32_t group,
 
 template <int ASRC, int WBITS>
 __global__ void __launch_bounds__(64 * kSkMaxWaves)
-skinny_gemm_kernel(const void* __restrict__ a_src, const float* __restrict__ row_scale_in,
+skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, const float* __restrict__ row_scale_in,
                    const uint8_t* __restrict__ bt, const float* __restrict__ col_scale, int32_t sstride,
                    int32_t M, int32_t N, int32_t K, int32_t group, int32_t nw, int32_t abits, int32_t qa_off,
-                   SkinnyOut so, int32_t* __restrict__ dbg, uint8_t* __restrict__ cq_out, float* __restrict__ sc_out) {
+                   SkinnyOut so, int32_t* __restrict__ dbg, uint8_t* __restrict__ cq_out, float* __restrict__ sc_out,
+                   SkinnyAppend ap) {
   // [0, qa_off): int32 tiles, [slot][row block][lane] (slot = wave for
   // per-channel weights, group for per-group ones); [qa_off, ...): Q(C) rows.
   extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];
@@ -163,20 +184,26 @@ skinny_gemm_kernel(const void* __restrict__ a_src, const float* __restrict__ row
 #pragma unroll
       for (int i = 0; i < kSkMaxRowChunks; ++i) {
         const int c = lane + 64 * i;
-        v[i] = c < nch ? *reinterpret_cast<const f16x8*>(ch + (int64_t)m * K + 8 * c) : f16x8{};
+        v[i] = c < nch ? *reinterpret_cast<const f16x8*>(ch + (int64_t)m * lda + 8 * c) : f16x8{};
       }
       float mx = 0.f;
 #pragma unroll
       for (int i = 0; i < kSkMaxRowChunks; ++i)
 #pragma unroll
         for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf((float)v[i][e]));
-      const float a = mul_rn(1.f, wave_max(mx));
+      const float a = mul_rn(clip, wave_max(mx));
       const float inv = a != 0.f ? div_rn(qm, a) : 0.f;
       const float sc = a != 0.f ? div_rn(a, qm) : 1.f;
       const bool own = (m % (int)gridDim.x) == (int)blockIdx.x;
+      // the cache row this sequence's codes also go to (integer caches)
+      const bool app = own && ap.mode == SK_APPEND_CODES;
+      const int32_t pos = app ? ap.seq_len[m] : 0;
+      const bool app_row = app && pos >= 0 && pos < ap.capacity;
+      uint8_t* crow = ap.data + ((int64_t)m * ap.capacity + (app_row ? pos : 0)) * (abits == 8 ? K : K / 2);
       if (lane == 0) {
         rsc[m] = sc;
-        if (own) sc_out[m] = sc;
+        if (own && sc_out) sc_out[m] = sc;
+        if (app_row) ap.scale[(int64_t)m * ap.capacity + pos] = sc;
       }
 #pragma unroll
       for (int i = 0; i < kSkMaxRowChunks; ++i) {
@@ -188,19 +215,29 @@ skinny_gemm_kernel(const void* __restrict__ a_src, const float* __restrict__ row
         const uint32_t lo = (q[0] & 0xff) | ((q[1] & 0xff) << 8) | ((q[2] & 0xff) << 16) | ((uint32_t)(q[3] & 0xff) << 24);
         const uint32_t hi = (q[4] & 0xff) | ((q[5] & 0xff) << 8) | ((q[6] & 0xff) << 16) | ((uint32_t)(q[7] & 0xff) << 24);
         *reinterpret_cast<uint2*>(qa + m * qa_ld + 8 * c) = make_uint2(lo, hi);
-        if (own) {
+        if (own && (cq_out || app_row)) {
           if (abits == 8) {
-            *reinterpret_cast<uint2*>(cq_out + (int64_t)m * K + 8 * c) = make_uint2(lo, hi);
+            if (cq_out) *reinterpret_cast<uint2*>(cq_out + (int64_t)m * K + 8 * c) = make_uint2(lo, hi);
+            if (app_row) *reinterpret_cast<uint2*>(crow + 8 * c) = make_uint2(lo, hi);
           } else {
             uint32_t p = 0;
 #pragma unroll
             for (int e = 0; e < 8; ++e) p |= (uint32_t)(q[e] & 0xf) << (4 * e);
-            *reinterpret_cast<uint32_t*>(cq_out + (int64_t)m * (K / 2) + 4 * c) = p;
+            if (cq_out) *reinterpret_cast<uint32_t*>(cq_out + (int64_t)m * (K / 2) + 4 * c) = p;
+            if (app_row) *reinterpret_cast<uint32_t*>(crow + 4 * c) = p;
           }
         }
       }
     }
     __syncthreads();
+    // the cache row of each sequence this workgroup owns is complete: advance
+    // its length (only the owning workgroup reads or writes seq_len[m] here)
+    if ((ap.mode == SK_APPEND_CODES || ap.mode == SK_APPEND_ADVANCE) && tid < M &&
+        (tid % (int)gridDim.x) == (int)blockIdx.x) {
+      const int32_t base = ap.seq_len[tid];
+      if (base >= ap.capacity && ap.overflow) *ap.overflow = 1;
+      ap.seq_len[tid] = base >= ap.capacity ? ap.capacity : base + 1;
+    }
   }
 
   // --- contraction over this wave's steps ------------------------------------
@@ -273,6 +310,11 @@ skinny_gemm_kernel(const void* __restrict__ a_src, const float* __restrict__ row
       y = mul_rn(S, rs);
     }
     sk_store(so, m, nn, y);
+    if (ap.mode == SK_APPEND_F16_ROW) {
+      const int32_t pos = ap.seq_len[m];
+      if (pos >= 0 && pos < ap.capacity)
+        reinterpret_cast<_Float16*>(ap.data)[((int64_t)m * ap.capacity + pos) * N + nn] = to_f16(y);
+    }
   }
 }
 
@@ -302,6 +344,13 @@ bool skinny_supported(int64_t M, int32_t K, int32_t group, bool f16q) {
 
 hipError_t launch_skinny(const GemmArgs& g, bool a_is_f16_latent, int32_t wbits, int32_t group, int32_t sstride,
                          hipStream_t s) {
+  return launch_skinny_fused(g, a_is_f16_latent ? SKA_F16_LATENT : SKA_CODES, 1.f, g.K, wbits, group, sstride,
+                             SkinnyAppendArgs{}, s);
+}
+
+hipError_t launch_skinny_fused(const GemmArgs& g, int32_t asrc, float clip, int64_t lda, int32_t wbits, int32_t group,
+                               int32_t sstride, const SkinnyAppendArgs& aa, hipStream_t s) {
+  const bool a_is_f16_latent = asrc != SKA_CODES;
   if (g.M == 0 || g.N == 0) return hipSuccess;
   if (!skinny_supported(g.M, g.K, group, a_is_f16_latent)) return hipErrorInvalidValue;
   SkinnyOut so{};
@@ -321,17 +370,19 @@ hipError_t launch_skinny(const GemmArgs& g, bool a_is_f16_latent, int32_t wbits,
     return p.lds > 65536 ? hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds)
                          : hipSuccess;
   };
-  KernelScope ks(a_is_f16_latent ? "skinny_up" : "skinny_down", s);
+  SkinnyAppend ap{(uint8_t*)aa.data, aa.scale, aa.seq_len, aa.overflow, aa.capacity, aa.mode};
+  KernelScope ks(asrc == SKA_F16_ACT ? "skinny_down_q" : a_is_f16_latent ? "skinny_up" : "skinny_down", s);
   if (!a_is_f16_latent) {
     auto k = wbits == 8 ? skinny_gemm_kernel<SK_A_I8, 8> : skinny_gemm_kernel<SK_A_I8, 4>;
     if (hipError_t e = allow((const void*)k); e != hipSuccess) return e;
-    QSVD_LAUNCH(ks, k, grid, block, p.lds, s, (const void*)g.a, g.row_scale, bt, g.col_scale, sstride, M, g.N,
-                       g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)nullptr, (float*)nullptr);
+    QSVD_LAUNCH(ks, k, grid, block, p.lds, s, (const void*)g.a, (int64_t)g.K, 1.f, g.row_scale, bt, g.col_scale,
+                       sstride, M, g.N, g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)nullptr,
+                       (float*)nullptr, ap);
   } else {
     auto k = wbits == 8 ? skinny_gemm_kernel<SK_A_F16Q, 8> : skinny_gemm_kernel<SK_A_F16Q, 4>;
     if (hipError_t e = allow((const void*)k); e != hipSuccess) return e;
-    QSVD_LAUNCH(ks, k, grid, block, p.lds, s, (const void*)g.a, (const float*)nullptr, bt, g.col_scale, sstride,
-                       M, g.N, g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)g.cq, g.sc);
+    QSVD_LAUNCH(ks, k, grid, block, p.lds, s, (const void*)g.a, lda, clip, (const float*)nullptr, bt, g.col_scale,
+                       sstride, M, g.N, g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)g.cq, g.sc, ap);
   }
   return hipGetLastError();
 }

@@ -178,6 +178,26 @@ def test_cache_append_validation(lib):
     assert B.qsvd_latent_cache_append(cache_struct(seq_len=0), FAKE, 0, 0, 1, 0) == B.QSVD_ERR_INVALID_ARG
 
 
+def test_decode_project_append_validation(lib):
+    """Every case fails before a launch; the capacity error leaves max_len alone."""
+    def call(layer=None, cache=None, ldx=256, bits=8, clip=1.0, ptrs=None):
+        p = ptrs or [FAKE] * 6
+        return B.qsvd_decode_project_append(layer or layer_struct(), cache or cache_struct(), FAKE, ldx, bits, clip,
+                                            *p, 0)
+    assert call(bits=5) == B.QSVD_ERR_INVALID_ARG
+    assert call(clip=0.0) == B.QSVD_ERR_INVALID_ARG
+    assert call(ldx=128) == B.QSVD_ERR_INVALID_ARG
+    assert call(ptrs=[FAKE, FAKE, 0, FAKE, FAKE, FAKE]) == B.QSVD_ERR_INVALID_ARG
+    assert call(cache=cache_struct(r=256)) == B.QSVD_ERR_INVALID_ARG
+    assert call(cache=cache_struct(fmt=B.QSVD_CACHE_I8, scale=FAKE), bits=4) == B.QSVD_ERR_UNSUPPORTED
+    assert call(cache=cache_struct(fmt=B.QSVD_CACHE_I4, scale=FAKE), bits=8) == B.QSVD_ERR_UNSUPPORTED
+    full = cache_struct(max_len=64)
+    assert call(cache=full) == B.QSVD_ERR_CAPACITY
+    assert full.max_len == 64
+    assert call(cache=cache_struct(batch=33)) == B.QSVD_ERR_UNSUPPORTED
+    assert call(ldx=260) == B.QSVD_ERR_UNSUPPORTED
+
+
 def test_prefill_attention_validation(lib):
     """Every case fails (or returns OK with nothing to do) before a launch."""
     def call(q=FAKE, k=FAKE, v=FAKE, batch=2, cu=FAKE, ms=64, hq=4, hkv=2, dh=64, sm=0.0, out=FAKE):

@@ -574,6 +574,106 @@ def test_prefill_attention_flash_13b_two_sequences():
     assert ok, info
 
 
+def _layer_for(shape_id):
+    """(layer shape, oracle layer, device layer, weight bits, group) of a decode projection case."""
+    if shape_id == "tiny":
+        wl = configs.get(1)
+        ol, dl = _layers_from_weight(gen.weight_matrix(wl), wl.layer)
+        return wl.layer, dl
+    if shape_id == "llava7b":
+        L = configs.LayerShape(d=4096, n_q_heads=32, n_kv_heads=32, head_dim=128, r=1536)
+        return L, _random_factor_layer(L, 7007)[1]
+    if shape_id == "qwen2vl":
+        L = configs.LayerShape(d=3584, n_q_heads=28, n_kv_heads=4, head_dim=128, r=1024)
+        return L, _random_factor_layer(L, 7008, w_bits=4, w_group=128)[1]
+    L = configs.LayerShape(d=5120, n_q_heads=40, n_kv_heads=40, head_dim=128, r=2048)
+    return L, _random_factor_layer(L, 7009, w_bits=4, w_group=128)[1]
+
+
+@pytest.mark.parametrize("shape_id,fmt,abits,batch,clip", [
+    ("tiny", B.QSVD_CACHE_F16, 8, 1, 1.0),
+    ("tiny", B.QSVD_CACHE_I8, 8, 3, 0.9),
+    ("llava7b", B.QSVD_CACHE_F16, 8, 16, 1.0),       # the bench's decode step
+    ("llava7b", B.QSVD_CACHE_I4, 4, 16, 1.0),
+    ("qwen2vl", B.QSVD_CACHE_I8, 8, 32, 1.0),        # 32 rows: the quantizer as its own launch
+    ("stack13b", B.QSVD_CACHE_I4, 4, 8, 1.0),        # d = 5120: the quantizer as its own launch
+], ids=["tiny-f16", "tiny-i8-clip", "llava7b-f16", "llava7b-i4", "qwen2vl-i8-w4", "13b-i4-w4a4"])
+def test_decode_project_append_equals_separate_calls(shape_id, fmt, abits, batch, clip):
+    """The fused decode projection with its cache append leaves every output
+    byte, cache byte and length exactly as quantize + projection (Q only) +
+    append do, on two caches holding the same ragged rows."""
+    torch = H.torch()
+    L, dl = _layer_for(shape_id)
+    per = 1 if abits == 8 else 2
+    lengths = [(37 * b + 5) % 61 for b in range(batch)]
+    cap = 64
+    width = L.r if fmt != B.QSVD_CACHE_I4 else L.r // 2
+    caches = [B.DeviceCache(fmt, batch, cap, L.r, lengths) for _ in range(2)]
+    fill = gen.random_rows(900 + batch, (batch, cap, width), 1.0)
+    for c in caches:
+        if fmt == B.QSVD_CACHE_F16:
+            c.data.copy_(H.dev(fill))
+        else:
+            c.data.copy_(H.dev(fill.view(np.uint16).astype(np.uint8)).view(c.data.dtype))
+            c.scale.copy_(H.dev(np.abs(fill[:, :, 0]).astype(np.float32) + 0.01))
+    X = gen.random_rows(950 + batch, (batch, L.d + 8), 1.0)
+    X[:, 7] *= 30.0
+    xd = H.dev(X)
+    s = B.stream_handle()
+    H.say(f"decode project+append {shape_id} fmt={fmt} a{abits} batch={batch}")
+    outs = []
+    for fused, c in ((False, caches[0]), (True, caches[1])):
+        xq = torch.empty((batch, L.d // per), dtype=torch.uint8, device="cuda")
+        sx = torch.empty((batch,), dtype=torch.float32, device="cuda")
+        c_h = torch.empty((batch, L.r), dtype=torch.float16, device="cuda")
+        cq = torch.empty((batch, L.r // per), dtype=torch.uint8, device="cuda")
+        sc = torch.empty((batch,), dtype=torch.float32, device="cuda")
+        q = torch.empty((batch, L.n_q), dtype=torch.float16, device="cuda")
+        if fused:
+            B.check(B.qsvd_decode_project_append(dl.c, c.c, B.ptr(xd), L.d + 8, abits, clip, B.ptr(xq), B.ptr(sx),
+                                                 B.ptr(c_h), B.ptr(cq), B.ptr(sc), B.ptr(q), s))
+        else:
+            B.check(B.qsvd_quantize_act(B.ptr(xd), batch, L.d, L.d + 8, abits, clip, B.ptr(xq), B.ptr(sx), s))
+            B.check(B.qsvd_lowrank_qkv_prefill(dl.c, B.ptr(xq), B.ptr(sx), batch, abits, B.QSVD_OUT_Q, B.ptr(c_h),
+                                               B.ptr(cq), B.ptr(sc), B.ptr(q), 0, 0, 0, 0, 0, 0, s))
+            if fmt == B.QSVD_CACHE_F16:
+                H.append(c, c_h=c_h, n_new=1)
+            else:
+                H.append(c, cq=cq, sc=sc, n_new=1)
+        outs.append({k: H.host(t).view(np.uint8).copy() for k, t in
+                     (("xq", xq), ("sx", sx), ("c_h", c_h), ("cq", cq), ("sc", sc), ("q", q))})
+    for k in outs[0]:
+        assert np.array_equal(outs[0][k], outs[1][k]), k
+    assert np.array_equal(H.host(caches[0].data).view(np.uint8), H.host(caches[1].data).view(np.uint8))
+    if fmt != B.QSVD_CACHE_F16:
+        assert np.array_equal(H.host(caches[0].scale).view(np.uint32), H.host(caches[1].scale).view(np.uint32))
+    assert list(H.host(caches[1].seq_len)) == [n + 1 for n in lengths]
+    assert caches[0].max_len == caches[1].max_len == max(lengths) + 1
+    assert int(H.host(caches[1].overflow)[0]) == 0
+
+
+def test_decode_project_append_capacity_on_device(tiny):
+    """A fused append the host bound cannot see running past capacity drops
+    the row, stops seq_len at capacity and raises the overflow flag."""
+    wl, ol, dl = tiny
+    L = wl.layer
+    torch = H.torch()
+    dc = B.DeviceCache(B.QSVD_CACHE_I8, 2, 8, L.r, [8, 3])
+    dc.c.max_len = 0
+    before = H.host(dc.data).copy()
+    x = H.dev(gen.random_rows(71, (2, L.d), 1.0))
+    bufs = [torch.empty(shape, dtype=dt, device="cuda") for shape, dt in
+            (((2, L.d), torch.int8), ((2,), torch.float32), ((2, L.r), torch.float16), ((2, L.r), torch.int8),
+             ((2,), torch.float32), ((2, L.n_q), torch.float16))]
+    B.check(B.qsvd_decode_project_append(dl.c, dc.c, B.ptr(x), L.d, 8, 1.0, *[B.ptr(t) for t in bufs],
+                                         B.stream_handle()))
+    got = H.host(dc.data)
+    assert np.array_equal(got[0], before[0])
+    assert np.array_equal(got[1, 3], H.host(bufs[3])[1])
+    assert list(H.host(dc.seq_len)) == [8, 4]
+    assert int(H.host(dc.overflow)[0]) == 1
+
+
 # ------------------------------------------------------------------ a5-a7: decode attention
 
 @pytest.mark.parametrize("mode", MODES, ids=MODE_IDS)
@@ -789,6 +889,73 @@ def test_decode_13b_int4_cache_full_size_sampled(stack13b):
         oc.append(0, None, q4, s4)
         assert np.array_equal(H.host(dc.data)[b, :L0 + 1], oc.data[0, :L0 + 1])
         want = O.attention_absorbed(ol, oc, ref["Q"][:, None, :], 1)[:, 0, :]
+        ok, info = H.close_enough(out[b:b + 1], want)
+        H.say(f"  b={b} max-abs, rel-L2, rms = {info}")
+        assert ok, (b, info)
+
+
+@pytest.mark.parametrize("M,tile_rows", [(5632, (2816, 2944)), (5600, (5504, 5600))],
+                         ids=["m5632-interior-tile-row", "m5600-ragged-last-tile-row"])
+def test_prefill_13b_w4a4_whole_tile_rows(stack13b, M, tile_rows):
+    """The stack's W4A4 prefill (d = 5120, r = 3072, N = 15360) checked over a
+    whole 128-row tile row of the products: an interior one at the full
+    8 x 704 = 5632 tokens, and the ragged last one (96 rows) at 5600 tokens;
+    codes, scales, C and Q / K / V bit-exact against the oracle."""
+    wl, L, ol, dl = stack13b
+    X = gen.prefill_activations(wl)[:M]
+    H.say(f"prefill 13b w4a4 M={M} rows {tile_rows}")
+    got = H.Prefill(dl, M, debug=False, abits=4).run(H.dev(X)).result()
+    rows = np.arange(*tile_rows)
+    ref = O.prefill(ol, X[rows], 4)
+    assert np.array_equal(got["xq"][rows].view(np.uint8), O.pack_int4(ref["xq"]))
+    assert np.array_equal(got["cq"][rows].view(np.uint8), O.pack_int4(ref["cq"]))
+    for key in ("sx", "sc"):
+        assert np.array_equal(got[key][rows].view(np.uint32), ref[key].view(np.uint32)), key
+    for key in ("C_h", "Q", "K", "V"):
+        assert np.array_equal(got[key][rows].view(np.uint16), ref[key].view(np.uint16)), key
+
+
+def test_decode_13b_int4_cache_rank_2048_plain_definition():
+    """A mid-range layer of the stack (r = 2048, two 128-column units per wave,
+    32-token tiles) at the full decode size (batch 8 over 4096 cached int4 rows,
+    W4A4 projection, 40 heads in 16-head blocks), two sequences against the
+    plain definition (K and V rebuilt from the cache, Eq. 5) rather than the
+    latent form."""
+    wl = gen.with_rank(configs.get(5), 2048)
+    L = configs.LayerShape(d=5120, n_q_heads=40, n_kv_heads=40, head_dim=128, r=2048)
+    ol, dl = _random_factor_layer(L, 12048, w_bits=4, w_group=128)
+    torch = H.torch()
+    batch, L0 = wl.decode_batch, wl.decode_ctx
+    cap = L0 + 4
+    rows = gen.latent_rows(wl, batch, L0)
+    data = np.zeros((batch, cap, L.r // 2), np.uint8)
+    scale = np.zeros((batch, cap), np.float32)
+    codes_of = {}
+    for b in range(batch):
+        codes, sc = O.quantize_act(rows[b], 4)
+        data[b, :L0], scale[b, :L0] = O.pack_int4(codes), sc
+        if b in (2, 7):
+            codes_of[b] = codes
+    dc = B.DeviceCache(B.QSVD_CACHE_I4, batch, cap, L.r, [L0] * batch)
+    dc.data.copy_(H.dev(data))
+    dc.scale.copy_(H.dev(scale))
+    xt = gen.decode_activations(wl, 3, batch=batch)
+    H.say(f"decode 13b int4 cache r={L.r} against the plain definition")
+    p = H.Prefill(dl, batch, mask=B.QSVD_OUT_Q, debug=False, abits=4).run(H.dev(xt))
+    cq4 = torch.empty((batch, L.r // 2), dtype=torch.uint8, device="cuda")
+    sc4 = torch.empty((batch,), dtype=torch.float32, device="cuda")
+    B.check(B.qsvd_quantize_act(B.ptr(p.c_h), batch, L.r, L.r, 4, 1.0, B.ptr(cq4), B.ptr(sc4), B.stream_handle()))
+    H.append(dc, cq=cq4, sc=sc4, n_new=1)
+    out = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
+    assert np.all(np.isfinite(out.astype(np.float32)))
+    for b in (2, 7):
+        ref = O.prefill(ol, xt[b:b + 1], 4)
+        assert np.array_equal(H.host(p.q)[b:b + 1].view(np.uint16), ref["Q"].view(np.uint16))
+        q4, s4 = O.quantize_act(ref["C_h"], 4)
+        oc = O.LatentCache(O.CACHE_I4, 1, cap, L.r)
+        oc.append(0, None, codes_of[b], scale[b, :L0])
+        oc.append(0, None, q4, s4)
+        want = O.attention_reference(ol, oc, ref["Q"][:, None, :], 1)[:, 0, :]
         ok, info = H.close_enough(out[b:b + 1], want)
         H.say(f"  b={b} max-abs, rel-L2, rms = {info}")
         assert ok, (b, info)
