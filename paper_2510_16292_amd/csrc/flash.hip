@@ -7,15 +7,18 @@
 // latent form, which the decode path uses because there only one query row
 // per sequence meets the whole cache.
 //
-// One workgroup of four waves takes 128 consecutive queries of one
-// (sequence, query head); wave w owns queries q0 + 32w .. +31.  Key/value
-// tiles of 64 tokens are staged in LDS (shared by the four waves; the next
-// tile's rows are already in registers while the current one is used).  Per
-// tile and wave, on the 32x32x16 fp16 matrix cores:
-//   S^T (64 keys x 32 queries) = K_tile Q_w^T        (contraction over dh)
+// One workgroup of eight waves takes 128 consecutive queries of one
+// (sequence, query head); wave w owns the 16-query block q0 + 16w .. +15 (the
+// code also takes several blocks per wave, which then share every key and
+// value fragment read from LDS; one block per wave with eight waves measured
+// fastest).  Key/value tiles of 64 tokens are staged in LDS (shared by the
+// waves; the next tile's rows are already in registers while the current one
+// is used).  Per tile, wave and query block, on the 16x16x32 fp16 matrix cores:
+//   S^T (64 keys x 16 queries) = K_tile Q_b^T        (contraction over dh)
 //   online softmax per query in fp32 (a query is one lane column; its 64
-//   scores sit in that lane and its partner lane l ^ 32)
-//   O^T (dh x 32 queries) += V_tile^T P^T            (contraction over keys)
+//   scores sit in that lane and the three lanes l ^ 16, l ^ 32, l ^ 48)
+//   O^T (dh x 16 queries) += V_tile^T P^T            (contraction over keys)
+// (16x16 products keep the accumulators small enough for two waves per SIMD.)
 // The query rows stay in registers for the whole kernel.  Keys past a query's
 // position, or past the sequence end, are masked.
 #include <math.h>
@@ -27,7 +30,9 @@ namespace qsvd {
 
 constexpr int kFaQ = 128;       // queries per workgroup
 constexpr int kFaK = 64;        // keys per tile
-constexpr int kFaWaves = 4;
+constexpr int kFaWaves = 8;
+constexpr int kFaQW = kFaQ / kFaWaves;   // queries per wave
+constexpr int kFaQB = kFaQW / 16;        // 16-query blocks per wave
 constexpr float kFaLog2e = 1.4426950408889634f;
 
 template <int DH>
@@ -36,12 +41,38 @@ struct FaCfg {
   static constexpr int VST = DH + 16;      // V tile row stride: the transposing reads hit distinct banks
   static constexpr int OST = DH + 8;       // output staging row stride
   static constexpr size_t kK = (size_t)kFaK * KST * 2, kV = (size_t)kFaK * VST * 2;
-  static constexpr size_t kOut = (size_t)kFaWaves * 32 * OST * 2;
+  static constexpr size_t kOut = (size_t)kFaWaves * kFaQW * OST * 2;
   static constexpr size_t kLds = kK + kV > kOut ? kK + kV : kOut;
   static constexpr int kChunks = kFaK * DH / 8;               // 16-byte runs per K (or V) tile
   static constexpr int kPerThread = kChunks / (kFaWaves * 64);
   static_assert(kChunks % (kFaWaves * 64) == 0, "whole runs per thread");
 };
+
+// Max and sum over the four 16-lane rows of a wave (lanes l, l ^ 16, l ^ 32,
+// l ^ 48), every lane receiving the result: gfx950's v_permlane32_swap and
+// v_permlane16_swap with both registers holding the value give each lane its
+// partner's value at vector-ALU latency (issued as asm with both registers
+// read-write; the s_nop covers the hazard of a vector write just before).
+__device__ __forceinline__ void fa_swap32(uint32_t& a, uint32_t& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void fa_swap16(uint32_t& a, uint32_t& b) {
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ float fa_rows4_max(float x) {
+  uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
+  fa_swap32(a, b);
+  uint32_t c = __builtin_bit_cast(uint32_t, fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b))), e = c;
+  fa_swap16(c, e);
+  return fmaxf(__builtin_bit_cast(float, c), __builtin_bit_cast(float, e));
+}
+__device__ __forceinline__ float fa_rows4_sum(float x) {
+  uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
+  fa_swap32(a, b);
+  uint32_t c = __builtin_bit_cast(uint32_t, __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b)), e = c;
+  fa_swap16(c, e);
+  return __builtin_bit_cast(float, c) + __builtin_bit_cast(float, e);
+}
 
 // Key/value tile t of the rows this thread stages (rows past the sequence end
 // re-read its last row; they are masked).
@@ -75,19 +106,19 @@ __device__ __forceinline__ void fa_store_tile(_Float16* ks, _Float16* vs, int ti
 }
 
 template <int DH>
-__global__ void __launch_bounds__(kFaWaves * 64)
+__global__ void __launch_bounds__(kFaWaves * 64, 2)
 prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k, const _Float16* __restrict__ v,
                      const int32_t* __restrict__ cu, int32_t n_seq, int32_t Hq, int32_t Hkv, int32_t n_qt,
                      float scale_log2, _Float16* __restrict__ out) {
   using C = FaCfg<DH>;
-  constexpr int KS = DH / 16;      // contraction steps of the score product
-  constexpr int OB = DH / 32;      // 32-channel blocks of the output
+  constexpr int KS = DH / 32;      // contraction steps of the score product
+  constexpr int OB = DH / 16;      // 16-channel blocks of the output
   constexpr int RUNS = DH / 8;     // 16-byte runs per row
   extern __shared__ __attribute__((aligned(16))) uint8_t fa_smem[];
   _Float16* ks = reinterpret_cast<_Float16*>(fa_smem);
   _Float16* vs = reinterpret_cast<_Float16*>(fa_smem + C::kK);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int l32 = lane & 31, half = lane >> 5, s16 = lane & 15, q16 = (lane >> 4) & 1;
+  const int l16 = lane & 15, g = lane >> 4;
 
   // Workgroup -> (sequence, head, query tile).  The query tiles of one
   // (sequence, head) read the same key/value rows, so they get ids that one
@@ -101,124 +132,140 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
   const int tok0 = cu[b], n = cu[b + 1] - tok0;
   const int q0 = qt * kFaQ;
   if (q0 >= n) return;
-  const int g = (h * Hkv) / Hq;
+  const int g_kv = (h * Hkv) / Hq;
   const int ldq = Hq * DH, ldkv = Hkv * DH;
   const int kend = min(n, q0 + kFaQ);              // keys this tile of queries can see
   const int n_tiles = (kend + kFaK - 1) / kFaK;
-  const int qw0 = q0 + 32 * w;                      // this wave's first query
-  const int my_q = qw0 + l32;
-
-  // query slots of the score product: step s, lane half -> channels 16 s + 8 half .. +7
-  f16x8 qf[KS];
-  {
-    const _Float16* qrow = q + (int64_t)(tok0 + min(my_q, n - 1)) * ldq + h * DH + 8 * half;
+  const int qw0 = q0 + kFaQW * w;                   // this wave's first query
+  int my_q[kFaQB];                                  // this lane's query in each block
 #pragma unroll
-    for (int s = 0; s < KS; ++s) qf[s] = *reinterpret_cast<const f16x8*>(qrow + 16 * s);
+  for (int qb = 0; qb < kFaQB; ++qb) my_q[qb] = qw0 + 16 * qb + l16;
+
+  // query slots of the score product: step s, lane group g -> channels 32 s + 8 g .. +7
+  f16x8 qf[kFaQB][KS];
+#pragma unroll
+  for (int qb = 0; qb < kFaQB; ++qb) {
+    const _Float16* qrow = q + (int64_t)(tok0 + min(my_q[qb], n - 1)) * ldq + h * DH + 8 * g;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qf[qb][s] = *reinterpret_cast<const f16x8*>(qrow + 32 * s);
   }
 
-  // this thread's 16-byte runs of a K (and V) tile: run e = tid + 256 i is
-  // row e / RUNS, columns 8 (e % RUNS) .. +7
   i32x4 kr[C::kPerThread], vr[C::kPerThread];
-
-  f32x16 o[OB];
+  f32x4 o[kFaQB][OB];
+  float m_run[kFaQB], l_run[kFaQB];
 #pragma unroll
-  for (int ob = 0; ob < OB; ++ob) o[ob] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.f;
+  for (int qb = 0; qb < kFaQB; ++qb) {
+#pragma unroll
+    for (int ob = 0; ob < OB; ++ob) o[qb][ob] = f32x4{};
+    m_run[qb] = -INFINITY;
+    l_run[qb] = 0.f;
+  }
   typedef short s16x4 __attribute__((ext_vector_type(4)));
   typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-  fa_load_tile<DH>(k, v, tok0, n, ldkv, g, 0, tid, kr, vr);
+  fa_load_tile<DH>(k, v, tok0, n, ldkv, g_kv, 0, tid, kr, vr);
   for (int t = 0; t < n_tiles; ++t) {
     __syncthreads();                                // every wave is done with the previous tile
     fa_store_tile<DH>(ks, vs, tid, kr, vr);
     __syncthreads();
-    if (t + 1 < n_tiles) fa_load_tile<DH>(k, v, tok0, n, ldkv, g, t + 1, tid, kr, vr);
+    if (t + 1 < n_tiles) fa_load_tile<DH>(k, v, tok0, n, ldkv, g_kv, t + 1, tid, kr, vr);
     const int kt0 = t * kFaK;
-    if (kt0 > qw0 + 31) continue;                   // every key of the tile is after this wave's queries
-    // S^T: block kb holds keys kt0 + 32 kb + 8 (v / 4) + 4 half + v % 4 of query my_q
-    f32x16 sacc[2] = {f32x16{}, f32x16{}};
+    if (kt0 > qw0 + kFaQW - 1) continue;            // every key of the tile is after this wave's queries
+    // S^T: key block kb, lane (query l16 of block qb, group g) holds keys kt0 + 16 kb + 4 g + v
+    f32x4 sacc[kFaQB][4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 4; ++kb) {
+#pragma unroll
+      for (int qb = 0; qb < kFaQB; ++qb) sacc[qb][kb] = f32x4{};
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        const f16x8 kf = *reinterpret_cast<const f16x8*>(ks + (32 * kb + l32) * C::KST + 16 * s + 8 * half);
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[s], sacc[kb], 0, 0, 0);
-      }
-    float sv[32];
-    float mx = -INFINITY;
+        const f16x8 kf = *reinterpret_cast<const f16x8*>(ks + (16 * kb + l16) * C::KST + 32 * s + 8 * g);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int vv = 0; vv < 16; ++vv) {
-        const int key = kt0 + 32 * kb + 8 * (vv >> 2) + 4 * half + (vv & 3);
-        const float x = sacc[kb][vv] * scale_log2;
-        sv[16 * kb + vv] = (key <= my_q && key < n) ? x : -INFINITY;
-        mx = fmaxf(mx, sv[16 * kb + vv]);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    float alpha = 1.f, ps = 0.f;
-    float p[32];
-    if (m_new == -INFINITY) {
-#pragma unroll
-      for (int i = 0; i < 32; ++i) p[i] = 0.f;
-    } else {
-      alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-#pragma unroll
-      for (int i = 0; i < 32; ++i) {
-        p[i] = __builtin_amdgcn_exp2f(sv[i] - m_new);
-        ps += p[i];
+        for (int qb = 0; qb < kFaQB; ++qb)
+          sacc[qb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[qb][s], sacc[qb][kb], 0, 0, 0);
       }
     }
-    ps += __shfl_xor(ps, 32, 64);
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-    if (__any(alpha != 1.f)) {
+    // softmax per query block; the scores become the probabilities in place
+    float p[kFaQB][4][4];
 #pragma unroll
-      for (int ob = 0; ob < OB; ++ob) o[ob] *= alpha;
-    }
-    // O^T += V^T P^T over the four 16-key steps (kb, mf): k-slot e of this lane
-    // is key 32 kb + 16 mf + 8 (e / 4) + 4 half + e % 4, i.e. score p[16 kb + 8 mf + e].
-    // The A operand comes from transposing reads: lane s of the 16-lane group
-    // (half, q16) addresses key 32 kb + 16 mf + 4 half + s / 4 (and + 8),
-    // channels 32 ob + 16 q16 + 4 (s % 4) .. +3, and receives its 4 keys of
-    // one channel.
+    for (int qb = 0; qb < kFaQB; ++qb) {
+      float mx = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int mf = 0; mf < 2; ++mf) {
-        f16x8 pf;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pf[e] = (_Float16)p[16 * kb + 8 * mf + e];
-        const int key = 32 * kb + 16 * mf + 4 * half + (s16 >> 2);
-#pragma unroll
-        for (int ob = 0; ob < OB; ++ob) {
-          const int col = 32 * ob + 16 * q16 + 4 * (s16 & 3);
-          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vs + key * C::VST + col));
-          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vs + (key + 8) * C::VST + col));
-          const f16x4 flo = __builtin_bit_cast(f16x4, lo), fhi = __builtin_bit_cast(f16x4, hi);
-          const f16x8 a = {flo[0], flo[1], flo[2], flo[3], fhi[0], fhi[1], fhi[2], fhi[3]};
-          o[ob] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pf, o[ob], 0, 0, 0);
+        for (int vv = 0; vv < 4; ++vv) {
+          const int key = kt0 + 16 * kb + 4 * g + vv;
+          p[qb][kb][vv] = (key <= my_q[qb] && key < n) ? sacc[qb][kb][vv] * scale_log2 : -INFINITY;
+          mx = fmaxf(mx, p[qb][kb][vv]);
         }
+      const float m_new = fmaxf(m_run[qb], fa_rows4_max(mx));
+      float alpha = 1.f, ps = 0.f;
+      if (m_new == -INFINITY) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int vv = 0; vv < 4; ++vv) p[qb][kb][vv] = 0.f;
+      } else {
+        alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int vv = 0; vv < 4; ++vv) {
+            p[qb][kb][vv] = __builtin_amdgcn_exp2f(p[qb][kb][vv] - m_new);
+            ps += p[qb][kb][vv];
+          }
       }
+      l_run[qb] = l_run[qb] * alpha + fa_rows4_sum(ps);
+      m_run[qb] = m_new;
+      if (__any(alpha != 1.f)) {
+#pragma unroll
+        for (int ob = 0; ob < OB; ++ob) o[qb][ob] *= alpha;
+      }
+    }
+    // O^T += V^T P^T in two 32-key steps st: k-slot e of lane group g is key
+    // 32 st + 16 (e / 4) + 4 g + e % 4, i.e. score p[2 st + e / 4][e % 4].
+    // The A operand comes from transposing reads: lane a of group g addresses
+    // key 4g + a/4 of the 16-key block, channels 16 ob + 4 (a % 4) .. +3, and
+    // lane i receives element i % 4 of the chunks of lanes i/4, 4 + i/4,
+    // 8 + i/4, 12 + i/4: channel 16 ob + i at keys 4g .. 4g+3 of the block.
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      f16x8 pf[kFaQB];
+#pragma unroll
+      for (int qb = 0; qb < kFaQB; ++qb)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[qb][e] = (_Float16)p[qb][2 * st + (e >> 2)][e & 3];
+      const int key = 32 * st + 4 * g + (l16 >> 2);
+#pragma unroll
+      for (int ob = 0; ob < OB; ++ob) {
+        const _Float16* a0 = vs + key * C::VST + 16 * ob + 4 * (l16 & 3);
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)a0);
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(a0 + 16 * C::VST));
+        const f16x4 flo = __builtin_bit_cast(f16x4, lo), fhi = __builtin_bit_cast(f16x4, hi);
+        const f16x8 a = {flo[0], flo[1], flo[2], flo[3], fhi[0], fhi[1], fhi[2], fhi[3]};
+#pragma unroll
+        for (int qb = 0; qb < kFaQB; ++qb) o[qb][ob] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, pf[qb], o[qb][ob], 0, 0, 0);
+      }
+    }
   }
 
   // O / l through LDS, so that each query row leaves as 16-byte runs: lane
-  // (l32, half) holds query qw0 + l32 at channels 32 ob + 8 vq + 4 half .. +3.
+  // (l16, g) holds query qw0 + 16 qb + l16 at channels 16 ob + 4 g .. +3.
   __syncthreads();
-  const float inv_l = l_run > 0.f ? 1.f / l_run : 0.f;
-  _Float16* ost = reinterpret_cast<_Float16*>(fa_smem) + w * 32 * C::OST;
+  _Float16* ost = reinterpret_cast<_Float16*>(fa_smem) + w * kFaQW * C::OST;
 #pragma unroll
-  for (int ob = 0; ob < OB; ++ob)
+  for (int qb = 0; qb < kFaQB; ++qb) {
+    const float inv_l = l_run[qb] > 0.f ? 1.f / l_run[qb] : 0.f;
 #pragma unroll
-    for (int vq = 0; vq < 4; ++vq) {
-      const f16x4 v4 = {(_Float16)(o[ob][4 * vq] * inv_l), (_Float16)(o[ob][4 * vq + 1] * inv_l),
-                        (_Float16)(o[ob][4 * vq + 2] * inv_l), (_Float16)(o[ob][4 * vq + 3] * inv_l)};
-      *reinterpret_cast<f16x4*>(ost + l32 * C::OST + 32 * ob + 8 * vq + 4 * half) = v4;
+    for (int ob = 0; ob < OB; ++ob) {
+      const f16x4 v4 = {(_Float16)(o[qb][ob][0] * inv_l), (_Float16)(o[qb][ob][1] * inv_l),
+                        (_Float16)(o[qb][ob][2] * inv_l), (_Float16)(o[qb][ob][3] * inv_l)};
+      *reinterpret_cast<f16x4*>(ost + (16 * qb + l16) * C::OST + 16 * ob + 4 * g) = v4;
     }
+  }
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < 32 * RUNS / 64; ++i) {
+  for (int i = 0; i < kFaQW * RUNS / 64; ++i) {
     const int e = lane + 64 * i, row = e / RUNS, c8 = e - row * RUNS;
     const int qq = qw0 + row;
     if (qq < n)
