@@ -51,6 +51,46 @@ __device__ __forceinline__ int quant_code(float v, float qm) {
   return (int)t;
 }
 
+// The same code in four VALU operations, for the row quantizers: y = fl(x * inv)
+// (an FMA with a -0 addend rounds the exact product once, as the product alone
+// does, and keeps its sign), clamped to [-qm, qm], then rounded half to even to
+// an integer by adding 1.5 * 2^23 (for |y| <= 2^22 the sum holds that integer in
+// its low mantissa bits).  The low byte (nibble) of the returned word is the
+// two's-complement code; inv == 0 (an all-zero row) gives code 0.
+__device__ __forceinline__ uint32_t code_bits(float x, float inv, float qm) {
+  const float y = __builtin_amdgcn_fmed3f(__builtin_fmaf(x, inv, -0.0f), -qm, qm);
+  return __float_as_uint(add_rn(y, 12582912.0f));
+}
+
+// Low bytes of four code words -> one word, element e in byte e.
+__device__ __forceinline__ uint32_t pack4_codes8(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3) {
+  const uint32_t p01 = __builtin_amdgcn_perm(b1, b0, 0x0c0c0400u);
+  const uint32_t p23 = __builtin_amdgcn_perm(b3, b2, 0x0c0c0400u);
+  return __builtin_amdgcn_perm(p23, p01, 0x05040100u);
+}
+
+// Low nibbles of eight code words -> one word, element e in bits 4e .. 4e+3.
+__device__ __forceinline__ uint32_t pack8_codes4(const uint32_t* b) {
+  const uint32_t lo = pack4_codes8(b[0], b[1], b[2], b[3]) & 0x0f0f0f0fu;
+  const uint32_t hi = pack4_codes8(b[4], b[5], b[6], b[7]) & 0x0f0f0f0fu;
+  const uint32_t l2 = lo | (lo >> 4), h2 = hi | (hi >> 4);   // bytes 0 and 2 hold nibble pairs
+  return __builtin_amdgcn_perm(h2, l2, 0x06040200u);
+}
+
+// Running max of |x| over fp16 values as bit patterns, two halves per lane
+// word: for non-NaN fp16 values |x| orders like the bits of |x|.
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u16x2 absmax_f16x8(u16x2 m, f16x8 v) {
+  const i32x4 w = __builtin_bit_cast(i32x4, v);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, (uint32_t)w[k] & 0x7fff7fffu));
+  return m;
+}
+__device__ __forceinline__ float absmax_value(u16x2 m) {
+  const uint16_t b = m.x > m.y ? m.x : m.y;
+  return (float)__builtin_bit_cast(_Float16, b);
+}
+
 // Output-tile order of the GEMM grids.  The chip dispatches workgroup i to
 // XCD i % 8, and each XCD has its own L2.  The ids one XCD receives are made
 // consecutive, and consecutive ids walk a block of gm tile rows column by

@@ -17,7 +17,7 @@ quantize_rows_kernel(const _Float16* __restrict__ x, int64_t M, int32_t K, int64
   const int nch = K >> 3;
   constexpr int REG = MAXC > 0 ? MAXC : 1;
   f16x8 v[REG];
-  float amax = 0.f;
+  u16x2 mb = u16x2{0, 0};
   if (MAXC > 0) {
 #pragma unroll
     for (int i = 0; i < REG; ++i) {
@@ -25,17 +25,11 @@ quantize_rows_kernel(const _Float16* __restrict__ x, int64_t M, int32_t K, int64
       v[i] = c < nch ? *reinterpret_cast<const f16x8*>(row + c * 8) : f16x8{};
     }
 #pragma unroll
-    for (int i = 0; i < REG; ++i)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)v[i][e]));
+    for (int i = 0; i < REG; ++i) mb = absmax_f16x8(mb, v[i]);
   } else {
-    for (int c = lane; c < nch; c += 64) {
-      const f16x8 t = *reinterpret_cast<const f16x8*>(row + c * 8);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)t[e]));
-    }
+    for (int c = lane; c < nch; c += 64) mb = absmax_f16x8(mb, *reinterpret_cast<const f16x8*>(row + c * 8));
   }
-  amax = wave_max(amax);
+  const float amax = wave_max(absmax_value(mb));
   const float qm = (float)((1 << (BITS - 1)) - 1);
   const float a = mul_rn(clip, amax);
   float inv = 0.f, s = 1.f;
@@ -45,19 +39,14 @@ quantize_rows_kernel(const _Float16* __restrict__ x, int64_t M, int32_t K, int64
   }
   if (lane == 0) sx[m] = s;
   auto emit = [&](int c, const f16x8& t) {
-    int q[8];
+    uint32_t q[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) q[e] = (a != 0.f) ? quant_code(mul_rn((float)t[e], inv), qm) : 0;
-    if (BITS == 8) {
-      uint32_t lo = (q[0] & 0xff) | ((q[1] & 0xff) << 8) | ((q[2] & 0xff) << 16) | ((uint32_t)(q[3] & 0xff) << 24);
-      uint32_t hi = (q[4] & 0xff) | ((q[5] & 0xff) << 8) | ((q[6] & 0xff) << 16) | ((uint32_t)(q[7] & 0xff) << 24);
-      *reinterpret_cast<uint2*>(xq + m * (int64_t)K + c * 8) = make_uint2(lo, hi);
-    } else {
-      uint32_t p = 0;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) p |= (uint32_t)(q[e] & 0xf) << (4 * e);
-      *reinterpret_cast<uint32_t*>(xq + m * (int64_t)(K / 2) + c * 4) = p;
-    }
+    for (int e = 0; e < 8; ++e) q[e] = code_bits((float)t[e], inv, qm);
+    if (BITS == 8)
+      *reinterpret_cast<uint2*>(xq + m * (int64_t)K + c * 8) =
+          make_uint2(pack4_codes8(q[0], q[1], q[2], q[3]), pack4_codes8(q[4], q[5], q[6], q[7]));
+    else
+      *reinterpret_cast<uint32_t*>(xq + m * (int64_t)(K / 2) + c * 4) = pack8_codes4(q);
   };
   if (MAXC > 0) {
 #pragma unroll

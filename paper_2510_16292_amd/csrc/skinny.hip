@@ -29,7 +29,8 @@
 
 namespace qsvd {
 
-constexpr int kSkCols = 16;        // output columns per workgroup
+constexpr int kSkCols = 16;        // output columns of one 16x16x64 product
+constexpr int kSkMinGrid = 256;    // workgroups wanted: one per CU
 constexpr int kSkMaxWaves = 16;
 constexpr int kSkBatch = 4;        // 64-byte contraction steps loaded per batch
 constexpr int kSkMaxRowChunks = 8;  // fp16 row pass: K <= 8 * 64 * 8 = 4096
@@ -120,7 +121,7 @@ skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, cons
                    const uint8_t* __restrict__ bt, const float* __restrict__ col_scale, int32_t sstride,
                    int32_t M, int32_t N, int32_t K, int32_t group, int32_t nw, int32_t abits, int32_t qa_off,
                    SkinnyOut so, int32_t* __restrict__ dbg, uint8_t* __restrict__ cq_out, float* __restrict__ sc_out,
-                   SkinnyAppend ap) {
+                   SkinnyAppend ap, int32_t cols) {
   // [0, qa_off): int32 tiles, [slot][row block][lane] (slot = wave for
   // per-channel weights, group for per-group ones); [qa_off, ...): Q(C) rows.
   extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];
@@ -129,8 +130,10 @@ skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, cons
   __shared__ float rsc[32];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, quad = lane >> 4;
-  const int32_t n = blockIdx.x * kSkCols + l16;           // this lane's weight row (output column)
-  const bool ncol = n < N;
+  // the workgroup's first `cols` (16, 8 or 4) product columns are output
+  // columns, the rest of the product stays zero
+  const int32_t n = blockIdx.x * cols + l16;           // this lane's weight row (output column)
+  const bool ncol = l16 < cols && n < N;
   const int rbl = (M + 15) / 16;
   const int qa_ld = K + 16;
   const float qm = (float)((1 << (abits - 1)) - 1);
@@ -144,16 +147,16 @@ skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, cons
   __shared__ float s_gscale[kSkMaxGroups * kSkCols];
   const int ng = group ? K / group : 0;
   float pre_rs = 1.f, pre_cs = 0.f;
-  if (tid < M * kSkCols) {
-    const int32_t nn = blockIdx.x * kSkCols + tid % kSkCols;
+  if (tid < M * cols) {
+    const int32_t nn = blockIdx.x * cols + tid % cols;
     if (nn < N) {
-      if (ASRC == SK_A_I8) pre_rs = row_scale_in[tid / kSkCols];
+      if (ASRC == SK_A_I8) pre_rs = row_scale_in[tid / cols];
       if (!group) pre_cs = col_scale[nn];
     }
   }
   for (int i = tid; i < ng * kSkCols; i += 64 * nw) {
-    const int32_t nn = blockIdx.x * kSkCols + i % kSkCols;
-    s_gscale[i] = nn < N ? col_scale[(int64_t)(i / kSkCols) * sstride + nn] : 0.f;
+    const int32_t nn = blockIdx.x * cols + i % kSkCols;
+    s_gscale[i] = i % kSkCols < cols && nn < N ? col_scale[(int64_t)(i / kSkCols) * sstride + nn] : 0.f;
   }
 
   i32x4 bw[kSkBatch];
@@ -186,12 +189,10 @@ skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, cons
         const int c = lane + 64 * i;
         v[i] = c < nch ? *reinterpret_cast<const f16x8*>(ch + (int64_t)m * lda + 8 * c) : f16x8{};
       }
-      float mx = 0.f;
+      u16x2 mb = u16x2{0, 0};
 #pragma unroll
-      for (int i = 0; i < kSkMaxRowChunks; ++i)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf((float)v[i][e]));
-      const float a = mul_rn(clip, wave_max(mx));
+      for (int i = 0; i < kSkMaxRowChunks; ++i) mb = absmax_f16x8(mb, v[i]);
+      const float a = mul_rn(clip, wave_max(absmax_value(mb)));
       const float inv = a != 0.f ? div_rn(qm, a) : 0.f;
       const float sc = a != 0.f ? div_rn(a, qm) : 1.f;
       const bool own = (m % (int)gridDim.x) == (int)blockIdx.x;
@@ -209,20 +210,17 @@ skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, cons
       for (int i = 0; i < kSkMaxRowChunks; ++i) {
         const int c = lane + 64 * i;
         if (c >= nch) continue;
-        int q[8];
+        uint32_t q[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) q[e] = inv == 0.f ? 0 : quant_code(mul_rn((float)v[i][e], inv), qm);
-        const uint32_t lo = (q[0] & 0xff) | ((q[1] & 0xff) << 8) | ((q[2] & 0xff) << 16) | ((uint32_t)(q[3] & 0xff) << 24);
-        const uint32_t hi = (q[4] & 0xff) | ((q[5] & 0xff) << 8) | ((q[6] & 0xff) << 16) | ((uint32_t)(q[7] & 0xff) << 24);
+        for (int e = 0; e < 8; ++e) q[e] = code_bits((float)v[i][e], inv, qm);
+        const uint32_t lo = pack4_codes8(q[0], q[1], q[2], q[3]), hi = pack4_codes8(q[4], q[5], q[6], q[7]);
         *reinterpret_cast<uint2*>(qa + m * qa_ld + 8 * c) = make_uint2(lo, hi);
         if (own && (cq_out || app_row)) {
           if (abits == 8) {
             if (cq_out) *reinterpret_cast<uint2*>(cq_out + (int64_t)m * K + 8 * c) = make_uint2(lo, hi);
             if (app_row) *reinterpret_cast<uint2*>(crow + 8 * c) = make_uint2(lo, hi);
           } else {
-            uint32_t p = 0;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) p |= (uint32_t)(q[e] & 0xf) << (4 * e);
+            const uint32_t p = pack8_codes4(q);
             if (cq_out) *reinterpret_cast<uint32_t*>(cq_out + (int64_t)m * (K / 2) + 4 * c) = p;
             if (app_row) *reinterpret_cast<uint32_t*>(crow + 4 * c) = p;
           }
@@ -290,9 +288,9 @@ skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, cons
   __syncthreads();
 
   // --- epilogue: one thread per output (row m, column n) ------------------------
-  for (int t = tid; t < M * kSkCols; t += 64 * nw) {
-    const int m = t / kSkCols, nl = t % kSkCols;
-    const int32_t nn = blockIdx.x * kSkCols + nl;
+  for (int t = tid; t < M * cols; t += 64 * nw) {
+    const int m = t / cols, nl = t % cols;
+    const int32_t nn = blockIdx.x * cols + nl;
     if (nn >= N) continue;
     const int rb = m >> 4, mm = m & 15, src = 16 * (mm >> 2) + nl, v = mm & 3;
     const bool first = t == tid;
@@ -322,10 +320,17 @@ struct SkinnyPlan {
   int nw;            // waves per workgroup
   int32_t qa_off;    // LDS bytes of the int32 tiles
   size_t lds;        // dynamic LDS bytes
+  int32_t cols;      // output columns per workgroup
 };
 
-static SkinnyPlan skinny_plan(int64_t M, int32_t K, int32_t group, bool f16q) {
+// Narrower column strips (8 or 4 of the product's 16 columns) while the grid
+// still fits one workgroup per CU: the weight stream then spreads over more
+// CUs, at the price of a repeated A operand (and row pass) per workgroup and
+// idle product columns.  (A second round of workgroups would double the time.)
+static SkinnyPlan skinny_plan(int64_t M, int32_t K, int32_t N, int32_t group, bool f16q) {
   SkinnyPlan p{};
+  p.cols = kSkCols;
+  while (p.cols > 4 && (N + p.cols / 2 - 1) / (p.cols / 2) <= kSkMinGrid) p.cols /= 2;
   const int steps = K / 64, ng = group ? K / group : 0;
   p.nw = std::min(kSkMaxWaves, group ? ng : steps);
   const int rbl = (int)((M + 15) / 16);
@@ -339,7 +344,7 @@ bool skinny_supported(int64_t M, int32_t K, int32_t group, bool f16q) {
   if (M < 1 || M > 32 || K < 64 || K % 64) return false;
   if (group && (group % 64 || K % group || K / group > kSkMaxGroups)) return false;
   if (f16q && K > kSkMaxRowChunks * 64 * 8) return false;
-  return skinny_plan(M, K, group, f16q).lds <= kSkLdsLimit;
+  return skinny_plan(M, K, kSkCols, group, f16q).lds <= kSkLdsLimit;
 }
 
 hipError_t launch_skinny(const GemmArgs& g, bool a_is_f16_latent, int32_t wbits, int32_t group, int32_t sstride,
@@ -361,8 +366,8 @@ hipError_t launch_skinny_fused(const GemmArgs& g, int32_t asrc, float clip, int6
     so.n0[i] = i < g.n_seg ? g.seg[i].n0 : 0;
     so.n[i] = i < g.n_seg ? g.seg[i].n : 0;
   }
-  const SkinnyPlan p = skinny_plan(g.M, g.K, group, a_is_f16_latent);
-  dim3 grid((g.N + kSkCols - 1) / kSkCols), block(64 * p.nw);
+  const SkinnyPlan p = skinny_plan(g.M, g.K, g.N, group, a_is_f16_latent);
+  dim3 grid((g.N + p.cols - 1) / p.cols), block(64 * p.nw);
   const int32_t M = (int32_t)g.M;
   const uint8_t* bt = (const uint8_t*)g.b;
   // more than 64 KB of dynamic LDS has to be allowed per kernel before the launch
@@ -377,12 +382,12 @@ hipError_t launch_skinny_fused(const GemmArgs& g, int32_t asrc, float clip, int6
     if (hipError_t e = allow((const void*)k); e != hipSuccess) return e;
     QSVD_LAUNCH(ks, k, grid, block, p.lds, s, (const void*)g.a, (int64_t)g.K, 1.f, g.row_scale, bt, g.col_scale,
                        sstride, M, g.N, g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)nullptr,
-                       (float*)nullptr, ap);
+                       (float*)nullptr, ap, p.cols);
   } else {
     auto k = wbits == 8 ? skinny_gemm_kernel<SK_A_F16Q, 8> : skinny_gemm_kernel<SK_A_F16Q, 4>;
     if (hipError_t e = allow((const void*)k); e != hipSuccess) return e;
     QSVD_LAUNCH(ks, k, grid, block, p.lds, s, (const void*)g.a, lda, clip, (const float*)nullptr, bt, g.col_scale,
-                       sstride, M, g.N, g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)g.cq, g.sc, ap);
+                       sstride, M, g.N, g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)g.cq, g.sc, ap, p.cols);
   }
   return hipGetLastError();
 }
