@@ -139,6 +139,34 @@ def timed_sample(fn, budget_s, max_iters):
     return n, time.perf_counter() - t0
 
 
+def replay_seconds(fn, per_graph, replays=5):
+    """Mean seconds per call of fn(stream_handle) when per_graph calls run back
+    to back: the calls are captured once into a graph, which is replayed
+    `replays` times between two events on the replay stream.  Short launches
+    timed one by one with their own events read several microseconds long, and
+    a host loop of short calls can be bound by the host; the replayed graph is
+    neither."""
+    import torch
+
+    from paper_2510_16292_amd import binding as B
+    fn(B.stream_handle())
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(per_graph):
+            fn(B.stream_handle())
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(replays):
+        g.replay()
+    e1.record()
+    e1.synchronize()
+    del g
+    return e0.elapsed_time(e1) * 1e-3 / (replays * per_graph)
+
+
 def layer_weights(wl, w_bits=8, w_group=0):
     from paper_2510_16292_amd import prep
     from workloads import gen
@@ -270,13 +298,20 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
     # cached tokens each attention launch reads (context after the append)
     ctx_read = sum(batch * (ctx0 + 1 + i // n_layers) for i in range(steps))
     attn_name = "latent_attn" if mode != B.QSVD_ATTN_RECONSTRUCT else "recon"
-    if profile:
-        B.profile_reset()
-        B.profile_enable(True, attn_name)
+    # the attention kernel's launches are timed with their own events on the
+    # launch stream in every 16th step of the timed region (an event pair per
+    # launch adds a few microseconds to its step)
+    sample = 16
+    B.profile_reset()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
-        step(i)
+        if profile and i % sample == 0:
+            B.profile_enable(True, attn_name)
+            step(i)
+            B.profile_enable(False)
+        else:
+            step(i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     B.profile_enable(False)
@@ -291,7 +326,9 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
         if n:
             avg_s = kms / n * 1e-3
             row_bytes = r * 2 if f16 else r + 4            # cached latent row (+ fp32 scale)
-            bytes_per_launch = ctx_read / steps * row_bytes
+            # cached tokens the sampled launches read
+            ctx_sampled = sum(batch * (ctx0 + 1 + i // n_layers) for i in range(0, steps, sample))
+            bytes_per_launch = ctx_sampled / len(range(0, steps, sample)) * row_bytes
             achieved = bytes_per_launch / avg_s / 1e9
             traffic = counted_traffic(traffic_summary) if traffic_summary and mode != B.QSVD_ATTN_RECONSTRUCT \
                 else None
@@ -303,15 +340,16 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
                                "bytes_per_launch": int(bytes_per_launch)}
     # the same step as four separate calls (quantize, projection, append,
     # attention), four visits of every layer after one, for comparison
-    reset()
-    for i in range(n_layers):
-        step_unfused(i)
-    torch.cuda.synchronize()
-    u0 = time.perf_counter()
-    for i in range(n_layers, 5 * n_layers):
-        step_unfused(i)
-    torch.cuda.synchronize()
-    res["unfused_ms_per_step"] = (time.perf_counter() - u0) * 1e3 / (4 * n_layers)
+    for key, fn in (("unfused_ms_per_step", step_unfused),):
+        reset()
+        for i in range(n_layers):
+            fn(i)
+        torch.cuda.synchronize()
+        u0 = time.perf_counter()
+        for i in range(n_layers, 5 * n_layers):
+            fn(i)
+        torch.cuda.synchronize()
+        res[key] = (time.perf_counter() - u0) * 1e3 / (4 * n_layers)
 
     # The same steps replayed from one captured graph of a full rotation
     # through the layers (launch grids follow each cache's host max_len, held
@@ -418,51 +456,38 @@ def bench_prefill(args, wl2, host_layer):
     s = B.stream_handle()
     P = B.ptr
 
-    def call():
-        B.check(B.qsvd_quantize_act(P(X), M, d, d, 8, 1.0, P(xq), P(sx), s))
-        B.check(B.qsvd_lowrank_qkv_prefill(dl.c, P(xq), P(sx), M, 8, 7, P(c_h), P(cq), P(sc), P(q), P(k), P(v),
-                                           0, 0, P(ws), wsb, s))
+    # one prefill call: the activation quantizer, then the projection (X W^d,
+    # the latent quantization Q(C), Q(C) W^u)
+    def quantize(st):
+        B.check(B.qsvd_quantize_act(P(X), M, d, d, 8, 1.0, P(xq), P(sx), st))
 
-    for _ in range(3):
-        call()
-    B.profile_reset()
-    B.profile_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.prefill_steps):
-        call()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    B.profile_enable(False)
-    gms, n = B.profile_read("gemm_i8")
-    qms, qn = B.profile_read("latent_quant")
-    B.profile_reset()
+    def project(st):
+        B.check(B.qsvd_lowrank_qkv_prefill(dl.c, P(xq), P(sx), M, 8, 7, P(c_h), P(cq), P(sc), P(q), P(k), P(v),
+                                           0, 0, P(ws), wsb, st))
+
+    def call(st):
+        quantize(st)
+        project(st)
+
     ops = 2.0 * M * (d * r + r * L.N)            # X W^d then Q(C) W^u, multiply-adds counted twice
-    gemm_s = gms * 1e-3 / args.prefill_steps
-    # the projection proper: both products and the latent quantization Q(C) between them
-    proj_s = (gms + qms) * 1e-3 / args.prefill_steps
+    reps = max(args.prefill_steps // 5, 1)
+    # the projection proper: both products and the latent quantization between them
+    proj_s = replay_seconds(project, reps)
+    call_s = replay_seconds(call, reps)
+    # Q(C) alone: the same kernel and grid as inside the projection call
+    lq_s = replay_seconds(lambda st: B.check(B.qsvd_quantize_act(P(c_h), M, r, r, 8, 1.0, P(cq), P(sc), st)), 20)
+    gemm_s = proj_s - lq_s
     # the activation quantizer alone, plain and with the online H1 rotation
     # (block Walsh-Hadamard of order 4096 with seeded signs): fp16 in, int8 + scale out
     signs = torch.from_numpy(np.where(np.arange(d) % 3 == 0, -1, 1).astype(np.int8)).cuda()
     quant = {}
-    for name, fn in (("plain", lambda: B.check(B.qsvd_quantize_act(P(X), M, d, d, 8, 1.0, P(xq), P(sx), s))),
-                     ("rotated", lambda: B.check(B.qsvd_quantize_act_rotated(P(X), M, d, d, 8, 1.0, P(signs), d,
-                                                                              P(xq), P(sx), s)))):
-        fn()
-        torch.cuda.synchronize()
-        B.profile_reset()
-        B.profile_enable(True, "quantize")
-        for _ in range(20):
-            fn()
-        torch.cuda.synchronize()
-        B.profile_enable(False)
-        qms, qn = B.profile_read("quantize")
-        B.profile_reset()
-        us = qms * 1e3 / qn
+    for name, fn in (("plain", quantize),
+                     ("rotated", lambda st: B.check(B.qsvd_quantize_act_rotated(P(X), M, d, d, 8, 1.0, P(signs), d,
+                                                                                 P(xq), P(sx), st)))):
+        us = replay_seconds(fn, 20) * 1e6
         qbytes = M * (2 * d + d + 4)
         quant[name] = {"us": round(us, 2), "GB/s": round(qbytes / (us * 1e-6) / 1e9, 1),
                        "frac": round(qbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
-    call_s = (t1 - t0) / args.prefill_steps
     tops = ops / proj_s / 1e12
     # causal attention of the 4 x 640 prompt over the projection's own Q, K, V
     # (fp16 matrix cores), and the latent (absorbed) form of the same
@@ -494,15 +519,16 @@ def bench_prefill(args, wl2, host_layer):
                               "kernel": "prefill_flash_kernel (fp16, 4 dh flop per causal pair and head)"}}
     # HBM bytes of one call's two products (both launches), from the committed counter summary
     traffic = counted_traffic(GEMM_TRAFFIC_SUMMARY) if (M, d, r, L.N) == (2560, 4096, 1536, 12288) else None
-    return {"value": round(tops, 1), "unit": "TOPS", "ms_per_call": round(call_s * 1e3, 4),
-            "kernels_ms_per_call": round(proj_s * 1e3, 4), "gemm_ms_per_call": round(gemm_s * 1e3, 4),
-            "latent_quant_ms_per_call": round(qms / args.prefill_steps, 4),
+    return {"value": round(tops, 1), "unit": "TOPS", "timing": "graph replay of back-to-back calls",
+            "ms_per_call": round(call_s * 1e3, 4),
+            "projection_ms_per_call": round(proj_s * 1e3, 4), "gemm_ms_per_call": round(gemm_s * 1e3, 4),
+            "latent_quant_ms_per_call": round(lq_s * 1e3, 4),
             "gemm_only_tops": round(ops / gemm_s / 1e12, 1), "call_tops": round(ops / call_s / 1e12, 1),
             "tokens": M, "gop_per_call": round(ops / 1e9, 2), "quantizer": quant, "attention": attention,
             "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
                          "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None if traffic is None else int(traffic),
                          "kernel": "gemm_i8 (X W^d, Q(C) W^u) + latent quantization Q(C)",
-                         "launches": n + qn}}
+                         "launches": 3 * reps * 5}}
 
 
 F16_PEAK_TFLOPS = 2500.0       # MI355X dense fp16 matrix peak, TFLOP/s
@@ -514,30 +540,18 @@ def causal_flops(lengths, n_q_heads, head_dim):
 
 
 def time_prefill_attention(q, k, v, lengths, n_q_heads, n_kv_heads, head_dim, reps):
-    """Mean launch time (s) of the causal prefill attention over the given rows,
-    from the kernel's own events on its launch stream."""
+    """Mean time (s) per causal prefill attention launch over the given rows,
+    launches back to back (graph replay)."""
     import torch
 
     from paper_2510_16292_amd import binding as B
     cu = torch.tensor(np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32), device="cuda")
     out = torch.empty_like(q)
-    s = B.stream_handle()
 
-    def call():
+    def call(st):
         B.check(B.qsvd_prefill_attention(B.ptr(q), B.ptr(k), B.ptr(v), len(lengths), B.ptr(cu), max(lengths),
-                                         n_q_heads, n_kv_heads, head_dim, 0.0, B.ptr(out), s))
-    for _ in range(3):
-        call()
-    torch.cuda.synchronize()
-    B.profile_reset()
-    B.profile_enable(True, "prefill_flash")
-    for _ in range(reps):
-        call()
-    torch.cuda.synchronize()
-    B.profile_enable(False)
-    ms, n = B.profile_read("prefill_flash")
-    B.profile_reset()
-    return ms * 1e-3 / n
+                                         n_q_heads, n_kv_heads, head_dim, 0.0, B.ptr(out), st))
+    return replay_seconds(call, reps)
 
 
 def stack_layers(wl5):
@@ -581,31 +595,27 @@ def bench_stack_prefill(args, wl5, ranks, layers):
     lib, s, P = B.lib(), B.stream_handle(), B.ptr
     xs_p = [P(x) for x in xs]
 
-    def stack_pass():
+    # a pass: per layer the 4-bit activation quantizer, then the projection
+    # (X W^d, Q(C), Q(C) W^u); the projections alone; the latent quantizations alone
+    def stack_pass(st, quantize=True, project=True, latent_only=False):
         for li, dl in enumerate(layers):
-            st = lib.qsvd_quantize_act(xs_p[li % 2], M, d, d, 4, 1.0, P(xq), P(sx), s)
-            st |= lib.qsvd_lowrank_qkv_prefill(dl.c, P(xq), P(sx), M, 4, 7, P(c_h), P(cq), P(sc), P(q), P(k), P(v),
-                                               0, 0, 0, 0, s)
-            if st:
-                raise B.QsvdError(st, B.last_error())
+            e = 0
+            if quantize:
+                e |= lib.qsvd_quantize_act(xs_p[li % 2], M, d, d, 4, 1.0, P(xq), P(sx), st)
+            if project:
+                e |= lib.qsvd_lowrank_qkv_prefill(dl.c, P(xq), P(sx), M, 4, 7, P(c_h), P(cq), P(sc), P(q), P(k),
+                                                  P(v), 0, 0, 0, 0, st)
+            if latent_only:
+                e |= lib.qsvd_quantize_act(P(c_h), M, ranks[li], ranks[li], 4, 1.0, P(cq), P(sc), st)
+            if e:
+                raise B.QsvdError(e, B.last_error())
 
-    stack_pass()
-    torch.cuda.synchronize()
-    B.profile_reset()
-    B.profile_enable(True)
-    t0 = time.perf_counter()
-    for _ in range(args.stack_passes):
-        stack_pass()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    B.profile_enable(False)
-    gms, n = B.profile_read("gemm")
-    qms, qn = B.profile_read("latent_quant")
-    B.profile_reset()
+    passes = max(args.stack_passes, 1)
+    pass_s = replay_seconds(stack_pass, 1, passes)
+    proj_s = replay_seconds(lambda st: stack_pass(st, quantize=False), 1, passes)
+    lq_s = replay_seconds(lambda st: stack_pass(st, quantize=False, project=False, latent_only=True), 1, passes)
+    gemm_s = proj_s - lq_s
     ops = sum(2.0 * M * r * (d + L.N) for r in ranks)
-    gemm_s = gms * 1e-3 / args.stack_passes
-    proj_s = (gms + qms) * 1e-3 / args.stack_passes
-    pass_s = (t1 - t0) / args.stack_passes
     tops = ops / proj_s / 1e12
     lengths = [M // wl5.prefill_batch] * wl5.prefill_batch
     att_s = time_prefill_attention(q, k, v, lengths, L.n_q_heads, L.n_kv_heads, L.head_dim, 40)
@@ -618,14 +628,16 @@ def bench_stack_prefill(args, wl5, ranks, layers):
                               "kernel": "prefill_flash_kernel (fp16)"}}
     del xs, xq, c_h, cq, q, k, v
     traffic = counted_traffic(STACK_GEMM_TRAFFIC_SUMMARY)
-    return {"value": round(tops, 1), "unit": "TOPS", "ms_per_pass": round(pass_s * 1e3, 3),
-            "kernels_ms_per_pass": round(proj_s * 1e3, 3), "gemm_ms_per_pass": round(gemm_s * 1e3, 3),
+    return {"value": round(tops, 1), "unit": "TOPS", "timing": "graph replay of whole passes",
+            "ms_per_pass": round(pass_s * 1e3, 3),
+            "projection_ms_per_pass": round(proj_s * 1e3, 3), "gemm_ms_per_pass": round(gemm_s * 1e3, 3),
+            "latent_quant_ms_per_pass": round(lq_s * 1e3, 3),
             "gemm_only_tops": round(ops / gemm_s / 1e12, 1), "call_tops": round(ops / pass_s / 1e12, 1),
             "tokens": M, "layers": len(ranks), "top_per_pass": round(ops / 1e12, 3), "attention": attention,
             "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
                          "frac": round(tops / INT8_PEAK_TOPS, 4), "traffic": None if traffic is None else int(traffic),
                          "kernel": "gemm_q4_pipe (X W^d and Q(C) W^u, int4 x int4) + latent quantization Q(C)",
-                         "launches": n + qn}}
+                         "launches": 3 * len(ranks) * passes}}
 
 
 def bench_stack_decode(args, wl5, ranks, layers):

@@ -277,9 +277,9 @@ qsvd_status qsvd_lowrank_qkv_prefill(const qsvd_layer* w, const void* xq, const 
                     "up-projection");
 }
 
-qsvd_status qsvd_decode_project_append(const qsvd_layer* w, qsvd_cache* c, const void* x, int64_t ldx,
-                                       int32_t act_bits, float clip, void* xq, float* sx, void* c_h, void* cq,
-                                       float* sc, void* q, void* stream) {
+static qsvd_status check_project_append(const qsvd_layer* w, const qsvd_cache* c, const void* x, int64_t ldx,
+                                        int32_t act_bits, float clip, const void* xq, const float* sx,
+                                        const void* c_h, const void* cq, const float* sc, const void* q) {
   qsvd_status st = check_layer(w);
   if (st != QSVD_OK) return st;
   st = check_cache(c);
@@ -300,13 +300,15 @@ qsvd_status qsvd_decode_project_append(const qsvd_layer* w, qsvd_cache* c, const
   if (ldx % 8 || !aligned(x, 16) || !aligned(c_h, 16) || !aligned(cq, 16) || !aligned(xq, 16) ||
       !aligned(w->a_t, 16) || !aligned(w->b_t, 16))
     return fail(QSVD_ERR_UNSUPPORTED, "ldx a multiple of 8 and 16-byte aligned x, xq, c_h, cq and weight codes");
-  hipStream_t s = (hipStream_t)stream;
-  const int32_t nq = w->n_q_heads * w->head_dim;
-  const int32_t N = nq + 2 * w->n_kv_heads * w->head_dim;
-  const bool f16c = c->fmt == QSVD_CACHE_F16;
+  return QSVD_OK;
+}
 
-  // X W^d -> C: the quantizer of the activations runs inside the product
-  // when its rows fit the workgroup's LDS, else as its own launch first
+// X W^d -> C (and, for fp16 caches, C's row into the cache): the quantizer of
+// the activations runs inside the product when its rows fit the workgroup's
+// LDS, else as its own launch first.
+static qsvd_status decode_down(const qsvd_layer* w, const qsvd_cache* c, const void* x, int64_t ldx,
+                               int32_t act_bits, float clip, void* xq, float* sx, void* c_h, hipStream_t s) {
+  const int64_t M = c->batch;
   GemmArgs g1{};
   g1.b = (const int8_t*)w->a_t;
   g1.col_scale = w->s_a;
@@ -316,29 +318,46 @@ qsvd_status qsvd_decode_project_append(const qsvd_layer* w, qsvd_cache* c, const
   g1.seg[0] = OutSeg{(_Float16*)c_h, w->r, 0, w->r};
   g1.n_seg = 1;
   g1.abits = act_bits;
-  SkinnyAppendArgs a1{c->data, c->scale, c->seq_len, c->overflow, c->capacity, f16c ? 1 : 0};
+  SkinnyAppendArgs a1{c->data, c->scale, c->seq_len, c->overflow, c->capacity,
+                      c->fmt == QSVD_CACHE_F16 ? 1 : 0};
   if (skinny_supported(M, w->d, w->w_group, true)) {
     g1.a = (const int8_t*)x;
     g1.cq = xq;
     g1.sc = sx;
-    st = hip_status(launch_skinny_fused(g1, SKA_F16_ACT, clip, ldx, w->w_bits, w->w_group, w->r, a1, s),
-                    "decode down-projection");
-  } else {
-    st = hip_status(launch_quantize_rows(x, M, w->d, ldx, act_bits, clip, xq, sx, s), "quantize_act");
-    if (st != QSVD_OK) return st;
-    g1.a = (const int8_t*)xq;
-    g1.row_scale = sx;
-    st = hip_status(launch_skinny_fused(g1, SKA_CODES, 1.f, w->d, w->w_bits, w->w_group, w->r, a1, s),
-                    "decode down-projection");
+    return hip_status(launch_skinny_fused(g1, SKA_F16_ACT, clip, ldx, w->w_bits, w->w_group, w->r, a1, s),
+                      "decode down-projection");
   }
+  qsvd_status st = hip_status(launch_quantize_rows(x, M, w->d, ldx, act_bits, clip, xq, sx, s), "quantize_act");
+  if (st != QSVD_OK) return st;
+  g1.a = (const int8_t*)xq;
+  g1.row_scale = sx;
+  return hip_status(launch_skinny_fused(g1, SKA_CODES, 1.f, w->d, w->w_bits, w->w_group, w->r, a1, s),
+                    "decode down-projection");
+}
+
+// The cache update of the up-projection: the Q(C) row of integer caches and
+// the length advance (fp16 caches got their row from the down-projection).
+static SkinnyAppendArgs up_append(const qsvd_cache* c) {
+  return SkinnyAppendArgs{c->data, c->scale, c->seq_len, c->overflow, c->capacity, c->fmt == QSVD_CACHE_F16 ? 3 : 2};
+}
+
+qsvd_status qsvd_decode_project_append(const qsvd_layer* w, qsvd_cache* c, const void* x, int64_t ldx,
+                                       int32_t act_bits, float clip, void* xq, float* sx, void* c_h, void* cq,
+                                       float* sc, void* q, void* stream) {
+  qsvd_status st = check_project_append(w, c, x, ldx, act_bits, clip, xq, sx, c_h, cq, sc, q);
+  if (st != QSVD_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  st = decode_down(w, c, x, ldx, act_bits, clip, xq, sx, c_h, s);
   if (st != QSVD_OK) return st;
 
   // Q(C) W^u_q -> Q, with the cache row (integer caches) and the length advance
+  const int32_t nq = w->n_q_heads * w->head_dim;
+  const int32_t N = nq + 2 * w->n_kv_heads * w->head_dim;
   GemmArgs g2{};
   g2.a = (const int8_t*)c_h;
   g2.b = (const int8_t*)w->b_t;
   g2.col_scale = w->s_b;
-  g2.M = M;
+  g2.M = c->batch;
   g2.N = nq;
   g2.K = w->r;
   g2.seg[0] = OutSeg{(_Float16*)q, nq, 0, nq};
@@ -346,8 +365,7 @@ qsvd_status qsvd_decode_project_append(const qsvd_layer* w, qsvd_cache* c, const
   g2.abits = act_bits;
   g2.cq = cq;
   g2.sc = sc;
-  SkinnyAppendArgs a2{c->data, c->scale, c->seq_len, c->overflow, c->capacity, f16c ? 3 : 2};
-  st = hip_status(launch_skinny_fused(g2, SKA_F16_LATENT, 1.f, w->r, w->w_bits, w->w_group, N, a2, s),
+  st = hip_status(launch_skinny_fused(g2, SKA_F16_LATENT, 1.f, w->r, w->w_bits, w->w_group, N, up_append(c), s),
                   "decode up-projection");
   if (st == QSVD_OK) c->max_len += 1;
   return st;

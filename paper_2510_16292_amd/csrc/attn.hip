@@ -114,6 +114,57 @@ __device__ __forceinline__ float rows4_sum(float x) {
 constexpr int kAbsorbJ = 64;
 constexpr int kAbsorbLd = kAbsorbJ + 16;   // stride 40 dwords = 8 (mod 32): conflict-free transpose reads
 
+// NT 16 x 16 tiles of q~ (16 query rows x 16 latent columns, at columns
+// col0 + 16 jj of the staged codes wk: row c = key channel, stride ld halves,
+// ld = 8 mod 32 dwords).  a[k]: this lane's query channels 32 k + 8 quad + e
+// of row l16; sc4[k][hh]: the weight scales of those channels.  For every
+// 32-channel step the scaled query q_c * s_c enters as an fp16 pair hi + lo
+// (the product of two fp16 MFMAs then carries it to about fp32 accuracy); the
+// MFMA needs 8 consecutive c of one column per lane, which two LDS transpose
+// reads deliver (lane s of each 16-lane group addresses row base + s/4 at
+// columns 4*(s%4)..+3 and receives 4 rows of one column).
+template <int NT>
+__device__ __forceinline__ void absorb_tiles(const f16x8* a, const f32x4 (*sc4)[2], int dh, const _Float16* wk,
+                                             int ld, int col0, int lane, f32x4* acc) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const int s16 = lane & 15, quad = lane >> 4;
+#pragma unroll
+  for (int jj = 0; jj < NT; ++jj) acc[jj] = f32x4{};
+#pragma unroll
+  for (int k = 0; k < 128 / 32; ++k) {
+    const int c0 = 32 * k;
+    if (c0 >= dh) break;
+    f16x8 ahi, alo;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float x = (float)a[k][e] * sc4[k][e >> 2][e & 3];
+      ahi[e] = to_f16(x);        // x rounded to fp32 first (no fused single rounding)
+      alo[e] = to_f16(x - (float)ahi[e]);
+    }
+#pragma unroll
+    for (int jj = 0; jj < NT; ++jj) {
+      const int row = c0 + 8 * quad + (s16 >> 2);
+      const int col = col0 + jj * 16 + 4 * (s16 & 3);
+      const s16x4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)&wk[row * ld + col]);
+      const s16x4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)&wk[(row + 4) * ld + col]);
+      const f16x4 f0 = __builtin_bit_cast(f16x4, x0), f1 = __builtin_bit_cast(f16x4, x1);
+      const f16x8 bw = {f0[0], f0[1], f0[2], f0[3], f1[0], f1[1], f1[2], f1[3]};
+      acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ahi, bw, acc[jj], 0, 0, 0);
+      acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(alo, bw, acc[jj], 0, 0, 0);
+    }
+  }
+}
+
+// int8 codes (16 per i32x4, element e in byte e) -> two fp16 x 8 (exact)
+__device__ __forceinline__ void codes16_to_f16(const uint32_t* wv, f16x8& lo, f16x8& hi) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    lo[k] = (_Float16)(float)(int8_t)(wv[k >> 2] >> (8 * (k & 3)));
+    hi[k] = (_Float16)(float)(int8_t)(wv[2 + (k >> 2)] >> (8 * (k & 3)));
+  }
+}
+
 __global__ void __launch_bounds__(64)
 absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, const float* __restrict__ sb,
               int32_t B, int32_t r, int32_t Hq, int32_t Hkv, int32_t dh, int32_t N, int32_t bits,
@@ -177,11 +228,7 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
     f16x8 lo, hi;
     if (bits == 8) {
       const uint32_t wv[4] = {raw[it].x, raw[it].y, raw[it].z, raw[it].w};
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        lo[k] = (_Float16)(float)(int8_t)(wv[k >> 2] >> (8 * (k & 3)));
-        hi[k] = (_Float16)(float)(int8_t)(wv[2 + (k >> 2)] >> (8 * (k & 3)));
-      }
+      codes16_to_f16(wv, lo, hi);
     } else {
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
@@ -193,49 +240,24 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
     *reinterpret_cast<f16x8*>(&wk[c * kAbsorbLd + j16 + 8]) = hi;
   }
   __syncthreads();
-  const int s16 = lane & 15;
-  typedef short s16x4 __attribute__((ext_vector_type(4)));
-  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
   for (int b0 = 0; b0 < B; b0 += 16) {
     const int bA = b0 + l16;
     const _Float16* qrow = q + (int64_t)min(bA, B - 1) * Hq * dh + h * dh + 8 * quad;
-    f32x4 acc[kAbsorbJ / 16];
-#pragma unroll
-    for (int jj = 0; jj < kAbsorbJ / 16; ++jj) acc[jj] = f32x4{};
+    f16x8 a[KC];
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
-      const int c0 = 32 * k;
-      if (c0 >= dh) break;
-      f16x8 a = b0 == 0 ? qa[k] : *reinterpret_cast<const f16x8*>(qrow + c0);
-      if (bA >= B) a = f16x8{};
-      // scaled query q_c * s_c as an fp16 pair hi + lo (the product of two
-      // fp16 MFMAs then carries it to about fp32 accuracy)
-      f16x8 ahi, alo;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x = (float)a[e] * sc4[k][e >> 2][e & 3];
-        ahi[e] = (_Float16)x;
-        alo[e] = (_Float16)(x - (float)ahi[e]);
-      }
-#pragma unroll
-      for (int jj = 0; jj < kAbsorbJ / 16; ++jj) {
-        const int row = c0 + 8 * quad + (s16 >> 2);
-        const int col = jj * 16 + 4 * (s16 & 3);
-        const s16x4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)&wk[row * kAbsorbLd + col]);
-        const s16x4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)&wk[(row + 4) * kAbsorbLd + col]);
-        const f16x4 f0 = __builtin_bit_cast(f16x4, x0), f1 = __builtin_bit_cast(f16x4, x1);
-        const f16x8 bw = {f0[0], f0[1], f0[2], f0[3], f1[0], f1[1], f1[2], f1[3]};
-        acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ahi, bw, acc[jj], 0, 0, 0);
-        acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(alo, bw, acc[jj], 0, 0, 0);
-      }
+      a[k] = 32 * k >= dh ? f16x8{} : b0 == 0 ? qa[k] : *reinterpret_cast<const f16x8*>(qrow + 32 * k);
+      if (bA >= B) a[k] = f16x8{};
     }
+    f32x4 acc[kAbsorbJ / 16];
+    absorb_tiles<kAbsorbJ / 16>(a, sc4, dh, wk, kAbsorbLd, 0, lane, acc);
     // lane holds column jb + 16*jj + l16 and sequences b0 + 4*quad + v; the
     // tile goes through LDS so that each sequence row leaves as 16-byte runs
 #pragma unroll
     for (int jj = 0; jj < kAbsorbJ / 16; ++jj)
 #pragma unroll
       for (int v = 0; v < 4; ++v)
-        ot[(4 * quad + v) * (kAbsorbJ + 8) + 16 * jj + l16] = (_Float16)(acc[jj][v] * scale);
+        ot[(4 * quad + v) * (kAbsorbJ + 8) + 16 * jj + l16] = to_f16(acc[jj][v] * scale);
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < 16 * kAbsorbJ / 8 / 64; ++i) {
@@ -1254,33 +1276,52 @@ static hipError_t dispatch_latent_pre(const AbsorbPlan& p, const qsvd_cache& c, 
 static hipError_t merge_and_project(const AttnArgs& a, const AbsorbPlan& p, const _Float16* opart, const float* ml,
                                     _Float16* olat, hipStream_t s);
 
+// The absorbed form's workspace: q~, the chunk partials (O, then m and l), O_lat.
+struct AbsorbWs {
+  _Float16* qt;
+  _Float16* opart;
+  float* ml;
+  _Float16* olat;
+};
+static AbsorbWs carve_absorbed(const AbsorbPlan& p, void* ws) {
+  uint8_t* base = (uint8_t*)ws;
+  AbsorbWs o;
+  o.qt = (_Float16*)base;
+  base += align256(p.qt_bytes);
+  o.opart = (_Float16*)base;
+  base += align256(p.opart_bytes);
+  o.ml = (float*)base;
+  base += align256(p.ml_bytes);
+  o.olat = (_Float16*)base;
+  return o;
+}
+
+// Everything after q~: the latent attention over the chunks, the merge and W^u_v.
+static hipError_t absorbed_from_qt(const AttnArgs& a, const AbsorbPlan& p, const AbsorbWs& b, hipStream_t s) {
+  const qsvd_cache& c = *a.c;
+  hipError_t e = c.fmt == QSVD_CACHE_F16 ? dispatch_latent<QSVD_CACHE_F16>(p, c, a.q_len, b.qt, b.opart, b.ml, s)
+                 : c.fmt == QSVD_CACHE_I8 ? dispatch_latent<QSVD_CACHE_I8>(p, c, a.q_len, b.qt, b.opart, b.ml, s)
+                                          : dispatch_latent<QSVD_CACHE_I4>(p, c, a.q_len, b.qt, b.opart, b.ml, s);
+  if (e != hipSuccess) return e;
+  return merge_and_project(a, p, b.opart, b.ml, b.olat, s);
+}
+
 hipError_t launch_attn_absorbed(const AttnArgs& a, void* ws, hipStream_t s) {
   const qsvd_layer& w = *a.w;
   const qsvd_cache& c = *a.c;
   const AbsorbPlan p = plan_absorbed(w, c, a.q_len);
   const int32_t rows = c.batch * a.q_len;     // (sequence, query) rows, sequence-major
-  uint8_t* base = (uint8_t*)ws;
-  _Float16* qt = (_Float16*)base;
-  base += align256(p.qt_bytes);
-  _Float16* opart = (_Float16*)base;
-  base += align256(p.opart_bytes);
-  float* ml = (float*)base;
-  base += align256(p.ml_bytes);
-  _Float16* olat = (_Float16*)base;
+  const AbsorbWs b = carve_absorbed(p, ws);
   const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
   {
     KernelScope ks("absorb_q", s);
     QSVD_LAUNCH(ks, absorb_kernel, dim3(p.hp, w.r / kAbsorbJ), dim3(64), 0, s, a.q,
                        (const uint8_t*)w.b_t, w.s_b, rows, w.r, w.n_q_heads, w.n_kv_heads,
-                       w.head_dim, N, w.w_bits, w.w_group, a.sm_scale * kLog2e, p.hp, qt);
+                       w.head_dim, N, w.w_bits, w.w_group, a.sm_scale * kLog2e, p.hp, b.qt);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = c.fmt == QSVD_CACHE_F16 ? dispatch_latent<QSVD_CACHE_F16>(p, c, a.q_len, qt, opart, ml, s)
-      : c.fmt == QSVD_CACHE_I8  ? dispatch_latent<QSVD_CACHE_I8>(p, c, a.q_len, qt, opart, ml, s)
-                                : dispatch_latent<QSVD_CACHE_I4>(p, c, a.q_len, qt, opart, ml, s);
-  if (e != hipSuccess) return e;
-  return merge_and_project(a, p, opart, ml, olat, s);
+  return absorbed_from_qt(a, p, b, s);
 }
 
 // Merge the chunk partials into O_lat, then o = O_lat W^u_v.

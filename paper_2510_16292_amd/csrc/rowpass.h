@@ -1,0 +1,103 @@
+// Row pass of the decode-size kernels: per-token symmetric quantization
+// (Section 4) of up to 32 fp16 rows by every workgroup that needs them as an
+// integer A operand, with the latent cache append folded in.
+#pragma once
+#include "common.h"
+
+namespace qsvd {
+
+constexpr int kSkMaxRowChunks = 8;  // 8-element chunks per lane: K <= 8 * 64 * 8 = 4096
+
+// The latent cache append fused into the decode-size projections (one new
+// row per sequence, row m of the product being sequence m's):
+//   SK_APPEND_F16_ROW  down-projection: the fp16 C row also goes to the cache
+//                      row seq_len[m] (the epilogue stores each element twice)
+//   SK_APPEND_CODES    up-projection: the row's Q(C) codes and scale also go to
+//                      the cache row seq_len[m], then seq_len[m] advances
+//   SK_APPEND_ADVANCE  up-projection over an fp16 cache: seq_len[m] advances
+// A row at or past capacity is not written; seq_len stops at capacity and the
+// overflow flag (when given) is set.
+enum { SK_APPEND_NONE = 0, SK_APPEND_F16_ROW = 1, SK_APPEND_CODES = 2, SK_APPEND_ADVANCE = 3 };
+struct SkinnyAppend {
+  uint8_t* data;       // cache rows
+  float* scale;        // integer caches: per-row scales
+  int32_t* seq_len;
+  int32_t* overflow;   // optional
+  int32_t capacity;
+  int32_t mode;
+};
+
+// Quantize rows m = w, w + nw, ... < M of the fp16 rows `ch` (row stride lda,
+// K <= 4096 columns): wave w holds a row in registers (8-element chunks lane,
+// lane + 64, ...), takes its max |x| round the wave, and writes its codes to
+// LDS (qa, row stride qa_ld, one byte per code) and its scale to rsc[m].  The
+// owning workgroup of row m (blockIdx.x == m mod gridDim.x) also stores the
+// codes and scale to cq_out / sc_out (when given) and, for SK_APPEND_CODES,
+// to the cache row seq_len[m].  MAXCH bounds the chunks per lane (K <= 512 MAXCH).
+template <int MAXCH = kSkMaxRowChunks>
+__device__ __forceinline__ void sk_row_pass(const _Float16* __restrict__ ch, int64_t lda, float clip, int32_t M,
+                                            int32_t K, int32_t abits, int w, int nw, int lane, int8_t* qa,
+                                            int qa_ld, float* rsc, uint8_t* __restrict__ cq_out,
+                                            float* __restrict__ sc_out, const SkinnyAppend& ap) {
+  const float qm = (float)((1 << (abits - 1)) - 1);
+  const int nch = K / 8;
+  for (int m = w; m < M; m += nw) {
+    f16x8 v[MAXCH];
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) {
+      const int c = lane + 64 * i;
+      v[i] = c < nch ? *reinterpret_cast<const f16x8*>(ch + (int64_t)m * lda + 8 * c) : f16x8{};
+    }
+    u16x2 mb = u16x2{0, 0};
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) mb = absmax_f16x8(mb, v[i]);
+    const float a = mul_rn(clip, wave_max(absmax_value(mb)));
+    const float inv = a != 0.f ? div_rn(qm, a) : 0.f;
+    const float sc = a != 0.f ? div_rn(a, qm) : 1.f;
+    const bool own = (m % (int)gridDim.x) == (int)blockIdx.x;
+    // the cache row this sequence's codes also go to (integer caches)
+    const bool app = own && ap.mode == SK_APPEND_CODES;
+    const int32_t pos = app ? ap.seq_len[m] : 0;
+    const bool app_row = app && pos >= 0 && pos < ap.capacity;
+    uint8_t* crow = ap.data + ((int64_t)m * ap.capacity + (app_row ? pos : 0)) * (abits == 8 ? K : K / 2);
+    if (lane == 0) {
+      rsc[m] = sc;
+      if (own && sc_out) sc_out[m] = sc;
+      if (app_row) ap.scale[(int64_t)m * ap.capacity + pos] = sc;
+    }
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) {
+      const int c = lane + 64 * i;
+      if (c >= nch) continue;
+      uint32_t q[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) q[e] = code_bits((float)v[i][e], inv, qm);
+      const uint32_t lo = pack4_codes8(q[0], q[1], q[2], q[3]), hi = pack4_codes8(q[4], q[5], q[6], q[7]);
+      *reinterpret_cast<uint2*>(qa + m * qa_ld + 8 * c) = make_uint2(lo, hi);
+      if (own && (cq_out || app_row)) {
+        if (abits == 8) {
+          if (cq_out) *reinterpret_cast<uint2*>(cq_out + (int64_t)m * K + 8 * c) = make_uint2(lo, hi);
+          if (app_row) *reinterpret_cast<uint2*>(crow + 8 * c) = make_uint2(lo, hi);
+        } else {
+          const uint32_t p = pack8_codes4(q);
+          if (cq_out) *reinterpret_cast<uint32_t*>(cq_out + (int64_t)m * (K / 2) + 4 * c) = p;
+          if (app_row) *reinterpret_cast<uint32_t*>(crow + 4 * c) = p;
+        }
+      }
+    }
+  }
+}
+
+// After the row pass (and a barrier): the cache row of each sequence this
+// workgroup owns is complete, so its length advances (only the owning
+// workgroup reads or writes seq_len[m] here).
+__device__ __forceinline__ void sk_advance(const SkinnyAppend& ap, int32_t M, int tid) {
+  if ((ap.mode == SK_APPEND_CODES || ap.mode == SK_APPEND_ADVANCE) && tid < M &&
+      (tid % (int)gridDim.x) == (int)blockIdx.x) {
+    const int32_t base = ap.seq_len[tid];
+    if (base >= ap.capacity && ap.overflow) *ap.overflow = 1;
+    ap.seq_len[tid] = base >= ap.capacity ? ap.capacity : base + 1;
+  }
+}
+
+}  // namespace qsvd

@@ -26,6 +26,7 @@
 
 #include "common.h"
 #include "launch.h"
+#include "rowpass.h"
 
 namespace qsvd {
 
@@ -33,7 +34,6 @@ constexpr int kSkCols = 16;        // output columns of one 16x16x64 product
 constexpr int kSkMinGrid = 256;    // workgroups wanted: one per CU
 constexpr int kSkMaxWaves = 16;
 constexpr int kSkBatch = 4;        // 64-byte contraction steps loaded per batch
-constexpr int kSkMaxRowChunks = 8;  // fp16 row pass: K <= 8 * 64 * 8 = 4096
 constexpr int kSkMaxGroups = 64;   // scale groups along the contraction
 constexpr size_t kSkLdsLimit = 160 * 1024 - 5 * 1024;   // dynamic LDS beside the static scale arrays
 
@@ -82,25 +82,6 @@ __device__ __forceinline__ i32x4 unpack16_i4(uint2 p) {
 // decode down-projection, with the caller's clip), 8- or 4-bit codes.
 enum { SK_A_I8 = 0, SK_A_F16Q = 1 };
 
-// The latent cache append fused into the decode-size projections (one new
-// row per sequence, row m of the product being sequence m's):
-//   SK_APPEND_F16_ROW  down-projection: the fp16 C row also goes to the cache
-//                      row seq_len[m] (the epilogue stores each element twice)
-//   SK_APPEND_CODES    up-projection: the row's Q(C) codes and scale also go to
-//                      the cache row seq_len[m], then seq_len[m] advances
-//   SK_APPEND_ADVANCE  up-projection over an fp16 cache: seq_len[m] advances
-// A row at or past capacity is not written; seq_len stops at capacity and the
-// overflow flag (when given) is set.
-enum { SK_APPEND_NONE = 0, SK_APPEND_F16_ROW = 1, SK_APPEND_CODES = 2, SK_APPEND_ADVANCE = 3 };
-struct SkinnyAppend {
-  uint8_t* data;       // cache rows
-  float* scale;        // integer caches: per-row scales
-  int32_t* seq_len;
-  int32_t* overflow;   // optional
-  int32_t capacity;
-  int32_t mode;
-};
-
 // Contraction steps [s0, s1) of wave w: contiguous ranges, whole groups when the
 // weights carry per-group scales.
 __device__ __forceinline__ void sk_span(int w, int nw, int32_t K, int32_t group, int& s0, int& s1) {
@@ -136,7 +117,6 @@ skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, cons
   const bool ncol = l16 < cols && n < N;
   const int rbl = (M + 15) / 16;
   const int qa_ld = K + 16;
-  const float qm = (float)((1 << (abits - 1)) - 1);
 
   int s0, s1;
   sk_span(w, nw, K, group, s0, s1);
@@ -178,64 +158,10 @@ skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, cons
   load_b(s0);
 
   if (ASRC == SK_A_F16Q) {
-    // row pass: wave w takes rows w, w + nw, ...; the row sits in registers
-    // (8-element chunks lane, lane + 64, ...), its max goes round the wave.
-    const _Float16* ch = reinterpret_cast<const _Float16*>(a_src);
-    const int nch = K / 8;
-    for (int m = w; m < M; m += nw) {
-      f16x8 v[kSkMaxRowChunks];
-#pragma unroll
-      for (int i = 0; i < kSkMaxRowChunks; ++i) {
-        const int c = lane + 64 * i;
-        v[i] = c < nch ? *reinterpret_cast<const f16x8*>(ch + (int64_t)m * lda + 8 * c) : f16x8{};
-      }
-      u16x2 mb = u16x2{0, 0};
-#pragma unroll
-      for (int i = 0; i < kSkMaxRowChunks; ++i) mb = absmax_f16x8(mb, v[i]);
-      const float a = mul_rn(clip, wave_max(absmax_value(mb)));
-      const float inv = a != 0.f ? div_rn(qm, a) : 0.f;
-      const float sc = a != 0.f ? div_rn(a, qm) : 1.f;
-      const bool own = (m % (int)gridDim.x) == (int)blockIdx.x;
-      // the cache row this sequence's codes also go to (integer caches)
-      const bool app = own && ap.mode == SK_APPEND_CODES;
-      const int32_t pos = app ? ap.seq_len[m] : 0;
-      const bool app_row = app && pos >= 0 && pos < ap.capacity;
-      uint8_t* crow = ap.data + ((int64_t)m * ap.capacity + (app_row ? pos : 0)) * (abits == 8 ? K : K / 2);
-      if (lane == 0) {
-        rsc[m] = sc;
-        if (own && sc_out) sc_out[m] = sc;
-        if (app_row) ap.scale[(int64_t)m * ap.capacity + pos] = sc;
-      }
-#pragma unroll
-      for (int i = 0; i < kSkMaxRowChunks; ++i) {
-        const int c = lane + 64 * i;
-        if (c >= nch) continue;
-        uint32_t q[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) q[e] = code_bits((float)v[i][e], inv, qm);
-        const uint32_t lo = pack4_codes8(q[0], q[1], q[2], q[3]), hi = pack4_codes8(q[4], q[5], q[6], q[7]);
-        *reinterpret_cast<uint2*>(qa + m * qa_ld + 8 * c) = make_uint2(lo, hi);
-        if (own && (cq_out || app_row)) {
-          if (abits == 8) {
-            if (cq_out) *reinterpret_cast<uint2*>(cq_out + (int64_t)m * K + 8 * c) = make_uint2(lo, hi);
-            if (app_row) *reinterpret_cast<uint2*>(crow + 8 * c) = make_uint2(lo, hi);
-          } else {
-            const uint32_t p = pack8_codes4(q);
-            if (cq_out) *reinterpret_cast<uint32_t*>(cq_out + (int64_t)m * (K / 2) + 4 * c) = p;
-            if (app_row) *reinterpret_cast<uint32_t*>(crow + 4 * c) = p;
-          }
-        }
-      }
-    }
+    sk_row_pass(reinterpret_cast<const _Float16*>(a_src), lda, clip, M, K, abits, w, nw, lane, qa, qa_ld, rsc,
+                cq_out, sc_out, ap);
     __syncthreads();
-    // the cache row of each sequence this workgroup owns is complete: advance
-    // its length (only the owning workgroup reads or writes seq_len[m] here)
-    if ((ap.mode == SK_APPEND_CODES || ap.mode == SK_APPEND_ADVANCE) && tid < M &&
-        (tid % (int)gridDim.x) == (int)blockIdx.x) {
-      const int32_t base = ap.seq_len[tid];
-      if (base >= ap.capacity && ap.overflow) *ap.overflow = 1;
-      ap.seq_len[tid] = base >= ap.capacity ? ap.capacity : base + 1;
-    }
+    sk_advance(ap, M, tid);
   }
 
   // --- contraction over this wave's steps ------------------------------------
