@@ -158,11 +158,8 @@ __device__ __forceinline__ void absorb_tiles(const f16x8* a, const f32x4 (*sc4)[
 
 // int8 codes (16 per i32x4, element e in byte e) -> two fp16 x 8 (exact)
 __device__ __forceinline__ void codes16_to_f16(const uint32_t* wv, f16x8& lo, f16x8& hi) {
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    lo[k] = (_Float16)(float)(int8_t)(wv[k >> 2] >> (8 * (k & 3)));
-    hi[k] = (_Float16)(float)(int8_t)(wv[2 + (k >> 2)] >> (8 * (k & 3)));
-  }
+  lo = cvt_i8x8(wv[0], wv[1]);
+  hi = cvt_i8x8(wv[2], wv[3]);
 }
 
 __global__ void __launch_bounds__(64)
@@ -230,11 +227,8 @@ absorb_kernel(const _Float16* __restrict__ q, const uint8_t* __restrict__ bt, co
       const uint32_t wv[4] = {raw[it].x, raw[it].y, raw[it].z, raw[it].w};
       codes16_to_f16(wv, lo, hi);
     } else {
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        lo[k] = (_Float16)(float)(((int)(raw[it].x << (28 - 4 * k))) >> 28);
-        hi[k] = (_Float16)(float)(((int)(raw[it].y << (28 - 4 * k))) >> 28);
-      }
+      lo = cvt_i4x8(raw[it].x);
+      hi = cvt_i4x8(raw[it].y);
     }
     *reinterpret_cast<f16x8*>(&wk[c * kAbsorbLd + j16]) = lo;
     *reinterpret_cast<f16x8*>(&wk[c * kAbsorbLd + j16 + 8]) = hi;
@@ -1109,17 +1103,7 @@ vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt,
 #pragma unroll
       for (int k = 0; k < kVprojBatch; ++k) {
         if (st0 + k >= s_end) continue;
-        f16x8 bw;
-        if (bits == 8) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            bw[e] = (_Float16)(float)(int8_t)(raw[k].x >> (8 * e));
-            bw[4 + e] = (_Float16)(float)(int8_t)(raw[k].y >> (8 * e));
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) bw[e] = (_Float16)(float)(((int)(raw[k].x << (28 - 4 * e))) >> 28);
-        }
+        const f16x8 bw = bits == 8 ? cvt_i8x8(raw[k].x, raw[k].y) : cvt_i4x8(raw[k].x);
         const f16x8 av = bA < B ? a[k] : f16x8{};
         const f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bw, f32x4{}, 0, 0, 0);
         if (group) {

@@ -44,19 +44,13 @@ __device__ __forceinline__ _Float16 to_f16(float v) {
   return (_Float16)v;
 }
 
-// Symmetric code: clamp(rint(v), -qm, qm), rint ties to even.
-__device__ __forceinline__ int quant_code(float v, float qm) {
-  float t = __builtin_rintf(v);
-  t = fminf(fmaxf(t, -qm), qm);
-  return (int)t;
-}
-
-// The same code in four VALU operations, for the row quantizers: y = fl(x * inv)
-// (an FMA with a -0 addend rounds the exact product once, as the product alone
-// does, and keeps its sign), clamped to [-qm, qm], then rounded half to even to
-// an integer by adding 1.5 * 2^23 (for |y| <= 2^22 the sum holds that integer in
-// its low mantissa bits).  The low byte (nibble) of the returned word is the
-// two's-complement code; inv == 0 (an all-zero row) gives code 0.
+// Symmetric code clamp(rint(x * inv), -qm, qm) (rint ties to even) in four VALU
+// operations: y = fl(x * inv) (an FMA with a -0 addend rounds the exact product
+// once, as the product alone does, and keeps its sign), clamped to [-qm, qm],
+// then rounded half to even to an integer by adding 1.5 * 2^23 (for |y| <= 2^22
+// the sum holds that integer in its low mantissa bits).  The low byte (nibble)
+// of the returned word is the two's-complement code; inv == 0 (an all-zero
+// row) gives code 0.
 __device__ __forceinline__ uint32_t code_bits(float x, float inv, float qm) {
   const float y = __builtin_amdgcn_fmed3f(__builtin_fmaf(x, inv, -0.0f), -qm, qm);
   return __float_as_uint(add_rn(y, 12582912.0f));

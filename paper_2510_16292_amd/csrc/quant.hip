@@ -185,19 +185,14 @@ quantize_rotated_kernel(const _Float16* __restrict__ x, int64_t M, int32_t K, in
   for (int j = 0; j < kRotMaxChunks; ++j) {
     const int ch = tid + j * kRotThreads;
     if (ch >= nch) continue;
-    int q[8];
+    uint32_t q[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) q[e] = (a != 0.f) ? quant_code(mul_rn(y[j][e], inv), qm) : 0;
-    if (BITS == 8) {
-      const uint32_t lo = (q[0] & 0xff) | ((q[1] & 0xff) << 8) | ((q[2] & 0xff) << 16) | ((uint32_t)(q[3] & 0xff) << 24);
-      const uint32_t hi = (q[4] & 0xff) | ((q[5] & 0xff) << 8) | ((q[6] & 0xff) << 16) | ((uint32_t)(q[7] & 0xff) << 24);
-      *reinterpret_cast<uint2*>(xq + m * (int64_t)K + ch * 8) = make_uint2(lo, hi);
-    } else {
-      uint32_t pk = 0;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pk |= (uint32_t)(q[e] & 0xf) << (4 * e);
-      *reinterpret_cast<uint32_t*>(xq + m * (int64_t)(K / 2) + ch * 4) = pk;
-    }
+    for (int e = 0; e < 8; ++e) q[e] = code_bits(y[j][e], inv, qm);
+    if (BITS == 8)
+      *reinterpret_cast<uint2*>(xq + m * (int64_t)K + ch * 8) =
+          make_uint2(pack4_codes8(q[0], q[1], q[2], q[3]), pack4_codes8(q[4], q[5], q[6], q[7]));
+    else
+      *reinterpret_cast<uint32_t*>(xq + m * (int64_t)(K / 2) + ch * 4) = pack8_codes4(q);
   }
 }
 
@@ -286,22 +281,16 @@ quantize_rotated_w64_kernel(const _Float16* __restrict__ x, int64_t M, int64_t l
   if (lane == 0) sx[m] = sc;
 #pragma unroll
   for (int i = 0; i < kRw / 16; ++i) {
-    int q[16];
+    uint32_t q[16];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) q[e] = (a != 0.f) ? quant_code(mul_rn(z[16 * i + e], inv), qm) : 0;
-    if (BITS == 8) {
-      uint32_t w[4];
-#pragma unroll
-      for (int d = 0; d < 4; ++d)
-        w[d] = (q[4 * d] & 0xff) | ((q[4 * d + 1] & 0xff) << 8) | ((q[4 * d + 2] & 0xff) << 16) |
-               ((uint32_t)(q[4 * d + 3] & 0xff) << 24);
-      *reinterpret_cast<uint4*>(xq + m * (int64_t)K + kRw * lane + 16 * i) = make_uint4(w[0], w[1], w[2], w[3]);
-    } else {
-      uint32_t w[2] = {0u, 0u};
-#pragma unroll
-      for (int e = 0; e < 16; ++e) w[e >> 3] |= (uint32_t)(q[e] & 0xf) << (4 * (e & 7));
-      *reinterpret_cast<uint2*>(xq + m * (int64_t)(K / 2) + (kRw * lane + 16 * i) / 2) = make_uint2(w[0], w[1]);
-    }
+    for (int e = 0; e < 16; ++e) q[e] = code_bits(z[16 * i + e], inv, qm);
+    if (BITS == 8)
+      *reinterpret_cast<uint4*>(xq + m * (int64_t)K + kRw * lane + 16 * i) =
+          make_uint4(pack4_codes8(q[0], q[1], q[2], q[3]), pack4_codes8(q[4], q[5], q[6], q[7]),
+                     pack4_codes8(q[8], q[9], q[10], q[11]), pack4_codes8(q[12], q[13], q[14], q[15]));
+    else
+      *reinterpret_cast<uint2*>(xq + m * (int64_t)(K / 2) + (kRw * lane + 16 * i) / 2) =
+          make_uint2(pack8_codes4(q), pack8_codes4(q + 8));
   }
 }
 
