@@ -41,6 +41,7 @@ GEMM_TRAFFIC_SUMMARY = "gemm_i8_llava7b_prefill_traffic.txt"
 GQA_TRAFFIC_SUMMARY = "latent_attn_qwen2vl_gqa_decode_traffic.txt"
 STACK_TRAFFIC_SUMMARY = "latent_attn_h16_13b_stack_decode_traffic.txt"
 STACK_GEMM_TRAFFIC_SUMMARY = "gemm_q4_13b_stack_prefill_traffic.txt"
+FLASH_TRAFFIC_SUMMARY = "prefill_flash_llava7b_traffic.txt"
 CPU_SAMPLE_S = 8.0           # seconds of oracle work per headline CPU baseline sample
 
 
@@ -510,12 +511,15 @@ def bench_prefill(args, wl2, host_layer):
     torch.cuda.synchronize()
     abs_s = (time.perf_counter() - a0) / 3
     del dc, wsa_t, oa
+    # HBM bytes of one launch on the 4 x 640 prompt, from the committed counter summary
+    flash_traffic = counted_traffic(FLASH_TRAFFIC_SUMMARY) if lengths == [640] * 4 else None
     attention = {"value": round(att_flops / att_s / 1e12, 1), "unit": "TFLOP/s", "us": round(att_s * 1e6, 2),
                  "gflop": round(att_flops / 1e9, 2), "lengths": lengths,
                  "absorbed_form_us": round(abs_s * 1e6, 1),
                  "roofline": {"bound": "mfma", "achieved": round(att_flops / att_s / 1e12, 1),
                               "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                              "frac": round(att_flops / att_s / 1e12 / F16_PEAK_TFLOPS, 4), "traffic": None,
+                              "frac": round(att_flops / att_s / 1e12 / F16_PEAK_TFLOPS, 4),
+                              "traffic": None if flash_traffic is None else int(flash_traffic),
                               "kernel": "prefill_flash_kernel (fp16, 4 dh flop per causal pair and head)"}}
     # HBM bytes of one call's two products (both launches), from the committed counter summary
     traffic = counted_traffic(GEMM_TRAFFIC_SUMMARY) if (M, d, r, L.N) == (2560, 4096, 1536, 12288) else None
