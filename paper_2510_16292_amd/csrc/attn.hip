@@ -291,10 +291,11 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
                    const float* __restrict__ pre, _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
   constexpr int KS = RW / 16;    // 16-wide contraction steps of the score MFMA
   constexpr int RB = RW / 32;    // 32-row blocks of the output MFMA
-  // Staged row stride in halves: RW + 16 makes the stride 8 (mod 32) dwords, so
-  // the 16 lanes of a transpose read (4 rows x 4 chunks of 8 bytes) hit
-  // distinct banks.
-  constexpr int CST = RW + 16;
+  // Staged row stride in halves: RW + 40 makes it an odd multiple of 4 dwords
+  // (mod 64), so the 16-byte row accesses of 16 consecutive rows fall on
+  // distinct groups of gfx950's 64 LDS banks (RW + 16, a multiple of 8, left
+  // them two-way conflicted: 1.39 conflict cycles per active LDS cycle, now 0.35).
+  constexpr int CST = RW + 40;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
@@ -637,7 +638,7 @@ struct H16Depth {
 template <int UMAX>
 constexpr size_t h16_lds_bytes() {
   constexpr int NB = H16Blocks<UMAX>::value;
-  return (size_t)kH16Waves * 16 * NB * (128 * UMAX + 16) * 2 + (size_t)(kH16Waves + 1) * NB * 64 * 16;
+  return (size_t)kH16Waves * 16 * NB * (128 * UMAX + 24) * 2 + (size_t)(kH16Waves + 1) * NB * 64 * 16;
 }
 
 // One wave's pass over the chunk [t_begin, t_end) for a wave owning U units
@@ -657,7 +658,10 @@ __device__ __forceinline__ void h16_wave(const _Float16* __restrict__ qrow, cons
   constexpr int RB = 8 * U;                              // 16-row blocks of the output product
   constexpr int NLD = F16C ? KS : (I4C ? U : KS / 2);    // 16-byte loads per token block
   constexpr int NLDA = NLD > 0 ? NLD : 1, KSA = KS > 0 ? KS : 1, RBA = RB > 0 ? RB : 1;
-  constexpr int CST = 128 * UMAX + 16;                   // staged row stride in halves: 8 (mod 64) dwords
+  // staged row stride in halves: 12 (mod 64) dwords, so the 16-byte row
+  // writes of 16 consecutive rows and the transposing reads (4 rows x 8
+  // dwords) fall on distinct banks of the 64
+  constexpr int CST = 128 * UMAX + 24;
   const int l16 = lane & 15, g = lane >> 4;
   // contraction slots of the score product: in step ks, lane group g feeds
   // latent columns slice0 + kcol(ks, g) .. +7 of token t0 + 16 bb + l16
@@ -840,7 +844,7 @@ latent_attn_h16_kernel(const _Float16* __restrict__ qt, const uint8_t* __restric
                        int32_t capacity, int32_t r, int32_t hp, int32_t chunk, int32_t n_chunks,
                        int32_t q_len, _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
   constexpr int NW = kH16Waves, NB = H16Blocks<UMAX>::value;
-  constexpr int CST = 128 * UMAX + 16;
+  constexpr int CST = 128 * UMAX + 24;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wu = __builtin_amdgcn_readfirstlane(w);     // wave-uniform copy: scalar branches below
@@ -1209,7 +1213,7 @@ size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c, int32_t
 template <int RW, int NW, int FMT, bool PRE = false>
 static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, int32_t q_len, const _Float16* qt,
                                 _Float16* opart, float* ml, hipStream_t s, const float* pre = nullptr) {
-  const size_t lds = (size_t)NW * 32 * (RW + 16) * 2 + (PRE ? 0 : (size_t)(NW + 1) * 1024 * 4);
+  const size_t lds = (size_t)NW * 32 * (RW + 40) * 2 + (PRE ? 0 : (size_t)(NW + 1) * 1024 * 4);
   auto kern = latent_attn_kernel<RW, NW, FMT, PRE>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
