@@ -186,18 +186,31 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
       }
     }
     // softmax per query block; the scores become the probabilities in place
+    // (tiles wholly before this wave's first query and inside the sequence
+    // need no mask)
+    const bool full = kt0 + kFaK - 1 <= qw0 && kt0 + kFaK <= n;
     float p[kFaQB][4][4];
 #pragma unroll
     for (int qb = 0; qb < kFaQB; ++qb) {
       float mx = -INFINITY;
+      if (full) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int vv = 0; vv < 4; ++vv) {
-          const int key = kt0 + 16 * kb + 4 * g + vv;
-          p[qb][kb][vv] = (key <= my_q[qb] && key < n) ? sacc[qb][kb][vv] * scale_log2 : -INFINITY;
-          mx = fmaxf(mx, p[qb][kb][vv]);
-        }
+          for (int vv = 0; vv < 4; ++vv) {
+            p[qb][kb][vv] = sacc[qb][kb][vv] * scale_log2;
+            mx = fmaxf(mx, p[qb][kb][vv]);
+          }
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int vv = 0; vv < 4; ++vv) {
+            const int key = kt0 + 16 * kb + 4 * g + vv;
+            p[qb][kb][vv] = (key <= my_q[qb] && key < n) ? sacc[qb][kb][vv] * scale_log2 : -INFINITY;
+            mx = fmaxf(mx, p[qb][kb][vv]);
+          }
+      }
       const float m_new = fmaxf(m_run[qb], fa_rows4_max(mx));
       float alpha = 1.f, ps = 0.f;
       if (m_new == -INFINITY) {
