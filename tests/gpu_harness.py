@@ -131,12 +131,21 @@ def append(dc, c_h=None, cq=None, sc=None, n_new=1):
     B.check(B.qsvd_latent_cache_append(dc.c, B.ptr(c_h), B.ptr(cq), B.ptr(sc), n_new, B.stream_handle()))
 
 
-def close_enough(got, want, max_abs=2e-2, rel_l2=1e-2):
+def close_enough(got, want, max_abs=2e-2, rel_l2=5e-3):
+    """Floating-point outputs against the oracle: every element within
+    max_abs * (1 + |want|) -- max_abs itself on outputs of unit scale; the fp16
+    roundings of the attention path (the absorbed query, the chunk partials,
+    the merged latent output, the output) are relative, so on larger outputs
+    the bound grows with the value -- and the whole within relative L2 error
+    rel_l2.  Returns (ok, (max-abs error, relative L2, rms of want, max
+    scaled error))."""
     got = np.asarray(got, dtype=np.float64)
     want = np.asarray(want, dtype=np.float64)
     err = np.abs(got - want)
+    scaled = err / (1.0 + np.abs(want))
     rel = np.linalg.norm(got - want) / max(np.linalg.norm(want), 1e-30)
-    return err.max() <= max_abs and rel <= rel_l2, (float(err.max()), float(rel), float(np.sqrt(np.mean(want ** 2))))
+    return scaled.max() <= max_abs and rel <= rel_l2, (float(err.max()), float(rel), float(np.sqrt(np.mean(want ** 2))),
+                                                       float(scaled.max()))
 
 
 def prefill_attention(q_dev, k_dev, v_dev, lengths, n_q_heads, n_kv_heads, head_dim, max_seqlen=None, sm_scale=0.0):

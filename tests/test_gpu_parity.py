@@ -758,7 +758,8 @@ def test_decode_llava7b_width_ragged(llava, mode):
 def test_decode_llava7b_full_size_sampled(llava):
     """The decode workload at its full size (16 sequences x 4096 cached tokens,
     fp16 latent cache of width 1536) in the launch configuration the bench
-    times; two sequences are checked against the oracle in full."""
+    times; every sequence against the oracle's absorbed form (pinned equal to
+    the plain definition), two also against the plain definition."""
     wl, ol, dl = llava
     batch, L0, cap = 16, 4096, 4096 + 8
     rows = gen.latent_rows(wl, batch, cap)
@@ -772,20 +773,23 @@ def test_decode_llava7b_full_size_sampled(llava):
     out2 = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
     assert np.array_equal(out.view(np.uint16), out2.view(np.uint16)), "decode attention is not deterministic"
     assert np.all(np.isfinite(out.astype(np.float32)))
-    for b in (0, 11):
-        oc = O.LatentCache(O.CACHE_F16, 1, cap, wl.layer.r)
-        oc.append(0, rows[b, :L0])
-        ref = O.decode_step(ol, oc, xt[b:b + 1], 8)
-        ok, info = H.close_enough(out[b:b + 1], ref["out"])
-        H.say(f"  b={b} max-abs, rel-L2, rms = {info}")
-        assert ok, (b, info)
+    for b in range(batch):
+        for plain in ((False, True) if b in (0, 11) else (False,)):
+            oc = O.LatentCache(O.CACHE_F16, 1, cap, wl.layer.r)
+            oc.append(0, rows[b, :L0])
+            ref = O.decode_step(ol, oc, xt[b:b + 1], 8, reference=plain)
+            ok, info = H.close_enough(out[b:b + 1], ref["out"])
+            H.say(f"  b={b} plain={plain} max-abs, rel-L2, rms = {info}")
+            assert ok, (b, plain, info)
 
 
 def test_decode_qwen2vl_w4a8_int8_cache_full_size(qwen):
     """The Qwen2-VL-7B-shaped decode workload at full size: 32 sequences x 8192
     cached tokens in an int8 latent cache with per-token scales, W4A8 projection
-    of the new tokens, grouped-query absorbed attention; two sequences checked
-    against the oracle in full, all outputs finite, run twice bit-identically."""
+    of the new tokens, grouped-query absorbed attention; every sequence
+    checked against the oracle's absorbed form (pinned equal to the plain
+    definition), two also against the plain definition; all outputs finite,
+    run twice bit-identically."""
     wl, ol, dl = qwen
     L = wl.layer
     batch, L0 = wl.decode_batch, wl.decode_ctx
@@ -802,15 +806,16 @@ def test_decode_qwen2vl_w4a8_int8_cache_full_size(qwen):
     out2 = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
     assert np.array_equal(out.view(np.uint16), out2.view(np.uint16))
     assert np.all(np.isfinite(out.astype(np.float32)))
-    for b in (0, 29):
-        oc = O.LatentCache(O.CACHE_I8, 1, cap, L.r)
-        oc.append(0, None, codes[b, :L0], scales[b, :L0])
-        ref = O.decode_step(ol, oc, xt[b:b + 1], 8)
-        assert np.array_equal(H.host(p.cq)[b:b + 1], ref["cq"])
-        assert np.array_equal(H.host(p.q)[b:b + 1].view(np.uint16), ref["Q"].view(np.uint16))
-        ok, info = H.close_enough(out[b:b + 1], ref["out"])
-        H.say(f"  b={b} max-abs, rel-L2, rms = {info}")
-        assert ok, (b, info)
+    for b in range(batch):
+        for plain in ((False, True) if b in (0, 29) else (False,)):
+            oc = O.LatentCache(O.CACHE_I8, 1, cap, L.r)
+            oc.append(0, None, codes[b, :L0], scales[b, :L0])
+            ref = O.decode_step(ol, oc, xt[b:b + 1], 8, reference=plain)
+            assert np.array_equal(H.host(p.cq)[b:b + 1], ref["cq"])
+            assert np.array_equal(H.host(p.q)[b:b + 1].view(np.uint16), ref["Q"].view(np.uint16))
+            ok, info = H.close_enough(out[b:b + 1], ref["out"])
+            H.say(f"  b={b} plain={plain} max-abs, rel-L2, rms = {info}")
+            assert ok, (b, plain, info)
 
 
 # ------------------------------------------------------------------ 13B-shaped stack layer at full size
@@ -851,8 +856,8 @@ def test_decode_13b_int4_cache_full_size_sampled(stack13b):
     """The stack's decode at full size for its widest layer: batch 8 over 4096
     cached tokens in an int4 latent cache (r = 3072, three 128-column units per
     wave), W4A4 projection of the new tokens, 40 query heads in 16-head blocks;
-    two sequences checked against the oracle's latent form, all outputs finite,
-    run twice bit-identically."""
+    every sequence checked against the oracle's latent form (pinned equal to
+    the plain definition), all outputs finite, run twice bit-identically."""
     wl, L, ol, dl = stack13b
     torch = H.torch()
     batch, L0 = wl.decode_batch, wl.decode_ctx
@@ -864,8 +869,7 @@ def test_decode_13b_int4_cache_full_size_sampled(stack13b):
     for b in range(batch):
         codes, sc = O.quantize_act(rows[b], 4)
         data[b, :L0], scale[b, :L0] = O.pack_int4(codes), sc
-        if b in (0, 5):
-            codes_of[b] = codes
+        codes_of[b] = codes
     dc = B.DeviceCache(B.QSVD_CACHE_I4, batch, cap, L.r, [L0] * batch)
     dc.data.copy_(H.dev(data))
     dc.scale.copy_(H.dev(scale))
@@ -880,7 +884,7 @@ def test_decode_13b_int4_cache_full_size_sampled(stack13b):
     out2 = H.host(H.decode_attention(dl, dc, p.q, B.QSVD_ATTN_AUTO))
     assert np.array_equal(out.view(np.uint16), out2.view(np.uint16))
     assert np.all(np.isfinite(out.astype(np.float32)))
-    for b in (0, 5):
+    for b in range(batch):
         ref = O.prefill(ol, xt[b:b + 1], 4)
         assert np.array_equal(H.host(p.q)[b:b + 1].view(np.uint16), ref["Q"].view(np.uint16))
         q4, s4 = O.quantize_act(ref["C_h"], 4)
