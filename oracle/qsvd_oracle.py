@@ -584,7 +584,8 @@ def attention_absorbed(layer: Layer, cache: LatentCache, q: np.ndarray, q_len: i
 
 
 def prefill_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, lengths: List[int], n_q_heads: int,
-                      n_kv_heads: int, head_dim: int, sm_scale: float = None) -> np.ndarray:
+                      n_kv_heads: int, head_dim: int, sm_scale: float = None,
+                      rope_theta: float = None) -> np.ndarray:
     """Causal self-attention of a prefill block over its own projections.
 
     In prefill every token of the prompt has its keys and values at hand: the
@@ -593,7 +594,9 @@ def prefill_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, lengths: List
     to tokens 0..i of the same sequence.  Q [M, Hq*dh], K and V [M, Hkv*dh]
     are token-major with the sequences back to back (`lengths`); query head h
     reads key/value head floor(h * Hkv / Hq); softmax scale 1/sqrt(dh) unless
-    given; fp64 throughout.  Returns fp64 [M, Hq*dh]."""
+    given; fp64 throughout.  With rope_theta, the Q and K rows of a sequence
+    are first rotated (:func:`rope`) at their positions 0..n-1 within it, as
+    the decode form does over the cache.  Returns fp64 [M, Hq*dh]."""
     dh = head_dim
     sm = 1.0 / np.sqrt(dh) if not sm_scale else sm_scale
     Q = np.asarray(Q, dtype=np.float64)
@@ -604,10 +607,14 @@ def prefill_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, lengths: List
     for n in lengths:
         if n == 0:                                      # an empty sequence has no query rows
             continue
+        Qs, Ks = Q[t0:t0 + n], K[t0:t0 + n]
+        if rope_theta:
+            Qs = rope(Qs, np.arange(n), rope_theta, dh)
+            Ks = rope(Ks, np.arange(n), rope_theta, dh)
         for h in range(n_q_heads):
             g = kv_group(h, n_q_heads, n_kv_heads)
-            qh = Q[t0:t0 + n, h * dh:(h + 1) * dh]
-            kh = K[t0:t0 + n, g * dh:(g + 1) * dh]
+            qh = Qs[:, h * dh:(h + 1) * dh]
+            kh = Ks[:, g * dh:(g + 1) * dh]
             vh = V[t0:t0 + n, g * dh:(g + 1) * dh]
             s = (qh @ kh.T) * sm
             s[np.triu_indices(n, 1)] = -np.inf          # query i sees keys 0..i

@@ -841,6 +841,60 @@ def check_rope():
     assert np.max(np.abs(plain - got)) > 1e-3
 
 
+def check_prefill_attention_rope():
+    """Rotary prefill attention: every query row of a sequence equals the
+    (separately pinned) rotary latent-cache attention of that query over the
+    cache truncated at its position, with the cache rows at positions 0..i; a
+    sequence gives the same rows alone as next to others; zero queries still
+    give the running mean of V (V is not rotated); rotation changes the result;
+    and with a single token it is the identity on V."""
+    g = np.random.default_rng(19)
+    theta = 500.0
+    for hq, hkv in ((4, 4), (6, 2)):
+        dh, d = 8, 40
+        N = (hq + 2 * hkv) * dh
+        W = g.standard_normal((d, N)) * 0.4
+        A, B = O.factors_from_weight(W, min(d, N), 0.5)
+        lengths = [10, 0, 6]
+        X = g.standard_normal((sum(lengths), d))
+        Y = X @ A @ B
+        Q, K, V = Y[:, :hq * dh], Y[:, hq * dh:(hq + hkv) * dh], Y[:, (hq + hkv) * dh:]
+        got = O.prefill_attention(Q, K, V, lengths, hq, hkv, dh, rope_theta=theta)
+        layer = _ExactLayer(d, A.shape[1], hq, hkv, dh, 8, 0, None, None, None, None, A, B)
+        t0 = 0
+        for n in lengths:
+            for i in range(n):
+                C_rows = X[t0:t0 + i + 1] @ A
+                want = O.attention_reference(layer, _ExactCache([C_rows]), Q[None, t0 + i:t0 + i + 1], q_len=1,
+                                             rope_theta=theta)[0, 0]
+                assert np.allclose(got[t0 + i], want, rtol=1e-9, atol=1e-12), (hq, hkv, n, i)
+            t0 += n
+        # the last sequence alone: the same rows (positions restart at 0 per sequence)
+        alone = O.prefill_attention(Q[10:], K[10:], V[10:], [6], hq, hkv, dh, rope_theta=theta)
+        assert np.allclose(alone, got[10:], rtol=1e-13, atol=1e-15)
+        plain = O.prefill_attention(Q, K, V, lengths, hq, hkv, dh)
+        assert np.max(np.abs(plain - got)) > 1e-3
+        # a single token attends only to itself: its value row, rotated or not
+        one = O.prefill_attention(Q[:1], K[:1], V[:1], [1], hq, hkv, dh, rope_theta=theta)
+        for h in range(hq):
+            gg = h // (hq // hkv)
+            assert np.allclose(one[0, h * dh:(h + 1) * dh], V[0, gg * dh:(gg + 1) * dh], rtol=1e-13, atol=1e-15)
+    hq, hkv, dh = 4, 2, 8
+    lengths = [7, 5]
+    M = sum(lengths)
+    K = g.standard_normal((M, hkv * dh))
+    V = g.standard_normal((M, hkv * dh))
+    out = O.prefill_attention(np.zeros((M, hq * dh)), K, V, lengths, hq, hkv, dh, rope_theta=theta)
+    t0 = 0
+    for n in lengths:
+        for i in range(n):
+            for h in range(hq):
+                gg = h // (hq // hkv)
+                want = V[t0:t0 + i + 1, gg * dh:(gg + 1) * dh].mean(axis=0)
+                assert np.allclose(out[t0 + i, h * dh:(h + 1) * dh], want, rtol=1e-12, atol=1e-14)
+        t0 += n
+
+
 # ---------------------------------------------------------------- P12-P13: cost model
 
 def check_cost_model():

@@ -192,6 +192,44 @@ def _prefill_attention_strict(Q, K, V, lengths, hq, hkv, dh, sm_scale=None):   #
     return out
 
 
+def _per_sequence_rope(x, lengths, theta, dh, reverse=False):
+    out = np.array(x, dtype=np.float64)
+    t0 = 0
+    for n in lengths:
+        pos = np.arange(n)[::-1] if reverse else np.arange(n)
+        out[t0:t0 + n] = _rope_freq_ok(out[t0:t0 + n], pos, theta, dh)
+        t0 += n
+    return out
+
+
+def _prefill_rope_rotates_v(Q, K, V, lengths, hq, hkv, dh, sm_scale=None, rope_theta=None):   # V turned too
+    if rope_theta:
+        V = _per_sequence_rope(V, lengths, rope_theta, dh)
+    return _good_prefill_attention(Q, K, V, lengths, hq, hkv, dh, sm_scale, rope_theta)
+
+
+def _prefill_rope_q_only(Q, K, V, lengths, hq, hkv, dh, sm_scale=None, rope_theta=None):   # keys left unturned
+    if rope_theta:
+        Q = _per_sequence_rope(Q, lengths, rope_theta, dh)
+    return _good_prefill_attention(Q, K, V, lengths, hq, hkv, dh, sm_scale)
+
+
+def _prefill_rope_reversed(Q, K, V, lengths, hq, hkv, dh, sm_scale=None, rope_theta=None):   # positions n-1..0
+    if rope_theta:
+        Q = _per_sequence_rope(Q, lengths, rope_theta, dh, reverse=True)
+        K = _per_sequence_rope(K, lengths, rope_theta, dh, reverse=True)
+    return _good_prefill_attention(Q, K, V, lengths, hq, hkv, dh, sm_scale)
+
+
+def _prefill_rope_global_positions_reversed(Q, K, V, lengths, hq, hkv, dh, sm_scale=None, rope_theta=None):
+    # positions counted over the whole block, last token first (only a constant
+    # shift of all positions would leave the scores unchanged)
+    if rope_theta:
+        Q = _per_sequence_rope(Q, [sum(lengths)], rope_theta, dh, reverse=True)
+        K = _per_sequence_rope(K, [sum(lengths)], rope_theta, dh, reverse=True)
+    return _good_prefill_attention(Q, K, V, lengths, hq, hkv, dh, sm_scale)
+
+
 def _snapshot_views(cache):                                  # no copy: later appends change it
     snap = dict(data=cache.data, seq_len=cache.seq_len)
     if cache.scale is not None:
@@ -224,6 +262,10 @@ MUTATIONS = [
     ("prefill_attention", _prefill_attention_one_sequence, [C.check_prefill_attention]),
     ("prefill_attention", _prefill_attention_strict, [C.check_prefill_attention]),
     ("kv_group", _kv_group_modulo, [C.check_prefill_attention]),
+    ("prefill_attention", _prefill_rope_rotates_v, [C.check_prefill_attention_rope]),
+    ("prefill_attention", _prefill_rope_q_only, [C.check_prefill_attention_rope]),
+    ("prefill_attention", _prefill_rope_reversed, [C.check_prefill_attention_rope]),
+    ("prefill_attention", _prefill_rope_global_positions_reversed, [C.check_prefill_attention_rope]),
     ("cache_snapshot", _snapshot_views, [C.check_cache_snapshot_resume]),
 ]
 

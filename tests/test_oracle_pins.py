@@ -31,6 +31,7 @@ PINS = [
     C.check_beta_objective_value,
     C.check_beta_search,
     C.check_rope,
+    C.check_prefill_attention_rope,
 ]
 
 
