@@ -513,6 +513,7 @@ def bench_prefill(args, wl2, host_layer):
     lengths = [M // wl2.prefill_batch] * wl2.prefill_batch
     att_s = time_prefill_attention(q, k, v, lengths, L.n_q_heads, L.n_kv_heads, L.head_dim, 20)
     att_flops = causal_flops(lengths, L.n_q_heads, L.head_dim)
+    rope_s = time_prefill_attention(q, k, v, lengths, L.n_q_heads, L.n_kv_heads, L.head_dim, 20, rope_theta=10000.0)
     dc = B.DeviceCache(B.QSVD_CACHE_F16, len(lengths), lengths[0], r, [0] * len(lengths))
     B.check(B.qsvd_latent_cache_append(dc.c, P(c_h), 0, 0, lengths[0], s))
     wsa = B.qsvd_decode_workspace_size(dl.c, dc.c, lengths[0], B.QSVD_ATTN_ABSORBED)
@@ -533,6 +534,8 @@ def bench_prefill(args, wl2, host_layer):
     attention = {"value": round(att_flops / att_s / 1e12, 1), "unit": "TFLOP/s", "us": round(att_s * 1e6, 2),
                  "gflop": round(att_flops / 1e9, 2), "lengths": lengths,
                  "absorbed_form_us": round(abs_s * 1e6, 1),
+                 "rotary": {"us": round(rope_s * 1e6, 2), "TFLOP/s": round(att_flops / rope_s / 1e12, 1),
+                            "rope_theta": 10000.0, "kernel": "prefill_flash_kernel, q and k turned in the kernel"},
                  "roofline": {"bound": "mfma", "achieved": round(att_flops / att_s / 1e12, 1),
                               "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                               "frac": round(att_flops / att_s / 1e12 / F16_PEAK_TFLOPS, 4),
@@ -560,10 +563,11 @@ def causal_flops(lengths, n_q_heads, head_dim):
     return float(sum(n * (n + 1) // 2 for n in lengths)) * n_q_heads * 4.0 * head_dim
 
 
-def time_prefill_attention(q, k, v, lengths, n_q_heads, n_kv_heads, head_dim, reps):
-    """Mean time (s) per causal prefill attention launch over the given rows,
-    launches back to back (graph replay), rotating through PREFILL_SETS copies
-    of q, k, v so that the last-level cache holds no launch's inputs."""
+def time_prefill_attention(q, k, v, lengths, n_q_heads, n_kv_heads, head_dim, reps, rope_theta=None):
+    """Mean time (s) per causal prefill attention launch over the given rows
+    (rotary with rope_theta), launches back to back (graph replay), rotating
+    through PREFILL_SETS copies of q, k, v so that the last-level cache holds
+    no launch's inputs."""
     import torch
 
     from paper_2510_16292_amd import binding as B
@@ -575,8 +579,13 @@ def time_prefill_attention(q, k, v, lengths, n_q_heads, n_kv_heads, head_dim, re
     def call(st):
         qq, kk, vv = sets[nxt[0] % PREFILL_SETS]
         nxt[0] += 1
-        B.check(B.qsvd_prefill_attention(B.ptr(qq), B.ptr(kk), B.ptr(vv), len(lengths), B.ptr(cu), max(lengths),
-                                         n_q_heads, n_kv_heads, head_dim, 0.0, B.ptr(out), st))
+        if rope_theta:
+            B.check(B.qsvd_prefill_attention_rope(B.ptr(qq), B.ptr(kk), B.ptr(vv), len(lengths), B.ptr(cu),
+                                                  max(lengths), n_q_heads, n_kv_heads, head_dim, 0.0, rope_theta,
+                                                  B.ptr(out), st))
+        else:
+            B.check(B.qsvd_prefill_attention(B.ptr(qq), B.ptr(kk), B.ptr(vv), len(lengths), B.ptr(cu), max(lengths),
+                                             n_q_heads, n_kv_heads, head_dim, 0.0, B.ptr(out), st))
     reps = max(reps // PREFILL_SETS, 1) * PREFILL_SETS
     t = replay_seconds(call, reps)
     del sets
@@ -648,9 +657,12 @@ def bench_stack_prefill(args, wl5, ranks, layers):
     tops = ops / proj_s / 1e12
     lengths = [M // wl5.prefill_batch] * wl5.prefill_batch
     att_s = time_prefill_attention(q, k, v, lengths, L.n_q_heads, L.n_kv_heads, L.head_dim, 40)
+    rope_s = time_prefill_attention(q, k, v, lengths, L.n_q_heads, L.n_kv_heads, L.head_dim, 40, rope_theta=10000.0)
     att_flops = causal_flops(lengths, L.n_q_heads, L.head_dim)
     attention = {"value": round(att_flops / att_s / 1e12, 1), "unit": "TFLOP/s", "us_per_layer": round(att_s * 1e6, 2),
                  "gflop_per_layer": round(att_flops / 1e9, 2), "lengths": lengths,
+                 "rotary": {"us_per_layer": round(rope_s * 1e6, 2), "TFLOP/s": round(att_flops / rope_s / 1e12, 1),
+                            "rope_theta": 10000.0},
                  "roofline": {"bound": "mfma", "achieved": round(att_flops / att_s / 1e12, 1),
                               "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                               "frac": round(att_flops / att_s / 1e12 / F16_PEAK_TFLOPS, 4), "traffic": None,

@@ -219,6 +219,24 @@ qsvd_status qsvd_prefill_attention(const void* q, const void* k, const void* v, 
                                    int32_t n_kv_heads, int32_t head_dim, float sm_scale, void* out,
                                    void* stream);
 
+/* qsvd_prefill_attention for layers that apply a rotary position embedding
+ * to q and k (the paper's layers have none; the position-encoded variant of
+ * the same prefill step, with the same rotation as
+ * qsvd_latent_decode_attention_rope).  Before the product, row i of a
+ * sequence (its position within that sequence, counted from 0) has the pairs
+ * (j, j + head_dim/2), j < head_dim/2, of every query and key head vector
+ * turned by the angle i * rope_theta^(-2j/head_dim): the angle is formed in
+ * revolutions and reduced to [0, 1) in fp64, its sine and cosine taken in
+ * fp32, and the turned rows rounded to fp16 before the products.  Values are
+ * not turned.  A decode step that continues the sequence over its cache sees
+ * the same key positions.  Same arguments, requirements and errors as
+ * qsvd_prefill_attention; rope_theta must be finite and > 1
+ * (QSVD_ERR_INVALID_ARG otherwise). */
+qsvd_status qsvd_prefill_attention_rope(const void* q, const void* k, const void* v, int32_t batch,
+                                        const int32_t* cu_seqlens, int32_t max_seqlen, int32_t n_q_heads,
+                                        int32_t n_kv_heads, int32_t head_dim, float sm_scale, float rope_theta,
+                                        void* out, void* stream);
+
 /* Attention of the newest queries of every sequence over its cached latent
  * rows (Section 3.1; decoding is l = 1): keys and values are C W^u_k and
  * C W^u_v of the stored rows (dequantized), softmax(q K^T * sm_scale) V with an

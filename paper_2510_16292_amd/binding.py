@@ -20,6 +20,7 @@ QSVD_OUT_Q, QSVD_OUT_K, QSVD_OUT_V = 1, 2, 4
 EXPORTED = [
     "qsvd_quantize_act", "qsvd_quantize_act_rotated", "qsvd_lowrank_qkv_prefill", "qsvd_prefill_workspace_size",
     "qsvd_latent_cache_append", "qsvd_decode_project_append", "qsvd_prefill_attention",
+    "qsvd_prefill_attention_rope",
     "qsvd_latent_decode_attention",
     "qsvd_latent_decode_attention_rope",
     "qsvd_decode_workspace_size", "qsvd_latent_decode_attention_noalloc", "qsvd_noalloc_scratch_bytes",
@@ -72,6 +73,7 @@ def lib():
             "qsvd_latent_cache_append": (I32, [CP, P, P, P, I32, P]),
             "qsvd_decode_project_append": (I32, [LP, CP, P, I64, I32, F, P, P, P, P, P, P, P]),
             "qsvd_prefill_attention": (I32, [P, P, P, I32, P, I32, I32, I32, I32, F, P, P]),
+            "qsvd_prefill_attention_rope": (I32, [P, P, P, I32, P, I32, I32, I32, I32, F, F, P, P]),
             "qsvd_latent_decode_attention": (I32, [LP, CP, P, I32, I32, F, P, P, SZ, P]),
             "qsvd_latent_decode_attention_rope": (I32, [LP, CP, P, I32, I32, F, F, P, P, SZ, P]),
             "qsvd_decode_workspace_size": (SZ, [LP, CP, I32, I32]),
@@ -123,6 +125,12 @@ def qsvd_prefill_attention(q, k, v, batch, cu_seqlens, max_seqlen, n_q_heads, n_
                            stream):
     return lib().qsvd_prefill_attention(q, k, v, batch, cu_seqlens, max_seqlen, n_q_heads, n_kv_heads, head_dim,
                                         sm_scale, out, stream)
+
+
+def qsvd_prefill_attention_rope(q, k, v, batch, cu_seqlens, max_seqlen, n_q_heads, n_kv_heads, head_dim, sm_scale,
+                                rope_theta, out, stream):
+    return lib().qsvd_prefill_attention_rope(q, k, v, batch, cu_seqlens, max_seqlen, n_q_heads, n_kv_heads,
+                                             head_dim, sm_scale, rope_theta, out, stream)
 
 
 def qsvd_latent_decode_attention(layer, cache, q, q_len, mode, sm_scale, out, ws, ws_bytes, stream):

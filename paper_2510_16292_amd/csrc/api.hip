@@ -388,9 +388,10 @@ qsvd_status qsvd_latent_cache_append(qsvd_cache* c, const void* c_h, const void*
   return st;
 }
 
-qsvd_status qsvd_prefill_attention(const void* q, const void* k, const void* v, int32_t batch,
-                                   const int32_t* cu_seqlens, int32_t max_seqlen, int32_t n_q_heads,
-                                   int32_t n_kv_heads, int32_t head_dim, float sm_scale, void* out, void* stream) {
+static qsvd_status prefill_attention(const void* q, const void* k, const void* v, int32_t batch,
+                                     const int32_t* cu_seqlens, int32_t max_seqlen, int32_t n_q_heads,
+                                     int32_t n_kv_heads, int32_t head_dim, float sm_scale, float rope_theta, void* out,
+                                     void* stream) {
   if (batch < 0 || max_seqlen < 0) return fail(QSVD_ERR_INVALID_ARG, "batch and max_seqlen must be >= 0");
   if (n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0) return fail(QSVD_ERR_INVALID_ARG, "head sizes must be positive");
   if (n_q_heads % n_kv_heads)
@@ -405,8 +406,24 @@ qsvd_status qsvd_prefill_attention(const void* q, const void* k, const void* v, 
     return fail(QSVD_ERR_UNSUPPORTED, "batch * n_q_heads * ceil(max_seqlen / 128) exceeds the grid");
   PrefillAttnArgs a{(const _Float16*)q, (const _Float16*)k, (const _Float16*)v, cu_seqlens, batch, max_seqlen,
                     n_q_heads, n_kv_heads, head_dim, sm_scale > 0.f ? sm_scale : 1.f / sqrtf((float)head_dim),
-                    (_Float16*)out};
+                    (_Float16*)out, rope_theta};
   return hip_status(launch_prefill_attention(a, (hipStream_t)stream), "prefill attention");
+}
+
+qsvd_status qsvd_prefill_attention(const void* q, const void* k, const void* v, int32_t batch,
+                                   const int32_t* cu_seqlens, int32_t max_seqlen, int32_t n_q_heads,
+                                   int32_t n_kv_heads, int32_t head_dim, float sm_scale, void* out, void* stream) {
+  return prefill_attention(q, k, v, batch, cu_seqlens, max_seqlen, n_q_heads, n_kv_heads, head_dim, sm_scale, 0.f,
+                           out, stream);
+}
+
+qsvd_status qsvd_prefill_attention_rope(const void* q, const void* k, const void* v, int32_t batch,
+                                        const int32_t* cu_seqlens, int32_t max_seqlen, int32_t n_q_heads,
+                                        int32_t n_kv_heads, int32_t head_dim, float sm_scale, float rope_theta,
+                                        void* out, void* stream) {
+  if (!(rope_theta > 1.f) || isinf(rope_theta)) return fail(QSVD_ERR_INVALID_ARG, "rope_theta must be finite and > 1");
+  return prefill_attention(q, k, v, batch, cu_seqlens, max_seqlen, n_q_heads, n_kv_heads, head_dim, sm_scale,
+                           rope_theta, out, stream);
 }
 
 size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int32_t q_len, int32_t mode) {

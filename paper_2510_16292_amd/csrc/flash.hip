@@ -21,6 +21,14 @@
 // (16x16 products keep the accumulators small enough for two waves per SIMD.)
 // The query rows stay in registers for the whole kernel.  Keys past a query's
 // position, or past the sequence end, are masked.
+//
+// Rotary layers (ROPE): a query row is turned once, in registers, at its
+// position within the sequence; a key row is turned while its tile moves from
+// registers into LDS, at its own position (rotate-half pairs j, j + dh/2 by
+// the angle pos * theta^(-2j/dh)).  The angle is formed in revolutions in
+// fp64 and reduced to [0, 1) there, then sine and cosine come from the
+// hardware's revolution-based instructions in fp32; the turned rows are
+// rounded to fp16 for the matrix cores, like the unturned ones.
 #include <math.h>
 
 #include "common.h"
@@ -43,6 +51,7 @@ struct FaCfg {
   static constexpr size_t kK = (size_t)kFaK * KST * 2, kV = (size_t)kFaK * VST * 2;
   static constexpr size_t kOut = (size_t)kFaWaves * kFaQW * OST * 2;
   static constexpr size_t kLds = kK + kV > kOut ? kK + kV : kOut;
+  static constexpr size_t kLdsRope = kLds + (size_t)(DH / 2) * sizeof(double);   // + revolutions per position of each pair
   static constexpr int kChunks = kFaK * DH / 8;               // 16-byte runs per K (or V) tile
   static constexpr int kPerThread = kChunks / (kFaWaves * 64);
   static_assert(kChunks % (kFaWaves * 64) == 0, "whole runs per thread");
@@ -74,42 +83,90 @@ __device__ __forceinline__ float fa_rows4_sum(float x) {
   return __builtin_bit_cast(float, c) + __builtin_bit_cast(float, e);
 }
 
-// Key/value tile t of the rows this thread stages (rows past the sequence end
-// re-read its last row; they are masked).
+// Rotary staging of a key tile: thread tid turns the 8 pairs of run pc
+// (channels 8 pc .. +7 with their partners dh/2 further) of row tid / PR.
 template <int DH>
+struct FaRope {
+  static constexpr int PR = DH / 16;                     // pair runs per row
+  static constexpr int kActive = kFaK * PR;              // threads with a key row to turn
+  static_assert(kActive <= kFaWaves * 64, "one pair run per thread");
+  static constexpr int KR = FaCfg<DH>::kPerThread > 2 ? FaCfg<DH>::kPerThread : 2;   // key registers per thread
+};
+
+// Key/value tile t of the rows this thread stages (rows past the sequence end
+// re-read its last row; they are masked).  With ROPE the key registers hold
+// the two halves of one pair run instead.
+template <int DH, bool ROPE>
 __device__ __forceinline__ void fa_load_tile(const _Float16* __restrict__ k, const _Float16* __restrict__ v, int tok0,
                                              int n, int ldkv, int g, int t, int tid,
-                                             i32x4 (&kr)[FaCfg<DH>::kPerThread], i32x4 (&vr)[FaCfg<DH>::kPerThread]) {
+                                             i32x4 (&kr)[FaRope<DH>::KR], i32x4 (&vr)[FaCfg<DH>::kPerThread]) {
   constexpr int RUNS = DH / 8;
 #pragma unroll
   for (int i = 0; i < FaCfg<DH>::kPerThread; ++i) {
     const int e = tid + kFaWaves * 64 * i, row = e / RUNS, c8 = e - row * RUNS;
     const int key = min(t * kFaK + row, n - 1);
     const int64_t off = (int64_t)(tok0 + key) * ldkv + g * DH + 8 * c8;
-    kr[i] = *reinterpret_cast<const i32x4*>(k + off);
+    if (!ROPE) kr[i] = *reinterpret_cast<const i32x4*>(k + off);
     vr[i] = *reinterpret_cast<const i32x4*>(v + off);
+  }
+  if (ROPE && tid < FaRope<DH>::kActive) {
+    constexpr int PR = FaRope<DH>::PR;
+    const int row = tid / PR, pc = tid - row * PR;
+    const int key = min(t * kFaK + row, n - 1);
+    const _Float16* src = k + (int64_t)(tok0 + key) * ldkv + g * DH + 8 * pc;
+    kr[0] = *reinterpret_cast<const i32x4*>(src);
+    kr[1] = *reinterpret_cast<const i32x4*>(src + DH / 2);
   }
 }
 
-// ... and its copy into the LDS tiles.
-template <int DH>
-__device__ __forceinline__ void fa_store_tile(_Float16* ks, _Float16* vs, int tid,
-                                              const i32x4 (&kr)[FaCfg<DH>::kPerThread],
+// Turn the rotate-half pairs (a[e], b[e]) of channels j0 + e by the angle
+// pos * theta^(-2j/dh): freq[j] holds theta^(-2j/dh) / (2 pi), so the angle
+// in revolutions is formed and reduced to [0, 1) in fp64 before the fp32
+// sine and cosine.
+__device__ __forceinline__ void fa_rope8(f16x8& a, f16x8& b, int pos, const double* freq) {
+  f16x8 ra, rb;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    double rev = (double)pos * freq[e];
+    rev -= floor(rev);
+    const float x = (float)rev;
+    const float c = __builtin_amdgcn_cosf(x), sn = __builtin_amdgcn_sinf(x);
+    const float fa = (float)a[e], fb = (float)b[e];
+    ra[e] = (_Float16)(fa * c - fb * sn);
+    rb[e] = (_Float16)(fb * c + fa * sn);
+  }
+  a = ra;
+  b = rb;
+}
+
+// ... and its copy into the LDS tiles (turning the keys of a rotary layer at
+// positions t * 64 + row).
+template <int DH, bool ROPE>
+__device__ __forceinline__ void fa_store_tile(_Float16* ks, _Float16* vs, int tid, int t, const double* freq,
+                                              const i32x4 (&kr)[FaRope<DH>::KR],
                                               const i32x4 (&vr)[FaCfg<DH>::kPerThread]) {
   constexpr int RUNS = DH / 8;
 #pragma unroll
   for (int i = 0; i < FaCfg<DH>::kPerThread; ++i) {
     const int e = tid + kFaWaves * 64 * i, row = e / RUNS, c8 = e - row * RUNS;
-    *reinterpret_cast<i32x4*>(ks + row * FaCfg<DH>::KST + 8 * c8) = kr[i];
+    if (!ROPE) *reinterpret_cast<i32x4*>(ks + row * FaCfg<DH>::KST + 8 * c8) = kr[i];
     *reinterpret_cast<i32x4*>(vs + row * FaCfg<DH>::VST + 8 * c8) = vr[i];
+  }
+  if (ROPE && tid < FaRope<DH>::kActive) {
+    constexpr int PR = FaRope<DH>::PR;
+    const int row = tid / PR, pc = tid - row * PR;
+    f16x8 a = __builtin_bit_cast(f16x8, kr[0]), b = __builtin_bit_cast(f16x8, kr[1]);
+    fa_rope8(a, b, t * kFaK + row, freq + 8 * pc);
+    *reinterpret_cast<f16x8*>(ks + row * FaCfg<DH>::KST + 8 * pc) = a;
+    *reinterpret_cast<f16x8*>(ks + row * FaCfg<DH>::KST + 8 * pc + DH / 2) = b;
   }
 }
 
-template <int DH>
+template <int DH, bool ROPE>
 __global__ void __launch_bounds__(kFaWaves * 64, 2)
 prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k, const _Float16* __restrict__ v,
                      const int32_t* __restrict__ cu, int32_t n_seq, int32_t Hq, int32_t Hkv, int32_t n_qt,
-                     float scale_log2, _Float16* __restrict__ out) {
+                     float scale_log2, double log2_theta, _Float16* __restrict__ out) {
   using C = FaCfg<DH>;
   constexpr int KS = DH / 32;      // contraction steps of the score product
   constexpr int OB = DH / 16;      // 16-channel blocks of the output
@@ -132,6 +189,11 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
   const int tok0 = cu[b], n = cu[b + 1] - tok0;
   const int q0 = qt * kFaQ;
   if (q0 >= n) return;
+  double* freq = reinterpret_cast<double*>(fa_smem + C::kLds);
+  if (ROPE) {
+    if (tid < DH / 2) freq[tid] = exp2(-2.0 * tid / DH * log2_theta) * 0.15915494309189533576888376337251;
+    __syncthreads();
+  }
   const int g_kv = (h * Hkv) / Hq;
   const int ldq = Hq * DH, ldkv = Hkv * DH;
   const int kend = min(n, q0 + kFaQ);              // keys this tile of queries can see
@@ -148,9 +210,14 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
     const _Float16* qrow = q + (int64_t)(tok0 + min(my_q[qb], n - 1)) * ldq + h * DH + 8 * g;
 #pragma unroll
     for (int s = 0; s < KS; ++s) qf[qb][s] = *reinterpret_cast<const f16x8*>(qrow + 32 * s);
+    if (ROPE) {                                     // slot s pairs with slot s + KS/2 (channels dh/2 further)
+#pragma unroll
+      for (int s = 0; s < KS / 2; ++s)
+        fa_rope8(qf[qb][s], qf[qb][s + KS / 2], min(my_q[qb], n - 1), freq + 32 * s + 8 * g);
+    }
   }
 
-  i32x4 kr[C::kPerThread], vr[C::kPerThread];
+  i32x4 kr[FaRope<DH>::KR], vr[C::kPerThread];
   f32x4 o[kFaQB][OB];
   float m_run[kFaQB], l_run[kFaQB];
 #pragma unroll
@@ -163,12 +230,12 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
   typedef short s16x4 __attribute__((ext_vector_type(4)));
   typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-  fa_load_tile<DH>(k, v, tok0, n, ldkv, g_kv, 0, tid, kr, vr);
+  fa_load_tile<DH, ROPE>(k, v, tok0, n, ldkv, g_kv, 0, tid, kr, vr);
   for (int t = 0; t < n_tiles; ++t) {
     __syncthreads();                                // every wave is done with the previous tile
-    fa_store_tile<DH>(ks, vs, tid, kr, vr);
+    fa_store_tile<DH, ROPE>(ks, vs, tid, t, freq, kr, vr);
     __syncthreads();
-    if (t + 1 < n_tiles) fa_load_tile<DH>(k, v, tok0, n, ldkv, g_kv, t + 1, tid, kr, vr);
+    if (t + 1 < n_tiles) fa_load_tile<DH, ROPE>(k, v, tok0, n, ldkv, g_kv, t + 1, tid, kr, vr);
     const int kt0 = t * kFaK;
     if (kt0 > qw0 + kFaQW - 1) continue;            // every key of the tile is after this wave's queries
     // S^T: key block kb, lane (query l16 of block qb, group g) holds keys kt0 + 16 kb + 4 g + v
@@ -287,17 +354,18 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
   }
 }
 
-template <int DH>
+template <int DH, bool ROPE>
 static hipError_t launch_flash(const PrefillAttnArgs& a, hipStream_t s) {
   using C = FaCfg<DH>;
-  auto kern = prefill_flash_kernel<DH>;
-  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::kLds);
+  auto kern = prefill_flash_kernel<DH, ROPE>;
+  const size_t lds = ROPE ? C::kLdsRope : C::kLds;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const int n_qt = (a.max_seqlen + kFaQ - 1) / kFaQ;
   const int64_t blocks = (int64_t)a.batch * a.n_q_heads * n_qt;
-  KernelScope ks("prefill_flash", s);
-  QSVD_LAUNCH(ks, kern, dim3((unsigned)blocks), dim3(kFaWaves * 64), C::kLds, s, a.q, a.k, a.v, a.cu_seqlens, a.batch,
-              a.n_q_heads, a.n_kv_heads, n_qt, a.sm_scale * kFaLog2e, a.out);
+  KernelScope ks(ROPE ? "prefill_flash_rope" : "prefill_flash", s);
+  QSVD_LAUNCH(ks, kern, dim3((unsigned)blocks), dim3(kFaWaves * 64), lds, s, a.q, a.k, a.v, a.cu_seqlens, a.batch,
+              a.n_q_heads, a.n_kv_heads, n_qt, a.sm_scale * kFaLog2e, ROPE ? log2((double)a.rope_theta) : 0.0, a.out);
   return hipGetLastError();
 }
 
@@ -305,7 +373,8 @@ bool prefill_attention_supported(int32_t head_dim) { return head_dim == 64 || he
 
 hipError_t launch_prefill_attention(const PrefillAttnArgs& a, hipStream_t s) {
   if (a.batch == 0 || a.max_seqlen == 0) return hipSuccess;
-  return a.head_dim == 128 ? launch_flash<128>(a, s) : launch_flash<64>(a, s);
+  if (a.rope_theta > 0.f) return a.head_dim == 128 ? launch_flash<128, true>(a, s) : launch_flash<64, true>(a, s);
+  return a.head_dim == 128 ? launch_flash<128, false>(a, s) : launch_flash<64, false>(a, s);
 }
 
 }  // namespace qsvd

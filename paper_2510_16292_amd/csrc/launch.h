@@ -137,6 +137,7 @@ struct PrefillAttnArgs {
   int32_t batch, max_seqlen, n_q_heads, n_kv_heads, head_dim;
   float sm_scale;
   _Float16* out;            // [M][n_q_heads * head_dim]
+  float rope_theta;         // > 0: rotary layer (q and k turned at their positions)
 };
 bool prefill_attention_supported(int32_t head_dim);
 hipError_t launch_prefill_attention(const PrefillAttnArgs& a, hipStream_t s);

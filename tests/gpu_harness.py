@@ -148,15 +148,21 @@ def close_enough(got, want, max_abs=2e-2, rel_l2=5e-3):
                                                        float(scaled.max()))
 
 
-def prefill_attention(q_dev, k_dev, v_dev, lengths, n_q_heads, n_kv_heads, head_dim, max_seqlen=None, sm_scale=0.0):
+def prefill_attention(q_dev, k_dev, v_dev, lengths, n_q_heads, n_kv_heads, head_dim, max_seqlen=None, sm_scale=0.0,
+                      rope_theta=None):
     """Causal prefill attention of sequences back to back (lengths) over the
-    device Q, K, V rows; returns the device output."""
+    device Q, K, V rows (rotary with rope_theta); returns the device output."""
     t = torch()
     cu = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
     cu_d = dev(cu)
     out = t.empty_like(q_dev)
     ms = max(lengths) if max_seqlen is None else max_seqlen
-    B.check(B.qsvd_prefill_attention(B.ptr(q_dev), B.ptr(k_dev), B.ptr(v_dev), len(lengths), B.ptr(cu_d), ms,
-                                     n_q_heads, n_kv_heads, head_dim, sm_scale, B.ptr(out), B.stream_handle()))
+    if rope_theta:
+        B.check(B.qsvd_prefill_attention_rope(B.ptr(q_dev), B.ptr(k_dev), B.ptr(v_dev), len(lengths), B.ptr(cu_d), ms,
+                                              n_q_heads, n_kv_heads, head_dim, sm_scale, rope_theta, B.ptr(out),
+                                              B.stream_handle()))
+    else:
+        B.check(B.qsvd_prefill_attention(B.ptr(q_dev), B.ptr(k_dev), B.ptr(v_dev), len(lengths), B.ptr(cu_d), ms,
+                                         n_q_heads, n_kv_heads, head_dim, sm_scale, B.ptr(out), B.stream_handle()))
     t.cuda.synchronize()
     return out

@@ -217,6 +217,24 @@ def test_prefill_attention_validation(lib):
     assert call(out=FAKE + 8) == B.QSVD_ERR_UNSUPPORTED
 
 
+def test_prefill_attention_rope_validation(lib):
+    """The rotary prefill entry validates like the plain one, and refuses a
+    rotary base that is not finite and > 1, all before any GPU work."""
+    def call(q=FAKE, batch=2, ms=64, hq=4, hkv=2, dh=64, sm=0.0, theta=10000.0, out=FAKE):
+        return B.qsvd_prefill_attention_rope(q, FAKE, FAKE, batch, FAKE, ms, hq, hkv, dh, sm, theta, out, 0)
+    for theta in (0.0, 1.0, -5.0, float("inf"), float("nan")):
+        assert call(theta=theta) == B.QSVD_ERR_INVALID_ARG, theta
+        assert "rope_theta" in B.last_error()
+    assert call(batch=-1) == B.QSVD_ERR_INVALID_ARG
+    assert call(hq=6, hkv=4) == B.QSVD_ERR_INVALID_ARG
+    assert call(sm=float("inf")) == B.QSVD_ERR_INVALID_ARG
+    assert call(batch=0) == B.QSVD_OK
+    assert call(ms=0) == B.QSVD_OK
+    assert call(q=0) == B.QSVD_ERR_INVALID_ARG
+    assert call(dh=96) == B.QSVD_ERR_UNSUPPORTED
+    assert call(out=FAKE + 8) == B.QSVD_ERR_UNSUPPORTED
+
+
 def test_noalloc_decode_validation(lib):
     """The allocation-free decode attention validates like the workspace entry
     point and refuses a call whose scratch need exceeds the static array, all

@@ -574,6 +574,83 @@ def test_prefill_attention_flash_13b_two_sequences():
     assert ok, info
 
 
+# ------------------------------------------------------------------ f3 at q_len > 1: rotary prefill attention
+
+def test_prefill_attention_rope_tiny_end_to_end(tiny):
+    """Tiny layer (4 heads x 64): the projection's own Q, K, V through the
+    rotary prefill attention against the oracle; its last row also against
+    the oracle's rotary attention over the latent cache at that position,
+    which a decode step continuing the prompt computes."""
+    wl, ol, dl = tiny
+    X = gen.prefill_activations(wl)
+    ref = O.prefill(ol, X, 8)
+    L = wl.layer
+    H.say("prefill flash rope tiny")
+    p = H.Prefill(dl, 64, mask=7, debug=False).run(H.dev(X))
+    out = H.host(H.prefill_attention(p.q, p.k, p.v, [64], L.n_q_heads, L.n_kv_heads, L.head_dim, rope_theta=10000.0))
+    want = O.prefill_attention(ref["Q"], ref["K"], ref["V"], [64], L.n_q_heads, L.n_kv_heads, L.head_dim,
+                               rope_theta=10000.0)
+    ok, info = H.close_enough(out, want)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+    oc = O.LatentCache(O.CACHE_F16, 1, 64, L.r)
+    oc.append(0, ref["C_h"])
+    last = O.attention_reference(ol, oc, ref["Q"][None, -1:], 1, rope_theta=10000.0)[0, 0]
+    assert np.abs(out[-1].astype(np.float64) - last).max() <= 2e-2
+    plain = O.prefill_attention(ref["Q"], ref["K"], ref["V"], [64], L.n_q_heads, L.n_kv_heads, L.head_dim)
+    assert not H.close_enough(out, plain)[0]
+
+
+@pytest.mark.parametrize("shape,lengths,theta", [
+    ((8, 2, 64), [1, 45, 130], 10000.0),          # grouped, ragged: one row, a partial tile, two query tiles
+    ((4, 4, 128), [0, 200, 129, 1], 10000.0),     # an empty sequence, tile edges at 128 + 1
+    ((28, 4, 128), [640, 300], 1e6),              # Qwen2-VL-shaped grouping, its rotary base
+    ((8, 2, 128), [3000], 10000.0),               # positions up to 2999: thousands of turns per pair 0
+], ids=["gqa8-2-dh64", "mha4-dh128-empty", "qwen28-4", "long3000"])
+def test_prefill_attention_rope_ragged(shape, lengths, theta):
+    """Rotary prefill attention over seeded Q, K, V rows against the oracle,
+    over ragged lengths, grouped heads, two rotary bases and long positions."""
+    hq, hkv, dh = shape
+    M = sum(lengths)
+    Q, K, V = _qkv(340 + hq, M, hq, hkv, dh)
+    H.say(f"prefill flash rope heads={hq}/{hkv} dh={dh} lengths={lengths} theta={theta}")
+    out = H.host(H.prefill_attention(H.dev(Q), H.dev(K), H.dev(V), lengths, hq, hkv, dh, rope_theta=theta))
+    want = O.prefill_attention(Q, K, V, lengths, hq, hkv, dh, rope_theta=theta)
+    ok, info = H.close_enough(out, want)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+
+
+def test_prefill_attention_rope_llava7b_full():
+    """The LLaVA-1.5-7B-shaped prompt batch at full size (4 x 640 tokens,
+    32 heads x 128, rotary base 10000) in the bench's launch configuration,
+    every output row against the oracle, run twice bit-identically."""
+    hq, hkv, dh = 32, 32, 128
+    Q, K, V = _qkv(710, 2560, hq, hkv, dh)
+    qd, kd, vd = H.dev(Q), H.dev(K), H.dev(V)
+    H.say("prefill flash rope llava7b 4 x 640")
+    out = H.host(H.prefill_attention(qd, kd, vd, [640] * 4, hq, hkv, dh, rope_theta=10000.0))
+    want = O.prefill_attention(Q, K, V, [640] * 4, hq, hkv, dh, rope_theta=10000.0)
+    ok, info = H.close_enough(out, want)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+    again = H.host(H.prefill_attention(qd, kd, vd, [640] * 4, hq, hkv, dh, rope_theta=10000.0))
+    assert np.array_equal(again.view(np.uint16), out.view(np.uint16))
+
+
+def test_prefill_attention_rope_13b_two_sequences():
+    """The 40-head 13B-shaped prompt (704 tokens per sequence) with rotary
+    embeddings on two of the batch's eight sequences, against the oracle."""
+    hq, hkv, dh = 40, 40, 128
+    Q, K, V = _qkv(810, 1408, hq, hkv, dh, scale=2.0)
+    H.say("prefill flash rope 13b two sequences")
+    out = H.host(H.prefill_attention(H.dev(Q), H.dev(K), H.dev(V), [704, 704], hq, hkv, dh, rope_theta=10000.0))
+    want = O.prefill_attention(Q, K, V, [704, 704], hq, hkv, dh, rope_theta=10000.0)
+    ok, info = H.close_enough(out, want)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+
+
 def _layer_for(shape_id):
     """(layer shape, oracle layer, device layer, weight bits, group) of a decode projection case."""
     if shape_id == "tiny":
