@@ -256,7 +256,7 @@ qsvd_status qsvd_prefill_attention_rope(const void* q, const void* k, const void
  * r in {128, 512, 1024, 1536} (with at most 32 heads) or r a multiple of 128
  * up to 3072, any cache format, and batch * q_len * ceil(n_q_heads / 16)
  * <= 65535 (batch * q_len <= 65535 with 32-head blocks); the reconstruct
- * form takes n_q_heads <= 32, q_len 1, capacity <= 16384 and any cache
+ * form takes n_q_heads <= 64, q_len 1, capacity <= 16384 and any cache
  * format (F16 rows rebuild on the fp16 products, I8 on the int8 products,
  * I4 on the 4-bit products).
  * Launch grids are sized from the host c->max_len and every length is read
@@ -298,7 +298,7 @@ size_t qsvd_noalloc_scratch_bytes(void);
  *                          needs n_q_heads <= 32 and r in {128, 512, 1024, 1536}
  *                          (QSVD_ERR_UNSUPPORTED otherwise)
  *   QSVD_ATTN_RECONSTRUCT  K and V rebuilt, plain attention; needs
- *                          n_q_heads <= 32 and capacity <= 16384
+ *                          n_q_heads <= 64 and capacity <= 16384
  *   QSVD_ATTN_AUTO         the first where it applies, else the second
  * Both take q_len 1 only and any cache format (F16, I8, I4), and one workspace
  * size serves both: qsvd_decode_workspace_size(w, c, 1, QSVD_ATTN_RECONSTRUCT)

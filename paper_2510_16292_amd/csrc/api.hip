@@ -502,7 +502,6 @@ static qsvd_status decode_attention(const qsvd_layer* w, const qsvd_cache* c, co
   if (absorbed && absorbed_grid_rows(*w, *c, q_len) > kMaxQueryRows)
     return fail(QSVD_ERR_UNSUPPORTED, "batch * q_len * head blocks must be at most %d", (int)kMaxQueryRows);
   if ((!absorbed || rope) && q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct-side forms take q_len 1 only");
-  if (!absorbed && w->n_q_heads > 32) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form takes at most 32 query heads");
   if (!absorbed && c->capacity > 16384)
     return fail(QSVD_ERR_UNSUPPORTED, "reconstruct form supports capacity <= 16384");
   const size_t need = absorbed && !rope ? attn_absorbed_workspace(*w, *c, q_len) : attn_reconstruct_workspace(*w, *c);

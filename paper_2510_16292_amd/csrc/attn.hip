@@ -990,23 +990,23 @@ merge_latent_kernel(const _Float16* __restrict__ o_part, const float* __restrict
 
 // ---------------------------------------------------------------------------
 // Merge the chunk partials of a sequence.  Chunk c holds m_c, l_c and the
-// normalized O_c / l_c as fp16 [x][32 heads]; with m = max m_c and
-// w_c = 2^(m_c - m) l_c, the result is sum_c w_c (O_c / l_c) / sum_c w_c.
-// The per-head weights are computed once per workgroup into LDS; each thread
-// then streams 8 heads of one row x with 16-byte loads.  Output is fp16,
-// head-major: [b][32][width] (latent form) or the final [b][Hq*width].
+// normalized O_c / l_c of a block of 32 heads as fp16 [x][32 heads]; with
+// m = max m_c and w_c = 2^(m_c - m) l_c, the result is
+// sum_c w_c (O_c / l_c) / sum_c w_c.  One workgroup per (64 rows x, sequence,
+// head block): the per-head weights are computed once into LDS; each thread
+// then streams 8 heads of one row x with 16-byte loads.  Output is the final
+// fp16 [b][Hq*width], head-major.
 // ---------------------------------------------------------------------------
-template <bool FINAL>
 __global__ void __launch_bounds__(256)
 combine_kernel(const _Float16* __restrict__ o_part, const float* __restrict__ ml_part,
                const int32_t* __restrict__ seq_len, int32_t chunk, int32_t n_chunks, int32_t n_launched,
-               int32_t width, int32_t Hq, _Float16* __restrict__ out) {
+               int32_t width, int32_t Hq, int32_t n_hb, _Float16* __restrict__ out) {
   __shared__ float wgt[kMaxChunks * 32];
   __shared__ float tile[64][33];
-  const int b = blockIdx.y, x0 = blockIdx.x * 64, tid = threadIdx.x;
+  const int b = blockIdx.y / n_hb, hb = blockIdx.y - b * n_hb, x0 = blockIdx.x * 64, tid = threadIdx.x;
   const int L = seq_len[b];
   const int nv = L > 0 ? min(min((L + chunk - 1) / chunk, n_launched), kMaxChunks) : 0;
-  const int64_t pb = (int64_t)b * n_chunks;
+  const int64_t pb = ((int64_t)b * n_hb + hb) * n_chunks;
   if (tid < 32) {
     float m = -INFINITY;
     for (int c = 0; c < nv; ++c) m = fmaxf(m, ml_part[(pb + c) * 64 + tid]);
@@ -1044,17 +1044,12 @@ combine_kernel(const _Float16* __restrict__ o_part, const float* __restrict__ ml
 #pragma unroll
   for (int e = 0; e < 8; ++e) tile[xl][h0 + e] = acc[e];
   __syncthreads();
-  // write head-major: thread -> head tid/8 (+32 per pass... 32 heads x 64 rows)
+  // write head-major: pass i covers heads 4 i .. 4 i + 3 of the block, 64 rows each
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const int e = tid + 256 * i, h = e >> 6, xl = e & 63, x = x0 + xl;
-    if (x >= width) continue;
-    const _Float16 v = (_Float16)tile[xl][h];
-    if (FINAL) {
-      if (h < Hq) out[((int64_t)b * Hq + h) * width + x] = v;
-    } else {
-      out[((int64_t)b * kHeadBlk + h) * width + x] = v;
-    }
+    const int hg = hb * kHeadBlk + h;
+    if (x < width && hg < Hq) out[((int64_t)b * Hq + hg) * width + x] = (_Float16)tile[xl][h];
   }
 }
 
@@ -1415,8 +1410,8 @@ __device__ __forceinline__ void rope_pair(float a, float b, float c, float s, fl
 // rows are staged in LDS with 16-byte loads (with rotary embeddings, each K^
 // pair (j, j + dh/2) is turned as it is staged, and the queries at position
 // seq_len - 1); scores, the softmax (one wave per head, a lane per token) and
-// P V^ read LDS.  Partials go out in the merge's layout: O/l as fp16
-// [chunk][x][32 heads], (m, l) per head.
+// P V^ read LDS.  Partials go out in the merge's layout: per block of 32
+// heads, O/l as fp16 [chunk][x][32 heads] and (m, l) per head.
 constexpr int RCH = 64;
 
 __host__ __device__ constexpr int recon_kld(int dh) { return dh + 8; }   // staged row stride (halves)
@@ -1429,7 +1424,7 @@ static size_t recon_attn_lds(int dh, int G) {
 __global__ void __launch_bounds__(256)
 recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ kv,
                   const int32_t* __restrict__ seq_len, int32_t capacity, int32_t Hq, int32_t Hkv,
-                  int32_t dh, float scale, int32_t n_chunks, const float2* __restrict__ rope,
+                  int32_t dh, float scale, int32_t n_chunks, int32_t n_hb, const float2* __restrict__ rope,
                   _Float16* __restrict__ o_part, float* __restrict__ ml_part) {
   extern __shared__ __attribute__((aligned(16))) uint8_t recon_smem[];
   const int b = blockIdx.y, ch = blockIdx.x, g = blockIdx.z, tid = threadIdx.x;
@@ -1534,25 +1529,30 @@ recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k
     }
   }
   __syncthreads();
-  const int64_t part = (int64_t)b * n_chunks + ch;
+  // partial rows of head h: block h / 32, column h % 32
+  auto part_of = [&](int h) { return ((int64_t)b * n_hb + h / kHeadBlk) * n_chunks + ch; };
   for (int hg = tid; hg < G; hg += 256) {
-    ml_part[part * 64 + h0 + hg] = red[hg];
-    ml_part[part * 64 + 32 + h0 + hg] = red[G + hg];
+    const int h = h0 + hg;
+    ml_part[part_of(h) * 64 + h % kHeadBlk] = red[hg];
+    ml_part[part_of(h) * 64 + 32 + h % kHeadBlk] = red[G + hg];
   }
   if (g == 0) {
-    // heads past Hq in the 32-wide partial rows: weight 0 in the merge
-    for (int h = Hq + tid; h < kHeadBlk; h += 256) {
-      ml_part[part * 64 + h] = 0.f;
-      ml_part[part * 64 + 32 + h] = 1.f;
+    // heads past Hq in the last block's partial rows: weight 0 in the merge
+    const int pad = n_hb * kHeadBlk - Hq;
+    for (int i = tid; i < pad; i += 256) {
+      const int h = Hq + i;
+      ml_part[part_of(h) * 64 + h % kHeadBlk] = 0.f;
+      ml_part[part_of(h) * 64 + 32 + h % kHeadBlk] = 1.f;
     }
-    for (int e = tid; e < dh * (kHeadBlk - Hq); e += 256) {
-      const int c = e / (kHeadBlk - Hq), h = Hq + e - c * (kHeadBlk - Hq);
-      o_part[(part * dh + c) * kHeadBlk + h] = (_Float16)0.f;
+    for (int e = tid; e < dh * pad; e += 256) {
+      const int c = e / pad, h = Hq + e - c * pad;
+      o_part[(part_of(h) * dh + c) * kHeadBlk + h % kHeadBlk] = (_Float16)0.f;
     }
   }
   // O^T[c][h] / l = sum_t p[h][t] V^[t][c] / l[h]: item (head hg, column pair c2)
   for (int e = tid; e < G * half; e += 256) {
     const int hg = e / half, c = 2 * (e - hg * half);
+    const int h = h0 + hg;
     const float* ph = ps + hg * RCH;
     float a0 = 0.f, a1 = 0.f;
     for (int tl = 0; tl < tn; ++tl) {
@@ -1561,8 +1561,8 @@ recon_attn_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k
       a1 = fmaf(ph[tl], (float)v2[1], a1);
     }
     const float il = 1.f / red[G + hg];
-    o_part[(part * dh + c) * kHeadBlk + h0 + hg] = (_Float16)(a0 * il);
-    o_part[(part * dh + c + 1) * kHeadBlk + h0 + hg] = (_Float16)(a1 * il);
+    o_part[(part_of(h) * dh + c) * kHeadBlk + h % kHeadBlk] = (_Float16)(a0 * il);
+    o_part[(part_of(h) * dh + c + 1) * kHeadBlk + h % kHeadBlk] = (_Float16)(a1 * il);
   }
 }
 
@@ -1724,7 +1724,7 @@ rope_scores_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ 
 
 struct ReconPlan {
   size_t kv_bytes, opart_bytes, ml_bytes, w16_bytes, rope_bytes;
-  int n_chunks;
+  int n_chunks, n_hb;       // context chunks of RCH tokens, blocks of 32 query heads
 };
 
 // (cos, sin) rows of the rotary table for every position a cache can hold.
@@ -1746,8 +1746,9 @@ static ReconPlan plan_recon(const qsvd_layer& w, const qsvd_cache& c) {
   const int nkv2 = 2 * w.n_kv_heads * w.head_dim;
   p.n_chunks = (c.capacity + RCH - 1) / RCH;
   p.kv_bytes = (size_t)c.batch * c.capacity * nkv2 * sizeof(_Float16);
-  p.opart_bytes = (size_t)c.batch * p.n_chunks * w.head_dim * kHeadBlk * sizeof(_Float16);
-  p.ml_bytes = (size_t)c.batch * p.n_chunks * 64 * sizeof(float);
+  p.n_hb = (w.n_q_heads + kHeadBlk - 1) / kHeadBlk;
+  p.opart_bytes = (size_t)c.batch * p.n_hb * p.n_chunks * w.head_dim * kHeadBlk * sizeof(_Float16);
+  p.ml_bytes = (size_t)c.batch * p.n_hb * p.n_chunks * 64 * sizeof(float);
   p.w16_bytes = c.fmt == QSVD_CACHE_F16 ? (size_t)nkv2 * w.r * sizeof(_Float16) : 0;
   p.rope_bytes = rope_table_bytes(w, c);
   return p;
@@ -1866,13 +1867,17 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
   {
     KernelScope ks("recon_attn", s);
     const size_t lds = recon_attn_lds(w.head_dim, G);
+    hipError_t ea = hipFuncSetAttribute((const void*)recon_attn_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                        (int)recon_attn_lds(128, kMaxAbsorbedHeads));
+    if (ea != hipSuccess) return ea;
     QSVD_LAUNCH(ks, recon_attn_kernel, dim3(nch, c.batch, w.n_kv_heads), dim3(256), lds, s, a.q, kv, c.seq_len,
-                c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, a.sm_scale * kLog2e, p.n_chunks, rope, opart, ml);
+                c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, a.sm_scale * kLog2e, p.n_chunks, p.n_hb, rope,
+                opart, ml);
   }
   {
     KernelScope ks("recon_combine", s);
-    QSVD_LAUNCH(ks, combine_kernel<true>, dim3((w.head_dim + 63) / 64, c.batch), dim3(256), 0, s, opart, ml,
-                       c.seq_len, RCH, p.n_chunks, nch, w.head_dim, w.n_q_heads, a.out);
+    QSVD_LAUNCH(ks, combine_kernel, dim3((w.head_dim + 63) / 64, c.batch * p.n_hb), dim3(256), 0, s, opart, ml,
+                c.seq_len, RCH, p.n_chunks, nch, w.head_dim, w.n_q_heads, p.n_hb, a.out);
   }
   return hipGetLastError();
 }

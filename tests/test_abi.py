@@ -269,11 +269,18 @@ def test_decode_validation(lib):
     assert _decode(L, cache_struct(r=256)) == B.QSVD_ERR_INVALID_ARG
     assert _decode(L, cache_struct(max_len=0)) == B.QSVD_ERR_INVALID_ARG
     assert _decode(layer_struct(n_q_heads=80, n_kv_heads=8, head_dim=64), C) == B.QSVD_ERR_UNSUPPORTED
-    # more than 32 query heads: absorbed form only (16-head blocks), r a multiple of 128
+    # more than 32 query heads: absorbed form with 16-head blocks (r a multiple
+    # of 128), or the reconstruct form with its partials in two 32-head blocks
     wide = layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64)
-    assert _decode(wide, C, mode=B.QSVD_ATTN_RECONSTRUCT) == B.QSVD_ERR_UNSUPPORTED
-    assert _decode(layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64, r=192), cache_struct(r=192)) == \
-        B.QSVD_ERR_UNSUPPORTED
+    need_w = B.qsvd_decode_workspace_size(wide, C, 1, B.QSVD_ATTN_RECONSTRUCT)
+    assert need_w > 0
+    assert _decode(wide, C, mode=B.QSVD_ATTN_RECONSTRUCT, ws_bytes=need_w - 1) == B.QSVD_ERR_WORKSPACE
+    # r 192 has no absorbed plan at 40 heads: AUTO takes the reconstruct form
+    w192, c192 = layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64, r=192), cache_struct(r=192)
+    assert _decode(w192, c192, mode=B.QSVD_ATTN_ABSORBED) == B.QSVD_ERR_UNSUPPORTED
+    need192 = B.qsvd_decode_workspace_size(w192, c192, 1, B.QSVD_ATTN_AUTO)
+    assert need192 == B.qsvd_decode_workspace_size(w192, c192, 1, B.QSVD_ATTN_RECONSTRUCT) > 0
+    assert _decode(w192, c192, ws_bytes=need192 - 1) == B.QSVD_ERR_WORKSPACE
     assert _decode(layer_struct(r=3200), cache_struct(r=3200), mode=B.QSVD_ATTN_ABSORBED) == B.QSVD_ERR_UNSUPPORTED
     # three head blocks x 64 sequences x 400 queries exceed the grid's rows
     big = cache_struct(batch=64, max_len=2000, capacity=4096)
@@ -319,7 +326,9 @@ def test_decode_rope_validation(lib):
         B.QSVD_ERR_UNSUPPORTED
     wide = layer_struct(n_q_heads=40, n_kv_heads=8, head_dim=64)
     assert _decode_rope(wide, C, mode=B.QSVD_ATTN_ABSORBED) == B.QSVD_ERR_UNSUPPORTED
-    assert _decode_rope(wide, C) == B.QSVD_ERR_UNSUPPORTED                  # AUTO -> full rebuild: <= 32 heads
+    need_w = B.qsvd_decode_workspace_size(wide, C, 1, B.QSVD_ATTN_RECONSTRUCT)
+    assert _decode_rope(wide, C, ws_bytes=need_w - 1) == B.QSVD_ERR_WORKSPACE   # AUTO -> full rebuild, 40 heads
+    assert _decode_rope(layer_struct(n_q_heads=80, n_kv_heads=8, head_dim=64), C) == B.QSVD_ERR_UNSUPPORTED
     for mode in (B.QSVD_ATTN_AUTO, B.QSVD_ATTN_ABSORBED, B.QSVD_ATTN_RECONSTRUCT):
         assert _decode_rope(L, C, q_len=2, mode=mode) == B.QSVD_ERR_UNSUPPORTED
     assert _decode_rope(L, cache_struct(capacity=20000), mode=B.QSVD_ATTN_RECONSTRUCT) == B.QSVD_ERR_UNSUPPORTED

@@ -1515,6 +1515,54 @@ def test_decode_rope_head_dims(shape, fmt):
         assert ok, (mode, info)
 
 
+@pytest.mark.parametrize("shape,r", [((40, 40, 128), 1024), ((40, 8, 64), 512), ((64, 64, 64), 512)],
+                         ids=["mha40_dh128", "g5_40_dh64", "mha64_dh64"])
+@pytest.mark.parametrize("fmt", [O.CACHE_F16, O.CACHE_I8, O.CACHE_I4], ids=["f16", "i8", "i4"])
+def test_decode_reconstruct_wide_heads(shape, r, fmt):
+    """More than 32 query heads in the full-rebuild form, whose partials go
+    out in blocks of 32 heads: 40 heads x 128 (the 13B-shaped layer's heads),
+    40 over 8 (a group of five straddles heads 30-34, across the blocks) and
+    the 64-head maximum; ragged lengths 3 / 130 / 257 of every cache format,
+    with rotary embeddings (AUTO also takes this form for them) and without,
+    against the oracle."""
+    Hq, Hkv, dh = shape
+    L = configs.LayerShape(d=512, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=dh, r=r)
+    ol, dl = _random_factor_layer(L, 1300 + Hq + Hkv + dh)
+    wl = configs.Workload(97, "wide-heads", L, "gaussian", 8, 0, 8, fmt)
+    oc, dc = _prefilled_caches(wl, fmt, [3, 130, 257], 264)
+    g = np.random.default_rng(Hq * 11 + Hkv + dh)
+    q = (g.standard_normal((3, Hq * dh)) * 4.0).astype(np.float16)
+    q_dev = H.dev(q)
+    for theta, mode in ((1.0e4, B.QSVD_ATTN_RECONSTRUCT), (1.0e4, B.QSVD_ATTN_AUTO), (None, B.QSVD_ATTN_RECONSTRUCT)):
+        H.say(f"decode wide heads Hq={Hq} Hkv={Hkv} dh={dh} r={r} fmt={fmt} theta={theta} mode={mode}")
+        ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, rope_theta=theta)[:, 0, :]
+        out = H.host(H.decode_attention(dl, dc, q_dev, mode, rope_theta=theta))
+        ok, info = H.close_enough(out, ref)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (theta, mode, info)
+
+
+def test_decode_rope_13b_shape_full_rebuild():
+    """The 13B-shaped layer at its size (40 heads x 128, r = 2048, int4
+    weights in groups of 128) over an int4 latent cache of 8 sequences with
+    the workload's prompt and decode lengths (704 tokens and more), rotary
+    embeddings (base 1e4) in the full-rebuild form, every sequence against
+    the oracle."""
+    L = configs.LayerShape(d=5120, n_q_heads=40, n_kv_heads=40, head_dim=128, r=2048)
+    ol, dl = _random_factor_layer(L, 1340, w_bits=4, w_group=128)
+    wl = configs.Workload(98, "13b-rope", L, "gaussian", 4, 128, 4, O.CACHE_I4)
+    lengths = [704, 705, 720, 740, 760, 800, 830, 832]
+    oc, dc = _prefilled_caches(wl, O.CACHE_I4, lengths, 832)
+    g = np.random.default_rng(5120)
+    q = (g.standard_normal((8, 40 * 128)) * 2.0).astype(np.float16)
+    H.say("decode rope 13b shape full rebuild")
+    ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, rope_theta=1.0e4)[:, 0, :]
+    out = H.host(H.decode_attention(dl, dc, H.dev(q), B.QSVD_ATTN_AUTO, rope_theta=1.0e4))
+    ok, info = H.close_enough(out, ref)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+
+
 @pytest.mark.parametrize("mode", ROPE_MODES, ids=ROPE_MODE_IDS)
 def test_decode_rope_empty_sequence(gqa, mode):
     """A sequence with nothing cached (length 0) beside ragged ones (33, 70):
