@@ -772,6 +772,24 @@ def bench_stack_decode(args, wl5, ranks, layers):
                            "traffic": None if traffic is None else int(traffic),
                            "kernel": "latent_attn_h16_kernel (int4 cache)", "launches": n,
                            "bytes_per_launch": int(attn_bytes / n)}
+    # the rotary variant of layer 0's attention (40 heads: the full-rebuild
+    # form, K and V rebuilt from the int4 cache and K turned per position),
+    # attention call alone over the final context, a few calls
+    reset(ctx0 + steps - 1)
+    rws_b = B.qsvd_decode_workspace_size(layers[0].c, caches[0].c, 1, B.QSVD_ATTN_RECONSTRUCT)
+    rws = torch.empty((rws_b,), dtype=torch.uint8, device="cuda")
+    rope_call = lambda: B.check(lib.qsvd_latent_decode_attention_rope(layers[0].c, caches[0].c, P(q), 1,
+                                                                      B.QSVD_ATTN_AUTO, 0.0, 1.0e4, P(out), P(rws),
+                                                                      rws_b, s))
+    rope_call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(3):
+        rope_call()
+    torch.cuda.synchronize()
+    res["rotary_attention_us"] = {"us": round((time.perf_counter() - t0) * 1e6 / 3, 1), "rope_theta": 1.0e4,
+                                  "form": "full rebuild (K, V from the int4 cache), 40 heads"}
+    del rws
     if args.no_graph:
         res.update(value=res["eager_tokens_per_s"], unit="tokens/s", ms_per_step=res["eager_ms_per_step"],
                    us_per_layer_step=round(eager_s * 1e6 / len(ranks), 2), timing="eager")
