@@ -304,6 +304,10 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   // 256 threads add the NW partials in wave order into ssum4 [v/4][lane].
   f32x4* spart4 = reinterpret_cast<f32x4*>(smem + NW * 32 * CST * 2);
   f32x4* ssum4 = spart4 + NW * 256;
+  // Integer rows: the per-token scales of the wave's tile, staged with it
+  // (each lane loads the scale of its own row, and reads back the 16 of the
+  // tokens whose scores it holds).
+  float* scl = reinterpret_cast<float*>(smem + NW * 32 * CST * 2 + (PRE ? 0 : (size_t)(NW + 1) * 1024 * 4)) + w * 32;
 
   // Workgroup row blockIdx.y is query i of sequence b (q_len queries per
   // sequence, the last q_len cached positions): it sees positions
@@ -335,17 +339,22 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   // (t0 + 8*(v/4) + 4*half + v%4).
   constexpr bool I4C = FMT == QSVD_CACHE_I4;
   constexpr int NLD = F16C ? KS : KS / 2;
+  // Staging the tile before the score product (and reissuing the loads
+  // first) measured faster for fp16 rows and keeps the widest integer
+  // slices from spilling; narrower integer slices convert in registers
+  // and feed the score product directly.
+  constexpr bool kStageFirst = F16C || RW >= 192;
+  // Tiles in flight per wave: narrow integer slices keep two (a 32-token
+  // tile of them is only 4 KB per wave, so one in flight leaves each tile
+  // waiting most of a memory round trip); the loop then takes the tiles in
+  // pairs, slot sl holding the tile 32 * sl tokens in, with every load
+  // unconditional (clamped) so the loads in flight can be counted.
+  constexpr int KD = (!kStageFirst && !PRE) ? 2 : 1;
   using RawT = typename std::conditional<F16C, f16x8, typename std::conditional<I4C, uint2, uint4>::type>::type;
-  RawT raw[NLD];
-  float sc_next[F16C ? 1 : 16], sc_cur[F16C ? 1 : 16];
-  auto load_tile = [&](int t0) {
-    if constexpr (!F16C) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
-        sc_next[v] = cscale[(int64_t)b * capacity + min(t, L - 1)];
-      }
-    }
+  RawT raw[KD][NLD];
+  float scr[KD], sc_cur[F16C ? 1 : 16];
+  auto load_tile = [&](int sl, int t0) {
+    if constexpr (!F16C) scr[sl] = cscale[(int64_t)b * capacity + min(t0 + l32, L - 1)];
     // rows past the chunk end are masked; re-read the last row instead of
     // fetching the next chunk's rows
     const int tk = min(t0 + l32, t_end - 1);
@@ -353,27 +362,51 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
       if constexpr (F16C)
-        raw[i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const _Float16*>(cdata) + off + kcol(i, half));
+        raw[sl][i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const _Float16*>(cdata) + off + kcol(i, half));
       else if constexpr (I4C)
-        raw[i] = *reinterpret_cast<const RawT*>(cdata + (off + kcol(2 * i, half)) / 2);
+        raw[sl][i] = *reinterpret_cast<const RawT*>(cdata + (off + kcol(2 * i, half)) / 2);
       else
-        raw[i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const int8_t*>(cdata) + off + kcol(2 * i, half));
+        raw[sl][i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const int8_t*>(cdata) + off + kcol(2 * i, half));
     }
   };
-  // Staging the tile before the score product (and reissuing the loads
-  // first) measured faster for fp16 rows and keeps the widest integer
-  // slices from spilling; narrower integer slices convert in registers
-  // and feed the score product directly.
-  constexpr bool kStageFirst = F16C || RW >= 192;
-  load_tile(t_begin);
-  // the query slice is read after the first tile's loads are out (it is an
-  // L2 hit, the tile comes from HBM)
-  if constexpr (!PRE) {
-    const _Float16* qrow = qt + ((int64_t)vb * kHeadBlk + l32) * r + slice0;
+  // the scales of tokens t0 + 8*(v/4) + 4*half + v%4, from the wave's staged copy
+  auto read_scales = [&]() {
+    if constexpr (!F16C) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, half));
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 q4 = *reinterpret_cast<const f32x4*>(scl + 8 * j + 4 * half);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sc_cur[4 * j + e] = q4[e];
+      }
+    }
+  };
+  // With one tile in flight the query slice is read after the first tile's
+  // loads are out (it is an L2 hit, the tile comes from HBM).  With two, the
+  // loads go out in the order the loop consumes them (query, slot 0, slot 1),
+  // so that the wait before each use can leave the later ones in flight.
+  auto load_query = [&]() {
+    if constexpr (!PRE) {
+      const _Float16* qrow = qt + ((int64_t)vb * kHeadBlk + l32) * r + slice0;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, half));
+    }
+  };
+  if constexpr (KD > 1) {
+    load_query();
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int sl = 0; sl < KD; ++sl) {
+      load_tile(sl, t_begin + 32 * sl);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+    load_tile(0, t_begin);
+    load_query();
   }
-  for (int t0 = t_begin; t0 < t_end; t0 += 32) {
+  for (int tb = t_begin; tb < t_end; tb += 32 * KD) {
+#pragma unroll
+  for (int sl = 0; sl < KD; ++sl) {
+    const int t0 = tb + 32 * sl;
     f32x16 sacc = f32x16{};
     float s[16];
     if constexpr (PRE) {
@@ -388,31 +421,31 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
       if constexpr (F16C) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(ks, half)) = raw[ks];
+          *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(ks, half)) = raw[sl][ks];
       } else {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) sc_cur[v] = sc_next[v];
+        scl[l32] = scr[sl];
 #pragma unroll
         for (int i = 0; i < NLD; ++i) {
           f16x8 c0, c1;
           if constexpr (I4C) {
-            c0 = cvt_i4x8(raw[i].x);
-            c1 = cvt_i4x8(raw[i].y);
+            c0 = cvt_i4x8(raw[sl][i].x);
+            c1 = cvt_i4x8(raw[sl][i].y);
           } else {
-            c0 = cvt_i8x8(raw[i].x, raw[i].y);
-            c1 = cvt_i8x8(raw[i].z, raw[i].w);
+            c0 = cvt_i8x8(raw[sl][i].x, raw[sl][i].y);
+            c1 = cvt_i8x8(raw[sl][i].z, raw[sl][i].w);
           }
           *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i, half)) = c0;
           *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i + 1, half)) = c1;
         }
       }
-      if (t0 + 32 < t_end) load_tile(t0 + 32);
+      if (KD > 1 || t0 + 32 < t_end) load_tile(sl, t0 + 32 * KD);
       asm volatile("" ::: "memory");
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
         if (t >= t_end) s[v] = -INFINITY;
       }
+      read_scales();
     } else {
     if constexpr (kStageFirst) {
     // The tile (as exact fp16) goes to this wave's LDS copy first, so that
@@ -422,25 +455,24 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     if constexpr (F16C) {
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(ks, half)) = raw[ks];
+        *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(ks, half)) = raw[sl][ks];
     } else {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sc_cur[v] = sc_next[v];
+      scl[l32] = scr[sl];
 #pragma unroll
       for (int i = 0; i < NLD; ++i) {
         f16x8 c0, c1;
         if constexpr (I4C) {
-          c0 = cvt_i4x8(raw[i].x);
-          c1 = cvt_i4x8(raw[i].y);
+          c0 = cvt_i4x8(raw[sl][i].x);
+          c1 = cvt_i4x8(raw[sl][i].y);
         } else {
-          c0 = cvt_i8x8(raw[i].x, raw[i].y);
-          c1 = cvt_i8x8(raw[i].z, raw[i].w);
+          c0 = cvt_i8x8(raw[sl][i].x, raw[sl][i].y);
+          c1 = cvt_i8x8(raw[sl][i].z, raw[sl][i].w);
         }
         *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i, half)) = c0;
         *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i + 1, half)) = c1;
       }
     }
-    if (t0 + 32 < t_end) load_tile(t0 + 32);
+    if (KD > 1 || t0 + 32 < t_end) load_tile(sl, t0 + 32 * KD);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
@@ -459,18 +491,17 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     f16x8 cf[KS];
     if constexpr (F16C) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) cf[ks] = raw[ks];
+      for (int ks = 0; ks < KS; ++ks) cf[ks] = raw[sl][ks];
     } else {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sc_cur[v] = sc_next[v];
+      scl[l32] = scr[sl];
 #pragma unroll
       for (int i = 0; i < NLD; ++i) {
         if constexpr (I4C) {
-          cf[2 * i] = cvt_i4x8(raw[i].x);
-          cf[2 * i + 1] = cvt_i4x8(raw[i].y);
+          cf[2 * i] = cvt_i4x8(raw[sl][i].x);
+          cf[2 * i + 1] = cvt_i4x8(raw[sl][i].y);
         } else {
-          cf[2 * i] = cvt_i8x8(raw[i].x, raw[i].y);
-          cf[2 * i + 1] = cvt_i8x8(raw[i].z, raw[i].w);
+          cf[2 * i] = cvt_i8x8(raw[sl][i].x, raw[sl][i].y);
+          cf[2 * i + 1] = cvt_i8x8(raw[sl][i].z, raw[sl][i].w);
         }
       }
     }
@@ -482,7 +513,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
       *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(ks, half)) = cf[ks];
     // The next tile streams in while this one is reduced, normalized and
     // multiplied into the output.
-    if (t0 + 32 < t_end) load_tile(t0 + 32);
+    if (KD > 1 || t0 + 32 < t_end) load_tile(sl, t0 + 32 * KD);
     }
 #pragma unroll
     for (int vb = 0; vb < 4; ++vb)
@@ -496,6 +527,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     }
     __syncthreads();
     // Lane l holds head l32 and tokens t0 + 8*(v/4) + 4*half + v%4.
+    read_scales();
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
@@ -567,6 +599,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
         const f16x8 a = {flo[0], flo[1], flo[2], flo[3], fhi[0], fhi[1], fhi[2], fhi[3]};
         o[rb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pf[mf], o[rb], 0, 0, 0);
       }
+  }
   }
 
   const int64_t part = (int64_t)vb * n_chunks + ch;
@@ -1208,7 +1241,8 @@ size_t attn_absorbed_workspace(const qsvd_layer& w, const qsvd_cache& c, int32_t
 template <int RW, int NW, int FMT, bool PRE = false>
 static hipError_t launch_latent(const AbsorbPlan& p, const qsvd_cache& c, int32_t q_len, const _Float16* qt,
                                 _Float16* opart, float* ml, hipStream_t s, const float* pre = nullptr) {
-  const size_t lds = (size_t)NW * 32 * (RW + 40) * 2 + (PRE ? 0 : (size_t)(NW + 1) * 1024 * 4);
+  const size_t lds = (size_t)NW * 32 * (RW + 40) * 2 + (PRE ? 0 : (size_t)(NW + 1) * 1024 * 4) +
+                     (FMT == QSVD_CACHE_F16 ? 0 : (size_t)NW * 32 * 4);
   auto kern = latent_attn_kernel<RW, NW, FMT, PRE>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
