@@ -474,7 +474,8 @@ def check_softmax_special_cases():
 
 def check_causal_prefix_consistency():
     """Query i of a q_len block sees exactly the first L-q_len+i+1 positions:
-    it equals a single query over the cache truncated to that length."""
+    it equals a single query over the cache truncated to that length (also
+    with rotary embeddings, where that length fixes the query's position)."""
     layer = tiny_layer()
     X = gen.prefill_activations(tiny_workload())
     cache, proj = build_cache(layer, O.CACHE_F16, X, [64])
@@ -484,6 +485,15 @@ def check_causal_prefix_consistency():
         sub = O.LatentCache(O.CACHE_F16, 1, 64, layer.r)
         sub.append(0, cache.data[0, :64 - 6 + i + 1])
         one = O.attention_reference(layer, sub, q[:, i:i + 1], q_len=1)
+        assert np.allclose(block[0, i], one[0, 0], rtol=1e-12, atol=1e-15)
+    # the same with rotary embeddings: query i of the block sits at position L - q_len + i
+    block = O.attention_reference(layer, cache, q, q_len=6, rope_theta=500.0)
+    plain = O.attention_reference(layer, cache, q, q_len=6)
+    assert np.max(np.abs(block - plain)) > 1e-3
+    for i in range(6):
+        sub = O.LatentCache(O.CACHE_F16, 1, 64, layer.r)
+        sub.append(0, cache.data[0, :64 - 6 + i + 1])
+        one = O.attention_reference(layer, sub, q[:, i:i + 1], q_len=1, rope_theta=500.0)
         assert np.allclose(block[0, i], one[0, 0], rtol=1e-12, atol=1e-15)
 
 
