@@ -247,8 +247,8 @@ qsvd_status qsvd_prefill_attention_rope(const void* q, const void* k, const void
  *   q     device fp16 [batch][q_len][Hq*hd] (the Q output of the projection)
  *   out   device fp16 [batch][q_len][Hq*hd]
  *   mode  QSVD_ATTN_ABSORBED (latent form), QSVD_ATTN_RECONSTRUCT (K, V
- *         rebuilt per cached token; q_len 1 only) or QSVD_ATTN_AUTO (absorbed
- *         when its shape is supported)
+ *         rebuilt per cached token) or QSVD_ATTN_AUTO (absorbed when its shape
+ *         is supported)
  *   sm_scale  0 selects 1/sqrt(head_dim)
  *   ws    device workspace of at least qsvd_decode_workspace_size() bytes
  * Requires head_dim % 32 == 0 and <= 128, batch <= 64, q_len <= max_len,
@@ -256,8 +256,9 @@ qsvd_status qsvd_prefill_attention_rope(const void* q, const void* k, const void
  * r in {128, 512, 1024, 1536} (with at most 32 heads) or r a multiple of 128
  * up to 3072, any cache format, and batch * q_len * ceil(n_q_heads / 16)
  * <= 65535 (batch * q_len <= 65535 with 32-head blocks); the reconstruct
- * form takes n_q_heads <= 64, q_len 1, capacity <= 16384 and any cache
- * format (F16 rows rebuild on the fp16 products, I8 on the int8 products,
+ * form takes n_q_heads <= 64, capacity <= 16384 and any cache format, and
+ * with q_len > 1 (causal attention of the last q_len positions over the
+ * rebuilt rows on the fp16 matrix cores) head_dim 64 or 128 (F16 rows rebuild on the fp16 products, I8 on the int8 products,
  * I4 on the 4-bit products).
  * Launch grids are sized from the host c->max_len and every length is read
  * from seq_len on the device, so a call may be captured in a graph and
@@ -287,10 +288,12 @@ size_t qsvd_noalloc_scratch_bytes(void);
 /* The same attention for layers that apply a rotary position embedding to q
  * and k (the paper's layers have none; this is the position-encoded variant
  * of Section 3.1's decode step).  Every rebuilt key row at position t and the
- * query at position seq_len[b] - 1 are rotated before the product: each head
- * vector's pairs (j, j + head_dim/2), j < head_dim/2, are turned by the angle
- * t * rope_theta^(-2j/head_dim), formed and reduced modulo 2 pi in fp64 and
- * evaluated in fp32.  Values are not rotated.  Because a key then depends on
+ * queries at their positions (seq_len[b] - q_len + i) are rotated before the
+ * product: each head vector's pairs (j, j + head_dim/2), j < head_dim/2, are
+ * turned by the angle t * rope_theta^(-2j/head_dim), formed and reduced
+ * modulo one turn in fp64 and evaluated in fp32 (q_len 1: a cos/sin table
+ * per call; q_len > 1: the hardware's sine and cosine of the reduced angle in
+ * turns).  Values are not rotated.  Because a key then depends on
  * its position, it cannot be folded into the query, so the keys are rebuilt
  * in both forms:
  *   QSVD_ATTN_ABSORBED     K rebuilt and rotated for the scores, the value side
@@ -298,11 +301,15 @@ size_t qsvd_noalloc_scratch_bytes(void);
  *                          needs n_q_heads <= 32 and r in {128, 512, 1024, 1536}
  *                          (QSVD_ERR_UNSUPPORTED otherwise)
  *   QSVD_ATTN_RECONSTRUCT  K and V rebuilt, plain attention; needs
- *                          n_q_heads <= 64 and capacity <= 16384
- *   QSVD_ATTN_AUTO         the first where it applies, else the second
- * Both take q_len 1 only and any cache format (F16, I8, I4), and one workspace
- * size serves both: qsvd_decode_workspace_size(w, c, 1, QSVD_ATTN_RECONSTRUCT)
- * bytes.  rope_theta must be finite and > 1 (QSVD_ERR_INVALID_ARG otherwise). */
+ *                          n_q_heads <= 64 and capacity <= 16384; with
+ *                          q_len > 1 (query i at position seq_len[b] -
+ *                          q_len + i, causal) head_dim 64 or 128
+ *   QSVD_ATTN_AUTO         the first where it applies (q_len 1), else the second
+ * The latent-value form takes q_len 1 (QSVD_ERR_UNSUPPORTED otherwise).  Both
+ * take any cache format (F16, I8, I4), and one workspace size serves both:
+ * qsvd_decode_workspace_size(w, c, q_len, QSVD_ATTN_RECONSTRUCT) bytes (the
+ * same for every q_len).  rope_theta must be finite and > 1
+ * (QSVD_ERR_INVALID_ARG otherwise). */
 qsvd_status qsvd_latent_decode_attention_rope(const qsvd_layer* w, const qsvd_cache* c,
                                               const void* q, int32_t q_len, int32_t mode,
                                               float sm_scale, float rope_theta, void* out,

@@ -432,7 +432,7 @@ size_t qsvd_decode_workspace_size(const qsvd_layer* w, const qsvd_cache* c, int3
   if ((int64_t)c->batch * q_len > kMaxQueryRows) return 0;
   const bool abs_ok = absorbed_supported(*w, *c);
   if (mode == QSVD_ATTN_RECONSTRUCT || (mode == QSVD_ATTN_AUTO && !abs_ok))
-    return q_len == 1 ? attn_reconstruct_workspace(*w, *c) : 0;
+    return q_len == 1 || prefill_attention_supported(w->head_dim) ? attn_reconstruct_workspace(*w, *c) : 0;
   if (absorbed_grid_rows(*w, *c, q_len) > kMaxQueryRows) return 0;
   return attn_absorbed_workspace(*w, *c, q_len);
 }
@@ -498,10 +498,13 @@ static qsvd_status decode_attention(const qsvd_layer* w, const qsvd_cache* c, co
   if (mode == QSVD_ATTN_ABSORBED && !abs_ok)
     return fail(QSVD_ERR_UNSUPPORTED, rope ? "the rotary latent-value form needs n_q_heads <= 32 and r in {128, 512, 1024, 1536}"
                                            : "absorbed form needs r in {128, 512, 1024, 1536} or a multiple of 128 up to 3072");
-  const bool absorbed = mode == QSVD_ATTN_ABSORBED || (mode == QSVD_ATTN_AUTO && abs_ok);
+  // the rotary latent-value form takes one query per sequence; AUTO then rebuilds K and V
+  const bool absorbed = mode == QSVD_ATTN_ABSORBED || (mode == QSVD_ATTN_AUTO && abs_ok && !(rope && q_len > 1));
   if (absorbed && absorbed_grid_rows(*w, *c, q_len) > kMaxQueryRows)
     return fail(QSVD_ERR_UNSUPPORTED, "batch * q_len * head blocks must be at most %d", (int)kMaxQueryRows);
-  if ((!absorbed || rope) && q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct-side forms take q_len 1 only");
+  if (absorbed && rope && q_len != 1) return fail(QSVD_ERR_UNSUPPORTED, "the rotary latent-value form takes q_len 1 only");
+  if (!absorbed && q_len != 1 && !prefill_attention_supported(w->head_dim))
+    return fail(QSVD_ERR_UNSUPPORTED, "the reconstruct form with q_len > 1 needs head_dim 64 or 128");
   if (!absorbed && c->capacity > 16384)
     return fail(QSVD_ERR_UNSUPPORTED, "reconstruct form supports capacity <= 16384");
   const size_t need = absorbed && !rope ? attn_absorbed_workspace(*w, *c, q_len) : attn_reconstruct_workspace(*w, *c);

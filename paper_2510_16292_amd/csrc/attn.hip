@@ -1895,6 +1895,14 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
   const int len = c.max_len > 0 ? c.max_len : 1;
   hipError_t e = rebuild_rows(a, nkv2, w16, kv, s);
   if (e != hipSuccess) return e;
+  if (a.q_len > 1) {
+    // several queries per sequence: causal attention of the last q_len
+    // positions over the rebuilt rows on the fp16 matrix cores (rotary
+    // embeddings turned in that kernel at each row's position)
+    const CacheAttnArgs ca{a.q, kv, c.seq_len, c.batch, c.capacity, a.q_len, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                           a.sm_scale, a.rope_theta, a.out};
+    return launch_cache_attention(ca, s);
+  }
   if (rope && (e = launch_rope_table(a, rope, s)) != hipSuccess) return e;
   const int nch = (len + RCH - 1) / RCH;
   const int G = w.n_q_heads / w.n_kv_heads;

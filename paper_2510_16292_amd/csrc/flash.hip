@@ -162,11 +162,19 @@ __device__ __forceinline__ void fa_store_tile(_Float16* ks, _Float16* vs, int ti
   }
 }
 
-template <int DH, bool ROPE>
+// Cache mode: the queries are the last q_len positions of each sequence of a
+// cache and the keys and values its rebuilt rows (row b * capacity + t,
+// position t < seq_len[b], row stride ldkv).
+struct FaCacheArgs {
+  const int32_t* seq_len;
+  int32_t capacity, q_len, ldkv;
+};
+
+template <int DH, bool ROPE, bool CACHE>
 __global__ void __launch_bounds__(kFaWaves * 64, 2)
 prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ k, const _Float16* __restrict__ v,
                      const int32_t* __restrict__ cu, int32_t n_seq, int32_t Hq, int32_t Hkv, int32_t n_qt,
-                     float scale_log2, double log2_theta, _Float16* __restrict__ out) {
+                     float scale_log2, double log2_theta, FaCacheArgs ca, _Float16* __restrict__ out) {
   using C = FaCfg<DH>;
   constexpr int KS = DH / 32;      // contraction steps of the score product
   constexpr int OB = DH / 16;      // 16-channel blocks of the output
@@ -186,17 +194,41 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
   if (total % 8 == 0) lin = (lin % 8) * (total / 8) + lin / 8;
   const int grp = lin / n_qt, qt = n_qt - 1 - (lin - grp * n_qt);
   const int b = grp / Hq, h = grp - b * Hq;
-  const int tok0 = cu[b], n = cu[b + 1] - tok0;
+  // this sequence's rows: query i (i < nq) is row q_row0 + i at position
+  // q_off + i, key t (t < nk) is row k_row0 + t at position t; query i sees
+  // the keys at positions <= q_off + i
+  int q_row0, nq, k_row0, nk, q_off;
+  if (CACHE) {
+    nk = min(ca.seq_len[b], ca.capacity);
+    nq = ca.q_len;
+    q_row0 = b * nq;
+    k_row0 = b * ca.capacity;
+    q_off = nk - nq;
+  } else {
+    q_row0 = k_row0 = cu[b];
+    nq = nk = cu[b + 1] - q_row0;
+    q_off = 0;
+  }
   const int q0 = qt * kFaQ;
-  if (q0 >= n) return;
+  if (q0 >= nq) return;
   double* freq = reinterpret_cast<double*>(fa_smem + C::kLds);
   if (ROPE) {
     if (tid < DH / 2) freq[tid] = exp2(-2.0 * tid / DH * log2_theta) * 0.15915494309189533576888376337251;
     __syncthreads();
   }
   const int g_kv = (h * Hkv) / Hq;
-  const int ldq = Hq * DH, ldkv = Hkv * DH;
-  const int kend = min(n, q0 + kFaQ);              // keys this tile of queries can see
+  const int ldq = Hq * DH, ldkv = CACHE ? ca.ldkv : Hkv * DH;
+  const int kend = min(nk, q_off + min(nq, q0 + kFaQ));   // keys this tile of queries can see
+  if (kend <= 0) {
+    // no query of the tile sees a position (a cache shorter than the query
+    // block): zeros, as for every query without a visible position
+#pragma unroll
+    for (int i = 0; i < kFaQ * RUNS / (kFaWaves * 64); ++i) {
+      const int e = tid + kFaWaves * 64 * i, row = e / RUNS, c8 = e - row * RUNS;
+      if (q0 + row < nq) *reinterpret_cast<f16x8*>(out + (int64_t)(q_row0 + q0 + row) * ldq + h * DH + 8 * c8) = f16x8{};
+    }
+    return;
+  }
   const int n_tiles = (kend + kFaK - 1) / kFaK;
   const int qw0 = q0 + kFaQW * w;                   // this wave's first query
   int my_q[kFaQB];                                  // this lane's query in each block
@@ -207,13 +239,13 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
   f16x8 qf[kFaQB][KS];
 #pragma unroll
   for (int qb = 0; qb < kFaQB; ++qb) {
-    const _Float16* qrow = q + (int64_t)(tok0 + min(my_q[qb], n - 1)) * ldq + h * DH + 8 * g;
+    const _Float16* qrow = q + (int64_t)(q_row0 + min(my_q[qb], nq - 1)) * ldq + h * DH + 8 * g;
 #pragma unroll
     for (int s = 0; s < KS; ++s) qf[qb][s] = *reinterpret_cast<const f16x8*>(qrow + 32 * s);
     if (ROPE) {                                     // slot s pairs with slot s + KS/2 (channels dh/2 further)
 #pragma unroll
       for (int s = 0; s < KS / 2; ++s)
-        fa_rope8(qf[qb][s], qf[qb][s + KS / 2], min(my_q[qb], n - 1), freq + 32 * s + 8 * g);
+        fa_rope8(qf[qb][s], qf[qb][s + KS / 2], q_off + min(my_q[qb], nq - 1), freq + 32 * s + 8 * g);
     }
   }
 
@@ -230,14 +262,14 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
   typedef short s16x4 __attribute__((ext_vector_type(4)));
   typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-  fa_load_tile<DH, ROPE>(k, v, tok0, n, ldkv, g_kv, 0, tid, kr, vr);
+  fa_load_tile<DH, ROPE>(k, v, k_row0, nk, ldkv, g_kv, 0, tid, kr, vr);
   for (int t = 0; t < n_tiles; ++t) {
     __syncthreads();                                // every wave is done with the previous tile
     fa_store_tile<DH, ROPE>(ks, vs, tid, t, freq, kr, vr);
     __syncthreads();
-    if (t + 1 < n_tiles) fa_load_tile<DH, ROPE>(k, v, tok0, n, ldkv, g_kv, t + 1, tid, kr, vr);
+    if (t + 1 < n_tiles) fa_load_tile<DH, ROPE>(k, v, k_row0, nk, ldkv, g_kv, t + 1, tid, kr, vr);
     const int kt0 = t * kFaK;
-    if (kt0 > qw0 + kFaQW - 1) continue;            // every key of the tile is after this wave's queries
+    if (kt0 > q_off + qw0 + kFaQW - 1) continue;    // every key of the tile is after this wave's queries
     // S^T: key block kb, lane (query l16 of block qb, group g) holds keys kt0 + 16 kb + 4 g + v
     f32x4 sacc[kFaQB][4];
 #pragma unroll
@@ -255,7 +287,7 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
     // softmax per query block; the scores become the probabilities in place
     // (tiles wholly before this wave's first query and inside the sequence
     // need no mask)
-    const bool full = kt0 + kFaK - 1 <= qw0 && kt0 + kFaK <= n;
+    const bool full = kt0 + kFaK - 1 <= q_off + qw0 && kt0 + kFaK <= nk;
     float p[kFaQB][4][4];
 #pragma unroll
     for (int qb = 0; qb < kFaQB; ++qb) {
@@ -274,7 +306,7 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
 #pragma unroll
           for (int vv = 0; vv < 4; ++vv) {
             const int key = kt0 + 16 * kb + 4 * g + vv;
-            p[qb][kb][vv] = (key <= my_q[qb] && key < n) ? sacc[qb][kb][vv] * scale_log2 : -INFINITY;
+            p[qb][kb][vv] = (key <= q_off + my_q[qb] && key < nk) ? sacc[qb][kb][vv] * scale_log2 : -INFINITY;
             mx = fmaxf(mx, p[qb][kb][vv]);
           }
       }
@@ -348,24 +380,25 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
   for (int i = 0; i < kFaQW * RUNS / 64; ++i) {
     const int e = lane + 64 * i, row = e / RUNS, c8 = e - row * RUNS;
     const int qq = qw0 + row;
-    if (qq < n)
-      *reinterpret_cast<f16x8*>(out + (int64_t)(tok0 + qq) * ldq + h * DH + 8 * c8) =
+    if (qq < nq)
+      *reinterpret_cast<f16x8*>(out + (int64_t)(q_row0 + qq) * ldq + h * DH + 8 * c8) =
           *reinterpret_cast<const f16x8*>(ost + row * C::OST + 8 * c8);
   }
 }
 
-template <int DH, bool ROPE>
-static hipError_t launch_flash(const PrefillAttnArgs& a, hipStream_t s) {
+template <int DH, bool ROPE, bool CACHE>
+static hipError_t launch_flash(const PrefillAttnArgs& a, const FaCacheArgs& ca, hipStream_t s) {
   using C = FaCfg<DH>;
-  auto kern = prefill_flash_kernel<DH, ROPE>;
+  auto kern = prefill_flash_kernel<DH, ROPE, CACHE>;
   const size_t lds = ROPE ? C::kLdsRope : C::kLds;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  const int n_qt = (a.max_seqlen + kFaQ - 1) / kFaQ;
+  const int n_qt = ((CACHE ? ca.q_len : a.max_seqlen) + kFaQ - 1) / kFaQ;
   const int64_t blocks = (int64_t)a.batch * a.n_q_heads * n_qt;
-  KernelScope ks(ROPE ? "prefill_flash_rope" : "prefill_flash", s);
+  KernelScope ks(CACHE ? "cache_flash" : ROPE ? "prefill_flash_rope" : "prefill_flash", s);
   QSVD_LAUNCH(ks, kern, dim3((unsigned)blocks), dim3(kFaWaves * 64), lds, s, a.q, a.k, a.v, a.cu_seqlens, a.batch,
-              a.n_q_heads, a.n_kv_heads, n_qt, a.sm_scale * kFaLog2e, ROPE ? log2((double)a.rope_theta) : 0.0, a.out);
+              a.n_q_heads, a.n_kv_heads, n_qt, a.sm_scale * kFaLog2e, ROPE ? log2((double)a.rope_theta) : 0.0, ca,
+              a.out);
   return hipGetLastError();
 }
 
@@ -373,8 +406,23 @@ bool prefill_attention_supported(int32_t head_dim) { return head_dim == 64 || he
 
 hipError_t launch_prefill_attention(const PrefillAttnArgs& a, hipStream_t s) {
   if (a.batch == 0 || a.max_seqlen == 0) return hipSuccess;
-  if (a.rope_theta > 0.f) return a.head_dim == 128 ? launch_flash<128, true>(a, s) : launch_flash<64, true>(a, s);
-  return a.head_dim == 128 ? launch_flash<128, false>(a, s) : launch_flash<64, false>(a, s);
+  const FaCacheArgs none{};
+  if (a.rope_theta > 0.f)
+    return a.head_dim == 128 ? launch_flash<128, true, false>(a, none, s) : launch_flash<64, true, false>(a, none, s);
+  return a.head_dim == 128 ? launch_flash<128, false, false>(a, none, s) : launch_flash<64, false, false>(a, none, s);
+}
+
+// Queries of several positions per sequence over a cache's rebuilt K^ | V^
+// rows (the reconstruct form with q_len > 1).
+hipError_t launch_cache_attention(const CacheAttnArgs& c, hipStream_t s) {
+  if (c.batch == 0 || c.q_len == 0) return hipSuccess;
+  const int nkv = c.n_kv_heads * c.head_dim;
+  PrefillAttnArgs a{c.q, c.kv, c.kv + nkv, nullptr, c.batch, c.q_len, c.n_q_heads, c.n_kv_heads, c.head_dim,
+                    c.sm_scale, c.out, c.rope_theta};
+  const FaCacheArgs ca{c.seq_len, c.capacity, c.q_len, 2 * nkv};
+  if (c.rope_theta > 0.f)
+    return c.head_dim == 128 ? launch_flash<128, true, true>(a, ca, s) : launch_flash<64, true, true>(a, ca, s);
+  return c.head_dim == 128 ? launch_flash<128, false, true>(a, ca, s) : launch_flash<64, false, true>(a, ca, s);
 }
 
 }  // namespace qsvd

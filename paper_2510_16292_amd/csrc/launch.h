@@ -142,4 +142,14 @@ struct PrefillAttnArgs {
 bool prefill_attention_supported(int32_t head_dim);
 hipError_t launch_prefill_attention(const PrefillAttnArgs& a, hipStream_t s);
 
+struct CacheAttnArgs {
+  const _Float16* q;        // [batch][q_len][n_q_heads * head_dim]
+  const _Float16* kv;       // rebuilt rows [batch][capacity][2 * n_kv_heads * head_dim]: K^ then V^
+  const int32_t* seq_len;   // device [batch]
+  int32_t batch, capacity, q_len, n_q_heads, n_kv_heads, head_dim;
+  float sm_scale, rope_theta;
+  _Float16* out;            // [batch][q_len][n_q_heads * head_dim]
+};
+hipError_t launch_cache_attention(const CacheAttnArgs& c, hipStream_t s);
+
 }  // namespace qsvd

@@ -261,7 +261,14 @@ def test_decode_validation(lib):
     L, C = layer_struct(), cache_struct()
     assert _decode(L, C, q_len=0) == B.QSVD_ERR_INVALID_ARG
     assert _decode(L, C, q_len=11) == B.QSVD_ERR_INVALID_ARG                  # more queries than cached tokens
-    assert _decode(L, C, q_len=2, mode=B.QSVD_ATTN_RECONSTRUCT) == B.QSVD_ERR_UNSUPPORTED
+    # the reconstruct form with q_len > 1 (the cache-mode flash kernel) needs head_dim 64 or 128
+    need_q2 = B.qsvd_decode_workspace_size(L, C, 2, B.QSVD_ATTN_RECONSTRUCT)
+    assert need_q2 == B.qsvd_decode_workspace_size(L, C, 1, B.QSVD_ATTN_RECONSTRUCT) > 0
+    assert _decode(L, C, q_len=2, mode=B.QSVD_ATTN_RECONSTRUCT, ws_bytes=need_q2 - 1) == B.QSVD_ERR_WORKSPACE
+    assert _decode(layer_struct(head_dim=32, n_q_heads=8, n_kv_heads=8), C, q_len=2,
+                   mode=B.QSVD_ATTN_RECONSTRUCT) == B.QSVD_ERR_UNSUPPORTED
+    assert B.qsvd_decode_workspace_size(layer_struct(head_dim=32, n_q_heads=8, n_kv_heads=8), C, 2,
+                                        B.QSVD_ATTN_RECONSTRUCT) == 0
     assert _decode(L, cache_struct(batch=64, max_len=2000, capacity=4096), q_len=1025) == B.QSVD_ERR_UNSUPPORTED
     assert _decode(L, C, mode=3) == B.QSVD_ERR_INVALID_ARG
     assert _decode(L, C, sm=-1.0) == B.QSVD_ERR_INVALID_ARG
@@ -301,7 +308,6 @@ def test_decode_validation(lib):
     assert _decode(L, C, mode=B.QSVD_ATTN_ABSORBED, ws_bytes=need - 1) == B.QSVD_ERR_WORKSPACE
     need_r = B.qsvd_decode_workspace_size(L, C, 1, B.QSVD_ATTN_RECONSTRUCT)
     assert _decode(L, C, mode=B.QSVD_ATTN_RECONSTRUCT, ws_bytes=need_r - 1) == B.QSVD_ERR_WORKSPACE
-    assert B.qsvd_decode_workspace_size(L, C, 2, B.QSVD_ATTN_RECONSTRUCT) == 0
     assert B.qsvd_decode_workspace_size(L, C, 0, 0) == 0
     # q_len > 1 (absorbed): one query row block per (sequence, query)
     need2 = B.qsvd_decode_workspace_size(L, C, 2, B.QSVD_ATTN_ABSORBED)
@@ -316,8 +322,9 @@ def _decode_rope(layer, cache, theta=10000.0, q_len=1, mode=0, ws_bytes=1 << 40)
 def test_decode_rope_validation(lib):
     """Every case fails before a launch.  Rotary layers run the form with the
     value side in latent space (ABSORBED, or AUTO where its 32-head plans
-    apply) or the full rebuild (RECONSTRUCT), q_len 1, with a base above 1;
-    one workspace size (the reconstruct query) serves both."""
+    apply; q_len 1) or the full rebuild (RECONSTRUCT; any q_len, head_dim 64
+    or 128 above 1), with a base above 1; one workspace size (the
+    reconstruct query) serves both."""
     L, C = layer_struct(), cache_struct()
     for theta in (0.0, -5.0, 1.0, float("inf"), float("nan")):
         assert _decode_rope(L, C, theta=theta) == B.QSVD_ERR_INVALID_ARG
@@ -330,7 +337,11 @@ def test_decode_rope_validation(lib):
     assert _decode_rope(wide, C, ws_bytes=need_w - 1) == B.QSVD_ERR_WORKSPACE   # AUTO -> full rebuild, 40 heads
     assert _decode_rope(layer_struct(n_q_heads=80, n_kv_heads=8, head_dim=64), C) == B.QSVD_ERR_UNSUPPORTED
     for mode in (B.QSVD_ATTN_AUTO, B.QSVD_ATTN_ABSORBED, B.QSVD_ATTN_RECONSTRUCT):
-        assert _decode_rope(L, C, q_len=2, mode=mode) == B.QSVD_ERR_UNSUPPORTED
+        if mode == B.QSVD_ATTN_ABSORBED:          # the latent-value form: one query per sequence
+            assert _decode_rope(L, C, q_len=2, mode=mode) == B.QSVD_ERR_UNSUPPORTED
+        else:                                     # AUTO and RECONSTRUCT rebuild K and V for q_len > 1
+            need2 = B.qsvd_decode_workspace_size(L, C, 2, B.QSVD_ATTN_RECONSTRUCT)
+            assert _decode_rope(L, C, q_len=2, mode=mode, ws_bytes=need2 - 1) == B.QSVD_ERR_WORKSPACE
     assert _decode_rope(L, cache_struct(capacity=20000), mode=B.QSVD_ATTN_RECONSTRUCT) == B.QSVD_ERR_UNSUPPORTED
     assert _decode_rope(L, C, mode=3) == B.QSVD_ERR_INVALID_ARG
     for c in (C, cache_struct(fmt=B.QSVD_CACHE_I8, scale=FAKE), cache_struct(fmt=B.QSVD_CACHE_I4, scale=FAKE)):

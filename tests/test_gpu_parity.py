@@ -1515,6 +1515,77 @@ def test_decode_rope_head_dims(shape, fmt):
         assert ok, (mode, info)
 
 
+def _check_qlen_block(out, ref, lengths, q_len):
+    """Rows with a visible position against the oracle; rows whose position
+    precedes the cache (a sequence shorter than the query block) are zeros."""
+    for b, n in enumerate(lengths):
+        for i in range(q_len):
+            if n - q_len + i < 0:
+                assert not np.any(out[b, i].astype(np.float32)), (b, i)
+    keep = [(b, i) for b, n in enumerate(lengths) for i in range(q_len) if n - q_len + i >= 0]
+    got = np.stack([out[b, i] for b, i in keep])
+    want = np.stack([ref[b, i] for b, i in keep])
+    ok, info = H.close_enough(got, want)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+
+
+@pytest.mark.parametrize("theta", [None, 1.0e4], ids=["plain", "rope"])
+@pytest.mark.parametrize("fmt", [O.CACHE_F16, O.CACHE_I8, O.CACHE_I4], ids=["f16", "i8", "i4"])
+def test_decode_reconstruct_qlen_block(gqa, fmt, theta):
+    """Several queries per sequence in the full-rebuild form (grouped heads
+    8/2, dh 64): the last 5 positions of ragged caches 3 / 45 / 130 (the
+    first sequence shorter than the block: its first two rows see nothing
+    and are zeros), causal, with and without rotary embeddings (the rotary
+    latent-value form takes one query, so AUTO rebuilds here), against the
+    oracle."""
+    L, ol, dl = gqa
+    lengths, q_len = [3, 45, 130], 5
+    wl = configs.Workload(99, "qlen-block", L, "gaussian", 8, 0, 8, fmt)
+    oc, dc = _prefilled_caches(wl, fmt, lengths, 136)
+    g = np.random.default_rng(55)
+    q = (g.standard_normal((3, q_len, L.n_q_heads * L.head_dim)) * 4.0).astype(np.float16)
+    ref = np.zeros(q.shape, np.float64)
+    for b, n in enumerate(lengths):
+        k = min(q_len, n)
+        ref[b:b + 1, q_len - k:] = O.attention_reference(ol, oc, q.astype(np.float64)[:, q_len - k:], q_len=k,
+                                                         batches=[b], rope_theta=theta)[b:b + 1]
+    modes = [B.QSVD_ATTN_RECONSTRUCT] + ([B.QSVD_ATTN_AUTO] if theta else [])
+    for mode in modes:
+        H.say(f"decode q_len block fmt={fmt} theta={theta} mode={mode}")
+        out = H.host(H.decode_attention(dl, dc, H.dev(q), mode, q_len=q_len, rope_theta=theta))
+        _check_qlen_block(out.reshape(q.shape), ref, lengths, q_len)
+
+
+def test_decode_rope_qlen_llava7b_chunk(llava):
+    """A 64-query chunk continuing two LLaVA-7B-shaped sequences (32 heads x
+    128, r = 1536, fp16 cache of 200 and 1000 tokens) with rotary embeddings
+    in the full-rebuild form, against the oracle; the plain form of the same
+    block against the absorbed form's result."""
+    wl, ol, dl = llava
+    L = wl.layer
+    lengths, q_len, cap = [200, 1000], 64, 1008
+    rows = gen.latent_rows(wl, 2, cap)
+    oc = O.LatentCache(O.CACHE_F16, 2, cap, L.r)
+    for b, n in enumerate(lengths):
+        oc.append(b, rows[b, :n])
+    dc = B.DeviceCache(B.QSVD_CACHE_F16, 2, cap, L.r, lengths)
+    dc.data.copy_(H.dev(oc.data))
+    g = np.random.default_rng(64)
+    q = (g.standard_normal((2, q_len, L.n_q_heads * L.head_dim)) * 2.0).astype(np.float16)
+    q_dev = H.dev(q)
+    H.say("decode rope q_len 64 llava7b")
+    ref = O.attention_reference(ol, oc, q.astype(np.float64), q_len=q_len, rope_theta=1.0e4)
+    out = H.host(H.decode_attention(dl, dc, q_dev, B.QSVD_ATTN_RECONSTRUCT, q_len=q_len, rope_theta=1.0e4))
+    _check_qlen_block(out.reshape(q.shape), ref, lengths, q_len)
+    H.say("decode plain q_len 64 llava7b: rebuild vs absorbed")
+    rec = H.host(H.decode_attention(dl, dc, q_dev, B.QSVD_ATTN_RECONSTRUCT, q_len=q_len)).reshape(q.shape)
+    ab = H.host(H.decode_attention(dl, dc, q_dev, B.QSVD_ATTN_ABSORBED, q_len=q_len)).reshape(q.shape)
+    want = O.attention_reference(ol, oc, q.astype(np.float64), q_len=q_len)
+    _check_qlen_block(rec, want, lengths, q_len)
+    _check_qlen_block(ab, want, lengths, q_len)
+
+
 @pytest.mark.parametrize("shape,r", [((40, 40, 128), 1024), ((40, 8, 64), 512), ((64, 64, 64), 512)],
                          ids=["mha40_dh128", "g5_40_dh64", "mha64_dh64"])
 @pytest.mark.parametrize("fmt", [O.CACHE_F16, O.CACHE_I8, O.CACHE_I4], ids=["f16", "i8", "i4"])
