@@ -1119,6 +1119,7 @@ vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt,
     for (int st0 = s_begin; st0 < s_end; st0 += kVprojBatch) {
       f16x8 a[kVprojBatch];
       uint2 raw[kVprojBatch];
+      float gsc[kVprojBatch];      // per-group scales, loaded with the codes
 #pragma unroll
       for (int k = 0; k < kVprojBatch; ++k) {
         const int j = (st0 + k) * 32;
@@ -1130,6 +1131,7 @@ vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt,
             raw[k].x = *reinterpret_cast<const uint32_t*>(bt + ((int64_t)n * r + j + 8 * quad) / 2);
             raw[k].y = 0u;
           }
+          gsc[k] = group ? sb[(int64_t)(j / group) * N + n] : 1.f;
         }
       }
 #pragma unroll
@@ -1139,7 +1141,7 @@ vproj_kernel(const _Float16* __restrict__ o_lat, const uint8_t* __restrict__ bt,
         const f16x8 av = bA < B ? a[k] : f16x8{};
         const f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bw, f32x4{}, 0, 0, 0);
         if (group) {
-          const float sc = sb[(int64_t)(((st0 + k) * 32) / group) * N + n];
+          const float sc = gsc[k];
 #pragma unroll
           for (int v = 0; v < 4; ++v) res[v] = fmaf(acc[v], sc, res[v]);
         } else {

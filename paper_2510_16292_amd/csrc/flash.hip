@@ -219,7 +219,7 @@ prefill_flash_kernel(const _Float16* __restrict__ q, const _Float16* __restrict_
   const int g_kv = (h * Hkv) / Hq;
   const int ldq = Hq * DH, ldkv = CACHE ? ca.ldkv : Hkv * DH;
   const int kend = min(nk, q_off + min(nq, q0 + kFaQ));   // keys this tile of queries can see
-  if (kend <= 0) {
+  if (CACHE && kend <= 0) {
     // no query of the tile sees a position (a cache shorter than the query
     // block): zeros, as for every query without a visible position
 #pragma unroll
