@@ -118,7 +118,7 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
   constexpr int TI = WM / 32, TJ = WN / 32;
   extern __shared__ __attribute__((aligned(1024))) uint8_t pipe_smem[];
   __shared__ __attribute__((aligned(16))) float s_rs[BM];
-  __shared__ float s_cs[BN];
+  __shared__ __attribute__((aligned(16))) float s_cs[BN];
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w / (BN / WN), wn = w % (BN / WN);
   const int l32 = lane & 31, hl = lane >> 5;
@@ -188,10 +188,10 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
 #pragma unroll
       for (int j = 0; j < TJ; ++j)
         if constexpr (F16)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, af[kk][i]),
-                                                             __builtin_bit_cast(f16x8, bf[kk][j]), acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, bf[kk][j]),
+                                                             __builtin_bit_cast(f16x8, af[kk][i]), acc[i][j], 0, 0, 0);
         else
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk][i], bf[kk][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bf[kk][j], af[kk][i], acc[i][j], 0, 0, 0);
   };
 
   // One MFMA goes out before each LDS read of the other half, so the reads
@@ -234,17 +234,19 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
   // Epilogue.  The integer accumulators are dumped as they are (debug only);
   // the dequantized fp16 tile of each wave is staged in LDS (the stages are
   // free once every wave is past its last product) and written back as
-  // 16-byte runs of one row.  Lane holds column wn*WN + 32j + l32 and rows
-  // wm*WM + 32i + 8(v/4) + 4hl + v%4.
+  // 16-byte runs of one row.  The products take B's fragment as their first
+  // operand, so lane holds row wm*WM + 32i + l32 and the four consecutive
+  // columns wn*WN + 32j + 8(v/4) + 4hl + 0..3: one 8-byte LDS write per
+  // four outputs.
   if constexpr (DBG) {
 #pragma unroll
     for (int j = 0; j < TJ; ++j) {
-      const int32_t n = n0 + wn * WN + 32 * j + l32;
 #pragma unroll
       for (int i = 0; i < TI; ++i)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int64_t m = m0 + wm * WM + 32 * i + 8 * (v >> 2) + 4 * hl + (v & 3);
+          const int64_t m = m0 + wm * WM + 32 * i + l32;
+          const int32_t n = n0 + wn * WN + 32 * j + 8 * (v >> 2) + 4 * hl + (v & 3);
           if (m < M && n < N) dbg[m * N + n] = acc[i][j][v];
         }
     }
@@ -253,17 +255,19 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
   constexpr int OST = WN + 8;                   // staged row stride in halves
   _Float16* ost = reinterpret_cast<_Float16*>(pipe_smem) + w * WM * OST;
 #pragma unroll
-  for (int j = 0; j < TJ; ++j) {
-    const float csn = s_cs[wn * WN + 32 * j + l32];
+  for (int i = 0; i < TI; ++i) {
+    const int rl = 32 * i + l32;                 // this lane's row
+    const float rsm = s_rs[wm * WM + rl];
 #pragma unroll
-    for (int i = 0; i < TI; ++i)
+    for (int j = 0; j < TJ; ++j)
 #pragma unroll
       for (int vq = 0; vq < 4; ++vq) {
-        const int rl = 32 * i + 8 * vq + 4 * hl;  // 4 consecutive rows of this lane
-        const f32x4 r4 = *reinterpret_cast<const f32x4*>(&s_rs[wm * WM + rl]);
+        const int cl = 32 * j + 8 * vq + 4 * hl;  // its 4 consecutive columns
+        const f32x4 c4 = *reinterpret_cast<const f32x4*>(&s_cs[wn * WN + cl]);
+        f16x4 o4;
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          ost[(rl + e) * OST + 32 * j + l32] = to_f16(dequant(acc[i][j][4 * vq + e], r4[e], csn));
+        for (int e = 0; e < 4; ++e) o4[e] = to_f16(dequant(acc[i][j][4 * vq + e], rsm, c4[e]));
+        *reinterpret_cast<f16x4*>(ost + rl * OST + cl) = o4;
         // one accumulator block at a time: keeps the live registers few
         __builtin_amdgcn_sched_barrier(0);
       }
