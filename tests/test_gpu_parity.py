@@ -1487,6 +1487,8 @@ def test_decode_rope_latent_v_llava7b_width(llava):
             ok, info = H.close_enough(out, ref)
             H.say(f"  mode={mode} max-abs, rel-L2, rms = {info}")
             assert ok, (mode, info)
+            again = H.host(H.decode_attention(dl, dc, H.dev(q), mode, rope_theta=theta))
+            assert np.array_equal(out.view(np.uint16), again.view(np.uint16)), (mode, "not deterministic")
 
 
 @pytest.mark.parametrize("shape", [(12, 4, 96), (32, 4, 32), (16, 16, 64), (32, 8, 128)],
@@ -1578,6 +1580,8 @@ def test_decode_rope_qlen_llava7b_chunk(llava):
     ref = O.attention_reference(ol, oc, q.astype(np.float64), q_len=q_len, rope_theta=1.0e4)
     out = H.host(H.decode_attention(dl, dc, q_dev, B.QSVD_ATTN_RECONSTRUCT, q_len=q_len, rope_theta=1.0e4))
     _check_qlen_block(out.reshape(q.shape), ref, lengths, q_len)
+    again = H.host(H.decode_attention(dl, dc, q_dev, B.QSVD_ATTN_RECONSTRUCT, q_len=q_len, rope_theta=1.0e4))
+    assert np.array_equal(out.view(np.uint16), again.view(np.uint16)), "not deterministic"
     H.say("decode plain q_len 64 llava7b: rebuild vs absorbed")
     rec = H.host(H.decode_attention(dl, dc, q_dev, B.QSVD_ATTN_RECONSTRUCT, q_len=q_len)).reshape(q.shape)
     ab = H.host(H.decode_attention(dl, dc, q_dev, B.QSVD_ATTN_ABSORBED, q_len=q_len)).reshape(q.shape)
@@ -1611,6 +1615,8 @@ def test_decode_reconstruct_wide_heads(shape, r, fmt):
         ok, info = H.close_enough(out, ref)
         H.say(f"  max-abs, rel-L2, rms = {info}")
         assert ok, (theta, mode, info)
+        again = H.host(H.decode_attention(dl, dc, q_dev, mode, rope_theta=theta))
+        assert np.array_equal(out.view(np.uint16), again.view(np.uint16)), (theta, mode, "not deterministic")
 
 
 def test_decode_rope_13b_shape_full_rebuild():
