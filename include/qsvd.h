@@ -252,14 +252,16 @@ qsvd_status qsvd_prefill_attention_rope(const void* q, const void* k, const void
  *   sm_scale  0 selects 1/sqrt(head_dim)
  *   ws    device workspace of at least qsvd_decode_workspace_size() bytes
  * Requires head_dim % 32 == 0 and <= 128, batch <= 64, q_len <= max_len,
- * 16-byte aligned q, out and s_b.  The absorbed form takes n_q_heads <= 64,
- * r in {128, 512, 1024, 1536} (with at most 32 heads) or r a multiple of 128
- * up to 3072, any cache format, and batch * q_len * ceil(n_q_heads / 16)
- * <= 65535 (batch * q_len <= 65535 with 32-head blocks); the reconstruct
- * form takes n_q_heads <= 64, capacity <= 16384 and any cache format, and
- * with q_len > 1 (causal attention of the last q_len positions over the
- * rebuilt rows on the fp16 matrix cores) head_dim 64 or 128 (F16 rows rebuild on the fp16 products, I8 on the int8 products,
- * I4 on the 4-bit products).
+ * w_group 0 or a multiple of 64, 16-byte aligned q, out and s_b (else
+ * QSVD_ERR_UNSUPPORTED or QSVD_ERR_INVALID_ARG).  The absorbed form takes
+ * n_q_heads <= 64, r in {128, 512, 1024, 1536} (with at most 32 heads) or r
+ * a multiple of 128 up to 3072, any cache format, and
+ * batch * q_len * ceil(n_q_heads / 16) <= 65535 (batch * q_len <= 65535
+ * with 32-head blocks).  The reconstruct form takes n_q_heads <= 64,
+ * capacity <= 16384 and any cache format (F16 rows rebuild on the fp16
+ * products, I8 on the int8 products, I4 on the 4-bit products), and with
+ * q_len > 1 (causal attention of the last q_len positions over the rebuilt
+ * rows on the fp16 matrix cores) head_dim 64 or 128.
  * Launch grids are sized from the host c->max_len and every length is read
  * from seq_len on the device, so a call may be captured in a graph and
  * replayed while the cache grows, provided c->max_len at capture is at least
@@ -308,7 +310,7 @@ size_t qsvd_noalloc_scratch_bytes(void);
  * The latent-value form takes q_len 1 (QSVD_ERR_UNSUPPORTED otherwise).  Both
  * take any cache format (F16, I8, I4), and one workspace size serves both:
  * qsvd_decode_workspace_size(w, c, q_len, QSVD_ATTN_RECONSTRUCT) bytes (the
- * same for every q_len).  rope_theta must be finite and > 1
+ * same for every q_len the forms take).  rope_theta must be finite and > 1
  * (QSVD_ERR_INVALID_ARG otherwise). */
 qsvd_status qsvd_latent_decode_attention_rope(const qsvd_layer* w, const qsvd_cache* c,
                                               const void* q, int32_t q_len, int32_t mode,
