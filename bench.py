@@ -230,7 +230,9 @@ def run_decode(wl, host_layer, fmt, n_layers, batch, ctx0, steps, warmup, mode_n
 
     L = wl.layer
     r, d, nq = L.r, L.d, L.n_q
-    visits = max(-(-steps // n_layers), -(-warmup // n_layers), 1)
+    # every layer is visited at most this often by one pass (the unfused
+    # comparison below makes five visits per layer)
+    visits = max(-(-steps // n_layers), -(-warmup // n_layers), 5)
     cap = ctx0 + visits + 1
     mode = {"auto": B.QSVD_ATTN_AUTO, "absorbed": B.QSVD_ATTN_ABSORBED,
             "reconstruct": B.QSVD_ATTN_RECONSTRUCT}[mode_name]

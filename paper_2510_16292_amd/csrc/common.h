@@ -100,9 +100,18 @@ __device__ __forceinline__ void xcd_tile(int id, int tiles, int tiles_n, int gm,
 }
 
 // Tile rows per group: the block height that minimizes the operand row
-// blocks one XCD touches, gm + (tiles / 8) / gm.
-inline int xcd_group_rows(int64_t tiles_m, int64_t tiles_n) {
+// blocks one XCD touches, gm + (tiles / 8) / gm.  When an XCD's share is
+// many rounds of the `conc` tiles it runs at once, the L2 only ever holds the
+// operands of the tiles in flight, so the block height that keeps those
+// fewest, about sqrt(conc) (a column-first walk of gm rows has gm row blocks
+// and conc / gm column blocks in flight), is taken instead.
+inline int xcd_group_rows(int64_t tiles_m, int64_t tiles_n, int conc = 0) {
   const double per_xcd = (double)(tiles_m * tiles_n) / 8;
+  if (conc > 0 && per_xcd > 4.0 * conc && tiles_n * tiles_n >= conc) {
+    int g = 1;
+    while ((g + 1) * (g + 1) <= conc) ++g;
+    if ((int64_t)g < tiles_m) return g;
+  }
   int best = (int)tiles_m;
   double best_cost = 1e300;
   for (int c = 1; c <= tiles_m; ++c) {

@@ -308,6 +308,9 @@ static DevSegs to_dev(const GemmArgs& g) {
   return d;
 }
 
+// Tiles one XCD runs at once: its 32 CUs, one workgroup each.
+constexpr int kGemmTilesPerXcd = 32;
+
 template <int BM, int BN, int WM, int WN, int NS, bool DBG, bool F16 = false>
 static hipError_t launch_pipe(const GemmArgs& g, const DevSegs& sg, hipStream_t s) {
   using C = PipeCfg<BM, BN, WM, WN, NS>;
@@ -319,7 +322,7 @@ static hipError_t launch_pipe(const GemmArgs& g, const DevSegs& sg, hipStream_t 
   const int32_t kbytes = F16 ? 2 * g.K : g.K;
   KernelScope ks(F16 ? "gemm_f16_pipe" : "gemm_i8_pipe", s);
   QSVD_LAUNCH(ks, kern, dim3((unsigned)(tm * tn)), dim3(C::kThreads), C::kLds, s, g.a, g.b, g.row_scale, g.col_scale,
-                     g.M, g.N, kbytes, tn, xcd_group_rows(tm, tn), sg, g.dbg);
+                     g.M, g.N, kbytes, tn, xcd_group_rows(tm, tn, kGemmTilesPerXcd), sg, g.dbg);
   return hipGetLastError();
 }
 
