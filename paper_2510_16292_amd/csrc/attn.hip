@@ -1758,6 +1758,27 @@ rope_scores_kernel(const _Float16* __restrict__ q, const _Float16* __restrict__ 
     }
 }
 
+// The turned, scaled queries of the fused rotary scores:
+// qrot[b][h][c] = scale * rot(q[b][h], position seq_len[b] - 1)[c], fp32.
+__global__ void __launch_bounds__(256)
+rope_query_kernel(const _Float16* __restrict__ q, const int32_t* __restrict__ seq_len, int32_t capacity,
+                  int32_t batch, int32_t Hq, int32_t dh, float scale, const float2* __restrict__ rope,
+                  float* __restrict__ qrot) {
+  const int half = dh >> 1;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // one pair (b, h, j)
+  if (e >= (int64_t)batch * Hq * half) return;
+  const int j = (int)(e % half);
+  const int64_t bh = e / half;
+  const int b = (int)(bh / Hq);
+  const int L = min(seq_len[b], capacity);
+  const float2 cs = rope[(int64_t)max(L - 1, 0) * half + j];
+  const _Float16* qr = q + bh * dh;
+  float ra, rb;
+  rope_pair((float)qr[j], (float)qr[j + half], cs.x, cs.y, &ra, &rb);
+  qrot[bh * dh + j] = ra * scale;
+  qrot[bh * dh + j + half] = rb * scale;
+}
+
 struct ReconPlan {
   size_t kv_bytes, opart_bytes, ml_bytes, w16_bytes, rope_bytes;
   int n_chunks, n_hb;       // context chunks of RCH tokens, blocks of 32 query heads
@@ -1802,10 +1823,20 @@ struct RopeLatentPlan {
   AbsorbPlan ap;
 };
 
+// The key rebuild with the rotary scores in its epilogue (fp16 caches, and
+// int8 caches with per-channel int8 weights; head_dim 32, 64 or 128): the
+// turned keys never leave the product, and their workspace holds the turned
+// queries instead.
+static bool rope_fused_supported(const qsvd_layer& w, const qsvd_cache& c) {
+  const bool prod = c.fmt == QSVD_CACHE_F16 || (c.fmt == QSVD_CACHE_I8 && w.w_bits == 8 && !w.w_group);
+  return prod && (w.head_dim == 32 || w.head_dim == 64 || w.head_dim == 128);
+}
+
 static RopeLatentPlan plan_rope_latent(const qsvd_layer& w, const qsvd_cache& c) {
   RopeLatentPlan p{};
   const int nkv = w.n_kv_heads * w.head_dim;
-  p.khat_bytes = (size_t)c.batch * c.capacity * nkv * sizeof(_Float16);
+  p.khat_bytes = rope_fused_supported(w, c) ? (size_t)c.batch * w.n_q_heads * w.head_dim * sizeof(float)
+                                             : (size_t)c.batch * c.capacity * nkv * sizeof(_Float16);
   p.pre_bytes = (size_t)c.batch * c.capacity * kHeadBlk * sizeof(float);
   p.w16_bytes = c.fmt == QSVD_CACHE_F16 ? (size_t)nkv * w.r * sizeof(_Float16) : 0;
   p.rope_bytes = rope_table_bytes(w, c);
@@ -1926,6 +1957,58 @@ hipError_t launch_attn_reconstruct(const AttnArgs& a, void* ws, hipStream_t s) {
   return hipGetLastError();
 }
 
+static hipError_t rebuild_rope_scores(const AttnArgs& a, _Float16* w16, float* qrot, const float2* rope, float* pre,
+                                      hipStream_t s) {
+  const qsvd_layer& w = *a.w;
+  const qsvd_cache& c = *a.c;
+  const int N = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim;
+  const int nq = w.n_q_heads * w.head_dim, nkv = w.n_kv_heads * w.head_dim;
+  const int len = c.max_len > 0 ? c.max_len : 1;
+  const bool f16 = c.fmt == QSVD_CACHE_F16;
+  {
+    KernelScope ks("rope_query", s);
+    const int64_t n = (int64_t)c.batch * w.n_q_heads * (w.head_dim / 2);
+    QSVD_LAUNCH(ks, rope_query_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.q, c.seq_len,
+                c.capacity, c.batch, w.n_q_heads, w.head_dim, a.sm_scale * kLog2e, rope, qrot);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (f16) {
+    KernelScope ks("recon_weights", s);
+    const int64_t runs = (int64_t)nkv * (w.r / 8);
+    QSVD_LAUNCH(ks, recon_weights_kernel, dim3((unsigned)((runs + 255) / 256)), dim3(256), 0, s,
+                (const uint8_t*)w.b_t, w.s_b, w.r, N, nq, nkv, w.w_bits, w.w_group, w16);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const size_t row_bytes = f16 ? (size_t)c.r * 2 : (size_t)c.r;
+  const bool one = c.batch == 1 || 4 * (int64_t)len >= 3 * (int64_t)c.capacity;
+  const int launches = one ? 1 : c.batch;
+  for (int i = 0; i < launches; ++i) {
+    GemmArgs g{};
+    const int64_t r0 = one ? 0 : (int64_t)i * c.capacity;
+    g.a = reinterpret_cast<const int8_t*>(reinterpret_cast<const uint8_t*>(c.data) + r0 * row_bytes);
+    g.row_scale = f16 ? nullptr : c.scale + r0;
+    g.M = one ? (c.batch == 1 ? len : (int64_t)c.batch * c.capacity) : len;
+    g.N = nkv;
+    g.K = w.r;
+    g.n_seg = 0;
+    g.abits = 8;
+    if (f16) {
+      g.b = reinterpret_cast<const int8_t*>(w16);
+      g.col_scale = w.w_group ? nullptr : w.s_b + nq;
+    } else {
+      g.b = reinterpret_cast<const int8_t*>(w.b_t) + (int64_t)nq * w.r;
+      g.col_scale = w.s_b + nq;
+    }
+    const RopeEpi re{qrot, rope, c.seq_len, pre, r0, c.capacity, w.n_q_heads, w.n_q_heads / w.n_kv_heads,
+                     w.head_dim};
+    const hipError_t e = launch_gemm_rope_scores(g, re, f16, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 hipError_t launch_attn_rope_latent(const AttnArgs& a, void* ws, hipStream_t s) {
   const qsvd_layer& w = *a.w;
   const qsvd_cache& c = *a.c;
@@ -1946,25 +2029,31 @@ hipError_t launch_attn_rope_latent(const AttnArgs& a, void* ws, hipStream_t s) {
   _Float16* olat = (_Float16*)base;
   const int nkv = w.n_kv_heads * w.head_dim;
   const int len = c.max_len > 0 ? c.max_len : 1;
-  hipError_t e = rebuild_rows(a, nkv, w16, khat, s);
-  if (e != hipSuccess) return e;
-  if ((e = launch_rope_table(a, rope, s)) != hipSuccess) return e;
-  {
-    KernelScope ks("rope_scores", s);
-    const int G = w.n_q_heads / w.n_kv_heads, nch = (len + RCH - 1) / RCH;
-    // runs of up to 8 key/value heads share the (cos, sin) registers, as long
-    // as the grid keeps about four workgroups per CU and the staged queries
-    // fit the default 64 KB of LDS (one head always does)
-    int hpb = std::min(w.n_kv_heads, 8);
-    while (hpb > 1 && ((int64_t)nch * c.batch * ((w.n_kv_heads + hpb - 1) / hpb) < 1024 ||
-                       rope_scores_lds(w.head_dim, hpb, G) > 65536))
-      hpb /= 2;
-    const unsigned runs = (unsigned)((w.n_kv_heads + hpb - 1) / hpb);
-    QSVD_LAUNCH(ks, rope_scores_kernel, dim3(nch, c.batch, runs), dim3(256), rope_scores_lds(w.head_dim, hpb, G), s,
-                a.q, khat, c.seq_len, c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, hpb, a.sm_scale * kLog2e,
-                rope, pre);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+  hipError_t e;
+  if (rope_fused_supported(w, c)) {
+    // the turned queries go where the rebuilt keys would be staged
+    if ((e = launch_rope_table(a, rope, s)) != hipSuccess) return e;
+    if ((e = rebuild_rope_scores(a, w16, reinterpret_cast<float*>(khat), rope, pre, s)) != hipSuccess) return e;
+  } else {
+    if ((e = rebuild_rows(a, nkv, w16, khat, s)) != hipSuccess) return e;
+    if ((e = launch_rope_table(a, rope, s)) != hipSuccess) return e;
+    {
+      KernelScope ks("rope_scores", s);
+      const int G = w.n_q_heads / w.n_kv_heads, nch = (len + RCH - 1) / RCH;
+      // runs of up to 8 key/value heads share the (cos, sin) registers, as long
+      // as the grid keeps about four workgroups per CU and the staged queries
+      // fit the default 64 KB of LDS (one head always does)
+      int hpb = std::min(w.n_kv_heads, 8);
+      while (hpb > 1 && ((int64_t)nch * c.batch * ((w.n_kv_heads + hpb - 1) / hpb) < 1024 ||
+                         rope_scores_lds(w.head_dim, hpb, G) > 65536))
+        hpb /= 2;
+      const unsigned runs = (unsigned)((w.n_kv_heads + hpb - 1) / hpb);
+      QSVD_LAUNCH(ks, rope_scores_kernel, dim3(nch, c.batch, runs), dim3(256), rope_scores_lds(w.head_dim, hpb, G), s,
+                  a.q, khat, c.seq_len, c.capacity, w.n_q_heads, w.n_kv_heads, w.head_dim, hpb, a.sm_scale * kLog2e,
+                  rope, pre);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
   }
   e = c.fmt == QSVD_CACHE_F16 ? dispatch_latent_pre<QSVD_CACHE_F16>(p.ap, c, pre, opart, ml, s)
       : c.fmt == QSVD_CACHE_I8  ? dispatch_latent_pre<QSVD_CACHE_I8>(p.ap, c, pre, opart, ml, s)

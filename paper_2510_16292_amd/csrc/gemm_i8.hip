@@ -106,12 +106,12 @@ struct PipeCfg {
   static constexpr size_t kLds = kStages > kOut ? kStages : kOut;
 };
 
-template <int BM, int BN, int WM, int WN, int NS, bool DBG, bool F16>
+template <int BM, int BN, int WM, int WN, int NS, bool DBG, bool F16, bool RS = false>
 __global__ void __launch_bounds__((PipeCfg<BM, BN, WM, WN, NS>::kThreads))
 gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
                     const float* __restrict__ rs, const float* __restrict__ cs,
                     int64_t M, int32_t N, int32_t K, int32_t n_tiles_n, int32_t gm, DevSegs sg,
-                    int32_t* __restrict__ dbg) {
+                    int32_t* __restrict__ dbg, RopeEpi re) {
   using C = PipeCfg<BM, BN, WM, WN, NS>;
   using Acc = std::conditional_t<F16, f32x16, i32x16>;
   static_assert(!(DBG && F16), "accumulator dumps are for the integer products");
@@ -272,6 +272,59 @@ gemm_i8_pipe_kernel(const int8_t* __restrict__ A, const int8_t* __restrict__ B,
         __builtin_amdgcn_sched_barrier(0);
       }
   }
+  if constexpr (RS) {
+    // Rotary scores of the tile's rows: item (row, head of the tile), the
+    // threads of a wave on consecutive rows of one head.  The staged element
+    // (row, col) sits in the LDS rows of wave (row / WM, col / WN).
+    __syncthreads();
+    const int dh = re.dh, half = dh >> 1, hpt = BN / dh;
+    auto staged = [&](int row, int col) {
+      const int wv = (row / WM) * (BN / WN) + col / WN;
+      return *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(pipe_smem) +
+                                             (size_t)wv * WM * OST + (row % WM) * OST + col % WN);
+    };
+    for (int it = tid; it < BM * hpt; it += C::kThreads) {
+      const int row = it % BM, hl = it / BM;
+      const int64_t m = m0 + row;
+      const int32_t col0 = hl * dh, gkv = (n0 + col0) / dh;
+      if (m >= M || n0 + col0 >= N) continue;
+      const int64_t bt = re.row0 + m;
+      const int b = (int)(bt / re.capacity), t = (int)(bt - (int64_t)b * re.capacity);
+      if (t >= min(re.seq_len[b], re.capacity)) continue;
+      float* prow = re.pre + bt * 32;
+      const float4* cst = reinterpret_cast<const float4*>(re.rope + (int64_t)t * half);
+      for (int g = 0; g < re.G; ++g) {
+        const float4* qh = reinterpret_cast<const float4*>(re.qrot + ((int64_t)b * re.Hq + gkv * re.G + g) * dh);
+        // rot(k) . q over the pairs (j, j + half):
+        //   cos * (k_j q_j + k'_j q'_j) + sin * (k_j q'_j - k'_j q_j)
+        float acc = 0.f;
+        for (int j0 = 0; j0 < half; j0 += 8) {
+          const f16x8 ka = staged(row, col0 + j0), kb = staged(row, col0 + half + j0);
+          float4 c4[4], qa[2], qb[2];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) c4[u] = cst[j0 / 2 + u];
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            qa[u] = qh[j0 / 4 + u];
+            qb[u] = qh[(half + j0) / 4 + u];
+          }
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const float a = (float)ka[i], bb = (float)kb[i];
+            const float qj = qa[i / 4][i % 4], qk = qb[i / 4][i % 4];
+            const float cs_c = (i & 1) ? c4[i / 2].z : c4[i / 2].x, cs_s = (i & 1) ? c4[i / 2].w : c4[i / 2].y;
+            const float uu = fmaf(bb, qk, a * qj), vv = fmaf(-bb, qj, a * qk);
+            acc = fmaf(cs_c, uu, acc);
+            acc = fmaf(cs_s, vv, acc);
+          }
+        }
+        prow[gkv * re.G + g] = acc;
+      }
+      if (n0 + col0 == 0)
+        for (int h = re.Hq; h < 32; ++h) prow[h] = 0.f;
+    }
+    return;
+  }
   // Output rows leave non-temporally: the tile is written once and read by
   // a later kernel, so it need not displace the operands in L2.
   constexpr int CPR = WN / 8;                   // 16-byte chunks per staged row
@@ -311,18 +364,18 @@ static DevSegs to_dev(const GemmArgs& g) {
 // Tiles one XCD runs at once: its 32 CUs, one workgroup each.
 constexpr int kGemmTilesPerXcd = 32;
 
-template <int BM, int BN, int WM, int WN, int NS, bool DBG, bool F16 = false>
-static hipError_t launch_pipe(const GemmArgs& g, const DevSegs& sg, hipStream_t s) {
+template <int BM, int BN, int WM, int WN, int NS, bool DBG, bool F16 = false, bool RS = false>
+static hipError_t launch_pipe(const GemmArgs& g, const DevSegs& sg, hipStream_t s, const RopeEpi& re = RopeEpi{}) {
   using C = PipeCfg<BM, BN, WM, WN, NS>;
-  auto kern = gemm_i8_pipe_kernel<BM, BN, WM, WN, NS, DBG, F16>;
+  auto kern = gemm_i8_pipe_kernel<BM, BN, WM, WN, NS, DBG, F16, RS>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::kLds);
   if (e != hipSuccess) return e;
   const int tn = (g.N + BN - 1) / BN;
   const int64_t tm = (g.M + BM - 1) / BM;
   const int32_t kbytes = F16 ? 2 * g.K : g.K;
-  KernelScope ks(F16 ? "gemm_f16_pipe" : "gemm_i8_pipe", s);
+  KernelScope ks(RS ? "rope_rebuild_scores" : F16 ? "gemm_f16_pipe" : "gemm_i8_pipe", s);
   QSVD_LAUNCH(ks, kern, dim3((unsigned)(tm * tn)), dim3(C::kThreads), C::kLds, s, g.a, g.b, g.row_scale, g.col_scale,
-                     g.M, g.N, kbytes, tn, xcd_group_rows(tm, tn, kGemmTilesPerXcd), sg, g.dbg);
+                     g.M, g.N, kbytes, tn, xcd_group_rows(tm, tn, kGemmTilesPerXcd), sg, g.dbg, re);
   return hipGetLastError();
 }
 
@@ -354,6 +407,19 @@ hipError_t launch_gemm_f16(const GemmArgs& g, hipStream_t s) {
   const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
   return big_tiles >= 256 ? launch_pipe<256, 256, 128, 64, 4, false, true>(g, sg, s)
                           : launch_pipe<128, 128, 64, 64, 6, false, true>(g, sg, s);
+}
+
+hipError_t launch_gemm_rope_scores(const GemmArgs& g, const RopeEpi& re, bool f16, hipStream_t s) {
+  if (g.M == 0 || g.N == 0) return hipSuccess;
+  if ((f16 ? g.K % (PBK / 2) : g.K % PBK) || g.dbg || g.cq) return hipErrorInvalidValue;
+  if (re.dh < 32 || 128 % re.dh || g.N % re.dh || re.Hq > 32 || re.G < 1) return hipErrorInvalidValue;
+  const DevSegs sg{};
+  const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  if (f16)
+    return big_tiles >= 256 ? launch_pipe<256, 256, 128, 64, 4, false, true, true>(g, sg, s, re)
+                            : launch_pipe<128, 128, 64, 64, 6, false, true, true>(g, sg, s, re);
+  return big_tiles >= 256 ? launch_pipe<256, 256, 128, 64, 4, false, false, true>(g, sg, s, re)
+                          : launch_pipe<128, 128, 64, 64, 6, false, false, true>(g, sg, s, re);
 }
 
 }  // namespace qsvd

@@ -60,6 +60,22 @@ struct GemmArgs {
   float* sc;
   int32_t abits;
 };
+// Rotary scores straight from a key-rebuild product (the fused form of the
+// rotary decode's scores): product row m0 + i is cache position t of sequence
+// b ((row0 + m) = b * capacity + t); each head's dh columns of the dequantized
+// fp16 row are turned at position t with the (cos, sin) table rope[t][dh/2],
+// rounded to fp16 and dotted in fp32 with the G turned, scaled queries
+// qrot[b][Hq][dh] of its query heads; pre[b][t][32] receives the scores
+// (heads Hq .. 31 zero), positions t >= seq_len[b] are skipped.
+struct RopeEpi {
+  const float* qrot;
+  const float2* rope;
+  const int32_t* seq_len;
+  float* pre;
+  int64_t row0;
+  int32_t capacity, Hq, G, dh;
+};
+
 // Tiled int8 GEMM for M > 32 (prefill); with g.cq set, the fp16 result is also
 // quantized per row into g.cq / g.sc.
 hipError_t launch_gemm_i8(const GemmArgs& g, hipStream_t s);
@@ -68,6 +84,10 @@ hipError_t launch_gemm_i8(const GemmArgs& g, hipStream_t s);
 // col_scale with NULL scale vectors read as 1; no accumulator dumps or row
 // quantization.
 hipError_t launch_gemm_f16(const GemmArgs& g, hipStream_t s);
+// The int8 (f16 false) or fp16 product of a key rebuild with the rotary-score
+// epilogue instead of stores: N = n_kv_heads * dh, dh dividing the 128- or
+// 256-column tile (32, 64 or 128).
+hipError_t launch_gemm_rope_scores(const GemmArgs& g, const RopeEpi& re, bool f16, hipStream_t s);
 
 // The same products with 4-bit activations and/or int4 weights, per-channel or
 // per-group (group contraction elements, a multiple of 64; scale of group g
