@@ -6,7 +6,8 @@
 
 namespace qsvd {
 
-constexpr int kSkMaxRowChunks = 8;  // 8-element chunks per lane: K <= 8 * 64 * 8 = 4096
+constexpr int kSkMaxRowChunks = 8;  // 8-element chunks per lane held at once: 8 * 64 * 8 = 4096 columns
+constexpr int kSkMaxRowK = 16384;   // wider rows are read twice (max pass, then codes)
 
 // The latent cache append fused into the decode-size projections (one new
 // row per sequence, row m of the product being sequence m's):
@@ -35,7 +36,7 @@ struct SkinnyAppend {
 // codes and scale to cq_out / sc_out (when given) and, for SK_APPEND_CODES,
 // to the cache row seq_len[m].  MAXCH bounds the chunks per lane (K <= 512 MAXCH).
 template <int MAXCH = kSkMaxRowChunks>
-__device__ __forceinline__ void sk_row_pass(const _Float16* __restrict__ ch, int64_t lda, float clip, int32_t M,
+__device__ __forceinline__ void sk_row_pass_narrow(const _Float16* __restrict__ ch, int64_t lda, float clip, int32_t M,
                                             int32_t K, int32_t abits, int w, int nw, int lane, int8_t* qa,
                                             int qa_ld, float* rsc, uint8_t* __restrict__ cq_out,
                                             float* __restrict__ sc_out, const SkinnyAppend& ap) {
@@ -86,6 +87,85 @@ __device__ __forceinline__ void sk_row_pass(const _Float16* __restrict__ ch, int
       }
     }
   }
+}
+
+// The same for rows of more than 512 MAXCH columns: a wave takes MAXCH
+// chunks per lane at a time, all of them for the max |x|, then again for the
+// codes (two reads of the row, the registers of the narrow pass).
+template <int MAXCH = kSkMaxRowChunks>
+__device__ __forceinline__ void sk_row_pass_wide(const _Float16* __restrict__ ch, int64_t lda, float clip, int32_t M,
+                                            int32_t K, int32_t abits, int w, int nw, int lane, int8_t* qa,
+                                            int qa_ld, float* rsc, uint8_t* __restrict__ cq_out,
+                                            float* __restrict__ sc_out, const SkinnyAppend& ap) {
+  const float qm = (float)((1 << (abits - 1)) - 1);
+  const int nch = K / 8;
+  const bool wide = nch > 64 * MAXCH;
+  for (int m = w; m < M; m += nw) {
+    f16x8 v[MAXCH];
+    auto load = [&](int c0) {
+#pragma unroll
+      for (int i = 0; i < MAXCH; ++i) {
+        const int c = c0 + lane + 64 * i;
+        v[i] = c < nch ? *reinterpret_cast<const f16x8*>(ch + (int64_t)m * lda + 8 * c) : f16x8{};
+      }
+    };
+    u16x2 mb = u16x2{0, 0};
+    for (int c0 = 0; c0 < nch; c0 += 64 * MAXCH) {
+      load(c0);
+#pragma unroll
+      for (int i = 0; i < MAXCH; ++i) mb = absmax_f16x8(mb, v[i]);
+    }
+    const float a = mul_rn(clip, wave_max(absmax_value(mb)));
+    const float inv = a != 0.f ? div_rn(qm, a) : 0.f;
+    const float sc = a != 0.f ? div_rn(a, qm) : 1.f;
+    const bool own = (m % (int)gridDim.x) == (int)blockIdx.x;
+    // the cache row this sequence's codes also go to (integer caches)
+    const bool app = own && ap.mode == SK_APPEND_CODES;
+    const int32_t pos = app ? ap.seq_len[m] : 0;
+    const bool app_row = app && pos >= 0 && pos < ap.capacity;
+    uint8_t* crow = ap.data + ((int64_t)m * ap.capacity + (app_row ? pos : 0)) * (abits == 8 ? K : K / 2);
+    if (lane == 0) {
+      rsc[m] = sc;
+      if (own && sc_out) sc_out[m] = sc;
+      if (app_row) ap.scale[(int64_t)m * ap.capacity + pos] = sc;
+    }
+    for (int c0 = 0; c0 < nch; c0 += 64 * MAXCH) {
+    if (wide) load(c0);     // (a row of at most 512 MAXCH columns is still in v)
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) {
+      const int c = c0 + lane + 64 * i;
+      if (c >= nch) continue;
+      uint32_t q[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) q[e] = code_bits((float)v[i][e], inv, qm);
+      const uint32_t lo = pack4_codes8(q[0], q[1], q[2], q[3]), hi = pack4_codes8(q[4], q[5], q[6], q[7]);
+      *reinterpret_cast<uint2*>(qa + m * qa_ld + 8 * c) = make_uint2(lo, hi);
+      if (own && (cq_out || app_row)) {
+        if (abits == 8) {
+          if (cq_out) *reinterpret_cast<uint2*>(cq_out + (int64_t)m * K + 8 * c) = make_uint2(lo, hi);
+          if (app_row) *reinterpret_cast<uint2*>(crow + 8 * c) = make_uint2(lo, hi);
+        } else {
+          const uint32_t p = pack8_codes4(q);
+          if (cq_out) *reinterpret_cast<uint32_t*>(cq_out + (int64_t)m * (K / 2) + 4 * c) = p;
+          if (app_row) *reinterpret_cast<uint32_t*>(crow + 4 * c) = p;
+        }
+      }
+    }
+    }
+  }
+}
+
+// The row pass of a kernel built for rows up to 512 MAXCH columns (WIDE
+// false) or wider ones.
+template <bool WIDE, int MAXCH = kSkMaxRowChunks>
+__device__ __forceinline__ void sk_row_pass(const _Float16* __restrict__ ch, int64_t lda, float clip, int32_t M,
+                                            int32_t K, int32_t abits, int w, int nw, int lane, int8_t* qa,
+                                            int qa_ld, float* rsc, uint8_t* __restrict__ cq_out,
+                                            float* __restrict__ sc_out, const SkinnyAppend& ap) {
+  if constexpr (WIDE)
+    sk_row_pass_wide<MAXCH>(ch, lda, clip, M, K, abits, w, nw, lane, qa, qa_ld, rsc, cq_out, sc_out, ap);
+  else
+    sk_row_pass_narrow<MAXCH>(ch, lda, clip, M, K, abits, w, nw, lane, qa, qa_ld, rsc, cq_out, sc_out, ap);
 }
 
 // After the row pass (and a barrier): the cache row of each sequence this

@@ -96,7 +96,7 @@ __device__ __forceinline__ void sk_span(int w, int nw, int32_t K, int32_t group,
   }
 }
 
-template <int ASRC, int WBITS>
+template <int ASRC, int WBITS, bool WIDE = false>
 __global__ void __launch_bounds__(64 * kSkMaxWaves)
 skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, const float* __restrict__ row_scale_in,
                    const uint8_t* __restrict__ bt, const float* __restrict__ col_scale, int32_t sstride,
@@ -158,8 +158,8 @@ skinny_gemm_kernel(const void* __restrict__ a_src, int64_t lda, float clip, cons
   load_b(s0);
 
   if (ASRC == SK_A_F16Q) {
-    sk_row_pass(reinterpret_cast<const _Float16*>(a_src), lda, clip, M, K, abits, w, nw, lane, qa, qa_ld, rsc,
-                cq_out, sc_out, ap);
+    sk_row_pass<WIDE>(reinterpret_cast<const _Float16*>(a_src), lda, clip, M, K, abits, w, nw, lane, qa, qa_ld,
+                      rsc, cq_out, sc_out, ap);
     __syncthreads();
     sk_advance(ap, M, tid);
   }
@@ -269,7 +269,7 @@ static SkinnyPlan skinny_plan(int64_t M, int32_t K, int32_t N, int32_t group, bo
 bool skinny_supported(int64_t M, int32_t K, int32_t group, bool f16q) {
   if (M < 1 || M > 32 || K < 64 || K % 64) return false;
   if (group && (group % 64 || K % group || K / group > kSkMaxGroups)) return false;
-  if (f16q && K > kSkMaxRowChunks * 64 * 8) return false;
+  if (f16q && K > kSkMaxRowK) return false;
   return skinny_plan(M, K, kSkCols, group, f16q).lds <= kSkLdsLimit;
 }
 
@@ -310,7 +310,10 @@ hipError_t launch_skinny_fused(const GemmArgs& g, int32_t asrc, float clip, int6
                        sstride, M, g.N, g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)nullptr,
                        (float*)nullptr, ap, p.cols);
   } else {
-    auto k = wbits == 8 ? skinny_gemm_kernel<SK_A_F16Q, 8> : skinny_gemm_kernel<SK_A_F16Q, 4>;
+    // rows wider than the row pass holds at once take the two-read variant
+    const bool wide = g.K > 64 * 8 * kSkMaxRowChunks;
+    auto k = wbits == 8 ? (wide ? skinny_gemm_kernel<SK_A_F16Q, 8, true> : skinny_gemm_kernel<SK_A_F16Q, 8>)
+                        : (wide ? skinny_gemm_kernel<SK_A_F16Q, 4, true> : skinny_gemm_kernel<SK_A_F16Q, 4>);
     if (hipError_t e = allow((const void*)k); e != hipSuccess) return e;
     QSVD_LAUNCH(ks, k, grid, block, p.lds, s, (const void*)g.a, lda, clip, (const float*)nullptr, bt, g.col_scale,
                        sstride, M, g.N, g.K, group, p.nw, g.abits, p.qa_off, so, g.dbg, (uint8_t*)g.cq, g.sc, ap, p.cols);
