@@ -259,6 +259,9 @@ static SkinnyPlan skinny_plan(int64_t M, int32_t K, int32_t N, int32_t group, bo
   while (p.cols > 4 && (N + p.cols / 2 - 1) / (p.cols / 2) <= kSkMinGrid) p.cols /= 2;
   const int steps = K / 64, ng = group ? K / group : 0;
   p.nw = std::min(kSkMaxWaves, group ? ng : steps);
+  // more column blocks than CUs: workgroups of at most half the waves, so
+  // that two share a CU and the grid still takes one round
+  if ((N + p.cols - 1) / p.cols > kSkMinGrid) p.nw = std::min(p.nw, kSkMaxWaves / 2);
   const int rbl = (int)((M + 15) / 16);
   const size_t tiles = (size_t)(group ? ng : p.nw) * rbl * 64 * sizeof(i32x4);
   p.qa_off = (int32_t)tiles;
