@@ -1517,6 +1517,31 @@ def test_decode_rope_head_dims(shape, fmt):
         assert ok, (mode, info)
 
 
+@pytest.mark.parametrize("fmt", [O.CACHE_F16, O.CACHE_I8], ids=["f16", "i8"])
+def test_decode_rope_latent_short_lengths(fmt):
+    """The rotary latent-value form when the cached lengths are short against
+    the capacity (3 / 17 / 40 of 304), so the key rebuild runs one product per
+    sequence over its own rows (the scores come from the products' epilogue
+    for these caches); GQA 4 query heads per key/value head at dh 128 and MHA
+    at dh 64, against the oracle, run twice bit-identically."""
+    for shape in ((32, 8, 128), (16, 16, 64)):
+        Hq, Hkv, dh = shape
+        L = configs.LayerShape(d=512, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=dh, r=512)
+        ol, dl = _random_factor_layer(L, 1300 + dh + Hq)
+        wl = configs.Workload(97, "rope-short", L, "gaussian", 8, 0, 8, fmt)
+        oc, dc = _prefilled_caches(wl, fmt, [3, 17, 40], 304)
+        g = np.random.default_rng(dh * 11 + Hq)
+        q = (g.standard_normal((3, Hq * dh)) * 4.0).astype(np.float16)
+        ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1, rope_theta=1.0e4)[:, 0, :]
+        H.say(f"decode rope latent short lengths Hq={Hq} Hkv={Hkv} dh={dh} fmt={fmt}")
+        out = H.host(H.decode_attention(dl, dc, H.dev(q), B.QSVD_ATTN_ABSORBED, rope_theta=1.0e4))
+        ok, info = H.close_enough(out, ref)
+        H.say(f"  max-abs, rel-L2, rms = {info}")
+        assert ok, (shape, info)
+        again = H.host(H.decode_attention(dl, dc, H.dev(q), B.QSVD_ATTN_ABSORBED, rope_theta=1.0e4))
+        assert np.array_equal(out.view(np.uint16), again.view(np.uint16)), (shape, "not deterministic")
+
+
 def _check_qlen_block(out, ref, lengths, q_len):
     """Rows with a visible position against the oracle; rows whose position
     precedes the cache (a sequence shorter than the query block) are zeros."""
