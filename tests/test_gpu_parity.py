@@ -673,8 +673,15 @@ def _layer_for(shape_id):
     ("llava7b", B.QSVD_CACHE_F16, 8, 16, 1.0),       # the bench's decode step
     ("llava7b", B.QSVD_CACHE_I4, 4, 16, 1.0),
     ("qwen2vl", B.QSVD_CACHE_I8, 8, 32, 1.0),        # 32 rows: the quantizer as its own launch
-    ("stack13b", B.QSVD_CACHE_I4, 4, 8, 1.0),        # d = 5120: the quantizer as its own launch
-], ids=["tiny-f16", "tiny-i8-clip", "llava7b-f16", "llava7b-i4", "qwen2vl-i8-w4", "13b-i4-w4a4"])
+    # d = 5120, wider than one wave's registers: 8 rows take two waves each
+    # (each half read once), 3 and 5 rows four and three waves (uneven parts),
+    # 16 rows one wave each (the row read twice)
+    ("stack13b", B.QSVD_CACHE_I4, 4, 8, 1.0),
+    ("stack13b", B.QSVD_CACHE_I8, 8, 3, 0.9),
+    ("stack13b", B.QSVD_CACHE_F16, 4, 5, 1.0),
+    ("stack13b", B.QSVD_CACHE_I8, 8, 16, 1.0),
+], ids=["tiny-f16", "tiny-i8-clip", "llava7b-f16", "llava7b-i4", "qwen2vl-i8-w4", "13b-i4-w4a4", "13b-i8-b3",
+        "13b-f16-a4-b5", "13b-i8-b16"])
 def test_decode_project_append_equals_separate_calls(shape_id, fmt, abits, batch, clip):
     """The fused decode projection with its cache append leaves every output
     byte, cache byte and length exactly as quantize + projection (Q only) +
