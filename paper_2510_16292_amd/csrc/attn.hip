@@ -353,20 +353,66 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   using RawT = typename std::conditional<F16C, f16x8, typename std::conditional<I4C, uint2, uint4>::type>::type;
   RawT raw[KD][NLD];
   float scr[KD], sc_cur[F16C ? 1 : 16];
+  // Where load i of a lane goes in the wave's 32 x RW tile.  A tile that is
+  // staged in LDS before any use is read row-major: consecutive lanes take
+  // consecutive 16-byte (fp16, int8) or 8-byte (int4) chunks of a row slice
+  // (24 lanes per 192-column fp16 slice), so one load instruction covers
+  // whole cache lines (8 of them for fp16) instead of a 32-byte piece of 32
+  // rows.  A tile that feeds the score product from registers keeps the
+  // product's operand layout: row l32, the columns of contraction step i.
+  constexpr bool kRowMajor = kStageFirst || PRE;
+  constexpr int CPR = F16C ? RW / 8 : RW / 16;     // load chunks per row slice
+  // the lane pattern repeats every P loads (64 P chunks = RPP whole rows),
+  // so a lane holds only P distinct (row, column) pairs
+  static_assert(CPR <= 64, "a row slice of at most 64 load chunks");
+  constexpr int P = CPR / (CPR & -CPR);     // CPR / gcd(64, CPR)
+  constexpr int RPP = 64 * P / CPR;
+  auto trow = [&](int i) { return kRowMajor ? (i / P) * RPP + (64 * (i % P) + lane) / CPR : l32; };
+  auto tcol = [&](int i) {
+    return kRowMajor ? (F16C ? 8 : 16) * ((64 * (i % P) + lane) % CPR) : kcol(F16C ? i : 2 * i, half);
+  };
+  // this sequence's rows: element (t, x) at byte (t * r + x) * elem
+  const int64_t seq_elems = (int64_t)b * capacity * r;
+  const uint8_t* cseq = cdata + (F16C ? 2 * seq_elems : I4C ? seq_elems / 2 : seq_elems);
+  // Row-major tiles come through range-checked buffer loads: one buffer per
+  // group of RPP rows, ending at the chunk end, so rows past it read as zeros
+  // (and are masked) without a memory access; a lane's offset into the group
+  // is one of P constants.
+  const int row_bytes = F16C ? 2 * r : I4C ? r / 2 : r;
+  constexpr int CB = I4C ? 8 : 16;                  // bytes per load chunk
+  int voff[P];
+#pragma unroll
+  for (int j = 0; j < P; ++j)
+    voff[j] = trow(j) * row_bytes + CB * ((64 * j + lane) % CPR) + (F16C ? 2 * slice0 : I4C ? slice0 / 2 : slice0);
   auto load_tile = [&](int sl, int t0) {
     if constexpr (!F16C) scr[sl] = cscale[(int64_t)b * capacity + min(t0 + l32, L - 1)];
-    // rows past the chunk end are masked; re-read the last row instead of
-    // fetching the next chunk's rows
-    const int tk = min(t0 + l32, t_end - 1);
-    const int64_t off = ((int64_t)b * capacity + tk) * r + slice0;     // element index of the row slice
+    if constexpr (kRowMajor) {
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      if constexpr (F16C)
-        raw[sl][i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const _Float16*>(cdata) + off + kcol(i, half));
-      else if constexpr (I4C)
-        raw[sl][i] = *reinterpret_cast<const RawT*>(cdata + (off + kcol(2 * i, half)) / 2);
-      else
-        raw[sl][i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const int8_t*>(cdata) + off + kcol(2 * i, half));
+      for (int q = 0; q < NLD / P; ++q) {
+        const int t = t0 + RPP * q;
+        // (uniform; readfirstlane keeps the resource in scalar registers)
+        const int nrows = __builtin_amdgcn_readfirstlane(max(0, min(RPP, t_end - t)));
+        const auto rs = __builtin_amdgcn_make_buffer_rsrc((void*)(cseq + (int64_t)t * row_bytes), (short)0,
+                                                          nrows * row_bytes, 0x00020000);
+#pragma unroll
+        for (int j = 0; j < P; ++j) {
+          if constexpr (I4C)
+            raw[sl][P * q + j] = __builtin_bit_cast(RawT, __builtin_amdgcn_raw_buffer_load_b64(rs, voff[j], 0, 0));
+          else
+            raw[sl][P * q + j] = __builtin_bit_cast(RawT, __builtin_amdgcn_raw_buffer_load_b128(rs, voff[j], 0, 0));
+        }
+      }
+    } else {
+      // rows past the chunk end are masked; re-read the last row instead of
+      // fetching the next chunk's rows
+      const int64_t off = ((int64_t)b * capacity + min(t0 + l32, t_end - 1)) * r + slice0;
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        if constexpr (I4C)
+          raw[sl][i] = *reinterpret_cast<const RawT*>(cdata + (off + kcol(2 * i, half)) / 2);
+        else
+          raw[sl][i] = *reinterpret_cast<const RawT*>(reinterpret_cast<const int8_t*>(cdata) + off + kcol(2 * i, half));
+      }
     }
   };
   // the scales of tokens t0 + 8*(v/4) + 4*half + v%4, from the wave's staged copy
@@ -421,7 +467,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
       if constexpr (F16C) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(ks, half)) = raw[sl][ks];
+          *reinterpret_cast<f16x8*>(cst + trow(ks) * CST + tcol(ks)) = raw[sl][ks];
       } else {
         scl[l32] = scr[sl];
 #pragma unroll
@@ -434,8 +480,8 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
             c0 = cvt_i8x8(raw[sl][i].x, raw[sl][i].y);
             c1 = cvt_i8x8(raw[sl][i].z, raw[sl][i].w);
           }
-          *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i, half)) = c0;
-          *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i + 1, half)) = c1;
+          *reinterpret_cast<f16x8*>(cst + trow(i) * CST + tcol(i)) = c0;
+          *reinterpret_cast<f16x8*>(cst + trow(i) * CST + tcol(i) + 8) = c1;
         }
       }
       if (KD > 1 || t0 + 32 < t_end) load_tile(sl, t0 + 32 * KD);
@@ -455,7 +501,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     if constexpr (F16C) {
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(ks, half)) = raw[sl][ks];
+        *reinterpret_cast<f16x8*>(cst + trow(ks) * CST + tcol(ks)) = raw[sl][ks];
     } else {
       scl[l32] = scr[sl];
 #pragma unroll
@@ -468,8 +514,8 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
           c0 = cvt_i8x8(raw[sl][i].x, raw[sl][i].y);
           c1 = cvt_i8x8(raw[sl][i].z, raw[sl][i].w);
         }
-        *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i, half)) = c0;
-        *reinterpret_cast<f16x8*>(cst + l32 * CST + kcol(2 * i + 1, half)) = c1;
+        *reinterpret_cast<f16x8*>(cst + trow(i) * CST + tcol(i)) = c0;
+        *reinterpret_cast<f16x8*>(cst + trow(i) * CST + tcol(i) + 8) = c1;
       }
     }
     if (KD > 1 || t0 + 32 < t_end) load_tile(sl, t0 + 32 * KD);
