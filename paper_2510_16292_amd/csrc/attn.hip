@@ -430,11 +430,32 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
   // loads are out (it is an L2 hit, the tile comes from HBM).  With two, the
   // loads go out in the order the loop consumes them (query, slot 0, slot 1),
   // so that the wait before each use can leave the later ones in flight.
+  // The slice (32 heads x RW) is read row-major like a staged tile, whole
+  // cache lines per load instruction, then passed through the wave's LDS
+  // copy (free until the first tile is staged) into the score product's
+  // operand layout.
+  constexpr int CPQ = RW / 8;     // 16-byte chunks per head row of the slice
   auto load_query = [&]() {
     if constexpr (!PRE) {
-      const _Float16* qrow = qt + ((int64_t)vb * kHeadBlk + l32) * r + slice0;
+      const _Float16* qb = qt + (int64_t)vb * kHeadBlk * r + slice0;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, half));
+      for (int ks = 0; ks < KS; ++ks) {
+        const int c = 64 * ks + lane;
+        qf[ks] = *reinterpret_cast<const f16x8*>(qb + (int64_t)(c / CPQ) * r + 8 * (c % CPQ));
+      }
+    }
+  };
+  auto query_operands = [&]() {
+    if constexpr (!PRE) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int c = 64 * ks + lane;
+        *reinterpret_cast<f16x8*>(cst + (c / CPQ) * CST + 8 * (c % CPQ)) = qf[ks];
+      }
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(cst + l32 * CST + kcol(ks, half));
+      asm volatile("" ::: "memory");
     }
   };
   if constexpr (KD > 1) {
@@ -449,6 +470,7 @@ latent_attn_kernel(const _Float16* __restrict__ qt, const uint8_t* __restrict__ 
     load_tile(0, t_begin);
     load_query();
   }
+  query_operands();
   for (int tb = t_begin; tb < t_end; tb += 32 * KD) {
 #pragma unroll
   for (int sl = 0; sl < KD; ++sl) {
