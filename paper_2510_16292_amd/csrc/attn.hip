@@ -769,9 +769,20 @@ __device__ __forceinline__ void h16_wave(const _Float16* __restrict__ qrow, cons
   auto kcol = [](int ks, int gg) {
     return F16C ? 32 * ks + 8 * gg : (I4C ? 128 * (ks >> 2) + 32 * gg + 8 * (ks & 3) : 64 * (ks >> 1) + 16 * gg + 8 * (ks & 1));
   };
+  // The query slice (16 heads x 128 U columns) is read row-major, whole
+  // cache lines per load instruction, and turned into the score product's
+  // operand layout through the wave's LDS copy once the first tiles' loads
+  // are out.
+  constexpr int CPQ = 16 * U;      // 16-byte chunks per head row of the slice
   f16x8 qf[KSA];
+  {
+    const _Float16* qb = qrow - (int64_t)l16 * r;
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(qrow + kcol(ks, g));
+    for (int ks = 0; ks < KS; ++ks) {
+      const int c = 64 * ks + lane;
+      qf[ks] = *reinterpret_cast<const f16x8*>(qb + (int64_t)(c / CPQ) * r + 8 * (c % CPQ));
+    }
+  }
   f32x4 o[RBA];
 #pragma unroll
   for (int rb = 0; rb < RBA; ++rb) o[rb] = f32x4{};
@@ -802,6 +813,15 @@ __device__ __forceinline__ void h16_wave(const _Float16* __restrict__ qrow, cons
 
 #pragma unroll
   for (int d = 0; d < D; ++d) load(d, t_begin + T * d);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const int c = 64 * ks + lane;
+    *reinterpret_cast<f16x8*>(cst + (c / CPQ) * CST + 8 * (c % CPQ)) = qf[ks];
+  }
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const f16x8*>(cst + l16 * CST + kcol(ks, g));
+  asm volatile("" ::: "memory");
   for (int base = t_begin; base < t_end; base += T * D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
