@@ -974,7 +974,7 @@ def cpu_baseline_other(factors2):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs the QSVD hot path on one GPU only; multi-GPU runs are not part of it "
+        print("bench.py: the QSVD hot path is measured on one GPU only; multi-GPU runs are not supported "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
     import torch
