@@ -839,6 +839,28 @@ def test_decode_llava7b_width_ragged(llava, mode):
     assert ok, info
 
 
+@pytest.mark.parametrize("fmt", [O.CACHE_F16, O.CACHE_I8, O.CACHE_I4], ids=["f16", "i8", "i4"])
+def test_decode_llava7b_width_odd_capacity_full(llava, fmt):
+    """The 32-head r = 1536 attention reads its staged tiles in range-checked
+    groups of 8 (fp16) or 16 (integer) rows that end at the chunk end: a
+    capacity of 1001 rows (a multiple of neither), one sequence filling it,
+    one ending two rows short, one of a single row and one of 17, in every
+    cache format, against the oracle; a second call gives the same bytes."""
+    wl, ol, dl = llava
+    lengths = [1001, 999, 1, 17]
+    oc, dc = _prefilled_caches(wl, fmt, lengths, 1001)
+    g = np.random.default_rng(1001)
+    q = (g.standard_normal((4, wl.layer.n_q_heads * wl.layer.head_dim)) * 2.0).astype(np.float16)
+    H.say(f"decode llava7b width odd capacity fmt={fmt}")
+    ref = O.attention_reference(ol, oc, q.astype(np.float64)[:, None, :], 1)[:, 0, :]
+    out = H.host(H.decode_attention(dl, dc, H.dev(q), B.QSVD_ATTN_ABSORBED))
+    ok, info = H.close_enough(out, ref)
+    H.say(f"  max-abs, rel-L2, rms = {info}")
+    assert ok, info
+    again = H.host(H.decode_attention(dl, dc, H.dev(q), B.QSVD_ATTN_ABSORBED))
+    assert np.array_equal(out.view(np.uint16), again.view(np.uint16))
+
+
 def test_decode_llava7b_full_size_sampled(llava):
     """The decode workload at its full size (16 sequences x 4096 cached tokens,
     fp16 latent cache of width 1536) in the launch configuration the bench
